@@ -1,0 +1,451 @@
+"""Plain CPU oracle of the Huff-LLM bf16 weight codec (HLF1 container).
+
+TEST INFRASTRUCTURE ONLY: this module exists to check the product path. Only
+the tests, the smoke entry point and the benchmark's CPU-baseline leg may
+import it; the library never does, and it shares no code with the library.
+
+What it computes, following the paper (Huff-LLM, arXiv 2502.00922):
+
+* Sec. 2.1, Eq. 1: a float is sign, biased exponent and mantissa fields.
+* Sec. 5.1 (compression experiments): bf16 weights are split 1-4-4-7: the
+  sign and the 7 mantissa bits stay raw, the 8 exponent bits become two 4-bit
+  groups, each Huffman coded. Codebooks are per weight matrix.
+* Sec. 3.1: the split fields are Huffman coded once, offline, on a CPU.
+* Sec. 3.2: the decoder matches a window of L_max bits against the codebook,
+  emits the symbol and advances its start pointer by the code length; the
+  sign is passed through and the fields are concatenated back to 16 bits.
+
+Readings where the paper is silent (each is written down in the design notes):
+code-length limit L_max = 12 by default (Sec. 3.2 / 5.2 report 12 as the
+empirical maximum); textbook heap Huffman with ties broken leaf-before-node,
+leaves by symbol, nodes by creation order; package-merge when the Huffman code
+is longer than L_max; canonical code values in the RFC 1951 Sec. 3.2.2 order;
+codes emitted most-significant bit first into a stream packed least-significant
+bit first; a one-symbol field gets code length 0; segments of S weights along a
+row are the unit of independent decoding.
+
+Container layout (little-endian; sections start at 64-byte boundaries):
+  header (128 B), seg_bits u16[n_seg], grp_off u32[n_grp + 1] (16-byte
+  units), stream (one 16-byte aligned bit stream per group of 64 segments),
+  raw u8[n] (sign<<7 | mantissa, interleaved per group in 8-byte units).
+"""
+from __future__ import annotations
+
+import heapq
+import math
+import struct
+from fractions import Fraction
+from typing import Dict, List, Sequence, Tuple
+
+import numpy as np
+
+MAGIC = 0x31464C48          # 'HLF1'
+VERSION = 1
+HEADER_BYTES = 128
+GROUP_SEGS = 64             # segments per group (one per lane of a 64-wide wavefront)
+RAW_UNIT = 8                # bytes of one segment's raw plane stored contiguously
+UNIT_BYTES = 16             # group streams are padded to 128 bits
+SECTION_ALIGN = 64
+NSYM = 16                   # both exponent groups are 4-bit symbols
+
+
+# --------------------------------------------------------------------------
+# Field split (Sec. 2.1 Eq. 1; bf16 1-4-4-7 split of Sec. 5.1)
+# --------------------------------------------------------------------------
+
+def split_fields(w: np.ndarray):
+    """bf16 bit patterns -> (sign, exponent-high nibble, exponent-low nibble, mantissa).
+
+    bf16 = sign (bit 15) | exponent (bits 14..7) | mantissa (bits 6..0); the
+    1-4-4-7 split reads the fields most-significant first."""
+    w = np.asarray(w, dtype=np.uint16).astype(np.uint32)
+    s = (w >> 15) & 0x1
+    eh = (w >> 11) & 0xF
+    el = (w >> 7) & 0xF
+    m = w & 0x7F
+    return s, eh, el, m
+
+
+def join_fields(s, eh, el, m) -> np.ndarray:
+    """Concatenate the fields back into the 16-bit weight (Sec. 3.2)."""
+    s, eh, el, m = (np.asarray(a, dtype=np.uint32) for a in (s, eh, el, m))
+    return ((s << 15) | (eh << 11) | (el << 7) | m).astype(np.uint16)
+
+
+def raw_byte(s, m) -> np.ndarray:
+    """The raw (uncompressed) part of a weight: sign above the 7 mantissa bits."""
+    return ((np.asarray(s, np.uint32) << 7) | np.asarray(m, np.uint32)).astype(np.uint8)
+
+
+# --------------------------------------------------------------------------
+# Histograms and entropy (Sec. 3.1, entropy-of-splits table)
+# --------------------------------------------------------------------------
+
+def histogram(sym: np.ndarray, nsym: int = NSYM) -> List[int]:
+    sym = np.asarray(sym).ravel()
+    return [int(np.count_nonzero(sym == v)) for v in range(nsym)]
+
+
+def entropy_bits(freqs: Sequence[int]) -> float:
+    """Empirical entropy in bits per symbol."""
+    n = sum(freqs)
+    h = 0.0
+    for f in freqs:
+        if f:
+            p = f / n
+            h -= p * math.log2(p)
+    return h
+
+
+def kraft_sum(lengths: Sequence[int]) -> Fraction:
+    return sum((Fraction(1, 2 ** l) for l in lengths if l > 0), Fraction(0))
+
+
+# --------------------------------------------------------------------------
+# Huffman code lengths, length limit, canonical codes
+# --------------------------------------------------------------------------
+
+def huffman_lengths(freqs: Sequence[int]) -> List[int]:
+    """Textbook Huffman: repeatedly merge the two lightest nodes.
+
+    Heap key (weight, kind, id): leaves (kind 0, id = symbol) pop before
+    internal nodes (kind 1, id = creation order) of equal weight. A code
+    length is the depth of the symbol's leaf. Absent symbols get length 0;
+    a field with a single present symbol gets length 0 (no bits)."""
+    present = [s for s, f in enumerate(freqs) if f > 0]
+    if not present:
+        raise ValueError("empty alphabet")
+    lengths = [0] * len(freqs)
+    if len(present) == 1:
+        return lengths
+    heap = [(freqs[s], 0, s) for s in present]
+    heapq.heapify(heap)
+    children: Dict[Tuple[int, int], Tuple[Tuple[int, int], Tuple[int, int]]] = {}
+    next_id = 0
+    while len(heap) > 1:
+        a = heapq.heappop(heap)
+        b = heapq.heappop(heap)
+        node = (a[0] + b[0], 1, next_id)
+        children[(1, next_id)] = ((a[1], a[2]), (b[1], b[2]))
+        next_id += 1
+        heapq.heappush(heap, node)
+    root = (heap[0][1], heap[0][2])
+    stack = [(root, 0)]
+    while stack:
+        (kind, ident), depth = stack.pop()
+        if kind == 0:
+            lengths[ident] = depth
+        else:
+            left, right = children[(kind, ident)]
+            stack.append((left, depth + 1))
+            stack.append((right, depth + 1))
+    return lengths
+
+
+def package_merge_lengths(freqs: Sequence[int], lmax: int) -> List[int]:
+    """Optimal prefix-code lengths with every length <= lmax (package-merge).
+
+    Items are the present symbols sorted by (weight, symbol). Starting from
+    that list, lmax - 1 times: pair consecutive items into packages (an odd
+    last item is dropped) and merge them with the leaves by weight, a leaf
+    before a package on equal weight. The first 2(n-1) items of the final list
+    are selected; a symbol's length is the number of selected items holding it."""
+    present = sorted((f, s) for s, f in enumerate(freqs) if f > 0)
+    n = len(present)
+    lengths = [0] * len(freqs)
+    if n == 0:
+        raise ValueError("empty alphabet")
+    if n == 1:
+        return lengths
+    if n > 2 ** lmax:
+        raise ValueError("alphabet too large for lmax")
+    leaves = [(f, 0, (s,)) for f, s in present]
+    cur = list(leaves)
+    for _ in range(lmax - 1):
+        packages = [(cur[2 * i][0] + cur[2 * i + 1][0], 1, cur[2 * i][2] + cur[2 * i + 1][2])
+                    for i in range(len(cur) // 2)]
+        cur = sorted(leaves + packages, key=lambda it: (it[0], it[1]))   # stable
+    for item in cur[: 2 * (n - 1)]:
+        for s in item[2]:
+            lengths[s] += 1
+    return lengths
+
+
+def limited_lengths(freqs: Sequence[int], lmax: int) -> List[int]:
+    """Huffman lengths, replaced by package-merge lengths if any exceeds lmax."""
+    h = huffman_lengths(freqs)
+    if max(h) <= lmax:
+        return h
+    return package_merge_lengths(freqs, lmax)
+
+
+def canonical_codes(lengths: Sequence[int]) -> List[int]:
+    """Canonical code values (RFC 1951 Sec. 3.2.2): shorter codes first, equal
+    lengths in increasing symbol order. Entries with length 0 get code 0."""
+    maxl = max(lengths) if lengths else 0
+    bl_count = [0] * (maxl + 1)
+    for l in lengths:
+        if l:
+            bl_count[l] += 1
+    next_code = [0] * (maxl + 2)
+    code = 0
+    for bits in range(1, maxl + 1):
+        code = (code + bl_count[bits - 1]) << 1
+        next_code[bits] = code
+    codes = [0] * len(lengths)
+    for s, l in enumerate(lengths):
+        if l:
+            codes[s] = next_code[l]
+            next_code[l] += 1
+    return codes
+
+
+class FieldCode:
+    """One field's codebook: lengths, canonical codes and a bit-serial decoder."""
+
+    def __init__(self, lengths: Sequence[int], nsym_present: int, single: int):
+        self.lengths = list(lengths)
+        self.nsym = nsym_present
+        self.single = single
+        self.codes = canonical_codes(self.lengths)
+        # Decoder tables: for each length, the first code value and its symbols.
+        maxl = max(self.lengths) if any(self.lengths) else 0
+        self.by_len: Dict[int, Tuple[int, List[int]]] = {}
+        for l in range(1, maxl + 1):
+            syms = [s for s in range(len(self.lengths)) if self.lengths[s] == l]
+            if syms:
+                self.by_len[l] = (self.codes[syms[0]], syms)
+        self.maxl = maxl
+
+    @classmethod
+    def from_freqs(cls, freqs: Sequence[int], lmax: int) -> "FieldCode":
+        present = [s for s, f in enumerate(freqs) if f > 0]
+        return cls(limited_lengths(freqs, lmax), len(present), present[0] if len(present) == 1 else 0)
+
+    def decode_one(self, bits: List[int], pos: int) -> Tuple[int, int]:
+        """Read one code MSB-first starting at bit ``pos``; returns (symbol, new pos)."""
+        if self.nsym == 1:
+            return self.single, pos
+        code = 0
+        for l in range(1, self.maxl + 1):
+            code = (code << 1) | bits[pos]
+            pos += 1
+            if l in self.by_len:
+                first, syms = self.by_len[l]
+                if 0 <= code - first < len(syms):
+                    return syms[code - first], pos
+        raise ValueError("invalid code in stream")
+
+
+def bit_reverse(value: int, nbits: int) -> int:
+    r = 0
+    for i in range(nbits):
+        r = (r << 1) | ((value >> i) & 1)
+    return r
+
+
+# --------------------------------------------------------------------------
+# Container (HLF1)
+# --------------------------------------------------------------------------
+
+def _align(x: int, a: int = SECTION_ALIGN) -> int:
+    return (x + a - 1) // a * a
+
+
+def layout(rows: int, cols: int, seg_len: int) -> Dict[str, int]:
+    n = rows * cols
+    n_seg = n // seg_len
+    n_grp = (n_seg + GROUP_SEGS - 1) // GROUP_SEGS
+    off_seg_bits = HEADER_BYTES
+    off_grp_off = _align(off_seg_bits + 2 * n_seg)
+    off_stream = _align(off_grp_off + 4 * (n_grp + 1))
+    return dict(n=n, n_seg=n_seg, n_grp=n_grp, off_seg_bits=off_seg_bits,
+                off_grp_off=off_grp_off, off_stream=off_stream)
+
+
+def check_shape(rows: int, cols: int, seg_len: int, lmax: int) -> None:
+    if rows < 1 or cols < 1:
+        raise ValueError("empty matrix")
+    if not (4 <= lmax <= 15):
+        raise ValueError("lmax must be in [4, 15]")
+    if seg_len < 8 or seg_len > 512 or seg_len % 8 or cols % seg_len:
+        raise ValueError("segment length must be a multiple of 8 in [8, 512] dividing cols")
+
+
+def raw_pos(idx: np.ndarray, n_seg: int, seg_len: int) -> np.ndarray:
+    """Byte offset in the raw plane of the weights with row-major indices ``idx``.
+
+    Group g holds segments 64g .. 64g+G-1 (G = 64 except maybe the last) and
+    starts at byte 64*S*g. Weight t of the segment with in-group index lam is
+    stored at ((t // 8) * G + lam) * 8 + t % 8 within its group."""
+    idx = np.asarray(idx, dtype=np.int64)
+    j = idx // seg_len
+    t = idx % seg_len
+    g = j // GROUP_SEGS
+    lam = j % GROUP_SEGS
+    G = np.minimum(GROUP_SEGS, n_seg - g * GROUP_SEGS)
+    return g * GROUP_SEGS * seg_len + ((t // RAW_UNIT) * G + lam) * RAW_UNIT + (t % RAW_UNIT)
+
+
+def build_codebooks(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode]:
+    """Per-matrix codebooks for the two exponent nibbles (Sec. 5.1)."""
+    _, eh, el, _ = split_fields(w)
+    return FieldCode.from_freqs(histogram(eh), lmax), FieldCode.from_freqs(histogram(el), lmax)
+
+
+def segment_stream(eh_seg, el_seg, ceh: FieldCode, cel: FieldCode) -> Tuple[int, int]:
+    """Bit stream of one segment as (integer, bit count).
+
+    For each weight in order: code(eh) then code(el), each emitted MSB-first;
+    stream bit k is bit k of the integer (least-significant first)."""
+    rev_eh = [bit_reverse(ceh.codes[v], ceh.lengths[v]) for v in range(NSYM)]
+    rev_el = [bit_reverse(cel.codes[v], cel.lengths[v]) for v in range(NSYM)]
+    acc = 0
+    pos = 0
+    for a, b in zip(eh_seg, el_seg):
+        la = ceh.lengths[a] if ceh.nsym > 1 else 0
+        lb = cel.lengths[b] if cel.nsym > 1 else 0
+        acc |= (rev_eh[a] | (rev_el[b] << la)) << pos
+        pos += la + lb
+    return acc, pos
+
+
+def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
+           codebooks: Tuple[FieldCode, FieldCode] = None) -> bytes:
+    """Compress a bf16 matrix [rows, cols] (uint16 bit patterns) into HLF1 bytes."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    rows, cols = w.shape
+    check_shape(rows, cols, seg_len, lmax)
+    ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
+    lay = layout(rows, cols, seg_len)
+    n, n_seg, n_grp = lay["n"], lay["n_seg"], lay["n_grp"]
+    s, eh, el, m = split_fields(w.ravel())
+    eh_l, el_l = eh.tolist(), el.tolist()
+
+    seg_bits = np.zeros(n_seg, dtype=np.uint16)
+    grp_off = np.zeros(n_grp + 1, dtype=np.uint32)
+    chunks: List[bytes] = []
+    units_total = 0
+    max_units = 0
+    for g in range(n_grp):
+        gacc, gpos = 0, 0
+        for j in range(g * GROUP_SEGS, min(n_seg, (g + 1) * GROUP_SEGS)):
+            a, b = j * seg_len, (j + 1) * seg_len
+            acc, nb = segment_stream(eh_l[a:b], el_l[a:b], ceh, cel)
+            seg_bits[j] = nb
+            gacc |= acc << gpos
+            gpos += nb
+        units = (gpos + 127) // 128
+        chunks.append(gacc.to_bytes(units * UNIT_BYTES, "little"))
+        grp_off[g] = units_total
+        units_total += units
+        max_units = max(max_units, units)
+    grp_off[n_grp] = units_total
+    stream = b"".join(chunks)
+
+    off_raw = _align(lay["off_stream"] + len(stream))
+    total = off_raw + n
+    raw = np.zeros(n, dtype=np.uint8)
+    raw[raw_pos(np.arange(n), n_seg, seg_len)] = raw_byte(s, m)
+
+    out = bytearray(total)
+    out[0:HEADER_BYTES] = pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, lay["off_seg_bits"],
+                                      lay["off_grp_off"], lay["off_stream"], off_raw, total,
+                                      max_units, ceh, cel)
+    out[lay["off_seg_bits"]:lay["off_seg_bits"] + 2 * n_seg] = seg_bits.tobytes()
+    out[lay["off_grp_off"]:lay["off_grp_off"] + 4 * (n_grp + 1)] = grp_off.tobytes()
+    out[lay["off_stream"]:lay["off_stream"] + len(stream)] = stream
+    out[off_raw:off_raw + n] = raw.tobytes()
+    return bytes(out)
+
+
+HEADER_FMT = "<IHBBQQIIQQQQQQQIBBBB16s16s"
+
+
+def pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, off_sb, off_go, off_st, off_raw, total,
+                max_units, ceh: FieldCode, cel: FieldCode) -> bytes:
+    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, 0, rows, cols, seg_len, GROUP_SEGS,
+                    n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units,
+                    ceh.nsym, cel.nsym, ceh.single, cel.single,
+                    bytes(ceh.lengths), bytes(cel.lengths))
+    assert len(h) == HEADER_BYTES
+    return h
+
+
+def parse_header(blob: bytes) -> Dict[str, object]:
+    f = struct.unpack(HEADER_FMT, blob[:HEADER_BYTES])
+    keys = ["magic", "version", "lmax", "flags", "rows", "cols", "seg_len", "grp_segs", "n_seg",
+            "n_grp", "off_seg_bits", "off_grp_off", "off_stream", "off_raw", "total_bytes",
+            "max_grp_units", "eh_nsym", "el_nsym", "eh_single", "el_single", "eh_len", "el_len"]
+    h = dict(zip(keys, f))
+    h["eh_len"] = list(h["eh_len"])
+    h["el_len"] = list(h["el_len"])
+    if h["magic"] != MAGIC or h["version"] != VERSION:
+        raise ValueError("not an HLF1 container")
+    return h
+
+
+def header_codebooks(h) -> Tuple[FieldCode, FieldCode]:
+    return (FieldCode(h["eh_len"], h["eh_nsym"], h["eh_single"]),
+            FieldCode(h["el_len"], h["el_nsym"], h["el_single"]))
+
+
+def _sections(blob: bytes, h):
+    n_seg, n_grp = h["n_seg"], h["n_grp"]
+    seg_bits = np.frombuffer(blob, np.uint16, n_seg, h["off_seg_bits"])
+    grp_off = np.frombuffer(blob, np.uint32, n_grp + 1, h["off_grp_off"])
+    return seg_bits, grp_off
+
+
+def decode_segments(blob: bytes, segs: Sequence[int]) -> Dict[int, np.ndarray]:
+    """Bit-serial decode of selected segments; returns {segment: uint16[S]}."""
+    h = parse_header(blob)
+    ceh, cel = header_codebooks(h)
+    S = h["seg_len"]
+    seg_bits, grp_off = _sections(blob, h)
+    n_seg = h["n_seg"]
+    raw_plane = np.frombuffer(blob, np.uint8, n_seg * S, h["off_raw"])
+    out = {}
+    by_group: Dict[int, List[int]] = {}
+    for j in segs:
+        by_group.setdefault(j // GROUP_SEGS, []).append(j)
+    for g, js in by_group.items():
+        a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
+        b = h["off_stream"] + int(grp_off[g + 1]) * UNIT_BYTES
+        bits = np.unpackbits(np.frombuffer(blob[a:b], np.uint8), bitorder="little").tolist()
+        starts = {}
+        p = 0
+        for j in range(g * GROUP_SEGS, min(n_seg, (g + 1) * GROUP_SEGS)):
+            starts[j] = p
+            p += int(seg_bits[j])
+        for j in js:
+            pos = starts[j]
+            eh = np.zeros(S, np.uint32)
+            el = np.zeros(S, np.uint32)
+            for t in range(S):
+                eh[t], pos = ceh.decode_one(bits, pos)
+                el[t], pos = cel.decode_one(bits, pos)
+            if pos - starts[j] != int(seg_bits[j]):
+                raise ValueError("segment length mismatch")
+            rawpos = raw_pos(np.arange(j * S, (j + 1) * S), n_seg, S)
+            r = raw_plane[rawpos].astype(np.uint32)
+            out[j] = join_fields(r >> 7, eh, el, r & 0x7F)
+    return out
+
+
+def decode(blob: bytes) -> np.ndarray:
+    """Decompress a whole HLF1 container back to the bf16 matrix (uint16)."""
+    h = parse_header(blob)
+    S = h["seg_len"]
+    segs = decode_segments(blob, range(h["n_seg"]))
+    w = np.concatenate([segs[j] for j in range(h["n_seg"])])
+    return w.reshape(h["rows"], h["cols"])
+
+
+def payload_bits(w: np.ndarray, ceh: FieldCode, cel: FieldCode) -> int:
+    """Sum of code lengths plus 8 raw bits per weight (size without metadata)."""
+    _, eh, el, _ = split_fields(w)
+    he, hl = histogram(eh), histogram(el)
+    le = ceh.lengths if ceh.nsym > 1 else [0] * NSYM
+    ll = cel.lengths if cel.nsym > 1 else [0] * NSYM
+    return sum(f * l for f, l in zip(he, le)) + sum(f * l for f, l in zip(hl, ll)) + 8 * int(np.size(w))
