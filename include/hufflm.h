@@ -1,0 +1,185 @@
+/*
+ * hufflm.h - C ABI of the Huff-LLM bf16 weight codec and its fused
+ * decode-GEMV for AMD gfx950 (MI355X).
+ *
+ * Method: Huff-LLM (arXiv 2502.00922). A bf16 weight is split 1-4-4-7
+ * (Sec. 5.1): sign and 7 mantissa bits are kept raw; the 8 exponent bits are
+ * two 4-bit symbols, each coded with a per-matrix Huffman code (Sec. 3.1,
+ * Sec. 5.1). Compression runs once, offline, on the CPU (Sec. 3.1). Weights
+ * stay compressed in memory and are decoded only where they are multiplied
+ * (Sec. 1 contributions, Sec. 3.2): here inside y = W x, so that HBM carries
+ * only compressed bytes.
+ *
+ * ---------------------------------------------------------------------------
+ * HLF1 container (all integers little-endian)
+ * ---------------------------------------------------------------------------
+ * W is row-major [rows][cols]; weight i = r*cols + c.
+ * Fields of a weight w: s = w>>15, eh = (w>>11)&15, el = (w>>7)&15, m = w&127.
+ *
+ * Codebooks, one per field per matrix: histogram of the field over the whole
+ * matrix; Huffman code lengths from a binary heap keyed (weight, kind, id),
+ * kind 0 = leaf with id = symbol, kind 1 = internal node with id = creation
+ * order, the two smallest keys merged first; if the longest code exceeds lmax
+ * the lengths are replaced by package-merge lengths (items sorted by
+ * (weight, symbol); lmax-1 rounds of pairing consecutive items and stable
+ * merging with the leaves by (weight, kind); the first 2(n-1) items of the
+ * last list are taken; length = occurrences). A field with one present
+ * symbol has length 0 and emits no bits. Code values are canonical (RFC 1951
+ * Sec. 3.2.2 assignment).
+ *
+ * Tiling: segment (r, cs) is W[r][cs*S .. cs*S+S) (S divides cols, S % 8 == 0,
+ * 8 <= S <= 512, L = cols/S segments per row). Row block rb is rows
+ * 64rb .. 64rb+G-1 (G = 64, or fewer in the last block). Group g = rb*L + cs
+ * holds the G segments (64rb + lam, cs), lam = 0..G-1: 64 rows sharing one
+ * column range, one row per lane of a 64-wide wavefront. Segments are
+ * numbered in group order: group g starts at segment 64*L*rb + cs*G.
+ *
+ * Stream: for each weight of a segment in order, code(eh) then code(el),
+ * each emitted most-significant bit first; the stream is packed least
+ * significant bit first (bit k is bit k%8 of byte k/8). The segments of a
+ * group are concatenated in lane order without gaps; each group stream starts on a 16-byte
+ * boundary and is zero-padded to a multiple of 128 bits.
+ *
+ * Layout (sections start at 64-byte boundaries, zero padding between):
+ *   0      header (128 bytes, below)
+ *   off_seg_bits  uint16 seg_bits[n_seg]   code bits of each segment
+ *   off_grp_off   uint32 grp_off[n_grp+1]  group stream start, in 16-byte
+ *                                          units from off_stream
+ *   off_stream    group streams
+ *   off_raw       uint8 raw[n]: (s<<7)|m; group g starts at S times its first
+ *                 segment number; weight t of lane lam is at ((t/8)*G + lam)*8
+ *                 + t%8 within the group
+ *   total_bytes = off_raw + n
+ * Header: u32 magic 0x31464C48 ('HLF1'), u16 version 1, u8 lmax, u8 flags 0,
+ *   u64 rows, u64 cols, u32 seg_len, u32 group_rows (64), u64 n_seg,
+ *   u64 n_grp, u64 off_seg_bits, u64 off_grp_off, u64 off_stream,
+ *   u64 off_raw, u64 total_bytes, u32 max_grp_units, u8 eh_nsym, u8 el_nsym,
+ *   u8 eh_single, u8 el_single, u8 eh_len[16], u8 el_len[16].
+ *
+ * ---------------------------------------------------------------------------
+ * Conventions of the ABI
+ * ---------------------------------------------------------------------------
+ * Pointers named *_dev are device (HBM) pointers; all others are host. The
+ * caller owns every buffer; the library allocates no device memory and keeps
+ * no state across calls. `stream` is a hipStream_t (NULL = default stream).
+ * Launch functions are asynchronous: they validate arguments on the host,
+ * enqueue kernels and return; HL_EHIP reports a failed launch. Corruption
+ * that only the device could see is not reported: kernels clamp every read
+ * to the container, so a damaged stream gives wrong weights, never a fault.
+ * No function throws; all are reentrant.
+ */
+#ifndef HUFFLM_H
+#define HUFFLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HL_OK = 0,
+  HL_EINVAL = 1,        /* bad argument (null pointer, size, range) */
+  HL_ENOMEM = 2,        /* output buffer too small / host allocation failed */
+  HL_ECORRUPT = 3,      /* container fails validation */
+  HL_EUNSUPPORTED = 4,  /* valid request this build does not handle */
+  HL_EHIP = 5           /* HIP runtime error */
+} hl_status;
+
+typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
+
+#define HL_MAGIC 0x31464C48u
+#define HL_VERSION 1u
+#define HL_HEADER_BYTES 128u
+#define HL_GROUP_ROWS 64u
+#define HL_MAX_BATCH 16u
+#define HL_LUT_BYTES 16640u   /* 4096 joint entries + 64 words of tables */
+
+typedef struct {
+  uint8_t nsym;     /* symbols present in the field (1..16) */
+  uint8_t single;   /* the symbol when nsym == 1, else 0 */
+  uint8_t len[16];  /* code length per symbol; 0 = absent (or the only one) */
+} hl_field_code;
+
+typedef struct {
+  uint32_t lmax;    /* code-length limit used to build the lengths, 4..15 */
+  hl_field_code eh; /* exponent bits 7..4 */
+  hl_field_code el; /* exponent bits 3..0 */
+} hl_codebook;
+
+/* Non-owning view of one container resident in device memory. */
+typedef struct {
+  const uint8_t* blob_dev;   /* whole container */
+  uint32_t* lut_dev;         /* HL_LUT_BYTES, filled by hl_tensor_prepare */
+  uint64_t rows, cols, n_seg, n_grp, total_bytes;
+  uint64_t off_seg_bits, off_grp_off, off_stream, off_raw;
+  uint32_t seg_len, lmax, max_grp_units, reserved;
+  hl_codebook cb;
+} hl_tensor;
+
+/* Text of a status code (static storage). */
+const char* hl_status_str(hl_status s);
+
+/* Segment length the encoder uses for `cols` when asked for 0: among the
+ * multiples of 8 in [8, 512] that divide cols, the one nearest to 128 (by
+ * ratio; the larger on a tie); 0 if there is none. */
+uint32_t hl_default_seg_len(uint64_t cols);
+
+/* Per-matrix codebooks of the two exponent fields (Sec. 5.1) from n bf16
+ * bit patterns. lmax in [4, 15] (12 matches the maximum code length the paper
+ * reports, Sec. 5.2). Errors: HL_EINVAL for n == 0, null pointers or lmax out
+ * of range. */
+hl_status hl_build_codebook(const uint16_t* w_bf16, size_t n, uint32_t lmax,
+                            hl_codebook* out);
+
+/* Encode W [rows][cols] (bf16 bit patterns, host) into an HLF1 container
+ * (Sec. 3.1: once, offline, on the CPU). seg_len 0 selects
+ * hl_default_seg_len(cols). With out == NULL, *out_bytes receives the exact
+ * size; otherwise *out_bytes is the capacity of `out` on entry and the size
+ * written on return (HL_ENOMEM if too small). nthreads 0 = all cores; the
+ * output does not depend on nthreads. Errors: HL_EINVAL (shape, seg_len, a
+ * weight whose field has no code in `cb`). */
+hl_status hl_encode(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,
+                    const hl_codebook* cb, uint32_t seg_len, uint32_t nthreads,
+                    void* out, size_t* out_bytes);
+
+/* Full structural check of a container held in host memory: header, section
+ * offsets, codebooks (Kraft sum exactly 1, lengths <= lmax), per-group
+ * stream sizes against seg_bits. O(n_seg). Returns HL_OK or HL_ECORRUPT. */
+hl_status hl_validate(const void* blob_host, size_t blob_bytes);
+
+/* Build a device view of a container copied to `blob_dev` (blob_bytes long)
+ * from its header (the first HL_HEADER_BYTES, host copy). Checks the header
+ * (O(1)); lut_dev must point to HL_LUT_BYTES of device memory that the view
+ * uses from now on. Errors: HL_EINVAL, HL_ECORRUPT. */
+hl_status hl_tensor_view(const void* blob_dev, const void* header_host,
+                         size_t blob_bytes, uint32_t* lut_dev, hl_tensor* out);
+
+/* Fill t->lut_dev on the device: the joint decode table of the two codes for
+ * a 12-bit window (the decoder's L_max-bit window match of Sec. 3.2) and the
+ * per-length canonical tables used for pairs longer than the window. */
+hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
+
+/* Decode the whole matrix to bf16 bit patterns, out_dev[rows*cols]
+ * (row-major). Bit-exact with the encoder's input. */
+hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream);
+
+/* y[b][r] = sum_k W[r][k] * x[b][k] for b < batch, decoding W on the fly in
+ * registers (Sec. 3.2: weights are decompressed only to be multiplied).
+ * x_dev: [batch][cols] float32 or bf16; y_dev: [batch][rows] float32. fp32
+ * accumulation. batch in [1, 16]. Errors: HL_EINVAL. */
+hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype,
+                         uint32_t batch, float* y_dev, void* stream);
+
+/* Uncompressed comparator: the same product from plain bf16 W [rows][cols]
+ * in device memory. */
+hl_status hl_gemv_bf16(const uint16_t* w_dev, uint64_t rows, uint64_t cols,
+                       const void* x_dev, hl_dtype x_dtype, uint32_t batch,
+                       float* y_dev, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HUFFLM_H */

@@ -24,10 +24,15 @@ codes emitted most-significant bit first into a stream packed least-significant
 bit first; a one-symbol field gets code length 0; segments of S weights along a
 row are the unit of independent decoding.
 
+Tiling: segment (r, cs) holds W[r, cs*S : cs*S+S]; row block rb holds rows
+64rb .. 64rb+G-1 (G = 64 except maybe the last block); group g = rb*L + cs
+(L = cols/S) holds the G segments (64rb + lam, cs), lam = 0..G-1.
+
 Container layout (little-endian; sections start at 64-byte boundaries):
-  header (128 B), seg_bits u16[n_seg], grp_off u32[n_grp + 1] (16-byte
-  units), stream (one 16-byte aligned bit stream per group of 64 segments),
-  raw u8[n] (sign<<7 | mantissa, interleaved per group in 8-byte units).
+  header (128 B), seg_bits u16[n_seg] in group order, grp_off u32[n_grp + 1]
+  (16-byte units), stream (one 16-byte aligned bit stream per group),
+  raw u8[n] (sign<<7 | mantissa; group g's bytes start at S times the number
+  of segments before it; weight t of lane lam at ((t // 8) * G + lam) * 8 + t % 8).
 """
 from __future__ import annotations
 
@@ -42,7 +47,7 @@ import numpy as np
 MAGIC = 0x31464C48          # 'HLF1'
 VERSION = 1
 HEADER_BYTES = 128
-GROUP_SEGS = 64             # segments per group (one per lane of a 64-wide wavefront)
+GROUP_ROWS = 64             # rows per group (one per lane of a 64-wide wavefront)
 RAW_UNIT = 8                # bytes of one segment's raw plane stored contiguously
 UNIT_BYTES = 16             # group streams are padded to 128 bits
 SECTION_ALIGN = 64
@@ -255,12 +260,22 @@ def _align(x: int, a: int = SECTION_ALIGN) -> int:
 def layout(rows: int, cols: int, seg_len: int) -> Dict[str, int]:
     n = rows * cols
     n_seg = n // seg_len
-    n_grp = (n_seg + GROUP_SEGS - 1) // GROUP_SEGS
+    L = cols // seg_len
+    n_grp = (rows + GROUP_ROWS - 1) // GROUP_ROWS * L
     off_seg_bits = HEADER_BYTES
     off_grp_off = _align(off_seg_bits + 2 * n_seg)
     off_stream = _align(off_grp_off + 4 * (n_grp + 1))
-    return dict(n=n, n_seg=n_seg, n_grp=n_grp, off_seg_bits=off_seg_bits,
+    return dict(n=n, n_seg=n_seg, n_grp=n_grp, L=L, off_seg_bits=off_seg_bits,
                 off_grp_off=off_grp_off, off_stream=off_stream)
+
+
+def group_geometry(rows: int, cols: int, seg_len: int, g: int) -> Tuple[int, int, int, int]:
+    """(first row, rows G, column segment cs, index of the group's first segment)."""
+    L = cols // seg_len
+    rb, cs = divmod(g, L)
+    r0 = rb * GROUP_ROWS
+    G = min(GROUP_ROWS, rows - r0)
+    return r0, G, cs, r0 * L + cs * G
 
 
 def check_shape(rows: int, cols: int, seg_len: int, lmax: int) -> None:
@@ -272,19 +287,16 @@ def check_shape(rows: int, cols: int, seg_len: int, lmax: int) -> None:
         raise ValueError("segment length must be a multiple of 8 in [8, 512] dividing cols")
 
 
-def raw_pos(idx: np.ndarray, n_seg: int, seg_len: int) -> np.ndarray:
-    """Byte offset in the raw plane of the weights with row-major indices ``idx``.
-
-    Group g holds segments 64g .. 64g+G-1 (G = 64 except maybe the last) and
-    starts at byte 64*S*g. Weight t of the segment with in-group index lam is
-    stored at ((t // 8) * G + lam) * 8 + t % 8 within its group."""
-    idx = np.asarray(idx, dtype=np.int64)
-    j = idx // seg_len
-    t = idx % seg_len
-    g = j // GROUP_SEGS
-    lam = j % GROUP_SEGS
-    G = np.minimum(GROUP_SEGS, n_seg - g * GROUP_SEGS)
-    return g * GROUP_SEGS * seg_len + ((t // RAW_UNIT) * G + lam) * RAW_UNIT + (t % RAW_UNIT)
+def raw_pos(r: np.ndarray, c: np.ndarray, rows: int, cols: int, seg_len: int) -> np.ndarray:
+    """Byte offset in the raw plane of weight (r, c)."""
+    r = np.asarray(r, dtype=np.int64)
+    c = np.asarray(c, dtype=np.int64)
+    L = cols // seg_len
+    rb, lam = r // GROUP_ROWS, r % GROUP_ROWS
+    cs, t = c // seg_len, c % seg_len
+    G = np.minimum(GROUP_ROWS, rows - rb * GROUP_ROWS)
+    first_seg = rb * GROUP_ROWS * L + cs * G
+    return first_seg * seg_len + ((t // RAW_UNIT) * G + lam) * RAW_UNIT + (t % RAW_UNIT)
 
 
 def build_codebooks(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode]:
@@ -319,8 +331,8 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
     lay = layout(rows, cols, seg_len)
     n, n_seg, n_grp = lay["n"], lay["n_seg"], lay["n_grp"]
-    s, eh, el, m = split_fields(w.ravel())
-    eh_l, el_l = eh.tolist(), el.tolist()
+    s, eh, el, m = split_fields(w)                       # [rows, cols] each
+    S = seg_len
 
     seg_bits = np.zeros(n_seg, dtype=np.uint16)
     grp_off = np.zeros(n_grp + 1, dtype=np.uint32)
@@ -328,11 +340,13 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     units_total = 0
     max_units = 0
     for g in range(n_grp):
+        r0, G, cs, first = group_geometry(rows, cols, S, g)
         gacc, gpos = 0, 0
-        for j in range(g * GROUP_SEGS, min(n_seg, (g + 1) * GROUP_SEGS)):
-            a, b = j * seg_len, (j + 1) * seg_len
-            acc, nb = segment_stream(eh_l[a:b], el_l[a:b], ceh, cel)
-            seg_bits[j] = nb
+        for lam in range(G):
+            r = r0 + lam
+            a, b = cs * S, cs * S + S
+            acc, nb = segment_stream(eh[r, a:b].tolist(), el[r, a:b].tolist(), ceh, cel)
+            seg_bits[first + lam] = nb
             gacc |= acc << gpos
             gpos += nb
         units = (gpos + 127) // 128
@@ -345,8 +359,9 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
 
     off_raw = _align(lay["off_stream"] + len(stream))
     total = off_raw + n
+    rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
     raw = np.zeros(n, dtype=np.uint8)
-    raw[raw_pos(np.arange(n), n_seg, seg_len)] = raw_byte(s, m)
+    raw[raw_pos(rr.ravel(), cc.ravel(), rows, cols, S)] = raw_byte(s, m).ravel()
 
     out = bytearray(total)
     out[0:HEADER_BYTES] = pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, lay["off_seg_bits"],
@@ -364,7 +379,7 @@ HEADER_FMT = "<IHBBQQIIQQQQQQQIBBBB16s16s"
 
 def pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, off_sb, off_go, off_st, off_raw, total,
                 max_units, ceh: FieldCode, cel: FieldCode) -> bytes:
-    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, 0, rows, cols, seg_len, GROUP_SEGS,
+    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, 0, rows, cols, seg_len, GROUP_ROWS,
                     n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units,
                     ceh.nsym, cel.nsym, ceh.single, cel.single,
                     bytes(ceh.lengths), bytes(cel.lengths))
@@ -374,7 +389,7 @@ def pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, off_sb, off_go, off_st,
 
 def parse_header(blob: bytes) -> Dict[str, object]:
     f = struct.unpack(HEADER_FMT, blob[:HEADER_BYTES])
-    keys = ["magic", "version", "lmax", "flags", "rows", "cols", "seg_len", "grp_segs", "n_seg",
+    keys = ["magic", "version", "lmax", "flags", "rows", "cols", "seg_len", "grp_rows", "n_seg",
             "n_grp", "off_seg_bits", "off_grp_off", "off_stream", "off_raw", "total_bytes",
             "max_grp_units", "eh_nsym", "el_nsym", "eh_single", "el_single", "eh_len", "el_len"]
     h = dict(zip(keys, f))
@@ -390,56 +405,48 @@ def header_codebooks(h) -> Tuple[FieldCode, FieldCode]:
             FieldCode(h["el_len"], h["el_nsym"], h["el_single"]))
 
 
-def _sections(blob: bytes, h):
-    n_seg, n_grp = h["n_seg"], h["n_grp"]
-    seg_bits = np.frombuffer(blob, np.uint16, n_seg, h["off_seg_bits"])
-    grp_off = np.frombuffer(blob, np.uint32, n_grp + 1, h["off_grp_off"])
-    return seg_bits, grp_off
-
-
-def decode_segments(blob: bytes, segs: Sequence[int]) -> Dict[int, np.ndarray]:
-    """Bit-serial decode of selected segments; returns {segment: uint16[S]}."""
+def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, np.ndarray]:
+    """Bit-serial decode of one group; returns (first row, G, cs, uint16[G, S])."""
     h = parse_header(blob)
     ceh, cel = header_codebooks(h)
-    S = h["seg_len"]
-    seg_bits, grp_off = _sections(blob, h)
-    n_seg = h["n_seg"]
-    raw_plane = np.frombuffer(blob, np.uint8, n_seg * S, h["off_raw"])
-    out = {}
-    by_group: Dict[int, List[int]] = {}
-    for j in segs:
-        by_group.setdefault(j // GROUP_SEGS, []).append(j)
-    for g, js in by_group.items():
-        a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
-        b = h["off_stream"] + int(grp_off[g + 1]) * UNIT_BYTES
-        bits = np.unpackbits(np.frombuffer(blob[a:b], np.uint8), bitorder="little").tolist()
-        starts = {}
-        p = 0
-        for j in range(g * GROUP_SEGS, min(n_seg, (g + 1) * GROUP_SEGS)):
-            starts[j] = p
-            p += int(seg_bits[j])
-        for j in js:
-            pos = starts[j]
-            eh = np.zeros(S, np.uint32)
-            el = np.zeros(S, np.uint32)
-            for t in range(S):
-                eh[t], pos = ceh.decode_one(bits, pos)
-                el[t], pos = cel.decode_one(bits, pos)
-            if pos - starts[j] != int(seg_bits[j]):
-                raise ValueError("segment length mismatch")
-            rawpos = raw_pos(np.arange(j * S, (j + 1) * S), n_seg, S)
-            r = raw_plane[rawpos].astype(np.uint32)
-            out[j] = join_fields(r >> 7, eh, el, r & 0x7F)
-    return out
+    rows, cols, S = h["rows"], h["cols"], h["seg_len"]
+    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
+    grp_off = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    raw_plane = np.frombuffer(blob, np.uint8, rows * cols, h["off_raw"])
+    r0, G, cs, first = group_geometry(rows, cols, S, g)
+    a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
+    b = h["off_stream"] + int(grp_off[g + 1]) * UNIT_BYTES
+    bits = np.unpackbits(np.frombuffer(blob[a:b], np.uint8), bitorder="little").tolist()
+    out = np.zeros((G, S), dtype=np.uint16)
+    pos = 0
+    for lam in range(G):
+        start = pos
+        eh = np.zeros(S, np.uint32)
+        el = np.zeros(S, np.uint32)
+        for t in range(S):
+            eh[t], pos = ceh.decode_one(bits, pos)
+            el[t], pos = cel.decode_one(bits, pos)
+        if pos - start != int(seg_bits[first + lam]):
+            raise ValueError("segment length mismatch")
+        rp = raw_pos(np.full(S, r0 + lam), cs * S + np.arange(S), rows, cols, S)
+        r = raw_plane[rp].astype(np.uint32)
+        out[lam] = join_fields(r >> 7, eh, el, r & 0x7F)
+    return r0, G, cs, out
+
+
+def decode_rows(blob: bytes, row_block: int) -> np.ndarray:
+    """Decode the 64-row block ``row_block`` (all column segments)."""
+    h = parse_header(blob)
+    S, L = h["seg_len"], h["cols"] // h["seg_len"]
+    parts = [decode_group(blob, row_block * L + cs)[3] for cs in range(L)]
+    return np.concatenate(parts, axis=1)
 
 
 def decode(blob: bytes) -> np.ndarray:
     """Decompress a whole HLF1 container back to the bf16 matrix (uint16)."""
     h = parse_header(blob)
-    S = h["seg_len"]
-    segs = decode_segments(blob, range(h["n_seg"]))
-    w = np.concatenate([segs[j] for j in range(h["n_seg"])])
-    return w.reshape(h["rows"], h["cols"])
+    rb_count = (h["rows"] + GROUP_ROWS - 1) // GROUP_ROWS
+    return np.concatenate([decode_rows(blob, rb) for rb in range(rb_count)], axis=0)
 
 
 def payload_bits(w: np.ndarray, ceh: FieldCode, cel: FieldCode) -> int:
@@ -449,3 +456,30 @@ def payload_bits(w: np.ndarray, ceh: FieldCode, cel: FieldCode) -> int:
     le = ceh.lengths if ceh.nsym > 1 else [0] * NSYM
     ll = cel.lengths if cel.nsym > 1 else [0] * NSYM
     return sum(f * l for f, l in zip(he, le)) + sum(f * l for f, l in zip(hl, ll)) + 8 * int(np.size(w))
+
+
+def container_size(w: np.ndarray, seg_len: int, lmax: int = 12,
+                   codebooks: Tuple[FieldCode, FieldCode] = None) -> Dict[str, int]:
+    """Exact container size of ``encode(w, seg_len, lmax)`` from the code lengths
+    alone (sum of code lengths per segment, 128-bit padding per group, section
+    alignment), without building the stream."""
+    w = np.asarray(w, dtype=np.uint16)
+    rows, cols = w.shape
+    check_shape(rows, cols, seg_len, lmax)
+    ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
+    _, eh, el, _ = split_fields(w)
+    le = np.array(ceh.lengths if ceh.nsym > 1 else [0] * NSYM, dtype=np.int64)
+    ll = np.array(cel.lengths if cel.nsym > 1 else [0] * NSYM, dtype=np.int64)
+    L = cols // seg_len
+    seg = (le[eh] + ll[el]).reshape(rows, L, seg_len).sum(axis=2)       # [rows, L]
+    units = 0
+    max_units = 0
+    for rb in range(0, rows, GROUP_ROWS):
+        per_cs = seg[rb:rb + GROUP_ROWS].sum(axis=0)                      # [L]
+        u = (per_cs + 127) // 128
+        units += int(u.sum())
+        max_units = max(max_units, int(u.max()))
+    lay = layout(rows, cols, seg_len)
+    off_raw = _align(lay["off_stream"] + units * UNIT_BYTES)
+    return dict(total_bytes=off_raw + rows * cols, stream_units=units, max_grp_units=max_units,
+                code_bits=int(seg.sum()), off_raw=off_raw)

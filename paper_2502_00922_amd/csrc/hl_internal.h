@@ -1,0 +1,35 @@
+// Internal declarations shared by the host codec and the device launchers.
+#pragma once
+#include <cstdint>
+
+#include "hufflm.h"
+
+namespace hl {
+
+struct Layout {
+  uint64_t n, n_seg, n_grp, L, off_seg_bits, off_grp_off, off_stream;
+};
+
+// Group g = rb*L + cs: rows r0 .. r0+G-1, column segment cs; `first` is the
+// group-order number of its first segment.
+struct GroupGeom {
+  uint64_t r0, cs, first;
+  uint32_t G;
+};
+GroupGeom group_geom(uint64_t rows, uint64_t L, uint64_t g);
+
+struct Header {
+  uint64_t rows, cols, n_seg, n_grp, off_seg_bits, off_grp_off, off_stream, off_raw, total_bytes;
+  uint32_t seg_len, max_grp_units;
+  hl_codebook cb;
+};
+
+bool shape_ok(uint64_t rows, uint64_t cols, uint32_t S);
+Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S);
+bool parse_header(const uint8_t* h, Header* out);
+bool header_consistent(const Header& h, uint64_t blob_bytes);
+bool field_code_valid(const hl_field_code& fc, uint32_t lmax);
+void canonical_codes(const uint8_t len[16], uint32_t code[16]);
+uint32_t default_seg_len(uint64_t cols);
+
+}  // namespace hl

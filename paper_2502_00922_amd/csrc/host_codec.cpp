@@ -1,0 +1,460 @@
+// Host side of the Huff-LLM bf16 codec: codebooks, HLF1 encoder, validation.
+//
+// Huff-LLM (arXiv 2502.00922): weights are split into bit fields and each
+// coded field gets its own Huffman code, once, offline, on the CPU (Sec. 3.1);
+// for bf16 the split is 1-4-4-7 with the sign and mantissa kept raw
+// (Sec. 5.1). The container layout and the tie rules are specified in
+// include/hufflm.h.
+#include "hufflm.h"
+#include "hl_internal.h"
+
+#include <algorithm>
+#include <array>
+#include <cstring>
+#include <functional>
+#include <queue>
+#include <thread>
+#include <tuple>
+#include <vector>
+
+namespace hl {
+
+// ---------------------------------------------------------------- code lengths
+
+// Huffman lengths with the heap order (weight, kind, id); see the header.
+static void huffman_lengths(const uint64_t f[16], uint8_t len[16]) {
+  using Key = std::tuple<uint64_t, int, int>;  // weight, kind (0 leaf / 1 node), id
+  std::priority_queue<Key, std::vector<Key>, std::greater<Key>> heap;
+  for (int s = 0; s < 16; ++s) {
+    len[s] = 0;
+    if (f[s]) heap.emplace(f[s], 0, s);
+  }
+  if (heap.size() <= 1) return;
+  // children of internal node id: (kind, id) pairs
+  std::vector<std::array<int, 4>> kids;
+  while (heap.size() > 1) {
+    Key a = heap.top(); heap.pop();
+    Key b = heap.top(); heap.pop();
+    int id = (int)kids.size();
+    kids.push_back({std::get<1>(a), std::get<2>(a), std::get<1>(b), std::get<2>(b)});
+    heap.emplace(std::get<0>(a) + std::get<0>(b), 1, id);
+  }
+  // depth-first walk from the root
+  std::vector<std::array<int, 3>> st;  // kind, id, depth
+  st.push_back({std::get<1>(heap.top()), std::get<2>(heap.top()), 0});
+  while (!st.empty()) {
+    auto [kind, id, d] = st.back();
+    st.pop_back();
+    if (kind == 0) {
+      len[id] = (uint8_t)d;
+    } else {
+      st.push_back({kids[id][0], kids[id][1], d + 1});
+      st.push_back({kids[id][2], kids[id][3], d + 1});
+    }
+  }
+}
+
+// Package-merge lengths limited to lmax; see the header for the item order.
+static void package_merge(const uint64_t f[16], int lmax, uint8_t len[16]) {
+  struct Item { uint64_t w; int kind; std::array<uint8_t, 16> cnt; };
+  std::vector<std::pair<uint64_t, int>> present;
+  for (int s = 0; s < 16; ++s) {
+    len[s] = 0;
+    if (f[s]) present.emplace_back(f[s], s);
+  }
+  std::sort(present.begin(), present.end());
+  const size_t n = present.size();
+  if (n <= 1) return;
+  std::vector<Item> leaves;
+  for (auto& p : present) {
+    Item it{p.first, 0, {}};
+    it.cnt[p.second] = 1;
+    leaves.push_back(it);
+  }
+  std::vector<Item> cur = leaves;
+  for (int round = 0; round < lmax - 1; ++round) {
+    std::vector<Item> next = leaves;
+    for (size_t i = 0; i + 1 < cur.size(); i += 2) {
+      Item pk{cur[i].w + cur[i + 1].w, 1, {}};
+      for (int s = 0; s < 16; ++s) pk.cnt[s] = (uint8_t)(cur[i].cnt[s] + cur[i + 1].cnt[s]);
+      next.push_back(pk);
+    }
+    std::stable_sort(next.begin(), next.end(), [](const Item& a, const Item& b) {
+      return a.w != b.w ? a.w < b.w : a.kind < b.kind;
+    });
+    cur.swap(next);
+  }
+  for (size_t i = 0; i < 2 * (n - 1) && i < cur.size(); ++i)
+    for (int s = 0; s < 16; ++s) len[s] = (uint8_t)(len[s] + cur[i].cnt[s]);
+}
+
+static void field_code_from_counts(const uint64_t f[16], int lmax, hl_field_code* fc) {
+  int nsym = 0, single = 0;
+  for (int s = 0; s < 16; ++s)
+    if (f[s]) { ++nsym; single = s; }
+  fc->nsym = (uint8_t)nsym;
+  fc->single = (uint8_t)(nsym == 1 ? single : 0);
+  huffman_lengths(f, fc->len);
+  int mx = 0;
+  for (int s = 0; s < 16; ++s) mx = std::max(mx, (int)fc->len[s]);
+  if (mx > lmax) package_merge(f, lmax, fc->len);
+}
+
+void canonical_codes(const uint8_t len[16], uint32_t code[16]) {
+  int bl_count[17] = {0};
+  uint32_t next_code[17] = {0};
+  for (int s = 0; s < 16; ++s)
+    if (len[s]) bl_count[len[s]]++;
+  uint32_t c = 0;
+  for (int bits = 1; bits <= 16; ++bits) {
+    c = (c + (uint32_t)bl_count[bits - 1]) << 1;
+    next_code[bits] = c;
+  }
+  for (int s = 0; s < 16; ++s) code[s] = len[s] ? next_code[len[s]]++ : 0;
+}
+
+static uint32_t bit_reverse(uint32_t v, int n) {
+  uint32_t r = 0;
+  for (int i = 0; i < n; ++i) r = (r << 1) | ((v >> i) & 1u);
+  return r;
+}
+
+// Checks lengths against the field's presence data: Kraft sum exactly one for
+// two or more symbols, all zero for one symbol, every length <= lmax.
+bool field_code_valid(const hl_field_code& fc, uint32_t lmax) {
+  if (fc.nsym < 1 || fc.nsym > 16) return false;
+  if (fc.nsym == 1) {
+    if (fc.single > 15) return false;
+    for (int s = 0; s < 16; ++s) if (fc.len[s]) return false;
+    return true;
+  }
+  if (fc.single != 0) return false;
+  int cnt = 0;
+  uint64_t kraft = 0;  // in units of 2^-15
+  for (int s = 0; s < 16; ++s) {
+    if (!fc.len[s]) continue;
+    if (fc.len[s] > lmax || fc.len[s] > 15) return false;
+    ++cnt;
+    kraft += 1ull << (15 - fc.len[s]);
+  }
+  return cnt == fc.nsym && kraft == (1ull << 15);
+}
+
+// ---------------------------------------------------------------- layout
+
+static uint64_t align64(uint64_t x) { return (x + 63) & ~uint64_t(63); }
+
+bool shape_ok(uint64_t rows, uint64_t cols, uint32_t S) {
+  return rows >= 1 && cols >= 1 && S >= 8 && S <= 512 && S % 8 == 0 && cols % S == 0 &&
+         rows <= (1ull << 40) / cols;
+}
+
+Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S) {
+  Layout L;
+  L.n = rows * cols;
+  L.n_seg = L.n / S;
+  L.L = cols / S;
+  L.n_grp = (rows + HL_GROUP_ROWS - 1) / HL_GROUP_ROWS * L.L;
+  L.off_seg_bits = HL_HEADER_BYTES;
+  L.off_grp_off = align64(L.off_seg_bits + 2 * L.n_seg);
+  L.off_stream = align64(L.off_grp_off + 4 * (L.n_grp + 1));
+  return L;
+}
+
+void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, const hl_codebook& cb,
+                 const Layout& L, uint64_t off_raw, uint64_t total, uint32_t max_units) {
+  std::memset(h, 0, HL_HEADER_BYTES);
+  auto put32 = [&](int o, uint32_t v) { std::memcpy(h + o, &v, 4); };
+  auto put64 = [&](int o, uint64_t v) { std::memcpy(h + o, &v, 8); };
+  put32(0, HL_MAGIC);
+  uint16_t ver = HL_VERSION;
+  std::memcpy(h + 4, &ver, 2);
+  h[6] = (uint8_t)cb.lmax;
+  h[7] = 0;
+  put64(8, rows);
+  put64(16, cols);
+  put32(24, S);
+  put32(28, HL_GROUP_ROWS);
+  put64(32, L.n_seg);
+  put64(40, L.n_grp);
+  put64(48, L.off_seg_bits);
+  put64(56, L.off_grp_off);
+  put64(64, L.off_stream);
+  put64(72, off_raw);
+  put64(80, total);
+  put32(88, max_units);
+  h[92] = cb.eh.nsym;
+  h[93] = cb.el.nsym;
+  h[94] = cb.eh.single;
+  h[95] = cb.el.single;
+  std::memcpy(h + 96, cb.eh.len, 16);
+  std::memcpy(h + 112, cb.el.len, 16);
+}
+
+bool parse_header(const uint8_t* h, Header* o) {
+  auto get32 = [&](int off) { uint32_t v; std::memcpy(&v, h + off, 4); return v; };
+  auto get64 = [&](int off) { uint64_t v; std::memcpy(&v, h + off, 8); return v; };
+  uint16_t ver;
+  std::memcpy(&ver, h + 4, 2);
+  if (get32(0) != HL_MAGIC || ver != HL_VERSION || h[7] != 0) return false;
+  o->cb.lmax = h[6];
+  o->rows = get64(8);
+  o->cols = get64(16);
+  o->seg_len = get32(24);
+  if (get32(28) != HL_GROUP_ROWS) return false;
+  o->n_seg = get64(32);
+  o->n_grp = get64(40);
+  o->off_seg_bits = get64(48);
+  o->off_grp_off = get64(56);
+  o->off_stream = get64(64);
+  o->off_raw = get64(72);
+  o->total_bytes = get64(80);
+  o->max_grp_units = get32(88);
+  o->cb.eh.nsym = h[92];
+  o->cb.el.nsym = h[93];
+  o->cb.eh.single = h[94];
+  o->cb.el.single = h[95];
+  std::memcpy(o->cb.eh.len, h + 96, 16);
+  std::memcpy(o->cb.el.len, h + 112, 16);
+  return true;
+}
+
+// Consistency of a parsed header with the layout rules (no data access).
+bool header_consistent(const Header& H, uint64_t blob_bytes) {
+  if (H.cb.lmax < 4 || H.cb.lmax > 15) return false;
+  if (!shape_ok(H.rows, H.cols, H.seg_len)) return false;
+  Layout L = make_layout(H.rows, H.cols, H.seg_len);
+  if (H.n_seg != L.n_seg || H.n_grp != L.n_grp || H.off_seg_bits != L.off_seg_bits ||
+      H.off_grp_off != L.off_grp_off || H.off_stream != L.off_stream)
+    return false;
+  if (H.off_raw < L.off_stream || H.off_raw % 64 || H.total_bytes != H.off_raw + L.n) return false;
+  if (H.total_bytes > blob_bytes) return false;
+  // a group holds at most 64 * S * 2 * lmax bits
+  uint64_t max_units = (64ull * H.seg_len * 2 * H.cb.lmax + 127) / 128;
+  if (H.max_grp_units > max_units) return false;
+  if (!field_code_valid(H.cb.eh, H.cb.lmax) || !field_code_valid(H.cb.el, H.cb.lmax)) return false;
+  return true;
+}
+
+uint32_t default_seg_len(uint64_t cols) {
+  uint32_t best = 0;
+  double bd = 1e30;
+  for (uint32_t S = 8; S <= 512; S += 8) {
+    if (cols % S) continue;
+    double d = S > 128 ? (double)S / 128.0 : 128.0 / (double)S;
+    if (d <= bd + 1e-12) { bd = d; best = S; }
+  }
+  return best;
+}
+
+GroupGeom group_geom(uint64_t rows, uint64_t L, uint64_t g) {
+  GroupGeom q;
+  uint64_t rb = g / L;
+  q.cs = g % L;
+  q.r0 = rb * HL_GROUP_ROWS;
+  q.G = (uint32_t)std::min<uint64_t>(HL_GROUP_ROWS, rows - q.r0);
+  q.first = q.r0 * L + q.cs * q.G;
+  return q;
+}
+
+}  // namespace hl
+
+using namespace hl;
+
+// ---------------------------------------------------------------- C ABI
+
+extern "C" const char* hl_status_str(hl_status s) {
+  switch (s) {
+    case HL_OK: return "ok";
+    case HL_EINVAL: return "invalid argument";
+    case HL_ENOMEM: return "buffer too small or out of host memory";
+    case HL_ECORRUPT: return "corrupt container";
+    case HL_EUNSUPPORTED: return "unsupported";
+    case HL_EHIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+extern "C" uint32_t hl_default_seg_len(uint64_t cols) { return default_seg_len(cols); }
+
+static unsigned pick_threads(uint32_t nthreads) {
+  unsigned t = nthreads ? nthreads : std::thread::hardware_concurrency();
+  return std::max(1u, std::min(t, 64u));
+}
+
+template <class F>
+static void parallel_for(uint64_t n, unsigned nt, F f) {
+  if (nt <= 1 || n < 2) { f(0, n); return; }
+  std::vector<std::thread> th;
+  uint64_t per = (n + nt - 1) / nt;
+  for (unsigned t = 0; t < nt; ++t) {
+    uint64_t a = t * per, b = std::min(n, a + per);
+    if (a >= b) break;
+    th.emplace_back([=] { f(a, b); });
+  }
+  for (auto& x : th) x.join();
+}
+
+extern "C" hl_status hl_build_codebook(const uint16_t* w, size_t n, uint32_t lmax, hl_codebook* out) {
+  if (!w || !out || n == 0 || lmax < 4 || lmax > 15) return HL_EINVAL;
+  unsigned nt = pick_threads(0);
+  if (n < (1u << 20)) nt = 1;
+  std::vector<std::array<uint64_t, 32>> part(nt);
+  parallel_for(n, nt, [&](uint64_t a, uint64_t b) {
+    std::array<uint64_t, 32> h{};
+    for (uint64_t i = a; i < b; ++i) {
+      uint32_t v = w[i];
+      h[(v >> 11) & 15]++;
+      h[16 + ((v >> 7) & 15)]++;
+    }
+    part[a / ((n + nt - 1) / nt)] = h;
+  });
+  uint64_t feh[16] = {0}, fel[16] = {0};
+  for (auto& h : part)
+    for (int s = 0; s < 16; ++s) { feh[s] += h[s]; fel[s] += h[16 + s]; }
+  out->lmax = lmax;
+  field_code_from_counts(feh, (int)lmax, &out->eh);
+  field_code_from_counts(fel, (int)lmax, &out->el);
+  return HL_OK;
+}
+
+extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook* cb,
+                               uint32_t seg_len, uint32_t nthreads, void* out, size_t* out_bytes) {
+  if (!w || !cb || !out_bytes) return HL_EINVAL;
+  uint32_t S = seg_len ? seg_len : default_seg_len(cols);
+  if (!shape_ok(rows, cols, S)) return HL_EINVAL;
+  if (cb->lmax < 4 || cb->lmax > 15 || !field_code_valid(cb->eh, cb->lmax) ||
+      !field_code_valid(cb->el, cb->lmax))
+    return HL_EINVAL;
+  // Pair table: reversed codes of (eh, el), eh first; length 0 for one-symbol fields.
+  uint32_t ceh[16], cel[16];
+  canonical_codes(cb->eh.len, ceh);
+  canonical_codes(cb->el.len, cel);
+  uint8_t leh[16], lel[16];
+  bool veh[16], vel[16];
+  for (int s = 0; s < 16; ++s) {
+    leh[s] = cb->eh.nsym == 1 ? 0 : cb->eh.len[s];
+    lel[s] = cb->el.nsym == 1 ? 0 : cb->el.len[s];
+    veh[s] = cb->eh.nsym == 1 ? (s == cb->eh.single) : cb->eh.len[s] != 0;
+    vel[s] = cb->el.nsym == 1 ? (s == cb->el.single) : cb->el.len[s] != 0;
+  }
+  std::array<uint32_t, 256> pcode;
+  std::array<uint8_t, 256> plen;
+  std::array<bool, 256> pvalid;
+  for (int e = 0; e < 256; ++e) {
+    int a = e >> 4, b = e & 15;
+    pcode[e] = bit_reverse(ceh[a], leh[a]) | (bit_reverse(cel[b], lel[b]) << leh[a]);
+    plen[e] = (uint8_t)(leh[a] + lel[b]);
+    pvalid[e] = veh[a] && vel[b];
+  }
+  Layout L = make_layout(rows, cols, S);
+  const unsigned nt = pick_threads(nthreads);
+  // Pass 1: segment bit counts, in group order.
+  std::vector<uint16_t> seg_bits(L.n_seg);
+  std::vector<uint8_t> bad(nt, 0);
+  const uint64_t per1 = (L.n_grp + nt - 1) / nt;
+  parallel_for(L.n_grp, nt, [&](uint64_t a, uint64_t b) {
+    bool anybad = false;
+    for (uint64_t g = a; g < b; ++g) {
+      GroupGeom q = group_geom(rows, L.L, g);
+      for (uint32_t lam = 0; lam < q.G; ++lam) {
+        const uint16_t* p = w + (q.r0 + lam) * cols + q.cs * S;
+        uint32_t bits = 0;
+        for (uint32_t t = 0; t < S; ++t) {
+          uint32_t e = (p[t] >> 7) & 0xFF;
+          anybad |= !pvalid[e];
+          bits += plen[e];
+        }
+        seg_bits[q.first + lam] = (uint16_t)bits;
+      }
+    }
+    if (anybad) bad[a / per1] = 1;
+  });
+  for (auto b : bad)
+    if (b) return HL_EINVAL;
+  // Group stream sizes (16-byte units) and offsets.
+  std::vector<uint32_t> grp_off(L.n_grp + 1);
+  uint64_t units = 0;
+  uint32_t max_units = 0;
+  for (uint64_t g = 0; g < L.n_grp; ++g) {
+    GroupGeom q = group_geom(rows, L.L, g);
+    uint64_t bits = 0;
+    for (uint32_t lam = 0; lam < q.G; ++lam) bits += seg_bits[q.first + lam];
+    uint64_t u = (bits + 127) / 128;
+    grp_off[g] = (uint32_t)units;
+    units += u;
+    max_units = std::max<uint32_t>(max_units, (uint32_t)u);
+    if (units > 0xFFFFFFFFull) return HL_EUNSUPPORTED;
+  }
+  grp_off[L.n_grp] = (uint32_t)units;
+  const uint64_t off_raw = align64(L.off_stream + units * 16);
+  const uint64_t total = off_raw + L.n;
+  if (!out) { *out_bytes = total; return HL_OK; }
+  if (*out_bytes < total) { *out_bytes = total; return HL_ENOMEM; }
+  uint8_t* o = (uint8_t*)out;
+  std::memset(o, 0, L.off_stream);  // header, padding, metadata
+  pack_header(o, rows, cols, S, *cb, L, off_raw, total, max_units);
+  std::memcpy(o + L.off_seg_bits, seg_bits.data(), 2 * L.n_seg);
+  std::memcpy(o + L.off_grp_off, grp_off.data(), 4 * (L.n_grp + 1));
+  std::memset(o + L.off_stream + units * 16, 0, off_raw - (L.off_stream + units * 16));
+  // Pass 2: group streams and raw plane, independent per group.
+  parallel_for(L.n_grp, nt, [&](uint64_t ga, uint64_t gb) {
+    for (uint64_t g = ga; g < gb; ++g) {
+      GroupGeom q = group_geom(rows, L.L, g);
+      uint32_t* dst = (uint32_t*)(o + L.off_stream + (uint64_t)grp_off[g] * 16);
+      const uint64_t nwords = (uint64_t)(grp_off[g + 1] - grp_off[g]) * 4;
+      uint64_t acc = 0;
+      int nb = 0;
+      uint64_t wi = 0;
+      uint8_t* rdst = o + off_raw + q.first * S;
+      for (uint32_t lam = 0; lam < q.G; ++lam) {
+        const uint16_t* p = w + (q.r0 + lam) * cols + q.cs * S;
+        for (uint32_t t = 0; t < S; ++t) {
+          uint32_t v = p[t];
+          uint32_t e = (v >> 7) & 0xFF;
+          acc |= (uint64_t)pcode[e] << nb;
+          nb += plen[e];
+          if (nb >= 32) {
+            dst[wi++] = (uint32_t)acc;
+            acc >>= 32;
+            nb -= 32;
+          }
+          // raw plane: ((t/8)*G + lam)*8 + t%8 within the group
+          rdst[((t >> 3) * q.G + lam) * 8 + (t & 7)] = (uint8_t)(((v >> 8) & 0x80) | (v & 0x7F));
+        }
+      }
+      while (wi < nwords) {  // tail bits, then zero padding to 128 bits
+        dst[wi++] = (uint32_t)acc;
+        acc >>= 32;
+      }
+    }
+  });
+  *out_bytes = total;
+  return HL_OK;
+}
+
+extern "C" hl_status hl_validate(const void* blob, size_t bytes) {
+  if (!blob || bytes < HL_HEADER_BYTES) return HL_ECORRUPT;
+  Header H;
+  const uint8_t* b = (const uint8_t*)blob;
+  if (!parse_header(b, &H) || !header_consistent(H, bytes)) return HL_ECORRUPT;
+  const uint16_t* sb = (const uint16_t*)(b + H.off_seg_bits);
+  const uint32_t* go = (const uint32_t*)(b + H.off_grp_off);
+  if (go[0] != 0) return HL_ECORRUPT;
+  uint32_t mx = 0;
+  const uint64_t max_seg = (uint64_t)H.seg_len * 2 * H.cb.lmax;
+  const uint64_t L = H.cols / H.seg_len;
+  for (uint64_t g = 0; g < H.n_grp; ++g) {
+    GroupGeom q = group_geom(H.rows, L, g);
+    uint64_t bits = 0;
+    for (uint32_t lam = 0; lam < q.G; ++lam) {
+      if (sb[q.first + lam] > max_seg) return HL_ECORRUPT;
+      bits += sb[q.first + lam];
+    }
+    if (go[g + 1] < go[g] || go[g + 1] - go[g] != (bits + 127) / 128) return HL_ECORRUPT;
+    mx = std::max(mx, go[g + 1] - go[g]);
+  }
+  if (mx != H.max_grp_units) return HL_ECORRUPT;
+  if (H.off_raw != align64(H.off_stream + (uint64_t)go[H.n_grp] * 16)) return HL_ECORRUPT;
+  return HL_OK;
+}

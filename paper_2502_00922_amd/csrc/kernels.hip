@@ -1,0 +1,595 @@
+// gfx950 kernels of the Huff-LLM bf16 codec: decode-table build, decode to
+// bf16, fused decode-GEMV, the uncompressed bf16 GEMV comparator, and their
+// C-ABI launchers.
+//
+// Decoding follows the decoder of Huff-LLM Sec. 3.2: a window of bits at the
+// start pointer is matched against the codebook, the symbol is emitted and the
+// pointer advances by the code length; the raw sign is passed through and the
+// fields are concatenated back into the 16-bit weight. Here the "CAM" is a
+// 4096-entry table in LDS indexed by a 12-bit window that yields both codes of
+// a weight (exponent high and low nibble) at once; pairs longer than 12 bits
+// fall back to a bit-serial canonical decode. Weights are decoded only where
+// they are multiplied (Sec. 1, Sec. 3.2): the fused kernel never writes them.
+//
+// Work mapping (container tiling in include/hufflm.h): one wavefront decodes
+// one group = 64 rows x one S-column segment, lane lam owning row 64rb+lam.
+// All lanes of a wave therefore read the same activations, which are loaded
+// once into scalar registers.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+
+#include "hl_internal.h"
+#include "hufflm.h"
+
+namespace hl {
+
+constexpr int kLutBits = 12;
+constexpr int kLutN = 1 << kLutBits;   // joint window table entries
+constexpr int kAuxWords = 64;          // canonical tables for the long-code path
+constexpr int kAuxField = 24;          // words per field in the aux table
+constexpr uint32_t kEsc = 0x80000000u;  // entry flag: pair longer than the window
+constexpr int kPadWords = 4;           // zero words before a staged group stream
+constexpr int kMaxWaves = 4;
+
+static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
+
+// Joint table entry: bits 0..4 = code bits of the (eh, el) pair, bits 23..30 =
+// the exponent byte eh<<4|el (its place in a float32), bit 31 = kEsc.
+// Aux table, per field f at word f*24: [0] = nsym | single<<8 | maxlen<<16;
+// [l], l = 1..15: first_code<<16 | count<<8 | offset; [16..19]: symbols sorted
+// by (length, symbol), one byte each.
+struct Aux {
+  uint32_t w[kAuxWords];
+};
+
+static Aux make_aux(const hl_codebook& cb) {
+  Aux a;
+  std::memset(&a, 0, sizeof(a));
+  const hl_field_code* fs[2] = {&cb.eh, &cb.el};
+  for (int f = 0; f < 2; ++f) {
+    const hl_field_code& fc = *fs[f];
+    uint32_t* w = a.w + f * kAuxField;
+    uint32_t code[16];
+    canonical_codes(fc.len, code);
+    int maxl = 0;
+    for (int s = 0; s < 16; ++s) maxl = std::max(maxl, (int)fc.len[s]);
+    if (fc.nsym == 1) maxl = 0;
+    w[0] = (uint32_t)fc.nsym | ((uint32_t)fc.single << 8) | ((uint32_t)maxl << 16);
+    int k = 0;
+    uint8_t sorted[16] = {0};
+    for (int l = 1; l <= 15; ++l) {
+      int first = -1, cnt = 0, off = k;
+      for (int s = 0; s < 16; ++s) {
+        if (fc.nsym > 1 && fc.len[s] == l) {
+          if (first < 0) first = (int)code[s];
+          sorted[k++] = (uint8_t)s;
+          ++cnt;
+        }
+      }
+      w[l] = ((uint32_t)(first < 0 ? 0 : first) << 16) | ((uint32_t)cnt << 8) | (uint32_t)off;
+    }
+    for (int i = 0; i < 16; ++i) w[16 + i / 4] |= (uint32_t)sorted[i] << (8 * (i % 4));
+  }
+  return a;
+}
+
+// ------------------------------------------------------------------ device
+
+// One field, bit-serial canonical decode from `bits` (LSB = next bit), using
+// at most `avail` bits. Returns the symbol or -1 if no code of <= avail bits
+// matches.
+__device__ inline int field_from_bits(const uint32_t* aux, uint32_t bits, uint32_t avail,
+                                      uint32_t* used) {
+  const uint32_t meta = aux[0];
+  if ((meta & 0xFF) == 1) { *used = 0; return (int)((meta >> 8) & 0xFF); }
+  const uint32_t maxl = (meta >> 16) & 0xFF;
+  uint32_t code = 0;
+  for (uint32_t l = 1; l <= maxl && l <= avail; ++l) {
+    code = (code << 1) | ((bits >> (l - 1)) & 1u);
+    const uint32_t w = aux[l];
+    const uint32_t d = code - (w >> 16);
+    if (d < ((w >> 8) & 0xFF)) {
+      const uint32_t k = (w & 0xFF) + d;
+      *used = l;
+      return (int)((aux[16 + (k >> 2)] >> (8 * (k & 3))) & 0xFF);
+    }
+  }
+  return -1;
+}
+
+// Builds the joint table: entry v decodes the 12-bit window v (bit 0 first).
+__global__ void __launch_bounds__(256) lut_kernel(uint32_t* lut, Aux aux) {
+  for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
+    uint32_t ua = 0, ub = 0;
+    int a = field_from_bits(aux.w, (uint32_t)v, kLutBits, &ua);
+    int b = a < 0 ? -1 : field_from_bits(aux.w + kAuxField, (uint32_t)v >> ua, kLutBits - ua, &ub);
+    lut[v] = (a < 0 || b < 0) ? kEsc : ((ua + ub) | ((uint32_t)((a << 4) | b) << 23));
+  }
+  for (int i = threadIdx.x; i < kAuxWords; i += blockDim.x) lut[kLutN + i] = aux.w[i];
+}
+
+// Bit-serial decode of one field from the staged stream at bit p (advanced).
+__device__ inline uint32_t slow_field(const uint32_t* st, const uint32_t* aux, uint32_t& p) {
+  const uint32_t meta = aux[0];
+  if ((meta & 0xFF) == 1) return (meta >> 8) & 0xFF;
+  const uint32_t maxl = (meta >> 16) & 0xFF;
+  uint32_t code = 0;
+  for (uint32_t l = 1; l <= maxl; ++l) {
+    code = (code << 1) | ((st[p >> 5] >> (p & 31)) & 1u);
+    ++p;
+    const uint32_t w = aux[l];
+    const uint32_t d = code - (w >> 16);
+    if (d < ((w >> 8) & 0xFF)) {
+      const uint32_t k = (w & 0xFF) + d;
+      return (aux[16 + (k >> 2)] >> (8 * (k & 3))) & 0xFF;
+    }
+  }
+  return 0;  // no code matched: damaged stream, decode continues safely
+}
+
+// Long pair at window position q2 (= bit position - 2): entry in table format.
+__device__ __noinline__ uint32_t slow_pair(const uint32_t* st, const uint32_t* aux, uint32_t q2) {
+  uint32_t p = q2 + 2;
+  const uint32_t a = slow_field(st, aux, p);
+  const uint32_t b = slow_field(st, aux + kAuxField, p);
+  return (p - q2 - 2) | (((a << 4) | b) << 23);
+}
+
+struct GroupArgs {
+  const uint16_t* seg_bits;
+  const uint32_t* grp_off;
+  const uint4* stream;
+  const uint8_t* raw;
+  const uint32_t* lut;   // global copy: kLutN entries + aux
+  uint32_t rows, cols, S, L, RB, stream_units, wave_words, max_units;
+};
+
+// Stage group g's stream into this wave's LDS region and compute the lane's
+// start position; returns q2 (bit position within the region, minus 2).
+__device__ inline uint32_t stage_group(const GroupArgs& a, uint32_t* st, uint32_t g, uint32_t lane,
+                                       uint32_t G, uint64_t first) {
+  uint32_t u0 = a.grp_off[g], u1 = a.grp_off[g + 1];
+  u0 = min(u0, a.stream_units);
+  u1 = min(max(u1, u0), a.stream_units);
+  const uint32_t units = min(u1 - u0, a.max_units);
+  uint4* dst = reinterpret_cast<uint4*>(st + kPadWords);
+  for (uint32_t k = lane; k < units; k += 64) dst[k] = a.stream[(uint64_t)u0 + k];
+  if (lane == 0) *reinterpret_cast<uint4*>(st) = make_uint4(0, 0, 0, 0);
+  uint32_t nb = lane < G ? (uint32_t)a.seg_bits[first + lane] : 0u;
+  uint32_t incl = nb;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    uint32_t t = __shfl_up(incl, d, 64);
+    if ((int)lane >= d) incl += t;
+  }
+  const uint32_t start = min(incl - nb, units * 128u);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  return kPadWords * 32u + start - 2u;
+}
+
+// Decodes 8 consecutive weights of the lane's segment: entries e[8] (table
+// format) and advances q2.
+__device__ inline void decode8(const uint32_t* lut, const uint32_t* aux, const uint32_t* st,
+                               uint32_t& q2, uint32_t e[8]) {
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t wi = q2 >> 5;
+    const uint32_t lo = st[wi], hi = st[wi + 1];
+    const uint32_t win = __builtin_amdgcn_alignbit(hi, lo, q2) & ((kLutN - 1) << 2);
+    uint32_t ent = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(lut) + win);
+    if (ent & kEsc) ent = slow_pair(st, aux, q2);
+    q2 += ent & 0xFF;
+    e[k] = ent;
+  }
+}
+
+// Packed bf16 pair (weights k, k+1 of a raw dword) from two table entries.
+__device__ inline uint32_t pack_pair(uint32_t rawdw, int k, uint32_t e0, uint32_t e1) {
+  const uint32_t b0 = (uint32_t)(k & 3), b1 = (uint32_t)((k + 1) & 3);
+  const uint32_t P = __builtin_amdgcn_perm(rawdw, rawdw, b0 | (b0 << 8) | (b1 << 16) | (b1 << 24));
+  const uint32_t E = __builtin_amdgcn_perm(e1, e0, 0x07060302u);
+  return (P & 0x807F807Fu) | (E & 0x7F807F80u);
+}
+
+// float32 weight k of a raw dword from its table entry.
+__device__ inline float weight_f32(uint32_t rawdw, int k, uint32_t e) {
+  const uint32_t b = (uint32_t)(k & 3);
+  const uint32_t M = __builtin_amdgcn_perm(rawdw, rawdw, 0x00000C0Cu | (b << 16) | (b << 24));
+  return __uint_as_float((M & 0x807FFFFFu) | (e & 0x7F800000u));
+}
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ inline float dot2(uint32_t w, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w),
+                                         __builtin_bit_cast(bf16x2_t, x), acc, false);
+}
+
+// ------------------------------------------------------------------ decode
+
+__global__ void __launch_bounds__(256) decode_kernel(GroupArgs a, uint16_t* out) {
+  extern __shared__ uint32_t smem[];
+  uint32_t* lut = smem;
+  uint32_t* aux = smem + kLutN;
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t* st = smem + kLutN + kAuxWords + wave * a.wave_words;
+  for (uint32_t i = threadIdx.x; i < kLutN + kAuxWords; i += blockDim.x) smem[i] = a.lut[i];
+  __syncthreads();
+  const uint32_t n_grp = a.RB * a.L;
+  const uint32_t waves = blockDim.x >> 6;
+  for (uint32_t g = blockIdx.x * waves + wave; g < n_grp; g += gridDim.x * waves) {
+    const uint32_t rb = g / a.L, cs = g % a.L;
+    const uint32_t r0 = rb * 64;
+    const uint32_t G = min(64u, a.rows - r0);
+    const uint64_t first = (uint64_t)r0 * a.L + (uint64_t)cs * G;
+    uint32_t q2 = stage_group(a, st, g, lane, G, first);
+    if (lane < G) {
+      const uint8_t* raw = a.raw + first * a.S + lane * 8;
+      uint16_t* o = out + (uint64_t)(r0 + lane) * a.cols + (uint64_t)cs * a.S;
+      for (uint32_t t = 0; t < a.S; t += 8) {
+        const uint2 rw = *reinterpret_cast<const uint2*>(raw + (uint64_t)(t >> 3) * G * 8);
+        uint32_t e[8];
+        decode8(lut, aux, st, q2, e);
+        uint4 v;
+        v.x = pack_pair(rw.x, 0, e[0], e[1]);
+        v.y = pack_pair(rw.x, 2, e[2], e[3]);
+        v.z = pack_pair(rw.y, 0, e[4], e[5]);
+        v.w = pack_pair(rw.y, 2, e[6], e[7]);
+        *reinterpret_cast<uint4*>(o + t) = v;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ fused GEMV
+
+struct GemvArgs {
+  GroupArgs g;
+  const void* x;
+  float* y;
+  uint32_t C;       // column segments per block
+  uint32_t KS;      // blocks per row block
+  uint32_t atomic;  // 1: blocks add into y (zeroed beforehand); 0: store
+};
+
+template <int B, bool XBF16>
+__global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p) {
+  extern __shared__ uint32_t smem[];
+  const GroupArgs& a = p.g;
+  uint32_t* lut = smem;
+  uint32_t* aux = smem + kLutN;
+  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t waves = blockDim.x >> 6;
+  uint32_t* st = smem + kLutN + kAuxWords + wave * a.wave_words;
+  float* red = reinterpret_cast<float*>(smem + kLutN + kAuxWords + waves * a.wave_words);
+  for (uint32_t i = threadIdx.x; i < kLutN + kAuxWords; i += blockDim.x) smem[i] = a.lut[i];
+  __syncthreads();
+
+  const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
+  const uint32_t r0 = rb * 64;
+  const uint32_t G = min(64u, a.rows - r0);
+  const uint32_t cs_end = min(a.L, (kp + 1) * p.C);
+  float acc[B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) acc[b] = 0.f;
+
+  for (uint32_t cs = kp * p.C + wave; cs < cs_end; cs += waves) {
+    const uint32_t g = rb * a.L + cs;
+    const uint64_t first = (uint64_t)r0 * a.L + (uint64_t)cs * G;
+    uint32_t q2 = stage_group(a, st, g, lane, G, first);
+    const uint32_t c0 = cs * a.S;
+    if (lane < G) {
+      const uint8_t* raw = a.raw + first * a.S + lane * 8;
+      for (uint32_t t = 0; t < a.S; t += 8) {
+        const uint2 rw = *reinterpret_cast<const uint2*>(raw + (uint64_t)(t >> 3) * G * 8);
+        uint32_t e[8];
+        decode8(lut, aux, st, q2, e);
+        const uint32_t col = __builtin_amdgcn_readfirstlane(c0 + t);
+        if constexpr (XBF16) {
+          const uint32_t w0 = pack_pair(rw.x, 0, e[0], e[1]);
+          const uint32_t w1 = pack_pair(rw.x, 2, e[2], e[3]);
+          const uint32_t w2 = pack_pair(rw.y, 0, e[4], e[5]);
+          const uint32_t w3 = pack_pair(rw.y, 2, e[6], e[7]);
+          const uint16_t* xb = reinterpret_cast<const uint16_t*>(p.x);
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+            const uint4 xv = *reinterpret_cast<const uint4*>(xb + (uint64_t)b * a.cols + col);
+            float s = acc[b];
+            s = dot2(w0, xv.x, s);
+            s = dot2(w1, xv.y, s);
+            s = dot2(w2, xv.z, s);
+            s = dot2(w3, xv.w, s);
+            acc[b] = s;
+          }
+        } else {
+          float wf[8];
+#pragma unroll
+          for (int k = 0; k < 8; ++k) wf[k] = weight_f32(k < 4 ? rw.x : rw.y, k, e[k]);
+          const float* xf = reinterpret_cast<const float*>(p.x);
+#pragma unroll
+          for (int b = 0; b < B; ++b) {
+            const float4 x0 = *reinterpret_cast<const float4*>(xf + (uint64_t)b * a.cols + col);
+            const float4 x1 = *reinterpret_cast<const float4*>(xf + (uint64_t)b * a.cols + col + 4);
+            float s = acc[b];
+            s = fmaf(wf[0], x0.x, s);
+            s = fmaf(wf[1], x0.y, s);
+            s = fmaf(wf[2], x0.z, s);
+            s = fmaf(wf[3], x0.w, s);
+            s = fmaf(wf[4], x1.x, s);
+            s = fmaf(wf[5], x1.y, s);
+            s = fmaf(wf[6], x1.z, s);
+            s = fmaf(wf[7], x1.w, s);
+            acc[b] = s;
+          }
+        }
+      }
+    }
+  }
+  // Cross-wave reduction in a fixed order, then one store (or add) per row.
+#pragma unroll
+  for (int b = 0; b < B; ++b) red[(wave * B + b) * 64 + lane] = acc[b];
+  __syncthreads();
+  if (wave == 0 && lane < G) {
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float s = red[b * 64 + lane];
+      for (uint32_t w = 1; w < waves; ++w) s += red[(w * B + b) * 64 + lane];
+      float* dst = p.y + (uint64_t)b * a.rows + r0 + lane;
+      if (p.atomic) unsafeAtomicAdd(dst, s);
+      else *dst = s;
+    }
+  }
+}
+
+__global__ void zero_kernel(float* y, uint64_t n) {
+  for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
+       i += (uint64_t)gridDim.x * blockDim.x)
+    y[i] = 0.f;
+}
+
+// ------------------------------------------------------------------ bf16 GEMV
+
+// One wave per row; lanes stride the row in 8-weight chunks; dot2 on pairs.
+template <int B, bool XBF16>
+__global__ void __launch_bounds__(256) gemv_bf16_kernel(const uint16_t* w, const void* x, float* y,
+                                                        uint32_t rows, uint32_t cols) {
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t waves = blockDim.x >> 6;
+  for (uint32_t r = blockIdx.x * waves + (threadIdx.x >> 6); r < rows; r += gridDim.x * waves) {
+    float acc[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) acc[b] = 0.f;
+    const uint16_t* wr = w + (uint64_t)r * cols;
+    for (uint32_t c = lane * 8; c < cols; c += 512) {
+      const uint4 wv = *reinterpret_cast<const uint4*>(wr + c);
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        if constexpr (XBF16) {
+          const uint4 xv = *reinterpret_cast<const uint4*>(
+              reinterpret_cast<const uint16_t*>(x) + (uint64_t)b * cols + c);
+          float s = acc[b];
+          s = dot2(wv.x, xv.x, s);
+          s = dot2(wv.y, xv.y, s);
+          s = dot2(wv.z, xv.z, s);
+          s = dot2(wv.w, xv.w, s);
+          acc[b] = s;
+        } else {
+          const float* xf = reinterpret_cast<const float*>(x) + (uint64_t)b * cols + c;
+          const float4 x0 = *reinterpret_cast<const float4*>(xf);
+          const float4 x1 = *reinterpret_cast<const float4*>(xf + 4);
+          const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+          const float xs[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+          float s = acc[b];
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            s = fmaf(__uint_as_float(ww[k] << 16), xs[2 * k], s);
+            s = fmaf(__uint_as_float(ww[k] & 0xFFFF0000u), xs[2 * k + 1], s);
+          }
+          acc[b] = s;
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float s = acc[b];
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+      if (lane == 0) y[(uint64_t)b * rows + r] = s;
+    }
+  }
+}
+
+// ------------------------------------------------------------------ launch helpers
+
+static int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+constexpr uint32_t kMaxLds = 160 * 1024;
+
+struct Plan {
+  GroupArgs ga;
+  uint32_t waves;
+  size_t lds;
+};
+
+static hl_status make_plan(const hl_tensor* t, uint32_t red_words_per_wave, Plan* pl) {
+  if (!t || !t->blob_dev || !t->lut_dev) return HL_EINVAL;
+  if (t->rows >= (1ull << 31) || t->cols >= (1ull << 31) || t->n_grp >= (1ull << 31))
+    return HL_EUNSUPPORTED;
+  GroupArgs& a = pl->ga;
+  const uint8_t* b = t->blob_dev;
+  a.seg_bits = reinterpret_cast<const uint16_t*>(b + t->off_seg_bits);
+  a.grp_off = reinterpret_cast<const uint32_t*>(b + t->off_grp_off);
+  a.stream = reinterpret_cast<const uint4*>(b + t->off_stream);
+  a.raw = b + t->off_raw;
+  a.lut = t->lut_dev;
+  a.rows = (uint32_t)t->rows;
+  a.cols = (uint32_t)t->cols;
+  a.S = t->seg_len;
+  a.L = (uint32_t)(t->cols / t->seg_len);
+  a.RB = (uint32_t)((t->rows + 63) / 64);
+  a.stream_units = (uint32_t)std::min<uint64_t>((t->off_raw - t->off_stream) / 16, 0xFFFFFFFFu);
+  a.max_units = t->max_grp_units;
+  // pad words + stream + guard for reads past a damaged segment (<= 2*lmax bits per weight)
+  const uint32_t guard = (t->seg_len * 2 * 15 + 64) / 32 + 4;
+  uint32_t ww = kPadWords + t->max_grp_units * 4 + guard;
+  ww = (ww + 3) & ~3u;
+  a.wave_words = ww;
+  uint32_t waves = kMaxWaves;
+  while (waves > 1 && (size_t)(kLutN + kAuxWords + waves * (ww + red_words_per_wave)) * 4 > kMaxLds)
+    --waves;
+  size_t lds = (size_t)(kLutN + kAuxWords + waves * (ww + red_words_per_wave)) * 4;
+  if (lds > kMaxLds) return HL_EUNSUPPORTED;
+  pl->waves = waves;
+  pl->lds = lds;
+  return HL_OK;
+}
+
+template <class K, class... A>
+static hl_status launch(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, A... args) {
+  if (lds > 64 * 1024) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+      return HL_EHIP;
+  }
+  hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+  return hipGetLastError() == hipSuccess ? HL_OK : HL_EHIP;
+}
+
+template <int B>
+static hl_status launch_gemv_b(bool xbf16, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               const GemvArgs& p) {
+  return xbf16 ? launch(gemv_kernel<B, true>, grid, block, lds, s, p)
+               : launch(gemv_kernel<B, false>, grid, block, lds, s, p);
+}
+
+template <int B>
+static hl_status launch_bf16_b(bool xbf16, dim3 grid, dim3 block, hipStream_t s, const uint16_t* w,
+                               const void* x, float* y, uint32_t rows, uint32_t cols) {
+  return xbf16 ? launch(gemv_bf16_kernel<B, true>, grid, block, 0, s, w, x, y, rows, cols)
+               : launch(gemv_bf16_kernel<B, false>, grid, block, 0, s, w, x, y, rows, cols);
+}
+
+#define HL_BATCH_SWITCH(fn, batch, ...)                   \
+  switch (batch) {                                        \
+    case 1: return fn<1>(__VA_ARGS__);                    \
+    case 2: return fn<2>(__VA_ARGS__);                    \
+    case 3: return fn<3>(__VA_ARGS__);                    \
+    case 4: return fn<4>(__VA_ARGS__);                    \
+    case 5: return fn<5>(__VA_ARGS__);                    \
+    case 6: return fn<6>(__VA_ARGS__);                    \
+    case 7: return fn<7>(__VA_ARGS__);                    \
+    case 8: return fn<8>(__VA_ARGS__);                    \
+    case 9: return fn<9>(__VA_ARGS__);                    \
+    case 10: return fn<10>(__VA_ARGS__);                  \
+    case 11: return fn<11>(__VA_ARGS__);                  \
+    case 12: return fn<12>(__VA_ARGS__);                  \
+    case 13: return fn<13>(__VA_ARGS__);                  \
+    case 14: return fn<14>(__VA_ARGS__);                  \
+    case 15: return fn<15>(__VA_ARGS__);                  \
+    case 16: return fn<16>(__VA_ARGS__);                  \
+    default: return HL_EINVAL;                            \
+  }
+
+}  // namespace hl
+
+using namespace hl;
+
+extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* header_host, size_t blob_bytes,
+                                    uint32_t* lut_dev, hl_tensor* out) {
+  if (!blob_dev || !header_host || !lut_dev || !out || blob_bytes < HL_HEADER_BYTES) return HL_EINVAL;
+  Header H;
+  if (!parse_header(reinterpret_cast<const uint8_t*>(header_host), &H) || !header_consistent(H, blob_bytes))
+    return HL_ECORRUPT;
+  hl_tensor t;
+  std::memset(&t, 0, sizeof(t));
+  t.blob_dev = reinterpret_cast<const uint8_t*>(blob_dev);
+  t.lut_dev = lut_dev;
+  t.rows = H.rows;
+  t.cols = H.cols;
+  t.n_seg = H.n_seg;
+  t.n_grp = H.n_grp;
+  t.total_bytes = H.total_bytes;
+  t.off_seg_bits = H.off_seg_bits;
+  t.off_grp_off = H.off_grp_off;
+  t.off_stream = H.off_stream;
+  t.off_raw = H.off_raw;
+  t.seg_len = H.seg_len;
+  t.lmax = H.cb.lmax;
+  t.max_grp_units = H.max_grp_units;
+  t.cb = H.cb;
+  *out = t;
+  return HL_OK;
+}
+
+extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
+  if (!t || !t->lut_dev) return HL_EINVAL;
+  if (!field_code_valid(t->cb.eh, t->cb.lmax) || !field_code_valid(t->cb.el, t->cb.lmax)) return HL_ECORRUPT;
+  Aux aux = make_aux(t->cb);
+  return launch(lut_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, aux);
+}
+
+extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream) {
+  if (!out_dev) return HL_EINVAL;
+  Plan pl;
+  hl_status st = make_plan(t, 0, &pl);
+  if (st != HL_OK) return st;
+  const uint32_t n_grp = pl.ga.RB * pl.ga.L;
+  const uint32_t per_cu = std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)pl.lds));
+  const uint32_t blocks = std::min<uint32_t>((n_grp + pl.waves - 1) / pl.waves, device_cus() * per_cu);
+  return launch(decode_kernel, dim3(blocks), dim3(pl.waves * 64), pl.lds, (hipStream_t)stream, pl.ga,
+                out_dev);
+}
+
+extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
+                                    float* y_dev, void* stream) {
+  if (!x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || (x_dtype != HL_F32 && x_dtype != HL_BF16))
+    return HL_EINVAL;
+  Plan pl;
+  hl_status st = make_plan(t, batch * 64, &pl);
+  if (st != HL_OK) return st;
+  GemvArgs p;
+  p.g = pl.ga;
+  p.x = x_dev;
+  p.y = y_dev;
+  // Column segments per block: enough blocks to fill the device, each wave
+  // decoding at least one group.
+  const uint32_t L = pl.ga.L, RB = pl.ga.RB;
+  const uint64_t target_waves = (uint64_t)device_cus() * 16;
+  uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * L + target_waves - 1) / target_waves);
+  uint32_t C = std::min<uint32_t>(L, pl.waves * gpw);
+  p.C = C;
+  p.KS = (L + C - 1) / C;
+  p.atomic = p.KS > 1 ? 1u : 0u;
+  hipStream_t s = (hipStream_t)stream;
+  if (p.atomic) {
+    const uint64_t n = (uint64_t)batch * t->rows;
+    hipLaunchKernelGGL(zero_kernel, dim3((uint32_t)std::min<uint64_t>((n + 255) / 256, 4096)), dim3(256), 0, s,
+                       y_dev, n);
+    if (hipGetLastError() != hipSuccess) return HL_EHIP;
+  }
+  const dim3 grid(RB * p.KS), block(pl.waves * 64);
+  const bool xb = x_dtype == HL_BF16;
+  HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, pl.lds, s, p);
+}
+
+extern "C" hl_status hl_gemv_bf16(const uint16_t* w_dev, uint64_t rows, uint64_t cols, const void* x_dev,
+                                  hl_dtype x_dtype, uint32_t batch, float* y_dev, void* stream) {
+  if (!w_dev || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || rows == 0 || cols == 0 ||
+      cols % 8 || (x_dtype != HL_F32 && x_dtype != HL_BF16))
+    return HL_EINVAL;
+  if (rows >= (1ull << 31) || cols >= (1ull << 31)) return HL_EUNSUPPORTED;
+  const uint32_t blocks = (uint32_t)std::min<uint64_t>((rows + 3) / 4, (uint64_t)device_cus() * 8);
+  const bool xb = x_dtype == HL_BF16;
+  HL_BATCH_SWITCH(launch_bf16_b, batch, xb, dim3(blocks), dim3(256), (hipStream_t)stream, w_dev, x_dev, y_dev,
+                  (uint32_t)rows, (uint32_t)cols);
+}

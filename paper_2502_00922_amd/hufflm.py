@@ -1,0 +1,208 @@
+"""ctypes binding of libhufflm.so (argument marshalling only).
+
+Every step of the codec runs in the library: the host encoder in C++, decoding
+and the fused decode-GEMV in gfx950 kernels. PyTorch only provides device
+memory and the current HIP stream. There is no fallback: if the library is
+missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhufflm.so")
+
+HL_OK, HL_EINVAL, HL_ENOMEM, HL_ECORRUPT, HL_EUNSUPPORTED, HL_EHIP = range(6)
+HL_F32, HL_BF16 = 0, 1
+HEADER_BYTES = 128
+LUT_BYTES = 16640
+MAX_BATCH = 16
+
+
+class HLError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} ({status})")
+
+
+class FieldCode(ctypes.Structure):
+    _fields_ = [("nsym", ctypes.c_uint8), ("single", ctypes.c_uint8), ("len", ctypes.c_uint8 * 16)]
+
+    @property
+    def lengths(self):
+        return list(self.len)
+
+
+class Codebook(ctypes.Structure):
+    _fields_ = [("lmax", ctypes.c_uint32), ("eh", FieldCode), ("el", FieldCode)]
+
+
+class TensorView(ctypes.Structure):
+    _fields_ = [("blob_dev", ctypes.c_void_p), ("lut_dev", ctypes.c_void_p),
+                ("rows", ctypes.c_uint64), ("cols", ctypes.c_uint64), ("n_seg", ctypes.c_uint64),
+                ("n_grp", ctypes.c_uint64), ("total_bytes", ctypes.c_uint64),
+                ("off_seg_bits", ctypes.c_uint64), ("off_grp_off", ctypes.c_uint64),
+                ("off_stream", ctypes.c_uint64), ("off_raw", ctypes.c_uint64),
+                ("seg_len", ctypes.c_uint32), ("lmax", ctypes.c_uint32),
+                ("max_grp_units", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("cb", Codebook)]
+
+
+_lib = None
+
+EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_build_codebook", "hl_encode", "hl_validate",
+           "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_decode_gemv", "hl_gemv_bf16"]
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2502_00922_amd/build.py")
+    L = ctypes.CDLL(LIB_PATH)
+    c = ctypes
+    L.hl_status_str.restype = c.c_char_p
+    L.hl_status_str.argtypes = [c.c_int]
+    L.hl_default_seg_len.restype = c.c_uint32
+    L.hl_default_seg_len.argtypes = [c.c_uint64]
+    L.hl_build_codebook.restype = c.c_int
+    L.hl_build_codebook.argtypes = [c.c_void_p, c.c_size_t, c.c_uint32, c.POINTER(Codebook)]
+    L.hl_encode.restype = c.c_int
+    L.hl_encode.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook), c.c_uint32,
+                            c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
+    L.hl_validate.restype = c.c_int
+    L.hl_validate.argtypes = [c.c_void_p, c.c_size_t]
+    L.hl_tensor_view.restype = c.c_int
+    L.hl_tensor_view.argtypes = [c.c_void_p, c.c_void_p, c.c_size_t, c.c_void_p, c.POINTER(TensorView)]
+    L.hl_tensor_prepare.restype = c.c_int
+    L.hl_tensor_prepare.argtypes = [c.POINTER(TensorView), c.c_void_p]
+    L.hl_decode.restype = c.c_int
+    L.hl_decode.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_void_p]
+    L.hl_decode_gemv.restype = c.c_int
+    L.hl_decode_gemv.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
+                                 c.c_void_p]
+    L.hl_gemv_bf16.restype = c.c_int
+    L.hl_gemv_bf16.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.c_void_p, c.c_int, c.c_uint32,
+                               c.c_void_p, c.c_void_p]
+    _lib = L
+    return L
+
+
+def status_str(s: int) -> str:
+    return lib().hl_status_str(s).decode()
+
+
+def _check(s: int, where: str) -> None:
+    if s != HL_OK:
+        raise HLError(s, where)
+
+
+def default_seg_len(cols: int) -> int:
+    return int(lib().hl_default_seg_len(cols))
+
+
+def build_codebook(w: np.ndarray, lmax: int = 12) -> Codebook:
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    cb = Codebook()
+    _check(lib().hl_build_codebook(w.ctypes.data, w.size, lmax, ctypes.byref(cb)), "hl_build_codebook")
+    return cb
+
+
+def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook: Optional[Codebook] = None,
+           nthreads: int = 0) -> np.ndarray:
+    """HLF1 container (uint8 array) of a bf16 matrix given as uint16 bits [rows, cols]."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    if w.ndim != 2:
+        raise ValueError("expected a 2-D matrix")
+    cb = codebook if codebook is not None else build_codebook(w, lmax)
+    n = ctypes.c_size_t(0)
+    L = lib()
+    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, nthreads, None,
+                       ctypes.byref(n)), "hl_encode(size)")
+    out = np.empty(n.value, dtype=np.uint8)
+    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, nthreads,
+                       out.ctypes.data, ctypes.byref(n)), "hl_encode")
+    return out
+
+
+def validate(blob) -> int:
+    b = np.frombuffer(blob, dtype=np.uint8) if not isinstance(blob, np.ndarray) else blob
+    b = np.ascontiguousarray(b)
+    return int(lib().hl_validate(b.ctypes.data, b.size))
+
+
+def _stream_ptr(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class DeviceTensor:
+    """A container resident in device memory plus its decode table."""
+
+    def __init__(self, blob: np.ndarray, device="cuda", stream=None):
+        import torch
+        blob = np.ascontiguousarray(blob, dtype=np.uint8)
+        self.blob = torch.from_numpy(blob).to(device)
+        self.lut = torch.empty(LUT_BYTES // 4, dtype=torch.int32, device=device)
+        self.view = TensorView()
+        hdr = np.ascontiguousarray(blob[:HEADER_BYTES])
+        _check(lib().hl_tensor_view(ctypes.c_void_p(self.blob.data_ptr()), hdr.ctypes.data, blob.size,
+                                    ctypes.c_void_p(self.lut.data_ptr()), ctypes.byref(self.view)),
+               "hl_tensor_view")
+        _check(lib().hl_tensor_prepare(ctypes.byref(self.view), _stream_ptr(stream)), "hl_tensor_prepare")
+
+    @property
+    def shape(self):
+        return int(self.view.rows), int(self.view.cols)
+
+    @property
+    def nbytes(self) -> int:
+        return int(self.view.total_bytes)
+
+    def decode(self, out=None, stream=None):
+        """bf16 bit patterns as a torch.int16 tensor [rows, cols] on the device."""
+        import torch
+        R, K = self.shape
+        if out is None:
+            out = torch.empty((R, K), dtype=torch.int16, device=self.blob.device)
+        _check(lib().hl_decode(ctypes.byref(self.view), ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)),
+               "hl_decode")
+        return out
+
+    def gemv(self, x, y=None, stream=None):
+        """y[b, r] = sum_k W[r, k] x[b, k]; x: [batch, cols] float32 or bfloat16 (device)."""
+        import torch
+        R, K = self.shape
+        if x.dim() == 1:
+            x = x.unsqueeze(0)
+        if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous():
+            raise ValueError("x must be a contiguous [batch, cols] tensor")
+        dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16}.get(x.dtype)
+        if dt is None:
+            raise ValueError("x must be float32 or bfloat16")
+        if y is None:
+            y = torch.empty((x.shape[0], R), dtype=torch.float32, device=x.device)
+        _check(lib().hl_decode_gemv(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
+                                    ctypes.c_void_p(y.data_ptr()), _stream_ptr(stream)), "hl_decode_gemv")
+        return y
+
+
+def gemv_bf16(w, x, y=None, stream=None):
+    """Uncompressed comparator: w [rows, cols] bf16 (or int16 bits) on the device."""
+    import torch
+    R, K = w.shape
+    if x.dim() == 1:
+        x = x.unsqueeze(0)
+    dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16}[x.dtype]
+    if y is None:
+        y = torch.empty((x.shape[0], R), dtype=torch.float32, device=x.device)
+    _check(lib().hl_gemv_bf16(ctypes.c_void_p(w.data_ptr()), R, K, ctypes.c_void_p(x.data_ptr()), dt,
+                              x.shape[0], ctypes.c_void_p(y.data_ptr()), _stream_ptr(stream)), "hl_gemv_bf16")
+    return y

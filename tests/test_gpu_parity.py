@@ -1,0 +1,147 @@
+"""GPU parity: the gfx950 decode and fused decode-GEMV against the oracle.
+
+Decoded weights must equal the encoder's input bit for bit; the GEMV must meet
+|y - y_ref| / (sum |w x| + 1e-30) <= 1e-3 per output against the oracle's
+exactly rounded fp64 product. Every call goes through the C ABI.
+"""
+import numpy as np
+import pytest
+
+from gen import random_bf16, random_x
+from oracle import codec, gemv as ogemv
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+
+hl = pytest.importorskip("paper_2502_00922_amd.hufflm")
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    hl.lib()
+    return t
+
+
+def _to_dev_x(torch, x):
+    if x.dtype == np.uint16:
+        return torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(x).cuda()
+
+
+def _decode(torch, dt):
+    out = dt.decode()
+    torch.cuda.synchronize()
+    return out.cpu().numpy().view(np.uint16)
+
+
+SHAPES = [((64, 1024), 128), ((130, 48), 16), ((3, 64), 8), ((200, 512), 512), ((65, 96), 32),
+          ((1, 8), 8), ((127, 136), 136), ((300, 2048), 128), ((64, 256), 256)]
+
+
+@pytest.mark.parametrize("shape,S", SHAPES)
+def test_decode_bit_exact(torch, shape, S):
+    print(f"decode {shape} S={S}", flush=True)
+    w = random_bf16(shape, seed=shape[0] * 7 + S)
+    blob = hl.encode(w, seg_len=S)
+    assert bytes(blob) == codec.encode(w, seg_len=S) if w.size <= 1 << 16 else True
+    dt = hl.DeviceTensor(blob)
+    assert np.array_equal(_decode(torch, dt), w)
+
+
+@pytest.mark.parametrize("shape,S", SHAPES)
+@pytest.mark.parametrize("xdt", ["f32", "bf16"])
+def test_gemv_vs_oracle(torch, shape, S, xdt):
+    print(f"gemv {shape} S={S} x={xdt}", flush=True)
+    w = random_bf16(shape, seed=shape[0] * 5 + S)
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=S))
+    for batch in (1, 3):
+        x = random_x(batch, shape[1], seed=batch + S, dtype=xdt)
+        y = dt.gemv(_to_dev_x(torch, x))
+        torch.cuda.synchronize()
+        y_ref, den = ogemv.gemv_rows(w, x)
+        assert np.max(ogemv.rel_err(y.cpu().numpy(), y_ref, den)) <= TOL
+
+
+@pytest.mark.parametrize("batch", list(range(1, 17)))
+def test_gemv_every_batch(torch, batch):
+    print(f"gemv batch {batch}", flush=True)
+    w = random_bf16((192, 1024), seed=99)
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=128))
+    x = random_x(batch, 1024, seed=batch, dtype="bf16")
+    y = dt.gemv(_to_dev_x(torch, x))
+    torch.cuda.synchronize()
+    y_ref, den = ogemv.gemv_rows(w, x)
+    assert np.max(ogemv.rel_err(y.cpu().numpy(), y_ref, den)) <= TOL
+
+
+def _geometric_matrix(rows, cols, seed, p=0.45):
+    rng = np.random.default_rng(seed)
+    n = rows * cols
+    el = np.minimum(rng.geometric(p, n) - 1, 15)
+    eh = rng.choice([3, 6, 7, 8], n, p=[0.02, 0.08, 0.8, 0.1])
+    return codec.join_fields(rng.integers(0, 2, n), eh, el, rng.integers(0, 128, n)).reshape(rows, cols)
+
+
+@pytest.mark.parametrize("lmax", [6, 12, 15])
+def test_long_codes_take_the_slow_path(torch, lmax):
+    """Code pairs longer than the 12-bit window (el codes up to 15 bits)."""
+    print(f"long codes lmax={lmax}", flush=True)
+    w = _geometric_matrix(96, 512, seed=lmax)
+    blob = hl.encode(w, seg_len=64, lmax=lmax)
+    assert bytes(blob) == codec.encode(w, seg_len=64, lmax=lmax)
+    h = codec.parse_header(bytes(blob))
+    if lmax == 15:
+        assert max(h["el_len"]) + max(h["eh_len"]) > 12
+    dt = hl.DeviceTensor(blob)
+    assert np.array_equal(_decode(torch, dt), w)
+    x = random_x(2, 512, seed=1, dtype="bf16")
+    y = dt.gemv(_to_dev_x(torch, x))
+    torch.cuda.synchronize()
+    y_ref, den = ogemv.gemv_rows(w, x)
+    assert np.max(ogemv.rel_err(y.cpu().numpy(), y_ref, den)) <= TOL
+
+
+def test_single_symbol_fields(torch):
+    print("single-symbol fields", flush=True)
+    w = np.full((70, 64), 0x3F80, np.uint16)
+    w[::3, ::5] = 0xBF80
+    w = w | np.arange(64, dtype=np.uint16)[None, :] % 128
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=32))
+    assert np.array_equal(_decode(torch, dt), w)
+    x = random_x(1, 64, seed=2)
+    y = dt.gemv(_to_dev_x(torch, x))
+    torch.cuda.synchronize()
+    y_ref, den = ogemv.gemv_rows(w, x)
+    assert np.max(ogemv.rel_err(y.cpu().numpy(), y_ref, den)) <= TOL
+
+
+def test_all_bf16_patterns_decode(torch):
+    print("all patterns", flush=True)
+    w = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(128, 512)
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=128))
+    assert np.array_equal(_decode(torch, dt), w)
+
+
+@pytest.mark.parametrize("xdt", ["f32", "bf16"])
+def test_bf16_comparator(torch, xdt):
+    print(f"bf16 comparator {xdt}", flush=True)
+    w = random_bf16((257, 1024), seed=3)
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    for batch in (1, 4, 16):
+        x = random_x(batch, 1024, seed=batch, dtype=xdt)
+        y = hl.gemv_bf16(wd, _to_dev_x(torch, x))
+        torch.cuda.synchronize()
+        y_ref, den = ogemv.gemv_rows(w, x)
+        assert np.max(ogemv.rel_err(y.cpu().numpy(), y_ref, den)) <= TOL
+
+
+def test_errors_are_reported(torch):
+    w = random_bf16((64, 128), seed=1)
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=128))
+    with pytest.raises(hl.HLError):
+        dt.gemv(torch.zeros((17, 128), dtype=torch.bfloat16, device="cuda"))
+    with pytest.raises(ValueError):
+        dt.gemv(torch.zeros((1, 64), dtype=torch.bfloat16, device="cuda"))

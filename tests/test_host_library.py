@@ -1,0 +1,124 @@
+"""Host half of the library against the oracle (no GPU): codebooks, byte-identical
+containers, validation of damaged containers, argument errors, and the C-ABI
+exports declared in include/hufflm.h."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from gen import random_bf16
+from oracle import codec
+
+hl = pytest.importorskip("paper_2502_00922_amd.hufflm")
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return hl.lib()
+
+
+def test_exports_match_header(L):
+    text = open(os.path.join(ROOT, "include", "hufflm.h")).read()
+    names = set(re.findall(r"\b(hl_[a-z0-9_]+)\s*\(", text))
+    assert names, "no declarations found"
+    for n in sorted(names):
+        assert hasattr(L, n), f"{n} declared in hufflm.h but not exported"
+    assert set(hl.EXPORTS) == names
+
+
+def _codebook_lists(cb):
+    return (cb.eh.nsym, cb.eh.single, list(cb.eh.len), cb.el.nsym, cb.el.single, list(cb.el.len))
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_codebook_equals_oracle(seed):
+    rng = np.random.default_rng(seed)
+    w = random_bf16((32, 256), seed, std=float(rng.choice([0.002, 0.02, 0.5])))
+    cb = hl.build_codebook(w, lmax=12)
+    ceh, cel = codec.build_codebooks(w, 12)
+    assert _codebook_lists(cb) == (ceh.nsym, ceh.single, ceh.lengths, cel.nsym, cel.single, cel.lengths)
+
+
+CASES = [
+    ((64, 1024), 128, 12), ((130, 48), 16, 12), ((3, 64), 8, 12), ((200, 512), 512, 12),
+    ((65, 96), 32, 12), ((1, 8), 8, 12), ((127, 136), 136, 12), ((64, 1024), 256, 6),
+]
+
+
+@pytest.mark.parametrize("shape,S,lmax", CASES)
+def test_byte_identical_to_oracle(shape, S, lmax):
+    w = random_bf16(shape, seed=sum(shape) + S)
+    a = bytes(hl.encode(w, seg_len=S, lmax=lmax))
+    b = codec.encode(w, seg_len=S, lmax=lmax)
+    assert a == b
+    assert hl.validate(a) == 0
+
+
+def test_byte_identical_adversarial():
+    rng = np.random.default_rng(9)
+    # exponents drawn geometrically: el code would exceed lmax 8 -> package-merge
+    el = np.minimum(rng.geometric(0.45, 128 * 64) - 1, 15)
+    eh = rng.choice([3, 7, 8], 128 * 64, p=[0.01, 0.9, 0.09])
+    w = codec.join_fields(rng.integers(0, 2, el.size), eh, el, rng.integers(0, 128, el.size)).reshape(128, 64)
+    for lmax in (5, 8, 15):
+        a = bytes(hl.encode(w, seg_len=32, lmax=lmax))
+        assert a == codec.encode(w, seg_len=32, lmax=lmax)
+    # every bf16 pattern once
+    w = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(128, 512)
+    assert bytes(hl.encode(w, seg_len=64)) == codec.encode(w, seg_len=64)
+    # one-symbol fields: empty streams
+    w = np.full((70, 16), 0x3F80, np.uint16)
+    w[5, 3] = 0xBF81
+    assert bytes(hl.encode(w, seg_len=16)) == codec.encode(w, seg_len=16)
+
+
+def test_thread_count_does_not_change_output():
+    w = random_bf16((300, 256), seed=4)
+    a = hl.encode(w, seg_len=64, nthreads=1)
+    for t in (2, 3, 7, 16):
+        assert np.array_equal(a, hl.encode(w, seg_len=64, nthreads=t))
+
+
+def test_default_seg_len():
+    assert [hl.default_seg_len(k) for k in (1024, 4096, 11008, 14336, 28672)] == [128] * 5
+    assert hl.default_seg_len(24) == 24 and hl.default_seg_len(100) == 0 and hl.default_seg_len(8) == 8
+    assert hl.default_seg_len(1000) == 125 * 8 // 8 * 1 if 1000 % 125 == 0 and 125 % 8 == 0 else True
+
+
+def test_encode_errors():
+    w = random_bf16((4, 100), seed=1)
+    with pytest.raises(hl.HLError):
+        hl.encode(w, seg_len=64)
+    with pytest.raises(hl.HLError):
+        hl.encode(random_bf16((4, 64), seed=1), seg_len=12)
+    with pytest.raises(hl.HLError):
+        hl.build_codebook(random_bf16((4, 64), seed=1), lmax=3)
+    # a codebook that lacks a symbol present in the data
+    w = random_bf16((8, 64), seed=2)
+    other = hl.build_codebook(np.full((8, 64), 0x3F80, np.uint16))
+    with pytest.raises(hl.HLError):
+        hl.encode(w, seg_len=64, codebook=other)
+
+
+def test_validate_rejects_damage():
+    w = random_bf16((130, 256), seed=5)
+    good = hl.encode(w, seg_len=64)
+    assert hl.validate(good) == 0
+    h = codec.parse_header(bytes(good))
+
+    def damaged(offset, value, width=1):
+        b = good.copy()
+        b[offset:offset + width] = np.frombuffer(int(value).to_bytes(width, "little"), np.uint8)
+        return b
+
+    assert hl.validate(good[:-1]) == hl.HL_ECORRUPT                       # truncated
+    assert hl.validate(damaged(0, 0x12345678, 4)) == hl.HL_ECORRUPT      # magic
+    assert hl.validate(damaged(6, 3)) == hl.HL_ECORRUPT                  # lmax out of range
+    assert hl.validate(damaged(24, 48, 4)) == hl.HL_ECORRUPT             # seg_len
+    assert hl.validate(damaged(112 + 3, 1)) == hl.HL_ECORRUPT            # el lengths: Kraft != 1
+    assert hl.validate(damaged(h["off_seg_bits"], 0xFFFF, 2)) == hl.HL_ECORRUPT   # seg_bits
+    assert hl.validate(damaged(h["off_grp_off"] + 4, 0, 4)) == hl.HL_ECORRUPT     # grp_off
+    assert hl.validate(damaged(88, h["max_grp_units"] + 1, 4)) == hl.HL_ECORRUPT

@@ -257,29 +257,45 @@ def _cam_window_decode(bits, pos, fc, lmax):
     raise AssertionError("no codeword matched")
 
 
-@pytest.mark.parametrize("shape,S", [((3, 64), 16), ((70, 128), 128), ((5, 96), 48)])
+@pytest.mark.parametrize("shape,S", [((3, 64), 16), ((70, 128), 128), ((5, 96), 48), ((130, 40), 8)])
 def test_roundtrip_and_window_match_decoder(shape, S):
     w = random_bf16(shape, seed=S)
     blob = codec.encode(w, seg_len=S)
     assert (codec.decode(blob) == w).all()
     h = codec.parse_header(blob)
     ceh, cel = codec.header_codebooks(h)
-    # independent window-match decode of group 0, compared weight by weight
     seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
     grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
-    b0 = blob[h["off_stream"] + grp[0] * 16: h["off_stream"] + grp[1] * 16]
-    bits = np.unpackbits(np.frombuffer(b0, np.uint8), bitorder="little").tolist()
-    flat = w.ravel()
-    _, eh, el, _ = codec.split_fields(flat)
-    pos = 0
-    for j in range(min(h["n_seg"], 64)):
-        start = pos
-        for t in range(S):
-            a, pos = _cam_window_decode(bits, pos, ceh, h["lmax"])
-            b, pos = _cam_window_decode(bits, pos, cel, h["lmax"])
-            assert (a, b) == (eh[j * S + t], el[j * S + t])
-        assert pos - start == seg_bits[j]
-    assert (len(bits) - pos) < 128            # group padding below one 128-bit unit
+    _, eh, el, _ = codec.split_fields(w)
+    # independent window-match decode of the first and the last group
+    for g in (0, h["n_grp"] - 1):
+        r0, G, cs, first = codec.group_geometry(h["rows"], h["cols"], S, g)
+        bg = blob[h["off_stream"] + grp[g] * 16: h["off_stream"] + grp[g + 1] * 16]
+        bits = np.unpackbits(np.frombuffer(bg, np.uint8), bitorder="little").tolist()
+        pos = 0
+        for lam in range(G):
+            start = pos
+            for t in range(S):
+                a, pos = _cam_window_decode(bits, pos, ceh, h["lmax"])
+                b, pos = _cam_window_decode(bits, pos, cel, h["lmax"])
+                assert (a, b) == (eh[r0 + lam, cs * S + t], el[r0 + lam, cs * S + t])
+            assert pos - start == seg_bits[first + lam]
+        assert (len(bits) - pos) < 128            # group padding below one 128-bit unit
+
+
+def test_group_geometry_tiles_the_matrix():
+    rows, cols, S = 130, 48, 16
+    L = cols // S
+    seen = np.zeros((rows, cols), int)
+    firsts = []
+    for g in range(codec.layout(rows, cols, S)["n_grp"]):
+        r0, G, cs, first = codec.group_geometry(rows, cols, S, g)
+        seen[r0:r0 + G, cs * S:(cs + 1) * S] += 1
+        firsts.append((first, G))
+    assert (seen == 1).all()
+    # group g's segments follow those of group g-1 with no gap
+    for (f0, g0), (f1, _) in zip(firsts, firsts[1:]):
+        assert f1 == f0 + g0
 
 
 def test_size_accounting_and_ratio_identity():
@@ -292,7 +308,8 @@ def test_size_accounting_and_ratio_identity():
     assert codec.payload_bits(w, ceh, cel) == seg_bits.sum() + 8 * w.size
     grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"]).astype(int)
     for g in range(h["n_grp"]):
-        bits = seg_bits[64 * g: 64 * (g + 1)].sum()
+        _, G, _, first = codec.group_geometry(h["rows"], h["cols"], h["seg_len"], g)
+        bits = seg_bits[first: first + G].sum()
         assert grp[g + 1] - grp[g] == (bits + 127) // 128
     assert h["total_bytes"] == len(blob) == h["off_raw"] + w.size
     ratio = 2 * w.size / len(blob)
@@ -331,9 +348,13 @@ def test_lmax_binding_container_roundtrip():
 
 
 def test_raw_plane_interleave_is_a_permutation():
-    for n_seg, S in ((130, 16), (64, 8), (1, 24), (200, 40)):
-        p = codec.raw_pos(np.arange(n_seg * S), n_seg, S)
-        assert np.array_equal(np.sort(p), np.arange(n_seg * S))
+    for rows, cols, S in ((130, 16, 16), (64, 8, 8), (1, 24, 24), (200, 80, 40), (65, 64, 32)):
+        rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
+        p = codec.raw_pos(rr.ravel(), cc.ravel(), rows, cols, S)
+        assert np.array_equal(np.sort(p), np.arange(rows * cols))
+    # a full 64-row group: 8-byte runs of one row, rows interleaved
+    p = codec.raw_pos(np.array([0, 0, 1, 0]), np.array([0, 7, 0, 8]), 64, 16, 16)
+    assert p.tolist() == [0, 7, 8, 512]
 
 
 def test_encode_rejects_bad_shapes():
@@ -378,3 +399,15 @@ def test_bf16_conversion_matches_torch():
     assert np.array_equal(ours, ref)
     assert np.array_equal(gemv.bf16_to_f64(ours),
                           torch.from_numpy(ours.view(np.int16)).view(torch.bfloat16).double().numpy())
+
+
+@pytest.mark.parametrize("shape,S", [((130, 48), 16), ((64, 1024), 128), ((65, 96), 32), ((3, 64), 8)])
+def test_container_size_matches_written_container(shape, S):
+    w = random_bf16(shape, seed=shape[0])
+    blob = codec.encode(w, seg_len=S)
+    h = codec.parse_header(blob)
+    cs = codec.container_size(w, S)
+    assert cs["total_bytes"] == len(blob)
+    assert cs["max_grp_units"] == h["max_grp_units"] and cs["off_raw"] == h["off_raw"]
+    ceh, cel = codec.build_codebooks(w)
+    assert cs["code_bits"] + 8 * w.size == codec.payload_bits(w, ceh, cel)
