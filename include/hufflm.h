@@ -94,7 +94,7 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
 #define HL_HEADER_BYTES 128u
 #define HL_GROUP_ROWS 64u
 #define HL_MAX_BATCH 16u
-#define HL_LUT_BYTES 16640u   /* 4096 joint entries + 64 words of tables */
+#define HL_LUT_BYTES 33024u   /* 8192 joint entries + 64 words of tables */
 
 typedef struct {
   uint8_t nsym;     /* symbols present in the field (1..16) */
@@ -157,7 +157,7 @@ hl_status hl_tensor_view(const void* blob_dev, const void* header_host,
                          size_t blob_bytes, uint32_t* lut_dev, hl_tensor* out);
 
 /* Fill t->lut_dev on the device: the joint decode table of the two codes for
- * a 12-bit window (the decoder's L_max-bit window match of Sec. 3.2) and the
+ * a 13-bit window (the decoder's L_max-bit window match of Sec. 3.2) and the
  * per-length canonical tables used for pairs longer than the window. */
 hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
 
@@ -165,12 +165,23 @@ hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
  * (row-major). Bit-exact with the encoder's input. */
 hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream);
 
+/* Bytes of device workspace hl_decode_gemv may use for cross-block partial
+ * sums of `t` at this batch (0 on bad arguments). */
+size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch);
+
 /* y[b][r] = sum_k W[r][k] * x[b][k] for b < batch, decoding W on the fly in
  * registers (Sec. 3.2: weights are decompressed only to be multiplied).
- * x_dev: [batch][cols] float32 or bf16; y_dev: [batch][rows] float32. fp32
- * accumulation. batch in [1, 16]. Errors: HL_EINVAL. */
+ * x_dev: [batch][cols] float32 or bf16; y_dev: [batch][rows] float32 (fully
+ * written). fp32 accumulation; every output is summed in a fixed order, so
+ * results do not vary between runs. batch in [1, 16].
+ * workspace_dev: hl_gemv_workspace_bytes(t, batch) bytes, zero-filled by the
+ * caller once before first use; each call leaves it ready for the next. Calls
+ * that may run concurrently need separate workspaces. With NULL (or too
+ * small) the product is still computed, with less parallelism for matrices
+ * with few rows. Errors: HL_EINVAL. */
 hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype,
-                         uint32_t batch, float* y_dev, void* stream);
+                         uint32_t batch, float* y_dev, void* workspace_dev,
+                         size_t workspace_bytes, void* stream);
 
 /* Uncompressed comparator: the same product from plain bf16 W [rows][cols]
  * in device memory. */

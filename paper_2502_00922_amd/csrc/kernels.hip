@@ -6,8 +6,8 @@
 // start pointer is matched against the codebook, the symbol is emitted and the
 // pointer advances by the code length; the raw sign is passed through and the
 // fields are concatenated back into the 16-bit weight. Here the "CAM" is a
-// 4096-entry table in LDS indexed by a 12-bit window that yields both codes of
-// a weight (exponent high and low nibble) at once; pairs longer than 12 bits
+// 8192-entry table in LDS indexed by a 13-bit window that yields both codes of
+// a weight (exponent high and low nibble) at once; pairs longer than 13 bits
 // fall back to a bit-serial canonical decode. Weights are decoded only where
 // they are multiplied (Sec. 1, Sec. 3.2): the fused kernel never writes them.
 //
@@ -25,18 +25,21 @@
 
 namespace hl {
 
-constexpr int kLutBits = 12;
+constexpr int kLutBits = 13;
 constexpr int kLutN = 1 << kLutBits;   // joint window table entries
 constexpr int kAuxWords = 64;          // canonical tables for the long-code path
 constexpr int kAuxField = 24;          // words per field in the aux table
-constexpr uint32_t kEsc = 0x80000000u;  // entry flag: pair longer than the window
+constexpr uint32_t kEsc = 0x40u;        // entry of a pair longer than the window
 constexpr int kPadWords = 4;           // zero words before a staged group stream
-constexpr int kMaxWaves = 4;
+constexpr int kMaxWaves = 8;
 
 static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
 
 // Joint table entry: bits 0..4 = code bits of the (eh, el) pair, bits 23..30 =
-// the exponent byte eh<<4|el (its place in a float32), bit 31 = kEsc.
+// the exponent byte eh<<4|el (its place in a float32), all other bits zero.
+// A window whose pair is longer than 13 bits maps to kEsc (0x40): as a shift
+// it moves nothing, as a position increment it adds 64, which four pairs of at
+// most 13 bits cannot reach, so one compare per four weights finds it.
 // Aux table, per field f at word f*24: [0] = nsym | single<<8 | maxlen<<16;
 // [l], l = 1..15: first_code<<16 | count<<8 | offset; [16..19]: symbols sorted
 // by (length, symbol), one byte each.
@@ -77,6 +80,10 @@ static Aux make_aux(const hl_codebook& cb) {
 
 // ------------------------------------------------------------------ device
 
+// Joint table and aux tables, at a fixed LDS address in every kernel that decodes.
+__shared__ uint32_t s_tab[kLutN + kAuxWords];
+extern __shared__ uint32_t s_dyn[];
+
 // One field, bit-serial canonical decode from `bits` (LSB = next bit), using
 // at most `avail` bits. Returns the symbol or -1 if no code of <= avail bits
 // matches.
@@ -99,8 +106,8 @@ __device__ inline int field_from_bits(const uint32_t* aux, uint32_t bits, uint32
   return -1;
 }
 
-// Builds the joint table: entry v decodes the 12-bit window v (bit 0 first).
-__global__ void __launch_bounds__(256) lut_kernel(uint32_t* lut, Aux aux) {
+// Builds the joint table: entry v decodes the 13-bit window v (bit 0 first).
+__global__ void __launch_bounds__(512) lut_kernel(uint32_t* lut, Aux aux) {
   for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
     uint32_t ua = 0, ub = 0;
     int a = field_from_bits(aux.w, (uint32_t)v, kLutBits, &ua);
@@ -146,44 +153,131 @@ struct GroupArgs {
   uint32_t rows, cols, S, L, RB, stream_units, wave_words, max_units;
 };
 
-// Stage group g's stream into this wave's LDS region and compute the lane's
-// start position; returns q2 (bit position within the region, minus 2).
+// Copies the joint table and the aux tables into LDS, four 16-byte loads in
+// flight per thread.
+__device__ inline void load_tables(const uint32_t* lut) {
+  constexpr uint32_t kVec = (kLutN + kAuxWords) / 4;  // uint4 count
+  const uint4* src = reinterpret_cast<const uint4*>(lut);
+  uint4* dst = reinterpret_cast<uint4*>(s_tab);
+  const uint32_t n = blockDim.x;
+  for (uint32_t k = threadIdx.x; k < kVec; k += 4 * n) {
+    const uint4 v0 = src[k];
+    const uint4 v1 = k + n < kVec ? src[k + n] : v0;
+    const uint4 v2 = k + 2 * n < kVec ? src[k + 2 * n] : v0;
+    const uint4 v3 = k + 3 * n < kVec ? src[k + 3 * n] : v0;
+    dst[k] = v0;
+    if (k + n < kVec) dst[k + n] = v1;
+    if (k + 2 * n < kVec) dst[k + 2 * n] = v2;
+    if (k + 3 * n < kVec) dst[k + 3 * n] = v3;
+  }
+}
+
+__device__ inline void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Stages group g's stream into this wave's LDS region (after kPadWords zero
+// words) and returns the lane's start as pos2 = bit position in the region - 2.
+// Reads are clamped to the stream section and to the region size.
 __device__ inline uint32_t stage_group(const GroupArgs& a, uint32_t* st, uint32_t g, uint32_t lane,
                                        uint32_t G, uint64_t first) {
+  const uint32_t nb = lane < G ? (uint32_t)a.seg_bits[first + lane] : 0u;
   uint32_t u0 = a.grp_off[g], u1 = a.grp_off[g + 1];
   u0 = min(u0, a.stream_units);
   u1 = min(max(u1, u0), a.stream_units);
   const uint32_t units = min(u1 - u0, a.max_units);
   uint4* dst = reinterpret_cast<uint4*>(st + kPadWords);
-  for (uint32_t k = lane; k < units; k += 64) dst[k] = a.stream[(uint64_t)u0 + k];
+  const uint4* src = a.stream + u0;
+  uint32_t k = lane;
+  for (; k + 192 < units; k += 256) {
+    const uint4 v0 = src[k], v1 = src[k + 64], v2 = src[k + 128], v3 = src[k + 192];
+    dst[k] = v0;
+    dst[k + 64] = v1;
+    dst[k + 128] = v2;
+    dst[k + 192] = v3;
+  }
+  for (; k < units; k += 64) dst[k] = src[k];
   if (lane == 0) *reinterpret_cast<uint4*>(st) = make_uint4(0, 0, 0, 0);
-  uint32_t nb = lane < G ? (uint32_t)a.seg_bits[first + lane] : 0u;
   uint32_t incl = nb;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    uint32_t t = __shfl_up(incl, d, 64);
+    const uint32_t t = __shfl_up(incl, d, 64);
     if ((int)lane >= d) incl += t;
   }
   const uint32_t start = min(incl - nb, units * 128u);
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   return kPadWords * 32u + start - 2u;
 }
 
-// Decodes 8 consecutive weights of the lane's segment: entries e[8] (table
-// format) and advances q2.
-__device__ inline void decode8(const uint32_t* lut, const uint32_t* aux, const uint32_t* st,
-                               uint32_t& q2, uint32_t e[8]) {
+// Positions: pos2 = bit position in the wave's LDS region minus 2, so that
+// the window's low 15 bits hold two old bits and the 13-bit peek already
+// scaled by 4, the byte offset of a table entry. In the fast loop pos2
+// accumulates whole table entries; only bits 0..22 are the position (exponent
+// bytes pile up above bit 22), so positions are read through kPosMask.
+constexpr uint32_t kPosMask = 0x7FFFFFu;
+
+// 64-bit window of stream bits [pos2, pos2 + 64) from the staged region.
+__device__ inline uint64_t load_window(const uint32_t* st, uint32_t pos2) {
+  const uint32_t wi = (pos2 & kPosMask) >> 5;
+  const uint32_t a = st[wi], b = st[wi + 1], c = st[wi + 2];
+  return ((uint64_t)__builtin_amdgcn_alignbit(c, b, pos2) << 32) | __builtin_amdgcn_alignbit(b, a, pos2);
+}
+
+__device__ inline uint32_t lut_at(uint32_t w) {
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_tab) +
+                                            (w & ((kLutN - 1) << 2)));
+}
+
+// Window shift by a table entry: v_lshrrev_b64 uses bits 0..5 of the entry,
+// which are the pair length (or 0 for kEsc).
+__device__ inline uint64_t shift_window(uint64_t w, uint32_t ent) {
+  uint64_t r;
+  asm("v_lshrrev_b64 %0, %1, %2" : "=v"(r) : "v"(ent), "v"(w));
+  return r;
+}
+
+struct Dec4 {
+  uint32_t pos2, e0, e1, e2, e3;
+};
+
+// Careful path: one weight at a time, long pairs decoded bit-serially.
+__device__ __noinline__ Dec4 decode4_careful(uint32_t st_off, uint32_t pos2) {
+  const uint32_t* st = s_dyn + st_off;
+  const uint32_t* aux = s_tab + kLutN;
+  uint32_t e[4];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    const uint32_t wi = q2 >> 5;
-    const uint32_t lo = st[wi], hi = st[wi + 1];
-    const uint32_t win = __builtin_amdgcn_alignbit(hi, lo, q2) & ((kLutN - 1) << 2);
-    uint32_t ent = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(lut) + win);
-    if (ent & kEsc) ent = slow_pair(st, aux, q2);
-    q2 += ent & 0xFF;
+  for (int k = 0; k < 4; ++k) {
+    uint32_t ent = lut_at((uint32_t)load_window(st, pos2));
+    if (ent & kEsc) ent = slow_pair(st, aux, pos2);
+    pos2 += ent & 0xFF;
     e[k] = ent;
+  }
+  return Dec4{pos2, e[0], e[1], e[2], e[3]};
+}
+
+// Decodes 4 weights: table entries e[4] (bits 23..30 = exponent byte), pos2
+// advanced. Four pairs of at most 13 bits fit in one 64-bit window, so the
+// window is loaded once; a long pair anywhere sends the lane through the
+// careful path from the block's start.
+__device__ inline void decode4(const uint32_t* st, uint32_t st_off, uint32_t& pos2, uint32_t* e) {
+  const uint32_t p0 = pos2 & kPosMask;
+  uint64_t W = load_window(st, p0);
+  e[0] = lut_at((uint32_t)W);
+  W = shift_window(W, e[0]);
+  e[1] = lut_at((uint32_t)W);
+  W = shift_window(W, e[1]);
+  e[2] = lut_at((uint32_t)W);
+  W = shift_window(W, e[2]);
+  e[3] = lut_at((uint32_t)W);
+  pos2 = p0 + e[0] + e[1] + e[2] + e[3];
+  if (((pos2 - p0) & kPosMask) >= 64u) {
+    const Dec4 d = decode4_careful(st_off, p0);
+    pos2 = d.pos2;
+    e[0] = d.e0;
+    e[1] = d.e1;
+    e[2] = d.e2;
+    e[3] = d.e3;
   }
 }
 
@@ -209,15 +303,17 @@ __device__ inline float dot2(uint32_t w, uint32_t x, float acc) {
                                          __builtin_bit_cast(bf16x2_t, x), acc, false);
 }
 
+__device__ inline uint2 raw_load(const uint8_t* raw, uint32_t t, uint32_t G) {
+  return *reinterpret_cast<const uint2*>(raw + (uint64_t)(t >> 3) * G * 8);
+}
+
 // ------------------------------------------------------------------ decode
 
-__global__ void __launch_bounds__(256) decode_kernel(GroupArgs a, uint16_t* out) {
-  extern __shared__ uint32_t smem[];
-  uint32_t* lut = smem;
-  uint32_t* aux = smem + kLutN;
+__global__ void __launch_bounds__(512) decode_kernel(GroupArgs a, uint16_t* out) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t* st = smem + kLutN + kAuxWords + wave * a.wave_words;
-  for (uint32_t i = threadIdx.x; i < kLutN + kAuxWords; i += blockDim.x) smem[i] = a.lut[i];
+  const uint32_t st_off = wave * a.wave_words;
+  uint32_t* st = s_dyn + st_off;
+  load_tables(a.lut);
   __syncthreads();
   const uint32_t n_grp = a.RB * a.L;
   const uint32_t waves = blockDim.x >> 6;
@@ -226,14 +322,18 @@ __global__ void __launch_bounds__(256) decode_kernel(GroupArgs a, uint16_t* out)
     const uint32_t r0 = rb * 64;
     const uint32_t G = min(64u, a.rows - r0);
     const uint64_t first = (uint64_t)r0 * a.L + (uint64_t)cs * G;
-    uint32_t q2 = stage_group(a, st, g, lane, G, first);
+    uint32_t pos2 = stage_group(a, st, g, lane, G, first);
+    wave_sync_lds();
     if (lane < G) {
       const uint8_t* raw = a.raw + first * a.S + lane * 8;
       uint16_t* o = out + (uint64_t)(r0 + lane) * a.cols + (uint64_t)cs * a.S;
+      uint2 rn = raw_load(raw, 0, G);
       for (uint32_t t = 0; t < a.S; t += 8) {
-        const uint2 rw = *reinterpret_cast<const uint2*>(raw + (uint64_t)(t >> 3) * G * 8);
+        const uint2 rw = rn;
+        if (t + 8 < a.S) rn = raw_load(raw, t + 8, G);
         uint32_t e[8];
-        decode8(lut, aux, st, q2, e);
+        decode4(st, st_off, pos2, e);
+        decode4(st, st_off, pos2, e + 4);
         uint4 v;
         v.x = pack_pair(rw.x, 0, e[0], e[1]);
         v.y = pack_pair(rw.x, 2, e[2], e[3]);
@@ -242,6 +342,7 @@ __global__ void __launch_bounds__(256) decode_kernel(GroupArgs a, uint16_t* out)
         *reinterpret_cast<uint4*>(o + t) = v;
       }
     }
+    wave_sync_lds();
   }
 }
 
@@ -251,22 +352,142 @@ struct GemvArgs {
   GroupArgs g;
   const void* x;
   float* y;
-  uint32_t C;       // column segments per block
-  uint32_t KS;      // blocks per row block
-  uint32_t atomic;  // 1: blocks add into y (zeroed beforehand); 0: store
+  float* partial;     // workspace: KS x B x (RB*64) partial sums (KS > 1)
+  uint32_t* counter;  // workspace: RB arrival counters, zero between calls
+  uint32_t C;         // column segments per block
+  uint32_t KS;        // blocks per row block
+  uint32_t x_words;   // LDS words of one wave's activation slice
 };
 
+// Direct global-to-LDS copies (no VGPR staging): every lane moves `size`
+// bytes from its own address to lds_base + lane * size; lds_base is
+// wave-uniform.
+__device__ inline void dma16(const void* src, uint32_t* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ inline void dma4(const void* src, uint32_t* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+}
+
+__device__ inline void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }    // vmcnt(0)
+__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }  // lgkmcnt(0)
+
+// Per-wave LDS region of the fused kernel, in words:
+//   [0, wave_words)                 stream: kPadWords zeros, group stream, guard
+//   [wave_words, +16*S)             raw plane of the group (64*S bytes)
+//   [wave_words + 16*S, +x_words)   activation slice [batch][S]
+struct WaveLds {
+  uint32_t* st;
+  uint32_t* raw;
+  uint32_t* xs;
+  uint32_t st_off;
+};
+
+// Issues the group's copies: stream units, raw plane and activation slice
+// (all asynchronous, counted by vmcnt); returns the lane's segment length.
 template <int B, bool XBF16>
-__global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p) {
-  extern __shared__ uint32_t smem[];
+__device__ inline uint32_t issue_group(const GemvArgs& p, const WaveLds& w, uint32_t g, uint32_t lane,
+                                       uint32_t G, uint64_t first, uint32_t c0, uint32_t* units_out) {
   const GroupArgs& a = p.g;
-  uint32_t* lut = smem;
-  uint32_t* aux = smem + kLutN;
+  const uint32_t S = a.S;
+  const uint32_t nb = lane < G ? (uint32_t)a.seg_bits[first + lane] : 0u;
+  uint32_t u0 = a.grp_off[g], u1 = a.grp_off[g + 1];
+  u0 = min(u0, a.stream_units);
+  u1 = min(max(u1, u0), a.stream_units);
+  const uint32_t units = min(u1 - u0, a.max_units);
+  *units_out = units;
+  for (uint32_t k0 = 0; k0 < units; k0 += 64)
+    if (k0 + lane < units) dma16(a.stream + (uint64_t)u0 + k0 + lane, w.st + kPadWords + k0 * 4);
+  const uint32_t raw_words = G * S / 4;
+  const uint32_t* rsrc = reinterpret_cast<const uint32_t*>(a.raw + first * S);
+  for (uint32_t k0 = 0; k0 < raw_words; k0 += 64)
+    if (k0 + lane < raw_words) dma4(rsrc + k0 + lane, w.raw + k0);
+  constexpr uint32_t kXPer = XBF16 ? 8 : 4;  // activations per 16 bytes
+  const uint32_t per_row = S / kXPer, total = per_row * B;
+  const uint4* xsrc = reinterpret_cast<const uint4*>(p.x);
+  const uint32_t row_u4 = a.cols / kXPer, c0_u4 = c0 / kXPer;
+  for (uint32_t k0 = 0; k0 < total; k0 += 64) {
+    const uint32_t k = k0 + lane;
+    if (k < total) {
+      const uint32_t b = k / per_row, j = k - b * per_row;
+      dma16(xsrc + (uint64_t)b * row_u4 + c0_u4 + j, w.xs + k0 * 4);
+    }
+  }
+  if (lane == 0) *reinterpret_cast<uint4*>(w.st) = make_uint4(0, 0, 0, 0);
+  return nb;
+}
+
+// Lane start (pos2) from the segment lengths: exclusive wave prefix sum.
+__device__ inline uint32_t lane_start(uint32_t nb, uint32_t lane, uint32_t units) {
+  uint32_t incl = nb;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t t = __shfl_up(incl, d, 64);
+    if ((int)lane >= d) incl += t;
+  }
+  return kPadWords * 32u + min(incl - nb, units * 128u) - 2u;
+}
+
+// Multiply-accumulate of 8 decoded weights (entries e, raw dword pair rw)
+// with the activations at column offset t of the staged slice.
+template <int B, bool XBF16>
+__device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint32_t* xs, uint32_t S,
+                            uint32_t t) {
+  if constexpr (XBF16) {
+    const uint32_t w0 = pack_pair(rw.x, 0, e[0], e[1]);
+    const uint32_t w1 = pack_pair(rw.x, 2, e[2], e[3]);
+    const uint32_t w2 = pack_pair(rw.y, 0, e[4], e[5]);
+    const uint32_t w3 = pack_pair(rw.y, 2, e[6], e[7]);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * (S / 2) + t / 2);
+      float s = acc[b];
+      s = dot2(w0, xv.x, s);
+      s = dot2(w1, xv.y, s);
+      s = dot2(w2, xv.z, s);
+      s = dot2(w3, xv.w, s);
+      acc[b] = s;
+    }
+  } else {
+    float wf[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) wf[k] = weight_f32(k < 4 ? rw.x : rw.y, k, e[k]);
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const float* xf = reinterpret_cast<const float*>(xs) + b * S + t;
+      const float4 x0 = *reinterpret_cast<const float4*>(xf);
+      const float4 x1 = *reinterpret_cast<const float4*>(xf + 4);
+      float s = acc[b];
+      s = fmaf(wf[0], x0.x, s);
+      s = fmaf(wf[1], x0.y, s);
+      s = fmaf(wf[2], x0.z, s);
+      s = fmaf(wf[3], x0.w, s);
+      s = fmaf(wf[4], x1.x, s);
+      s = fmaf(wf[5], x1.y, s);
+      s = fmaf(wf[6], x1.z, s);
+      s = fmaf(wf[7], x1.w, s);
+      acc[b] = s;
+    }
+  }
+}
+
+// Fused decode-GEMV. Block = (row block rb, k-part kp); its waves take the
+// column segments of [kp*C, min(L, (kp+1)*C)) in turn. For each group a wave
+// copies stream, raw plane and activations straight into its LDS region,
+// waits once, then decodes and multiplies out of LDS.
+template <int B, bool XBF16>
+__global__ void __launch_bounds__(512) gemv_kernel(GemvArgs p) {
+  const GroupArgs& a = p.g;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t waves = blockDim.x >> 6;
-  uint32_t* st = smem + kLutN + kAuxWords + wave * a.wave_words;
-  float* red = reinterpret_cast<float*>(smem + kLutN + kAuxWords + waves * a.wave_words);
-  for (uint32_t i = threadIdx.x; i < kLutN + kAuxWords; i += blockDim.x) smem[i] = a.lut[i];
+  const uint32_t S = a.S;
+  const uint32_t per_wave = a.wave_words + 16 * S + p.x_words;
+  WaveLds w;
+  w.st_off = wave * per_wave;
+  w.st = s_dyn + w.st_off;
+  w.raw = w.st + a.wave_words;
+  w.xs = w.raw + 16 * S;
+  load_tables(a.lut);
   __syncthreads();
 
   const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
@@ -280,82 +501,73 @@ __global__ void __launch_bounds__(256) gemv_kernel(GemvArgs p) {
   for (uint32_t cs = kp * p.C + wave; cs < cs_end; cs += waves) {
     const uint32_t g = rb * a.L + cs;
     const uint64_t first = (uint64_t)r0 * a.L + (uint64_t)cs * G;
-    uint32_t q2 = stage_group(a, st, g, lane, G, first);
-    const uint32_t c0 = cs * a.S;
+    uint32_t units;
+    const uint32_t nb = issue_group<B, XBF16>(p, w, g, lane, G, first, cs * S, &units);
+    uint32_t pos2 = lane_start(nb, lane, units);
+    wait_vm0();
+    wave_sync_lds();
     if (lane < G) {
-      const uint8_t* raw = a.raw + first * a.S + lane * 8;
-      for (uint32_t t = 0; t < a.S; t += 8) {
-        const uint2 rw = *reinterpret_cast<const uint2*>(raw + (uint64_t)(t >> 3) * G * 8);
+      const uint2* rl = reinterpret_cast<const uint2*>(w.raw) + lane;
+      for (uint32_t t = 0; t < S; t += 8) {
+        const uint2 rw = rl[(t >> 3) * G];
         uint32_t e[8];
-        decode8(lut, aux, st, q2, e);
-        const uint32_t col = __builtin_amdgcn_readfirstlane(c0 + t);
-        if constexpr (XBF16) {
-          const uint32_t w0 = pack_pair(rw.x, 0, e[0], e[1]);
-          const uint32_t w1 = pack_pair(rw.x, 2, e[2], e[3]);
-          const uint32_t w2 = pack_pair(rw.y, 0, e[4], e[5]);
-          const uint32_t w3 = pack_pair(rw.y, 2, e[6], e[7]);
-          const uint16_t* xb = reinterpret_cast<const uint16_t*>(p.x);
-#pragma unroll
-          for (int b = 0; b < B; ++b) {
-            const uint4 xv = *reinterpret_cast<const uint4*>(xb + (uint64_t)b * a.cols + col);
-            float s = acc[b];
-            s = dot2(w0, xv.x, s);
-            s = dot2(w1, xv.y, s);
-            s = dot2(w2, xv.z, s);
-            s = dot2(w3, xv.w, s);
-            acc[b] = s;
-          }
-        } else {
-          float wf[8];
-#pragma unroll
-          for (int k = 0; k < 8; ++k) wf[k] = weight_f32(k < 4 ? rw.x : rw.y, k, e[k]);
-          const float* xf = reinterpret_cast<const float*>(p.x);
-#pragma unroll
-          for (int b = 0; b < B; ++b) {
-            const float4 x0 = *reinterpret_cast<const float4*>(xf + (uint64_t)b * a.cols + col);
-            const float4 x1 = *reinterpret_cast<const float4*>(xf + (uint64_t)b * a.cols + col + 4);
-            float s = acc[b];
-            s = fmaf(wf[0], x0.x, s);
-            s = fmaf(wf[1], x0.y, s);
-            s = fmaf(wf[2], x0.z, s);
-            s = fmaf(wf[3], x0.w, s);
-            s = fmaf(wf[4], x1.x, s);
-            s = fmaf(wf[5], x1.y, s);
-            s = fmaf(wf[6], x1.z, s);
-            s = fmaf(wf[7], x1.w, s);
-            acc[b] = s;
-          }
-        }
+        decode4(w.st, w.st_off, pos2, e);
+        decode4(w.st, w.st_off, pos2, e + 4);
+        mac8<B, XBF16>(acc, e, rw, w.xs, S, t);
       }
     }
+    wait_lgkm0();
+    wave_sync_lds();
   }
-  // Cross-wave reduction in a fixed order, then one store (or add) per row.
+  // Cross-wave reduction in a fixed order (the wave regions are free now).
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(s_dyn);
 #pragma unroll
   for (int b = 0; b < B; ++b) red[(wave * B + b) * 64 + lane] = acc[b];
   __syncthreads();
-  if (wave == 0 && lane < G) {
+  if (wave != 0) return;
+  float s[B];
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    s[b] = red[b * 64 + lane];
+    for (uint32_t v = 1; v < waves; ++v) s[b] += red[(v * B + b) * 64 + lane];
+  }
+  const uint32_t ldy = a.rows;
+  if (p.KS == 1) {
+    if (lane < G)
+#pragma unroll
+      for (int b = 0; b < B; ++b) p.y[(uint64_t)b * ldy + r0 + lane] = s[b];
+    return;
+  }
+  // Several blocks share this row block: publish the partial sums, and the
+  // last block to arrive adds them in k-part order and resets the counter.
+  const uint32_t ldp = a.RB * 64;
+#pragma unroll
+  for (int b = 0; b < B; ++b) p.partial[((uint64_t)kp * B + b) * ldp + r0 + lane] = s[b];
+  __threadfence();
+  uint32_t old = 0;
+  if (lane == 0) old = atomicAdd(p.counter + rb, 1u);
+  old = __shfl(old, 0, 64);
+  if (old != p.KS - 1) return;
+  __threadfence();
+  if (lane < G) {
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-      float s = red[b * 64 + lane];
-      for (uint32_t w = 1; w < waves; ++w) s += red[(w * B + b) * 64 + lane];
-      float* dst = p.y + (uint64_t)b * a.rows + r0 + lane;
-      if (p.atomic) unsafeAtomicAdd(dst, s);
-      else *dst = s;
+      float t = 0.f;
+      for (uint32_t k = 0; k < p.KS; ++k)
+        t += __hip_atomic_load(p.partial + ((uint64_t)k * B + b) * ldp + r0 + lane, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      p.y[(uint64_t)b * ldy + r0 + lane] = t;
     }
   }
-}
-
-__global__ void zero_kernel(float* y, uint64_t n) {
-  for (uint64_t i = blockIdx.x * (uint64_t)blockDim.x + threadIdx.x; i < n;
-       i += (uint64_t)gridDim.x * blockDim.x)
-    y[i] = 0.f;
+  if (lane == 0) __hip_atomic_store(p.counter + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ------------------------------------------------------------------ bf16 GEMV
 
 // One wave per row; lanes stride the row in 8-weight chunks; dot2 on pairs.
 template <int B, bool XBF16>
-__global__ void __launch_bounds__(256) gemv_bf16_kernel(const uint16_t* w, const void* x, float* y,
+__global__ void __launch_bounds__(512) gemv_bf16_kernel(const uint16_t* w, const void* x, float* y,
                                                         uint32_t rows, uint32_t cols) {
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t waves = blockDim.x >> 6;
@@ -421,7 +633,7 @@ struct Plan {
   size_t lds;
 };
 
-static hl_status make_plan(const hl_tensor* t, uint32_t red_words_per_wave, Plan* pl) {
+static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, Plan* pl) {
   if (!t || !t->blob_dev || !t->lut_dev) return HL_EINVAL;
   if (t->rows >= (1ull << 31) || t->cols >= (1ull << 31) || t->n_grp >= (1ull << 31))
     return HL_EUNSUPPORTED;
@@ -443,12 +655,14 @@ static hl_status make_plan(const hl_tensor* t, uint32_t red_words_per_wave, Plan
   const uint32_t guard = (t->seg_len * 2 * 15 + 64) / 32 + 4;
   uint32_t ww = kPadWords + t->max_grp_units * 4 + guard;
   ww = (ww + 3) & ~3u;
+  extra_words_per_wave = (extra_words_per_wave + 3) & ~3u;
   a.wave_words = ww;
+  // LDS: the static tables plus, per wave, the stream region and the extras.
+  const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
   uint32_t waves = kMaxWaves;
-  while (waves > 1 && (size_t)(kLutN + kAuxWords + waves * (ww + red_words_per_wave)) * 4 > kMaxLds)
-    --waves;
-  size_t lds = (size_t)(kLutN + kAuxWords + waves * (ww + red_words_per_wave)) * 4;
-  if (lds > kMaxLds) return HL_EUNSUPPORTED;
+  while (waves > 1 && tab + (size_t)waves * (ww + extra_words_per_wave) * 4 > kMaxLds) --waves;
+  const size_t lds = (size_t)waves * (ww + extra_words_per_wave) * 4;
+  if (tab + lds > kMaxLds) return HL_EUNSUPPORTED;
   pl->waves = waves;
   pl->lds = lds;
   return HL_OK;
@@ -456,7 +670,7 @@ static hl_status make_plan(const hl_tensor* t, uint32_t red_words_per_wave, Plan
 
 template <class K, class... A>
 static hl_status launch(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, A... args) {
-  if (lds > 64 * 1024) {
+  if (lds + (kLutN + kAuxWords) * 4 > 64 * 1024) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
       return HL_EHIP;
@@ -544,42 +758,65 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
   hl_status st = make_plan(t, 0, &pl);
   if (st != HL_OK) return st;
   const uint32_t n_grp = pl.ga.RB * pl.ga.L;
-  const uint32_t per_cu = std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)pl.lds));
+  const uint32_t per_cu =
+      std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)(pl.lds + (kLutN + kAuxWords) * 4)));
   const uint32_t blocks = std::min<uint32_t>((n_grp + pl.waves - 1) / pl.waves, device_cus() * per_cu);
   return launch(decode_kernel, dim3(blocks), dim3(pl.waves * 64), pl.lds, (hipStream_t)stream, pl.ga,
                 out_dev);
 }
 
+static uint32_t ks_cap(uint32_t L) { return std::min<uint32_t>(L, 64); }
+
+static uint64_t workspace_counter_bytes(uint32_t RB) { return ((uint64_t)RB * 4 + 255) & ~255ull; }
+
+extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
+  if (!t || t->seg_len == 0 || batch < 1 || batch > HL_MAX_BATCH) return 0;
+  const uint32_t RB = (uint32_t)((t->rows + 63) / 64);
+  const uint32_t L = (uint32_t)(t->cols / t->seg_len);
+  return workspace_counter_bytes(RB) + (uint64_t)ks_cap(L) * batch * RB * 64 * 4;
+}
+
 extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
-                                    float* y_dev, void* stream) {
+                                    float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (!x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || (x_dtype != HL_F32 && x_dtype != HL_BF16))
     return HL_EINVAL;
+  const bool xb = x_dtype == HL_BF16;
+  const uint32_t x_words = t ? (xb ? t->seg_len * batch / 2 : t->seg_len * batch) : 0;
   Plan pl;
-  hl_status st = make_plan(t, batch * 64, &pl);
+  hl_status st = make_plan(t, 16 * (t ? t->seg_len : 0) + x_words, &pl);
   if (st != HL_OK) return st;
   GemvArgs p;
+  std::memset(&p, 0, sizeof(p));
   p.g = pl.ga;
   p.x = x_dev;
   p.y = y_dev;
+  p.x_words = x_words;
   // Column segments per block: enough blocks to fill the device, each wave
-  // decoding at least one group.
+  // decoding at least one group; KS blocks share a row block.
   const uint32_t L = pl.ga.L, RB = pl.ga.RB;
   const uint64_t target_waves = (uint64_t)device_cus() * 16;
-  uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * L + target_waves - 1) / target_waves);
+  const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * L + target_waves - 1) / target_waves);
   uint32_t C = std::min<uint32_t>(L, pl.waves * gpw);
-  p.C = C;
-  p.KS = (L + C - 1) / C;
-  p.atomic = p.KS > 1 ? 1u : 0u;
-  hipStream_t s = (hipStream_t)stream;
-  if (p.atomic) {
-    const uint64_t n = (uint64_t)batch * t->rows;
-    hipLaunchKernelGGL(zero_kernel, dim3((uint32_t)std::min<uint64_t>((n + 255) / 256, 4096)), dim3(256), 0, s,
-                       y_dev, n);
-    if (hipGetLastError() != hipSuccess) return HL_EHIP;
+  uint32_t KS = (L + C - 1) / C;
+  if (KS > ks_cap(L)) {
+    KS = ks_cap(L);
+    C = (L + KS - 1) / KS;
+    KS = (L + C - 1) / C;
   }
-  const dim3 grid(RB * p.KS), block(pl.waves * 64);
-  const bool xb = x_dtype == HL_BF16;
-  HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, pl.lds, s, p);
+  if (KS > 1 && (!workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch))) {
+    KS = 1;  // no room for partial sums: one block per row block
+    C = L;
+  }
+  p.C = C;
+  p.KS = KS;
+  if (KS > 1) {
+    p.counter = reinterpret_cast<uint32_t*>(workspace_dev);
+    p.partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
+  }
+  const dim3 grid(RB * KS), block(pl.waves * 64);
+  // the cross-wave reduction reuses the wave regions
+  const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * batch * 64 * 4);
+  HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
 }
 
 extern "C" hl_status hl_gemv_bf16(const uint16_t* w_dev, uint64_t rows, uint64_t cols, const void* x_dev,

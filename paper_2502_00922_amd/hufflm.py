@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(HERE, "libhufflm.so")
 HL_OK, HL_EINVAL, HL_ENOMEM, HL_ECORRUPT, HL_EUNSUPPORTED, HL_EHIP = range(6)
 HL_F32, HL_BF16 = 0, 1
 HEADER_BYTES = 128
-LUT_BYTES = 16640
+LUT_BYTES = 33024
 MAX_BATCH = 16
 
 
@@ -55,7 +55,8 @@ class TensorView(ctypes.Structure):
 _lib = None
 
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_build_codebook", "hl_encode", "hl_validate",
-           "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_decode_gemv", "hl_gemv_bf16"]
+           "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
+           "hl_decode_gemv", "hl_gemv_bf16"]
 
 
 def lib() -> ctypes.CDLL:
@@ -84,9 +85,11 @@ def lib() -> ctypes.CDLL:
     L.hl_tensor_prepare.argtypes = [c.POINTER(TensorView), c.c_void_p]
     L.hl_decode.restype = c.c_int
     L.hl_decode.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_void_p]
+    L.hl_gemv_workspace_bytes.restype = c.c_size_t
+    L.hl_gemv_workspace_bytes.argtypes = [c.POINTER(TensorView), c.c_uint32]
     L.hl_decode_gemv.restype = c.c_int
     L.hl_decode_gemv.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
-                                 c.c_void_p]
+                                 c.c_void_p, c.c_size_t, c.c_void_p]
     L.hl_gemv_bf16.restype = c.c_int
     L.hl_gemv_bf16.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.c_void_p, c.c_int, c.c_uint32,
                                c.c_void_p, c.c_void_p]
@@ -176,8 +179,21 @@ class DeviceTensor:
                "hl_decode")
         return out
 
-    def gemv(self, x, y=None, stream=None):
-        """y[b, r] = sum_k W[r, k] x[b, k]; x: [batch, cols] float32 or bfloat16 (device)."""
+    def workspace(self, batch: int = MAX_BATCH):
+        """Zeroed device workspace for gemv at up to ``batch`` rows (cached)."""
+        import torch
+        need = int(lib().hl_gemv_workspace_bytes(ctypes.byref(self.view), batch))
+        ws = getattr(self, "_ws", None)
+        if ws is None or ws.numel() < need:
+            ws = torch.zeros(max(need, 4), dtype=torch.uint8, device=self.blob.device)
+            self._ws = ws
+        return ws
+
+    def gemv(self, x, y=None, stream=None, workspace=None):
+        """y[b, r] = sum_k W[r, k] x[b, k]; x: [batch, cols] float32 or bfloat16 (device).
+
+        ``workspace`` defaults to a cached zeroed buffer owned by this tensor;
+        pass False to run without one."""
         import torch
         R, K = self.shape
         if x.dim() == 1:
@@ -189,8 +205,13 @@ class DeviceTensor:
             raise ValueError("x must be float32 or bfloat16")
         if y is None:
             y = torch.empty((x.shape[0], R), dtype=torch.float32, device=x.device)
+        if workspace is None:
+            workspace = self.workspace()
+        ws_ptr, ws_n = (None, 0) if workspace is False else (ctypes.c_void_p(workspace.data_ptr()),
+                                                              workspace.numel())
         _check(lib().hl_decode_gemv(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
-                                    ctypes.c_void_p(y.data_ptr()), _stream_ptr(stream)), "hl_decode_gemv")
+                                    ctypes.c_void_p(y.data_ptr()), ws_ptr, ws_n, _stream_ptr(stream)),
+               "hl_decode_gemv")
         return y
 
 

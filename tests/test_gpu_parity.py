@@ -87,14 +87,14 @@ def _geometric_matrix(rows, cols, seed, p=0.45):
 
 @pytest.mark.parametrize("lmax", [6, 12, 15])
 def test_long_codes_take_the_slow_path(torch, lmax):
-    """Code pairs longer than the 12-bit window (el codes up to 15 bits)."""
+    """Code pairs longer than the 13-bit window (el codes up to 15 bits)."""
     print(f"long codes lmax={lmax}", flush=True)
     w = _geometric_matrix(96, 512, seed=lmax)
     blob = hl.encode(w, seg_len=64, lmax=lmax)
     assert bytes(blob) == codec.encode(w, seg_len=64, lmax=lmax)
     h = codec.parse_header(bytes(blob))
     if lmax == 15:
-        assert max(h["el_len"]) + max(h["eh_len"]) > 12
+        assert max(h["el_len"]) + max(h["eh_len"]) > 13
     dt = hl.DeviceTensor(blob)
     assert np.array_equal(_decode(torch, dt), w)
     x = random_x(2, 512, seed=1, dtype="bf16")
