@@ -34,7 +34,7 @@
  * column range, one row per lane of a 64-wide wavefront. Segments are
  * numbered in group order: group g starts at segment 64*L*rb + cs*G.
  *
- * Stream: for each weight of a segment in order, code(eh) then code(el),
+ * Stream: for each weight of a segment in order, code(el) then code(eh),
  * each emitted most-significant bit first; the stream is packed least
  * significant bit first (bit k is bit k%8 of byte k/8). The segments of a
  * group are concatenated in lane order without gaps; each group stream starts on a 16-byte

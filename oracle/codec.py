@@ -20,8 +20,9 @@ code-length limit L_max = 12 by default (Sec. 3.2 / 5.2 report 12 as the
 empirical maximum); textbook heap Huffman with ties broken leaf-before-node,
 leaves by symbol, nodes by creation order; package-merge when the Huffman code
 is longer than L_max; canonical code values in the RFC 1951 Sec. 3.2.2 order;
-codes emitted most-significant bit first into a stream packed least-significant
-bit first; a one-symbol field gets code length 0; segments of S weights along a
+each weight's pair stored as code(el) then code(eh); codes emitted
+most-significant bit first into a stream packed least-significant bit first;
+a one-symbol field gets code length 0; segments of S weights along a
 row are the unit of independent decoding.
 
 Tiling: segment (r, cs) holds W[r, cs*S : cs*S+S]; row block rb holds rows
@@ -308,7 +309,7 @@ def build_codebooks(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode
 def segment_stream(eh_seg, el_seg, ceh: FieldCode, cel: FieldCode) -> Tuple[int, int]:
     """Bit stream of one segment as (integer, bit count).
 
-    For each weight in order: code(eh) then code(el), each emitted MSB-first;
+    For each weight in order: code(el) then code(eh), each emitted MSB-first;
     stream bit k is bit k of the integer (least-significant first)."""
     rev_eh = [bit_reverse(ceh.codes[v], ceh.lengths[v]) for v in range(NSYM)]
     rev_el = [bit_reverse(cel.codes[v], cel.lengths[v]) for v in range(NSYM)]
@@ -317,7 +318,7 @@ def segment_stream(eh_seg, el_seg, ceh: FieldCode, cel: FieldCode) -> Tuple[int,
     for a, b in zip(eh_seg, el_seg):
         la = ceh.lengths[a] if ceh.nsym > 1 else 0
         lb = cel.lengths[b] if cel.nsym > 1 else 0
-        acc |= (rev_eh[a] | (rev_el[b] << la)) << pos
+        acc |= (rev_el[b] | (rev_eh[a] << lb)) << pos
         pos += la + lb
     return acc, pos
 
@@ -424,8 +425,8 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, np.ndarray]:
         eh = np.zeros(S, np.uint32)
         el = np.zeros(S, np.uint32)
         for t in range(S):
-            eh[t], pos = ceh.decode_one(bits, pos)
             el[t], pos = cel.decode_one(bits, pos)
+            eh[t], pos = ceh.decode_one(bits, pos)
         if pos - start != int(seg_bits[first + lam]):
             raise ValueError("segment length mismatch")
         rp = raw_pos(np.full(S, r0 + lam), cs * S + np.arange(S), rows, cols, S)

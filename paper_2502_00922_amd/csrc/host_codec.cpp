@@ -326,7 +326,7 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   if (cb->lmax < 4 || cb->lmax > 15 || !field_code_valid(cb->eh, cb->lmax) ||
       !field_code_valid(cb->el, cb->lmax))
     return HL_EINVAL;
-  // Pair table: reversed codes of (eh, el), eh first; length 0 for one-symbol fields.
+  // Pair table: reversed codes of the pair, el first; length 0 for one-symbol fields.
   uint32_t ceh[16], cel[16];
   canonical_codes(cb->eh.len, ceh);
   canonical_codes(cb->el.len, cel);
@@ -343,7 +343,7 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   std::array<bool, 256> pvalid;
   for (int e = 0; e < 256; ++e) {
     int a = e >> 4, b = e & 15;
-    pcode[e] = bit_reverse(ceh[a], leh[a]) | (bit_reverse(cel[b], lel[b]) << leh[a]);
+    pcode[e] = bit_reverse(cel[b], lel[b]) | (bit_reverse(ceh[a], leh[a]) << lel[b]);
     plen[e] = (uint8_t)(leh[a] + lel[b]);
     pvalid[e] = veh[a] && vel[b];
   }

@@ -35,7 +35,7 @@ constexpr int kMaxWaves = 8;
 
 static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
 
-// Joint table entry: bits 0..4 = code bits of the (eh, el) pair, bits 23..30 =
+// Joint table entry: bits 0..4 = code bits of the (el, eh) pair, bits 23..30 =
 // the exponent byte eh<<4|el (its place in a float32), all other bits zero.
 // A window whose pair is longer than 13 bits maps to kEsc (0x40): as a shift
 // it moves nothing, as a position increment it adds 64, which four pairs of at
@@ -110,8 +110,8 @@ __device__ inline int field_from_bits(const uint32_t* aux, uint32_t bits, uint32
 __global__ void __launch_bounds__(512) lut_kernel(uint32_t* lut, Aux aux) {
   for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
     uint32_t ua = 0, ub = 0;
-    int a = field_from_bits(aux.w, (uint32_t)v, kLutBits, &ua);
-    int b = a < 0 ? -1 : field_from_bits(aux.w + kAuxField, (uint32_t)v >> ua, kLutBits - ua, &ub);
+    const int b = field_from_bits(aux.w + kAuxField, (uint32_t)v, kLutBits, &ub);           // el first
+    const int a = b < 0 ? -1 : field_from_bits(aux.w, (uint32_t)v >> ub, kLutBits - ub, &ua);
     lut[v] = (a < 0 || b < 0) ? kEsc : ((ua + ub) | ((uint32_t)((a << 4) | b) << 23));
   }
   for (int i = threadIdx.x; i < kAuxWords; i += blockDim.x) lut[kLutN + i] = aux.w[i];
@@ -139,8 +139,8 @@ __device__ inline uint32_t slow_field(const uint32_t* st, const uint32_t* aux, u
 // Long pair at window position q2 (= bit position - 2): entry in table format.
 __device__ __noinline__ uint32_t slow_pair(const uint32_t* st, const uint32_t* aux, uint32_t q2) {
   uint32_t p = q2 + 2;
+  const uint32_t b = slow_field(st, aux + kAuxField, p);  // el first
   const uint32_t a = slow_field(st, aux, p);
-  const uint32_t b = slow_field(st, aux + kAuxField, p);
   return (p - q2 - 2) | (((a << 4) | b) << 23);
 }
 
@@ -541,15 +541,19 @@ __global__ void __launch_bounds__(512) gemv_kernel(GemvArgs p) {
   }
   // Several blocks share this row block: publish the partial sums, and the
   // last block to arrive adds them in k-part order and resets the counter.
+  // Partials are written and read with agent-scope atomics, which bypass the
+  // per-XCD caches; once the stores are complete (vmcnt 0) the counter
+  // increment orders them, so no cache write-back or invalidate is needed.
   const uint32_t ldp = a.RB * 64;
 #pragma unroll
-  for (int b = 0; b < B; ++b) p.partial[((uint64_t)kp * B + b) * ldp + r0 + lane] = s[b];
-  __threadfence();
+  for (int b = 0; b < B; ++b)
+    __hip_atomic_store(p.partial + ((uint64_t)kp * B + b) * ldp + r0 + lane, s[b], __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   uint32_t old = 0;
-  if (lane == 0) old = atomicAdd(p.counter + rb, 1u);
+  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   old = __shfl(old, 0, 64);
   if (old != p.KS - 1) return;
-  __threadfence();
   if (lane < G) {
 #pragma unroll
     for (int b = 0; b < B; ++b) {

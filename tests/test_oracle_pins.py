@@ -276,8 +276,8 @@ def test_roundtrip_and_window_match_decoder(shape, S):
         for lam in range(G):
             start = pos
             for t in range(S):
-                a, pos = _cam_window_decode(bits, pos, ceh, h["lmax"])
                 b, pos = _cam_window_decode(bits, pos, cel, h["lmax"])
+                a, pos = _cam_window_decode(bits, pos, ceh, h["lmax"])
                 assert (a, b) == (eh[r0 + lam, cs * S + t], el[r0 + lam, cs * S + t])
             assert pos - start == seg_bits[first + lam]
         assert (len(bits) - pos) < 128            # group padding below one 128-bit unit
