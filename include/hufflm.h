@@ -114,7 +114,7 @@ typedef struct {
   uint32_t* lut_dev;         /* HL_LUT_BYTES, filled by hl_tensor_prepare */
   uint64_t rows, cols, n_seg, n_grp, total_bytes;
   uint64_t off_seg_bits, off_grp_off, off_stream, off_raw;
-  uint32_t seg_len, lmax, max_grp_units, reserved;
+  uint32_t seg_len, lmax, max_grp_units, max_seg_bits;
   hl_codebook cb;
 } hl_tensor;
 
@@ -150,10 +150,10 @@ hl_status hl_encode(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,
 hl_status hl_validate(const void* blob_host, size_t blob_bytes);
 
 /* Build a device view of a container copied to `blob_dev` (blob_bytes long)
- * from its header (the first HL_HEADER_BYTES, host copy). Checks the header
- * (O(1)); lut_dev must point to HL_LUT_BYTES of device memory that the view
- * uses from now on. Errors: HL_EINVAL, HL_ECORRUPT. */
-hl_status hl_tensor_view(const void* blob_dev, const void* header_host,
+ * from its host copy `blob_host` (the same bytes), which is fully validated
+ * (as hl_validate, O(n_seg)). lut_dev must point to HL_LUT_BYTES of device
+ * memory that the view uses from now on. Errors: HL_EINVAL, HL_ECORRUPT. */
+hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
                          size_t blob_bytes, uint32_t* lut_dev, hl_tensor* out);
 
 /* Fill t->lut_dev on the device: the joint decode table of the two codes for

@@ -31,5 +31,8 @@ bool header_consistent(const Header& h, uint64_t blob_bytes);
 bool field_code_valid(const hl_field_code& fc, uint32_t lmax);
 void canonical_codes(const uint8_t len[16], uint32_t code[16]);
 uint32_t default_seg_len(uint64_t cols);
+// Full structural check of a host copy; fills the header and the longest
+// segment (in code bits).
+hl_status validate_blob(const uint8_t* b, size_t bytes, Header* out, uint32_t* max_seg_bits);
 
 }  // namespace hl

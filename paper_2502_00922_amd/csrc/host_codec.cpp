@@ -433,28 +433,39 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   return HL_OK;
 }
 
-extern "C" hl_status hl_validate(const void* blob, size_t bytes) {
-  if (!blob || bytes < HL_HEADER_BYTES) return HL_ECORRUPT;
+namespace hl {
+
+hl_status validate_blob(const uint8_t* b, size_t bytes, Header* out, uint32_t* max_seg_bits) {
+  if (!b || bytes < HL_HEADER_BYTES) return HL_ECORRUPT;
   Header H;
-  const uint8_t* b = (const uint8_t*)blob;
   if (!parse_header(b, &H) || !header_consistent(H, bytes)) return HL_ECORRUPT;
   const uint16_t* sb = (const uint16_t*)(b + H.off_seg_bits);
   const uint32_t* go = (const uint32_t*)(b + H.off_grp_off);
   if (go[0] != 0) return HL_ECORRUPT;
-  uint32_t mx = 0;
+  uint32_t mx = 0, mseg = 0;
   const uint64_t max_seg = (uint64_t)H.seg_len * 2 * H.cb.lmax;
   const uint64_t L = H.cols / H.seg_len;
   for (uint64_t g = 0; g < H.n_grp; ++g) {
     GroupGeom q = group_geom(H.rows, L, g);
     uint64_t bits = 0;
     for (uint32_t lam = 0; lam < q.G; ++lam) {
-      if (sb[q.first + lam] > max_seg) return HL_ECORRUPT;
-      bits += sb[q.first + lam];
+      const uint32_t v = sb[q.first + lam];
+      if (v > max_seg) return HL_ECORRUPT;
+      bits += v;
+      mseg = std::max(mseg, v);
     }
     if (go[g + 1] < go[g] || go[g + 1] - go[g] != (bits + 127) / 128) return HL_ECORRUPT;
     mx = std::max(mx, go[g + 1] - go[g]);
   }
   if (mx != H.max_grp_units) return HL_ECORRUPT;
   if (H.off_raw != align64(H.off_stream + (uint64_t)go[H.n_grp] * 16)) return HL_ECORRUPT;
+  if (out) *out = H;
+  if (max_seg_bits) *max_seg_bits = mseg;
   return HL_OK;
+}
+
+}  // namespace hl
+
+extern "C" hl_status hl_validate(const void* blob, size_t bytes) {
+  return validate_blob((const uint8_t*)blob, bytes, nullptr, nullptr);
 }

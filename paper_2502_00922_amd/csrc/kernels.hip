@@ -5,16 +5,20 @@
 // Decoding follows the decoder of Huff-LLM Sec. 3.2: a window of bits at the
 // start pointer is matched against the codebook, the symbol is emitted and the
 // pointer advances by the code length; the raw sign is passed through and the
-// fields are concatenated back into the 16-bit weight. Here the "CAM" is a
+// fields are concatenated back into the 16-bit weight. Here the "CAM" is an
 // 8192-entry table in LDS indexed by a 13-bit window that yields both codes of
-// a weight (exponent high and low nibble) at once; pairs longer than 13 bits
+// a weight (exponent low and high nibble) at once; pairs longer than 13 bits
 // fall back to a bit-serial canonical decode. Weights are decoded only where
 // they are multiplied (Sec. 1, Sec. 3.2): the fused kernel never writes them.
 //
 // Work mapping (container tiling in include/hufflm.h): one wavefront decodes
 // one group = 64 rows x one S-column segment, lane lam owning row 64rb+lam.
-// All lanes of a wave therefore read the same activations, which are loaded
-// once into scalar registers.
+// Per group a wave copies, straight from HBM into its LDS region:
+//   * each lane's part of the group stream into a column of words (word j of
+//     lane lam at row j, column lam), so that window reads never share an
+//     LDS bank between lanes;
+//   * the raw sign/mantissa plane ([t/8][lane] in 8-byte units);
+//   * the activation slice x[b][c0 .. c0+S), which every lane reads alike.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -29,9 +33,9 @@ constexpr int kLutBits = 13;
 constexpr int kLutN = 1 << kLutBits;   // joint window table entries
 constexpr int kAuxWords = 64;          // canonical tables for the long-code path
 constexpr int kAuxField = 24;          // words per field in the aux table
-constexpr uint32_t kEsc = 0x40u;        // entry of a pair longer than the window
-constexpr int kPadWords = 4;           // zero words before a staged group stream
+constexpr uint32_t kEsc = 0x40u;       // entry of a pair longer than the window
 constexpr int kMaxWaves = 8;
+constexpr uint32_t kCol = 64;          // row stride of the stream columns, in words
 
 static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
 
@@ -40,9 +44,9 @@ static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
 // A window whose pair is longer than 13 bits maps to kEsc (0x40): as a shift
 // it moves nothing, as a position increment it adds 64, which four pairs of at
 // most 13 bits cannot reach, so one compare per four weights finds it.
-// Aux table, per field f at word f*24: [0] = nsym | single<<8 | maxlen<<16;
-// [l], l = 1..15: first_code<<16 | count<<8 | offset; [16..19]: symbols sorted
-// by (length, symbol), one byte each.
+// Aux table, per field f (0 = eh, 1 = el) at word f*24: [0] = nsym |
+// single<<8 | maxlen<<16; [l], l = 1..15: first_code<<16 | count<<8 | offset;
+// [16..19]: symbols sorted by (length, symbol), one byte each.
 struct Aux {
   uint32_t w[kAuxWords];
 };
@@ -107,51 +111,15 @@ __device__ inline int field_from_bits(const uint32_t* aux, uint32_t bits, uint32
 }
 
 // Builds the joint table: entry v decodes the 13-bit window v (bit 0 first).
-__global__ void __launch_bounds__(512) lut_kernel(uint32_t* lut, Aux aux) {
+__global__ void __launch_bounds__(256) lut_kernel(uint32_t* lut, Aux aux) {
   for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
     uint32_t ua = 0, ub = 0;
-    const int b = field_from_bits(aux.w + kAuxField, (uint32_t)v, kLutBits, &ub);           // el first
+    const int b = field_from_bits(aux.w + kAuxField, (uint32_t)v, kLutBits, &ub);  // el first
     const int a = b < 0 ? -1 : field_from_bits(aux.w, (uint32_t)v >> ub, kLutBits - ub, &ua);
     lut[v] = (a < 0 || b < 0) ? kEsc : ((ua + ub) | ((uint32_t)((a << 4) | b) << 23));
   }
   for (int i = threadIdx.x; i < kAuxWords; i += blockDim.x) lut[kLutN + i] = aux.w[i];
 }
-
-// Bit-serial decode of one field from the staged stream at bit p (advanced).
-__device__ inline uint32_t slow_field(const uint32_t* st, const uint32_t* aux, uint32_t& p) {
-  const uint32_t meta = aux[0];
-  if ((meta & 0xFF) == 1) return (meta >> 8) & 0xFF;
-  const uint32_t maxl = (meta >> 16) & 0xFF;
-  uint32_t code = 0;
-  for (uint32_t l = 1; l <= maxl; ++l) {
-    code = (code << 1) | ((st[p >> 5] >> (p & 31)) & 1u);
-    ++p;
-    const uint32_t w = aux[l];
-    const uint32_t d = code - (w >> 16);
-    if (d < ((w >> 8) & 0xFF)) {
-      const uint32_t k = (w & 0xFF) + d;
-      return (aux[16 + (k >> 2)] >> (8 * (k & 3))) & 0xFF;
-    }
-  }
-  return 0;  // no code matched: damaged stream, decode continues safely
-}
-
-// Long pair at window position q2 (= bit position - 2): entry in table format.
-__device__ __noinline__ uint32_t slow_pair(const uint32_t* st, const uint32_t* aux, uint32_t q2) {
-  uint32_t p = q2 + 2;
-  const uint32_t b = slow_field(st, aux + kAuxField, p);  // el first
-  const uint32_t a = slow_field(st, aux, p);
-  return (p - q2 - 2) | (((a << 4) | b) << 23);
-}
-
-struct GroupArgs {
-  const uint16_t* seg_bits;
-  const uint32_t* grp_off;
-  const uint4* stream;
-  const uint8_t* raw;
-  const uint32_t* lut;   // global copy: kLutN entries + aux
-  uint32_t rows, cols, S, L, RB, stream_units, wave_words, max_units;
-};
 
 // Copies the joint table and the aux tables into LDS, four 16-byte loads in
 // flight per thread.
@@ -177,50 +145,59 @@ __device__ inline void wave_sync_lds() {
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
+__device__ inline void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ inline void wait_vm1() { asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); }
+__device__ inline void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
-// Stages group g's stream into this wave's LDS region (after kPadWords zero
-// words) and returns the lane's start as pos2 = bit position in the region - 2.
-// Reads are clamped to the stream section and to the region size.
-__device__ inline uint32_t stage_group(const GroupArgs& a, uint32_t* st, uint32_t g, uint32_t lane,
-                                       uint32_t G, uint64_t first) {
-  const uint32_t nb = lane < G ? (uint32_t)a.seg_bits[first + lane] : 0u;
-  uint32_t u0 = a.grp_off[g], u1 = a.grp_off[g + 1];
-  u0 = min(u0, a.stream_units);
-  u1 = min(max(u1, u0), a.stream_units);
-  const uint32_t units = min(u1 - u0, a.max_units);
-  uint4* dst = reinterpret_cast<uint4*>(st + kPadWords);
-  const uint4* src = a.stream + u0;
-  uint32_t k = lane;
-  for (; k + 192 < units; k += 256) {
-    const uint4 v0 = src[k], v1 = src[k + 64], v2 = src[k + 128], v3 = src[k + 192];
-    dst[k] = v0;
-    dst[k + 64] = v1;
-    dst[k + 128] = v2;
-    dst[k + 192] = v3;
-  }
-  for (; k < units; k += 64) dst[k] = src[k];
-  if (lane == 0) *reinterpret_cast<uint4*>(st) = make_uint4(0, 0, 0, 0);
-  uint32_t incl = nb;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t t = __shfl_up(incl, d, 64);
-    if ((int)lane >= d) incl += t;
-  }
-  const uint32_t start = min(incl - nb, units * 128u);
-  return kPadWords * 32u + start - 2u;
+// Direct global-to-LDS copies (no VGPR staging): every lane moves `size`
+// bytes from its own address to lds_base + lane * size; lds_base is
+// wave-uniform.
+__device__ inline void dma16(const void* src, uint32_t* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+__device__ inline void dma4(const void* src, uint32_t* lds_base) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
 }
 
-// Positions: pos2 = bit position in the wave's LDS region minus 2, so that
-// the window's low 15 bits hold two old bits and the 13-bit peek already
-// scaled by 4, the byte offset of a table entry. In the fast loop pos2
-// accumulates whole table entries; only bits 0..22 are the position (exponent
-// bytes pile up above bit 22), so positions are read through kPosMask.
+// ---- stream columns
+// A lane's column pointer `sc` addresses its row-0 word; word j is sc[j*64].
+// Row 0 is padding: a lane's first stream word sits in row 1, so positions
+// start at 32 + (start bit within that word).
+//
+// Positions: pos2 = column bit position minus 2, so that the window's low
+// 15 bits hold two old bits and the 13-bit peek already scaled by 4, the
+// byte offset of a table entry. In the fast loop pos2 accumulates whole table
+// entries; only bits 0..22 are the position (exponent bytes pile up above bit
+// 22), so positions are read through kPosMask.
 constexpr uint32_t kPosMask = 0x7FFFFFu;
 
-// 64-bit window of stream bits [pos2, pos2 + 64) from the staged region.
-__device__ inline uint64_t load_window(const uint32_t* st, uint32_t pos2) {
-  const uint32_t wi = (pos2 & kPosMask) >> 5;
-  const uint32_t a = st[wi], b = st[wi + 1], c = st[wi + 2];
+__device__ inline uint32_t col_word(const uint32_t* sc, uint32_t j) { return sc[j * kCol]; }
+
+// Bit-serial decode of one field from the lane's column at bit p (advanced);
+// rows beyond jmax are read as row jmax.
+__device__ inline uint32_t slow_field(const uint32_t* sc, const uint32_t* aux, uint32_t& p, uint32_t jmax) {
+  const uint32_t meta = aux[0];
+  if ((meta & 0xFF) == 1) return (meta >> 8) & 0xFF;
+  const uint32_t maxl = (meta >> 16) & 0xFF;
+  uint32_t code = 0;
+  for (uint32_t l = 1; l <= maxl; ++l) {
+    code = (code << 1) | ((col_word(sc, min(p >> 5, jmax)) >> (p & 31)) & 1u);
+    ++p;
+    const uint32_t w = aux[l];
+    const uint32_t d = code - (w >> 16);
+    if (d < ((w >> 8) & 0xFF)) {
+      const uint32_t k = (w & 0xFF) + d;
+      return (aux[16 + (k >> 2)] >> (8 * (k & 3))) & 0xFF;
+    }
+  }
+  return 0;  // no code matched: damaged stream, decode continues safely
+}
+
+// 64-bit window of column bits [pos2, pos2 + 64); jmax bounds the first row
+// read (two more rows follow) so that a damaged stream cannot leave the region.
+__device__ inline uint64_t load_window(const uint32_t* sc, uint32_t pos2, uint32_t jmax) {
+  const uint32_t j = min((pos2 & kPosMask) >> 5, jmax);
+  const uint32_t a = col_word(sc, j), b = col_word(sc, j + 1), c = col_word(sc, j + 2);
   return ((uint64_t)__builtin_amdgcn_alignbit(c, b, pos2) << 32) | __builtin_amdgcn_alignbit(b, a, pos2);
 }
 
@@ -242,14 +219,19 @@ struct Dec4 {
 };
 
 // Careful path: one weight at a time, long pairs decoded bit-serially.
-__device__ __noinline__ Dec4 decode4_careful(uint32_t st_off, uint32_t pos2) {
-  const uint32_t* st = s_dyn + st_off;
+__device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
+  const uint32_t* sc = s_dyn + sc_off;
   const uint32_t* aux = s_tab + kLutN;
   uint32_t e[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    uint32_t ent = lut_at((uint32_t)load_window(st, pos2));
-    if (ent & kEsc) ent = slow_pair(st, aux, pos2);
+    uint32_t ent = lut_at((uint32_t)load_window(sc, pos2, jmax));
+    if (ent & kEsc) {
+      uint32_t p = pos2 + 2;
+      const uint32_t b = slow_field(sc, aux + kAuxField, p, jmax + 2);  // el first
+      const uint32_t a = slow_field(sc, aux, p, jmax + 2);
+      ent = (p - pos2 - 2) | (((a << 4) | b) << 23);
+    }
     pos2 += ent & 0xFF;
     e[k] = ent;
   }
@@ -260,9 +242,10 @@ __device__ __noinline__ Dec4 decode4_careful(uint32_t st_off, uint32_t pos2) {
 // advanced. Four pairs of at most 13 bits fit in one 64-bit window, so the
 // window is loaded once; a long pair anywhere sends the lane through the
 // careful path from the block's start.
-__device__ inline void decode4(const uint32_t* st, uint32_t st_off, uint32_t& pos2, uint32_t* e) {
+__device__ inline void decode4(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2,
+                               uint32_t* e) {
   const uint32_t p0 = pos2 & kPosMask;
-  uint64_t W = load_window(st, p0);
+  uint64_t W = load_window(sc, p0, jmax);
   e[0] = lut_at((uint32_t)W);
   W = shift_window(W, e[0]);
   e[1] = lut_at((uint32_t)W);
@@ -272,7 +255,7 @@ __device__ inline void decode4(const uint32_t* st, uint32_t st_off, uint32_t& po
   e[3] = lut_at((uint32_t)W);
   pos2 = p0 + e[0] + e[1] + e[2] + e[3];
   if (((pos2 - p0) & kPosMask) >= 64u) {
-    const Dec4 d = decode4_careful(st_off, p0);
+    const Dec4 d = decode4_careful(sc_off, jmax, p0);
     pos2 = d.pos2;
     e[0] = d.e0;
     e[1] = d.e1;
@@ -303,37 +286,123 @@ __device__ inline float dot2(uint32_t w, uint32_t x, float acc) {
                                          __builtin_bit_cast(bf16x2_t, x), acc, false);
 }
 
-__device__ inline uint2 raw_load(const uint8_t* raw, uint32_t t, uint32_t G) {
-  return *reinterpret_cast<const uint2*>(raw + (uint64_t)(t >> 3) * G * 8);
+// ------------------------------------------------------------------ staging
+
+struct GroupArgs {
+  const uint16_t* seg_bits;
+  const uint32_t* grp_off;
+  const uint4* stream;
+  const uint8_t* raw;
+  const uint32_t* lut;   // global copy: kLutN entries + aux
+  uint32_t rows, cols, S, L, RB, stream_units, max_units;
+  uint32_t col_rows;     // rows of the stream columns (row 0 = padding)
+};
+
+// Group geometry and its metadata (segment length of the lane, stream units).
+struct Meta {
+  uint64_t first;  // group-order number of the group's first segment
+  uint32_t r0, G, cs, nb, u0, units;
+};
+
+// Issues the metadata loads of group g (vector loads, counted by vmcnt).
+__device__ inline Meta load_meta(const GroupArgs& a, uint32_t g, uint32_t lane) {
+  Meta m;
+  const uint32_t rb = g / a.L;
+  m.cs = g - rb * a.L;
+  m.r0 = rb * 64;
+  m.G = min(64u, a.rows - m.r0);
+  m.first = (uint64_t)m.r0 * a.L + (uint64_t)m.cs * m.G;
+  m.nb = lane < m.G ? (uint32_t)a.seg_bits[m.first + lane] : 0u;
+  m.u0 = a.grp_off[g + (lane & 1)];  // lane 0: start, lane 1: end
+  m.units = 0;
+  return m;
+}
+
+__device__ inline uint32_t wave_max(uint32_t v) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, d, 64));
+  return v;
+}
+
+// Copies the group's stream into the lane columns of region `cols`; returns
+// the lane's pos2 (column bit position - 2).
+__device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta& m, uint32_t lane) {
+  uint32_t v0 = (uint32_t)__shfl((int)m.u0, 0, 64), v1 = (uint32_t)__shfl((int)m.u0, 1, 64);
+  v0 = min(v0, a.stream_units);
+  v1 = min(max(v1, v0), a.stream_units);
+  m.u0 = v0;
+  m.units = min(v1 - v0, a.max_units);
+  uint32_t incl = m.nb;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t t = __shfl_up(incl, d, 64);
+    if ((int)lane >= d) incl += t;
+  }
+  const uint32_t start = min(incl - m.nb, m.units * 128u);
+  const uint32_t ws = start >> 5, bit0 = start & 31;
+  // words the lane's windows read: its bits plus two words of window overrun
+  const uint32_t nw = ((bit0 + m.nb + 31) >> 5) + 2;
+  const uint32_t J = m.units ? min(wave_max(nw), a.col_rows - 1) : 0u;
+  const uint32_t* src = reinterpret_cast<const uint32_t*>(a.stream + m.u0);
+  const uint32_t last = m.units * 4 - 1;
+  for (uint32_t j = 0; j < J; ++j) dma4(src + min(ws + j, last), cols + (j + 1) * kCol);
+  return 30u + bit0;
+}
+
+// Copies the group's raw plane (G*S bytes) into `raw_lds`.
+__device__ inline void issue_raw(const GroupArgs& a, uint32_t* raw_lds, const Meta& m, uint32_t lane) {
+  const uint32_t bytes = m.G * a.S;
+  const uint8_t* src = a.raw + m.first * a.S;
+  if ((a.S & 15) == 0) {
+    const uint32_t n = bytes / 16;
+    for (uint32_t k0 = 0; k0 < n; k0 += 64)
+      if (k0 + lane < n) dma16(src + (uint64_t)(k0 + lane) * 16, raw_lds + k0 * 4);
+  } else {
+    const uint32_t n = bytes / 4;
+    for (uint32_t k0 = 0; k0 < n; k0 += 64)
+      if (k0 + lane < n) dma4(src + (uint64_t)(k0 + lane) * 4, raw_lds + k0);
+  }
 }
 
 // ------------------------------------------------------------------ decode
 
+// Decode to bf16. Waves take groups in turn; region per wave: stream columns
+// then the raw plane.
 __global__ void __launch_bounds__(512) decode_kernel(GroupArgs a, uint16_t* out) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const uint32_t st_off = wave * a.wave_words;
-  uint32_t* st = s_dyn + st_off;
+  const uint32_t waves = blockDim.x >> 6;
+  const uint32_t per_wave = a.col_rows * kCol + 16 * a.S;
+  uint32_t* cols = s_dyn + wave * per_wave;
+  uint32_t* raw_lds = cols + a.col_rows * kCol;
+  const uint32_t sc_off = wave * per_wave + lane;
+  const uint32_t* sc = s_dyn + sc_off;
+  const uint32_t jmax = a.col_rows - 3;
+  const uint32_t n_grp = a.RB * a.L;
+  const uint32_t stride = gridDim.x * waves;
+  uint32_t g = blockIdx.x * waves + wave;
+  Meta m;
+  if (g < n_grp) m = load_meta(a, g, lane);
   load_tables(a.lut);
   __syncthreads();
-  const uint32_t n_grp = a.RB * a.L;
-  const uint32_t waves = blockDim.x >> 6;
-  for (uint32_t g = blockIdx.x * waves + wave; g < n_grp; g += gridDim.x * waves) {
-    const uint32_t rb = g / a.L, cs = g % a.L;
-    const uint32_t r0 = rb * 64;
-    const uint32_t G = min(64u, a.rows - r0);
-    const uint64_t first = (uint64_t)r0 * a.L + (uint64_t)cs * G;
-    uint32_t pos2 = stage_group(a, st, g, lane, G, first);
+  for (; g < n_grp; g += stride) {
+    uint32_t pos2 = issue_stream(a, cols, m, lane);
+    issue_raw(a, raw_lds, m, lane);
+    const Meta cur = m;
+    if (g + stride < n_grp) {
+      m = load_meta(a, g + stride, lane);
+      wait_vm1();
+    } else {
+      wait_vm0();
+    }
     wave_sync_lds();
-    if (lane < G) {
-      const uint8_t* raw = a.raw + first * a.S + lane * 8;
-      uint16_t* o = out + (uint64_t)(r0 + lane) * a.cols + (uint64_t)cs * a.S;
-      uint2 rn = raw_load(raw, 0, G);
+    if (lane < cur.G) {
+      const uint2* rl = reinterpret_cast<const uint2*>(raw_lds) + lane;
+      uint16_t* o = out + (uint64_t)(cur.r0 + lane) * a.cols + (uint64_t)cur.cs * a.S;
       for (uint32_t t = 0; t < a.S; t += 8) {
-        const uint2 rw = rn;
-        if (t + 8 < a.S) rn = raw_load(raw, t + 8, G);
+        const uint2 rw = rl[(t >> 3) * cur.G];
         uint32_t e[8];
-        decode4(st, st_off, pos2, e);
-        decode4(st, st_off, pos2, e + 4);
+        decode4(sc, sc_off, jmax, pos2, e);
+        decode4(sc, sc_off, jmax, pos2, e + 4);
         uint4 v;
         v.x = pack_pair(rw.x, 0, e[0], e[1]);
         v.y = pack_pair(rw.x, 2, e[2], e[3]);
@@ -342,6 +411,7 @@ __global__ void __launch_bounds__(512) decode_kernel(GroupArgs a, uint16_t* out)
         *reinterpret_cast<uint4*>(o + t) = v;
       }
     }
+    wait_lgkm0();
     wave_sync_lds();
   }
 }
@@ -359,73 +429,20 @@ struct GemvArgs {
   uint32_t x_words;   // LDS words of one wave's activation slice
 };
 
-// Direct global-to-LDS copies (no VGPR staging): every lane moves `size`
-// bytes from its own address to lds_base + lane * size; lds_base is
-// wave-uniform.
-__device__ inline void dma16(const void* src, uint32_t* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-}
-__device__ inline void dma4(const void* src, uint32_t* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
-}
-
-__device__ inline void wait_vm0() { __builtin_amdgcn_s_waitcnt(0x0F70); }    // vmcnt(0)
-__device__ inline void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }  // lgkmcnt(0)
-
-// Per-wave LDS region of the fused kernel, in words:
-//   [0, wave_words)                 stream: kPadWords zeros, group stream, guard
-//   [wave_words, +16*S)             raw plane of the group (64*S bytes)
-//   [wave_words + 16*S, +x_words)   activation slice [batch][S]
-struct WaveLds {
-  uint32_t* st;
-  uint32_t* raw;
-  uint32_t* xs;
-  uint32_t st_off;
-};
-
-// Issues the group's copies: stream units, raw plane and activation slice
-// (all asynchronous, counted by vmcnt); returns the lane's segment length.
+// Copies x[b][c0 .. c0+S) for every batch row into xs ([batch][S]).
 template <int B, bool XBF16>
-__device__ inline uint32_t issue_group(const GemvArgs& p, const WaveLds& w, uint32_t g, uint32_t lane,
-                                       uint32_t G, uint64_t first, uint32_t c0, uint32_t* units_out) {
-  const GroupArgs& a = p.g;
-  const uint32_t S = a.S;
-  const uint32_t nb = lane < G ? (uint32_t)a.seg_bits[first + lane] : 0u;
-  uint32_t u0 = a.grp_off[g], u1 = a.grp_off[g + 1];
-  u0 = min(u0, a.stream_units);
-  u1 = min(max(u1, u0), a.stream_units);
-  const uint32_t units = min(u1 - u0, a.max_units);
-  *units_out = units;
-  for (uint32_t k0 = 0; k0 < units; k0 += 64)
-    if (k0 + lane < units) dma16(a.stream + (uint64_t)u0 + k0 + lane, w.st + kPadWords + k0 * 4);
-  const uint32_t raw_words = G * S / 4;
-  const uint32_t* rsrc = reinterpret_cast<const uint32_t*>(a.raw + first * S);
-  for (uint32_t k0 = 0; k0 < raw_words; k0 += 64)
-    if (k0 + lane < raw_words) dma4(rsrc + k0 + lane, w.raw + k0);
+__device__ inline void issue_x(const GemvArgs& p, uint32_t* xs, uint32_t c0, uint32_t lane) {
   constexpr uint32_t kXPer = XBF16 ? 8 : 4;  // activations per 16 bytes
-  const uint32_t per_row = S / kXPer, total = per_row * B;
+  const uint32_t per_row = p.g.S / kXPer, total = per_row * B;
   const uint4* xsrc = reinterpret_cast<const uint4*>(p.x);
-  const uint32_t row_u4 = a.cols / kXPer, c0_u4 = c0 / kXPer;
+  const uint32_t row_u4 = p.g.cols / kXPer, c0_u4 = c0 / kXPer;
   for (uint32_t k0 = 0; k0 < total; k0 += 64) {
     const uint32_t k = k0 + lane;
     if (k < total) {
       const uint32_t b = k / per_row, j = k - b * per_row;
-      dma16(xsrc + (uint64_t)b * row_u4 + c0_u4 + j, w.xs + k0 * 4);
+      dma16(xsrc + (uint64_t)b * row_u4 + c0_u4 + j, xs + k0 * 4);
     }
   }
-  if (lane == 0) *reinterpret_cast<uint4*>(w.st) = make_uint4(0, 0, 0, 0);
-  return nb;
-}
-
-// Lane start (pos2) from the segment lengths: exclusive wave prefix sum.
-__device__ inline uint32_t lane_start(uint32_t nb, uint32_t lane, uint32_t units) {
-  uint32_t incl = nb;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const uint32_t t = __shfl_up(incl, d, 64);
-    if ((int)lane >= d) incl += t;
-  }
-  return kPadWords * 32u + min(incl - nb, units * 128u) - 2u;
 }
 
 // Multiply-accumulate of 8 decoded weights (entries e, raw dword pair rw)
@@ -472,48 +489,55 @@ __device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint3
 }
 
 // Fused decode-GEMV. Block = (row block rb, k-part kp); its waves take the
-// column segments of [kp*C, min(L, (kp+1)*C)) in turn. For each group a wave
-// copies stream, raw plane and activations straight into its LDS region,
-// waits once, then decodes and multiplies out of LDS.
+// column segments of [kp*C, min(L, (kp+1)*C)) in turn. Region per wave:
+// stream columns, raw plane, activation slice.
 template <int B, bool XBF16>
 __global__ void __launch_bounds__(512) gemv_kernel(GemvArgs p) {
   const GroupArgs& a = p.g;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t waves = blockDim.x >> 6;
   const uint32_t S = a.S;
-  const uint32_t per_wave = a.wave_words + 16 * S + p.x_words;
-  WaveLds w;
-  w.st_off = wave * per_wave;
-  w.st = s_dyn + w.st_off;
-  w.raw = w.st + a.wave_words;
-  w.xs = w.raw + 16 * S;
-  load_tables(a.lut);
-  __syncthreads();
+  const uint32_t per_wave = a.col_rows * kCol + 16 * S + p.x_words;
+  uint32_t* cols = s_dyn + wave * per_wave;
+  uint32_t* raw_lds = cols + a.col_rows * kCol;
+  uint32_t* xs = raw_lds + 16 * S;
+  const uint32_t sc_off = wave * per_wave + lane;
+  const uint32_t* sc = s_dyn + sc_off;
+  const uint32_t jmax = a.col_rows - 3;
 
   const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
   const uint32_t r0 = rb * 64;
   const uint32_t G = min(64u, a.rows - r0);
   const uint32_t cs_end = min(a.L, (kp + 1) * p.C);
+  uint32_t cs = kp * p.C + wave;
+  Meta m;
+  if (cs < cs_end) m = load_meta(a, rb * a.L + cs, lane);
+  load_tables(a.lut);
+  __syncthreads();
+
   float acc[B];
 #pragma unroll
   for (int b = 0; b < B; ++b) acc[b] = 0.f;
 
-  for (uint32_t cs = kp * p.C + wave; cs < cs_end; cs += waves) {
-    const uint32_t g = rb * a.L + cs;
-    const uint64_t first = (uint64_t)r0 * a.L + (uint64_t)cs * G;
-    uint32_t units;
-    const uint32_t nb = issue_group<B, XBF16>(p, w, g, lane, G, first, cs * S, &units);
-    uint32_t pos2 = lane_start(nb, lane, units);
-    wait_vm0();
+  for (; cs < cs_end; cs += waves) {
+    uint32_t pos2 = issue_stream(a, cols, m, lane);
+    issue_raw(a, raw_lds, m, lane);
+    issue_x<B, XBF16>(p, xs, cs * S, lane);
+    if (cs + waves < cs_end) {
+      m = load_meta(a, rb * a.L + cs + waves, lane);
+      wait_vm1();
+    } else {
+      wait_vm0();
+    }
     wave_sync_lds();
     if (lane < G) {
-      const uint2* rl = reinterpret_cast<const uint2*>(w.raw) + lane;
+      const uint2* rl = reinterpret_cast<const uint2*>(raw_lds) + lane;
       for (uint32_t t = 0; t < S; t += 8) {
         const uint2 rw = rl[(t >> 3) * G];
         uint32_t e[8];
-        decode4(w.st, w.st_off, pos2, e);
-        decode4(w.st, w.st_off, pos2, e + 4);
-        mac8<B, XBF16>(acc, e, rw, w.xs, S, t);
+        decode4(sc, sc_off, jmax, pos2, e);
+        decode4(sc, sc_off, jmax, pos2, e + 4);
+        mac8<B, XBF16>(acc, e, rw, xs, S, t);
       }
     }
     wait_lgkm0();
@@ -549,7 +573,7 @@ __global__ void __launch_bounds__(512) gemv_kernel(GemvArgs p) {
   for (int b = 0; b < B; ++b)
     __hip_atomic_store(p.partial + ((uint64_t)kp * B + b) * ldp + r0 + lane, s[b], __ATOMIC_RELAXED,
                        __HIP_MEMORY_SCOPE_AGENT);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  wait_vm0();
   uint32_t old = 0;
   if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   old = __shfl(old, 0, 64);
@@ -637,6 +661,10 @@ struct Plan {
   size_t lds;
 };
 
+// Rows of the stream columns: row 0 padding, the longest segment starting at
+// bit 31 of row 1, two rows of window overrun.
+static uint32_t col_rows_for(uint32_t max_seg_bits) { return 1 + ((31 + max_seg_bits + 31) >> 5) + 2; }
+
 static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, Plan* pl) {
   if (!t || !t->blob_dev || !t->lut_dev) return HL_EINVAL;
   if (t->rows >= (1ull << 31) || t->cols >= (1ull << 31) || t->n_grp >= (1ull << 31))
@@ -655,17 +683,13 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, Pl
   a.RB = (uint32_t)((t->rows + 63) / 64);
   a.stream_units = (uint32_t)std::min<uint64_t>((t->off_raw - t->off_stream) / 16, 0xFFFFFFFFu);
   a.max_units = t->max_grp_units;
-  // pad words + stream + guard for reads past a damaged segment (<= 2*lmax bits per weight)
-  const uint32_t guard = (t->seg_len * 2 * 15 + 64) / 32 + 4;
-  uint32_t ww = kPadWords + t->max_grp_units * 4 + guard;
-  ww = (ww + 3) & ~3u;
-  extra_words_per_wave = (extra_words_per_wave + 3) & ~3u;
-  a.wave_words = ww;
-  // LDS: the static tables plus, per wave, the stream region and the extras.
+  a.col_rows = col_rows_for(t->max_seg_bits);
+  const uint32_t per_wave = a.col_rows * kCol + 16 * t->seg_len + extra_words_per_wave;
+  // LDS: the static tables plus one region per wave.
   const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
   uint32_t waves = kMaxWaves;
-  while (waves > 1 && tab + (size_t)waves * (ww + extra_words_per_wave) * 4 > kMaxLds) --waves;
-  const size_t lds = (size_t)waves * (ww + extra_words_per_wave) * 4;
+  while (waves > 1 && tab + (size_t)waves * per_wave * 4 > kMaxLds) --waves;
+  const size_t lds = (size_t)waves * per_wave * 4;
   if (tab + lds > kMaxLds) return HL_EUNSUPPORTED;
   pl->waves = waves;
   pl->lds = lds;
@@ -722,12 +746,13 @@ static hl_status launch_bf16_b(bool xbf16, dim3 grid, dim3 block, hipStream_t s,
 
 using namespace hl;
 
-extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* header_host, size_t blob_bytes,
+extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* blob_host, size_t blob_bytes,
                                     uint32_t* lut_dev, hl_tensor* out) {
-  if (!blob_dev || !header_host || !lut_dev || !out || blob_bytes < HL_HEADER_BYTES) return HL_EINVAL;
+  if (!blob_dev || !blob_host || !lut_dev || !out || blob_bytes < HL_HEADER_BYTES) return HL_EINVAL;
   Header H;
-  if (!parse_header(reinterpret_cast<const uint8_t*>(header_host), &H) || !header_consistent(H, blob_bytes))
-    return HL_ECORRUPT;
+  uint32_t mseg = 0;
+  const hl_status v = validate_blob(reinterpret_cast<const uint8_t*>(blob_host), blob_bytes, &H, &mseg);
+  if (v != HL_OK) return v;
   hl_tensor t;
   std::memset(&t, 0, sizeof(t));
   t.blob_dev = reinterpret_cast<const uint8_t*>(blob_dev);
@@ -744,6 +769,7 @@ extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* header_hos
   t.seg_len = H.seg_len;
   t.lmax = H.cb.lmax;
   t.max_grp_units = H.max_grp_units;
+  t.max_seg_bits = mseg;
   t.cb = H.cb;
   *out = t;
   return HL_OK;
@@ -787,7 +813,7 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   const bool xb = x_dtype == HL_BF16;
   const uint32_t x_words = t ? (xb ? t->seg_len * batch / 2 : t->seg_len * batch) : 0;
   Plan pl;
-  hl_status st = make_plan(t, 16 * (t ? t->seg_len : 0) + x_words, &pl);
+  hl_status st = make_plan(t, x_words, &pl);
   if (st != HL_OK) return st;
   GemvArgs p;
   std::memset(&p, 0, sizeof(p));

@@ -48,7 +48,7 @@ class TensorView(ctypes.Structure):
                 ("off_seg_bits", ctypes.c_uint64), ("off_grp_off", ctypes.c_uint64),
                 ("off_stream", ctypes.c_uint64), ("off_raw", ctypes.c_uint64),
                 ("seg_len", ctypes.c_uint32), ("lmax", ctypes.c_uint32),
-                ("max_grp_units", ctypes.c_uint32), ("reserved", ctypes.c_uint32),
+                ("max_grp_units", ctypes.c_uint32), ("max_seg_bits", ctypes.c_uint32),
                 ("cb", Codebook)]
 
 
@@ -155,8 +155,7 @@ class DeviceTensor:
         self.blob = torch.from_numpy(blob).to(device)
         self.lut = torch.empty(LUT_BYTES // 4, dtype=torch.int32, device=device)
         self.view = TensorView()
-        hdr = np.ascontiguousarray(blob[:HEADER_BYTES])
-        _check(lib().hl_tensor_view(ctypes.c_void_p(self.blob.data_ptr()), hdr.ctypes.data, blob.size,
+        _check(lib().hl_tensor_view(ctypes.c_void_p(self.blob.data_ptr()), blob.ctypes.data, blob.size,
                                     ctypes.c_void_p(self.lut.data_ptr()), ctypes.byref(self.view)),
                "hl_tensor_view")
         _check(lib().hl_tensor_prepare(ctypes.byref(self.view), _stream_ptr(stream)), "hl_tensor_prepare")
