@@ -34,7 +34,7 @@ constexpr int kLutN = 1 << kLutBits;   // joint window table entries
 constexpr int kAuxWords = 64;          // canonical tables for the long-code path
 constexpr int kAuxField = 24;          // words per field in the aux table
 constexpr uint32_t kEsc = 0x40u;       // entry of a pair longer than the window
-constexpr int kMaxWaves = 8;
+constexpr int kMaxWaves = 16;
 constexpr uint32_t kCol = 64;          // row stride of the stream columns, in words
 
 static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
@@ -368,7 +368,7 @@ __device__ inline void issue_raw(const GroupArgs& a, uint32_t* raw_lds, const Me
 
 // Decode to bf16. Waves take groups in turn; region per wave: stream columns
 // then the raw plane.
-__global__ void __launch_bounds__(512) decode_kernel(GroupArgs a, uint16_t* out) {
+__global__ void __launch_bounds__(1024) decode_kernel(GroupArgs a, uint16_t* out) {
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t waves = blockDim.x >> 6;
   const uint32_t per_wave = a.col_rows * kCol + 16 * a.S;
@@ -492,7 +492,7 @@ __device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint3
 // column segments of [kp*C, min(L, (kp+1)*C)) in turn. Region per wave:
 // stream columns, raw plane, activation slice.
 template <int B, bool XBF16>
-__global__ void __launch_bounds__(512) gemv_kernel(GemvArgs p) {
+__global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
   const GroupArgs& a = p.g;
   const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const uint32_t waves = blockDim.x >> 6;
@@ -595,7 +595,7 @@ __global__ void __launch_bounds__(512) gemv_kernel(GemvArgs p) {
 
 // One wave per row; lanes stride the row in 8-weight chunks; dot2 on pairs.
 template <int B, bool XBF16>
-__global__ void __launch_bounds__(512) gemv_bf16_kernel(const uint16_t* w, const void* x, float* y,
+__global__ void __launch_bounds__(1024) gemv_bf16_kernel(const uint16_t* w, const void* x, float* y,
                                                         uint32_t rows, uint32_t cols) {
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t waves = blockDim.x >> 6;
