@@ -75,9 +75,9 @@ def cpu_oracle_baseline(blob: bytes, W, x, seconds: float):
     n_w, t_start = 0, time.perf_counter()
     groups = 0
     for g in order:
-        r0, G, cs, wdec = codec.decode_group(blob, int(g))
+        r0, G, c0, GC, wdec = codec.decode_group(blob, int(g))
         S = h["seg_len"]
-        xs = x[:, cs * S:(cs + 1) * S]
+        xs = x[:, c0 * S:(c0 + GC) * S]
         ogemv.gemv_rows(wdec, xs)
         n_w += wdec.size
         groups += 1
@@ -86,7 +86,7 @@ def cpu_oracle_baseline(blob: bytes, W, x, seconds: float):
     dt = time.perf_counter() - t_start
     rate = n_w / dt
     return dict(value=round(2 * rate / 1e9, 6), unit="GB/s", cores=1, kind="oracle",
-                sample=f"{groups} random 64x{h['seg_len']} groups ({n_w} weights) of the same matrix: "
+                sample=f"{groups} random groups of 64 segments x {h['seg_len']} weights ({n_w} weights) of the same matrix: "
                        f"bit-serial decode + fp64 products, {dt:.1f} s, single-threaded Python")
 
 

@@ -28,16 +28,19 @@
  * Sec. 3.2.2 assignment).
  *
  * Tiling: segment (r, cs) is W[r][cs*S .. cs*S+S) (S divides cols, S % 8 == 0,
- * 8 <= S <= 512, L = cols/S segments per row). Row block rb is rows
- * 64rb .. 64rb+G-1 (G = 64, or fewer in the last block). Group g = rb*L + cs
- * holds the G segments (64rb + lam, cs), lam = 0..G-1: 64 rows sharing one
- * column range, one row per lane of a 64-wide wavefront. Segments are
- * numbered in group order: group g starts at segment 64*L*rb + cs*G.
+ * 8 <= S <= 512, L = cols/S segments per row). A group is GR rows x GC
+ * consecutive column segments, GR*GC = 64 (GR = group_rows, a power of two,
+ * with GC dividing L): row block rb is rows GR*rb .. GR*rb+G-1 (G = GR, or
+ * fewer in the last block), column block cb is segments cb*GC .. cb*GC+GC-1,
+ * and group g = rb*(L/GC) + cb. Its N = G*GC segments are numbered
+ * mu = j*G + i for row offset i < G and segment offset j < GC; a 64-wide
+ * wavefront decodes one group, one segment per lane. Segments are numbered in
+ * group order: group g starts at segment GR*rb*L + cb*GC*G.
  *
  * Stream: for each weight of a segment in order, code(el) then code(eh),
  * each emitted most-significant bit first; the stream is packed least
  * significant bit first (bit k is bit k%8 of byte k/8). The segments of a
- * group are concatenated in lane order without gaps; each group stream starts on a 16-byte
+ * group are concatenated in mu order without gaps; each group stream starts on a 16-byte
  * boundary and is zero-padded to a multiple of 128 bits.
  *
  * Layout (sections start at 64-byte boundaries, zero padding between):
@@ -47,11 +50,11 @@
  *                                          units from off_stream
  *   off_stream    group streams
  *   off_raw       uint8 raw[n]: (s<<7)|m; group g starts at S times its first
- *                 segment number; weight t of lane lam is at ((t/8)*G + lam)*8
+ *                 segment number; weight t of segment mu is at ((t/8)*N + mu)*8
  *                 + t%8 within the group
  *   total_bytes = off_raw + n
  * Header: u32 magic 0x31464C48 ('HLF1'), u16 version 1, u8 lmax, u8 flags 0,
- *   u64 rows, u64 cols, u32 seg_len, u32 group_rows (64), u64 n_seg,
+ *   u64 rows, u64 cols, u32 seg_len, u32 group_rows (GR), u64 n_seg,
  *   u64 n_grp, u64 off_seg_bits, u64 off_grp_off, u64 off_stream,
  *   u64 off_raw, u64 total_bytes, u32 max_grp_units, u8 eh_nsym, u8 el_nsym,
  *   u8 eh_single, u8 el_single, u8 eh_len[16], u8 el_len[16].
@@ -92,7 +95,7 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
 #define HL_MAGIC 0x31464C48u
 #define HL_VERSION 1u
 #define HL_HEADER_BYTES 128u
-#define HL_GROUP_ROWS 64u
+#define HL_GROUP_SEGS 64u
 #define HL_MAX_BATCH 16u
 #define HL_LUT_BYTES 33024u   /* 8192 joint entries + 64 words of tables */
 
@@ -114,7 +117,7 @@ typedef struct {
   uint32_t* lut_dev;         /* HL_LUT_BYTES, filled by hl_tensor_prepare */
   uint64_t rows, cols, n_seg, n_grp, total_bytes;
   uint64_t off_seg_bits, off_grp_off, off_stream, off_raw;
-  uint32_t seg_len, lmax, max_grp_units, max_seg_bits;
+  uint32_t seg_len, grp_rows, lmax, max_grp_units, max_seg_bits, reserved;
   hl_codebook cb;
 } hl_tensor;
 
@@ -133,16 +136,21 @@ uint32_t hl_default_seg_len(uint64_t cols);
 hl_status hl_build_codebook(const uint16_t* w_bf16, size_t n, uint32_t lmax,
                             hl_codebook* out);
 
+/* Group rows the encoder uses when asked for 0: 16 (16 rows x 4 segments)
+ * when 4 divides the segments per row, else 32, else 64. */
+uint32_t hl_default_grp_rows(uint64_t cols, uint32_t seg_len);
+
 /* Encode W [rows][cols] (bf16 bit patterns, host) into an HLF1 container
  * (Sec. 3.1: once, offline, on the CPU). seg_len 0 selects
- * hl_default_seg_len(cols). With out == NULL, *out_bytes receives the exact
- * size; otherwise *out_bytes is the capacity of `out` on entry and the size
- * written on return (HL_ENOMEM if too small). nthreads 0 = all cores; the
- * output does not depend on nthreads. Errors: HL_EINVAL (shape, seg_len, a
- * weight whose field has no code in `cb`). */
+ * hl_default_seg_len(cols); grp_rows 0 selects hl_default_grp_rows. With
+ * out == NULL, *out_bytes receives the exact size; otherwise *out_bytes is the
+ * capacity of `out` on entry and the size written on return (HL_ENOMEM if too
+ * small). nthreads 0 = all cores; the output does not depend on nthreads.
+ * Errors: HL_EINVAL (shape, seg_len, grp_rows, a weight whose field has no
+ * code in `cb`). */
 hl_status hl_encode(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,
-                    const hl_codebook* cb, uint32_t seg_len, uint32_t nthreads,
-                    void* out, size_t* out_bytes);
+                    const hl_codebook* cb, uint32_t seg_len, uint32_t grp_rows,
+                    uint32_t nthreads, void* out, size_t* out_bytes);
 
 /* Full structural check of a container held in host memory: header, section
  * offsets, codebooks (Kraft sum exactly 1, lengths <= lmax), per-group

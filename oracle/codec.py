@@ -25,15 +25,19 @@ most-significant bit first into a stream packed least-significant bit first;
 a one-symbol field gets code length 0; segments of S weights along a
 row are the unit of independent decoding.
 
-Tiling: segment (r, cs) holds W[r, cs*S : cs*S+S]; row block rb holds rows
-64rb .. 64rb+G-1 (G = 64 except maybe the last block); group g = rb*L + cs
-(L = cols/S) holds the G segments (64rb + lam, cs), lam = 0..G-1.
+Tiling: segment (r, cs) holds W[r, cs*S : cs*S+S] (L = cols/S segments per
+row). A group is GR rows x GC consecutive column segments (GR*GC = 64): row
+block rb holds rows GR*rb .. GR*rb+G-1 (G = GR except maybe in the last
+block), column block cb holds segments cb*GC .. cb*GC+GC-1, and group
+g = rb*(L/GC) + cb. Its G*GC segments are numbered mu = j*G + i for row
+offset i < G and segment offset j < GC.
 
 Container layout (little-endian; sections start at 64-byte boundaries):
   header (128 B), seg_bits u16[n_seg] in group order, grp_off u32[n_grp + 1]
-  (16-byte units), stream (one 16-byte aligned bit stream per group),
-  raw u8[n] (sign<<7 | mantissa; group g's bytes start at S times the number
-  of segments before it; weight t of lane lam at ((t // 8) * G + lam) * 8 + t % 8).
+  (16-byte units), stream (one 16-byte aligned bit stream per group, its
+  segments concatenated in mu order), raw u8[n] (sign<<7 | mantissa; group g's
+  bytes start at S times the number of segments before it; weight t of
+  segment mu at ((t // 8) * N + mu) * 8 + t % 8, N = G*GC).
 """
 from __future__ import annotations
 
@@ -48,7 +52,7 @@ import numpy as np
 MAGIC = 0x31464C48          # 'HLF1'
 VERSION = 1
 HEADER_BYTES = 128
-GROUP_ROWS = 64             # rows per group (one per lane of a 64-wide wavefront)
+GROUP_SEGS = 64             # segments per group (one per lane of a 64-wide wavefront)
 RAW_UNIT = 8                # bytes of one segment's raw plane stored contiguously
 UNIT_BYTES = 16             # group streams are padded to 128 bits
 SECTION_ALIGN = 64
@@ -258,46 +262,66 @@ def _align(x: int, a: int = SECTION_ALIGN) -> int:
     return (x + a - 1) // a * a
 
 
-def layout(rows: int, cols: int, seg_len: int) -> Dict[str, int]:
+def default_grp_rows(cols: int, seg_len: int) -> int:
+    """16 rows x 4 segments when the segments per row allow it, else 32 x 2, else 64 x 1."""
+    L = cols // seg_len
+    for gc in (4, 2, 1):
+        if L % gc == 0:
+            return GROUP_SEGS // gc
+    return GROUP_SEGS
+
+
+def layout(rows: int, cols: int, seg_len: int, grp_rows: int = GROUP_SEGS) -> Dict[str, int]:
     n = rows * cols
     n_seg = n // seg_len
     L = cols // seg_len
-    n_grp = (rows + GROUP_ROWS - 1) // GROUP_ROWS * L
+    GC = GROUP_SEGS // grp_rows
+    n_grp = (rows + grp_rows - 1) // grp_rows * (L // GC)
     off_seg_bits = HEADER_BYTES
     off_grp_off = _align(off_seg_bits + 2 * n_seg)
     off_stream = _align(off_grp_off + 4 * (n_grp + 1))
-    return dict(n=n, n_seg=n_seg, n_grp=n_grp, L=L, off_seg_bits=off_seg_bits,
+    return dict(n=n, n_seg=n_seg, n_grp=n_grp, L=L, GC=GC, off_seg_bits=off_seg_bits,
                 off_grp_off=off_grp_off, off_stream=off_stream)
 
 
-def group_geometry(rows: int, cols: int, seg_len: int, g: int) -> Tuple[int, int, int, int]:
-    """(first row, rows G, column segment cs, index of the group's first segment)."""
+def group_geometry(rows: int, cols: int, seg_len: int, g: int,
+                   grp_rows: int = GROUP_SEGS) -> Tuple[int, int, int, int, int]:
+    """(first row r0, rows G, first column segment, first segment number, GC) of group g.
+
+    Segment mu of the group is (r0 + mu % G, first column segment + mu // G)."""
     L = cols // seg_len
-    rb, cs = divmod(g, L)
-    r0 = rb * GROUP_ROWS
-    G = min(GROUP_ROWS, rows - r0)
-    return r0, G, cs, r0 * L + cs * G
+    GC = GROUP_SEGS // grp_rows
+    rb, cb = divmod(g, L // GC)
+    r0 = rb * grp_rows
+    G = min(grp_rows, rows - r0)
+    return r0, G, cb * GC, r0 * L + cb * GC * G, GC
 
 
-def check_shape(rows: int, cols: int, seg_len: int, lmax: int) -> None:
+def check_shape(rows: int, cols: int, seg_len: int, lmax: int, grp_rows: int = GROUP_SEGS) -> None:
     if rows < 1 or cols < 1:
         raise ValueError("empty matrix")
     if not (4 <= lmax <= 15):
         raise ValueError("lmax must be in [4, 15]")
     if seg_len < 8 or seg_len > 512 or seg_len % 8 or cols % seg_len:
         raise ValueError("segment length must be a multiple of 8 in [8, 512] dividing cols")
+    if grp_rows not in (1, 2, 4, 8, 16, 32, 64) or (cols // seg_len) % (GROUP_SEGS // grp_rows):
+        raise ValueError("group rows must be a power of two whose 64/GR divides the segments per row")
 
 
-def raw_pos(r: np.ndarray, c: np.ndarray, rows: int, cols: int, seg_len: int) -> np.ndarray:
+def raw_pos(r: np.ndarray, c: np.ndarray, rows: int, cols: int, seg_len: int,
+            grp_rows: int = GROUP_SEGS) -> np.ndarray:
     """Byte offset in the raw plane of weight (r, c)."""
     r = np.asarray(r, dtype=np.int64)
     c = np.asarray(c, dtype=np.int64)
     L = cols // seg_len
-    rb, lam = r // GROUP_ROWS, r % GROUP_ROWS
+    GC = GROUP_SEGS // grp_rows
+    rb, i = r // grp_rows, r % grp_rows
     cs, t = c // seg_len, c % seg_len
-    G = np.minimum(GROUP_ROWS, rows - rb * GROUP_ROWS)
-    first_seg = rb * GROUP_ROWS * L + cs * G
-    return first_seg * seg_len + ((t // RAW_UNIT) * G + lam) * RAW_UNIT + (t % RAW_UNIT)
+    cb, j = cs // GC, cs % GC
+    G = np.minimum(grp_rows, rows - rb * grp_rows)
+    mu = j * G + i
+    first_seg = rb * grp_rows * L + cb * GC * G
+    return first_seg * seg_len + ((t // RAW_UNIT) * (G * GC) + mu) * RAW_UNIT + (t % RAW_UNIT)
 
 
 def build_codebooks(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode]:
@@ -324,13 +348,14 @@ def segment_stream(eh_seg, el_seg, ceh: FieldCode, cel: FieldCode) -> Tuple[int,
 
 
 def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
-           codebooks: Tuple[FieldCode, FieldCode] = None) -> bytes:
+           codebooks: Tuple[FieldCode, FieldCode] = None, grp_rows: int = None) -> bytes:
     """Compress a bf16 matrix [rows, cols] (uint16 bit patterns) into HLF1 bytes."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     rows, cols = w.shape
-    check_shape(rows, cols, seg_len, lmax)
+    GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
+    check_shape(rows, cols, seg_len, lmax, GR)
     ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
-    lay = layout(rows, cols, seg_len)
+    lay = layout(rows, cols, seg_len, GR)
     n, n_seg, n_grp = lay["n"], lay["n_seg"], lay["n_grp"]
     s, eh, el, m = split_fields(w)                       # [rows, cols] each
     S = seg_len
@@ -341,13 +366,13 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     units_total = 0
     max_units = 0
     for g in range(n_grp):
-        r0, G, cs, first = group_geometry(rows, cols, S, g)
+        r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
         gacc, gpos = 0, 0
-        for lam in range(G):
-            r = r0 + lam
-            a, b = cs * S, cs * S + S
-            acc, nb = segment_stream(eh[r, a:b].tolist(), el[r, a:b].tolist(), ceh, cel)
-            seg_bits[first + lam] = nb
+        for mu in range(G * GC):
+            r = r0 + mu % G
+            a = (c0 + mu // G) * S
+            acc, nb = segment_stream(eh[r, a:a + S].tolist(), el[r, a:a + S].tolist(), ceh, cel)
+            seg_bits[first + mu] = nb
             gacc |= acc << gpos
             gpos += nb
         units = (gpos + 127) // 128
@@ -362,10 +387,10 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     total = off_raw + n
     rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
     raw = np.zeros(n, dtype=np.uint8)
-    raw[raw_pos(rr.ravel(), cc.ravel(), rows, cols, S)] = raw_byte(s, m).ravel()
+    raw[raw_pos(rr.ravel(), cc.ravel(), rows, cols, S, GR)] = raw_byte(s, m).ravel()
 
     out = bytearray(total)
-    out[0:HEADER_BYTES] = pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, lay["off_seg_bits"],
+    out[0:HEADER_BYTES] = pack_header(rows, cols, seg_len, lmax, GR, n_seg, n_grp, lay["off_seg_bits"],
                                       lay["off_grp_off"], lay["off_stream"], off_raw, total,
                                       max_units, ceh, cel)
     out[lay["off_seg_bits"]:lay["off_seg_bits"] + 2 * n_seg] = seg_bits.tobytes()
@@ -378,9 +403,9 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
 HEADER_FMT = "<IHBBQQIIQQQQQQQIBBBB16s16s"
 
 
-def pack_header(rows, cols, seg_len, lmax, n_seg, n_grp, off_sb, off_go, off_st, off_raw, total,
+def pack_header(rows, cols, seg_len, lmax, grp_rows, n_seg, n_grp, off_sb, off_go, off_st, off_raw, total,
                 max_units, ceh: FieldCode, cel: FieldCode) -> bytes:
-    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, 0, rows, cols, seg_len, GROUP_ROWS,
+    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, 0, rows, cols, seg_len, grp_rows,
                     n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units,
                     ceh.nsym, cel.nsym, ceh.single, cel.single,
                     bytes(ceh.lengths), bytes(cel.lengths))
@@ -406,48 +431,48 @@ def header_codebooks(h) -> Tuple[FieldCode, FieldCode]:
             FieldCode(h["el_len"], h["el_nsym"], h["el_single"]))
 
 
-def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, np.ndarray]:
-    """Bit-serial decode of one group; returns (first row, G, cs, uint16[G, S])."""
+def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
+    """Bit-serial decode of one group.
+
+    Returns (first row r0, rows G, first column segment, GC, uint16[G, GC*S])."""
     h = parse_header(blob)
     ceh, cel = header_codebooks(h)
-    rows, cols, S = h["rows"], h["cols"], h["seg_len"]
+    rows, cols, S, GR = h["rows"], h["cols"], h["seg_len"], h["grp_rows"]
     seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
     grp_off = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
     raw_plane = np.frombuffer(blob, np.uint8, rows * cols, h["off_raw"])
-    r0, G, cs, first = group_geometry(rows, cols, S, g)
+    r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
     a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
     b = h["off_stream"] + int(grp_off[g + 1]) * UNIT_BYTES
     bits = np.unpackbits(np.frombuffer(blob[a:b], np.uint8), bitorder="little").tolist()
-    out = np.zeros((G, S), dtype=np.uint16)
+    out = np.zeros((G, GC * S), dtype=np.uint16)
     pos = 0
-    for lam in range(G):
+    for mu in range(G * GC):
+        i, j = mu % G, mu // G
         start = pos
         eh = np.zeros(S, np.uint32)
         el = np.zeros(S, np.uint32)
         for t in range(S):
             el[t], pos = cel.decode_one(bits, pos)
             eh[t], pos = ceh.decode_one(bits, pos)
-        if pos - start != int(seg_bits[first + lam]):
+        if pos - start != int(seg_bits[first + mu]):
             raise ValueError("segment length mismatch")
-        rp = raw_pos(np.full(S, r0 + lam), cs * S + np.arange(S), rows, cols, S)
+        cols_of = (c0 + j) * S + np.arange(S)
+        rp = raw_pos(np.full(S, r0 + i), cols_of, rows, cols, S, GR)
         r = raw_plane[rp].astype(np.uint32)
-        out[lam] = join_fields(r >> 7, eh, el, r & 0x7F)
-    return r0, G, cs, out
-
-
-def decode_rows(blob: bytes, row_block: int) -> np.ndarray:
-    """Decode the 64-row block ``row_block`` (all column segments)."""
-    h = parse_header(blob)
-    S, L = h["seg_len"], h["cols"] // h["seg_len"]
-    parts = [decode_group(blob, row_block * L + cs)[3] for cs in range(L)]
-    return np.concatenate(parts, axis=1)
+        out[i, j * S:(j + 1) * S] = join_fields(r >> 7, eh, el, r & 0x7F)
+    return r0, G, c0, GC, out
 
 
 def decode(blob: bytes) -> np.ndarray:
     """Decompress a whole HLF1 container back to the bf16 matrix (uint16)."""
     h = parse_header(blob)
-    rb_count = (h["rows"] + GROUP_ROWS - 1) // GROUP_ROWS
-    return np.concatenate([decode_rows(blob, rb) for rb in range(rb_count)], axis=0)
+    w = np.zeros((h["rows"], h["cols"]), dtype=np.uint16)
+    S = h["seg_len"]
+    for g in range(h["n_grp"]):
+        r0, G, c0, GC, part = decode_group(blob, g)
+        w[r0:r0 + G, c0 * S:(c0 + GC) * S] = part
+    return w
 
 
 def payload_bits(w: np.ndarray, ceh: FieldCode, cel: FieldCode) -> int:
@@ -460,27 +485,30 @@ def payload_bits(w: np.ndarray, ceh: FieldCode, cel: FieldCode) -> int:
 
 
 def container_size(w: np.ndarray, seg_len: int, lmax: int = 12,
-                   codebooks: Tuple[FieldCode, FieldCode] = None) -> Dict[str, int]:
-    """Exact container size of ``encode(w, seg_len, lmax)`` from the code lengths
-    alone (sum of code lengths per segment, 128-bit padding per group, section
-    alignment), without building the stream."""
+                   codebooks: Tuple[FieldCode, FieldCode] = None, grp_rows: int = None) -> Dict[str, int]:
+    """Exact container size of ``encode(w, seg_len, lmax, grp_rows=...)`` from the
+    code lengths alone (sum of code lengths per segment, 128-bit padding per
+    group, section alignment), without building the stream."""
     w = np.asarray(w, dtype=np.uint16)
     rows, cols = w.shape
-    check_shape(rows, cols, seg_len, lmax)
+    GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
+    check_shape(rows, cols, seg_len, lmax, GR)
     ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
     _, eh, el, _ = split_fields(w)
     le = np.array(ceh.lengths if ceh.nsym > 1 else [0] * NSYM, dtype=np.int64)
     ll = np.array(cel.lengths if cel.nsym > 1 else [0] * NSYM, dtype=np.int64)
     L = cols // seg_len
+    GC = GROUP_SEGS // GR
     seg = (le[eh] + ll[el]).reshape(rows, L, seg_len).sum(axis=2)       # [rows, L]
     units = 0
     max_units = 0
-    for rb in range(0, rows, GROUP_ROWS):
-        per_cs = seg[rb:rb + GROUP_ROWS].sum(axis=0)                      # [L]
-        u = (per_cs + 127) // 128
+    for rb in range(0, rows, GR):
+        per_cs = seg[rb:rb + GR].sum(axis=0)                              # [L]
+        per_grp = per_cs.reshape(L // GC, GC).sum(axis=1)
+        u = (per_grp + 127) // 128
         units += int(u.sum())
         max_units = max(max_units, int(u.max()))
-    lay = layout(rows, cols, seg_len)
+    lay = layout(rows, cols, seg_len, GR)
     off_raw = _align(lay["off_stream"] + units * UNIT_BYTES)
     return dict(total_bytes=off_raw + rows * cols, stream_units=units, max_grp_units=max_units,
-                code_bits=int(seg.sum()), off_raw=off_raw)
+                code_bits=int(seg.sum()), off_raw=off_raw, grp_rows=GR)

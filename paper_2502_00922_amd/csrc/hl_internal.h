@@ -8,24 +8,28 @@ namespace hl {
 
 struct Layout {
   uint64_t n, n_seg, n_grp, L, off_seg_bits, off_grp_off, off_stream;
+  uint32_t GR, GC;
 };
 
-// Group g = rb*L + cs: rows r0 .. r0+G-1, column segment cs; `first` is the
+// Group g = rb*(L/GC) + cb: rows r0 .. r0+G-1 and column segments
+// c0 .. c0+GC-1; segment mu = j*G + i is (r0 + i, c0 + j); `first` is the
 // group-order number of its first segment.
 struct GroupGeom {
-  uint64_t r0, cs, first;
-  uint32_t G;
+  uint64_t r0, c0, first;
+  uint32_t G, GC;
 };
-GroupGeom group_geom(uint64_t rows, uint64_t L, uint64_t g);
+GroupGeom group_geom(uint64_t rows, uint64_t L, uint32_t GR, uint64_t g);
+bool grp_rows_ok(uint64_t cols, uint32_t S, uint32_t GR);
+uint32_t default_grp_rows(uint64_t cols, uint32_t S);
 
 struct Header {
   uint64_t rows, cols, n_seg, n_grp, off_seg_bits, off_grp_off, off_stream, off_raw, total_bytes;
-  uint32_t seg_len, max_grp_units;
+  uint32_t seg_len, grp_rows, max_grp_units;
   hl_codebook cb;
 };
 
 bool shape_ok(uint64_t rows, uint64_t cols, uint32_t S);
-Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S);
+Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR);
 bool parse_header(const uint8_t* h, Header* out);
 bool header_consistent(const Header& h, uint64_t blob_bytes);
 bool field_code_valid(const hl_field_code& fc, uint32_t lmax);

@@ -149,12 +149,25 @@ bool shape_ok(uint64_t rows, uint64_t cols, uint32_t S) {
          rows <= (1ull << 40) / cols;
 }
 
-Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S) {
+bool grp_rows_ok(uint64_t cols, uint32_t S, uint32_t GR) {
+  if (GR == 0 || GR > HL_GROUP_SEGS || (GR & (GR - 1))) return false;
+  return S && (cols / S) % (HL_GROUP_SEGS / GR) == 0;
+}
+
+uint32_t default_grp_rows(uint64_t cols, uint32_t S) {
+  for (uint32_t gc : {4u, 2u, 1u})
+    if (S && (cols / S) % gc == 0) return HL_GROUP_SEGS / gc;
+  return HL_GROUP_SEGS;
+}
+
+Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR) {
   Layout L;
   L.n = rows * cols;
   L.n_seg = L.n / S;
   L.L = cols / S;
-  L.n_grp = (rows + HL_GROUP_ROWS - 1) / HL_GROUP_ROWS * L.L;
+  L.GR = GR;
+  L.GC = HL_GROUP_SEGS / GR;
+  L.n_grp = (rows + GR - 1) / GR * (L.L / L.GC);
   L.off_seg_bits = HL_HEADER_BYTES;
   L.off_grp_off = align64(L.off_seg_bits + 2 * L.n_seg);
   L.off_stream = align64(L.off_grp_off + 4 * (L.n_grp + 1));
@@ -174,7 +187,7 @@ void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, const hl_
   put64(8, rows);
   put64(16, cols);
   put32(24, S);
-  put32(28, HL_GROUP_ROWS);
+  put32(28, L.GR);
   put64(32, L.n_seg);
   put64(40, L.n_grp);
   put64(48, L.off_seg_bits);
@@ -201,7 +214,7 @@ bool parse_header(const uint8_t* h, Header* o) {
   o->rows = get64(8);
   o->cols = get64(16);
   o->seg_len = get32(24);
-  if (get32(28) != HL_GROUP_ROWS) return false;
+  o->grp_rows = get32(28);
   o->n_seg = get64(32);
   o->n_grp = get64(40);
   o->off_seg_bits = get64(48);
@@ -222,8 +235,8 @@ bool parse_header(const uint8_t* h, Header* o) {
 // Consistency of a parsed header with the layout rules (no data access).
 bool header_consistent(const Header& H, uint64_t blob_bytes) {
   if (H.cb.lmax < 4 || H.cb.lmax > 15) return false;
-  if (!shape_ok(H.rows, H.cols, H.seg_len)) return false;
-  Layout L = make_layout(H.rows, H.cols, H.seg_len);
+  if (!shape_ok(H.rows, H.cols, H.seg_len) || !grp_rows_ok(H.cols, H.seg_len, H.grp_rows)) return false;
+  Layout L = make_layout(H.rows, H.cols, H.seg_len, H.grp_rows);
   if (H.n_seg != L.n_seg || H.n_grp != L.n_grp || H.off_seg_bits != L.off_seg_bits ||
       H.off_grp_off != L.off_grp_off || H.off_stream != L.off_stream)
     return false;
@@ -247,13 +260,15 @@ uint32_t default_seg_len(uint64_t cols) {
   return best;
 }
 
-GroupGeom group_geom(uint64_t rows, uint64_t L, uint64_t g) {
+GroupGeom group_geom(uint64_t rows, uint64_t L, uint32_t GR, uint64_t g) {
   GroupGeom q;
-  uint64_t rb = g / L;
-  q.cs = g % L;
-  q.r0 = rb * HL_GROUP_ROWS;
-  q.G = (uint32_t)std::min<uint64_t>(HL_GROUP_ROWS, rows - q.r0);
-  q.first = q.r0 * L + q.cs * q.G;
+  q.GC = HL_GROUP_SEGS / GR;
+  const uint64_t CB = L / q.GC;
+  const uint64_t rb = g / CB;
+  q.c0 = (g % CB) * q.GC;
+  q.r0 = rb * GR;
+  q.G = (uint32_t)std::min<uint64_t>(GR, rows - q.r0);
+  q.first = q.r0 * L + q.c0 * q.G;
   return q;
 }
 
@@ -318,11 +333,18 @@ extern "C" hl_status hl_build_codebook(const uint16_t* w, size_t n, uint32_t lma
   return HL_OK;
 }
 
+extern "C" uint32_t hl_default_grp_rows(uint64_t cols, uint32_t seg_len) {
+  return default_grp_rows(cols, seg_len ? seg_len : default_seg_len(cols));
+}
+
 extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook* cb,
-                               uint32_t seg_len, uint32_t nthreads, void* out, size_t* out_bytes) {
+                               uint32_t seg_len, uint32_t grp_rows, uint32_t nthreads, void* out,
+                               size_t* out_bytes) {
   if (!w || !cb || !out_bytes) return HL_EINVAL;
   uint32_t S = seg_len ? seg_len : default_seg_len(cols);
   if (!shape_ok(rows, cols, S)) return HL_EINVAL;
+  const uint32_t GR = grp_rows ? grp_rows : default_grp_rows(cols, S);
+  if (!grp_rows_ok(cols, S, GR)) return HL_EINVAL;
   if (cb->lmax < 4 || cb->lmax > 15 || !field_code_valid(cb->eh, cb->lmax) ||
       !field_code_valid(cb->el, cb->lmax))
     return HL_EINVAL;
@@ -347,7 +369,7 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
     plen[e] = (uint8_t)(leh[a] + lel[b]);
     pvalid[e] = veh[a] && vel[b];
   }
-  Layout L = make_layout(rows, cols, S);
+  Layout L = make_layout(rows, cols, S, GR);
   const unsigned nt = pick_threads(nthreads);
   // Pass 1: segment bit counts, in group order.
   std::vector<uint16_t> seg_bits(L.n_seg);
@@ -356,16 +378,16 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   parallel_for(L.n_grp, nt, [&](uint64_t a, uint64_t b) {
     bool anybad = false;
     for (uint64_t g = a; g < b; ++g) {
-      GroupGeom q = group_geom(rows, L.L, g);
-      for (uint32_t lam = 0; lam < q.G; ++lam) {
-        const uint16_t* p = w + (q.r0 + lam) * cols + q.cs * S;
+      GroupGeom q = group_geom(rows, L.L, GR, g);
+      for (uint32_t mu = 0; mu < q.G * q.GC; ++mu) {
+        const uint16_t* p = w + (q.r0 + mu % q.G) * cols + (q.c0 + mu / q.G) * S;
         uint32_t bits = 0;
         for (uint32_t t = 0; t < S; ++t) {
           uint32_t e = (p[t] >> 7) & 0xFF;
           anybad |= !pvalid[e];
           bits += plen[e];
         }
-        seg_bits[q.first + lam] = (uint16_t)bits;
+        seg_bits[q.first + mu] = (uint16_t)bits;
       }
     }
     if (anybad) bad[a / per1] = 1;
@@ -377,9 +399,9 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   uint64_t units = 0;
   uint32_t max_units = 0;
   for (uint64_t g = 0; g < L.n_grp; ++g) {
-    GroupGeom q = group_geom(rows, L.L, g);
+    GroupGeom q = group_geom(rows, L.L, GR, g);
     uint64_t bits = 0;
-    for (uint32_t lam = 0; lam < q.G; ++lam) bits += seg_bits[q.first + lam];
+    for (uint32_t mu = 0; mu < q.G * q.GC; ++mu) bits += seg_bits[q.first + mu];
     uint64_t u = (bits + 127) / 128;
     grp_off[g] = (uint32_t)units;
     units += u;
@@ -400,15 +422,16 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   // Pass 2: group streams and raw plane, independent per group.
   parallel_for(L.n_grp, nt, [&](uint64_t ga, uint64_t gb) {
     for (uint64_t g = ga; g < gb; ++g) {
-      GroupGeom q = group_geom(rows, L.L, g);
+      GroupGeom q = group_geom(rows, L.L, GR, g);
       uint32_t* dst = (uint32_t*)(o + L.off_stream + (uint64_t)grp_off[g] * 16);
       const uint64_t nwords = (uint64_t)(grp_off[g + 1] - grp_off[g]) * 4;
       uint64_t acc = 0;
       int nb = 0;
       uint64_t wi = 0;
       uint8_t* rdst = o + off_raw + q.first * S;
-      for (uint32_t lam = 0; lam < q.G; ++lam) {
-        const uint16_t* p = w + (q.r0 + lam) * cols + q.cs * S;
+      const uint32_t NG = q.G * q.GC;
+      for (uint32_t mu = 0; mu < NG; ++mu) {
+        const uint16_t* p = w + (q.r0 + mu % q.G) * cols + (q.c0 + mu / q.G) * S;
         for (uint32_t t = 0; t < S; ++t) {
           uint32_t v = p[t];
           uint32_t e = (v >> 7) & 0xFF;
@@ -419,8 +442,8 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
             acc >>= 32;
             nb -= 32;
           }
-          // raw plane: ((t/8)*G + lam)*8 + t%8 within the group
-          rdst[((t >> 3) * q.G + lam) * 8 + (t & 7)] = (uint8_t)(((v >> 8) & 0x80) | (v & 0x7F));
+          // raw plane: ((t/8)*NG + mu)*8 + t%8 within the group
+          rdst[((t >> 3) * NG + mu) * 8 + (t & 7)] = (uint8_t)(((v >> 8) & 0x80) | (v & 0x7F));
         }
       }
       while (wi < nwords) {  // tail bits, then zero padding to 128 bits
@@ -446,10 +469,10 @@ hl_status validate_blob(const uint8_t* b, size_t bytes, Header* out, uint32_t* m
   const uint64_t max_seg = (uint64_t)H.seg_len * 2 * H.cb.lmax;
   const uint64_t L = H.cols / H.seg_len;
   for (uint64_t g = 0; g < H.n_grp; ++g) {
-    GroupGeom q = group_geom(H.rows, L, g);
+    GroupGeom q = group_geom(H.rows, L, H.grp_rows, g);
     uint64_t bits = 0;
-    for (uint32_t lam = 0; lam < q.G; ++lam) {
-      const uint32_t v = sb[q.first + lam];
+    for (uint32_t mu = 0; mu < q.G * q.GC; ++mu) {
+      const uint32_t v = sb[q.first + mu];
       if (v > max_seg) return HL_ECORRUPT;
       bits += v;
       mseg = std::max(mseg, v);

@@ -12,13 +12,15 @@
 // they are multiplied (Sec. 1, Sec. 3.2): the fused kernel never writes them.
 //
 // Work mapping (container tiling in include/hufflm.h): one wavefront decodes
-// one group = 64 rows x one S-column segment, lane lam owning row 64rb+lam.
+// one group = G rows x GC column segments (G*GC <= 64), lane mu owning the
+// segment of row r0 + mu % G and column segment c0 + mu / G.
 // Per group a wave copies, straight from HBM into its LDS region:
 //   * each lane's part of the group stream into a column of words (word j of
 //     lane lam at row j, column lam), so that window reads never share an
 //     LDS bank between lanes;
 //   * the raw sign/mantissa plane ([t/8][lane] in 8-byte units);
-//   * the activation slice x[b][c0 .. c0+S), which every lane reads alike.
+//   * the activation slice x[b][c0*S .. (c0+GC)*S), which lanes of the same
+//     column segment read alike.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -294,25 +296,26 @@ struct GroupArgs {
   const uint4* stream;
   const uint8_t* raw;
   const uint32_t* lut;   // global copy: kLutN entries + aux
-  uint32_t rows, cols, S, L, RB, stream_units, max_units;
+  uint32_t rows, cols, S, L, GR, GC, CB, RB, stream_units, max_units;
   uint32_t col_rows;     // rows of the stream columns (row 0 = padding)
 };
 
 // Group geometry and its metadata (segment length of the lane, stream units).
 struct Meta {
   uint64_t first;  // group-order number of the group's first segment
-  uint32_t r0, G, cs, nb, u0, units;
+  uint32_t r0, G, N, c0, nb, u0, units;
 };
 
-// Issues the metadata loads of group g (vector loads, counted by vmcnt).
+// Group g's geometry, and its metadata loads (vector loads, counted by vmcnt).
 __device__ inline Meta load_meta(const GroupArgs& a, uint32_t g, uint32_t lane) {
   Meta m;
-  const uint32_t rb = g / a.L;
-  m.cs = g - rb * a.L;
-  m.r0 = rb * 64;
-  m.G = min(64u, a.rows - m.r0);
-  m.first = (uint64_t)m.r0 * a.L + (uint64_t)m.cs * m.G;
-  m.nb = lane < m.G ? (uint32_t)a.seg_bits[m.first + lane] : 0u;
+  const uint32_t rb = g / a.CB;
+  m.c0 = (g - rb * a.CB) * a.GC;
+  m.r0 = rb * a.GR;
+  m.G = min(a.GR, a.rows - m.r0);
+  m.N = m.G * a.GC;
+  m.first = (uint64_t)m.r0 * a.L + (uint64_t)m.c0 * m.G;
+  m.nb = lane < m.N ? (uint32_t)a.seg_bits[m.first + lane] : 0u;
   m.u0 = a.grp_off[g + (lane & 1)];  // lane 0: start, lane 1: end
   m.units = 0;
   return m;
@@ -349,9 +352,9 @@ __device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta
   return 30u + bit0;
 }
 
-// Copies the group's raw plane (G*S bytes) into `raw_lds`.
+// Copies the group's raw plane (N*S bytes) into `raw_lds`.
 __device__ inline void issue_raw(const GroupArgs& a, uint32_t* raw_lds, const Meta& m, uint32_t lane) {
-  const uint32_t bytes = m.G * a.S;
+  const uint32_t bytes = m.N * a.S;
   const uint8_t* src = a.raw + m.first * a.S;
   if ((a.S & 15) == 0) {
     const uint32_t n = bytes / 16;
@@ -377,7 +380,7 @@ __global__ void __launch_bounds__(1024) decode_kernel(GroupArgs a, uint16_t* out
   const uint32_t sc_off = wave * per_wave + lane;
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t jmax = a.col_rows - 3;
-  const uint32_t n_grp = a.RB * a.L;
+  const uint32_t n_grp = a.RB * a.CB;
   const uint32_t stride = gridDim.x * waves;
   uint32_t g = blockIdx.x * waves + wave;
   Meta m;
@@ -395,11 +398,12 @@ __global__ void __launch_bounds__(1024) decode_kernel(GroupArgs a, uint16_t* out
       wait_vm0();
     }
     wave_sync_lds();
-    if (lane < cur.G) {
+    if (lane < cur.N) {
       const uint2* rl = reinterpret_cast<const uint2*>(raw_lds) + lane;
-      uint16_t* o = out + (uint64_t)(cur.r0 + lane) * a.cols + (uint64_t)cur.cs * a.S;
+      const uint32_t i = lane % cur.G, j = lane / cur.G;
+      uint16_t* o = out + (uint64_t)(cur.r0 + i) * a.cols + (uint64_t)(cur.c0 + j) * a.S;
       for (uint32_t t = 0; t < a.S; t += 8) {
-        const uint2 rw = rl[(t >> 3) * cur.G];
+        const uint2 rw = rl[(t >> 3) * cur.N];
         uint32_t e[8];
         decode4(sc, sc_off, jmax, pos2, e);
         decode4(sc, sc_off, jmax, pos2, e + 4);
@@ -429,13 +433,13 @@ struct GemvArgs {
   uint32_t x_words;   // LDS words of one wave's activation slice
 };
 
-// Copies x[b][c0 .. c0+S) for every batch row into xs ([batch][S]).
+// Copies x[b][c0*S .. (c0+GC)*S) for every batch row into xs ([batch][GC*S]).
 template <int B, bool XBF16>
 __device__ inline void issue_x(const GemvArgs& p, uint32_t* xs, uint32_t c0, uint32_t lane) {
   constexpr uint32_t kXPer = XBF16 ? 8 : 4;  // activations per 16 bytes
-  const uint32_t per_row = p.g.S / kXPer, total = per_row * B;
+  const uint32_t per_row = p.g.GC * p.g.S / kXPer, total = per_row * B;
   const uint4* xsrc = reinterpret_cast<const uint4*>(p.x);
-  const uint32_t row_u4 = p.g.cols / kXPer, c0_u4 = c0 / kXPer;
+  const uint32_t row_u4 = p.g.cols / kXPer, c0_u4 = c0 * p.g.S / kXPer;
   for (uint32_t k0 = 0; k0 < total; k0 += 64) {
     const uint32_t k = k0 + lane;
     if (k < total) {
@@ -446,9 +450,10 @@ __device__ inline void issue_x(const GemvArgs& p, uint32_t* xs, uint32_t c0, uin
 }
 
 // Multiply-accumulate of 8 decoded weights (entries e, raw dword pair rw)
-// with the activations at column offset t of the staged slice.
+// with the activations x[b][t .. t+8) of the lane's slice; xs points at the
+// lane's segment in batch row 0, ldx is the slice's row length.
 template <int B, bool XBF16>
-__device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint32_t* xs, uint32_t S,
+__device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint32_t* xs, uint32_t ldx,
                             uint32_t t) {
   if constexpr (XBF16) {
     const uint32_t w0 = pack_pair(rw.x, 0, e[0], e[1]);
@@ -457,7 +462,7 @@ __device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint3
     const uint32_t w3 = pack_pair(rw.y, 2, e[6], e[7]);
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-      const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * (S / 2) + t / 2);
+      const uint4 xv = *reinterpret_cast<const uint4*>(xs + b * (ldx / 2) + t / 2);
       float s = acc[b];
       s = dot2(w0, xv.x, s);
       s = dot2(w1, xv.y, s);
@@ -471,7 +476,7 @@ __device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint3
     for (int k = 0; k < 8; ++k) wf[k] = weight_f32(k < 4 ? rw.x : rw.y, k, e[k]);
 #pragma unroll
     for (int b = 0; b < B; ++b) {
-      const float* xf = reinterpret_cast<const float*>(xs) + b * S + t;
+      const float* xf = reinterpret_cast<const float*>(xs) + b * ldx + t;
       const float4 x0 = *reinterpret_cast<const float4*>(xf);
       const float4 x1 = *reinterpret_cast<const float4*>(xf + 4);
       float s = acc[b];
@@ -489,7 +494,7 @@ __device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint3
 }
 
 // Fused decode-GEMV. Block = (row block rb, k-part kp); its waves take the
-// column segments of [kp*C, min(L, (kp+1)*C)) in turn. Region per wave:
+// column blocks of [kp*C, min(CB, (kp+1)*C)) in turn. Region per wave:
 // stream columns, raw plane, activation slice.
 template <int B, bool XBF16>
 __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
@@ -506,12 +511,15 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
   const uint32_t jmax = a.col_rows - 3;
 
   const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
-  const uint32_t r0 = rb * 64;
-  const uint32_t G = min(64u, a.rows - r0);
-  const uint32_t cs_end = min(a.L, (kp + 1) * p.C);
-  uint32_t cs = kp * p.C + wave;
+  const uint32_t r0 = rb * a.GR;
+  const uint32_t G = min(a.GR, a.rows - r0);
+  const uint32_t N = G * a.GC;
+  const uint32_t ldx = a.GC * S;  // slice row length
+  const uint32_t* xl = xs + (XBF16 ? (lane / G) * (S / 2) : (lane / G) * S);
+  const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
+  uint32_t cb = kp * p.C + wave;
   Meta m;
-  if (cs < cs_end) m = load_meta(a, rb * a.L + cs, lane);
+  if (cb < cb_end) m = load_meta(a, rb * a.CB + cb, lane);
   load_tables(a.lut);
   __syncthreads();
 
@@ -519,42 +527,53 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
 #pragma unroll
   for (int b = 0; b < B; ++b) acc[b] = 0.f;
 
-  for (; cs < cs_end; cs += waves) {
+  for (; cb < cb_end; cb += waves) {
     uint32_t pos2 = issue_stream(a, cols, m, lane);
     issue_raw(a, raw_lds, m, lane);
-    issue_x<B, XBF16>(p, xs, cs * S, lane);
-    if (cs + waves < cs_end) {
-      m = load_meta(a, rb * a.L + cs + waves, lane);
+    issue_x<B, XBF16>(p, xs, m.c0, lane);
+    if (cb + waves < cb_end) {
+      m = load_meta(a, rb * a.CB + cb + waves, lane);
       wait_vm1();
     } else {
       wait_vm0();
     }
     wave_sync_lds();
-    if (lane < G) {
+    if (lane < N) {
       const uint2* rl = reinterpret_cast<const uint2*>(raw_lds) + lane;
       for (uint32_t t = 0; t < S; t += 8) {
-        const uint2 rw = rl[(t >> 3) * G];
+        const uint2 rw = rl[(t >> 3) * N];
         uint32_t e[8];
         decode4(sc, sc_off, jmax, pos2, e);
         decode4(sc, sc_off, jmax, pos2, e + 4);
-        mac8<B, XBF16>(acc, e, rw, xs, S, t);
+        mac8<B, XBF16>(acc, e, rw, xl, ldx, t);
       }
     }
     wait_lgkm0();
     wave_sync_lds();
   }
-  // Cross-wave reduction in a fixed order (the wave regions are free now).
+  // Reduction in a fixed order (the wave regions are free now): across waves
+  // per lane, then across the GC lanes of each row.
   __syncthreads();
   float* red = reinterpret_cast<float*>(s_dyn);
 #pragma unroll
   for (int b = 0; b < B; ++b) red[(wave * B + b) * 64 + lane] = acc[b];
   __syncthreads();
   if (wave != 0) return;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    float t = red[b * 64 + lane];
+    for (uint32_t v = 1; v < waves; ++v) t += red[(v * B + b) * 64 + lane];
+    red[b * 64 + lane] = t;
+  }
+  wait_lgkm0();
+  wave_sync_lds();
   float s[B];
 #pragma unroll
   for (int b = 0; b < B; ++b) {
-    s[b] = red[b * 64 + lane];
-    for (uint32_t v = 1; v < waves; ++v) s[b] += red[(v * B + b) * 64 + lane];
+    float t = 0.f;
+    if (lane < G)
+      for (uint32_t j = 0; j < a.GC; ++j) t += red[b * 64 + j * G + lane];
+    s[b] = t;
   }
   const uint32_t ldy = a.rows;
   if (p.KS == 1) {
@@ -568,11 +587,12 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
   // Partials are written and read with agent-scope atomics, which bypass the
   // per-XCD caches; once the stores are complete (vmcnt 0) the counter
   // increment orders them, so no cache write-back or invalidate is needed.
-  const uint32_t ldp = a.RB * 64;
+  const uint32_t ldp = a.RB * a.GR;
+  if (lane < G)
 #pragma unroll
-  for (int b = 0; b < B; ++b)
-    __hip_atomic_store(p.partial + ((uint64_t)kp * B + b) * ldp + r0 + lane, s[b], __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+    for (int b = 0; b < B; ++b)
+      __hip_atomic_store(p.partial + ((uint64_t)kp * B + b) * ldp + r0 + lane, s[b], __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   wait_vm0();
   uint32_t old = 0;
   if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -680,7 +700,10 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, Pl
   a.cols = (uint32_t)t->cols;
   a.S = t->seg_len;
   a.L = (uint32_t)(t->cols / t->seg_len);
-  a.RB = (uint32_t)((t->rows + 63) / 64);
+  a.GR = t->grp_rows;
+  a.GC = HL_GROUP_SEGS / t->grp_rows;
+  a.CB = a.L / a.GC;
+  a.RB = (uint32_t)((t->rows + a.GR - 1) / a.GR);
   a.stream_units = (uint32_t)std::min<uint64_t>((t->off_raw - t->off_stream) / 16, 0xFFFFFFFFu);
   a.max_units = t->max_grp_units;
   a.col_rows = col_rows_for(t->max_seg_bits);
@@ -767,6 +790,7 @@ extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
   t.off_stream = H.off_stream;
   t.off_raw = H.off_raw;
   t.seg_len = H.seg_len;
+  t.grp_rows = H.grp_rows;
   t.lmax = H.cb.lmax;
   t.max_grp_units = H.max_grp_units;
   t.max_seg_bits = mseg;
@@ -787,7 +811,7 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
   Plan pl;
   hl_status st = make_plan(t, 0, &pl);
   if (st != HL_OK) return st;
-  const uint32_t n_grp = pl.ga.RB * pl.ga.L;
+  const uint32_t n_grp = pl.ga.RB * pl.ga.CB;
   const uint32_t per_cu =
       std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)(pl.lds + (kLutN + kAuxWords) * 4)));
   const uint32_t blocks = std::min<uint32_t>((n_grp + pl.waves - 1) / pl.waves, device_cus() * per_cu);
@@ -795,23 +819,29 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
                 out_dev);
 }
 
-static uint32_t ks_cap(uint32_t L) { return std::min<uint32_t>(L, 64); }
+static uint32_t ks_cap(uint32_t CB) { return std::min<uint32_t>(CB, 64); }
 
 static uint64_t workspace_counter_bytes(uint32_t RB) { return ((uint64_t)RB * 4 + 255) & ~255ull; }
 
 extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
-  if (!t || t->seg_len == 0 || batch < 1 || batch > HL_MAX_BATCH) return 0;
-  const uint32_t RB = (uint32_t)((t->rows + 63) / 64);
-  const uint32_t L = (uint32_t)(t->cols / t->seg_len);
-  return workspace_counter_bytes(RB) + (uint64_t)ks_cap(L) * batch * RB * 64 * 4;
+  if (!t || t->seg_len == 0 || t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS || batch < 1 ||
+      batch > HL_MAX_BATCH)
+    return 0;
+  const uint32_t GR = t->grp_rows;
+  const uint32_t RB = (uint32_t)((t->rows + GR - 1) / GR);
+  const uint32_t CB = (uint32_t)(t->cols / t->seg_len) / (HL_GROUP_SEGS / GR);
+  return workspace_counter_bytes(RB) + (uint64_t)ks_cap(CB) * batch * RB * GR * 4;
 }
 
 extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
                                     float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
-  if (!x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || (x_dtype != HL_F32 && x_dtype != HL_BF16))
+  if (!t || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || (x_dtype != HL_F32 && x_dtype != HL_BF16))
     return HL_EINVAL;
+  if (t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS) return HL_EINVAL;
   const bool xb = x_dtype == HL_BF16;
-  const uint32_t x_words = t ? (xb ? t->seg_len * batch / 2 : t->seg_len * batch) : 0;
+  // activation slice of one group: GC*S columns per batch row
+  const uint32_t slice = (HL_GROUP_SEGS / t->grp_rows) * t->seg_len;
+  const uint32_t x_words = xb ? slice * batch / 2 : slice * batch;
   Plan pl;
   hl_status st = make_plan(t, x_words, &pl);
   if (st != HL_OK) return st;
@@ -821,21 +851,21 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   p.x = x_dev;
   p.y = y_dev;
   p.x_words = x_words;
-  // Column segments per block: enough blocks to fill the device, each wave
+  // Column blocks per block: enough blocks to fill the device, each wave
   // decoding at least one group; KS blocks share a row block.
-  const uint32_t L = pl.ga.L, RB = pl.ga.RB;
+  const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
   const uint64_t target_waves = (uint64_t)device_cus() * 16;
-  const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * L + target_waves - 1) / target_waves);
-  uint32_t C = std::min<uint32_t>(L, pl.waves * gpw);
-  uint32_t KS = (L + C - 1) / C;
-  if (KS > ks_cap(L)) {
-    KS = ks_cap(L);
-    C = (L + KS - 1) / KS;
-    KS = (L + C - 1) / C;
+  const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * CB + target_waves - 1) / target_waves);
+  uint32_t C = std::min<uint32_t>(CB, pl.waves * gpw);
+  uint32_t KS = (CB + C - 1) / C;
+  if (KS > ks_cap(CB)) {
+    KS = ks_cap(CB);
+    C = (CB + KS - 1) / KS;
+    KS = (CB + C - 1) / C;
   }
   if (KS > 1 && (!workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch))) {
     KS = 1;  // no room for partial sums: one block per row block
-    C = L;
+    C = CB;
   }
   p.C = C;
   p.KS = KS;
@@ -844,7 +874,7 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     p.partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
   }
   const dim3 grid(RB * KS), block(pl.waves * 64);
-  // the cross-wave reduction reuses the wave regions
+  // the reduction reuses the wave regions
   const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * batch * 64 * 4);
   HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
 }

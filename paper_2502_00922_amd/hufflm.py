@@ -47,14 +47,16 @@ class TensorView(ctypes.Structure):
                 ("n_grp", ctypes.c_uint64), ("total_bytes", ctypes.c_uint64),
                 ("off_seg_bits", ctypes.c_uint64), ("off_grp_off", ctypes.c_uint64),
                 ("off_stream", ctypes.c_uint64), ("off_raw", ctypes.c_uint64),
-                ("seg_len", ctypes.c_uint32), ("lmax", ctypes.c_uint32),
+                ("seg_len", ctypes.c_uint32), ("grp_rows", ctypes.c_uint32), ("lmax", ctypes.c_uint32),
                 ("max_grp_units", ctypes.c_uint32), ("max_seg_bits", ctypes.c_uint32),
+                ("reserved", ctypes.c_uint32),
                 ("cb", Codebook)]
 
 
 _lib = None
 
-EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_build_codebook", "hl_encode", "hl_validate",
+EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
+           "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
            "hl_decode_gemv", "hl_gemv_bf16"]
 
@@ -72,11 +74,13 @@ def lib() -> ctypes.CDLL:
     L.hl_status_str.argtypes = [c.c_int]
     L.hl_default_seg_len.restype = c.c_uint32
     L.hl_default_seg_len.argtypes = [c.c_uint64]
+    L.hl_default_grp_rows.restype = c.c_uint32
+    L.hl_default_grp_rows.argtypes = [c.c_uint64, c.c_uint32]
     L.hl_build_codebook.restype = c.c_int
     L.hl_build_codebook.argtypes = [c.c_void_p, c.c_size_t, c.c_uint32, c.POINTER(Codebook)]
     L.hl_encode.restype = c.c_int
     L.hl_encode.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook), c.c_uint32,
-                            c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
+                            c.c_uint32, c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
     L.hl_validate.restype = c.c_int
     L.hl_validate.argtypes = [c.c_void_p, c.c_size_t]
     L.hl_tensor_view.restype = c.c_int
@@ -117,8 +121,12 @@ def build_codebook(w: np.ndarray, lmax: int = 12) -> Codebook:
     return cb
 
 
+def default_grp_rows(cols: int, seg_len: int = 0) -> int:
+    return int(lib().hl_default_grp_rows(cols, seg_len))
+
+
 def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook: Optional[Codebook] = None,
-           nthreads: int = 0) -> np.ndarray:
+           nthreads: int = 0, grp_rows: int = 0) -> np.ndarray:
     """HLF1 container (uint8 array) of a bf16 matrix given as uint16 bits [rows, cols]."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     if w.ndim != 2:
@@ -126,10 +134,10 @@ def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook: Optional[C
     cb = codebook if codebook is not None else build_codebook(w, lmax)
     n = ctypes.c_size_t(0)
     L = lib()
-    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, nthreads, None,
-                       ctypes.byref(n)), "hl_encode(size)")
+    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,
+                       None, ctypes.byref(n)), "hl_encode(size)")
     out = np.empty(n.value, dtype=np.uint8)
-    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, nthreads,
+    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,
                        out.ctypes.data, ctypes.byref(n)), "hl_encode")
     return out
 

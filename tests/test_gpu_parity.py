@@ -37,26 +37,29 @@ def _decode(torch, dt):
     return out.cpu().numpy().view(np.uint16)
 
 
-SHAPES = [((64, 1024), 128), ((130, 48), 16), ((3, 64), 8), ((200, 512), 512), ((65, 96), 32),
-          ((1, 8), 8), ((127, 136), 136), ((300, 2048), 128), ((64, 256), 256)]
+# (shape, segment length, group rows; 0 = the encoder's default)
+SHAPES = [((64, 1024), 128, 0), ((130, 48), 16, 0), ((3, 64), 8, 0), ((200, 512), 512, 0), ((65, 96), 32, 0),
+          ((1, 8), 8, 0), ((127, 136), 136, 0), ((300, 2048), 128, 0), ((64, 256), 256, 0),
+          ((300, 2048), 64, 64), ((129, 1024), 64, 8), ((77, 512), 16, 32), ((19, 1024), 8, 1)]
 
 
-@pytest.mark.parametrize("shape,S", SHAPES)
-def test_decode_bit_exact(torch, shape, S):
-    print(f"decode {shape} S={S}", flush=True)
+@pytest.mark.parametrize("shape,S,GR", SHAPES)
+def test_decode_bit_exact(torch, shape, S, GR):
+    print(f"decode {shape} S={S} GR={GR}", flush=True)
     w = random_bf16(shape, seed=shape[0] * 7 + S)
-    blob = hl.encode(w, seg_len=S)
-    assert bytes(blob) == codec.encode(w, seg_len=S) if w.size <= 1 << 16 else True
+    blob = hl.encode(w, seg_len=S, grp_rows=GR)
+    if w.size <= 1 << 16:
+        assert bytes(blob) == codec.encode(w, seg_len=S, grp_rows=GR or None)
     dt = hl.DeviceTensor(blob)
     assert np.array_equal(_decode(torch, dt), w)
 
 
-@pytest.mark.parametrize("shape,S", SHAPES)
+@pytest.mark.parametrize("shape,S,GR", SHAPES)
 @pytest.mark.parametrize("xdt", ["f32", "bf16"])
-def test_gemv_vs_oracle(torch, shape, S, xdt):
-    print(f"gemv {shape} S={S} x={xdt}", flush=True)
+def test_gemv_vs_oracle(torch, shape, S, GR, xdt):
+    print(f"gemv {shape} S={S} GR={GR} x={xdt}", flush=True)
     w = random_bf16(shape, seed=shape[0] * 5 + S)
-    dt = hl.DeviceTensor(hl.encode(w, seg_len=S))
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=S, grp_rows=GR))
     for batch in (1, 3):
         x = random_x(batch, shape[1], seed=batch + S, dtype=xdt)
         y = dt.gemv(_to_dev_x(torch, x))

@@ -43,16 +43,17 @@ def test_codebook_equals_oracle(seed):
 
 
 CASES = [
-    ((64, 1024), 128, 12), ((130, 48), 16, 12), ((3, 64), 8, 12), ((200, 512), 512, 12),
-    ((65, 96), 32, 12), ((1, 8), 8, 12), ((127, 136), 136, 12), ((64, 1024), 256, 6),
+    ((64, 1024), 128, 12, 0), ((130, 48), 16, 12, 0), ((3, 64), 8, 12, 0), ((200, 512), 512, 12, 0),
+    ((65, 96), 32, 12, 0), ((1, 8), 8, 12, 0), ((127, 136), 136, 12, 0), ((64, 1024), 256, 6, 0),
+    ((130, 512), 64, 12, 64), ((130, 512), 64, 12, 8), ((37, 256), 32, 12, 32), ((21, 512), 8, 12, 1),
 ]
 
 
-@pytest.mark.parametrize("shape,S,lmax", CASES)
-def test_byte_identical_to_oracle(shape, S, lmax):
+@pytest.mark.parametrize("shape,S,lmax,GR", CASES)
+def test_byte_identical_to_oracle(shape, S, lmax, GR):
     w = random_bf16(shape, seed=sum(shape) + S)
-    a = bytes(hl.encode(w, seg_len=S, lmax=lmax))
-    b = codec.encode(w, seg_len=S, lmax=lmax)
+    a = bytes(hl.encode(w, seg_len=S, lmax=lmax, grp_rows=GR))
+    b = codec.encode(w, seg_len=S, lmax=lmax, grp_rows=GR or None)
     assert a == b
     assert hl.validate(a) == 0
 
@@ -80,6 +81,13 @@ def test_thread_count_does_not_change_output():
     a = hl.encode(w, seg_len=64, nthreads=1)
     for t in (2, 3, 7, 16):
         assert np.array_equal(a, hl.encode(w, seg_len=64, nthreads=t))
+
+
+def test_default_grp_rows():
+    for cols, S in ((4096, 128), (11008, 344), (48, 16), (80, 8), (1024, 64)):
+        assert hl.default_grp_rows(cols, S) == codec.default_grp_rows(cols, S)
+    with pytest.raises(hl.HLError):
+        hl.encode(random_bf16((4, 48), seed=1), seg_len=16, grp_rows=16)
 
 
 def test_default_seg_len():

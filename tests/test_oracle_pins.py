@@ -257,45 +257,59 @@ def _cam_window_decode(bits, pos, fc, lmax):
     raise AssertionError("no codeword matched")
 
 
-@pytest.mark.parametrize("shape,S", [((3, 64), 16), ((70, 128), 128), ((5, 96), 48), ((130, 40), 8)])
-def test_roundtrip_and_window_match_decoder(shape, S):
-    w = random_bf16(shape, seed=S)
-    blob = codec.encode(w, seg_len=S)
+@pytest.mark.parametrize("shape,S,GR", [((3, 64), 16, 64), ((70, 128), 128, 64), ((5, 96), 48, 32),
+                                        ((130, 40), 8, 64), ((37, 256), 32, 16), ((20, 128), 16, 8)])
+def test_roundtrip_and_window_match_decoder(shape, S, GR):
+    w = random_bf16(shape, seed=S + GR)
+    blob = codec.encode(w, seg_len=S, grp_rows=GR)
     assert (codec.decode(blob) == w).all()
     h = codec.parse_header(blob)
+    assert h["grp_rows"] == GR
     ceh, cel = codec.header_codebooks(h)
     seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
     grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
     _, eh, el, _ = codec.split_fields(w)
     # independent window-match decode of the first and the last group
     for g in (0, h["n_grp"] - 1):
-        r0, G, cs, first = codec.group_geometry(h["rows"], h["cols"], S, g)
+        r0, G, c0, first, GC = codec.group_geometry(h["rows"], h["cols"], S, g, GR)
         bg = blob[h["off_stream"] + grp[g] * 16: h["off_stream"] + grp[g + 1] * 16]
         bits = np.unpackbits(np.frombuffer(bg, np.uint8), bitorder="little").tolist()
         pos = 0
-        for lam in range(G):
+        for mu in range(G * GC):
+            r, c = r0 + mu % G, (c0 + mu // G) * S
             start = pos
             for t in range(S):
                 b, pos = _cam_window_decode(bits, pos, cel, h["lmax"])
                 a, pos = _cam_window_decode(bits, pos, ceh, h["lmax"])
-                assert (a, b) == (eh[r0 + lam, cs * S + t], el[r0 + lam, cs * S + t])
-            assert pos - start == seg_bits[first + lam]
+                assert (a, b) == (eh[r, c + t], el[r, c + t])
+            assert pos - start == seg_bits[first + mu]
         assert (len(bits) - pos) < 128            # group padding below one 128-bit unit
 
 
-def test_group_geometry_tiles_the_matrix():
-    rows, cols, S = 130, 48, 16
-    L = cols // S
+@pytest.mark.parametrize("GR", [64, 32, 16, 8, 1])
+def test_group_geometry_tiles_the_matrix(GR):
+    rows, cols, S = 130, 512, 8
     seen = np.zeros((rows, cols), int)
     firsts = []
-    for g in range(codec.layout(rows, cols, S)["n_grp"]):
-        r0, G, cs, first = codec.group_geometry(rows, cols, S, g)
-        seen[r0:r0 + G, cs * S:(cs + 1) * S] += 1
-        firsts.append((first, G))
+    for g in range(codec.layout(rows, cols, S, GR)["n_grp"]):
+        r0, G, c0, first, GC = codec.group_geometry(rows, cols, S, g, GR)
+        for mu in range(G * GC):
+            r, c = r0 + mu % G, (c0 + mu // G) * S
+            seen[r, c:c + S] += 1
+        firsts.append((first, G * GC))
     assert (seen == 1).all()
     # group g's segments follow those of group g-1 with no gap
-    for (f0, g0), (f1, _) in zip(firsts, firsts[1:]):
-        assert f1 == f0 + g0
+    for (f0, n0), (f1, _) in zip(firsts, firsts[1:]):
+        assert f1 == f0 + n0
+
+
+def test_default_group_rows():
+    assert codec.default_grp_rows(4096, 128) == 16
+    assert codec.default_grp_rows(11008, 344) == 16      # 32 segments per row
+    assert codec.default_grp_rows(48, 16) == 64          # 3 segments per row
+    assert codec.default_grp_rows(80, 8) == 32           # 10 segments per row
+    with pytest.raises(ValueError):
+        codec.encode(random_bf16((4, 48), seed=1), seg_len=16, grp_rows=16)
 
 
 def test_size_accounting_and_ratio_identity():
@@ -308,8 +322,8 @@ def test_size_accounting_and_ratio_identity():
     assert codec.payload_bits(w, ceh, cel) == seg_bits.sum() + 8 * w.size
     grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"]).astype(int)
     for g in range(h["n_grp"]):
-        _, G, _, first = codec.group_geometry(h["rows"], h["cols"], h["seg_len"], g)
-        bits = seg_bits[first: first + G].sum()
+        _, G, _, first, GC = codec.group_geometry(h["rows"], h["cols"], h["seg_len"], g, h["grp_rows"])
+        bits = seg_bits[first: first + G * GC].sum()
         assert grp[g + 1] - grp[g] == (bits + 127) // 128
     assert h["total_bytes"] == len(blob) == h["off_raw"] + w.size
     ratio = 2 * w.size / len(blob)
@@ -347,14 +361,23 @@ def test_lmax_binding_container_roundtrip():
     assert (codec.decode(blob) == w).all()
 
 
-def test_raw_plane_interleave_is_a_permutation():
-    for rows, cols, S in ((130, 16, 16), (64, 8, 8), (1, 24, 24), (200, 80, 40), (65, 64, 32)):
+@pytest.mark.parametrize("GR", [64, 16, 8])
+def test_raw_plane_interleave_is_a_permutation(GR):
+    for rows, cols, S in ((130, 64, 16), (64, 64, 8), (1, 96, 24), (200, 320, 40), (65, 256, 32)):
+        if (cols // S) % (64 // GR):
+            continue
         rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
-        p = codec.raw_pos(rr.ravel(), cc.ravel(), rows, cols, S)
+        p = codec.raw_pos(rr.ravel(), cc.ravel(), rows, cols, S, GR)
         assert np.array_equal(np.sort(p), np.arange(rows * cols))
-    # a full 64-row group: 8-byte runs of one row, rows interleaved
-    p = codec.raw_pos(np.array([0, 0, 1, 0]), np.array([0, 7, 0, 8]), 64, 16, 16)
+
+
+def test_raw_plane_interleave_examples():
+    # a full 64-row group (GR = 64): 8-byte runs of one row, rows interleaved
+    p = codec.raw_pos(np.array([0, 0, 1, 0]), np.array([0, 7, 0, 8]), 64, 16, 16, 64)
     assert p.tolist() == [0, 7, 8, 512]
+    # GR = 16: segment mu = j*16 + i; row 1 of the second segment is mu = 17
+    p = codec.raw_pos(np.array([1, 0]), np.array([16, 8]), 16, 64, 16, 16)
+    assert p.tolist() == [17 * 8, 64 * 8]
 
 
 def test_encode_rejects_bad_shapes():
@@ -401,12 +424,14 @@ def test_bf16_conversion_matches_torch():
                           torch.from_numpy(ours.view(np.int16)).view(torch.bfloat16).double().numpy())
 
 
-@pytest.mark.parametrize("shape,S", [((130, 48), 16), ((64, 1024), 128), ((65, 96), 32), ((3, 64), 8)])
+@pytest.mark.parametrize("shape,S", [((130, 48), 16), ((64, 1024), 128), ((65, 96), 32), ((3, 64), 8),
+                                     ((70, 512), 64)])
 def test_container_size_matches_written_container(shape, S):
     w = random_bf16(shape, seed=shape[0])
     blob = codec.encode(w, seg_len=S)
     h = codec.parse_header(blob)
     cs = codec.container_size(w, S)
+    assert cs["grp_rows"] == h["grp_rows"]
     assert cs["total_bytes"] == len(blob)
     assert cs["max_grp_units"] == h["max_grp_units"] and cs["off_raw"] == h["off_raw"]
     ceh, cel = codec.build_codebooks(w)
