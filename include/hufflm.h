@@ -125,8 +125,10 @@ typedef struct {
 const char* hl_status_str(hl_status s);
 
 /* Segment length the encoder uses for `cols` when asked for 0: among the
- * multiples of 8 in [8, 512] that divide cols, the one nearest to 128 (by
- * ratio; the larger on a tie); 0 if there is none. */
+ * multiples of 8 in [8, 128] that divide cols with cols/S a multiple of 4
+ * (16-row groups), the one nearest to 64 by ratio, the larger on a tie; if
+ * there is none, among the multiples of 8 in [8, 512] that divide cols, the
+ * one nearest to 128; 0 if there is none. */
 uint32_t hl_default_seg_len(uint64_t cols);
 
 /* Per-matrix codebooks of the two exponent fields (Sec. 5.1) from n bf16

@@ -249,15 +249,22 @@ bool header_consistent(const Header& H, uint64_t blob_bytes) {
   return true;
 }
 
-uint32_t default_seg_len(uint64_t cols) {
+// Nearest (by ratio, the larger on a tie) to `target` among the multiples of
+// 8 in [8, hi] that divide cols, restricted to cols/S % 4 == 0 if quad.
+static uint32_t nearest_seg_len(uint64_t cols, uint32_t target, uint32_t hi, bool quad) {
   uint32_t best = 0;
   double bd = 1e30;
-  for (uint32_t S = 8; S <= 512; S += 8) {
-    if (cols % S) continue;
-    double d = S > 128 ? (double)S / 128.0 : 128.0 / (double)S;
+  for (uint32_t S = 8; S <= hi; S += 8) {
+    if (cols % S || (quad && (cols / S) % 4)) continue;
+    double d = S > target ? (double)S / target : (double)target / S;
     if (d <= bd + 1e-12) { bd = d; best = S; }
   }
   return best;
+}
+
+uint32_t default_seg_len(uint64_t cols) {
+  const uint32_t S = nearest_seg_len(cols, 64, 128, true);
+  return S ? S : nearest_seg_len(cols, 128, 512, false);
 }
 
 GroupGeom group_geom(uint64_t rows, uint64_t L, uint32_t GR, uint64_t g) {

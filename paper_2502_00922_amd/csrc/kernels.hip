@@ -35,7 +35,7 @@ constexpr int kLutBits = 13;
 constexpr int kLutN = 1 << kLutBits;   // joint window table entries
 constexpr int kAuxWords = 64;          // canonical tables for the long-code path
 constexpr int kAuxField = 24;          // words per field in the aux table
-constexpr uint32_t kEsc = 0x40u;       // entry of a pair longer than the window
+constexpr uint32_t kEsc = 0x80u;       // entry of a pair longer than the window
 constexpr int kMaxWaves = 16;
 constexpr uint32_t kCol = 64;          // row stride of the stream columns, in words
 
@@ -43,9 +43,9 @@ static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
 
 // Joint table entry: bits 0..4 = code bits of the (el, eh) pair, bits 23..30 =
 // the exponent byte eh<<4|el (its place in a float32), all other bits zero.
-// A window whose pair is longer than 13 bits maps to kEsc (0x40): as a shift
-// it moves nothing, as a position increment it adds 64, which four pairs of at
-// most 13 bits cannot reach, so one compare per four weights finds it.
+// A window whose pair is longer than 13 bits maps to kEsc (0x80): as a shift
+// it moves nothing, as a position increment it adds 128, which eight pairs of
+// at most 13 bits cannot reach, so one compare per eight weights finds it.
 // Aux table, per field f (0 = eh, 1 = el) at word f*24: [0] = nsym |
 // single<<8 | maxlen<<16; [l], l = 1..15: first_code<<16 | count<<8 | offset;
 // [16..19]: symbols sorted by (length, symbol), one byte each.
@@ -142,14 +142,58 @@ __device__ inline void load_tables(const uint32_t* lut) {
   }
 }
 
+// The same copy in two halves, so that a kernel can request the table first
+// and issue its other loads before the stores wait for it: fetch holds up to
+// five 16-byte pieces per thread in registers (blocks of at least 423
+// threads, i.e. 7 waves, which the launcher guarantees), store writes them.
+constexpr uint32_t kTabPieces = 5;
+constexpr uint32_t kTabVec = (kLutN + kAuxWords) / 4;
+constexpr uint32_t kTabMinThreads = (kTabVec + kTabPieces - 1) / kTabPieces;
+
+struct TableRegs {
+  uint4 v[kTabPieces];
+};
+
+__device__ inline TableRegs table_fetch(const uint32_t* lut) {
+  const uint4* src = reinterpret_cast<const uint4*>(lut);
+  const uint32_t n = blockDim.x;
+  TableRegs r;
+#pragma unroll
+  for (uint32_t i = 0; i < kTabPieces; ++i) r.v[i] = src[min(threadIdx.x + i * n, kTabVec - 1)];
+  return r;
+}
+
+__device__ inline void table_store(const TableRegs& r) {
+  uint4* dst = reinterpret_cast<uint4*>(s_tab);
+  const uint32_t n = blockDim.x;
+  // unconditional (a clamped piece rewrites the last one with its own value):
+  // a predicated store would let the compiler sink its load next to it
+#pragma unroll
+  for (uint32_t i = 0; i < kTabPieces; ++i) dst[min(threadIdx.x + i * n, kTabVec - 1)] = r.v[i];
+}
+
 __device__ inline void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
-__device__ inline void wait_vm0() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-__device__ inline void wait_vm1() { asm volatile("s_waitcnt vmcnt(1)" ::: "memory"); }
-__device__ inline void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// s_waitcnt through the builtin, so that the compiler's own wait insertion
+// knows what has completed. gfx9 encoding: vmcnt in bits 3..0 and 15..14,
+// expcnt in 6..4, lgkmcnt in 11..8; a field at its maximum does not wait.
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+constexpr int kWaitLgkm0 = 15 | (3 << 14) | (7 << 4);
+__device__ inline void wait_vm0() {
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+  asm volatile("" ::: "memory");
+}
+__device__ inline void wait_vm1() {
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(1));
+  asm volatile("" ::: "memory");
+}
+__device__ inline void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+  asm volatile("" ::: "memory");
+}
 
 // Direct global-to-LDS copies (no VGPR staging): every lane moves `size`
 // bytes from its own address to lds_base + lane * size; lds_base is
@@ -221,6 +265,7 @@ struct Dec4 {
 };
 
 // Careful path: one weight at a time, long pairs decoded bit-serially.
+// pos2: a clean position (no exponent bits above bit 22).
 __device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t* aux = s_tab + kLutN;
@@ -240,14 +285,12 @@ __device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uin
   return Dec4{pos2, e[0], e[1], e[2], e[3]};
 }
 
-// Decodes 4 weights: table entries e[4] (bits 23..30 = exponent byte), pos2
-// advanced. Four pairs of at most 13 bits fit in one 64-bit window, so the
-// window is loaded once; a long pair anywhere sends the lane through the
-// careful path from the block's start.
-__device__ inline void decode4(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2,
-                               uint32_t* e) {
-  const uint32_t p0 = pos2 & kPosMask;
-  uint64_t W = load_window(sc, p0, jmax);
+// Decodes 4 weights from one 64-bit window (four pairs of at most 13 bits
+// fit): table entries e[4] (bits 23..30 = exponent byte), p advanced by the
+// whole entries. Bits 0..22 of a position are the bit position; the exponent
+// bytes pile up above them and are never read.
+__device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t& p, uint32_t* e) {
+  uint64_t W = load_window(sc, p, jmax);
   e[0] = lut_at((uint32_t)W);
   W = shift_window(W, e[0]);
   e[1] = lut_at((uint32_t)W);
@@ -255,15 +298,33 @@ __device__ inline void decode4(const uint32_t* sc, uint32_t sc_off, uint32_t jma
   e[2] = lut_at((uint32_t)W);
   W = shift_window(W, e[2]);
   e[3] = lut_at((uint32_t)W);
-  pos2 = p0 + e[0] + e[1] + e[2] + e[3];
-  if (((pos2 - p0) & kPosMask) >= 64u) {
-    const Dec4 d = decode4_careful(sc_off, jmax, p0);
-    pos2 = d.pos2;
-    e[0] = d.e0;
-    e[1] = d.e1;
-    e[2] = d.e2;
-    e[3] = d.e3;
+  p = p + e[0] + e[1] + e[2] + e[3];
+}
+
+// Decodes 8 weights. A long pair anywhere (an escape adds 128 to the low bits
+// of the position; eight short pairs add at most 104) sends the lane through
+// the careful path from the first of the eight. After an escape the second
+// window may be read at a wrong (clamped, in-region) position; its entries are
+// discarded.
+__device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* e) {
+  const uint32_t p0 = pos2;
+  uint32_t p = p0;
+  decode4_fast(sc, jmax, p, e);
+  decode4_fast(sc, jmax, p, e + 4);
+  if ((p - p0) & (kPosMask & ~0x7Fu)) {
+    const Dec4 d0 = decode4_careful(sc_off, jmax, p0 & kPosMask);
+    const Dec4 d1 = decode4_careful(sc_off, jmax, d0.pos2);
+    p = d1.pos2;
+    e[0] = d0.e0;
+    e[1] = d0.e1;
+    e[2] = d0.e2;
+    e[3] = d0.e3;
+    e[4] = d1.e0;
+    e[5] = d1.e1;
+    e[6] = d1.e2;
+    e[7] = d1.e3;
   }
+  pos2 = p;
 }
 
 // Packed bf16 pair (weights k, k+1 of a raw dword) from two table entries.
@@ -303,7 +364,9 @@ struct GroupArgs {
 // Group geometry and its metadata (segment length of the lane, stream units).
 struct Meta {
   uint64_t first;  // group-order number of the group's first segment
-  uint32_t r0, G, N, c0, nb, u0, units;
+  uint32_t r0, G, N, c0;
+  uint32_t nbw;    // the dword holding the lane's 16-bit segment length
+  uint32_t u0, units;
 };
 
 // Group g's geometry, and its metadata loads (vector loads, counted by vmcnt).
@@ -315,7 +378,11 @@ __device__ inline Meta load_meta(const GroupArgs& a, uint32_t g, uint32_t lane) 
   m.G = min(a.GR, a.rows - m.r0);
   m.N = m.G * a.GC;
   m.first = (uint64_t)m.r0 * a.L + (uint64_t)m.c0 * m.G;
-  m.nb = lane < m.N ? (uint32_t)a.seg_bits[m.first + lane] : 0u;
+  // A whole dword, used as loaded (no conversion that would wait on it here);
+  // the half-word is picked and masked to lanes < N at use. The dword at an
+  // even index of the last segment reaches 2 bytes past the lengths table,
+  // into the padding before the group offsets.
+  m.nbw = reinterpret_cast<const uint32_t*>(a.seg_bits)[(m.first + min(lane, m.N - 1)) >> 1];
   m.u0 = a.grp_off[g + (lane & 1)];  // lane 0: start, lane 1: end
   m.units = 0;
   return m;
@@ -330,25 +397,31 @@ __device__ inline uint32_t wave_max(uint32_t v) {
 // Copies the group's stream into the lane columns of region `cols`; returns
 // the lane's pos2 (column bit position - 2).
 __device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta& m, uint32_t lane) {
-  uint32_t v0 = (uint32_t)__shfl((int)m.u0, 0, 64), v1 = (uint32_t)__shfl((int)m.u0, 1, 64);
+  // group start and end (lanes 0 and 1), wave-uniform: the copies below take
+  // a scalar base and a 32-bit lane offset
+  uint32_t v0 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 0);
+  uint32_t v1 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 1);
   v0 = min(v0, a.stream_units);
   v1 = min(max(v1, v0), a.stream_units);
   m.u0 = v0;
   m.units = min(v1 - v0, a.max_units);
-  uint32_t incl = m.nb;
+  const uint32_t half = (uint32_t)(m.first + min(lane, m.N - 1)) & 1u;
+  const uint32_t nb = lane < m.N ? (m.nbw >> (16 * half)) & 0xFFFFu : 0u;
+  uint32_t incl = nb;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
     const uint32_t t = __shfl_up(incl, d, 64);
     if ((int)lane >= d) incl += t;
   }
-  const uint32_t start = min(incl - m.nb, m.units * 128u);
+  const uint32_t start = min(incl - nb, m.units * 128u);
   const uint32_t ws = start >> 5, bit0 = start & 31;
   // words the lane's windows read: its bits plus two words of window overrun
-  const uint32_t nw = ((bit0 + m.nb + 31) >> 5) + 2;
+  const uint32_t nw = ((bit0 + nb + 31) >> 5) + 2;
   const uint32_t J = m.units ? min(wave_max(nw), a.col_rows - 1) : 0u;
-  const uint32_t* src = reinterpret_cast<const uint32_t*>(a.stream + m.u0);
+  const uint8_t* src = reinterpret_cast<const uint8_t*>(a.stream + m.u0);  // uniform
   const uint32_t last = m.units * 4 - 1;
-  for (uint32_t j = 0; j < J; ++j) dma4(src + min(ws + j, last), cols + (j + 1) * kCol);
+  // 32-bit byte offsets, so that the copy addresses as scalar base + lane offset
+  for (uint32_t j = 0; j < J; ++j) dma4(src + (uint32_t)(min(ws + j, last) * 4u), cols + (j + 1) * kCol);
   return 30u + bit0;
 }
 
@@ -372,7 +445,7 @@ __device__ inline void issue_raw(const GroupArgs& a, uint32_t* raw_lds, const Me
 // Decode to bf16. Waves take groups in turn; region per wave: stream columns
 // then the raw plane.
 __global__ void __launch_bounds__(1024) decode_kernel(GroupArgs a, uint16_t* out) {
-  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
   const uint32_t per_wave = a.col_rows * kCol + 16 * a.S;
   uint32_t* cols = s_dyn + wave * per_wave;
@@ -405,8 +478,7 @@ __global__ void __launch_bounds__(1024) decode_kernel(GroupArgs a, uint16_t* out
       for (uint32_t t = 0; t < a.S; t += 8) {
         const uint2 rw = rl[(t >> 3) * cur.N];
         uint32_t e[8];
-        decode4(sc, sc_off, jmax, pos2, e);
-        decode4(sc, sc_off, jmax, pos2, e + 4);
+        decode8(sc, sc_off, jmax, pos2, e);
         uint4 v;
         v.x = pack_pair(rw.x, 0, e[0], e[1]);
         v.y = pack_pair(rw.x, 2, e[2], e[3]);
@@ -428,9 +500,10 @@ struct GemvArgs {
   float* y;
   float* partial;     // workspace: KS x B x (RB*64) partial sums (KS > 1)
   uint32_t* counter;  // workspace: RB arrival counters, zero between calls
-  uint32_t C;         // column segments per block
+  uint32_t C;         // column blocks per block
   uint32_t KS;        // blocks per row block
   uint32_t x_words;   // LDS words of one wave's activation slice
+  uint32_t B;         // batch rows
 };
 
 // Copies x[b][c0*S .. (c0+GC)*S) for every batch row into xs ([batch][GC*S]).
@@ -499,7 +572,7 @@ __device__ inline void mac8(float* acc, const uint32_t* e, uint2 rw, const uint3
 template <int B, bool XBF16>
 __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
   const GroupArgs& a = p.g;
-  const uint32_t lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
   const uint32_t S = a.S;
   const uint32_t per_wave = a.col_rows * kCol + 16 * S + p.x_words;
@@ -543,8 +616,7 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
       for (uint32_t t = 0; t < S; t += 8) {
         const uint2 rw = rl[(t >> 3) * N];
         uint32_t e[8];
-        decode4(sc, sc_off, jmax, pos2, e);
-        decode4(sc, sc_off, jmax, pos2, e + 4);
+        decode8(sc, sc_off, jmax, pos2, e);
         mac8<B, XBF16>(acc, e, rw, xl, ldx, t);
       }
     }
@@ -606,6 +678,159 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
         t += __hip_atomic_load(p.partial + ((uint64_t)k * B + b) * ldp + r0 + lane, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
       p.y[(uint64_t)b * ldy + r0 + lane] = t;
+    }
+  }
+  if (lane == 0) __hip_atomic_store(p.counter + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ------------------------------------------------------------------ fused GEMV on matrix cores
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// Fused decode-GEMV for 16-row groups (GR = 16, GC = 4) and bf16 x, on the
+// 16x16x32 bf16 matrix instruction. A group is exactly one A operand per
+// 8-weight step: lane l = 16q + i decodes row r0 + i of column segment c0 + q,
+// and its 8 weights are A[i][8q .. 8q+8); lane l also holds the activations
+// x[n = i][(c0 + q)*S + t .. +8) as B[8q .. 8q+8][n]. The product sums the
+// four segments' 8-weight pieces into C[row][n] (lane l: rows 4q .. 4q+3,
+// batch i). Batch rows past B and rows past the block's G repeat valid data
+// and are never written.
+//
+// Only the stream goes through LDS (DMA into lane columns); raw bytes and x
+// are read straight into registers, KP steps ahead of their use, the last
+// chunk of a group prefetching the next group's first chunk. SP = S/8 steps
+// per group, unrolled so that every wait on a prefetch is exact.
+template <int SP>
+__global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
+  constexpr int KP = SP < 8 ? SP : SP == 8 ? 8 : 4;  // 16 steps at depth 8 exceed 128 VGPRs
+  const GroupArgs& a = p.g;
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t waves = blockDim.x >> 6;
+  constexpr uint32_t S = SP * 8;
+  const uint32_t per_wave = a.col_rows * kCol;
+  uint32_t* cols = s_dyn + wave * per_wave;
+  const uint32_t jmax = a.col_rows - 3;
+
+  const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
+  const uint32_t r0 = rb * 16;
+  const uint32_t G = min(16u, a.rows - r0);
+  const uint32_t N = G * 4;
+  const uint32_t i = lane & 15, q = lane >> 4;
+  const uint32_t mu = q * G + min(i, G - 1);  // the segment this lane decodes
+  const uint32_t sc_off = wave * per_wave + mu;
+  const uint32_t* sc = s_dyn + sc_off;
+  const uint32_t rstride = N * 8;  // bytes between 8-weight steps of the raw plane
+  const uint16_t* xrow = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
+
+  const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
+  uint32_t cb = kp * p.C + wave;
+  // The table is requested first: its LDS stores then wait only for it, not
+  // for the metadata and the HBM reads of the first group behind it. The
+  // first group's loads are unconditional (a wave without a group reads its
+  // block's last group and discards it), so that no merge of paths makes the
+  // compiler wait early.
+  const TableRegs tab = table_fetch(a.lut);
+  Meta m = load_meta(a, rb * a.CB + min(cb, a.CB - 1), lane);
+  uint2 rw[KP];
+  uint4 xv[KP];
+  {
+    const uint8_t* r = a.raw + m.first * S + mu * 8;
+    const uint16_t* x = xrow + m.c0 * S;
+#pragma unroll
+    for (int k = 0; k < KP; ++k) {
+      rw[k] = *reinterpret_cast<const uint2*>(r + k * rstride);
+      xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
+    }
+  }
+  table_store(tab);
+  __syncthreads();
+
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (; cb < cb_end; cb += waves) {
+    // The next group's metadata is requested ahead of this group's copies,
+    // so the one wait below covers both.
+    Meta cur = m;
+    const bool more = cb + waves < cb_end;
+    m = load_meta(a, rb * a.CB + (more ? cb + waves : cb), lane);  // unconditional: no merge to wait on
+    asm volatile("" ::: "memory");
+    uint32_t pos2 = issue_stream(a, cols, cur, lane);
+    const uint8_t* rcur = a.raw + cur.first * S + mu * 8;
+    const uint16_t* xcur = xrow + cur.c0 * S;
+    wait_vm0();
+    wave_sync_lds();
+    pos2 = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+    // prefetch source of the last chunk: the next group, else this chunk again
+    const uint8_t* rnext = more ? a.raw + m.first * S + mu * 8 : rcur + (SP - KP) * rstride;
+    const uint16_t* xnext = more ? xrow + m.c0 * S : xcur + (SP - KP) * 8;
+#pragma unroll
+    for (int t0 = 0; t0 < SP; t0 += KP) {
+      const uint8_t* rp = t0 + KP == SP ? rnext : rcur + (t0 + KP) * rstride;
+      const uint16_t* xp = t0 + KP == SP ? xnext : xcur + (t0 + KP) * 8;
+#pragma unroll
+      for (int k = 0; k < KP; ++k) {
+        uint32_t e[8];
+        decode8(sc, sc_off, jmax, pos2, e);
+        uint4 wv;
+        wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
+        wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
+        wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
+        wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
+                                                      __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
+        rw[k] = *reinterpret_cast<const uint2*>(rp + k * rstride);
+        xv[k] = *reinterpret_cast<const uint4*>(xp + k * 8);
+      }
+    }
+    wait_lgkm0();
+    wave_sync_lds();
+  }
+  wait_vm0();  // prefetches past the last group
+  // Sum over waves in a fixed order (the wave regions are free now).
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(s_dyn);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) red[(wave * 4 + v) * 64 + lane] = acc[v];
+  __syncthreads();
+  if (wave != 0) return;
+  float s[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    float t = red[v * 64 + lane];
+    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
+    s[v] = t;
+  }
+  const uint32_t n = i, ldy = a.rows;
+  const bool nb_ok = n < p.B;
+  if (p.KS == 1) {
+    if (nb_ok)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        if (4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = s[v];
+    return;
+  }
+  // Split over column blocks: the same protocol as the vector kernel.
+  const uint32_t ldp = a.RB * 16;
+  if (nb_ok)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      if (4 * q + v < G)
+        __hip_atomic_store(p.partial + ((uint64_t)kp * p.B + n) * ldp + r0 + 4 * q + v, s[v], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+  wait_vm0();
+  uint32_t old = 0;
+  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  old = __shfl(old, 0, 64);
+  if (old != p.KS - 1) return;
+  if (nb_ok) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if (4 * q + v >= G) continue;
+      float t = 0.f;
+      for (uint32_t k = 0; k < p.KS; ++k)
+        t += __hip_atomic_load(p.partial + ((uint64_t)k * p.B + n) * ldp + r0 + 4 * q + v, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
     }
   }
   if (lane == 0) __hip_atomic_store(p.counter + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -685,7 +910,8 @@ struct Plan {
 // bit 31 of row 1, two rows of window overrun.
 static uint32_t col_rows_for(uint32_t max_seg_bits) { return 1 + ((31 + max_seg_bits + 31) >> 5) + 2; }
 
-static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, Plan* pl) {
+// raw_lds: the kernel stages the raw plane (64*S bytes per wave) in LDS.
+static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bool raw_lds, Plan* pl) {
   if (!t || !t->blob_dev || !t->lut_dev) return HL_EINVAL;
   if (t->rows >= (1ull << 31) || t->cols >= (1ull << 31) || t->n_grp >= (1ull << 31))
     return HL_EUNSUPPORTED;
@@ -707,7 +933,7 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, Pl
   a.stream_units = (uint32_t)std::min<uint64_t>((t->off_raw - t->off_stream) / 16, 0xFFFFFFFFu);
   a.max_units = t->max_grp_units;
   a.col_rows = col_rows_for(t->max_seg_bits);
-  const uint32_t per_wave = a.col_rows * kCol + 16 * t->seg_len + extra_words_per_wave;
+  const uint32_t per_wave = a.col_rows * kCol + (raw_lds ? 16 * t->seg_len : 0) + extra_words_per_wave;
   // LDS: the static tables plus one region per wave.
   const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
   uint32_t waves = kMaxWaves;
@@ -735,6 +961,23 @@ static hl_status launch_gemv_b(bool xbf16, dim3 grid, dim3 block, size_t lds, hi
                                const GemvArgs& p) {
   return xbf16 ? launch(gemv_kernel<B, true>, grid, block, lds, s, p)
                : launch(gemv_kernel<B, false>, grid, block, lds, s, p);
+}
+
+// Segment lengths with a matrix-core instantiation (S = 8 * steps).
+static bool mfma_steps_ok(uint32_t steps) {
+  return steps == 1 || steps == 2 || steps == 4 || steps == 8 || steps == 16;
+}
+
+static hl_status launch_mfma(uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                             const GemvArgs& p) {
+  switch (steps) {
+    case 1: return launch(gemv_mfma_kernel<1>, grid, block, lds, s, p);
+    case 2: return launch(gemv_mfma_kernel<2>, grid, block, lds, s, p);
+    case 4: return launch(gemv_mfma_kernel<4>, grid, block, lds, s, p);
+    case 8: return launch(gemv_mfma_kernel<8>, grid, block, lds, s, p);
+    case 16: return launch(gemv_mfma_kernel<16>, grid, block, lds, s, p);
+    default: return HL_EUNSUPPORTED;
+  }
 }
 
 template <int B>
@@ -809,7 +1052,7 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
 extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream) {
   if (!out_dev) return HL_EINVAL;
   Plan pl;
-  hl_status st = make_plan(t, 0, &pl);
+  hl_status st = make_plan(t, 0, true, &pl);
   if (st != HL_OK) return st;
   const uint32_t n_grp = pl.ga.RB * pl.ga.CB;
   const uint32_t per_cu =
@@ -839,18 +1082,28 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     return HL_EINVAL;
   if (t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS) return HL_EINVAL;
   const bool xb = x_dtype == HL_BF16;
-  // activation slice of one group: GC*S columns per batch row
+  // 16-row groups with bf16 activations run on the matrix cores; the vector
+  // kernel stages raw bytes and the activation slice (GC*S columns per batch
+  // row) in LDS.
+  bool mfma = xb && t->grp_rows == 16 && t->seg_len % 8 == 0 && mfma_steps_ok(t->seg_len / 8);
   const uint32_t slice = (HL_GROUP_SEGS / t->grp_rows) * t->seg_len;
   const uint32_t x_words = xb ? slice * batch / 2 : slice * batch;
   Plan pl;
-  hl_status st = make_plan(t, x_words, &pl);
+  hl_status st = make_plan(t, mfma ? 0 : x_words, !mfma, &pl);
   if (st != HL_OK) return st;
+  if (mfma && pl.waves * 64 < kTabMinThreads) {
+    // too few waves fit for the matrix-core kernel's table copy
+    mfma = false;
+    st = make_plan(t, x_words, true, &pl);
+    if (st != HL_OK) return st;
+  }
   GemvArgs p;
   std::memset(&p, 0, sizeof(p));
   p.g = pl.ga;
   p.x = x_dev;
   p.y = y_dev;
-  p.x_words = x_words;
+  p.x_words = mfma ? 0 : x_words;
+  p.B = batch;
   // Column blocks per block: enough blocks to fill the device, each wave
   // decoding at least one group; KS blocks share a row block.
   const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
@@ -874,7 +1127,11 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     p.partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
   }
   const dim3 grid(RB * KS), block(pl.waves * 64);
-  // the reduction reuses the wave regions
+  if (mfma) {
+    // the reduction reuses the wave regions: 4 floats per lane per wave
+    const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * 4 * 64 * 4);
+    return launch_mfma(t->seg_len / 8, grid, block, lds, (hipStream_t)stream, p);
+  }
   const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * batch * 64 * 4);
   HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
 }

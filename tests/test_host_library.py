@@ -91,9 +91,12 @@ def test_default_grp_rows():
 
 
 def test_default_seg_len():
-    assert [hl.default_seg_len(k) for k in (1024, 4096, 11008, 14336, 28672)] == [128] * 5
+    # every projection width of the workloads: S = 64 with cols/S a multiple of 4
+    assert [hl.default_seg_len(k) for k in (1024, 4096, 8192, 11008, 14336, 28672)] == [64] * 6
     assert hl.default_seg_len(24) == 24 and hl.default_seg_len(100) == 0 and hl.default_seg_len(8) == 8
-    assert hl.default_seg_len(1000) == 125 * 8 // 8 * 1 if 1000 % 125 == 0 and 125 % 8 == 0 else True
+    assert hl.default_seg_len(96) == 24            # 96/24 = 4
+    assert hl.default_seg_len(48) == 48            # no quad split: nearest to 128
+    assert hl.default_seg_len(1000) == 0 or 1000 % hl.default_seg_len(1000) == 0
 
 
 def test_encode_errors():
