@@ -142,35 +142,9 @@ __device__ inline void load_tables(const uint32_t* lut) {
   }
 }
 
-// The same copy in two halves, so that a kernel can request the table first
-// and issue its other loads before the stores wait for it: fetch holds up to
-// five 16-byte pieces per thread in registers (blocks of at least 423
-// threads, i.e. 7 waves, which the launcher guarantees), store writes them.
-constexpr uint32_t kTabPieces = 5;
-constexpr uint32_t kTabVec = (kLutN + kAuxWords) / 4;
-constexpr uint32_t kTabMinThreads = (kTabVec + kTabPieces - 1) / kTabPieces;
-
-struct TableRegs {
-  uint4 v[kTabPieces];
-};
-
-__device__ inline TableRegs table_fetch(const uint32_t* lut) {
-  const uint4* src = reinterpret_cast<const uint4*>(lut);
-  const uint32_t n = blockDim.x;
-  TableRegs r;
-#pragma unroll
-  for (uint32_t i = 0; i < kTabPieces; ++i) r.v[i] = src[min(threadIdx.x + i * n, kTabVec - 1)];
-  return r;
-}
-
-__device__ inline void table_store(const TableRegs& r) {
-  uint4* dst = reinterpret_cast<uint4*>(s_tab);
-  const uint32_t n = blockDim.x;
-  // unconditional (a clamped piece rewrites the last one with its own value):
-  // a predicated store would let the compiler sink its load next to it
-#pragma unroll
-  for (uint32_t i = 0; i < kTabPieces; ++i) dst[min(threadIdx.x + i * n, kTabVec - 1)] = r.v[i];
-}
+// The same copy as direct global-to-LDS transfers (16 bytes per lane, no
+// registers): the caller waits for them (vmcnt) before its barrier.
+constexpr uint32_t kTabVec = (kLutN + kAuxWords) / 4;  // 16-byte pieces
 
 __device__ inline void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -203,6 +177,12 @@ __device__ inline void dma16(const void* src, uint32_t* lds_base) {
 }
 __device__ inline void dma4(const void* src, uint32_t* lds_base) {
   __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 4, 0, 0);
+}
+
+__device__ inline void table_dma(const uint32_t* lut) {
+  const uint32_t n = blockDim.x, w0 = threadIdx.x & ~63u, lane = threadIdx.x & 63;
+  for (uint32_t k0 = w0; k0 < kTabVec; k0 += n)
+    if (k0 + lane < kTabVec) dma16(lut + (k0 + lane) * 4, s_tab + k0 * 4);
 }
 
 // ---- stream columns
@@ -725,13 +705,15 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
 
   const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
   uint32_t cb = kp * p.C + wave;
-  // The table is requested first: its LDS stores then wait only for it, not
-  // for the metadata and the HBM reads of the first group behind it. The
-  // first group's loads are unconditional (a wave without a group reads its
-  // block's last group and discards it), so that no merge of paths makes the
-  // compiler wait early.
-  const TableRegs tab = table_fetch(a.lut);
-  Meta m = load_meta(a, rb * a.CB + min(cb, a.CB - 1), lane);
+  // Prologue: the first two groups' metadata and the first group's raw bytes
+  // and activations are requested together; once the metadata is in, the
+  // table and the first group's stream are copied to LDS, the two copies'
+  // latencies overlapping. All loads are unconditional (a wave without a
+  // group reads its block's last group and discards it), so that no merge of
+  // paths makes the compiler wait early.
+  const uint32_t cb0 = min(cb, a.CB - 1);
+  Meta m = load_meta(a, rb * a.CB + cb0, lane);
+  Meta mn = load_meta(a, rb * a.CB + (cb + waves < cb_end ? cb + waves : cb0), lane);
   uint2 rw[KP];
   uint4 xv[KP];
   {
@@ -743,26 +725,27 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
       xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
     }
   }
-  table_store(tab);
+  // the first use of the metadata stays behind the loads above
+  asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
+  table_dma(a.lut);
+  uint32_t pos2 = issue_stream(a, cols, m, lane);
+  wait_vm0();  // table and first stream copies (and the prefetches before them)
   __syncthreads();
 
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   for (; cb < cb_end; cb += waves) {
-    // The next group's metadata is requested ahead of this group's copies,
-    // so the one wait below covers both.
-    Meta cur = m;
+    // Group cb's stream copy is in flight; mn is the next group's metadata.
+    const Meta cur = m;
     const bool more = cb + waves < cb_end;
-    m = load_meta(a, rb * a.CB + (more ? cb + waves : cb), lane);  // unconditional: no merge to wait on
-    asm volatile("" ::: "memory");
-    uint32_t pos2 = issue_stream(a, cols, cur, lane);
-    const uint8_t* rcur = a.raw + cur.first * S + mu * 8;
-    const uint16_t* xcur = xrow + cur.c0 * S;
     wait_vm0();
     wave_sync_lds();
-    pos2 = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+    const uint32_t pos2l = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+    const uint8_t* rcur = a.raw + cur.first * S + mu * 8;
+    const uint16_t* xcur = xrow + cur.c0 * S;
     // prefetch source of the last chunk: the next group, else this chunk again
-    const uint8_t* rnext = more ? a.raw + m.first * S + mu * 8 : rcur + (SP - KP) * rstride;
-    const uint16_t* xnext = more ? xrow + m.c0 * S : xcur + (SP - KP) * 8;
+    const uint8_t* rnext = more ? a.raw + mn.first * S + mu * 8 : rcur + (SP - KP) * rstride;
+    const uint16_t* xnext = more ? xrow + mn.c0 * S : xcur + (SP - KP) * 8;
+    uint32_t pd = pos2l;
 #pragma unroll
     for (int t0 = 0; t0 < SP; t0 += KP) {
       const uint8_t* rp = t0 + KP == SP ? rnext : rcur + (t0 + KP) * rstride;
@@ -770,7 +753,7 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
 #pragma unroll
       for (int k = 0; k < KP; ++k) {
         uint32_t e[8];
-        decode8(sc, sc_off, jmax, pos2, e);
+        decode8(sc, sc_off, jmax, pd, e);
         uint4 wv;
         wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
         wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
@@ -784,6 +767,12 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
     }
     wait_lgkm0();
     wave_sync_lds();
+    if (more) {
+      // the group after next's metadata, then the next group's stream copy
+      m = mn;
+      mn = load_meta(a, rb * a.CB + (cb + 2 * waves < cb_end ? cb + 2 * waves : cb + waves), lane);
+      pos2 = issue_stream(a, cols, m, lane);
+    }
   }
   wait_vm0();  // prefetches past the last group
   // Sum over waves in a fixed order (the wave regions are free now).
@@ -792,6 +781,17 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
 #pragma unroll
   for (int v = 0; v < 4; ++v) red[(wave * 4 + v) * 64 + lane] = acc[v];
   __syncthreads();
+  const uint32_t n = i, ldy = a.rows;
+  const bool nb_ok = n < p.B;
+  if (p.KS == 1) {
+    // waves 0..3 each finish one of the four values of every lane
+    if (wave >= 4 || wave >= waves) return;
+    const uint32_t v = wave;
+    float t = red[v * 64 + lane];
+    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
+    if (nb_ok && 4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
+    return;
+  }
   if (wave != 0) return;
   float s[4];
 #pragma unroll
@@ -799,15 +799,6 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
     float t = red[v * 64 + lane];
     for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
     s[v] = t;
-  }
-  const uint32_t n = i, ldy = a.rows;
-  const bool nb_ok = n < p.B;
-  if (p.KS == 1) {
-    if (nb_ok)
-#pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = s[v];
-    return;
   }
   // Split over column blocks: the same protocol as the vector kernel.
   const uint32_t ldp = a.RB * 16;
@@ -1085,18 +1076,12 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   // 16-row groups with bf16 activations run on the matrix cores; the vector
   // kernel stages raw bytes and the activation slice (GC*S columns per batch
   // row) in LDS.
-  bool mfma = xb && t->grp_rows == 16 && t->seg_len % 8 == 0 && mfma_steps_ok(t->seg_len / 8);
+  const bool mfma = xb && t->grp_rows == 16 && t->seg_len % 8 == 0 && mfma_steps_ok(t->seg_len / 8);
   const uint32_t slice = (HL_GROUP_SEGS / t->grp_rows) * t->seg_len;
   const uint32_t x_words = xb ? slice * batch / 2 : slice * batch;
   Plan pl;
   hl_status st = make_plan(t, mfma ? 0 : x_words, !mfma, &pl);
   if (st != HL_OK) return st;
-  if (mfma && pl.waves * 64 < kTabMinThreads) {
-    // too few waves fit for the matrix-core kernel's table copy
-    mfma = false;
-    st = make_plan(t, x_words, true, &pl);
-    if (st != HL_OK) return st;
-  }
   GemvArgs p;
   std::memset(&p, 0, sizeof(p));
   p.g = pl.ga;
