@@ -11,13 +11,17 @@ Recipe (every draw is float32 from numpy's PCG64 ``default_rng``):
 * activations x ~ N(0, 1), as float32 or rounded to bfloat16.
 
 Seeds: the 1024x1024 single-matrix workload uses ``default_rng(0)`` and draws
-W, then the mask, then x, in that order. Every other matrix uses independent
-streams ``default_rng([0, cfg, layer, matrix, k])`` with k = 0 for the values,
-1 for x, 2 for the outlier mask and 3 for the scales, so a matrix can be
-regenerated alone and in row blocks.
+W, then the mask, then x, in that order. Every other matrix draws its values
+and its outlier mask per block of 256 rows, from the independent streams
+``default_rng([0, cfg, layer, matrix, k, block])`` with k = 0 for the values
+and 2 for the mask, and its x and scales from ``default_rng([0, cfg, layer,
+matrix, k])`` with k = 1 for x and 3 for the scales. A matrix or any row range
+of it can thus be regenerated alone, and the row blocks in parallel.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
 from typing import List, Optional
 
@@ -96,15 +100,33 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def _stream(spec: MatrixSpec, k: int) -> np.random.Generator:
-    return np.random.default_rng([0, spec.cfg, spec.layer, spec.index, k])
+ROW_BLOCK = 256
 
 
-def gen_matrix(spec: MatrixSpec, rows: Optional[slice] = None) -> np.ndarray:
+def _stream(spec: MatrixSpec, k: int, block: Optional[int] = None) -> np.random.Generator:
+    key = [0, spec.cfg, spec.layer, spec.index, k]
+    return np.random.default_rng(key if block is None else key + [block])
+
+
+def _row_block(spec: MatrixSpec, b: int, std: np.float32, scale: Optional[np.ndarray]) -> np.ndarray:
+    """Rows [b*ROW_BLOCK, min(rows, (b+1)*ROW_BLOCK)) as float32."""
+    R, K = spec.rows, spec.cols
+    n = min(R, (b + 1) * ROW_BLOCK) - b * ROW_BLOCK
+    w = _stream(spec, 0, b).standard_normal(n * K, dtype=np.float32) * std
+    mask = _stream(spec, 2, b).random(n * K, dtype=np.float32) < OUTLIER_P
+    w[mask] *= np.float32(OUTLIER_MUL)
+    w = w.reshape(n, K)
+    if scale is not None:
+        w *= scale[b * ROW_BLOCK:b * ROW_BLOCK + n, None]
+    return w
+
+
+def gen_matrix(spec: MatrixSpec, rows: Optional[slice] = None, threads: int = 0) -> np.ndarray:
     """bf16 bit patterns (uint16, shape [rows, cols]) of one matrix.
 
     ``rows`` selects a contiguous row range; the values equal the same rows of
-    the full matrix (except for workload 1, which is always drawn whole)."""
+    the full matrix (workload 1 is always drawn whole). Row blocks are drawn on
+    ``threads`` threads (0: all cores); the result does not depend on it."""
     R, K = spec.rows, spec.cols
     if spec.cfg == 1:
         rng = np.random.default_rng(0)
@@ -118,27 +140,27 @@ def gen_matrix(spec: MatrixSpec, rows: Optional[slice] = None) -> np.ndarray:
     if spec.layer_scale:
         u = _stream(spec, 3).uniform(1.0, 4.0)
         std = np.float32(BASE_STD / np.sqrt(u))
-    rv, rm = _stream(spec, 0), _stream(spec, 2)
-    # Advance both streams to row r0 so that a row block equals the full draw.
-    if r0:
-        _skip_normal(rv, r0 * K)
-        rm.random(r0 * K, dtype=np.float32)
-    n = (r1 - r0) * K
-    w = rv.standard_normal(n, dtype=np.float32) * std
-    mask = rm.random(n, dtype=np.float32) < OUTLIER_P
-    w[mask] *= np.float32(OUTLIER_MUL)
-    w = w.reshape(r1 - r0, K)
+    scale = None
     if spec.row_scale:
-        z = _stream(spec, 3).standard_normal(R, dtype=np.float32)[r0:r1]
-        w *= np.exp(np.float32(0.3) * z)[:, None].astype(np.float32)
-    return f32_to_bf16_bits(w)
+        z = _stream(spec, 3).standard_normal(R, dtype=np.float32)
+        scale = np.exp(np.float32(0.3) * z).astype(np.float32)
+    out = np.empty((r1 - r0, K), dtype=np.uint16)
+    b0, b1 = r0 // ROW_BLOCK, (r1 + ROW_BLOCK - 1) // ROW_BLOCK
 
+    def one(b):
+        lo = b * ROW_BLOCK
+        w = _row_block(spec, b, std, scale)
+        a, e = max(r0, lo), min(r1, lo + w.shape[0])
+        out[a - r0:e - r0] = f32_to_bf16_bits(w[a - lo:e - lo])
 
-def _skip_normal(rng: np.random.Generator, count: int, block: int = 1 << 24) -> None:
-    while count > 0:
-        m = min(count, block)
-        rng.standard_normal(m, dtype=np.float32)
-        count -= m
+    nt = threads or min(32, os.cpu_count() or 1)
+    if nt <= 1 or b1 - b0 <= 1:
+        for b in range(b0, b1):
+            one(b)
+    else:
+        with ThreadPoolExecutor(nt) as ex:
+            list(ex.map(one, range(b0, b1)))
+    return out
 
 
 def gen_x(spec: MatrixSpec, batch: int, dtype: str) -> np.ndarray:

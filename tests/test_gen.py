@@ -27,3 +27,10 @@ def test_distribution_workload1():
     assert 0.0003 < big.mean() < 0.0015
     x = gen_x(spec, 1, "f32")
     assert x.shape == (1, 1024) and x.dtype == np.float32
+
+
+def test_thread_count_and_block_boundaries():
+    spec = MatrixSpec(3, 0, 2, "down", 600, 64)
+    a = gen_matrix(spec, threads=1)
+    assert np.array_equal(a, gen_matrix(spec, threads=5))
+    assert np.array_equal(gen_matrix(spec, slice(250, 530), threads=3), a[250:530])
