@@ -742,14 +742,20 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
     const uint32_t pos2l = (uint32_t)__shfl((int)pos2, (int)mu, 64);
     const uint8_t* rcur = a.raw + cur.first * S + mu * 8;
     const uint16_t* xcur = xrow + cur.c0 * S;
-    // prefetch source of the last chunk: the next group, else this chunk again
-    const uint8_t* rnext = more ? a.raw + mn.first * S + mu * 8 : rcur + (SP - KP) * rstride;
-    const uint16_t* xnext = more ? xrow + mn.c0 * S : xcur + (SP - KP) * 8;
+    // Prefetch source of the last chunk: the next group; after the wave's
+    // last group, the lane's own first activation chunk (cache-resident) at
+    // stride 0, so that the pipeline's loads stay unconditional without
+    // reading HBM again.
+    const uint8_t* rnext = more ? a.raw + mn.first * S + mu * 8 : reinterpret_cast<const uint8_t*>(xcur);
+    const uint16_t* xnext = more ? xrow + mn.c0 * S : xcur;
+    const uint32_t rs_last = more ? rstride : 0u, xs_last = more ? 8u : 0u;
     uint32_t pd = pos2l;
 #pragma unroll
     for (int t0 = 0; t0 < SP; t0 += KP) {
-      const uint8_t* rp = t0 + KP == SP ? rnext : rcur + (t0 + KP) * rstride;
-      const uint16_t* xp = t0 + KP == SP ? xnext : xcur + (t0 + KP) * 8;
+      const bool last = t0 + KP == SP;
+      const uint8_t* rp = last ? rnext : rcur + (t0 + KP) * rstride;
+      const uint16_t* xp = last ? xnext : xcur + (t0 + KP) * 8;
+      const uint32_t rs = last ? rs_last : rstride, xs = last ? xs_last : 8u;
 #pragma unroll
       for (int k = 0; k < KP; ++k) {
         uint32_t e[8];
@@ -761,8 +767,8 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
         wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
                                                       __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
-        rw[k] = *reinterpret_cast<const uint2*>(rp + k * rstride);
-        xv[k] = *reinterpret_cast<const uint4*>(xp + k * 8);
+        rw[k] = *reinterpret_cast<const uint2*>(rp + k * rs);
+        xv[k] = *reinterpret_cast<const uint4*>(xp + k * xs);
       }
     }
     wait_lgkm0();
