@@ -146,6 +146,15 @@ __device__ inline void load_tables(const uint32_t* lut) {
 // registers): the caller waits for them (vmcnt) before its barrier.
 constexpr uint32_t kTabVec = (kLutN + kAuxWords) / 4;  // 16-byte pieces
 
+// Block barrier for LDS data only: waits for this wave's LDS accesses, not for
+// its outstanding global loads and copies (gfx950 barriers do not need them).
+__device__ inline void block_sync_lds() {
+  __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4));  // lgkmcnt(0)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 __device__ inline void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -245,8 +254,11 @@ struct Dec4 {
 };
 
 // Careful path: one weight at a time, long pairs decoded bit-serially.
-// pos2: a clean position (no exponent bits above bit 22).
-__device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
+// pos2: a clean position (no exponent bits above bit 22). The body is shared
+// by an out-of-line copy and an inlined one (see decode8).
+__device__ __attribute__((always_inline)) inline Dec4 decode4_careful_body(uint32_t sc_off, uint32_t jmax,
+                                                                           uint32_t pos2) {
+  asm volatile("" ::: "memory");  // keeps its table reads inside the (cold) path
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t* aux = s_tab + kLutN;
   uint32_t e[4];
@@ -263,6 +275,10 @@ __device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uin
     e[k] = ent;
   }
   return Dec4{pos2, e[0], e[1], e[2], e[3]};
+}
+
+__device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
+  return decode4_careful_body(sc_off, jmax, pos2);
 }
 
 // Decodes 4 weights from one 64-bit window (four pairs of at most 13 bits
@@ -286,14 +302,19 @@ __device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t&
 // the careful path from the first of the eight. After an escape the second
 // window may be read at a wrong (clamped, in-region) position; its entries are
 // discarded.
+// INLINE_SLOW selects an inlined, cold-placed careful path instead of a call:
+// a call makes the compiler wait for every load in flight whose register is
+// live across it, which the persistent kernel cannot afford.
+template <bool INLINE_SLOW = false>
 __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* e) {
   const uint32_t p0 = pos2;
   uint32_t p = p0;
   decode4_fast(sc, jmax, p, e);
   decode4_fast(sc, jmax, p, e + 4);
-  if ((p - p0) & (kPosMask & ~0x7Fu)) {
-    const Dec4 d0 = decode4_careful(sc_off, jmax, p0 & kPosMask);
-    const Dec4 d1 = decode4_careful(sc_off, jmax, d0.pos2);
+  if (__builtin_expect(((p - p0) & (kPosMask & ~0x7Fu)) != 0, 0)) {
+    const Dec4 d0 = INLINE_SLOW ? decode4_careful_body(sc_off, jmax, p0 & kPosMask)
+                                : decode4_careful(sc_off, jmax, p0 & kPosMask);
+    const Dec4 d1 = INLINE_SLOW ? decode4_careful_body(sc_off, jmax, d0.pos2) : decode4_careful(sc_off, jmax, d0.pos2);
     p = d1.pos2;
     e[0] = d0.e0;
     e[1] = d0.e1;
@@ -376,9 +397,12 @@ __device__ inline uint32_t wave_max(uint32_t v) {
 
 // Copies the group's stream into the lane columns of region `cols`; returns
 // the lane's pos2 (column bit position - 2).
-__device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta& m, uint32_t lane) {
-  // group start and end (lanes 0 and 1), wave-uniform: the copies below take
-  // a scalar base and a 32-bit lane offset
+// Group start and length (lanes 0 and 1 of the metadata, made wave-uniform so
+// that copies address as scalar base + 32-bit lane offset), and the lane's
+// first stream word ws and bit bit0 (segment lengths prefix-summed in lane
+// order); returns the lane's code bits.
+__device__ inline uint32_t stream_start(const GroupArgs& a, Meta& m, uint32_t lane, uint32_t& ws,
+                                        uint32_t& bit0) {
   uint32_t v0 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 0);
   uint32_t v1 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 1);
   v0 = min(v0, a.stream_units);
@@ -394,7 +418,17 @@ __device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta
     if ((int)lane >= d) incl += t;
   }
   const uint32_t start = min(incl - nb, m.units * 128u);
-  const uint32_t ws = start >> 5, bit0 = start & 31;
+  ws = start >> 5;
+  bit0 = start & 31;
+  return nb;
+}
+
+// Copies the group's stream into the lane columns of region `cols` (as many
+// rows as the longest lane needs); returns the lane's pos2 (column bit
+// position - 2).
+__device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta& m, uint32_t lane) {
+  uint32_t ws, bit0;
+  const uint32_t nb = stream_start(a, m, lane, ws, bit0);
   // words the lane's windows read: its bits plus two words of window overrun
   const uint32_t nw = ((bit0 + nb + 31) >> 5) + 2;
   const uint32_t J = m.units ? min(wave_max(nw), a.col_rows - 1) : 0u;
@@ -403,6 +437,52 @@ __device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta
   // 32-bit byte offsets, so that the copy addresses as scalar base + lane offset
   for (uint32_t j = 0; j < J; ++j) dma4(src + (uint32_t)(min(ws + j, last) * 4u), cols + (j + 1) * kCol);
   return 30u + bit0;
+}
+
+// The same with exactly JT rows (a compile-time count of copies, so that the
+// compiler can count the loads behind them). Rows past a lane's words repeat
+// the group's last word; a group without stream bits reads its first raw word.
+template <int JT>
+__device__ inline uint32_t issue_stream_fixed(const GroupArgs& a, uint32_t* cols, Meta& m, uint32_t lane) {
+  uint32_t ws, bit0;
+  stream_start(a, m, lane, ws, bit0);
+  const uint8_t* src = m.units ? reinterpret_cast<const uint8_t*>(a.stream + m.u0) : a.raw + m.first * a.S;
+  const uint32_t last = m.units ? m.units * 4 - 1 : 0u;
+#pragma unroll
+  for (int j = 0; j < JT; ++j) dma4(src + (uint32_t)(min(ws + j, last) * 4u), cols + (j + 1) * kCol);
+  return 30u + bit0;
+}
+
+typedef uint32_t u32x4_a4 __attribute__((ext_vector_type(4), aligned(4)));
+
+// The group's stream words for the lane columns, loaded into registers: JT
+// words per lane from its first word on (four per load). Words past the
+// group's stream are read from what follows it in the container (the next
+// group's stream or the raw plane, at most JT words on), as window overrun
+// only; a group without stream bits reads its raw bytes. Returns the lane's
+// pos2.
+template <int JT>
+__device__ inline uint32_t stream_load(const GroupArgs& a, Meta& m, uint32_t lane, u32x4_a4 (&sw)[JT / 4]) {
+  uint32_t ws, bit0;
+  stream_start(a, m, lane, ws, bit0);
+  const uint32_t* base = m.units ? reinterpret_cast<const uint32_t*>(a.stream + m.u0)
+                                 : reinterpret_cast<const uint32_t*>(a.raw + m.first * a.S);
+  const uint32_t w0 = m.units ? ws : 0u;
+#pragma unroll
+  for (int k = 0; k < JT / 4; ++k) sw[k] = *reinterpret_cast<const u32x4_a4*>(base + w0 + 4 * k);
+  return 30u + bit0;
+}
+
+// Writes the words of stream_load to the lane's column (rows 1..JT).
+template <int JT>
+__device__ inline void stream_store(uint32_t* cols, const u32x4_a4 (&sw)[JT / 4], uint32_t lane) {
+#pragma unroll
+  for (int k = 0; k < JT / 4; ++k) {
+    cols[(4 * k + 1) * kCol + lane] = sw[k].x;
+    cols[(4 * k + 2) * kCol + lane] = sw[k].y;
+    cols[(4 * k + 3) * kCol + lane] = sw[k].z;
+    cols[(4 * k + 4) * kCol + lane] = sw[k].w;
+  }
 }
 
 // Copies the group's raw plane (N*S bytes) into `raw_lds`.
@@ -833,6 +913,158 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
   if (lane == 0) __hip_atomic_store(p.counter + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ------------------------------------------------------------------ persistent fused GEMV
+
+// Persistent form of the matrix-core kernel for S = 64 and matrices with at
+// least one 16-row block per block of the grid and at least as many column
+// blocks as waves. Block b takes row blocks b, b + grid, ...; its waves take
+// the row block's column blocks wave, wave + waves, ... The table is copied
+// once per block.
+//
+// While a wave decodes group k from its LDS columns, group k+1's stream words
+// (JT per lane, four per load), raw bytes and activations are loaded into
+// registers and group k+2's metadata arrives; after the decode the stream
+// words are written to the columns. Only ordinary loads are in flight in the
+// loop (no LDS copies, which the compiler does not order with them), so every
+// wait the compiler places is exact. At a row block's end the waves add their
+// accumulators through their columns in a fixed order (before the next
+// group's words go in) and four waves write y.
+template <int JT>
+__global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
+  constexpr int SP = 8;
+  constexpr uint32_t S = SP * 8;
+  constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
+  static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
+  const GroupArgs& a = p.g;
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t waves = blockDim.x >> 6;
+  uint32_t* cols = s_dyn + wave * kBuf;
+  const uint32_t jmax = kRows - 3;
+  const uint32_t i = lane & 15, q = lane >> 4;
+  const uint16_t* xlane = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
+  const uint32_t CB = a.CB, RB = a.RB, L = a.L, nj = (CB + waves - 1) / waves;
+  const uint32_t last_group = RB * CB - 1;
+
+  // the wave's groups in order: round t (row block blockIdx.x + t*grid), step
+  // j; branch-free (a branch between a load and its use makes the compiler's
+  // wait for it conservative)
+  auto rb_of = [&](uint32_t t) { return blockIdx.x + t * gridDim.x; };
+  auto advance = [&](uint32_t& t, uint32_t& j) {
+    const bool same = wave + (j + 1) * waves < CB;
+    t = same ? t : t + 1;
+    j = same ? j + 1 : 0u;
+  };
+  auto group = [&](uint32_t t, uint32_t j) { return min(rb_of(t) * CB + wave + j * waves, last_group); };
+  auto lane_mu = [&](uint32_t rb) {
+    const uint32_t G = min(16u, a.rows - rb * 16);
+    return q * G + min(i, G - 1);
+  };
+
+  // Prologue: the first two groups' metadata, the table (copied to LDS), the
+  // first group's raw bytes and activations and its stream words.
+  uint32_t t1 = 0, j1 = 0;
+  advance(t1, j1);
+  const uint32_t g0 = group(0, 0);
+  const uint32_t g1 = rb_of(t1) < RB ? group(t1, j1) : g0;
+  Meta m0 = load_meta(a, g0, lane);
+  Meta m1 = load_meta(a, g1, lane);
+  table_dma(a.lut);
+  uint2 rw[SP];
+  uint4 xv[SP];
+  {
+    const uint32_t rb = g0 / CB;
+    const uint32_t G = min(16u, a.rows - rb * 16);
+    const uint8_t* r = a.raw + m0.first * S + lane_mu(rb) * 8;
+    const uint16_t* x = xlane + m0.c0 * S;
+#pragma unroll
+    for (int k = 0; k < SP; ++k) {
+      rw[k] = *reinterpret_cast<const uint2*>(r + k * G * 32u);
+      xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
+    }
+  }
+  u32x4_a4 sw[JT / 4];
+  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw);
+  stream_store<JT>(cols, sw, lane);
+  wait_vm0();  // the table copy
+  __syncthreads();
+
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (uint32_t t = 0; rb_of(t) < RB; ++t) {
+    const uint32_t rb = rb_of(t);
+    const uint32_t G = min(16u, a.rows - rb * 16);
+    const uint32_t mu = q * G + min(i, G - 1);
+    const uint32_t sc_off = wave * kBuf + mu;
+    const uint32_t* sc = s_dyn + sc_off;
+    for (uint32_t j = 0; j < nj; ++j) {
+      if (wave + j * waves >= CB) continue;
+      // the next two groups of this wave
+      uint32_t tn = t, jn = j;
+      advance(tn, jn);
+      const bool okn = rb_of(tn) < RB;
+      uint32_t t2 = tn, j2 = jn;
+      advance(t2, j2);
+      const uint32_t g2 = rb_of(t2) < RB ? group(t2, j2) : group(t, j);
+      const uint32_t rbn = okn ? rb_of(tn) : rb;
+      const uint32_t Gn = min(16u, a.rows - rbn * 16);
+      const uint64_t n_first = m1.first;
+      const uint32_t n_c0 = m1.c0;
+      // the next group's stream words (this group's again after the last),
+      // then the metadata of the group after it
+      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw);
+      m1 = load_meta(a, g2, lane);
+      // prefetch source: the next group, else the lane's cached activations at stride 0
+      const uint16_t* xcur = xlane + (wave + j * waves) * 4 * S;
+      const uint8_t* rp = okn ? a.raw + n_first * S + lane_mu(rbn) * 8 : reinterpret_cast<const uint8_t*>(xcur);
+      const uint16_t* xp = okn ? xlane + n_c0 * S : xcur;
+      const uint32_t rs = okn ? Gn * 32u : 0u, xs = okn ? 8u : 0u;
+      uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+#pragma unroll
+      for (int k = 0; k < SP; ++k) {
+        uint32_t e[8];
+        decode8<true>(sc, sc_off, jmax, pd, e);
+        uint4 wv;
+        wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
+        wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
+        wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
+        wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
+                                                      __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
+        rw[k] = *reinterpret_cast<const uint2*>(rp + k * rs);
+        xv[k] = *reinterpret_cast<const uint4*>(xp + k * xs);
+      }
+      wait_lgkm0();
+      wave_sync_lds();
+      pos2 = pos2n;
+      // the next group's words go in now, unless this was the wave's last
+      // group of the row block (the columns first carry the row block's sum)
+      if (okn && rb_of(tn) == rb) {
+        stream_store<JT>(cols, sw, lane);
+        wait_lgkm0();
+        wave_sync_lds();
+      }
+    }
+    // End of the row block: add the waves' accumulators in a fixed order
+    // (LDS-only barriers: the loads in flight stay in flight).
+    block_sync_lds();
+    float* red = reinterpret_cast<float*>(cols);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red[v * 64 + lane] = acc[v];
+    acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    block_sync_lds();
+    if (wave < 4) {
+      const uint32_t v = wave;
+      float sum = 0.f;
+      for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + w * kBuf)[v * 64 + lane];
+      if (i < p.B && 4 * q + v < G) p.y[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
+    }
+    block_sync_lds();
+    stream_store<JT>(cols, sw, lane);  // the next group's words, held back for the sum
+    wait_lgkm0();
+    wave_sync_lds();
+  }
+  wait_vm0();  // prefetches past the last group
+}
+
 // ------------------------------------------------------------------ bf16 GEMV
 
 // One wave per row; lanes stride the row in 8-weight chunks; dot2 on pairs.
@@ -958,6 +1190,24 @@ static hl_status launch_gemv_b(bool xbf16, dim3 grid, dim3 block, size_t lds, hi
                                const GemvArgs& p) {
   return xbf16 ? launch(gemv_kernel<B, true>, grid, block, lds, s, p)
                : launch(gemv_kernel<B, false>, grid, block, lds, s, p);
+}
+
+// Stream words per lane the persistent kernel is built for (the smallest one
+// not below the tensor's longest segment is used).
+static int stream_rows_for(uint32_t col_rows) {
+  static const int kJT[] = {12, 16, 20};
+  for (int jt : kJT)
+    if ((uint32_t)jt >= col_rows - 1) return jt;
+  return 0;
+}
+
+static hl_status launch_stream(int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s, const GemvArgs& p) {
+  switch (jt) {
+    case 12: return launch(gemv_stream_kernel<12>, grid, block, lds, s, p);
+    case 16: return launch(gemv_stream_kernel<16>, grid, block, lds, s, p);
+    case 20: return launch(gemv_stream_kernel<20>, grid, block, lds, s, p);
+    default: return HL_EUNSUPPORTED;
+  }
 }
 
 // Segment lengths with a matrix-core instantiation (S = 8 * steps).
@@ -1095,10 +1345,25 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   p.y = y_dev;
   p.x_words = mfma ? 0 : x_words;
   p.B = batch;
+  const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
+  const uint32_t cus = (uint32_t)device_cus();
+  // Persistent double-buffered kernel: S = 64, at least one row block per CU
+  // and two groups per wave.
+  if (mfma && t->seg_len == 64) {
+    const int jt = stream_rows_for(pl.ga.col_rows);
+    const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
+    const size_t per_wave = (size_t)(jt + 1) * kCol * 4;
+    uint32_t w = kMaxWaves;
+    while (w > 1 && tab + w * per_wave > kMaxLds) --w;
+    if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
+      p.C = CB;
+      p.KS = 1;
+      return launch_stream(jt, dim3(std::min(RB, cus)), dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
+    }
+  }
   // Column blocks per block: enough blocks to fill the device, each wave
   // decoding at least one group; KS blocks share a row block.
-  const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
-  const uint64_t target_waves = (uint64_t)device_cus() * 16;
+  const uint64_t target_waves = (uint64_t)cus * 16;
   const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * CB + target_waves - 1) / target_waves);
   uint32_t C = std::min<uint32_t>(CB, pl.waves * gpw);
   uint32_t KS = (CB + C - 1) / C;
