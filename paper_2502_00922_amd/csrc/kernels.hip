@@ -915,7 +915,7 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
 
 // ------------------------------------------------------------------ persistent fused GEMV
 
-// Persistent form of the matrix-core kernel for S = 64 and matrices with at
+// Persistent form of the matrix-core kernel for S = 8*SP (SP = 4 or 8) and matrices with at
 // least one 16-row block per block of the grid and at least as many column
 // blocks as waves. Block b takes row blocks b, b + grid, ...; its waves take
 // the row block's column blocks wave, wave + waves, ... The table is copied
@@ -929,9 +929,8 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
 // wait the compiler places is exact. At a row block's end the waves add their
 // accumulators through their columns in a fixed order (before the next
 // group's words go in) and four waves write y.
-template <int JT>
+template <int SP, int JT>
 __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
-  constexpr int SP = 8;
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
@@ -1193,19 +1192,30 @@ static hl_status launch_gemv_b(bool xbf16, dim3 grid, dim3 block, size_t lds, hi
 }
 
 // Stream words per lane the persistent kernel is built for (the smallest one
-// not below the tensor's longest segment is used).
-static int stream_rows_for(uint32_t col_rows) {
-  static const int kJT[] = {12, 16, 20};
-  for (int jt : kJT)
-    if ((uint32_t)jt >= col_rows - 1) return jt;
+// not below the tensor's longest segment is used), per segment length.
+static int stream_rows_for(uint32_t seg_len, uint32_t col_rows) {
+  static const int kJT64[] = {12, 16, 20}, kJT32[] = {8, 12};
+  if (seg_len != 64 && seg_len != 32) return 0;
+  const int* set = seg_len == 64 ? kJT64 : kJT32;
+  const int n = seg_len == 64 ? 3 : 2;
+  for (int k = 0; k < n; ++k)
+    if ((uint32_t)set[k] >= col_rows - 1) return set[k];
   return 0;
 }
 
-static hl_status launch_stream(int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s, const GemvArgs& p) {
+static hl_status launch_stream(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               const GemvArgs& p) {
+  if (seg_len == 64) {
+    switch (jt) {
+      case 12: return launch(gemv_stream_kernel<8, 12>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20>, grid, block, lds, s, p);
+      default: return HL_EUNSUPPORTED;
+    }
+  }
   switch (jt) {
-    case 12: return launch(gemv_stream_kernel<12>, grid, block, lds, s, p);
-    case 16: return launch(gemv_stream_kernel<16>, grid, block, lds, s, p);
-    case 20: return launch(gemv_stream_kernel<20>, grid, block, lds, s, p);
+    case 8: return launch(gemv_stream_kernel<4, 8>, grid, block, lds, s, p);
+    case 12: return launch(gemv_stream_kernel<4, 12>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
 }
@@ -1347,10 +1357,10 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   p.B = batch;
   const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
   const uint32_t cus = (uint32_t)device_cus();
-  // Persistent double-buffered kernel: S = 64, at least one row block per CU
-  // and two groups per wave.
-  if (mfma && t->seg_len == 64) {
-    const int jt = stream_rows_for(pl.ga.col_rows);
+  // Persistent kernel: S = 32 or 64, at least one row block per CU and two
+  // groups per wave.
+  if (mfma && (t->seg_len == 64 || t->seg_len == 32)) {
+    const int jt = stream_rows_for(t->seg_len, pl.ga.col_rows);
     const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
     const size_t per_wave = (size_t)(jt + 1) * kCol * 4;
     uint32_t w = kMaxWaves;
@@ -1358,7 +1368,8 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
       p.C = CB;
       p.KS = 1;
-      return launch_stream(jt, dim3(std::min(RB, cus)), dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
+      return launch_stream(t->seg_len, jt, dim3(std::min(RB, cus)), dim3(w * 64), w * per_wave, (hipStream_t)stream,
+                           p);
     }
   }
   // Column blocks per block: enough blocks to fill the device, each wave

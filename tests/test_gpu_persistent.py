@@ -1,0 +1,68 @@
+"""The persistent matrix-core decode-GEMV (chosen for 16-row groups at S = 32
+or 64 when a matrix has at least one row block per CU and two groups per wave:
+on a 256-CU MI355X, 4100 rows and 8192 (S = 64) or 4096 (S = 32) columns).
+
+The rows leave a ragged last row block (4 rows). Three weight distributions
+give short, typical and long codes, so that the kernel's instantiations for
+different stream lengths all run:
+* constant exponents (both fields single-symbol: no stream bits at all);
+* N(0, 0.02) with outliers (the workloads' distribution);
+* log-uniform magnitudes over 2^-60 .. 2^60 (long codes).
+Outputs: every row against a float64 product of the exact bf16 values, and
+sampled rows against the oracle's exactly rounded sums, at batch 1, 5 and 16.
+"""
+import numpy as np
+import pytest
+
+from gen import f32_to_bf16_bits, random_bf16, random_x
+from oracle import gemv as ogemv
+from oracle.gemv import bf16_to_f64
+
+hl = pytest.importorskip("paper_2502_00922_amd.hufflm")
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = pytest.importorskip("torch")
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def _weights(kind, rows, cols, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "constant_exponent":
+        v = (1.0 + 0.96 * rng.random((rows, cols), dtype=np.float32)) * np.where(rng.random((rows, cols)) < 0.5, -1, 1)
+        return f32_to_bf16_bits(v.astype(np.float32))
+    if kind == "gaussian":
+        return random_bf16((rows, cols), seed=seed)
+    mag = np.exp2(rng.uniform(-60, 60, (rows, cols))).astype(np.float32)
+    return f32_to_bf16_bits(mag * np.where(rng.random((rows, cols)) < 0.5, -1, 1).astype(np.float32))
+
+
+@pytest.mark.parametrize("S,cols", [(64, 8192), (32, 4096)])
+@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform"])
+def test_persistent_kernel(torch, S, cols, kind):
+    rows = 4100
+    print(f"persistent S={S} {rows}x{cols} {kind}", flush=True)
+    W = _weights(kind, rows, cols, seed=S + cols)
+    dt = hl.DeviceTensor(hl.encode(W, seg_len=S))
+    assert dt.view.grp_rows == 16
+    Wf = bf16_to_f64(W)
+    rng = np.random.default_rng(S)
+    sample = sorted({0, 15, 16, rows - 5, rows - 4, rows - 1} | set(int(r) for r in rng.integers(0, rows, 10)))
+    for B in (1, 5, 16):
+        xs = random_x(B, cols, seed=B, dtype="bf16")
+        x = torch.from_numpy(xs.view(np.int16)).cuda().view(torch.bfloat16)
+        y = dt.gemv(x).cpu().numpy().astype(np.float64)
+        Xf = bf16_to_f64(xs)
+        ref = Xf @ Wf.T
+        den = np.abs(Xf) @ np.abs(Wf).T
+        err = np.abs(y - ref) / (den + 1e-30)
+        assert err.max() <= TOL, (B, float(err.max()), int(np.argmax(err.max(0))))
+        yo, do = ogemv.gemv_rows(W, xs, rows=sample)
+        assert (np.abs(y[:, sample] - yo) / (do + 1e-30)).max() <= TOL
+    torch.cuda.synchronize()
