@@ -38,6 +38,15 @@ Container layout (little-endian; sections start at 64-byte boundaries):
   segments concatenated in mu order), raw u8[n] (sign<<7 | mantissa; group g's
   bytes start at S times the number of segments before it; weight t of
   segment mu at ((t // 8) * N + mu) * 8 + t % 8, N = G*GC).
+
+Whole-exponent variant (header flags = 1): the 8 exponent bits of a weight
+are one symbol of a single per-matrix 256-symbol Huffman code (the {1,8,7}
+split; Sec. 3.1 weighs the size of the symbol alphabet against the cost of a
+single-cycle CAM match, which a table lookup in local memory does not pay).
+Code lengths are limited to lmax in [8, 13]; the 256 lengths are stored in a
+256-byte section right after the header. Tiling, stream order (one code per
+weight, MSB-first, packed LSB-first), group padding and the raw plane are
+those of the split format.
 """
 from __future__ import annotations
 
@@ -57,6 +66,11 @@ RAW_UNIT = 8                # bytes of one segment's raw plane stored contiguous
 UNIT_BYTES = 16             # group streams are padded to 128 bits
 SECTION_ALIGN = 64
 NSYM = 16                   # both exponent groups are 4-bit symbols
+NSYM8 = 256                 # the whole exponent as one symbol
+FLAG_SPLIT = 0              # header flags: two 4-bit exponent codes
+FLAG_WHOLE_EXPONENT = 1     # header flags: one 8-bit exponent code
+LEN8_BYTES = 256            # whole-exponent code lengths, after the header
+LMAX8_MIN, LMAX8_MAX = 8, 13
 
 
 # --------------------------------------------------------------------------
@@ -271,13 +285,14 @@ def default_grp_rows(cols: int, seg_len: int) -> int:
     return GROUP_SEGS
 
 
-def layout(rows: int, cols: int, seg_len: int, grp_rows: int = GROUP_SEGS) -> Dict[str, int]:
+def layout(rows: int, cols: int, seg_len: int, grp_rows: int = GROUP_SEGS,
+           flags: int = FLAG_SPLIT) -> Dict[str, int]:
     n = rows * cols
     n_seg = n // seg_len
     L = cols // seg_len
     GC = GROUP_SEGS // grp_rows
     n_grp = (rows + grp_rows - 1) // grp_rows * (L // GC)
-    off_seg_bits = HEADER_BYTES
+    off_seg_bits = _align(HEADER_BYTES + (LEN8_BYTES if flags == FLAG_WHOLE_EXPONENT else 0))
     off_grp_off = _align(off_seg_bits + 2 * n_seg)
     off_stream = _align(off_grp_off + 4 * (n_grp + 1))
     return dict(n=n, n_seg=n_seg, n_grp=n_grp, L=L, GC=GC, off_seg_bits=off_seg_bits,
@@ -297,10 +312,14 @@ def group_geometry(rows: int, cols: int, seg_len: int, g: int,
     return r0, G, cb * GC, r0 * L + cb * GC * G, GC
 
 
-def check_shape(rows: int, cols: int, seg_len: int, lmax: int, grp_rows: int = GROUP_SEGS) -> None:
+def check_shape(rows: int, cols: int, seg_len: int, lmax: int, grp_rows: int = GROUP_SEGS,
+                flags: int = FLAG_SPLIT) -> None:
     if rows < 1 or cols < 1:
         raise ValueError("empty matrix")
-    if not (4 <= lmax <= 15):
+    if flags == FLAG_WHOLE_EXPONENT:
+        if not (LMAX8_MIN <= lmax <= LMAX8_MAX):
+            raise ValueError("lmax must be in [8, 13] for the whole-exponent code")
+    elif not (4 <= lmax <= 15):
         raise ValueError("lmax must be in [4, 15]")
     if seg_len < 8 or seg_len > 512 or seg_len % 8 or cols % seg_len:
         raise ValueError("segment length must be a multiple of 8 in [8, 512] dividing cols")
@@ -355,9 +374,23 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
     check_shape(rows, cols, seg_len, lmax, GR)
     ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
-    lay = layout(rows, cols, seg_len, GR)
+    _, eh, el, _ = split_fields(w)
+
+    def seg_stream(r, a, S):
+        return segment_stream(eh[r, a:a + S].tolist(), el[r, a:a + S].tolist(), ceh, cel)
+
+    def header(*geo):
+        return pack_header(rows, cols, seg_len, lmax, GR, *geo, ceh, cel)
+
+    return _assemble(w, seg_len, GR, FLAG_SPLIT, seg_stream, header, b"")
+
+
+def _assemble(w, seg_len, GR, flags, seg_stream, header, codebook_section) -> bytes:
+    """Container bytes from a per-segment stream function (both formats)."""
+    rows, cols = w.shape
+    lay = layout(rows, cols, seg_len, GR, flags)
     n, n_seg, n_grp = lay["n"], lay["n_seg"], lay["n_grp"]
-    s, eh, el, m = split_fields(w)                       # [rows, cols] each
+    s, _, _, m = split_fields(w)
     S = seg_len
 
     seg_bits = np.zeros(n_seg, dtype=np.uint16)
@@ -369,9 +402,7 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
         r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
         gacc, gpos = 0, 0
         for mu in range(G * GC):
-            r = r0 + mu % G
-            a = (c0 + mu // G) * S
-            acc, nb = segment_stream(eh[r, a:a + S].tolist(), el[r, a:a + S].tolist(), ceh, cel)
+            acc, nb = seg_stream(r0 + mu % G, (c0 + mu // G) * S, S)
             seg_bits[first + mu] = nb
             gacc |= acc << gpos
             gpos += nb
@@ -390,9 +421,9 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     raw[raw_pos(rr.ravel(), cc.ravel(), rows, cols, S, GR)] = raw_byte(s, m).ravel()
 
     out = bytearray(total)
-    out[0:HEADER_BYTES] = pack_header(rows, cols, seg_len, lmax, GR, n_seg, n_grp, lay["off_seg_bits"],
-                                      lay["off_grp_off"], lay["off_stream"], off_raw, total,
-                                      max_units, ceh, cel)
+    out[0:HEADER_BYTES] = header(n_seg, n_grp, lay["off_seg_bits"], lay["off_grp_off"],
+                                 lay["off_stream"], off_raw, total, max_units)
+    out[HEADER_BYTES:HEADER_BYTES + len(codebook_section)] = codebook_section
     out[lay["off_seg_bits"]:lay["off_seg_bits"] + 2 * n_seg] = seg_bits.tobytes()
     out[lay["off_grp_off"]:lay["off_grp_off"] + 4 * (n_grp + 1)] = grp_off.tobytes()
     out[lay["off_stream"]:lay["off_stream"] + len(stream)] = stream
@@ -400,12 +431,80 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     return bytes(out)
 
 
+# --------------------------------------------------------------------------
+# Whole-exponent variant (flags = 1)
+# --------------------------------------------------------------------------
+
+def exponent_byte(w: np.ndarray) -> np.ndarray:
+    """The 8-bit biased exponent of bf16 bit patterns (Sec. 2.1, Eq. 1)."""
+    return (np.asarray(w, dtype=np.uint16).astype(np.uint32) >> 7) & 0xFF
+
+
+def build_codebook8(w: np.ndarray, lmax: int = 12) -> FieldCode:
+    """Per-matrix 256-symbol code of the whole exponent, lengths <= lmax."""
+    if not (LMAX8_MIN <= lmax <= LMAX8_MAX):
+        raise ValueError("lmax must be in [8, 13] for the whole-exponent code")
+    return FieldCode.from_freqs(histogram(exponent_byte(w), NSYM8), lmax)
+
+
+def segment_stream8(e_seg, code: FieldCode) -> Tuple[int, int]:
+    """Bit stream of one segment, one code per weight, each MSB-first; stream
+    bit k is bit k of the integer."""
+    acc = 0
+    pos = 0
+    for e in e_seg:
+        l = code.lengths[e] if code.nsym > 1 else 0
+        acc |= bit_reverse(code.codes[e], l) << pos
+        pos += l
+    return acc, pos
+
+
+def encode8(w: np.ndarray, seg_len: int, lmax: int = 12, codebook: FieldCode = None,
+            grp_rows: int = None) -> bytes:
+    """Compress a bf16 matrix into an HLF1 container of the whole-exponent format."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    rows, cols = w.shape
+    GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
+    check_shape(rows, cols, seg_len, lmax, GR, FLAG_WHOLE_EXPONENT)
+    code = codebook if codebook is not None else build_codebook8(w, lmax)
+    if code.nsym > 1 and (max(code.lengths) > lmax or len(code.lengths) != NSYM8):
+        raise ValueError("codebook does not fit lmax")
+    e = exponent_byte(w)
+    for v in np.unique(e).tolist():
+        if (code.lengths[v] == 0) if code.nsym > 1 else (v != code.single):
+            raise ValueError("exponent without a code")
+
+    def seg_stream(r, a, S):
+        return segment_stream8(e[r, a:a + S].tolist(), code)
+
+    def header(n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units):
+        return struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, FLAG_WHOLE_EXPONENT, rows, cols, seg_len, GR,
+                           n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units,
+                           code.nsym & 0xFF, code.nsym >> 8, code.single, 0, bytes(16), bytes(16))
+
+    lens = bytes(code.lengths) if code.nsym > 1 else bytes(NSYM8)
+    return _assemble(w, seg_len, GR, FLAG_WHOLE_EXPONENT, seg_stream, header, lens)
+
+
+def header_codebook8(h) -> FieldCode:
+    return FieldCode(h["len8"], h["nsym8"], h["single8"])
+
+
+def container_size8(w: np.ndarray, seg_len: int, lmax: int = 12, codebook: FieldCode = None,
+                    grp_rows: int = None) -> Dict[str, int]:
+    """Exact size of ``encode8(w, ...)`` from the code lengths alone."""
+    w = np.asarray(w, dtype=np.uint16)
+    code = codebook if codebook is not None else build_codebook8(w, lmax)
+    le = np.array(code.lengths if code.nsym > 1 else [0] * NSYM8, dtype=np.int64)
+    return _size_from_bits(le[exponent_byte(w)], w.shape, seg_len, lmax, grp_rows, FLAG_WHOLE_EXPONENT)
+
+
 HEADER_FMT = "<IHBBQQIIQQQQQQQIBBBB16s16s"
 
 
 def pack_header(rows, cols, seg_len, lmax, grp_rows, n_seg, n_grp, off_sb, off_go, off_st, off_raw, total,
                 max_units, ceh: FieldCode, cel: FieldCode) -> bytes:
-    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, 0, rows, cols, seg_len, grp_rows,
+    h = struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, FLAG_SPLIT, rows, cols, seg_len, grp_rows,
                     n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units,
                     ceh.nsym, cel.nsym, ceh.single, cel.single,
                     bytes(ceh.lengths), bytes(cel.lengths))
@@ -423,6 +522,13 @@ def parse_header(blob: bytes) -> Dict[str, object]:
     h["el_len"] = list(h["el_len"])
     if h["magic"] != MAGIC or h["version"] != VERSION:
         raise ValueError("not an HLF1 container")
+    if h["flags"] == FLAG_WHOLE_EXPONENT:
+        # bytes 92..93: u16 symbol count; byte 94: the symbol when it is the only one
+        h["nsym8"] = h["eh_nsym"] | (h["el_nsym"] << 8)
+        h["single8"] = h["eh_single"]
+        h["len8"] = list(blob[HEADER_BYTES:HEADER_BYTES + LEN8_BYTES])
+    elif h["flags"] != FLAG_SPLIT:
+        raise ValueError("unknown format flags")
     return h
 
 
@@ -436,7 +542,11 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
 
     Returns (first row r0, rows G, first column segment, GC, uint16[G, GC*S])."""
     h = parse_header(blob)
-    ceh, cel = header_codebooks(h)
+    whole = h["flags"] == FLAG_WHOLE_EXPONENT
+    if whole:
+        code8 = header_codebook8(h)
+    else:
+        ceh, cel = header_codebooks(h)
     rows, cols, S, GR = h["rows"], h["cols"], h["seg_len"], h["grp_rows"]
     seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
     grp_off = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
@@ -453,8 +563,12 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
         eh = np.zeros(S, np.uint32)
         el = np.zeros(S, np.uint32)
         for t in range(S):
-            el[t], pos = cel.decode_one(bits, pos)
-            eh[t], pos = ceh.decode_one(bits, pos)
+            if whole:                       # one 8-bit symbol: eh, el are its nibbles
+                e, pos = code8.decode_one(bits, pos)
+                eh[t], el[t] = e >> 4, e & 15
+            else:
+                el[t], pos = cel.decode_one(bits, pos)
+                eh[t], pos = ceh.decode_one(bits, pos)
         if pos - start != int(seg_bits[first + mu]):
             raise ValueError("segment length mismatch")
         cols_of = (c0 + j) * S + np.arange(S)
@@ -490,16 +604,21 @@ def container_size(w: np.ndarray, seg_len: int, lmax: int = 12,
     code lengths alone (sum of code lengths per segment, 128-bit padding per
     group, section alignment), without building the stream."""
     w = np.asarray(w, dtype=np.uint16)
-    rows, cols = w.shape
-    GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
-    check_shape(rows, cols, seg_len, lmax, GR)
     ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
     _, eh, el, _ = split_fields(w)
     le = np.array(ceh.lengths if ceh.nsym > 1 else [0] * NSYM, dtype=np.int64)
     ll = np.array(cel.lengths if cel.nsym > 1 else [0] * NSYM, dtype=np.int64)
+    return _size_from_bits(le[eh] + ll[el], w.shape, seg_len, lmax, grp_rows, FLAG_SPLIT)
+
+
+def _size_from_bits(bits, shape, seg_len, lmax, grp_rows, flags) -> Dict[str, int]:
+    """Container size from the code bits of every weight ([rows, cols])."""
+    rows, cols = shape
+    GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
+    check_shape(rows, cols, seg_len, lmax, GR, flags)
     L = cols // seg_len
     GC = GROUP_SEGS // GR
-    seg = (le[eh] + ll[el]).reshape(rows, L, seg_len).sum(axis=2)       # [rows, L]
+    seg = bits.reshape(rows, L, seg_len).sum(axis=2)                      # [rows, L]
     units = 0
     max_units = 0
     for rb in range(0, rows, GR):
@@ -508,7 +627,7 @@ def container_size(w: np.ndarray, seg_len: int, lmax: int = 12,
         u = (per_grp + 127) // 128
         units += int(u.sum())
         max_units = max(max_units, int(u.max()))
-    lay = layout(rows, cols, seg_len, GR)
+    lay = layout(rows, cols, seg_len, GR, flags)
     off_raw = _align(lay["off_stream"] + units * UNIT_BYTES)
     return dict(total_bytes=off_raw + rows * cols, stream_units=units, max_grp_units=max_units,
                 code_bits=int(seg.sum()), off_raw=off_raw, grp_rows=GR)
