@@ -58,6 +58,9 @@ def parse():
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the launches the byte-counter passes measure")
     ap.add_argument("--no-graph", action="store_true", help="time individual launches instead of graph replays")
+    ap.add_argument("--format", choices=["split", "whole"], default="split",
+                    help="container of the headline: split exponent (two 4-bit codes) or whole exponent")
+    ap.add_argument("--no-variant", action="store_true", help="skip timing the other container format")
     return ap.parse_args()
 
 
@@ -153,6 +156,41 @@ def cpu_oracle_baseline(blob: bytes, W, x, seconds: float):
                        f"bit-serial decode + fp64 products, {dt:.1f} s, single-threaded Python")
 
 
+def measure_container(torch, hl, blob, spec, W, batches, args, single_launches):
+    """Times the fused decode-GEMV of one container at each batch size over
+    replicas of it that together exceed the last-level cache; checks sampled
+    outputs of the timed launches against the oracle."""
+    from gen import gen_x
+    from oracle import gemv as ogemv
+    R, K = spec.rows, spec.cols
+    nrep = max(2, math.ceil(COLD_BYTES / blob.size))
+    tensors = [hl.DeviceTensor(blob) for _ in range(nrep)]
+    torch.cuda.synchronize()
+    results = {}
+    for batch in batches:
+        xb = gen_x(spec, batch, "bf16")
+        xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+        y = torch.empty((batch, R), dtype=torch.float32, device="cuda")
+
+        def launch(i, xd=xd, y=y):
+            tensors[i].gemv(xd, y)
+
+        if single_launches or args.no_graph:
+            mean_ms, med_ms, ev_step_ms = time_launches(torch, launch, nrep, args.steps, args.warmup)
+        else:
+            mean_ms = med_ms = ev_step_ms = None
+        step_ms = ev_step_ms if args.no_graph else time_graph(torch, launch, nrep, args.steps, args.warmup)
+        rows = list(range(0, R, R // 16))
+        y_ref, den = ogemv.gemv_rows(W, xb, rows=rows)
+        err = float(np.max(ogemv.rel_err(y.cpu().numpy()[:, rows], y_ref, den)))
+        alg_bytes = blob.size + K * batch * 2 + R * batch * 4
+        results[batch] = dict(mean_ms=mean_ms, med_ms=med_ms, step_ms=step_ms, ev_step_ms=ev_step_ms,
+                              alg_bytes=alg_bytes, max_rel_err=err)
+    seg_len = int(tensors[0].view.seg_len)
+    del tensors
+    return results, seg_len
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -171,13 +209,13 @@ def main():
     R, K = spec.rows, spec.cols
     n = R * K
     W = gen_matrix(spec)
-    blob = hl.encode(W)
+    blobs = {f: hl.encode(W, whole_exponent=(f == "whole")) for f in ("split", "whole")}
+    blob = blobs[args.format]
     blob_b = bytes(blob)
     nrep = max(2, math.ceil(COLD_BYTES / blob.size))
-    tensors = [hl.DeviceTensor(blob) for _ in range(nrep)]
-    torch.cuda.synchronize()
 
     if args.traffic_run:
+        tensors = [hl.DeviceTensor(blob) for _ in range(nrep)]
         xb = gen_x(spec, 1, "bf16")
         xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
         y = torch.empty((1, R), dtype=torch.float32, device="cuda")
@@ -188,30 +226,27 @@ def main():
         for _ in range(10):
             dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"traffic_run": True, "kernel_sha256_16": kernel_hash(), "fused_launches": 100,
-                          "fused_alg_bytes": int(blob.size + K * 2 + R * 4), "copy_bytes": COPY_BYTES,
-                          "copies": 10}), flush=True)
+        print(json.dumps({"traffic_run": True, "format": args.format, "kernel_sha256_16": kernel_hash(),
+                          "fused_launches": 100, "fused_alg_bytes": int(blob.size + K * 2 + R * 4),
+                          "copy_bytes": COPY_BYTES, "copies": 10}), flush=True)
         return
 
-    results = {}
-    for batch in sorted({args.batch, 4} if args.batch == 1 else {args.batch}):
-        xb = gen_x(spec, batch, "bf16")
-        xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
-        y = torch.empty((batch, R), dtype=torch.float32, device="cuda")
-
-        def launch(i, xd=xd, y=y):
-            tensors[i].gemv(xd, y)
-
-        mean_ms, med_ms, ev_step_ms = time_launches(torch, launch, nrep, args.steps, args.warmup)
-        step_ms = ev_step_ms if args.no_graph else time_graph(torch, launch, nrep, args.steps, args.warmup)
-        # spot check of the timed output against the oracle on a few rows
-        from oracle import gemv as ogemv
-        rows = list(range(0, R, R // 16))
-        y_ref, den = ogemv.gemv_rows(W, xb, rows=rows)
-        err = float(np.max(ogemv.rel_err(y.cpu().numpy()[:, rows], y_ref, den)))
-        alg_bytes = blob.size + K * batch * 2 + R * batch * 4
-        results[batch] = dict(mean_ms=mean_ms, med_ms=med_ms, step_ms=step_ms, ev_step_ms=ev_step_ms,
-                              alg_bytes=alg_bytes, max_rel_err=err)
+    batches = sorted({args.batch, 4} if args.batch == 1 else {args.batch})
+    results, seg_len = measure_container(torch, hl, blob, spec, W, batches, args, single_launches=True)
+    variant = None
+    if not args.no_variant:
+        other = "whole" if args.format == "split" else "split"
+        vres, _ = measure_container(torch, hl, blobs[other], spec, W, batches, args, single_launches=False)
+        variant = {"format": other, "compressed_bytes": int(blobs[other].size),
+                   "compression_ratio": round(2 * n / blobs[other].size, 4),
+                   "bits_per_weight": round(8 * blobs[other].size / n, 4)}
+        for b, rr in vres.items():
+            variant[f"batch{b}"] = dict(
+                ms_per_step=round(rr["step_ms"], 5),
+                compressed_GBps=round(rr["alg_bytes"] / (rr["step_ms"] * 1e-3) / 1e9, 1),
+                effective_GBps=round(2 * n / (rr["step_ms"] * 1e-3) / 1e9, 1),
+                max_rel_err=rr["max_rel_err"])
+    torch.cuda.synchronize()
 
     cmp = {}
     if not args.no_compare:
@@ -255,6 +290,8 @@ def main():
                      torch_linear_ms=round(cmp[b]["torch_linear_ms"], 5),
                      speedup_vs_best_bf16=round(best / rr["step_ms"], 3))
         extra[f"batch{b}"] = e
+    if variant is not None:
+        extra["variant"] = variant
     out = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -270,7 +307,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": "4096x4096 bf16 projection, per-row LogNormal(0,0.3) scale, "
                                "N(0,0.02) + 0.1% outliers x20, seed 0; fused decode-GEMV",
-                   "rows": R, "cols": K, "batch": b0, "x_dtype": "bf16", "seg_len": int(tensors[0].view.seg_len),
+                   "rows": R, "cols": K, "batch": b0, "x_dtype": "bf16", "seg_len": seg_len,
+                   "format": "split exponent (4+4)" if args.format == "split" else "whole exponent (8)",
                    "compressed_bytes": int(blob.size), "compression_ratio": round(2 * n / blob.size, 4),
                    "bits_per_weight": round(8 * blob.size / n, 4), "replicas": nrep},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -53,11 +53,23 @@
  *                 segment number; weight t of segment mu is at ((t/8)*N + mu)*8
  *                 + t%8 within the group
  *   total_bytes = off_raw + n
- * Header: u32 magic 0x31464C48 ('HLF1'), u16 version 1, u8 lmax, u8 flags 0,
+ * Header: u32 magic 0x31464C48 ('HLF1'), u16 version 1, u8 lmax, u8 flags,
  *   u64 rows, u64 cols, u32 seg_len, u32 group_rows (GR), u64 n_seg,
  *   u64 n_grp, u64 off_seg_bits, u64 off_grp_off, u64 off_stream,
  *   u64 off_raw, u64 total_bytes, u32 max_grp_units, u8 eh_nsym, u8 el_nsym,
  *   u8 eh_single, u8 el_single, u8 eh_len[16], u8 el_len[16].
+ *
+ * flags 0 is the split format above. flags 1 is the whole-exponent format:
+ * the exponent byte e = (w>>7)&255 is one symbol of a single per-matrix code
+ * over 256 symbols (the same Huffman, package-merge and canonical rules, with
+ * lmax in [8, 13]), and the stream holds code(e) for each weight of a segment
+ * in order, most-significant bit first. Its 256 code lengths (u8, indexed by
+ * e) follow the header at byte 128, so off_seg_bits = 384. Header bytes
+ * 92..93 hold the u16 count of present exponent values, byte 94 the value
+ * when it is the only one (else 0), bytes 95..127 are zero. Everything else
+ * (tiling, padding, offsets, raw plane) is as in the split format. The split
+ * follows the paper's split-size analysis (Sec. 3.1): an 8-bit symbol is
+ * costly for a single-cycle CAM match, not for a table lookup in local memory.
  *
  * ---------------------------------------------------------------------------
  * Conventions of the ABI
@@ -98,6 +110,11 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
 #define HL_GROUP_SEGS 64u
 #define HL_MAX_BATCH 16u
 #define HL_LUT_BYTES 33024u   /* 8192 joint entries + 64 words of tables */
+#define HL_LEN8_BYTES 256u    /* whole-exponent code lengths after the header */
+#define HL_LMAX8_MIN 8u
+#define HL_LMAX8_MAX 13u
+
+typedef enum { HL_FORMAT_SPLIT = 0, HL_FORMAT_WHOLE_EXPONENT = 1 } hl_format;
 
 typedef struct {
   uint8_t nsym;     /* symbols present in the field (1..16) */
@@ -111,14 +128,25 @@ typedef struct {
   hl_field_code el; /* exponent bits 3..0 */
 } hl_codebook;
 
+/* Whole-exponent code (format 1). */
+typedef struct {
+  uint32_t lmax;      /* code-length limit used to build the lengths, 8..13 */
+  uint16_t nsym;      /* exponent values present (1..256) */
+  uint8_t single;     /* the value when nsym == 1, else 0 */
+  uint8_t reserved;   /* 0 */
+  uint8_t len[256];   /* code length per exponent value; 0 = absent (or the only one) */
+} hl_codebook8;
+
 /* Non-owning view of one container resident in device memory. */
 typedef struct {
   const uint8_t* blob_dev;   /* whole container */
   uint32_t* lut_dev;         /* HL_LUT_BYTES, filled by hl_tensor_prepare */
   uint64_t rows, cols, n_seg, n_grp, total_bytes;
   uint64_t off_seg_bits, off_grp_off, off_stream, off_raw;
-  uint32_t seg_len, grp_rows, lmax, max_grp_units, max_seg_bits, reserved;
+  uint32_t seg_len, grp_rows, lmax, max_grp_units, max_seg_bits;
+  uint32_t format;           /* hl_format: which of cb / cb8 is in use (the other is zero) */
   hl_codebook cb;
+  hl_codebook8 cb8;
 } hl_tensor;
 
 /* Text of a status code (static storage). */
@@ -154,6 +182,20 @@ hl_status hl_encode(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,
                     const hl_codebook* cb, uint32_t seg_len, uint32_t grp_rows,
                     uint32_t nthreads, void* out, size_t* out_bytes);
 
+/* Whole-exponent code (format 1) of n bf16 bit patterns: one code over the
+ * 256 exponent values (the 8-bit symbols of the split-size analysis,
+ * Sec. 3.1), built by the same rules as hl_build_codebook. lmax in [8, 13]
+ * (the decode table's 13-bit window then matches every code in one lookup).
+ * Errors: HL_EINVAL for n == 0, null pointers or lmax out of range. */
+hl_status hl_build_codebook8(const uint16_t* w_bf16, size_t n, uint32_t lmax,
+                             hl_codebook8* out);
+
+/* Encode W into an HLF1 container of the whole-exponent format (flags 1).
+ * Arguments, size query and errors as hl_encode. */
+hl_status hl_encode8(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,
+                     const hl_codebook8* cb, uint32_t seg_len, uint32_t grp_rows,
+                     uint32_t nthreads, void* out, size_t* out_bytes);
+
 /* Full structural check of a container held in host memory: header, section
  * offsets, codebooks (Kraft sum exactly 1, lengths <= lmax), per-group
  * stream sizes against seg_bits. O(n_seg). Returns HL_OK or HL_ECORRUPT. */
@@ -168,7 +210,9 @@ hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
 
 /* Fill t->lut_dev on the device: the joint decode table of the two codes for
  * a 13-bit window (the decoder's L_max-bit window match of Sec. 3.2) and the
- * per-length canonical tables used for pairs longer than the window. */
+ * per-length canonical tables used for pairs longer than the window. In the
+ * whole-exponent format the table decodes the one exponent code (never
+ * longer than the window) and the per-length tables are zero. */
 hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
 
 /* Decode the whole matrix to bf16 bit patterns, out_dev[rows*cols]

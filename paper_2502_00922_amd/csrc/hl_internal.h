@@ -24,16 +24,21 @@ uint32_t default_grp_rows(uint64_t cols, uint32_t S);
 
 struct Header {
   uint64_t rows, cols, n_seg, n_grp, off_seg_bits, off_grp_off, off_stream, off_raw, total_bytes;
-  uint32_t seg_len, grp_rows, max_grp_units;
-  hl_codebook cb;
+  uint32_t seg_len, grp_rows, max_grp_units, format, lmax;
+  hl_codebook cb;    // format 0 (zero otherwise)
+  hl_codebook8 cb8;  // format 1 (zero otherwise)
 };
 
 bool shape_ok(uint64_t rows, uint64_t cols, uint32_t S);
-Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR);
-bool parse_header(const uint8_t* h, Header* out);
+Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR, uint32_t format);
+// Reads the header and, in the whole-exponent format, the code-length section
+// (needs 384 bytes); false if the fixed fields are wrong or bytes too few.
+bool parse_header(const uint8_t* b, size_t bytes, Header* out);
 bool header_consistent(const Header& h, uint64_t blob_bytes);
 bool field_code_valid(const hl_field_code& fc, uint32_t lmax);
-void canonical_codes(const uint8_t len[16], uint32_t code[16]);
+bool code8_valid(const hl_codebook8& cb);
+// Canonical code values of n symbols with lengths <= 16 (RFC 1951 Sec. 3.2.2).
+void canonical_codes(const uint8_t* len, int n, uint32_t* code);
 uint32_t default_seg_len(uint64_t cols);
 // Full structural check of a host copy; fills the header and the longest
 // segment (in code bits).

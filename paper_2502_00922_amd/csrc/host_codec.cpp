@@ -22,10 +22,12 @@ namespace hl {
 // ---------------------------------------------------------------- code lengths
 
 // Huffman lengths with the heap order (weight, kind, id); see the header.
-static void huffman_lengths(const uint64_t f[16], uint8_t len[16]) {
+// f and len have n entries (16 for the exponent nibbles, 256 for the whole
+// exponent byte).
+static void huffman_lengths(const uint64_t* f, int n, uint8_t* len) {
   using Key = std::tuple<uint64_t, int, int>;  // weight, kind (0 leaf / 1 node), id
   std::priority_queue<Key, std::vector<Key>, std::greater<Key>> heap;
-  for (int s = 0; s < 16; ++s) {
+  for (int s = 0; s < n; ++s) {
     len[s] = 0;
     if (f[s]) heap.emplace(f[s], 0, s);
   }
@@ -55,37 +57,46 @@ static void huffman_lengths(const uint64_t f[16], uint8_t len[16]) {
 }
 
 // Package-merge lengths limited to lmax; see the header for the item order.
-static void package_merge(const uint64_t f[16], int lmax, uint8_t len[16]) {
-  struct Item { uint64_t w; int kind; std::array<uint8_t, 16> cnt; };
+// Requires at most 2^lmax present symbols.
+static void package_merge(const uint64_t* f, int n, int lmax, uint8_t* len) {
+  struct Item { uint64_t w; int kind; std::vector<uint8_t> cnt; };
   std::vector<std::pair<uint64_t, int>> present;
-  for (int s = 0; s < 16; ++s) {
+  for (int s = 0; s < n; ++s) {
     len[s] = 0;
     if (f[s]) present.emplace_back(f[s], s);
   }
   std::sort(present.begin(), present.end());
-  const size_t n = present.size();
-  if (n <= 1) return;
+  const size_t np = present.size();
+  if (np <= 1) return;
   std::vector<Item> leaves;
   for (auto& p : present) {
-    Item it{p.first, 0, {}};
+    Item it{p.first, 0, std::vector<uint8_t>(n, 0)};
     it.cnt[p.second] = 1;
-    leaves.push_back(it);
+    leaves.push_back(std::move(it));
   }
   std::vector<Item> cur = leaves;
   for (int round = 0; round < lmax - 1; ++round) {
     std::vector<Item> next = leaves;
     for (size_t i = 0; i + 1 < cur.size(); i += 2) {
-      Item pk{cur[i].w + cur[i + 1].w, 1, {}};
-      for (int s = 0; s < 16; ++s) pk.cnt[s] = (uint8_t)(cur[i].cnt[s] + cur[i + 1].cnt[s]);
-      next.push_back(pk);
+      Item pk{cur[i].w + cur[i + 1].w, 1, std::vector<uint8_t>(n)};
+      for (int s = 0; s < n; ++s) pk.cnt[s] = (uint8_t)(cur[i].cnt[s] + cur[i + 1].cnt[s]);
+      next.push_back(std::move(pk));
     }
     std::stable_sort(next.begin(), next.end(), [](const Item& a, const Item& b) {
       return a.w != b.w ? a.w < b.w : a.kind < b.kind;
     });
     cur.swap(next);
   }
-  for (size_t i = 0; i < 2 * (n - 1) && i < cur.size(); ++i)
-    for (int s = 0; s < 16; ++s) len[s] = (uint8_t)(len[s] + cur[i].cnt[s]);
+  for (size_t i = 0; i < 2 * (np - 1) && i < cur.size(); ++i)
+    for (int s = 0; s < n; ++s) len[s] = (uint8_t)(len[s] + cur[i].cnt[s]);
+}
+
+// Huffman lengths, replaced by package-merge lengths when longer than lmax.
+static void limited_lengths(const uint64_t* f, int n, int lmax, uint8_t* len) {
+  huffman_lengths(f, n, len);
+  int mx = 0;
+  for (int s = 0; s < n; ++s) mx = std::max(mx, (int)len[s]);
+  if (mx > lmax) package_merge(f, n, lmax, len);
 }
 
 static void field_code_from_counts(const uint64_t f[16], int lmax, hl_field_code* fc) {
@@ -94,23 +105,20 @@ static void field_code_from_counts(const uint64_t f[16], int lmax, hl_field_code
     if (f[s]) { ++nsym; single = s; }
   fc->nsym = (uint8_t)nsym;
   fc->single = (uint8_t)(nsym == 1 ? single : 0);
-  huffman_lengths(f, fc->len);
-  int mx = 0;
-  for (int s = 0; s < 16; ++s) mx = std::max(mx, (int)fc->len[s]);
-  if (mx > lmax) package_merge(f, lmax, fc->len);
+  limited_lengths(f, 16, lmax, fc->len);
 }
 
-void canonical_codes(const uint8_t len[16], uint32_t code[16]) {
+void canonical_codes(const uint8_t* len, int n, uint32_t* code) {
   int bl_count[17] = {0};
   uint32_t next_code[17] = {0};
-  for (int s = 0; s < 16; ++s)
+  for (int s = 0; s < n; ++s)
     if (len[s]) bl_count[len[s]]++;
   uint32_t c = 0;
   for (int bits = 1; bits <= 16; ++bits) {
     c = (c + (uint32_t)bl_count[bits - 1]) << 1;
     next_code[bits] = c;
   }
-  for (int s = 0; s < 16; ++s) code[s] = len[s] ? next_code[len[s]]++ : 0;
+  for (int s = 0; s < n; ++s) code[s] = len[s] ? next_code[len[s]]++ : 0;
 }
 
 static uint32_t bit_reverse(uint32_t v, int n) {
@@ -140,6 +148,26 @@ bool field_code_valid(const hl_field_code& fc, uint32_t lmax) {
   return cnt == fc.nsym && kraft == (1ull << 15);
 }
 
+// Whole-exponent code: as above over 256 symbols, lengths <= lmax in [8, 13].
+bool code8_valid(const hl_codebook8& cb) {
+  if (cb.lmax < HL_LMAX8_MIN || cb.lmax > HL_LMAX8_MAX || cb.reserved) return false;
+  if (cb.nsym < 1 || cb.nsym > 256) return false;
+  if (cb.nsym == 1) {
+    for (int s = 0; s < 256; ++s) if (cb.len[s]) return false;
+    return true;
+  }
+  if (cb.single != 0) return false;
+  int cnt = 0;
+  uint64_t kraft = 0;  // in units of 2^-15
+  for (int s = 0; s < 256; ++s) {
+    if (!cb.len[s]) continue;
+    if (cb.len[s] > cb.lmax) return false;
+    ++cnt;
+    kraft += 1ull << (15 - cb.len[s]);
+  }
+  return cnt == cb.nsym && kraft == (1ull << 15);
+}
+
 // ---------------------------------------------------------------- layout
 
 static uint64_t align64(uint64_t x) { return (x + 63) & ~uint64_t(63); }
@@ -160,7 +188,7 @@ uint32_t default_grp_rows(uint64_t cols, uint32_t S) {
   return HL_GROUP_SEGS;
 }
 
-Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR) {
+Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR, uint32_t format) {
   Layout L;
   L.n = rows * cols;
   L.n_seg = L.n / S;
@@ -168,22 +196,25 @@ Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR) {
   L.GR = GR;
   L.GC = HL_GROUP_SEGS / GR;
   L.n_grp = (rows + GR - 1) / GR * (L.L / L.GC);
-  L.off_seg_bits = HL_HEADER_BYTES;
+  L.off_seg_bits = align64(HL_HEADER_BYTES + (format == HL_FORMAT_WHOLE_EXPONENT ? HL_LEN8_BYTES : 0));
   L.off_grp_off = align64(L.off_seg_bits + 2 * L.n_seg);
   L.off_stream = align64(L.off_grp_off + 4 * (L.n_grp + 1));
   return L;
 }
 
-void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, const hl_codebook& cb,
-                 const Layout& L, uint64_t off_raw, uint64_t total, uint32_t max_units) {
+// Header of either format; in the whole-exponent format also the
+// code-length section that follows it.
+static void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, uint32_t format,
+                        uint32_t lmax, const hl_codebook* cb, const hl_codebook8* cb8, const Layout& L,
+                        uint64_t off_raw, uint64_t total, uint32_t max_units) {
   std::memset(h, 0, HL_HEADER_BYTES);
   auto put32 = [&](int o, uint32_t v) { std::memcpy(h + o, &v, 4); };
   auto put64 = [&](int o, uint64_t v) { std::memcpy(h + o, &v, 8); };
   put32(0, HL_MAGIC);
   uint16_t ver = HL_VERSION;
   std::memcpy(h + 4, &ver, 2);
-  h[6] = (uint8_t)cb.lmax;
-  h[7] = 0;
+  h[6] = (uint8_t)lmax;
+  h[7] = (uint8_t)format;
   put64(8, rows);
   put64(16, cols);
   put32(24, S);
@@ -196,21 +227,30 @@ void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, const hl_
   put64(72, off_raw);
   put64(80, total);
   put32(88, max_units);
-  h[92] = cb.eh.nsym;
-  h[93] = cb.el.nsym;
-  h[94] = cb.eh.single;
-  h[95] = cb.el.single;
-  std::memcpy(h + 96, cb.eh.len, 16);
-  std::memcpy(h + 112, cb.el.len, 16);
+  if (format == HL_FORMAT_WHOLE_EXPONENT) {
+    std::memcpy(h + 92, &cb8->nsym, 2);
+    h[94] = cb8->single;
+    std::memcpy(h + HL_HEADER_BYTES, cb8->len, HL_LEN8_BYTES);
+  } else {
+    h[92] = cb->eh.nsym;
+    h[93] = cb->el.nsym;
+    h[94] = cb->eh.single;
+    h[95] = cb->el.single;
+    std::memcpy(h + 96, cb->eh.len, 16);
+    std::memcpy(h + 112, cb->el.len, 16);
+  }
 }
 
-bool parse_header(const uint8_t* h, Header* o) {
+bool parse_header(const uint8_t* h, size_t bytes, Header* o) {
+  if (bytes < HL_HEADER_BYTES) return false;
   auto get32 = [&](int off) { uint32_t v; std::memcpy(&v, h + off, 4); return v; };
   auto get64 = [&](int off) { uint64_t v; std::memcpy(&v, h + off, 8); return v; };
   uint16_t ver;
   std::memcpy(&ver, h + 4, 2);
-  if (get32(0) != HL_MAGIC || ver != HL_VERSION || h[7] != 0) return false;
-  o->cb.lmax = h[6];
+  if (get32(0) != HL_MAGIC || ver != HL_VERSION || h[7] > HL_FORMAT_WHOLE_EXPONENT) return false;
+  std::memset(o, 0, sizeof(*o));
+  o->format = h[7];
+  o->lmax = h[6];
   o->rows = get64(8);
   o->cols = get64(16);
   o->seg_len = get32(24);
@@ -223,29 +263,49 @@ bool parse_header(const uint8_t* h, Header* o) {
   o->off_raw = get64(72);
   o->total_bytes = get64(80);
   o->max_grp_units = get32(88);
-  o->cb.eh.nsym = h[92];
-  o->cb.el.nsym = h[93];
-  o->cb.eh.single = h[94];
-  o->cb.el.single = h[95];
-  std::memcpy(o->cb.eh.len, h + 96, 16);
-  std::memcpy(o->cb.el.len, h + 112, 16);
+  if (o->format == HL_FORMAT_WHOLE_EXPONENT) {
+    if (bytes < HL_HEADER_BYTES + HL_LEN8_BYTES) return false;
+    for (int i = 95; i < (int)HL_HEADER_BYTES; ++i)
+      if (h[i]) return false;
+    o->cb8.lmax = o->lmax;
+    std::memcpy(&o->cb8.nsym, h + 92, 2);
+    o->cb8.single = h[94];
+    std::memcpy(o->cb8.len, h + HL_HEADER_BYTES, HL_LEN8_BYTES);
+  } else {
+    o->cb.lmax = o->lmax;
+    o->cb.eh.nsym = h[92];
+    o->cb.el.nsym = h[93];
+    o->cb.eh.single = h[94];
+    o->cb.el.single = h[95];
+    std::memcpy(o->cb.eh.len, h + 96, 16);
+    std::memcpy(o->cb.el.len, h + 112, 16);
+  }
   return true;
+}
+
+// Longest code of one weight: a pair of field codes, or one exponent code.
+static uint64_t weight_bits_max(const Header& H) {
+  return H.format == HL_FORMAT_WHOLE_EXPONENT ? H.lmax : 2ull * H.lmax;
 }
 
 // Consistency of a parsed header with the layout rules (no data access).
 bool header_consistent(const Header& H, uint64_t blob_bytes) {
-  if (H.cb.lmax < 4 || H.cb.lmax > 15) return false;
+  if (H.format == HL_FORMAT_WHOLE_EXPONENT) {
+    if (!code8_valid(H.cb8)) return false;
+  } else {
+    if (H.cb.lmax < 4 || H.cb.lmax > 15) return false;
+    if (!field_code_valid(H.cb.eh, H.cb.lmax) || !field_code_valid(H.cb.el, H.cb.lmax)) return false;
+  }
   if (!shape_ok(H.rows, H.cols, H.seg_len) || !grp_rows_ok(H.cols, H.seg_len, H.grp_rows)) return false;
-  Layout L = make_layout(H.rows, H.cols, H.seg_len, H.grp_rows);
+  Layout L = make_layout(H.rows, H.cols, H.seg_len, H.grp_rows, H.format);
   if (H.n_seg != L.n_seg || H.n_grp != L.n_grp || H.off_seg_bits != L.off_seg_bits ||
       H.off_grp_off != L.off_grp_off || H.off_stream != L.off_stream)
     return false;
   if (H.off_raw < L.off_stream || H.off_raw % 64 || H.total_bytes != H.off_raw + L.n) return false;
   if (H.total_bytes > blob_bytes) return false;
-  // a group holds at most 64 * S * 2 * lmax bits
-  uint64_t max_units = (64ull * H.seg_len * 2 * H.cb.lmax + 127) / 128;
+  // a group holds at most 64 * S weights of at most weight_bits_max bits
+  uint64_t max_units = (64ull * H.seg_len * weight_bits_max(H) + 127) / 128;
   if (H.max_grp_units > max_units) return false;
-  if (!field_code_valid(H.cb.eh, H.cb.lmax) || !field_code_valid(H.cb.el, H.cb.lmax)) return false;
   return true;
 }
 
@@ -317,26 +377,44 @@ static void parallel_for(uint64_t n, unsigned nt, F f) {
   for (auto& x : th) x.join();
 }
 
-extern "C" hl_status hl_build_codebook(const uint16_t* w, size_t n, uint32_t lmax, hl_codebook* out) {
-  if (!w || !out || n == 0 || lmax < 4 || lmax > 15) return HL_EINVAL;
+// Histogram of the bits (v >> shift) & mask of n weights, over all cores for
+// large inputs; nb = mask + 1 bins.
+static std::vector<uint64_t> histogram(const uint16_t* w, size_t n, int shift, uint32_t mask) {
+  const size_t nb = mask + 1;
   unsigned nt = pick_threads(0);
   if (n < (1u << 20)) nt = 1;
-  std::vector<std::array<uint64_t, 32>> part(nt);
+  const uint64_t per = (n + nt - 1) / nt;
+  std::vector<std::vector<uint64_t>> part(nt, std::vector<uint64_t>(nb, 0));
   parallel_for(n, nt, [&](uint64_t a, uint64_t b) {
-    std::array<uint64_t, 32> h{};
-    for (uint64_t i = a; i < b; ++i) {
-      uint32_t v = w[i];
-      h[(v >> 11) & 15]++;
-      h[16 + ((v >> 7) & 15)]++;
-    }
-    part[a / ((n + nt - 1) / nt)] = h;
+    std::vector<uint64_t>& h = part[a / per];
+    for (uint64_t i = a; i < b; ++i) h[(w[i] >> shift) & mask]++;
   });
-  uint64_t feh[16] = {0}, fel[16] = {0};
+  std::vector<uint64_t> f(nb, 0);
   for (auto& h : part)
-    for (int s = 0; s < 16; ++s) { feh[s] += h[s]; fel[s] += h[16 + s]; }
+    for (size_t s = 0; s < nb; ++s) f[s] += h[s];
+  return f;
+}
+
+extern "C" hl_status hl_build_codebook(const uint16_t* w, size_t n, uint32_t lmax, hl_codebook* out) {
+  if (!w || !out || n == 0 || lmax < 4 || lmax > 15) return HL_EINVAL;
+  const std::vector<uint64_t> feh = histogram(w, n, 11, 15), fel = histogram(w, n, 7, 15);
   out->lmax = lmax;
-  field_code_from_counts(feh, (int)lmax, &out->eh);
-  field_code_from_counts(fel, (int)lmax, &out->el);
+  field_code_from_counts(feh.data(), (int)lmax, &out->eh);
+  field_code_from_counts(fel.data(), (int)lmax, &out->el);
+  return HL_OK;
+}
+
+extern "C" hl_status hl_build_codebook8(const uint16_t* w, size_t n, uint32_t lmax, hl_codebook8* out) {
+  if (!w || !out || n == 0 || lmax < HL_LMAX8_MIN || lmax > HL_LMAX8_MAX) return HL_EINVAL;
+  const std::vector<uint64_t> f = histogram(w, n, 7, 255);
+  std::memset(out, 0, sizeof(*out));
+  out->lmax = lmax;
+  int nsym = 0, single = 0;
+  for (int s = 0; s < 256; ++s)
+    if (f[s]) { ++nsym; single = s; }
+  out->nsym = (uint16_t)nsym;
+  out->single = (uint8_t)(nsym == 1 ? single : 0);
+  limited_lengths(f.data(), 256, (int)lmax, out->len);
   return HL_OK;
 }
 
@@ -344,39 +422,63 @@ extern "C" uint32_t hl_default_grp_rows(uint64_t cols, uint32_t seg_len) {
   return default_grp_rows(cols, seg_len ? seg_len : default_seg_len(cols));
 }
 
-extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook* cb,
-                               uint32_t seg_len, uint32_t grp_rows, uint32_t nthreads, void* out,
-                               size_t* out_bytes) {
-  if (!w || !cb || !out_bytes) return HL_EINVAL;
-  uint32_t S = seg_len ? seg_len : default_seg_len(cols);
-  if (!shape_ok(rows, cols, S)) return HL_EINVAL;
-  const uint32_t GR = grp_rows ? grp_rows : default_grp_rows(cols, S);
-  if (!grp_rows_ok(cols, S, GR)) return HL_EINVAL;
-  if (cb->lmax < 4 || cb->lmax > 15 || !field_code_valid(cb->eh, cb->lmax) ||
-      !field_code_valid(cb->el, cb->lmax))
-    return HL_EINVAL;
-  // Pair table: reversed codes of the pair, el first; length 0 for one-symbol fields.
+// Code of each exponent byte e = (w >> 7) & 255 as it enters the stream: the
+// bit-reversed code (LSB-first packing of an MSB-first code), its length, and
+// whether e can be coded at all.
+struct ByteCode {
+  std::array<uint32_t, 256> code;
+  std::array<uint8_t, 256> len;
+  std::array<bool, 256> valid;
+};
+
+// Split format: the pair code(el) then code(eh).
+static ByteCode pair_code(const hl_codebook& cb) {
   uint32_t ceh[16], cel[16];
-  canonical_codes(cb->eh.len, ceh);
-  canonical_codes(cb->el.len, cel);
+  canonical_codes(cb.eh.len, 16, ceh);
+  canonical_codes(cb.el.len, 16, cel);
   uint8_t leh[16], lel[16];
   bool veh[16], vel[16];
   for (int s = 0; s < 16; ++s) {
-    leh[s] = cb->eh.nsym == 1 ? 0 : cb->eh.len[s];
-    lel[s] = cb->el.nsym == 1 ? 0 : cb->el.len[s];
-    veh[s] = cb->eh.nsym == 1 ? (s == cb->eh.single) : cb->eh.len[s] != 0;
-    vel[s] = cb->el.nsym == 1 ? (s == cb->el.single) : cb->el.len[s] != 0;
+    leh[s] = cb.eh.nsym == 1 ? 0 : cb.eh.len[s];
+    lel[s] = cb.el.nsym == 1 ? 0 : cb.el.len[s];
+    veh[s] = cb.eh.nsym == 1 ? (s == cb.eh.single) : cb.eh.len[s] != 0;
+    vel[s] = cb.el.nsym == 1 ? (s == cb.el.single) : cb.el.len[s] != 0;
   }
-  std::array<uint32_t, 256> pcode;
-  std::array<uint8_t, 256> plen;
-  std::array<bool, 256> pvalid;
+  ByteCode bc;
   for (int e = 0; e < 256; ++e) {
     int a = e >> 4, b = e & 15;
-    pcode[e] = bit_reverse(cel[b], lel[b]) | (bit_reverse(ceh[a], leh[a]) << lel[b]);
-    plen[e] = (uint8_t)(leh[a] + lel[b]);
-    pvalid[e] = veh[a] && vel[b];
+    bc.code[e] = bit_reverse(cel[b], lel[b]) | (bit_reverse(ceh[a], leh[a]) << lel[b]);
+    bc.len[e] = (uint8_t)(leh[a] + lel[b]);
+    bc.valid[e] = veh[a] && vel[b];
   }
-  Layout L = make_layout(rows, cols, S, GR);
+  return bc;
+}
+
+// Whole-exponent format: one code per exponent byte.
+static ByteCode whole_code(const hl_codebook8& cb) {
+  uint32_t c[256];
+  canonical_codes(cb.len, 256, c);
+  ByteCode bc;
+  for (int e = 0; e < 256; ++e) {
+    bc.len[e] = cb.nsym == 1 ? 0 : cb.len[e];
+    bc.code[e] = bit_reverse(c[e], bc.len[e]);
+    bc.valid[e] = cb.nsym == 1 ? e == cb.single : cb.len[e] != 0;
+  }
+  return bc;
+}
+
+// The encoder proper, shared by both formats: everything but the header and
+// the per-byte code table is format independent.
+static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, uint32_t seg_len,
+                             uint32_t grp_rows, uint32_t nthreads, uint32_t format, uint32_t lmax,
+                             const hl_codebook* cb, const hl_codebook8* cb8, const ByteCode& bc,
+                             void* out, size_t* out_bytes) {
+  const uint32_t S = seg_len;
+  const uint32_t GR = grp_rows;
+  const auto& pcode = bc.code;
+  const auto& plen = bc.len;
+  const auto& pvalid = bc.valid;
+  Layout L = make_layout(rows, cols, S, GR, format);
   const unsigned nt = pick_threads(nthreads);
   // Pass 1: segment bit counts, in group order.
   std::vector<uint16_t> seg_bits(L.n_seg);
@@ -421,8 +523,8 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   if (!out) { *out_bytes = total; return HL_OK; }
   if (*out_bytes < total) { *out_bytes = total; return HL_ENOMEM; }
   uint8_t* o = (uint8_t*)out;
-  std::memset(o, 0, L.off_stream);  // header, padding, metadata
-  pack_header(o, rows, cols, S, *cb, L, off_raw, total, max_units);
+  std::memset(o, 0, L.off_stream);  // header, codebook section, padding, metadata
+  pack_header(o, rows, cols, S, format, lmax, cb, cb8, L, off_raw, total, max_units);
   std::memcpy(o + L.off_seg_bits, seg_bits.data(), 2 * L.n_seg);
   std::memcpy(o + L.off_grp_off, grp_off.data(), 4 * (L.n_grp + 1));
   std::memset(o + L.off_stream + units * 16, 0, off_raw - (L.off_stream + units * 16));
@@ -463,17 +565,50 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   return HL_OK;
 }
 
+// Shape arguments of both encoders: the segment length and group rows used.
+static bool resolve_shape(uint64_t rows, uint64_t cols, uint32_t seg_len, uint32_t grp_rows, uint32_t* S,
+                          uint32_t* GR) {
+  *S = seg_len ? seg_len : default_seg_len(cols);
+  if (!shape_ok(rows, cols, *S)) return false;
+  *GR = grp_rows ? grp_rows : default_grp_rows(cols, *S);
+  return grp_rows_ok(cols, *S, *GR);
+}
+
+extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook* cb,
+                               uint32_t seg_len, uint32_t grp_rows, uint32_t nthreads, void* out,
+                               size_t* out_bytes) {
+  if (!w || !cb || !out_bytes) return HL_EINVAL;
+  uint32_t S, GR;
+  if (!resolve_shape(rows, cols, seg_len, grp_rows, &S, &GR)) return HL_EINVAL;
+  if (cb->lmax < 4 || cb->lmax > 15 || !field_code_valid(cb->eh, cb->lmax) ||
+      !field_code_valid(cb->el, cb->lmax))
+    return HL_EINVAL;
+  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_SPLIT, cb->lmax, cb, nullptr, pair_code(*cb),
+                     out, out_bytes);
+}
+
+extern "C" hl_status hl_encode8(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook8* cb,
+                                uint32_t seg_len, uint32_t grp_rows, uint32_t nthreads, void* out,
+                                size_t* out_bytes) {
+  if (!w || !cb || !out_bytes) return HL_EINVAL;
+  uint32_t S, GR;
+  if (!resolve_shape(rows, cols, seg_len, grp_rows, &S, &GR)) return HL_EINVAL;
+  if (!code8_valid(*cb)) return HL_EINVAL;
+  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_WHOLE_EXPONENT, cb->lmax, nullptr, cb,
+                     whole_code(*cb), out, out_bytes);
+}
+
 namespace hl {
 
 hl_status validate_blob(const uint8_t* b, size_t bytes, Header* out, uint32_t* max_seg_bits) {
   if (!b || bytes < HL_HEADER_BYTES) return HL_ECORRUPT;
   Header H;
-  if (!parse_header(b, &H) || !header_consistent(H, bytes)) return HL_ECORRUPT;
+  if (!parse_header(b, bytes, &H) || !header_consistent(H, bytes)) return HL_ECORRUPT;
   const uint16_t* sb = (const uint16_t*)(b + H.off_seg_bits);
   const uint32_t* go = (const uint32_t*)(b + H.off_grp_off);
   if (go[0] != 0) return HL_ECORRUPT;
   uint32_t mx = 0, mseg = 0;
-  const uint64_t max_seg = (uint64_t)H.seg_len * 2 * H.cb.lmax;
+  const uint64_t max_seg = (uint64_t)H.seg_len * weight_bits_max(H);
   const uint64_t L = H.cols / H.seg_len;
   for (uint64_t g = 0; g < H.n_grp; ++g) {
     GroupGeom q = group_geom(H.rows, L, H.grp_rows, g);

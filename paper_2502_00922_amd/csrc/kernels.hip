@@ -61,7 +61,7 @@ static Aux make_aux(const hl_codebook& cb) {
     const hl_field_code& fc = *fs[f];
     uint32_t* w = a.w + f * kAuxField;
     uint32_t code[16];
-    canonical_codes(fc.len, code);
+    canonical_codes(fc.len, 16, code);
     int maxl = 0;
     for (int s = 0; s < 16; ++s) maxl = std::max(maxl, (int)fc.len[s]);
     if (fc.nsym == 1) maxl = 0;
@@ -121,6 +121,62 @@ __global__ void __launch_bounds__(256) lut_kernel(uint32_t* lut, Aux aux) {
     lut[v] = (a < 0 || b < 0) ? kEsc : ((ua + ub) | ((uint32_t)((a << 4) | b) << 23));
   }
   for (int i = threadIdx.x; i < kAuxWords; i += blockDim.x) lut[kLutN + i] = aux.w[i];
+}
+
+// Whole-exponent code in canonical form: per length l = 1..13 the first code
+// value, the number of codes and the index of the first of them in `sym`,
+// the exponent values sorted by (length, value).
+struct Aux8 {
+  uint32_t nsym, single;
+  uint32_t first[kLutBits + 1], count[kLutBits + 1], off[kLutBits + 1];
+  uint8_t sym[256];
+};
+
+static Aux8 make_aux8(const hl_codebook8& cb) {
+  Aux8 a;
+  std::memset(&a, 0, sizeof(a));
+  a.nsym = cb.nsym;
+  a.single = cb.single;
+  if (cb.nsym == 1) return a;
+  uint32_t code[256];
+  canonical_codes(cb.len, 256, code);
+  uint32_t k = 0;
+  for (int l = 1; l <= kLutBits; ++l) {
+    a.off[l] = k;
+    for (int s = 0; s < 256; ++s) {
+      if (cb.len[s] != l) continue;
+      if (a.count[l] == 0) a.first[l] = code[s];
+      ++a.count[l];
+      a.sym[k++] = (uint8_t)s;
+    }
+  }
+  return a;
+}
+
+// Decode table of the whole-exponent format: entry v = the code that the
+// 13-bit window v (bit 0 first) starts with, as its length in bits 0..4 and
+// the exponent byte in bits 23..30, the entry format of the split table. A
+// complete code of at most 13 bits matches every window; kEsc is left only
+// for a damaged code. The aux words are zero (no long codes).
+__global__ void __launch_bounds__(256) lut8_kernel(uint32_t* lut, Aux8 a) {
+  for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
+    uint32_t ent = kEsc;
+    if (a.nsym == 1) {
+      ent = a.single << 23;
+    } else {
+      uint32_t code = 0;
+      for (uint32_t l = 1; l <= (uint32_t)kLutBits; ++l) {
+        code = (code << 1) | (((uint32_t)v >> (l - 1)) & 1u);
+        const uint32_t d = code - a.first[l];
+        if (d < a.count[l]) {
+          ent = l | ((uint32_t)a.sym[a.off[l] + d] << 23);
+          break;
+        }
+      }
+    }
+    lut[v] = ent;
+  }
+  for (int i = threadIdx.x; i < kAuxWords; i += blockDim.x) lut[kLutN + i] = 0;
 }
 
 // Copies the joint table and the aux tables into LDS, four 16-byte loads in
@@ -1291,16 +1347,23 @@ extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
   t.off_raw = H.off_raw;
   t.seg_len = H.seg_len;
   t.grp_rows = H.grp_rows;
-  t.lmax = H.cb.lmax;
+  t.lmax = H.lmax;
   t.max_grp_units = H.max_grp_units;
   t.max_seg_bits = mseg;
+  t.format = H.format;
   t.cb = H.cb;
+  t.cb8 = H.cb8;
   *out = t;
   return HL_OK;
 }
 
 extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
   if (!t || !t->lut_dev) return HL_EINVAL;
+  if (t->format == HL_FORMAT_WHOLE_EXPONENT) {
+    if (!code8_valid(t->cb8)) return HL_ECORRUPT;
+    return launch(lut8_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, make_aux8(t->cb8));
+  }
+  if (t->format != HL_FORMAT_SPLIT) return HL_EINVAL;
   if (!field_code_valid(t->cb.eh, t->cb.lmax) || !field_code_valid(t->cb.el, t->cb.lmax)) return HL_ECORRUPT;
   Aux aux = make_aux(t->cb);
   return launch(lut_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, aux);

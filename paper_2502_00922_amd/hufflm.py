@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(HERE, "libhufflm.so")
 
 HL_OK, HL_EINVAL, HL_ENOMEM, HL_ECORRUPT, HL_EUNSUPPORTED, HL_EHIP = range(6)
 HL_F32, HL_BF16 = 0, 1
+HL_FORMAT_SPLIT, HL_FORMAT_WHOLE_EXPONENT = 0, 1
 HEADER_BYTES = 128
 LUT_BYTES = 33024
 MAX_BATCH = 16
@@ -41,6 +42,15 @@ class Codebook(ctypes.Structure):
     _fields_ = [("lmax", ctypes.c_uint32), ("eh", FieldCode), ("el", FieldCode)]
 
 
+class Codebook8(ctypes.Structure):
+    _fields_ = [("lmax", ctypes.c_uint32), ("nsym", ctypes.c_uint16), ("single", ctypes.c_uint8),
+                ("reserved", ctypes.c_uint8), ("len", ctypes.c_uint8 * 256)]
+
+    @property
+    def lengths(self):
+        return list(self.len)
+
+
 class TensorView(ctypes.Structure):
     _fields_ = [("blob_dev", ctypes.c_void_p), ("lut_dev", ctypes.c_void_p),
                 ("rows", ctypes.c_uint64), ("cols", ctypes.c_uint64), ("n_seg", ctypes.c_uint64),
@@ -49,14 +59,14 @@ class TensorView(ctypes.Structure):
                 ("off_stream", ctypes.c_uint64), ("off_raw", ctypes.c_uint64),
                 ("seg_len", ctypes.c_uint32), ("grp_rows", ctypes.c_uint32), ("lmax", ctypes.c_uint32),
                 ("max_grp_units", ctypes.c_uint32), ("max_seg_bits", ctypes.c_uint32),
-                ("reserved", ctypes.c_uint32),
-                ("cb", Codebook)]
+                ("format", ctypes.c_uint32),
+                ("cb", Codebook), ("cb8", Codebook8)]
 
 
 _lib = None
 
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
-           "hl_validate",
+           "hl_build_codebook8", "hl_encode8", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
            "hl_decode_gemv", "hl_gemv_bf16"]
 
@@ -81,6 +91,11 @@ def lib() -> ctypes.CDLL:
     L.hl_encode.restype = c.c_int
     L.hl_encode.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook), c.c_uint32,
                             c.c_uint32, c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
+    L.hl_build_codebook8.restype = c.c_int
+    L.hl_build_codebook8.argtypes = [c.c_void_p, c.c_size_t, c.c_uint32, c.POINTER(Codebook8)]
+    L.hl_encode8.restype = c.c_int
+    L.hl_encode8.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook8), c.c_uint32,
+                             c.c_uint32, c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
     L.hl_validate.restype = c.c_int
     L.hl_validate.argtypes = [c.c_void_p, c.c_size_t]
     L.hl_tensor_view.restype = c.c_int
@@ -121,24 +136,40 @@ def build_codebook(w: np.ndarray, lmax: int = 12) -> Codebook:
     return cb
 
 
+def build_codebook8(w: np.ndarray, lmax: int = 12) -> Codebook8:
+    """Whole-exponent code: one 256-symbol code over the exponent bytes."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    cb = Codebook8()
+    _check(lib().hl_build_codebook8(w.ctypes.data, w.size, lmax, ctypes.byref(cb)), "hl_build_codebook8")
+    return cb
+
+
 def default_grp_rows(cols: int, seg_len: int = 0) -> int:
     return int(lib().hl_default_grp_rows(cols, seg_len))
 
 
-def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook: Optional[Codebook] = None,
-           nthreads: int = 0, grp_rows: int = 0) -> np.ndarray:
-    """HLF1 container (uint8 array) of a bf16 matrix given as uint16 bits [rows, cols]."""
+def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook=None,
+           nthreads: int = 0, grp_rows: int = 0, whole_exponent: bool = False) -> np.ndarray:
+    """HLF1 container (uint8 array) of a bf16 matrix given as uint16 bits [rows, cols].
+
+    whole_exponent selects the format with one 256-symbol exponent code
+    (``codebook`` then is a Codebook8)."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     if w.ndim != 2:
         raise ValueError("expected a 2-D matrix")
-    cb = codebook if codebook is not None else build_codebook(w, lmax)
-    n = ctypes.c_size_t(0)
     L = lib()
-    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,
-                       None, ctypes.byref(n)), "hl_encode(size)")
+    if whole_exponent:
+        cb = codebook if codebook is not None else build_codebook8(w, lmax)
+        fn, name = L.hl_encode8, "hl_encode8"
+    else:
+        cb = codebook if codebook is not None else build_codebook(w, lmax)
+        fn, name = L.hl_encode, "hl_encode"
+    n = ctypes.c_size_t(0)
+    _check(fn(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,
+              None, ctypes.byref(n)), name + "(size)")
     out = np.empty(n.value, dtype=np.uint8)
-    _check(L.hl_encode(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,
-                       out.ctypes.data, ctypes.byref(n)), "hl_encode")
+    _check(fn(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,
+              out.ctypes.data, ctypes.byref(n)), name)
     return out
 
 

@@ -2,6 +2,7 @@
 benchmark times (default segment length and group shape, cached workspace).
 
 Per matrix:
+Both container formats (split exponent; whole exponent on two workloads).
 * lossless: the device decode equals the generated weights bit for bit (a
   property at any size), and sampled groups decoded by the oracle's bit-serial
   decoder from the library's container equal them too;
@@ -39,14 +40,15 @@ def _sample_rows(R, rng, n=40):
     return sorted(r for r in rows if 0 <= r < R)
 
 
-def _check_matrix(torch, spec, batches, x_dtype, size_check):
-    print(f"workload {spec.cfg} layer {spec.layer} {spec.name} {spec.rows}x{spec.cols}", flush=True)
+def _check_matrix(torch, spec, batches, x_dtype, size_check, whole=False):
+    print(f"workload {spec.cfg} layer {spec.layer} {spec.name} {spec.rows}x{spec.cols} whole={whole}", flush=True)
     W = gen_matrix(spec)
-    blob = hl.encode(W)
-    h = codec.parse_header(bytes(blob[:128]))
+    blob = hl.encode(W, whole_exponent=whole)
+    h = codec.parse_header(bytes(blob[:384]))
     S = h["seg_len"]
     if size_check:
-        assert blob.size == codec.container_size(W, S)["total_bytes"]
+        size = codec.container_size8 if whole else codec.container_size
+        assert blob.size == size(W, S)["total_bytes"]
     dt = hl.DeviceTensor(blob)
     # lossless at full size
     dec = dt.decode()
@@ -79,6 +81,15 @@ def test_workload_full_size(torch, cfg):
     smallest = min(specs, key=lambda s: s.rows * s.cols)
     for spec in specs:
         _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest)
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_workload_full_size_whole_exponent(torch, cfg):
+    """The whole-exponent format on the 4096x4096 and the 8B-shaped layer workloads."""
+    specs = config_matrices(cfg)
+    smallest = min(specs, key=lambda s: s.rows * s.cols)
+    for spec in specs:
+        _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest, whole=True)
 
 
 @pytest.mark.slow

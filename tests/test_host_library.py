@@ -133,3 +133,87 @@ def test_validate_rejects_damage():
     assert hl.validate(damaged(h["off_seg_bits"], 0xFFFF, 2)) == hl.HL_ECORRUPT   # seg_bits
     assert hl.validate(damaged(h["off_grp_off"] + 4, 0, 4)) == hl.HL_ECORRUPT     # grp_off
     assert hl.validate(damaged(88, h["max_grp_units"] + 1, 4)) == hl.HL_ECORRUPT
+
+
+# ---------------------------------------------------------------- whole-exponent format
+@pytest.mark.parametrize("seed", range(4))
+def test_codebook8_equals_oracle(seed):
+    rng = np.random.default_rng(seed)
+    w = random_bf16((32, 256), seed, std=float(rng.choice([0.002, 0.02, 0.5])))
+    for lmax in (8, 12, 13):
+        cb = hl.build_codebook8(w, lmax=lmax)
+        ref = codec.build_codebook8(w, lmax)
+        assert (cb.nsym, cb.single, cb.lengths) == (ref.nsym, ref.single, ref.lengths)
+
+
+CASES8 = [((64, 1024), 64, 12, 0), ((130, 48), 16, 12, 0), ((3, 64), 8, 8, 0), ((65, 96), 32, 13, 0),
+          ((130, 512), 64, 12, 8), ((37, 256), 32, 10, 32), ((1, 8), 8, 12, 0), ((21, 512), 8, 12, 1)]
+
+
+@pytest.mark.parametrize("shape,S,lmax,GR", CASES8)
+def test_whole_exponent_byte_identical_to_oracle(shape, S, lmax, GR):
+    w = random_bf16(shape, seed=sum(shape) + S + 1)
+    a = bytes(hl.encode(w, seg_len=S, lmax=lmax, grp_rows=GR, whole_exponent=True))
+    assert a == codec.encode8(w, seg_len=S, lmax=lmax, grp_rows=GR or None)
+    assert hl.validate(a) == 0
+
+
+def test_whole_exponent_adversarial():
+    # every bf16 pattern once: all 256 exponent values, uniform -> 8-bit codes
+    w = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(128, 512)
+    for lmax in (8, 13):
+        assert bytes(hl.encode(w, seg_len=64, lmax=lmax, whole_exponent=True)) == codec.encode8(w, 64, lmax)
+    # exponent counts 2, 2, 4, ..., 2^14: the unlimited code reaches 14 bits
+    rng = np.random.default_rng(3)
+    e = np.concatenate([np.full(2, 100)] + [np.full(2 ** i, 100 + i) for i in range(1, 15)]).astype(np.uint32)
+    e = rng.permutation(e)
+    w = ((rng.integers(0, 2, e.size) << 15) | (e << 7) | rng.integers(0, 128, e.size)).astype(np.uint16)
+    w = w.reshape(128, 256)
+    assert max(codec.huffman_lengths(codec.histogram(e, 256))) > 13
+    for lmax in (8, 11, 13):
+        a = bytes(hl.encode(w, seg_len=32, lmax=lmax, whole_exponent=True))
+        assert a == codec.encode8(w, 32, lmax)
+    # one exponent value: no stream bits
+    w = np.full((70, 16), 0x3F80, np.uint16)
+    w[5, 3] = 0xBF81
+    a = bytes(hl.encode(w, seg_len=16, whole_exponent=True))
+    assert a == codec.encode8(w, 16) and codec.parse_header(a)["max_grp_units"] == 0
+
+
+def test_whole_exponent_threads_and_errors():
+    w = random_bf16((300, 256), seed=6)
+    a = hl.encode(w, seg_len=64, nthreads=1, whole_exponent=True)
+    for t in (3, 16):
+        assert np.array_equal(a, hl.encode(w, seg_len=64, nthreads=t, whole_exponent=True))
+    for bad in (7, 14):
+        with pytest.raises(hl.HLError):
+            hl.build_codebook8(w, lmax=bad)
+    other = hl.build_codebook8(np.full((8, 64), 0x3F80, np.uint16))
+    with pytest.raises(hl.HLError):
+        hl.encode(w, seg_len=64, codebook=other, whole_exponent=True)
+
+
+def test_whole_exponent_validate_rejects_damage():
+    w = random_bf16((130, 256), seed=7)
+    good = hl.encode(w, seg_len=64, whole_exponent=True)
+    assert hl.validate(good) == 0
+    h = codec.parse_header(bytes(good))
+    lens = h["len8"]
+    s_long = max(range(256), key=lambda s: lens[s])
+
+    def damaged(offset, value, width=1):
+        b = good.copy()
+        b[offset:offset + width] = np.frombuffer(int(value).to_bytes(width, "little"), np.uint8)
+        return b
+
+    assert hl.validate(good[:383]) == hl.HL_ECORRUPT                      # no room for the lengths
+    assert hl.validate(damaged(7, 2)) == hl.HL_ECORRUPT                   # unknown format
+    assert hl.validate(damaged(6, 14)) == hl.HL_ECORRUPT                  # lmax above the window
+    assert hl.validate(damaged(6, 7)) == hl.HL_ECORRUPT                   # lmax below 8
+    assert hl.validate(damaged(128 + s_long, lens[s_long] - 1)) == hl.HL_ECORRUPT   # Kraft > 1
+    assert hl.validate(damaged(92, h["nsym8"] + 1, 2)) == hl.HL_ECORRUPT  # symbol count
+    assert hl.validate(damaged(100, 1)) == hl.HL_ECORRUPT                 # reserved bytes
+    assert hl.validate(damaged(48, 128, 8)) == hl.HL_ECORRUPT             # off_seg_bits of the split format
+    assert hl.validate(damaged(h["off_seg_bits"], 0xFFFF, 2)) == hl.HL_ECORRUPT
+    # a split-format header over the whole-exponent body
+    assert hl.validate(damaged(7, 0)) == hl.HL_ECORRUPT
