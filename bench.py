@@ -42,7 +42,8 @@ METRIC = "effective decoded-weight GB/s in fused decode-GEMV; compressed-byte HB
 HBM_PEAK_GBS = 8000.0
 COLD_BYTES = 1.2 * (1 << 30)
 KERNEL_SRC = os.path.join(ROOT, "paper_2502_00922_amd", "csrc", "kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_traffic.txt")
+TRAFFIC_FILES = {"split": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_traffic.txt"),
+                 "whole": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_whole_exponent_traffic.txt")}
 COPY_BYTES = 256 << 20
 
 
@@ -68,17 +69,19 @@ def kernel_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def recorded_traffic(batch: int):
+def recorded_traffic(batch: int, fmt: str):
     """HBM bytes per launch from the committed counter summary, if it was taken
-    from the current kernel source at this batch size; else None."""
+    from the current kernel source for this container format and batch size;
+    else None."""
     try:
-        text = open(TRAFFIC_FILE).read()
+        text = open(TRAFFIC_FILES[fmt]).read()
     except OSError:
         return None
     h = re.search(r"kernel source sha256\[:16\]: ([0-9a-f]{16})", text)
     b = re.search(r"batch: (\d+)", text)
+    f = re.search(r"format: (\w+)", text)
     t = re.search(r"traffic_bytes_per_launch: (\d+)", text)
-    if not (h and b and t) or h.group(1) != kernel_hash() or int(b.group(1)) != batch:
+    if not (h and b and t and f) or h.group(1) != kernel_hash() or int(b.group(1)) != batch or f.group(1) != fmt:
         return None
     return int(t.group(1))
 
@@ -312,7 +315,7 @@ def main():
                    "compressed_bytes": int(blob.size), "compression_ratio": round(2 * n / blob.size, 4),
                    "bits_per_weight": round(8 * blob.size / n, 4), "replicas": nrep},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(b0)},
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(b0, args.format)},
         "cpu_baseline": cpu,
         "detail": extra,
     }
