@@ -212,7 +212,14 @@ def main():
     R, K = spec.rows, spec.cols
     n = R * K
     W = gen_matrix(spec)
-    blobs = {f: hl.encode(W, whole_exponent=(f == "whole")) for f in ("split", "whole")}
+    blobs, encoder = {}, {}
+    for f in ("split", "whole"):
+        t0 = time.perf_counter()
+        blobs[f] = hl.encode(W, whole_exponent=(f == "whole"))
+        dt = time.perf_counter() - t0
+        encoder[f] = dict(seconds=round(dt, 4), input_GBps=round(2 * n / dt / 1e9, 3))
+    encoder["threads"] = len(os.sched_getaffinity(0))
+    encoder["note"] = "host encode (codebook + container) of the same matrix, all threads of this process"
     blob = blobs[args.format]
     blob_b = bytes(blob)
     nrep = max(2, math.ceil(COLD_BYTES / blob.size))
@@ -295,6 +302,7 @@ def main():
         extra[f"batch{b}"] = e
     if variant is not None:
         extra["variant"] = variant
+    extra["encoder"] = encoder
     out = {
         "metric": METRIC,
         "value": round(value, 1),

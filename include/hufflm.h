@@ -175,7 +175,8 @@ uint32_t hl_default_grp_rows(uint64_t cols, uint32_t seg_len);
  * hl_default_seg_len(cols); grp_rows 0 selects hl_default_grp_rows. With
  * out == NULL, *out_bytes receives the exact size; otherwise *out_bytes is the
  * capacity of `out` on entry and the size written on return (HL_ENOMEM if too
- * small). nthreads 0 = all cores; the output does not depend on nthreads.
+ * small). nthreads 0 = the CPUs of the calling process's affinity mask (at most 64); the
+ * output does not depend on nthreads.
  * Errors: HL_EINVAL (shape, seg_len, grp_rows, a weight whose field has no
  * code in `cb`). */
 hl_status hl_encode(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,

@@ -8,6 +8,8 @@
 #include "hufflm.h"
 #include "hl_internal.h"
 
+#include <sched.h>
+
 #include <algorithm>
 #include <array>
 #include <cstring>
@@ -359,8 +361,15 @@ extern "C" const char* hl_status_str(hl_status s) {
 
 extern "C" uint32_t hl_default_seg_len(uint64_t cols) { return default_seg_len(cols); }
 
+// Threads for nthreads == 0: the CPUs this process may run on (its affinity
+// mask, not the whole machine), at most 64.
 static unsigned pick_threads(uint32_t nthreads) {
-  unsigned t = nthreads ? nthreads : std::thread::hardware_concurrency();
+  unsigned t = nthreads;
+  if (!t) {
+    cpu_set_t set;
+    t = sched_getaffinity(0, sizeof(set), &set) == 0 ? (unsigned)CPU_COUNT(&set)
+                                                      : std::thread::hardware_concurrency();
+  }
   return std::max(1u, std::min(t, 64u));
 }
 
