@@ -100,6 +100,12 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
+def bf16_bits_to_f16_bits(b: np.ndarray) -> np.ndarray:
+    """The float16 copy of bf16 weights (float16 rounding, nearest-even): the
+    FP16 release of a model trained in bf16. Returns uint16 bits."""
+    return bf16_bits_to_f32(b).astype(np.float16).view(np.uint16)
+
+
 ROW_BLOCK = 256
 
 
@@ -164,7 +170,8 @@ def gen_matrix(spec: MatrixSpec, rows: Optional[slice] = None, threads: int = 0)
 
 
 def gen_x(spec: MatrixSpec, batch: int, dtype: str) -> np.ndarray:
-    """Activation rows x[batch][cols]: float32, or bf16 bits (uint16) if dtype == 'bf16'."""
+    """Activation rows x[batch][cols]: float32, bf16 bits (uint16) if dtype ==
+    'bf16', or float16 values if dtype == 'f16'."""
     if spec.cfg == 1:
         rng = np.random.default_rng(0)
         rng.standard_normal((spec.rows, spec.cols), dtype=np.float32)
@@ -176,6 +183,8 @@ def gen_x(spec: MatrixSpec, batch: int, dtype: str) -> np.ndarray:
         return x
     if dtype == "bf16":
         return f32_to_bf16_bits(x)
+    if dtype == "f16":
+        return x.astype(np.float16)
     raise ValueError(dtype)
 
 
@@ -189,7 +198,15 @@ def random_bf16(shape, seed: int, std: float = BASE_STD, outliers: bool = True) 
     return f32_to_bf16_bits(w)
 
 
+def random_fp16(shape, seed: int, std: float = BASE_STD, outliers: bool = True) -> np.ndarray:
+    """FP16 bits of random_bf16's matrix (see bf16_bits_to_f16_bits)."""
+    return bf16_bits_to_f16_bits(random_bf16(shape, seed, std, outliers))
+
+
 def random_x(batch: int, cols: int, seed: int, dtype: str = "f32") -> np.ndarray:
+    """float32, bf16 bits (uint16) or float16 values."""
     rng = np.random.default_rng([8, seed])
     x = rng.standard_normal((batch, cols), dtype=np.float32)
+    if dtype == "f16":
+        return x.astype(np.float16)
     return x if dtype == "f32" else f32_to_bf16_bits(x)

@@ -47,6 +47,17 @@ Code lengths are limited to lmax in [8, 13]; the 256 lengths are stored in a
 256-byte section right after the header. Tiling, stream order (one code per
 weight, MSB-first, packed LSB-first), group padding and the raw plane are
 those of the split format.
+
+FP16 format (header flags = 2), the paper's own {1,5,5,5} split (Sec. 3.1,
+entropy-of-splits table and Huffman-flow figure; Sec. 3.2 decoder with three
+5-bit Huffman decoders): a float16 weight is sign (bit 15, kept raw), exponent
+e (bits 14..10), mantissa-high mh (bits 9..5) and mantissa-low ml (bits 4..0);
+e, mh and ml each get a per-matrix 32-symbol code, lmax in [5, 12]. Each
+weight's codes go into the stream as code(ml), code(e), code(mh). The three
+code-length tables (each: symbol count, single symbol, 32 lengths) follow the
+header in a 128-byte section. The raw plane holds the sign bits only: byte
+(segment number) * S/8 + t/8, bit t % 8, for weight t of a segment, segments
+numbered in group order.
 """
 from __future__ import annotations
 
@@ -71,6 +82,10 @@ FLAG_SPLIT = 0              # header flags: two 4-bit exponent codes
 FLAG_WHOLE_EXPONENT = 1     # header flags: one 8-bit exponent code
 LEN8_BYTES = 256            # whole-exponent code lengths, after the header
 LMAX8_MIN, LMAX8_MAX = 8, 13
+FLAG_FP16 = 2               # header flags: float16 {1,5,5,5}
+NSYM5 = 32                  # 5-bit fields of the float16 split
+CB16_BYTES = 128            # float16 code tables, after the header
+LMAX16_MIN, LMAX16_MAX = 5, 12
 
 
 # --------------------------------------------------------------------------
@@ -292,7 +307,8 @@ def layout(rows: int, cols: int, seg_len: int, grp_rows: int = GROUP_SEGS,
     L = cols // seg_len
     GC = GROUP_SEGS // grp_rows
     n_grp = (rows + grp_rows - 1) // grp_rows * (L // GC)
-    off_seg_bits = _align(HEADER_BYTES + (LEN8_BYTES if flags == FLAG_WHOLE_EXPONENT else 0))
+    extra = {FLAG_SPLIT: 0, FLAG_WHOLE_EXPONENT: LEN8_BYTES, FLAG_FP16: CB16_BYTES}[flags]
+    off_seg_bits = _align(HEADER_BYTES + extra)
     off_grp_off = _align(off_seg_bits + 2 * n_seg)
     off_stream = _align(off_grp_off + 4 * (n_grp + 1))
     return dict(n=n, n_seg=n_seg, n_grp=n_grp, L=L, GC=GC, off_seg_bits=off_seg_bits,
@@ -319,6 +335,9 @@ def check_shape(rows: int, cols: int, seg_len: int, lmax: int, grp_rows: int = G
     if flags == FLAG_WHOLE_EXPONENT:
         if not (LMAX8_MIN <= lmax <= LMAX8_MAX):
             raise ValueError("lmax must be in [8, 13] for the whole-exponent code")
+    elif flags == FLAG_FP16:
+        if not (LMAX16_MIN <= lmax <= LMAX16_MAX):
+            raise ValueError("lmax must be in [5, 12] for the float16 codes")
     elif not (4 <= lmax <= 15):
         raise ValueError("lmax must be in [4, 15]")
     if seg_len < 8 or seg_len > 512 or seg_len % 8 or cols % seg_len:
@@ -341,6 +360,42 @@ def raw_pos(r: np.ndarray, c: np.ndarray, rows: int, cols: int, seg_len: int,
     mu = j * G + i
     first_seg = rb * grp_rows * L + cb * GC * G
     return first_seg * seg_len + ((t // RAW_UNIT) * (G * GC) + mu) * RAW_UNIT + (t % RAW_UNIT)
+
+
+def raw_plane(w: np.ndarray, seg_len: int, grp_rows: int) -> np.ndarray:
+    """Raw plane of the bf16 formats: (sign<<7 | mantissa) of every weight at raw_pos."""
+    rows, cols = w.shape
+    s, _, _, m = split_fields(w)
+    rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
+    raw = np.zeros(rows * cols, dtype=np.uint8)
+    raw[raw_pos(rr.ravel(), cc.ravel(), rows, cols, seg_len, grp_rows)] = raw_byte(s, m).ravel()
+    return raw
+
+
+def segment_number(r, c, rows: int, cols: int, seg_len: int, grp_rows: int) -> np.ndarray:
+    """Group-order number of the segment holding weight (r, c)."""
+    r = np.asarray(r, dtype=np.int64)
+    c = np.asarray(c, dtype=np.int64)
+    L = cols // seg_len
+    GC = GROUP_SEGS // grp_rows
+    rb, i = r // grp_rows, r % grp_rows
+    cb, j = (c // seg_len) // GC, (c // seg_len) % GC
+    G = np.minimum(grp_rows, rows - rb * grp_rows)
+    return rb * grp_rows * L + cb * GC * G + j * G + i
+
+
+def sign_plane(w: np.ndarray, seg_len: int, grp_rows: int) -> np.ndarray:
+    """Raw plane of the float16 format: one sign bit per weight, S/8 bytes per
+    segment in group order; bit t % 8 of byte t // 8 is weight t's sign."""
+    rows, cols = w.shape
+    sgn = (np.asarray(w, np.uint16) >> 15).astype(np.uint8)
+    rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
+    seg = segment_number(rr, cc, rows, cols, seg_len, grp_rows)
+    t = cc % seg_len
+    byte = (seg * (seg_len // 8) + t // 8).ravel()
+    plane = np.zeros(rows * cols // 8, dtype=np.uint8)
+    np.bitwise_or.at(plane, byte, (sgn.ravel() << (t.ravel() % 8)).astype(np.uint8))
+    return plane
 
 
 def build_codebooks(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode]:
@@ -386,11 +441,10 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
 
 
 def _assemble(w, seg_len, GR, flags, seg_stream, header, codebook_section) -> bytes:
-    """Container bytes from a per-segment stream function (both formats)."""
+    """Container bytes from a per-segment stream function (all formats)."""
     rows, cols = w.shape
     lay = layout(rows, cols, seg_len, GR, flags)
     n, n_seg, n_grp = lay["n"], lay["n_seg"], lay["n_grp"]
-    s, _, _, m = split_fields(w)
     S = seg_len
 
     seg_bits = np.zeros(n_seg, dtype=np.uint16)
@@ -415,10 +469,8 @@ def _assemble(w, seg_len, GR, flags, seg_stream, header, codebook_section) -> by
     stream = b"".join(chunks)
 
     off_raw = _align(lay["off_stream"] + len(stream))
-    total = off_raw + n
-    rr, cc = np.meshgrid(np.arange(rows), np.arange(cols), indexing="ij")
-    raw = np.zeros(n, dtype=np.uint8)
-    raw[raw_pos(rr.ravel(), cc.ravel(), rows, cols, S, GR)] = raw_byte(s, m).ravel()
+    raw = sign_plane(w, S, GR) if flags == FLAG_FP16 else raw_plane(w, S, GR)
+    total = off_raw + raw.size
 
     out = bytearray(total)
     out[0:HEADER_BYTES] = header(n_seg, n_grp, lay["off_seg_bits"], lay["off_grp_off"],
@@ -499,6 +551,96 @@ def container_size8(w: np.ndarray, seg_len: int, lmax: int = 12, codebook: Field
     return _size_from_bits(le[exponent_byte(w)], w.shape, seg_len, lmax, grp_rows, FLAG_WHOLE_EXPONENT)
 
 
+# --------------------------------------------------------------------------
+# FP16 {1,5,5,5} format (flags = 2)
+# --------------------------------------------------------------------------
+
+def split_fields16(w: np.ndarray):
+    """float16 bit patterns -> (sign, exponent, mantissa-high, mantissa-low):
+    float16 = sign (bit 15) | exponent (bits 14..10) | mantissa (bits 9..0),
+    the mantissa halved into its high and low 5 bits (the {1,5,5,5} split)."""
+    w = np.asarray(w, dtype=np.uint16).astype(np.uint32)
+    return (w >> 15) & 1, (w >> 10) & 0x1F, (w >> 5) & 0x1F, w & 0x1F
+
+
+def join_fields16(s, e, mh, ml) -> np.ndarray:
+    s, e, mh, ml = (np.asarray(a, dtype=np.uint32) for a in (s, e, mh, ml))
+    return ((s << 15) | (e << 10) | (mh << 5) | ml).astype(np.uint16)
+
+
+def build_codebooks16(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode, FieldCode]:
+    """Per-matrix codes of the three 5-bit fields (exponent, mantissa-high, mantissa-low)."""
+    if not (LMAX16_MIN <= lmax <= LMAX16_MAX):
+        raise ValueError("lmax must be in [5, 12] for the float16 codes")
+    _, e, mh, ml = split_fields16(w)
+    return tuple(FieldCode.from_freqs(histogram(f, NSYM5), lmax) for f in (e, mh, ml))
+
+
+def segment_stream16(e_seg, mh_seg, ml_seg, ce: FieldCode, cmh: FieldCode, cml: FieldCode) -> Tuple[int, int]:
+    """Bit stream of one segment: per weight code(ml), code(e), code(mh), each
+    MSB-first; stream bit k is bit k of the integer."""
+    acc, pos = 0, 0
+    for e, mh, ml in zip(e_seg, mh_seg, ml_seg):
+        for code, v in ((cml, ml), (ce, e), (cmh, mh)):
+            l = code.lengths[v] if code.nsym > 1 else 0
+            acc |= bit_reverse(code.codes[v], l) << pos
+            pos += l
+    return acc, pos
+
+
+def _codebook16_section(codes) -> bytes:
+    out = bytearray(CB16_BYTES)
+    for f, c in enumerate(codes):
+        rec = bytes([c.nsym, c.single]) + (bytes(c.lengths) if c.nsym > 1 else bytes(NSYM5))
+        out[f * 34:(f + 1) * 34] = rec
+    return bytes(out)
+
+
+def encode16(w: np.ndarray, seg_len: int, lmax: int = 12, codebooks=None, grp_rows: int = None) -> bytes:
+    """Compress a float16 matrix [rows, cols] (uint16 bit patterns) into an HLF1
+    container of the float16 format."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    rows, cols = w.shape
+    GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
+    check_shape(rows, cols, seg_len, lmax, GR, FLAG_FP16)
+    codes = codebooks if codebooks is not None else build_codebooks16(w, lmax)
+    ce, cmh, cml = codes
+    _, e, mh, ml = split_fields16(w)
+    for c, f in ((ce, e), (cmh, mh), (cml, ml)):
+        if c.nsym > 1 and max(c.lengths) > lmax:
+            raise ValueError("codebook does not fit lmax")
+        for v in np.unique(f).tolist():
+            if (c.lengths[v] == 0) if c.nsym > 1 else (v != c.single):
+                raise ValueError("field value without a code")
+
+    def seg_stream(r, a, S):
+        return segment_stream16(e[r, a:a + S].tolist(), mh[r, a:a + S].tolist(), ml[r, a:a + S].tolist(),
+                                ce, cmh, cml)
+
+    def header(n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units):
+        return struct.pack(HEADER_FMT, MAGIC, VERSION, lmax, FLAG_FP16, rows, cols, seg_len, GR,
+                           n_seg, n_grp, off_sb, off_go, off_st, off_raw, total, max_units,
+                           0, 0, 0, 0, bytes(16), bytes(16))
+
+    return _assemble(w, seg_len, GR, FLAG_FP16, seg_stream, header, _codebook16_section(codes))
+
+
+def header_codebooks16(h) -> Tuple[FieldCode, FieldCode, FieldCode]:
+    return tuple(FieldCode(lens, nsym, single) for nsym, single, lens in h["cb16"])
+
+
+def container_size16(w: np.ndarray, seg_len: int, lmax: int = 12, codebooks=None,
+                     grp_rows: int = None) -> Dict[str, int]:
+    """Exact size of ``encode16(w, ...)`` from the code lengths alone."""
+    w = np.asarray(w, dtype=np.uint16)
+    codes = codebooks if codebooks is not None else build_codebooks16(w, lmax)
+    _, e, mh, ml = split_fields16(w)
+    bits = 0
+    for c, f in zip(codes, (e, mh, ml)):
+        bits = bits + np.array(c.lengths if c.nsym > 1 else [0] * NSYM5, dtype=np.int64)[f]
+    return _size_from_bits(bits, w.shape, seg_len, lmax, grp_rows, FLAG_FP16)
+
+
 HEADER_FMT = "<IHBBQQIIQQQQQQQIBBBB16s16s"
 
 
@@ -527,6 +669,10 @@ def parse_header(blob: bytes) -> Dict[str, object]:
         h["nsym8"] = h["eh_nsym"] | (h["el_nsym"] << 8)
         h["single8"] = h["eh_single"]
         h["len8"] = list(blob[HEADER_BYTES:HEADER_BYTES + LEN8_BYTES])
+    elif h["flags"] == FLAG_FP16:
+        # three records (exponent, mantissa-high, mantissa-low): nsym, single, 32 lengths
+        sec = blob[HEADER_BYTES:HEADER_BYTES + CB16_BYTES]
+        h["cb16"] = [(sec[f * 34], sec[f * 34 + 1], list(sec[f * 34 + 2:f * 34 + 34])) for f in range(3)]
     elif h["flags"] != FLAG_SPLIT:
         raise ValueError("unknown format flags")
     return h
@@ -542,6 +688,8 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
 
     Returns (first row r0, rows G, first column segment, GC, uint16[G, GC*S])."""
     h = parse_header(blob)
+    if h["flags"] == FLAG_FP16:
+        return _decode_group16(blob, h, g)
     whole = h["flags"] == FLAG_WHOLE_EXPONENT
     if whole:
         code8 = header_codebook8(h)
@@ -575,6 +723,35 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
         rp = raw_pos(np.full(S, r0 + i), cols_of, rows, cols, S, GR)
         r = raw_plane[rp].astype(np.uint32)
         out[i, j * S:(j + 1) * S] = join_fields(r >> 7, eh, el, r & 0x7F)
+    return r0, G, c0, GC, out
+
+
+def _decode_group16(blob: bytes, h, g: int):
+    """decode_group for the float16 format."""
+    ce, cmh, cml = header_codebooks16(h)
+    rows, cols, S, GR = h["rows"], h["cols"], h["seg_len"], h["grp_rows"]
+    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
+    grp_off = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    signs = np.frombuffer(blob, np.uint8, rows * cols // 8, h["off_raw"])
+    r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
+    a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
+    b = h["off_stream"] + int(grp_off[g + 1]) * UNIT_BYTES
+    bits = np.unpackbits(np.frombuffer(blob[a:b], np.uint8), bitorder="little").tolist()
+    out = np.zeros((G, GC * S), dtype=np.uint16)
+    pos = 0
+    for mu in range(G * GC):
+        i, j = mu % G, mu // G
+        start = pos
+        f = np.zeros((3, S), np.uint32)
+        for t in range(S):
+            f[2, t], pos = cml.decode_one(bits, pos)
+            f[0, t], pos = ce.decode_one(bits, pos)
+            f[1, t], pos = cmh.decode_one(bits, pos)
+        if pos - start != int(seg_bits[first + mu]):
+            raise ValueError("segment length mismatch")
+        t = np.arange(S)
+        sb = signs[(first + mu) * (S // 8) + t // 8]
+        out[i, j * S:(j + 1) * S] = join_fields16((sb >> (t % 8)) & 1, f[0], f[1], f[2])
     return r0, G, c0, GC, out
 
 
@@ -629,5 +806,6 @@ def _size_from_bits(bits, shape, seg_len, lmax, grp_rows, flags) -> Dict[str, in
         max_units = max(max_units, int(u.max()))
     lay = layout(rows, cols, seg_len, GR, flags)
     off_raw = _align(lay["off_stream"] + units * UNIT_BYTES)
-    return dict(total_bytes=off_raw + rows * cols, stream_units=units, max_grp_units=max_units,
+    raw_bytes = rows * cols // 8 if flags == FLAG_FP16 else rows * cols
+    return dict(total_bytes=off_raw + raw_bytes, stream_units=units, max_grp_units=max_units,
                 code_bits=int(seg.sum()), off_raw=off_raw, grp_rows=GR)
