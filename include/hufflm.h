@@ -71,6 +71,18 @@
  * follows the paper's split-size analysis (Sec. 3.1): an 8-bit symbol is
  * costly for a single-cycle CAM match, not for a table lookup in local memory.
  *
+ * flags 2 is the float16 format, the paper's {1,5,5,5} split (Sec. 3.1,
+ * Sec. 3.2): a float16 weight w is sign s = w>>15 (kept raw), exponent
+ * e = (w>>10)&31, mantissa-high mh = (w>>5)&31 and mantissa-low ml = w&31;
+ * e, mh and ml each have a per-matrix code over 32 symbols (the same rules,
+ * lmax in [5, 12]). The stream holds code(ml), code(e), code(mh) for each
+ * weight of a segment in order, each most-significant bit first. A 128-byte
+ * section after the header holds three records (e, mh, ml) of u8 nsym,
+ * u8 single, u8 len[32], then zeros; off_seg_bits = 256; header bytes 92..127
+ * are zero. The raw plane holds only signs: byte k*(S/8) + t/8, bit t%8 is the
+ * sign of weight t of the segment numbered k in group order, and
+ * total_bytes = off_raw + n/8.
+ *
  * ---------------------------------------------------------------------------
  * Conventions of the ABI
  * ---------------------------------------------------------------------------
@@ -102,7 +114,7 @@ typedef enum {
   HL_EHIP = 5           /* HIP runtime error */
 } hl_status;
 
-typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
+typedef enum { HL_F32 = 0, HL_BF16 = 1, HL_F16 = 2 } hl_dtype;
 
 #define HL_MAGIC 0x31464C48u
 #define HL_VERSION 1u
@@ -113,8 +125,11 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1 } hl_dtype;
 #define HL_LEN8_BYTES 256u    /* whole-exponent code lengths after the header */
 #define HL_LMAX8_MIN 8u
 #define HL_LMAX8_MAX 13u
+#define HL_CB16_BYTES 128u    /* float16 code tables after the header */
+#define HL_LMAX16_MIN 5u
+#define HL_LMAX16_MAX 12u
 
-typedef enum { HL_FORMAT_SPLIT = 0, HL_FORMAT_WHOLE_EXPONENT = 1 } hl_format;
+typedef enum { HL_FORMAT_SPLIT = 0, HL_FORMAT_WHOLE_EXPONENT = 1, HL_FORMAT_FP16 = 2 } hl_format;
 
 typedef struct {
   uint8_t nsym;     /* symbols present in the field (1..16) */
@@ -137,6 +152,21 @@ typedef struct {
   uint8_t len[256];   /* code length per exponent value; 0 = absent (or the only one) */
 } hl_codebook8;
 
+/* One 5-bit field of the float16 format. */
+typedef struct {
+  uint8_t nsym;     /* symbols present (1..32) */
+  uint8_t single;   /* the symbol when nsym == 1, else 0 */
+  uint8_t len[32];  /* code length per symbol; 0 = absent (or the only one) */
+} hl_field_code5;
+
+/* Float16 codes (format 2). */
+typedef struct {
+  uint32_t lmax;       /* code-length limit used to build the lengths, 5..12 */
+  hl_field_code5 e;    /* exponent, bits 14..10 */
+  hl_field_code5 mh;   /* mantissa bits 9..5 */
+  hl_field_code5 ml;   /* mantissa bits 4..0 */
+} hl_codebook16;
+
 /* Non-owning view of one container resident in device memory. */
 typedef struct {
   const uint8_t* blob_dev;   /* whole container */
@@ -144,9 +174,10 @@ typedef struct {
   uint64_t rows, cols, n_seg, n_grp, total_bytes;
   uint64_t off_seg_bits, off_grp_off, off_stream, off_raw;
   uint32_t seg_len, grp_rows, lmax, max_grp_units, max_seg_bits;
-  uint32_t format;           /* hl_format: which of cb / cb8 is in use (the other is zero) */
+  uint32_t format;           /* hl_format: which of cb / cb8 / cb16 is in use (the others are zero) */
   hl_codebook cb;
   hl_codebook8 cb8;
+  hl_codebook16 cb16;
 } hl_tensor;
 
 /* Text of a status code (static storage). */
@@ -196,6 +227,19 @@ hl_status hl_build_codebook8(const uint16_t* w_bf16, size_t n, uint32_t lmax,
 hl_status hl_encode8(const uint16_t* w_bf16, uint64_t rows, uint64_t cols,
                      const hl_codebook8* cb, uint32_t seg_len, uint32_t grp_rows,
                      uint32_t nthreads, void* out, size_t* out_bytes);
+
+/* Float16 codes (format 2, the paper's {1,5,5,5} split, Sec. 3.1) of n
+ * float16 bit patterns: one code per 5-bit field, built by the same rules as
+ * hl_build_codebook. lmax in [5, 12]. Errors: HL_EINVAL for n == 0, null
+ * pointers or lmax out of range. */
+hl_status hl_build_codebook16(const uint16_t* w_f16, size_t n, uint32_t lmax,
+                              hl_codebook16* out);
+
+/* Encode a float16 matrix W [rows][cols] into an HLF1 container of the
+ * float16 format (flags 2). Arguments, size query and errors as hl_encode. */
+hl_status hl_encode16(const uint16_t* w_f16, uint64_t rows, uint64_t cols,
+                      const hl_codebook16* cb, uint32_t seg_len, uint32_t grp_rows,
+                      uint32_t nthreads, void* out, size_t* out_bytes);
 
 /* Full structural check of a container held in host memory: header, section
  * offsets, codebooks (Kraft sum exactly 1, lengths <= lmax), per-group

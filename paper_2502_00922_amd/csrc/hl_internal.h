@@ -25,9 +25,13 @@ uint32_t default_grp_rows(uint64_t cols, uint32_t S);
 struct Header {
   uint64_t rows, cols, n_seg, n_grp, off_seg_bits, off_grp_off, off_stream, off_raw, total_bytes;
   uint32_t seg_len, grp_rows, max_grp_units, format, lmax;
-  hl_codebook cb;    // format 0 (zero otherwise)
-  hl_codebook8 cb8;  // format 1 (zero otherwise)
+  hl_codebook cb;      // format 0 (zero otherwise)
+  hl_codebook8 cb8;    // format 1 (zero otherwise)
+  hl_codebook16 cb16;  // format 2 (zero otherwise)
 };
+
+// Bytes of the raw plane: one per weight, or one sign bit per weight (float16).
+inline uint64_t raw_bytes(uint64_t n, uint32_t format) { return format == HL_FORMAT_FP16 ? n / 8 : n; }
 
 bool shape_ok(uint64_t rows, uint64_t cols, uint32_t S);
 Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR, uint32_t format);
@@ -37,6 +41,7 @@ bool parse_header(const uint8_t* b, size_t bytes, Header* out);
 bool header_consistent(const Header& h, uint64_t blob_bytes);
 bool field_code_valid(const hl_field_code& fc, uint32_t lmax);
 bool code8_valid(const hl_codebook8& cb);
+bool code16_valid(const hl_codebook16& cb);
 // Canonical code values of n symbols with lengths <= 16 (RFC 1951 Sec. 3.2.2).
 void canonical_codes(const uint8_t* len, int n, uint32_t* code);
 uint32_t default_seg_len(uint64_t cols);

@@ -170,6 +170,31 @@ bool code8_valid(const hl_codebook8& cb) {
   return cnt == cb.nsym && kraft == (1ull << 15);
 }
 
+// One 5-bit field of the float16 format: as field_code_valid over 32 symbols.
+static bool field5_valid(const hl_field_code5& fc, uint32_t lmax) {
+  if (fc.nsym < 1 || fc.nsym > 32) return false;
+  if (fc.nsym == 1) {
+    if (fc.single > 31) return false;
+    for (int s = 0; s < 32; ++s) if (fc.len[s]) return false;
+    return true;
+  }
+  if (fc.single != 0) return false;
+  int cnt = 0;
+  uint64_t kraft = 0;  // in units of 2^-15
+  for (int s = 0; s < 32; ++s) {
+    if (!fc.len[s]) continue;
+    if (fc.len[s] > lmax) return false;
+    ++cnt;
+    kraft += 1ull << (15 - fc.len[s]);
+  }
+  return cnt == fc.nsym && kraft == (1ull << 15);
+}
+
+bool code16_valid(const hl_codebook16& cb) {
+  if (cb.lmax < HL_LMAX16_MIN || cb.lmax > HL_LMAX16_MAX) return false;
+  return field5_valid(cb.e, cb.lmax) && field5_valid(cb.mh, cb.lmax) && field5_valid(cb.ml, cb.lmax);
+}
+
 // ---------------------------------------------------------------- layout
 
 static uint64_t align64(uint64_t x) { return (x + 63) & ~uint64_t(63); }
@@ -198,7 +223,10 @@ Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR, uint32
   L.GR = GR;
   L.GC = HL_GROUP_SEGS / GR;
   L.n_grp = (rows + GR - 1) / GR * (L.L / L.GC);
-  L.off_seg_bits = align64(HL_HEADER_BYTES + (format == HL_FORMAT_WHOLE_EXPONENT ? HL_LEN8_BYTES : 0));
+  const uint64_t section = format == HL_FORMAT_WHOLE_EXPONENT ? HL_LEN8_BYTES
+                           : format == HL_FORMAT_FP16        ? HL_CB16_BYTES
+                                                             : 0;
+  L.off_seg_bits = align64(HL_HEADER_BYTES + section);
   L.off_grp_off = align64(L.off_seg_bits + 2 * L.n_seg);
   L.off_stream = align64(L.off_grp_off + 4 * (L.n_grp + 1));
   return L;
@@ -207,8 +235,9 @@ Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR, uint32
 // Header of either format; in the whole-exponent format also the
 // code-length section that follows it.
 static void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, uint32_t format,
-                        uint32_t lmax, const hl_codebook* cb, const hl_codebook8* cb8, const Layout& L,
-                        uint64_t off_raw, uint64_t total, uint32_t max_units) {
+                        uint32_t lmax, const hl_codebook* cb, const hl_codebook8* cb8,
+                        const hl_codebook16* cb16, const Layout& L, uint64_t off_raw, uint64_t total,
+                        uint32_t max_units) {
   std::memset(h, 0, HL_HEADER_BYTES);
   auto put32 = [&](int o, uint32_t v) { std::memcpy(h + o, &v, 4); };
   auto put64 = [&](int o, uint64_t v) { std::memcpy(h + o, &v, 8); };
@@ -233,6 +262,15 @@ static void pack_header(uint8_t* h, uint64_t rows, uint64_t cols, uint32_t S, ui
     std::memcpy(h + 92, &cb8->nsym, 2);
     h[94] = cb8->single;
     std::memcpy(h + HL_HEADER_BYTES, cb8->len, HL_LEN8_BYTES);
+  } else if (format == HL_FORMAT_FP16) {
+    uint8_t* sec = h + HL_HEADER_BYTES;
+    std::memset(sec, 0, HL_CB16_BYTES);
+    const hl_field_code5* f[3] = {&cb16->e, &cb16->mh, &cb16->ml};
+    for (int k = 0; k < 3; ++k) {
+      sec[34 * k] = f[k]->nsym;
+      sec[34 * k + 1] = f[k]->single;
+      std::memcpy(sec + 34 * k + 2, f[k]->len, 32);
+    }
   } else {
     h[92] = cb->eh.nsym;
     h[93] = cb->el.nsym;
@@ -249,7 +287,7 @@ bool parse_header(const uint8_t* h, size_t bytes, Header* o) {
   auto get64 = [&](int off) { uint64_t v; std::memcpy(&v, h + off, 8); return v; };
   uint16_t ver;
   std::memcpy(&ver, h + 4, 2);
-  if (get32(0) != HL_MAGIC || ver != HL_VERSION || h[7] > HL_FORMAT_WHOLE_EXPONENT) return false;
+  if (get32(0) != HL_MAGIC || ver != HL_VERSION || h[7] > HL_FORMAT_FP16) return false;
   std::memset(o, 0, sizeof(*o));
   o->format = h[7];
   o->lmax = h[6];
@@ -273,6 +311,20 @@ bool parse_header(const uint8_t* h, size_t bytes, Header* o) {
     std::memcpy(&o->cb8.nsym, h + 92, 2);
     o->cb8.single = h[94];
     std::memcpy(o->cb8.len, h + HL_HEADER_BYTES, HL_LEN8_BYTES);
+  } else if (o->format == HL_FORMAT_FP16) {
+    if (bytes < HL_HEADER_BYTES + HL_CB16_BYTES) return false;
+    for (int i = 92; i < (int)HL_HEADER_BYTES; ++i)
+      if (h[i]) return false;
+    const uint8_t* sec = h + HL_HEADER_BYTES;
+    for (int i = 102; i < (int)HL_CB16_BYTES; ++i)
+      if (sec[i]) return false;
+    o->cb16.lmax = o->lmax;
+    hl_field_code5* f[3] = {&o->cb16.e, &o->cb16.mh, &o->cb16.ml};
+    for (int k = 0; k < 3; ++k) {
+      f[k]->nsym = sec[34 * k];
+      f[k]->single = sec[34 * k + 1];
+      std::memcpy(f[k]->len, sec + 34 * k + 2, 32);
+    }
   } else {
     o->cb.lmax = o->lmax;
     o->cb.eh.nsym = h[92];
@@ -287,13 +339,15 @@ bool parse_header(const uint8_t* h, size_t bytes, Header* o) {
 
 // Longest code of one weight: a pair of field codes, or one exponent code.
 static uint64_t weight_bits_max(const Header& H) {
-  return H.format == HL_FORMAT_WHOLE_EXPONENT ? H.lmax : 2ull * H.lmax;
+  return H.format == HL_FORMAT_WHOLE_EXPONENT ? H.lmax : H.format == HL_FORMAT_FP16 ? 3ull * H.lmax : 2ull * H.lmax;
 }
 
 // Consistency of a parsed header with the layout rules (no data access).
 bool header_consistent(const Header& H, uint64_t blob_bytes) {
   if (H.format == HL_FORMAT_WHOLE_EXPONENT) {
     if (!code8_valid(H.cb8)) return false;
+  } else if (H.format == HL_FORMAT_FP16) {
+    if (!code16_valid(H.cb16)) return false;
   } else {
     if (H.cb.lmax < 4 || H.cb.lmax > 15) return false;
     if (!field_code_valid(H.cb.eh, H.cb.lmax) || !field_code_valid(H.cb.el, H.cb.lmax)) return false;
@@ -303,7 +357,8 @@ bool header_consistent(const Header& H, uint64_t blob_bytes) {
   if (H.n_seg != L.n_seg || H.n_grp != L.n_grp || H.off_seg_bits != L.off_seg_bits ||
       H.off_grp_off != L.off_grp_off || H.off_stream != L.off_stream)
     return false;
-  if (H.off_raw < L.off_stream || H.off_raw % 64 || H.total_bytes != H.off_raw + L.n) return false;
+  if (H.off_raw < L.off_stream || H.off_raw % 64 || H.total_bytes != H.off_raw + raw_bytes(L.n, H.format))
+    return false;
   if (H.total_bytes > blob_bytes) return false;
   // a group holds at most 64 * S weights of at most weight_bits_max bits
   uint64_t max_units = (64ull * H.seg_len * weight_bits_max(H) + 127) / 128;
@@ -476,17 +531,58 @@ static ByteCode whole_code(const hl_codebook8& cb) {
   return bc;
 }
 
-// The encoder proper, shared by both formats: everything but the header and
-// the per-byte code table is format independent.
+// Per-weight coders. len/valid/emit see a weight's 16 bits; emit passes its
+// code parts, in stream order, to put(bit-reversed code, length).
+// bf16 formats: the exponent byte's code (a pair, or one whole-exponent code),
+// raw plane of (sign<<7 | mantissa) bytes.
+struct ByteCoder {
+  ByteCode bc;
+  static constexpr bool kSignPlane = false;
+  uint32_t len(uint32_t v) const { return bc.len[(v >> 7) & 0xFF]; }
+  bool valid(uint32_t v) const { return bc.valid[(v >> 7) & 0xFF]; }
+  template <class Put>
+  void emit(uint32_t v, Put put) const {
+    const uint32_t e = (v >> 7) & 0xFF;
+    put(bc.code[e], bc.len[e]);
+  }
+};
+
+// Float16 format: code(ml), code(e), code(mh); raw plane of sign bits.
+struct F16Coder {
+  uint32_t code[3][32];  // parts in stream order: ml, e, mh
+  uint8_t plen[3][32];
+  bool ok[3][32];
+  static constexpr bool kSignPlane = true;
+  static uint32_t part(uint32_t v, int k) { return k == 0 ? v & 31 : k == 1 ? (v >> 10) & 31 : (v >> 5) & 31; }
+  explicit F16Coder(const hl_codebook16& cb) {
+    const hl_field_code5* f[3] = {&cb.ml, &cb.e, &cb.mh};
+    for (int k = 0; k < 3; ++k) {
+      uint32_t c[32];
+      canonical_codes(f[k]->len, 32, c);
+      for (int s = 0; s < 32; ++s) {
+        plen[k][s] = f[k]->nsym == 1 ? 0 : f[k]->len[s];
+        code[k][s] = bit_reverse(c[s], plen[k][s]);
+        ok[k][s] = f[k]->nsym == 1 ? s == f[k]->single : f[k]->len[s] != 0;
+      }
+    }
+  }
+  uint32_t len(uint32_t v) const { return plen[0][part(v, 0)] + plen[1][part(v, 1)] + plen[2][part(v, 2)]; }
+  bool valid(uint32_t v) const { return ok[0][part(v, 0)] && ok[1][part(v, 1)] && ok[2][part(v, 2)]; }
+  template <class Put>
+  void emit(uint32_t v, Put put) const {
+    for (int k = 0; k < 3; ++k) put(code[k][part(v, k)], plen[k][part(v, k)]);
+  }
+};
+
+// The encoder proper, shared by all formats: everything but the header, the
+// per-weight coder and the raw plane's kind is format independent.
+template <class Coder>
 static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, uint32_t seg_len,
                              uint32_t grp_rows, uint32_t nthreads, uint32_t format, uint32_t lmax,
-                             const hl_codebook* cb, const hl_codebook8* cb8, const ByteCode& bc,
-                             void* out, size_t* out_bytes) {
+                             const hl_codebook* cb, const hl_codebook8* cb8, const hl_codebook16* cb16,
+                             const Coder& cd, void* out, size_t* out_bytes) {
   const uint32_t S = seg_len;
   const uint32_t GR = grp_rows;
-  const auto& pcode = bc.code;
-  const auto& plen = bc.len;
-  const auto& pvalid = bc.valid;
   Layout L = make_layout(rows, cols, S, GR, format);
   const unsigned nt = pick_threads(nthreads);
   // Pass 1: segment bit counts, in group order.
@@ -501,9 +597,8 @@ static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, ui
         const uint16_t* p = w + (q.r0 + mu % q.G) * cols + (q.c0 + mu / q.G) * S;
         uint32_t bits = 0;
         for (uint32_t t = 0; t < S; ++t) {
-          uint32_t e = (p[t] >> 7) & 0xFF;
-          anybad |= !pvalid[e];
-          bits += plen[e];
+          anybad |= !cd.valid(p[t]);
+          bits += cd.len(p[t]);
         }
         seg_bits[q.first + mu] = (uint16_t)bits;
       }
@@ -528,12 +623,12 @@ static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, ui
   }
   grp_off[L.n_grp] = (uint32_t)units;
   const uint64_t off_raw = align64(L.off_stream + units * 16);
-  const uint64_t total = off_raw + L.n;
+  const uint64_t total = off_raw + raw_bytes(L.n, format);
   if (!out) { *out_bytes = total; return HL_OK; }
   if (*out_bytes < total) { *out_bytes = total; return HL_ENOMEM; }
   uint8_t* o = (uint8_t*)out;
   std::memset(o, 0, L.off_stream);  // header, codebook section, padding, metadata
-  pack_header(o, rows, cols, S, format, lmax, cb, cb8, L, off_raw, total, max_units);
+  pack_header(o, rows, cols, S, format, lmax, cb, cb8, cb16, L, off_raw, total, max_units);
   std::memcpy(o + L.off_seg_bits, seg_bits.data(), 2 * L.n_seg);
   std::memcpy(o + L.off_grp_off, grp_off.data(), 4 * (L.n_grp + 1));
   std::memset(o + L.off_stream + units * 16, 0, off_raw - (L.off_stream + units * 16));
@@ -546,22 +641,38 @@ static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, ui
       uint64_t acc = 0;
       int nb = 0;
       uint64_t wi = 0;
-      uint8_t* rdst = o + off_raw + q.first * S;
+      // each part is at most 16 bits and nb < 32 before it: acc never overflows
+      auto put = [&](uint32_t code, uint32_t len) {
+        acc |= (uint64_t)code << nb;
+        nb += (int)len;
+        if (nb >= 32) {
+          dst[wi++] = (uint32_t)acc;
+          acc >>= 32;
+          nb -= 32;
+        }
+      };
       const uint32_t NG = q.G * q.GC;
       for (uint32_t mu = 0; mu < NG; ++mu) {
         const uint16_t* p = w + (q.r0 + mu % q.G) * cols + (q.c0 + mu / q.G) * S;
-        for (uint32_t t = 0; t < S; ++t) {
-          uint32_t v = p[t];
-          uint32_t e = (v >> 7) & 0xFF;
-          acc |= (uint64_t)pcode[e] << nb;
-          nb += plen[e];
-          if (nb >= 32) {
-            dst[wi++] = (uint32_t)acc;
-            acc >>= 32;
-            nb -= 32;
+        if (Coder::kSignPlane) {
+          // sign bits: byte (segment number)*S/8 + t/8, bit t%8
+          uint8_t* sdst = o + off_raw + (q.first + mu) * (S / 8);
+          for (uint32_t t = 0; t < S; t += 8) {
+            uint32_t byte = 0;
+            for (uint32_t k = 0; k < 8; ++k) {
+              cd.emit(p[t + k], put);
+              byte |= (uint32_t)(p[t + k] >> 15) << k;
+            }
+            sdst[t / 8] = (uint8_t)byte;
           }
+        } else {
           // raw plane: ((t/8)*NG + mu)*8 + t%8 within the group
-          rdst[((t >> 3) * NG + mu) * 8 + (t & 7)] = (uint8_t)(((v >> 8) & 0x80) | (v & 0x7F));
+          uint8_t* rdst = o + off_raw + q.first * S;
+          for (uint32_t t = 0; t < S; ++t) {
+            const uint32_t v = p[t];
+            cd.emit(v, put);
+            rdst[((t >> 3) * NG + mu) * 8 + (t & 7)] = (uint8_t)(((v >> 8) & 0x80) | (v & 0x7F));
+          }
         }
       }
       while (wi < nwords) {  // tail bits, then zero padding to 128 bits
@@ -592,8 +703,8 @@ extern "C" hl_status hl_encode(const uint16_t* w, uint64_t rows, uint64_t cols, 
   if (cb->lmax < 4 || cb->lmax > 15 || !field_code_valid(cb->eh, cb->lmax) ||
       !field_code_valid(cb->el, cb->lmax))
     return HL_EINVAL;
-  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_SPLIT, cb->lmax, cb, nullptr, pair_code(*cb),
-                     out, out_bytes);
+  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_SPLIT, cb->lmax, cb, nullptr, nullptr,
+                     ByteCoder{pair_code(*cb)}, out, out_bytes);
 }
 
 extern "C" hl_status hl_encode8(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook8* cb,
@@ -603,8 +714,37 @@ extern "C" hl_status hl_encode8(const uint16_t* w, uint64_t rows, uint64_t cols,
   uint32_t S, GR;
   if (!resolve_shape(rows, cols, seg_len, grp_rows, &S, &GR)) return HL_EINVAL;
   if (!code8_valid(*cb)) return HL_EINVAL;
-  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_WHOLE_EXPONENT, cb->lmax, nullptr, cb,
-                     whole_code(*cb), out, out_bytes);
+  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_WHOLE_EXPONENT, cb->lmax, nullptr, cb, nullptr,
+                     ByteCoder{whole_code(*cb)}, out, out_bytes);
+}
+
+extern "C" hl_status hl_build_codebook16(const uint16_t* w, size_t n, uint32_t lmax, hl_codebook16* out) {
+  if (!w || !out || n == 0 || lmax < HL_LMAX16_MIN || lmax > HL_LMAX16_MAX) return HL_EINVAL;
+  std::memset(out, 0, sizeof(*out));
+  out->lmax = lmax;
+  const int shift[3] = {10, 5, 0};
+  hl_field_code5* f[3] = {&out->e, &out->mh, &out->ml};
+  for (int k = 0; k < 3; ++k) {
+    const std::vector<uint64_t> h = histogram(w, n, shift[k], 31);
+    int nsym = 0, single = 0;
+    for (int s = 0; s < 32; ++s)
+      if (h[s]) { ++nsym; single = s; }
+    f[k]->nsym = (uint8_t)nsym;
+    f[k]->single = (uint8_t)(nsym == 1 ? single : 0);
+    limited_lengths(h.data(), 32, (int)lmax, f[k]->len);
+  }
+  return HL_OK;
+}
+
+extern "C" hl_status hl_encode16(const uint16_t* w, uint64_t rows, uint64_t cols, const hl_codebook16* cb,
+                                 uint32_t seg_len, uint32_t grp_rows, uint32_t nthreads, void* out,
+                                 size_t* out_bytes) {
+  if (!w || !cb || !out_bytes) return HL_EINVAL;
+  uint32_t S, GR;
+  if (!resolve_shape(rows, cols, seg_len, grp_rows, &S, &GR)) return HL_EINVAL;
+  if (!code16_valid(*cb)) return HL_EINVAL;
+  return encode_body(w, rows, cols, S, GR, nthreads, HL_FORMAT_FP16, cb->lmax, nullptr, nullptr, cb,
+                     F16Coder(*cb), out, out_bytes);
 }
 
 namespace hl {

@@ -997,7 +997,7 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   const uint32_t jmax = kRows - 3;
   const uint32_t i = lane & 15, q = lane >> 4;
   const uint16_t* xlane = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
-  const uint32_t CB = a.CB, RB = a.RB, L = a.L, nj = (CB + waves - 1) / waves;
+  const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
   const uint32_t last_group = RB * CB - 1;
 
   // the wave's groups in order: round t (row block blockIdx.x + t*grid), step
@@ -1353,6 +1353,7 @@ extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
   t.format = H.format;
   t.cb = H.cb;
   t.cb8 = H.cb8;
+  t.cb16 = H.cb16;
   *out = t;
   return HL_OK;
 }

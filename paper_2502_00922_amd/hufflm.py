@@ -17,8 +17,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libhufflm.so")
 
 HL_OK, HL_EINVAL, HL_ENOMEM, HL_ECORRUPT, HL_EUNSUPPORTED, HL_EHIP = range(6)
-HL_F32, HL_BF16 = 0, 1
-HL_FORMAT_SPLIT, HL_FORMAT_WHOLE_EXPONENT = 0, 1
+HL_F32, HL_BF16, HL_F16 = 0, 1, 2
+HL_FORMAT_SPLIT, HL_FORMAT_WHOLE_EXPONENT, HL_FORMAT_FP16 = 0, 1, 2
 HEADER_BYTES = 128
 LUT_BYTES = 33024
 MAX_BATCH = 16
@@ -51,6 +51,18 @@ class Codebook8(ctypes.Structure):
         return list(self.len)
 
 
+class FieldCode5(ctypes.Structure):
+    _fields_ = [("nsym", ctypes.c_uint8), ("single", ctypes.c_uint8), ("len", ctypes.c_uint8 * 32)]
+
+    @property
+    def lengths(self):
+        return list(self.len)
+
+
+class Codebook16(ctypes.Structure):
+    _fields_ = [("lmax", ctypes.c_uint32), ("e", FieldCode5), ("mh", FieldCode5), ("ml", FieldCode5)]
+
+
 class TensorView(ctypes.Structure):
     _fields_ = [("blob_dev", ctypes.c_void_p), ("lut_dev", ctypes.c_void_p),
                 ("rows", ctypes.c_uint64), ("cols", ctypes.c_uint64), ("n_seg", ctypes.c_uint64),
@@ -60,13 +72,13 @@ class TensorView(ctypes.Structure):
                 ("seg_len", ctypes.c_uint32), ("grp_rows", ctypes.c_uint32), ("lmax", ctypes.c_uint32),
                 ("max_grp_units", ctypes.c_uint32), ("max_seg_bits", ctypes.c_uint32),
                 ("format", ctypes.c_uint32),
-                ("cb", Codebook), ("cb8", Codebook8)]
+                ("cb", Codebook), ("cb8", Codebook8), ("cb16", Codebook16)]
 
 
 _lib = None
 
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
-           "hl_build_codebook8", "hl_encode8", "hl_validate",
+           "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
            "hl_decode_gemv", "hl_gemv_bf16"]
 
@@ -96,6 +108,11 @@ def lib() -> ctypes.CDLL:
     L.hl_encode8.restype = c.c_int
     L.hl_encode8.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook8), c.c_uint32,
                              c.c_uint32, c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
+    L.hl_build_codebook16.restype = c.c_int
+    L.hl_build_codebook16.argtypes = [c.c_void_p, c.c_size_t, c.c_uint32, c.POINTER(Codebook16)]
+    L.hl_encode16.restype = c.c_int
+    L.hl_encode16.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook16), c.c_uint32,
+                              c.c_uint32, c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
     L.hl_validate.restype = c.c_int
     L.hl_validate.argtypes = [c.c_void_p, c.c_size_t]
     L.hl_tensor_view.restype = c.c_int
@@ -144,21 +161,33 @@ def build_codebook8(w: np.ndarray, lmax: int = 12) -> Codebook8:
     return cb
 
 
+def build_codebook16(w: np.ndarray, lmax: int = 12) -> Codebook16:
+    """Float16 codes: one 32-symbol code per 5-bit field (exponent, mantissa halves)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    cb = Codebook16()
+    _check(lib().hl_build_codebook16(w.ctypes.data, w.size, lmax, ctypes.byref(cb)), "hl_build_codebook16")
+    return cb
+
+
 def default_grp_rows(cols: int, seg_len: int = 0) -> int:
     return int(lib().hl_default_grp_rows(cols, seg_len))
 
 
 def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook=None,
-           nthreads: int = 0, grp_rows: int = 0, whole_exponent: bool = False) -> np.ndarray:
+           nthreads: int = 0, grp_rows: int = 0, whole_exponent: bool = False, fp16: bool = False) -> np.ndarray:
     """HLF1 container (uint8 array) of a bf16 matrix given as uint16 bits [rows, cols].
 
     whole_exponent selects the format with one 256-symbol exponent code
-    (``codebook`` then is a Codebook8)."""
+    (``codebook`` then is a Codebook8); fp16 takes float16 bits and selects the
+    {1,5,5,5} format (``codebook``: a Codebook16)."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     if w.ndim != 2:
         raise ValueError("expected a 2-D matrix")
     L = lib()
-    if whole_exponent:
+    if fp16:
+        cb = codebook if codebook is not None else build_codebook16(w, lmax)
+        fn, name = L.hl_encode16, "hl_encode16"
+    elif whole_exponent:
         cb = codebook if codebook is not None else build_codebook8(w, lmax)
         fn, name = L.hl_encode8, "hl_encode8"
     else:

@@ -8,7 +8,7 @@ import re
 import numpy as np
 import pytest
 
-from gen import random_bf16
+from gen import random_bf16, random_fp16
 from oracle import codec
 
 hl = pytest.importorskip("paper_2502_00922_amd.hufflm")
@@ -217,3 +217,80 @@ def test_whole_exponent_validate_rejects_damage():
     assert hl.validate(damaged(h["off_seg_bits"], 0xFFFF, 2)) == hl.HL_ECORRUPT
     # a split-format header over the whole-exponent body
     assert hl.validate(damaged(7, 0)) == hl.HL_ECORRUPT
+
+
+# ---------------------------------------------------------------- float16 format
+def _cb16_lists(cb):
+    return [(f.nsym, f.single, list(f.len)) for f in (cb.e, cb.mh, cb.ml)]
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_codebook16_equals_oracle(seed):
+    w = random_fp16((32, 256), seed, std=[0.002, 0.02, 0.5][seed])
+    for lmax in (5, 9, 12):
+        cb = hl.build_codebook16(w, lmax=lmax)
+        ref = codec.build_codebooks16(w, lmax)
+        assert _cb16_lists(cb) == [(c.nsym, c.single, c.lengths if c.nsym > 1 else [0] * 32) for c in ref]
+
+
+CASES16 = [((64, 1024), 64, 12, 0), ((130, 48), 16, 12, 0), ((3, 64), 8, 5, 0), ((65, 96), 32, 9, 0),
+           ((130, 512), 64, 12, 8), ((37, 256), 32, 7, 32), ((1, 8), 8, 12, 0), ((21, 512), 8, 12, 1),
+           ((200, 512), 512, 12, 0)]
+
+
+@pytest.mark.parametrize("shape,S,lmax,GR", CASES16)
+def test_fp16_byte_identical_to_oracle(shape, S, lmax, GR):
+    w = random_fp16(shape, seed=sum(shape) + S + 2)
+    a = bytes(hl.encode(w, seg_len=S, lmax=lmax, grp_rows=GR, fp16=True))
+    assert a == codec.encode16(w, seg_len=S, lmax=lmax, grp_rows=GR or None)
+    assert hl.validate(a) == 0
+
+
+def test_fp16_adversarial_and_threads():
+    # every float16 pattern once: all fields uniform over 32 symbols
+    w = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(128, 512)
+    for lmax in (5, 12):
+        assert bytes(hl.encode(w, seg_len=64, lmax=lmax, fp16=True)) == codec.encode16(w, 64, lmax)
+    # geometric exponents with long codes cut by the limit; constant mantissa-low
+    rng = np.random.default_rng(4)
+    e = np.minimum(rng.geometric(0.4, 64 * 256), 30).astype(np.uint32)
+    w = ((rng.integers(0, 2, e.size) << 15) | (e << 10) | (rng.integers(0, 32, e.size) << 5))
+    w = w.astype(np.uint16).reshape(64, 256)
+    for lmax in (5, 8, 12):
+        assert bytes(hl.encode(w, seg_len=32, lmax=lmax, fp16=True)) == codec.encode16(w, 32, lmax)
+    w = random_fp16((300, 256), seed=6)
+    a = hl.encode(w, seg_len=64, nthreads=1, fp16=True)
+    for t in (3, 16):
+        assert np.array_equal(a, hl.encode(w, seg_len=64, nthreads=t, fp16=True))
+    for bad in (4, 13):
+        with pytest.raises(hl.HLError):
+            hl.build_codebook16(w, lmax=bad)
+    other = hl.build_codebook16(np.full((8, 64), 0x3C00, np.uint16))
+    with pytest.raises(hl.HLError):
+        hl.encode(w, seg_len=64, codebook=other, fp16=True)
+
+
+def test_fp16_validate_rejects_damage():
+    w = random_fp16((130, 256), seed=8)
+    good = hl.encode(w, seg_len=64, fp16=True)
+    assert hl.validate(good) == 0
+    h = codec.parse_header(bytes(good))
+    mh_lens = h["cb16"][1][2]
+    s_long = max(range(32), key=lambda s: mh_lens[s])
+
+    def damaged(offset, value, width=1):
+        b = good.copy()
+        b[offset:offset + width] = np.frombuffer(int(value).to_bytes(width, "little"), np.uint8)
+        return b
+
+    assert hl.validate(good[:-1]) == hl.HL_ECORRUPT                       # sign plane cut short
+    assert hl.validate(good[:255]) == hl.HL_ECORRUPT
+    assert hl.validate(damaged(7, 3)) == hl.HL_ECORRUPT                   # unknown format
+    assert hl.validate(damaged(6, 13)) == hl.HL_ECORRUPT                  # lmax above 12
+    assert hl.validate(damaged(6, 4)) == hl.HL_ECORRUPT                   # lmax below 5
+    assert hl.validate(damaged(128 + 34 + 2 + s_long, mh_lens[s_long] - 1)) == hl.HL_ECORRUPT  # Kraft
+    assert hl.validate(damaged(128 + 34, h["cb16"][1][0] + 1)) == hl.HL_ECORRUPT  # symbol count
+    assert hl.validate(damaged(128 + 110, 1)) == hl.HL_ECORRUPT           # section padding
+    assert hl.validate(damaged(93, 1)) == hl.HL_ECORRUPT                  # header bytes 92..127
+    assert hl.validate(damaged(h["off_seg_bits"], 0xFFFF, 2)) == hl.HL_ECORRUPT
+    assert hl.validate(damaged(7, 0)) == hl.HL_ECORRUPT                   # split header over the body
