@@ -121,7 +121,7 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1, HL_F16 = 2 } hl_dtype;
 #define HL_HEADER_BYTES 128u
 #define HL_GROUP_SEGS 64u
 #define HL_MAX_BATCH 16u
-#define HL_LUT_BYTES 33024u   /* 8192 joint entries + 64 words of tables */
+#define HL_LUT_BYTES 49440u   /* decode tables of the largest format (float16) */
 #define HL_LEN8_BYTES 256u    /* whole-exponent code lengths after the header */
 #define HL_LMAX8_MIN 8u
 #define HL_LMAX8_MAX 13u

@@ -39,7 +39,7 @@ constexpr uint32_t kEsc = 0x80u;       // entry of a pair longer than the window
 constexpr int kMaxWaves = 16;
 constexpr uint32_t kCol = 64;          // row stride of the stream columns, in words
 
-static_assert(HL_LUT_BYTES == (kLutN + kAuxWords) * 4, "table size");
+static_assert(HL_LUT_BYTES >= (kLutN + kAuxWords) * 4, "table size");
 
 // Joint table entry: bits 0..4 = code bits of the (el, eh) pair, bits 23..30 =
 // the exponent byte eh<<4|el (its place in a float32), all other bits zero.
@@ -53,36 +53,39 @@ struct Aux {
   uint32_t w[kAuxWords];
 };
 
+// One field's canonical tables in the aux format above, for an alphabet of
+// `alpha` symbols (16 or 32: the symbol bytes fill words 16..19 or 16..23).
+static void fill_aux_field(uint32_t* w, const uint8_t* len, int alpha, int nsym, int single) {
+  uint32_t code[32];
+  canonical_codes(len, alpha, code);
+  int maxl = 0;
+  for (int s = 0; s < alpha; ++s) maxl = std::max(maxl, (int)len[s]);
+  if (nsym == 1) maxl = 0;
+  w[0] = (uint32_t)nsym | ((uint32_t)single << 8) | ((uint32_t)maxl << 16);
+  int k = 0;
+  uint8_t sorted[32] = {0};
+  for (int l = 1; l <= 15; ++l) {
+    int first = -1, cnt = 0, off = k;
+    for (int s = 0; s < alpha; ++s) {
+      if (nsym > 1 && len[s] == l) {
+        if (first < 0) first = (int)code[s];
+        sorted[k++] = (uint8_t)s;
+        ++cnt;
+      }
+    }
+    w[l] = ((uint32_t)(first < 0 ? 0 : first) << 16) | ((uint32_t)cnt << 8) | (uint32_t)off;
+  }
+  for (int i = 0; i < alpha; ++i) w[16 + i / 4] |= (uint32_t)sorted[i] << (8 * (i % 4));
+}
+
 static Aux make_aux(const hl_codebook& cb) {
   Aux a;
   std::memset(&a, 0, sizeof(a));
-  const hl_field_code* fs[2] = {&cb.eh, &cb.el};
-  for (int f = 0; f < 2; ++f) {
-    const hl_field_code& fc = *fs[f];
-    uint32_t* w = a.w + f * kAuxField;
-    uint32_t code[16];
-    canonical_codes(fc.len, 16, code);
-    int maxl = 0;
-    for (int s = 0; s < 16; ++s) maxl = std::max(maxl, (int)fc.len[s]);
-    if (fc.nsym == 1) maxl = 0;
-    w[0] = (uint32_t)fc.nsym | ((uint32_t)fc.single << 8) | ((uint32_t)maxl << 16);
-    int k = 0;
-    uint8_t sorted[16] = {0};
-    for (int l = 1; l <= 15; ++l) {
-      int first = -1, cnt = 0, off = k;
-      for (int s = 0; s < 16; ++s) {
-        if (fc.nsym > 1 && fc.len[s] == l) {
-          if (first < 0) first = (int)code[s];
-          sorted[k++] = (uint8_t)s;
-          ++cnt;
-        }
-      }
-      w[l] = ((uint32_t)(first < 0 ? 0 : first) << 16) | ((uint32_t)cnt << 8) | (uint32_t)off;
-    }
-    for (int i = 0; i < 16; ++i) w[16 + i / 4] |= (uint32_t)sorted[i] << (8 * (i % 4));
-  }
+  fill_aux_field(a.w, cb.eh.len, 16, cb.eh.nsym, cb.eh.single);
+  fill_aux_field(a.w + kAuxField, cb.el.len, 16, cb.el.nsym, cb.el.single);
   return a;
 }
+
 
 // ------------------------------------------------------------------ device
 
@@ -804,6 +807,63 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
+// Sum of the waves' 16x16 accumulators and the output (fixed order), for the
+// matrix-core kernels; `red` is LDS free for 16 floats per lane per wave.
+__device__ inline void mfma_finish(const GemvArgs& p, const f32x4_t& acc, float* red, uint32_t wave,
+                                   uint32_t waves, uint32_t lane, uint32_t rb, uint32_t kp, uint32_t r0,
+                                   uint32_t G) {
+  const GroupArgs& a = p.g;
+  const uint32_t i = lane & 15, q = lane >> 4;
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < 4; ++v) red[(wave * 4 + v) * 64 + lane] = acc[v];
+  __syncthreads();
+  const uint32_t n = i, ldy = a.rows;
+  const bool nb_ok = n < p.B;
+  if (p.KS == 1) {
+    // waves 0..3 each finish one of the four values of every lane
+    if (wave >= 4 || wave >= waves) return;
+    const uint32_t v = wave;
+    float t = red[v * 64 + lane];
+    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
+    if (nb_ok && 4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
+    return;
+  }
+  if (wave != 0) return;
+  float s[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    float t = red[v * 64 + lane];
+    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
+    s[v] = t;
+  }
+  // Split over column blocks: the same protocol as the vector kernel.
+  const uint32_t ldp = a.RB * 16;
+  if (nb_ok)
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      if (4 * q + v < G)
+        __hip_atomic_store(p.partial + ((uint64_t)kp * p.B + n) * ldp + r0 + 4 * q + v, s[v], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+  wait_vm0();
+  uint32_t old = 0;
+  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  old = __shfl(old, 0, 64);
+  if (old != p.KS - 1) return;
+  if (nb_ok) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      if (4 * q + v >= G) continue;
+      float t = 0.f;
+      for (uint32_t k = 0; k < p.KS; ++k)
+        t += __hip_atomic_load(p.partial + ((uint64_t)k * p.B + n) * ldp + r0 + 4 * q + v, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
+    }
+  }
+  if (lane == 0) __hip_atomic_store(p.counter + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Fused decode-GEMV for 16-row groups (GR = 16, GC = 4) and bf16 x, on the
 // 16x16x32 bf16 matrix instruction. A group is exactly one A operand per
 // 8-weight step: lane l = 16q + i decodes row r0 + i of column segment c0 + q,
@@ -918,55 +978,7 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
   }
   wait_vm0();  // prefetches past the last group
   // Sum over waves in a fixed order (the wave regions are free now).
-  __syncthreads();
-  float* red = reinterpret_cast<float*>(s_dyn);
-#pragma unroll
-  for (int v = 0; v < 4; ++v) red[(wave * 4 + v) * 64 + lane] = acc[v];
-  __syncthreads();
-  const uint32_t n = i, ldy = a.rows;
-  const bool nb_ok = n < p.B;
-  if (p.KS == 1) {
-    // waves 0..3 each finish one of the four values of every lane
-    if (wave >= 4 || wave >= waves) return;
-    const uint32_t v = wave;
-    float t = red[v * 64 + lane];
-    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
-    if (nb_ok && 4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
-    return;
-  }
-  if (wave != 0) return;
-  float s[4];
-#pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    float t = red[v * 64 + lane];
-    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
-    s[v] = t;
-  }
-  // Split over column blocks: the same protocol as the vector kernel.
-  const uint32_t ldp = a.RB * 16;
-  if (nb_ok)
-#pragma unroll
-    for (int v = 0; v < 4; ++v)
-      if (4 * q + v < G)
-        __hip_atomic_store(p.partial + ((uint64_t)kp * p.B + n) * ldp + r0 + 4 * q + v, s[v], __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-  wait_vm0();
-  uint32_t old = 0;
-  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  old = __shfl(old, 0, 64);
-  if (old != p.KS - 1) return;
-  if (nb_ok) {
-#pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      if (4 * q + v >= G) continue;
-      float t = 0.f;
-      for (uint32_t k = 0; k < p.KS; ++k)
-        t += __hip_atomic_load(p.partial + ((uint64_t)k * p.B + n) * ldp + r0 + 4 * q + v, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-      p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
-    }
-  }
-  if (lane == 0) __hip_atomic_store(p.counter + rb, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  mfma_finish(p, acc, reinterpret_cast<float*>(s_dyn), wave, waves, lane, rb, kp, r0, G);
 }
 
 // ------------------------------------------------------------------ persistent fused GEMV
@@ -1120,6 +1132,321 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   wait_vm0();  // prefetches past the last group
 }
 
+// ------------------------------------------------------------------ float16 format
+
+// Decode tables of the float16 {1,5,5,5} format. Its kernels use no static
+// LDS: the tables sit at the start of the dynamic LDS, the wave regions after.
+//   [0, 8192)       pair table: entry v = the codes code(ml) code(e) that the
+//                   13-bit window v (bit 0 first) starts with: total length in
+//                   bits 0..4, (e<<10 | ml) in bits 16..30; kEsc16 if the pair
+//                   is longer than 13 bits;
+//   [8192, 12288)   mantissa-high table: entry v = code(mh) at the start of
+//                   the 12-bit window v: length in bits 0..4, mh<<5 in bits
+//                   16..30 (lmax <= 12, so every window matches);
+//   [12288, 12360)  canonical tables of ml, e and mh in the aux format, for
+//                   the bit-serial path.
+// ORing a weight's pair and mantissa-high entries gives its bits 0..14 in
+// bits 16..30. In the fast loop a position accumulates whole entries: bits
+// 0..15 are the position (a column holds fewer than 2^16 bits), the weight
+// bits pile up above. An escape adds 256, which eight weights of at most
+// 13 + 12 code bits (200) cannot reach.
+constexpr int kLutMBits = 12;
+constexpr int kLutMN = 1 << kLutMBits;
+constexpr int kAux16Words = 3 * kAuxField;
+constexpr uint32_t kTab16Words = kLutN + kLutMN + kAux16Words;
+constexpr uint32_t kEsc16 = 0x100u;
+constexpr uint32_t kPosMask16 = 0xFFFFu;
+constexpr uint32_t kAuxMl = 0, kAuxE = kAuxField, kAuxMh = 2 * kAuxField;
+
+static_assert(HL_LUT_BYTES == kTab16Words * 4, "the table buffer holds the largest format's tables");
+static_assert(kTab16Words % 4 == 0, "tables copy in 16-byte pieces");
+
+struct Aux16 {
+  uint32_t w[kAux16Words];
+};
+
+static Aux16 make_aux16(const hl_codebook16& cb) {
+  Aux16 a;
+  std::memset(&a, 0, sizeof(a));
+  fill_aux_field(a.w + kAuxMl, cb.ml.len, 32, cb.ml.nsym, cb.ml.single);
+  fill_aux_field(a.w + kAuxE, cb.e.len, 32, cb.e.nsym, cb.e.single);
+  fill_aux_field(a.w + kAuxMh, cb.mh.len, 32, cb.mh.nsym, cb.mh.single);
+  return a;
+}
+
+__global__ void __launch_bounds__(256) lut16_kernel(uint32_t* lut, Aux16 aux) {
+  for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
+    uint32_t ul = 0, ue = 0;
+    const int l = field_from_bits(aux.w + kAuxMl, (uint32_t)v, kLutBits, &ul);  // ml first
+    const int e = l < 0 ? -1 : field_from_bits(aux.w + kAuxE, (uint32_t)v >> ul, kLutBits - ul, &ue);
+    lut[v] = (l < 0 || e < 0) ? kEsc16 : ((ul + ue) | ((uint32_t)((e << 10) | l) << 16));
+  }
+  for (int v = threadIdx.x; v < kLutMN; v += blockDim.x) {
+    uint32_t um = 0;
+    const int m = field_from_bits(aux.w + kAuxMh, (uint32_t)v, kLutMBits, &um);
+    lut[kLutN + v] = m < 0 ? kEsc16 : (um | ((uint32_t)m << 21));
+  }
+  for (int i = threadIdx.x; i < kAux16Words; i += blockDim.x) lut[kLutN + kLutMN + i] = aux.w[i];
+}
+
+// Copies the float16 tables to the start of the dynamic LDS (16-byte pieces
+// through registers; kernels that wait on nothing else).
+__device__ inline void load_tables16(const uint32_t* lut) {
+  constexpr uint32_t kVec = kTab16Words / 4;
+  const uint4* src = reinterpret_cast<const uint4*>(lut);
+  uint4* dst = reinterpret_cast<uint4*>(s_dyn);
+  for (uint32_t k = threadIdx.x; k < kVec; k += blockDim.x) dst[k] = src[k];
+}
+
+// The same copy as direct global-to-LDS transfers (the caller waits, vmcnt).
+__device__ inline void table16_dma(const uint32_t* lut) {
+  constexpr uint32_t kVec = kTab16Words / 4;
+  const uint32_t n = blockDim.x, w0 = threadIdx.x & ~63u, lane = threadIdx.x & 63;
+  for (uint32_t k0 = w0; k0 < kVec; k0 += n)
+    if (k0 + lane < kVec) dma16(lut + (k0 + lane) * 4, s_dyn + k0 * 4);
+}
+
+__device__ inline uint32_t tab16_pair(uint32_t w) {
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + (w & ((kLutN - 1) << 2)));
+}
+__device__ inline uint32_t tab16_mh(uint32_t w) {
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + kLutN * 4 +
+                                            (w & ((kLutMN - 1) << 2)));
+}
+
+// 64-bit window of column bits [pos2, pos2 + 64), positions read through kPosMask16.
+__device__ inline uint64_t load_window16(const uint32_t* sc, uint32_t pos2, uint32_t jmax) {
+  const uint32_t j = min((pos2 & kPosMask16) >> 5, jmax);
+  const uint32_t a = col_word(sc, j), b = col_word(sc, j + 1), c = col_word(sc, j + 2);
+  return ((uint64_t)__builtin_amdgcn_alignbit(c, b, pos2) << 32) | __builtin_amdgcn_alignbit(b, a, pos2);
+}
+
+// Two weights from one 64-bit window (two weights of at most 13 + 12 code
+// bits fit): h[0..1] = weight bits 0..14 in bits 16..30 (other bits
+// meaningless), p advanced by the four whole entries.
+__device__ inline void decode2_f16(const uint32_t* sc, uint32_t jmax, uint32_t& p, uint32_t* h) {
+  uint64_t W = load_window16(sc, p, jmax);
+  const uint32_t a0 = tab16_pair((uint32_t)W);
+  W = shift_window(W, a0);
+  const uint32_t m0 = tab16_mh((uint32_t)W);
+  W = shift_window(W, m0);
+  const uint32_t a1 = tab16_pair((uint32_t)W);
+  W = shift_window(W, a1);
+  const uint32_t m1 = tab16_mh((uint32_t)W);
+  p = p + a0 + m0 + a1 + m1;
+  h[0] = a0 | m0;
+  h[1] = a1 | m1;
+}
+
+struct Dec8 {
+  uint32_t pos2, h[8];
+};
+
+// Careful path of the float16 format: eight weights, each field decoded
+// bit-serially (code(ml), code(e), code(mh)); pos2 clean (no weight bits
+// above bit 15).
+__device__ __attribute__((always_inline)) inline Dec8 decode8_f16_careful_body(uint32_t sc_off, uint32_t jmax,
+                                                                               uint32_t pos2) {
+  asm volatile("" ::: "memory");  // keeps its table reads inside the (cold) path
+  const uint32_t* sc = s_dyn + sc_off;
+  const uint32_t* aux = s_dyn + kLutN + kLutMN;
+  Dec8 d;
+  uint32_t p = pos2 + 2;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    const uint32_t ml = slow_field(sc, aux + kAuxMl, p, jmax + 2);
+    const uint32_t e = slow_field(sc, aux + kAuxE, p, jmax + 2);
+    const uint32_t mh = slow_field(sc, aux + kAuxMh, p, jmax + 2);
+    d.h[k] = (((e & 31) << 10) | ((mh & 31) << 5) | (ml & 31)) << 16;
+  }
+  d.pos2 = p - 2;
+  return d;
+}
+
+__device__ __noinline__ Dec8 decode8_f16_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
+  return decode8_f16_careful_body(sc_off, jmax, pos2);
+}
+
+// Eight float16 weights' bits 0..14 (in bits 16..30 of h[k]). A pair past the
+// 13-bit window anywhere sends the lane through the careful path from the
+// first of the eight (the fast entries read after an escape are discarded).
+__device__ inline void decode8_f16(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* h) {
+  const uint32_t p0 = pos2;
+  uint32_t p = p0;
+  decode2_f16(sc, jmax, p, h);
+  decode2_f16(sc, jmax, p, h + 2);
+  decode2_f16(sc, jmax, p, h + 4);
+  decode2_f16(sc, jmax, p, h + 6);
+  if (__builtin_expect(((p - p0) & 0xFF00u) != 0, 0)) {
+    const Dec8 d = decode8_f16_careful(sc_off, jmax, p0 & kPosMask16);
+    p = d.pos2;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) h[k] = d.h[k];
+  }
+  pos2 = p;
+}
+
+// Eight float16 weights packed in pairs (weight 2m in the low half of dword
+// m) from their decoded bits and the step's sign byte (bit k: weight k).
+__device__ inline uint4 pack8_f16(const uint32_t* h, uint32_t sb) {
+  uint32_t d[4];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const uint32_t v = __builtin_amdgcn_perm(h[2 * m + 1], h[2 * m], 0x07060302u) & 0x7FFF7FFFu;
+    d[m] = v | (((sb >> (2 * m)) & 1u) << 15) | (((sb >> (2 * m + 1)) & 1u) << 31);
+  }
+  return uint4{d[0], d[1], d[2], d[3]};
+}
+
+// Decode to float16 bits; waves take groups in turn; region per wave: the
+// stream columns. Signs are read straight from the sign plane.
+__global__ void __launch_bounds__(1024) decode16_kernel(GroupArgs a, uint16_t* out) {
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t waves = blockDim.x >> 6;
+  const uint32_t per_wave = a.col_rows * kCol;
+  uint32_t* cols = s_dyn + kTab16Words + wave * per_wave;
+  const uint32_t sc_off = kTab16Words + wave * per_wave + lane;
+  const uint32_t* sc = s_dyn + sc_off;
+  const uint32_t jmax = a.col_rows - 3;
+  const uint32_t n_grp = a.RB * a.CB;
+  const uint32_t stride = gridDim.x * waves;
+  const uint32_t sb_per_seg = a.S / 8;
+  uint32_t g = blockIdx.x * waves + wave;
+  Meta m;
+  if (g < n_grp) m = load_meta(a, g, lane);
+  load_tables16(a.lut);
+  __syncthreads();
+  for (; g < n_grp; g += stride) {
+    uint32_t pos2 = issue_stream(a, cols, m, lane);
+    const Meta cur = m;
+    if (g + stride < n_grp) m = load_meta(a, g + stride, lane);
+    wait_vm0();
+    wave_sync_lds();
+    if (lane < cur.N) {
+      const uint32_t i = lane % cur.G, j = lane / cur.G;
+      uint16_t* o = out + (uint64_t)(cur.r0 + i) * a.cols + (uint64_t)(cur.c0 + j) * a.S;
+      const uint8_t* sg = a.raw + (cur.first + lane) * sb_per_seg;
+      for (uint32_t t = 0; t < a.S; t += 8) {
+        uint32_t h[8];
+        decode8_f16(sc, sc_off, jmax, pos2, h);
+        *reinterpret_cast<uint4*>(o + t) = pack8_f16(h, sg[t >> 3]);
+      }
+    }
+    wait_lgkm0();
+    wave_sync_lds();
+  }
+}
+
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+
+// The lane's sign bytes of one group (S/8 = SP bytes of its segment).
+template <int SP>
+struct Signs {
+  uint4 v;
+  __device__ inline void load(const uint8_t* p) {
+    if constexpr (SP == 16) {
+      v = *reinterpret_cast<const uint4*>(p);
+    } else if constexpr (SP == 8) {
+      const uint2 t = *reinterpret_cast<const uint2*>(p);
+      v = uint4{t.x, t.y, 0u, 0u};
+    } else if constexpr (SP == 4) {
+      v = uint4{*reinterpret_cast<const uint32_t*>(p), 0u, 0u, 0u};
+    } else if constexpr (SP == 2) {
+      v = uint4{(uint32_t)*reinterpret_cast<const uint16_t*>(p), 0u, 0u, 0u};
+    } else {
+      v = uint4{(uint32_t)*p, 0u, 0u, 0u};
+    }
+  }
+  __device__ inline uint32_t byte(int t) const {
+    const uint32_t w = (t >> 2) == 0 ? v.x : (t >> 2) == 1 ? v.y : (t >> 2) == 2 ? v.z : v.w;
+    return (w >> (8 * (t & 3))) & 0xFFu;
+  }
+};
+
+// Fused decode-GEMV of the float16 format on the 16x16x32 float16 matrix
+// instruction (16-row groups, float16 x): the bf16 matrix-core kernel's
+// structure (lane 16q + i decodes row i of segment q; the A operand is its 8
+// weights, the B operand x[n = i][8 activations]), with the float16 decode
+// (two table reads per weight) and one sign load per lane and group.
+template <int SP>
+__global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
+  constexpr int KP = SP < 8 ? SP : SP == 8 ? 8 : 4;
+  const GroupArgs& a = p.g;
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t waves = blockDim.x >> 6;
+  constexpr uint32_t S = SP * 8;
+  const uint32_t per_wave = a.col_rows * kCol;
+  uint32_t* cols = s_dyn + kTab16Words + wave * per_wave;
+  const uint32_t jmax = a.col_rows - 3;
+
+  const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
+  const uint32_t r0 = rb * 16;
+  const uint32_t G = min(16u, a.rows - r0);
+  const uint32_t i = lane & 15, q = lane >> 4;
+  const uint32_t mu = q * G + min(i, G - 1);  // the segment this lane decodes
+  const uint32_t sc_off = kTab16Words + wave * per_wave + mu;
+  const uint32_t* sc = s_dyn + sc_off;
+  const uint16_t* xrow = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
+
+  const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
+  uint32_t cb = kp * p.C + wave;
+  const uint32_t cb0 = min(cb, a.CB - 1);
+  Meta m = load_meta(a, rb * a.CB + cb0, lane);
+  Meta mn = load_meta(a, rb * a.CB + (cb + waves < cb_end ? cb + waves : cb0), lane);
+  uint4 xv[KP];
+  Signs<SP> sg;
+  {
+    const uint16_t* x = xrow + m.c0 * S;
+#pragma unroll
+    for (int k = 0; k < KP; ++k) xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
+    sg.load(a.raw + (m.first + mu) * SP);
+  }
+  asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
+  table16_dma(a.lut);
+  uint32_t pos2 = issue_stream(a, cols, m, lane);
+  wait_vm0();
+  __syncthreads();
+
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (; cb < cb_end; cb += waves) {
+    const Meta cur = m;
+    const bool more = cb + waves < cb_end;
+    wait_vm0();
+    wave_sync_lds();
+    const uint32_t pos2l = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+    const uint16_t* xcur = xrow + cur.c0 * S;
+    const uint16_t* xnext = more ? xrow + mn.c0 * S : xcur;
+    const uint32_t xs_last = more ? 8u : 0u;
+    const Signs<SP> sgc = sg;
+    uint32_t pd = pos2l;
+#pragma unroll
+    for (int t0 = 0; t0 < SP; t0 += KP) {
+      const bool last = t0 + KP == SP;
+      const uint16_t* xp = last ? xnext : xcur + (t0 + KP) * 8;
+      const uint32_t xs = last ? xs_last : 8u;
+#pragma unroll
+      for (int k = 0; k < KP; ++k) {
+        uint32_t h[8];
+        decode8_f16(sc, sc_off, jmax, pd, h);
+        const uint4 wv = pack8_f16(h, sgc.byte(t0 + k));
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, wv),
+                                                     __builtin_bit_cast(f16x8_t, xv[k]), acc, 0, 0, 0);
+        xv[k] = *reinterpret_cast<const uint4*>(xp + k * xs);
+      }
+    }
+    wait_lgkm0();
+    wave_sync_lds();
+    if (more) {
+      m = mn;
+      mn = load_meta(a, rb * a.CB + (cb + 2 * waves < cb_end ? cb + 2 * waves : cb + waves), lane);
+      pos2 = issue_stream(a, cols, m, lane);
+      sg.load(a.raw + (m.first + mu) * SP);
+    }
+  }
+  wait_vm0();  // prefetches past the last group
+  mfma_finish(p, acc, reinterpret_cast<float*>(s_dyn + kTab16Words), wave, waves, lane, rb, kp, r0, G);
+}
+
 // ------------------------------------------------------------------ bf16 GEMV
 
 // One wave per row; lanes stride the row in 8-weight chunks; dot2 on pairs.
@@ -1187,8 +1514,10 @@ constexpr uint32_t kMaxLds = 160 * 1024;
 struct Plan {
   GroupArgs ga;
   uint32_t waves;
-  size_t lds;
+  size_t lds;       // dynamic LDS: (float16 tables) + the wave regions
 };
+
+static bool is_fp16(const hl_tensor* t) { return t->format == HL_FORMAT_FP16; }
 
 // Rows of the stream columns: row 0 padding, the longest segment starting at
 // bit 31 of row 1, two rows of window overrun.
@@ -1218,12 +1547,14 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bo
   a.max_units = t->max_grp_units;
   a.col_rows = col_rows_for(t->max_seg_bits);
   const uint32_t per_wave = a.col_rows * kCol + (raw_lds ? 16 * t->seg_len : 0) + extra_words_per_wave;
-  // LDS: the static tables plus one region per wave.
-  const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
+  // LDS: the tables (static for the bf16 formats, at the start of the
+  // dynamic region for float16) plus one region per wave.
+  const size_t tab_static = is_fp16(t) ? 0 : (size_t)(kLutN + kAuxWords) * 4;
+  const size_t tab_dyn = is_fp16(t) ? (size_t)kTab16Words * 4 : 0;
   uint32_t waves = kMaxWaves;
-  while (waves > 1 && tab + (size_t)waves * per_wave * 4 > kMaxLds) --waves;
-  const size_t lds = (size_t)waves * per_wave * 4;
-  if (tab + lds > kMaxLds) return HL_EUNSUPPORTED;
+  while (waves > 1 && tab_static + tab_dyn + (size_t)waves * per_wave * 4 > kMaxLds) --waves;
+  const size_t lds = tab_dyn + (size_t)waves * per_wave * 4;
+  if (tab_static + lds > kMaxLds) return HL_EUNSUPPORTED;
   pl->waves = waves;
   pl->lds = lds;
   return HL_OK;
@@ -1360,6 +1691,10 @@ extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
 
 extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
   if (!t || !t->lut_dev) return HL_EINVAL;
+  if (t->format == HL_FORMAT_FP16) {
+    if (!code16_valid(t->cb16)) return HL_ECORRUPT;
+    return launch(lut16_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, make_aux16(t->cb16));
+  }
   if (t->format == HL_FORMAT_WHOLE_EXPONENT) {
     if (!code8_valid(t->cb8)) return HL_ECORRUPT;
     return launch(lut8_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, make_aux8(t->cb8));
@@ -1373,9 +1708,15 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
 extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream) {
   if (!out_dev) return HL_EINVAL;
   Plan pl;
-  hl_status st = make_plan(t, 0, true, &pl);
+  hl_status st = make_plan(t, 0, !is_fp16(t), &pl);
   if (st != HL_OK) return st;
   const uint32_t n_grp = pl.ga.RB * pl.ga.CB;
+  if (is_fp16(t)) {
+    const uint32_t per_cu = std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)pl.lds));
+    const uint32_t blocks = std::min<uint32_t>((n_grp + pl.waves - 1) / pl.waves, device_cus() * per_cu);
+    return launch(decode16_kernel, dim3(blocks), dim3(pl.waves * 64), pl.lds, (hipStream_t)stream, pl.ga,
+                  out_dev);
+  }
   const uint32_t per_cu =
       std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)(pl.lds + (kLutN + kAuxWords) * 4)));
   const uint32_t blocks = std::min<uint32_t>((n_grp + pl.waves - 1) / pl.waves, device_cus() * per_cu);
@@ -1397,11 +1738,73 @@ extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
   return workspace_counter_bytes(RB) + (uint64_t)ks_cap(CB) * batch * RB * GR * 4;
 }
 
+// Column blocks per block (C) and blocks per row block (KS) of the
+// non-persistent kernels: enough blocks to fill the device, each wave decoding
+// at least one group; split over column blocks only with room for partials.
+static void choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, void* workspace_dev,
+                         size_t workspace_bytes, GemvArgs* p) {
+  const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
+  const uint64_t target_waves = (uint64_t)device_cus() * 16;
+  const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * CB + target_waves - 1) / target_waves);
+  uint32_t C = std::min<uint32_t>(CB, pl.waves * gpw);
+  uint32_t KS = (CB + C - 1) / C;
+  if (KS > ks_cap(CB)) {
+    KS = ks_cap(CB);
+    C = (CB + KS - 1) / KS;
+    KS = (CB + C - 1) / C;
+  }
+  if (KS > 1 && (!workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch))) {
+    KS = 1;  // no room for partial sums: one block per row block
+    C = CB;
+  }
+  p->C = C;
+  p->KS = KS;
+  if (KS > 1) {
+    p->counter = reinterpret_cast<uint32_t*>(workspace_dev);
+    p->partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
+  }
+}
+
+static hl_status launch_mfma16(uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               const GemvArgs& p) {
+  switch (steps) {
+    case 1: return launch(gemv16_mfma_kernel<1>, grid, block, lds, s, p);
+    case 2: return launch(gemv16_mfma_kernel<2>, grid, block, lds, s, p);
+    case 4: return launch(gemv16_mfma_kernel<4>, grid, block, lds, s, p);
+    case 8: return launch(gemv16_mfma_kernel<8>, grid, block, lds, s, p);
+    case 16: return launch(gemv16_mfma_kernel<16>, grid, block, lds, s, p);
+    default: return HL_EUNSUPPORTED;
+  }
+}
+
+// Float16 format: the matrix-core kernel only (16-row groups, float16 x).
+static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, float* y_dev, void* workspace_dev,
+                        size_t workspace_bytes, hipStream_t stream) {
+  if (t->grp_rows != 16 || t->seg_len % 8 || !mfma_steps_ok(t->seg_len / 8)) return HL_EUNSUPPORTED;
+  Plan pl;
+  hl_status st = make_plan(t, 0, false, &pl);
+  if (st != HL_OK) return st;
+  GemvArgs p;
+  std::memset(&p, 0, sizeof(p));
+  p.g = pl.ga;
+  p.x = x_dev;
+  p.y = y_dev;
+  p.B = batch;
+  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p);
+  const dim3 grid(pl.ga.RB * p.KS), block(pl.waves * 64);
+  // the reduction reuses the wave regions: 4 floats per lane per wave
+  const size_t lds = std::max<size_t>(pl.lds, (size_t)kTab16Words * 4 + (size_t)pl.waves * 4 * 64 * 4);
+  return launch_mfma16(t->seg_len / 8, grid, block, lds, stream, p);
+}
+
 extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
                                     float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
-  if (!t || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || (x_dtype != HL_F32 && x_dtype != HL_BF16))
+  if (!t || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH ||
+      (x_dtype != HL_F32 && x_dtype != HL_BF16 && x_dtype != HL_F16))
     return HL_EINVAL;
   if (t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS) return HL_EINVAL;
+  if (is_fp16(t) != (x_dtype == HL_F16)) return HL_EUNSUPPORTED;
+  if (is_fp16(t)) return gemv16(t, x_dev, batch, y_dev, workspace_dev, workspace_bytes, (hipStream_t)stream);
   const bool xb = x_dtype == HL_BF16;
   // 16-row groups with bf16 activations run on the matrix cores; the vector
   // kernel stages raw bytes and the activation slice (GC*S columns per batch
@@ -1436,27 +1839,9 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
                            p);
     }
   }
-  // Column blocks per block: enough blocks to fill the device, each wave
-  // decoding at least one group; KS blocks share a row block.
-  const uint64_t target_waves = (uint64_t)cus * 16;
-  const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * CB + target_waves - 1) / target_waves);
-  uint32_t C = std::min<uint32_t>(CB, pl.waves * gpw);
-  uint32_t KS = (CB + C - 1) / C;
-  if (KS > ks_cap(CB)) {
-    KS = ks_cap(CB);
-    C = (CB + KS - 1) / KS;
-    KS = (CB + C - 1) / C;
-  }
-  if (KS > 1 && (!workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch))) {
-    KS = 1;  // no room for partial sums: one block per row block
-    C = CB;
-  }
-  p.C = C;
-  p.KS = KS;
-  if (KS > 1) {
-    p.counter = reinterpret_cast<uint32_t*>(workspace_dev);
-    p.partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
-  }
+  // Column blocks per block and blocks per row block.
+  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p);
+  const uint32_t KS = p.KS;
   const dim3 grid(RB * KS), block(pl.waves * 64);
   if (mfma) {
     // the reduction reuses the wave regions: 4 floats per lane per wave

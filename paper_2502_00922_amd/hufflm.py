@@ -20,7 +20,7 @@ HL_OK, HL_EINVAL, HL_ENOMEM, HL_ECORRUPT, HL_EUNSUPPORTED, HL_EHIP = range(6)
 HL_F32, HL_BF16, HL_F16 = 0, 1, 2
 HL_FORMAT_SPLIT, HL_FORMAT_WHOLE_EXPONENT, HL_FORMAT_FP16 = 0, 1, 2
 HEADER_BYTES = 128
-LUT_BYTES = 33024
+LUT_BYTES = 49440
 MAX_BATCH = 16
 
 
@@ -237,7 +237,7 @@ class DeviceTensor:
         return int(self.view.total_bytes)
 
     def decode(self, out=None, stream=None):
-        """bf16 bit patterns as a torch.int16 tensor [rows, cols] on the device."""
+        """Weight bit patterns (bf16, or float16 for the float16 format) as a torch.int16 tensor [rows, cols] on the device."""
         import torch
         R, K = self.shape
         if out is None:
@@ -267,9 +267,9 @@ class DeviceTensor:
             x = x.unsqueeze(0)
         if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous():
             raise ValueError("x must be a contiguous [batch, cols] tensor")
-        dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16}.get(x.dtype)
+        dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16, torch.float16: HL_F16}.get(x.dtype)
         if dt is None:
-            raise ValueError("x must be float32 or bfloat16")
+            raise ValueError("x must be float32, bfloat16 or float16")
         if y is None:
             y = torch.empty((x.shape[0], R), dtype=torch.float32, device=x.device)
         if workspace is None:
