@@ -8,6 +8,13 @@ The compressed matrix is replicated in HBM past 1 GiB and steps rotate over
 the replicas, so every launch reads from HBM rather than the 256 MB
 last-level cache.
 
+The headline container is the paper's bf16 split (two 4-bit exponent codes);
+`--format` selects another. The same run times the other two formats under
+detail.variants: the whole exponent as one 8-bit symbol, and the paper's
+float16 {1,5,5,5} split on the float16 copy of the same matrix with float16
+activations. Uncompressed comparators: bf16 (this library's GEMV and torch)
+for the bf16 formats, float16 torch for the float16 one.
+
 Prints one JSON line (the driver's contract). The warm-up and the timed
 steps are each one HIP graph of back-to-back launches (rotating over the
 replicas), replayed on the launch stream, so that host-side launch cost stays
@@ -43,8 +50,13 @@ HBM_PEAK_GBS = 8000.0
 COLD_BYTES = 1.2 * (1 << 30)
 KERNEL_SRC = os.path.join(ROOT, "paper_2502_00922_amd", "csrc", "kernels.hip")
 TRAFFIC_FILES = {"split": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_traffic.txt"),
-                 "whole": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_whole_exponent_traffic.txt")}
+                 "whole": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_whole_exponent_traffic.txt"),
+                 "fp16": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_fp16_traffic.txt")}
 COPY_BYTES = 256 << 20
+# container format -> (encoder keywords, activation dtype of gen_x, weights of the oracle)
+FORMATS = {"split": ({}, "bf16", "bf16"),
+           "whole": ({"whole_exponent": True}, "bf16", "bf16"),
+           "fp16": ({"fp16": True}, "f16", "fp16")}
 
 
 def parse():
@@ -59,9 +71,10 @@ def parse():
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the launches the byte-counter passes measure")
     ap.add_argument("--no-graph", action="store_true", help="time individual launches instead of graph replays")
-    ap.add_argument("--format", choices=["split", "whole"], default="split",
-                    help="container of the headline: split exponent (two 4-bit codes) or whole exponent")
-    ap.add_argument("--no-variant", action="store_true", help="skip timing the other container format")
+    ap.add_argument("--format", choices=list(FORMATS), default="split",
+                    help="container of the headline: split exponent (two 4-bit codes), whole exponent, or "
+                         "the float16 {1,5,5,5} format on the float16 copy of the matrix")
+    ap.add_argument("--no-variant", action="store_true", help="skip timing the other container formats")
     return ap.parse_args()
 
 
@@ -134,7 +147,7 @@ def time_launches(torch, launch, nrep, steps, warmup):
     return float(per.mean()), float(np.median(per)), t0.elapsed_time(t1) / steps
 
 
-def cpu_oracle_baseline(blob: bytes, W, x, seconds: float):
+def cpu_oracle_baseline(blob: bytes, x, seconds: float, weights: str):
     """The oracle, as it stands, on a bounded sample: bit-serial decode of whole
     groups plus the exactly rounded fp64 partial products of those weights."""
     from oracle import codec, gemv as ogemv
@@ -147,7 +160,7 @@ def cpu_oracle_baseline(blob: bytes, W, x, seconds: float):
         r0, G, c0, GC, wdec = codec.decode_group(blob, int(g))
         S = h["seg_len"]
         xs = x[:, c0 * S:(c0 + GC) * S]
-        ogemv.gemv_rows(wdec, xs)
+        ogemv.gemv_rows(wdec, xs, weights=weights)
         n_w += wdec.size
         groups += 1
         if time.perf_counter() - t_start >= seconds and groups >= 4:
@@ -159,11 +172,19 @@ def cpu_oracle_baseline(blob: bytes, W, x, seconds: float):
                        f"bit-serial decode + fp64 products, {dt:.1f} s, single-threaded Python")
 
 
-def measure_container(torch, hl, blob, spec, W, batches, args, single_launches):
+def device_x(torch, spec, batch, fmt):
+    """(host copy, device tensor) of the activations for a container format."""
+    from gen import gen_x
+    xb = gen_x(spec, batch, FORMATS[fmt][1])
+    if xb.dtype == np.uint16:
+        return xb, torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+    return xb, torch.from_numpy(xb).cuda()
+
+
+def measure_container(torch, hl, blob, spec, W, batches, args, single_launches, fmt):
     """Times the fused decode-GEMV of one container at each batch size over
     replicas of it that together exceed the last-level cache; checks sampled
     outputs of the timed launches against the oracle."""
-    from gen import gen_x
     from oracle import gemv as ogemv
     R, K = spec.rows, spec.cols
     nrep = max(2, math.ceil(COLD_BYTES / blob.size))
@@ -171,8 +192,7 @@ def measure_container(torch, hl, blob, spec, W, batches, args, single_launches):
     torch.cuda.synchronize()
     results = {}
     for batch in batches:
-        xb = gen_x(spec, batch, "bf16")
-        xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+        xb, xd = device_x(torch, spec, batch, fmt)
         y = torch.empty((batch, R), dtype=torch.float32, device="cuda")
 
         def launch(i, xd=xd, y=y):
@@ -184,7 +204,7 @@ def measure_container(torch, hl, blob, spec, W, batches, args, single_launches):
             mean_ms = med_ms = ev_step_ms = None
         step_ms = ev_step_ms if args.no_graph else time_graph(torch, launch, nrep, args.steps, args.warmup)
         rows = list(range(0, R, R // 16))
-        y_ref, den = ogemv.gemv_rows(W, xb, rows=rows)
+        y_ref, den = ogemv.gemv_rows(W, xb, rows=rows, weights=FORMATS[fmt][2])
         err = float(np.max(ogemv.rel_err(y.cpu().numpy()[:, rows], y_ref, den)))
         alg_bytes = blob.size + K * batch * 2 + R * batch * 4
         results[batch] = dict(mean_ms=mean_ms, med_ms=med_ms, step_ms=step_ms, ev_step_ms=ev_step_ms,
@@ -205,17 +225,18 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     import paper_2502_00922_amd as hl
-    from gen import config_matrices, gen_matrix, gen_x
+    from gen import bf16_bits_to_f16_bits, config_matrices, gen_matrix
 
     hl.lib()
     spec = config_matrices(2)[0]
     R, K = spec.rows, spec.cols
     n = R * K
     W = gen_matrix(spec)
+    Ws = {"split": W, "whole": W, "fp16": bf16_bits_to_f16_bits(W)}
     blobs, encoder = {}, {}
-    for f in ("split", "whole"):
+    for f in FORMATS:
         t0 = time.perf_counter()
-        blobs[f] = hl.encode(W, whole_exponent=(f == "whole"))
+        blobs[f] = hl.encode(Ws[f], **FORMATS[f][0])
         dt = time.perf_counter() - t0
         encoder[f] = dict(seconds=round(dt, 4), input_GBps=round(2 * n / dt / 1e9, 3))
     encoder["threads"] = len(os.sched_getaffinity(0))
@@ -226,8 +247,7 @@ def main():
 
     if args.traffic_run:
         tensors = [hl.DeviceTensor(blob) for _ in range(nrep)]
-        xb = gen_x(spec, 1, "bf16")
-        xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+        _, xd = device_x(torch, spec, 1, args.format)
         y = torch.empty((1, R), dtype=torch.float32, device="cuda")
         for i in range(100):
             tensors[i % nrep].gemv(xd, y)
@@ -242,43 +262,55 @@ def main():
         return
 
     batches = sorted({args.batch, 4} if args.batch == 1 else {args.batch})
-    results, seg_len = measure_container(torch, hl, blob, spec, W, batches, args, single_launches=True)
-    variant = None
+    results, seg_len = measure_container(torch, hl, blob, spec, Ws[args.format], batches, args,
+                                         single_launches=True, fmt=args.format)
+    variants = {}
     if not args.no_variant:
-        other = "whole" if args.format == "split" else "split"
-        vres, _ = measure_container(torch, hl, blobs[other], spec, W, batches, args, single_launches=False)
-        variant = {"format": other, "compressed_bytes": int(blobs[other].size),
-                   "compression_ratio": round(2 * n / blobs[other].size, 4),
-                   "bits_per_weight": round(8 * blobs[other].size / n, 4)}
-        for b, rr in vres.items():
-            variant[f"batch{b}"] = dict(
-                ms_per_step=round(rr["step_ms"], 5),
-                compressed_GBps=round(rr["alg_bytes"] / (rr["step_ms"] * 1e-3) / 1e9, 1),
-                effective_GBps=round(2 * n / (rr["step_ms"] * 1e-3) / 1e9, 1),
-                max_rel_err=rr["max_rel_err"])
+        for other in FORMATS:
+            if other == args.format:
+                continue
+            vres, _ = measure_container(torch, hl, blobs[other], spec, Ws[other], batches, args,
+                                        single_launches=False, fmt=other)
+            v = {"compressed_bytes": int(blobs[other].size),
+                 "compression_ratio": round(2 * n / blobs[other].size, 4),
+                 "bits_per_weight": round(8 * blobs[other].size / n, 4)}
+            for b, rr in vres.items():
+                v[f"batch{b}"] = dict(
+                    ms_per_step=round(rr["step_ms"], 5),
+                    compressed_GBps=round(rr["alg_bytes"] / (rr["step_ms"] * 1e-3) / 1e9, 1),
+                    effective_GBps=round(2 * n / (rr["step_ms"] * 1e-3) / 1e9, 1),
+                    max_rel_err=rr["max_rel_err"])
+            variants[other] = v
     torch.cuda.synchronize()
 
-    cmp = {}
+    # uncompressed comparators on cold replicas: bf16 (this library's kernel
+    # and torch) for the bf16 formats, float16 (torch) for the float16 one
+    cmp = {"bf16": {}, "fp16": {}}
     if not args.no_compare:
-        wbf = torch.from_numpy(W.view(np.int16)).view(torch.bfloat16).cuda()
-        nrep_b = max(2, math.ceil(COLD_BYTES / (2 * n)))
-        wreps = [wbf.clone() for _ in range(nrep_b)]
-        for batch in results:
-            xb = gen_x(spec, batch, "bf16")
-            xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
-            y = torch.empty((batch, R), dtype=torch.float32, device="cuda")
-            timer = time_launches if args.no_graph else time_graph
-            m1 = timer(torch, lambda i: hl.gemv_bf16(wreps[i], xd, y), nrep_b, min(args.steps, 200), 10)
-            m2 = timer(torch, lambda i: torch.nn.functional.linear(xd, wreps[i]), nrep_b, min(args.steps, 200), 10)
-            if args.no_graph:
-                m1, m2 = m1[0], m2[0]
-            cmp[batch] = dict(hl_gemv_bf16_ms=m1, torch_linear_ms=m2)
-        del wreps, wbf
+        timer = time_launches if args.no_graph else time_graph
+        for dt_name, Wc in (("bf16", W), ("fp16", Ws["fp16"])):
+            tdt = torch.bfloat16 if dt_name == "bf16" else torch.float16
+            wdev = torch.from_numpy(Wc.view(np.int16)).view(tdt).cuda()
+            nrep_b = max(2, math.ceil(COLD_BYTES / (2 * n)))
+            wreps = [wdev.clone() for _ in range(nrep_b)]
+            for batch in results:
+                _, xd = device_x(torch, spec, batch, "split" if dt_name == "bf16" else "fp16")
+                y = torch.empty((batch, R), dtype=torch.float32, device="cuda")
+                c = {}
+                if dt_name == "bf16":
+                    c["hl_gemv_bf16_ms"] = timer(torch, lambda i: hl.gemv_bf16(wreps[i], xd, y), nrep_b,
+                                                 min(args.steps, 200), 10)
+                c["torch_linear_ms"] = timer(torch, lambda i: torch.nn.functional.linear(xd, wreps[i]), nrep_b,
+                                             min(args.steps, 200), 10)
+                if args.no_graph:
+                    c = {k: v[0] for k, v in c.items()}
+                cmp[dt_name][batch] = c
+            del wreps, wdev
 
     cpu = None
     if not args.no_cpu:
-        xb = gen_x(spec, 1, "bf16")
-        cpu = cpu_oracle_baseline(blob_b, W, xb, args.cpu_seconds)
+        xb, _ = device_x(torch, spec, 1, args.format)
+        cpu = cpu_oracle_baseline(blob_b, xb, args.cpu_seconds, FORMATS[args.format][2])
 
     b0 = args.batch
     r = results[b0]
@@ -294,14 +326,20 @@ def main():
                  ms_per_single_launch_events_median=round(rr["med_ms"], 5),
                  ms_per_step_single_launches=round(rr["ev_step_ms"], 5),
                  max_rel_err=rr["max_rel_err"])
-        if b in cmp:
-            best = min(cmp[b]["hl_gemv_bf16_ms"], cmp[b]["torch_linear_ms"])
-            e.update(bf16_gemv_ms=round(cmp[b]["hl_gemv_bf16_ms"], 5),
-                     torch_linear_ms=round(cmp[b]["torch_linear_ms"], 5),
-                     speedup_vs_best_bf16=round(best / rr["step_ms"], 3))
+        own = cmp["fp16" if args.format == "fp16" else "bf16"]
+        if b in own:
+            best = min(own[b].values())
+            e.update({k: round(v, 5) for k, v in own[b].items()})
+            e["speedup_vs_best_uncompressed"] = round(best / rr["step_ms"], 3)
         extra[f"batch{b}"] = e
-    if variant is not None:
-        extra["variant"] = variant
+    for f, v in variants.items():
+        own = cmp["fp16" if f == "fp16" else "bf16"]
+        for b in results:
+            if b in own:
+                v[f"batch{b}"]["speedup_vs_best_uncompressed"] = round(
+                    min(own[b].values()) / v[f"batch{b}"]["ms_per_step"], 3)
+    if variants:
+        extra["variants"] = variants
     extra["encoder"] = encoder
     out = {
         "metric": METRIC,
@@ -314,12 +352,13 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "f16" if args.format == "fp16" else "bf16",
         "data": "synthetic",
         "config": {"workload": "4096x4096 bf16 projection, per-row LogNormal(0,0.3) scale, "
                                "N(0,0.02) + 0.1% outliers x20, seed 0; fused decode-GEMV",
-                   "rows": R, "cols": K, "batch": b0, "x_dtype": "bf16", "seg_len": seg_len,
-                   "format": "split exponent (4+4)" if args.format == "split" else "whole exponent (8)",
+                   "rows": R, "cols": K, "batch": b0, "x_dtype": FORMATS[args.format][1], "seg_len": seg_len,
+                   "format": {"split": "bf16, split exponent (4+4)", "whole": "bf16, whole exponent (8)",
+                              "fp16": "float16 {1,5,5,5} (float16 copy of the matrix, float16 x)"}[args.format],
                    "compressed_bytes": int(blob.size), "compression_ratio": round(2 * n / blob.size, 4),
                    "bits_per_weight": round(8 * blob.size / n, 4), "replicas": nrep},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

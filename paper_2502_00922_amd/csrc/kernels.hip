@@ -419,6 +419,11 @@ struct GroupArgs {
   const uint32_t* lut;   // global copy: kLutN entries + aux
   uint32_t rows, cols, S, L, GR, GC, CB, RB, stream_units, max_units;
   uint32_t col_rows;     // rows of the stream columns (row 0 = padding)
+  // float16 format: LDS layout of its decode tables (see Tab16)
+  uint32_t t16_mask[3];  // window index mask of the ml, e, mh tables (bytes)
+  uint32_t t16_base[3];  // their byte offsets
+  uint32_t t16_aux;      // word offset of the bit-serial tables
+  uint32_t t16_words;    // words of all tables (a multiple of 4)
 };
 
 // Group geometry and its metadata (segment length of the lane, stream units).
@@ -1136,30 +1141,58 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
 
 // Decode tables of the float16 {1,5,5,5} format. Its kernels use no static
 // LDS: the tables sit at the start of the dynamic LDS, the wave regions after.
-//   [0, 8192)       pair table: entry v = the codes code(ml) code(e) that the
-//                   13-bit window v (bit 0 first) starts with: total length in
-//                   bits 0..4, (e<<10 | ml) in bits 16..30; kEsc16 if the pair
-//                   is longer than 13 bits;
-//   [8192, 12288)   mantissa-high table: entry v = code(mh) at the start of
-//                   the 12-bit window v: length in bits 0..4, mh<<5 in bits
-//                   16..30 (lmax <= 12, so every window matches);
-//   [12288, 12360)  canonical tables of ml, e and mh in the aux format, for
-//                   the bit-serial path.
-// ORing a weight's pair and mantissa-high entries gives its bits 0..14 in
-// bits 16..30. In the fast loop a position accumulates whole entries: bits
-// 0..15 are the position (a column holds fewer than 2^16 bits), the weight
-// bits pile up above. An escape adds 256, which eight weights of at most
-// 13 + 12 code bits (200) cannot reach.
-constexpr int kLutMBits = 12;
-constexpr int kLutMN = 1 << kLutMBits;
+// One table per field, in the order ml, e, mh, each indexed by an L-bit
+// window (bit 0 first) with L the field's longest code (0 for a one-symbol
+// field: one entry), so a complete code matches every window:
+//   ml: code length in bits 0..3, ml in bits 16..20;
+//   e:  length, e in bits 26..30;
+//   mh: length, mh in bits 21..25;
+// then the canonical tables of ml, e and mh in the aux format, for the
+// bit-serial path. ORing a weight's three entries gives its bits 0..14 in
+// bits 16..30. Sizing each table by its field's longest code keeps them small
+// (the near-uniform mh field has 5-bit codes: 32 entries), which leaves LDS
+// for 16 waves and spreads fewer distinct table words over the banks.
+// Joint tables of two fields would save a read per weight, but subnormal and
+// outlier weights carry two long codes at once (a pair past 13 bits in about
+// one weight in 500); at 64 lanes x 8 weights per step that would send most
+// steps through a slow path, and one table per field never needs one on such
+// data. Two weights (at most 72 code bits) are decoded per 64-bit window,
+// which holds 62 new bits; the rare pair longer than that (or a damaged code,
+// whose entry is kEsc16 = 256) sends the lane through the bit-serial path. In
+// the fast loop a position accumulates whole entries: bits 0..15 are the
+// position (a column holds fewer than 2^16 bits), the weight bits pile up
+// above.
+constexpr int kLut16MaxBits = 12;
 constexpr int kAux16Words = 3 * kAuxField;
-constexpr uint32_t kTab16Words = kLutN + kLutMN + kAux16Words;
+constexpr uint32_t kTab16MaxWords = 3 * (1u << kLut16MaxBits) + kAux16Words;
 constexpr uint32_t kEsc16 = 0x100u;
 constexpr uint32_t kPosMask16 = 0xFFFFu;
 constexpr uint32_t kAuxMl = 0, kAuxE = kAuxField, kAuxMh = 2 * kAuxField;
 
-static_assert(HL_LUT_BYTES == kTab16Words * 4, "the table buffer holds the largest format's tables");
-static_assert(kTab16Words % 4 == 0, "tables copy in 16-byte pieces");
+static_assert(HL_LUT_BYTES == kTab16MaxWords * 4, "the table buffer holds the largest format's tables");
+
+// LDS layout of the float16 tables of one codebook (the same on the host,
+// which builds them, and in the kernels, which read them).
+struct Tab16 {
+  uint32_t bits[3], base[3], aux, words;  // per field (ml, e, mh): window bits, word offset
+};
+
+static Tab16 tab16_layout(const hl_codebook16& cb) {
+  Tab16 t;
+  const hl_field_code5* f[3] = {&cb.ml, &cb.e, &cb.mh};
+  uint32_t off = 0;
+  for (int k = 0; k < 3; ++k) {
+    uint32_t L = 0;
+    if (f[k]->nsym > 1)
+      for (int s = 0; s < 32; ++s) L = std::max<uint32_t>(L, f[k]->len[s]);
+    t.bits[k] = L;
+    t.base[k] = off;
+    off += 1u << L;
+  }
+  t.aux = off;
+  t.words = (off + kAux16Words + 3) & ~3u;
+  return t;
+}
 
 struct Aux16 {
   uint32_t w[kAux16Words];
@@ -1174,44 +1207,42 @@ static Aux16 make_aux16(const hl_codebook16& cb) {
   return a;
 }
 
-__global__ void __launch_bounds__(256) lut16_kernel(uint32_t* lut, Aux16 aux) {
-  for (int v = threadIdx.x; v < kLutN; v += blockDim.x) {
-    uint32_t ul = 0, ue = 0;
-    const int l = field_from_bits(aux.w + kAuxMl, (uint32_t)v, kLutBits, &ul);  // ml first
-    const int e = l < 0 ? -1 : field_from_bits(aux.w + kAuxE, (uint32_t)v >> ul, kLutBits - ul, &ue);
-    lut[v] = (l < 0 || e < 0) ? kEsc16 : ((ul + ue) | ((uint32_t)((e << 10) | l) << 16));
+__global__ void __launch_bounds__(256) lut16_kernel(uint32_t* lut, Aux16 aux, Tab16 lay) {
+  const uint32_t auxoff[3] = {kAuxMl, kAuxE, kAuxMh}, shift[3] = {16, 26, 21};
+  for (int f = 0; f < 3; ++f) {
+    const uint32_t n = 1u << lay.bits[f];
+    for (uint32_t v = threadIdx.x; v < n; v += blockDim.x) {
+      uint32_t u = 0;
+      const int sym = field_from_bits(aux.w + auxoff[f], v, lay.bits[f], &u);
+      lut[lay.base[f] + v] = sym < 0 ? kEsc16 : (u | ((uint32_t)sym << shift[f]));
+    }
   }
-  for (int v = threadIdx.x; v < kLutMN; v += blockDim.x) {
-    uint32_t um = 0;
-    const int m = field_from_bits(aux.w + kAuxMh, (uint32_t)v, kLutMBits, &um);
-    lut[kLutN + v] = m < 0 ? kEsc16 : (um | ((uint32_t)m << 21));
-  }
-  for (int i = threadIdx.x; i < kAux16Words; i += blockDim.x) lut[kLutN + kLutMN + i] = aux.w[i];
+  for (uint32_t i = lay.aux + threadIdx.x; i < lay.words; i += blockDim.x)
+    lut[i] = i - lay.aux < (uint32_t)kAux16Words ? aux.w[i - lay.aux] : 0u;
 }
 
 // Copies the float16 tables to the start of the dynamic LDS (16-byte pieces
 // through registers; kernels that wait on nothing else).
-__device__ inline void load_tables16(const uint32_t* lut) {
-  constexpr uint32_t kVec = kTab16Words / 4;
-  const uint4* src = reinterpret_cast<const uint4*>(lut);
+__device__ inline void load_tables16(const GroupArgs& a) {
+  const uint32_t nv = a.t16_words / 4;
+  const uint4* src = reinterpret_cast<const uint4*>(a.lut);
   uint4* dst = reinterpret_cast<uint4*>(s_dyn);
-  for (uint32_t k = threadIdx.x; k < kVec; k += blockDim.x) dst[k] = src[k];
+  for (uint32_t k = threadIdx.x; k < nv; k += blockDim.x) dst[k] = src[k];
 }
 
 // The same copy as direct global-to-LDS transfers (the caller waits, vmcnt).
-__device__ inline void table16_dma(const uint32_t* lut) {
-  constexpr uint32_t kVec = kTab16Words / 4;
+__device__ inline void table16_dma(const GroupArgs& a) {
+  const uint32_t nv = a.t16_words / 4;
   const uint32_t n = blockDim.x, w0 = threadIdx.x & ~63u, lane = threadIdx.x & 63;
-  for (uint32_t k0 = w0; k0 < kVec; k0 += n)
-    if (k0 + lane < kVec) dma16(lut + (k0 + lane) * 4, s_dyn + k0 * 4);
+  for (uint32_t k0 = w0; k0 < nv; k0 += n)
+    if (k0 + lane < nv) dma16(a.lut + (k0 + lane) * 4, s_dyn + k0 * 4);
 }
 
-__device__ inline uint32_t tab16_pair(uint32_t w) {
-  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + (w & ((kLutN - 1) << 2)));
-}
-__device__ inline uint32_t tab16_mh(uint32_t w) {
-  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + kLutN * 4 +
-                                            (w & ((kLutMN - 1) << 2)));
+// Entry of field f's table for the window w (its index at bits 2.. of w).
+template <int F>
+__device__ inline uint32_t tab16(const GroupArgs& a, uint32_t w) {
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + a.t16_base[F] +
+                                            (w & a.t16_mask[F]));
 }
 
 // 64-bit window of column bits [pos2, pos2 + 64), positions read through kPosMask16.
@@ -1221,21 +1252,28 @@ __device__ inline uint64_t load_window16(const uint32_t* sc, uint32_t pos2, uint
   return ((uint64_t)__builtin_amdgcn_alignbit(c, b, pos2) << 32) | __builtin_amdgcn_alignbit(b, a, pos2);
 }
 
-// Two weights from one 64-bit window (two weights of at most 13 + 12 code
-// bits fit): h[0..1] = weight bits 0..14 in bits 16..30 (other bits
-// meaningless), p advanced by the four whole entries.
-__device__ inline void decode2_f16(const uint32_t* sc, uint32_t jmax, uint32_t& p, uint32_t* h) {
+// Two weights from one 64-bit window: h[0..1] = weight bits 0..14 in bits
+// 16..30 (other bits meaningless); p advanced by the six whole entries; flag
+// collects the window's consumption plus one (bit 6 or above set: the two
+// weights did not fit, or an escape).
+__device__ inline void decode2_f16(const GroupArgs& a, const uint32_t* sc, uint32_t jmax, uint32_t& p,
+                                   uint32_t& flag, uint32_t* h) {
   uint64_t W = load_window16(sc, p, jmax);
-  const uint32_t a0 = tab16_pair((uint32_t)W);
-  W = shift_window(W, a0);
-  const uint32_t m0 = tab16_mh((uint32_t)W);
-  W = shift_window(W, m0);
-  const uint32_t a1 = tab16_pair((uint32_t)W);
-  W = shift_window(W, a1);
-  const uint32_t m1 = tab16_mh((uint32_t)W);
-  p = p + a0 + m0 + a1 + m1;
-  h[0] = a0 | m0;
-  h[1] = a1 | m1;
+  uint32_t t[6];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    t[3 * k] = tab16<0>(a, (uint32_t)W);
+    W = shift_window(W, t[3 * k]);
+    t[3 * k + 1] = tab16<1>(a, (uint32_t)W);
+    W = shift_window(W, t[3 * k + 1]);
+    t[3 * k + 2] = tab16<2>(a, (uint32_t)W);
+    if (k == 0) W = shift_window(W, t[2]);
+  }
+  const uint32_t used = t[0] + t[1] + t[2] + t[3] + t[4] + t[5];
+  flag |= used + 1;
+  p += used;
+  h[0] = t[0] | t[1] | t[2];
+  h[1] = t[3] | t[4] | t[5];
 }
 
 struct Dec8 {
@@ -1246,10 +1284,10 @@ struct Dec8 {
 // bit-serially (code(ml), code(e), code(mh)); pos2 clean (no weight bits
 // above bit 15).
 __device__ __attribute__((always_inline)) inline Dec8 decode8_f16_careful_body(uint32_t sc_off, uint32_t jmax,
-                                                                               uint32_t pos2) {
+                                                                               uint32_t pos2, uint32_t aux_off) {
   asm volatile("" ::: "memory");  // keeps its table reads inside the (cold) path
   const uint32_t* sc = s_dyn + sc_off;
-  const uint32_t* aux = s_dyn + kLutN + kLutMN;
+  const uint32_t* aux = s_dyn + aux_off;
   Dec8 d;
   uint32_t p = pos2 + 2;
 #pragma unroll
@@ -1263,22 +1301,24 @@ __device__ __attribute__((always_inline)) inline Dec8 decode8_f16_careful_body(u
   return d;
 }
 
-__device__ __noinline__ Dec8 decode8_f16_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
-  return decode8_f16_careful_body(sc_off, jmax, pos2);
+__device__ __noinline__ Dec8 decode8_f16_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2, uint32_t aux_off) {
+  return decode8_f16_careful_body(sc_off, jmax, pos2, aux_off);
 }
 
-// Eight float16 weights' bits 0..14 (in bits 16..30 of h[k]). A pair past the
-// 13-bit window anywhere sends the lane through the careful path from the
-// first of the eight (the fast entries read after an escape are discarded).
-__device__ inline void decode8_f16(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* h) {
+// Eight float16 weights' bits 0..14 (in bits 16..30 of h[k]). A window that
+// could not hold its two weights (or an escape) anywhere sends the lane
+// through the careful path from the first of the eight; the fast entries read
+// after it are discarded.
+__device__ inline void decode8_f16(const GroupArgs& a, const uint32_t* sc, uint32_t sc_off, uint32_t jmax,
+                                   uint32_t& pos2, uint32_t* h) {
   const uint32_t p0 = pos2;
-  uint32_t p = p0;
-  decode2_f16(sc, jmax, p, h);
-  decode2_f16(sc, jmax, p, h + 2);
-  decode2_f16(sc, jmax, p, h + 4);
-  decode2_f16(sc, jmax, p, h + 6);
-  if (__builtin_expect(((p - p0) & 0xFF00u) != 0, 0)) {
-    const Dec8 d = decode8_f16_careful(sc_off, jmax, p0 & kPosMask16);
+  uint32_t p = p0, flag = 0;
+  decode2_f16(a, sc, jmax, p, flag, h);
+  decode2_f16(a, sc, jmax, p, flag, h + 2);
+  decode2_f16(a, sc, jmax, p, flag, h + 4);
+  decode2_f16(a, sc, jmax, p, flag, h + 6);
+  if (__builtin_expect((flag & 0xFFC0u) != 0, 0)) {
+    const Dec8 d = decode8_f16_careful(sc_off, jmax, p0 & kPosMask16, a.t16_aux);
     p = d.pos2;
 #pragma unroll
     for (int k = 0; k < 8; ++k) h[k] = d.h[k];
@@ -1304,8 +1344,8 @@ __global__ void __launch_bounds__(1024) decode16_kernel(GroupArgs a, uint16_t* o
   const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
   const uint32_t per_wave = a.col_rows * kCol;
-  uint32_t* cols = s_dyn + kTab16Words + wave * per_wave;
-  const uint32_t sc_off = kTab16Words + wave * per_wave + lane;
+  uint32_t* cols = s_dyn + a.t16_words + wave * per_wave;
+  const uint32_t sc_off = a.t16_words + wave * per_wave + lane;
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t jmax = a.col_rows - 3;
   const uint32_t n_grp = a.RB * a.CB;
@@ -1314,7 +1354,7 @@ __global__ void __launch_bounds__(1024) decode16_kernel(GroupArgs a, uint16_t* o
   uint32_t g = blockIdx.x * waves + wave;
   Meta m;
   if (g < n_grp) m = load_meta(a, g, lane);
-  load_tables16(a.lut);
+  load_tables16(a);
   __syncthreads();
   for (; g < n_grp; g += stride) {
     uint32_t pos2 = issue_stream(a, cols, m, lane);
@@ -1328,7 +1368,7 @@ __global__ void __launch_bounds__(1024) decode16_kernel(GroupArgs a, uint16_t* o
       const uint8_t* sg = a.raw + (cur.first + lane) * sb_per_seg;
       for (uint32_t t = 0; t < a.S; t += 8) {
         uint32_t h[8];
-        decode8_f16(sc, sc_off, jmax, pos2, h);
+        decode8_f16(a, sc, sc_off, jmax, pos2, h);
         *reinterpret_cast<uint4*>(o + t) = pack8_f16(h, sg[t >> 3]);
       }
     }
@@ -1376,7 +1416,7 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
   const uint32_t waves = blockDim.x >> 6;
   constexpr uint32_t S = SP * 8;
   const uint32_t per_wave = a.col_rows * kCol;
-  uint32_t* cols = s_dyn + kTab16Words + wave * per_wave;
+  uint32_t* cols = s_dyn + a.t16_words + wave * per_wave;
   const uint32_t jmax = a.col_rows - 3;
 
   const uint32_t rb = blockIdx.x / p.KS, kp = blockIdx.x % p.KS;
@@ -1384,7 +1424,7 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
   const uint32_t G = min(16u, a.rows - r0);
   const uint32_t i = lane & 15, q = lane >> 4;
   const uint32_t mu = q * G + min(i, G - 1);  // the segment this lane decodes
-  const uint32_t sc_off = kTab16Words + wave * per_wave + mu;
+  const uint32_t sc_off = a.t16_words + wave * per_wave + mu;
   const uint32_t* sc = s_dyn + sc_off;
   const uint16_t* xrow = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
 
@@ -1402,7 +1442,7 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
     sg.load(a.raw + (m.first + mu) * SP);
   }
   asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
-  table16_dma(a.lut);
+  table16_dma(a);
   uint32_t pos2 = issue_stream(a, cols, m, lane);
   wait_vm0();
   __syncthreads();
@@ -1427,7 +1467,7 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
 #pragma unroll
       for (int k = 0; k < KP; ++k) {
         uint32_t h[8];
-        decode8_f16(sc, sc_off, jmax, pd, h);
+        decode8_f16(a, sc, sc_off, jmax, pd, h);
         const uint4 wv = pack8_f16(h, sgc.byte(t0 + k));
         acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, wv),
                                                      __builtin_bit_cast(f16x8_t, xv[k]), acc, 0, 0, 0);
@@ -1444,7 +1484,7 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
     }
   }
   wait_vm0();  // prefetches past the last group
-  mfma_finish(p, acc, reinterpret_cast<float*>(s_dyn + kTab16Words), wave, waves, lane, rb, kp, r0, G);
+  mfma_finish(p, acc, reinterpret_cast<float*>(s_dyn + a.t16_words), wave, waves, lane, rb, kp, r0, G);
 }
 
 // ------------------------------------------------------------------ bf16 GEMV
@@ -1529,6 +1569,7 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bo
   if (t->rows >= (1ull << 31) || t->cols >= (1ull << 31) || t->n_grp >= (1ull << 31))
     return HL_EUNSUPPORTED;
   GroupArgs& a = pl->ga;
+  std::memset(&a, 0, sizeof(a));
   const uint8_t* b = t->blob_dev;
   a.seg_bits = reinterpret_cast<const uint16_t*>(b + t->off_seg_bits);
   a.grp_off = reinterpret_cast<const uint32_t*>(b + t->off_grp_off);
@@ -1549,8 +1590,17 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bo
   const uint32_t per_wave = a.col_rows * kCol + (raw_lds ? 16 * t->seg_len : 0) + extra_words_per_wave;
   // LDS: the tables (static for the bf16 formats, at the start of the
   // dynamic region for float16) plus one region per wave.
+  if (is_fp16(t)) {
+    const Tab16 lay = tab16_layout(t->cb16);
+    for (int k = 0; k < 3; ++k) {
+      a.t16_mask[k] = ((1u << lay.bits[k]) - 1) << 2;
+      a.t16_base[k] = lay.base[k] * 4;
+    }
+    a.t16_aux = lay.aux;
+    a.t16_words = lay.words;
+  }
   const size_t tab_static = is_fp16(t) ? 0 : (size_t)(kLutN + kAuxWords) * 4;
-  const size_t tab_dyn = is_fp16(t) ? (size_t)kTab16Words * 4 : 0;
+  const size_t tab_dyn = is_fp16(t) ? (size_t)a.t16_words * 4 : 0;
   uint32_t waves = kMaxWaves;
   while (waves > 1 && tab_static + tab_dyn + (size_t)waves * per_wave * 4 > kMaxLds) --waves;
   const size_t lds = tab_dyn + (size_t)waves * per_wave * 4;
@@ -1693,7 +1743,8 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
   if (!t || !t->lut_dev) return HL_EINVAL;
   if (t->format == HL_FORMAT_FP16) {
     if (!code16_valid(t->cb16)) return HL_ECORRUPT;
-    return launch(lut16_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, make_aux16(t->cb16));
+    return launch(lut16_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, make_aux16(t->cb16),
+                  tab16_layout(t->cb16));
   }
   if (t->format == HL_FORMAT_WHOLE_EXPONENT) {
     if (!code8_valid(t->cb8)) return HL_ECORRUPT;
@@ -1793,7 +1844,7 @@ static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, f
   choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p);
   const dim3 grid(pl.ga.RB * p.KS), block(pl.waves * 64);
   // the reduction reuses the wave regions: 4 floats per lane per wave
-  const size_t lds = std::max<size_t>(pl.lds, (size_t)kTab16Words * 4 + (size_t)pl.waves * 4 * 64 * 4);
+  const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.ga.t16_words * 4 + (size_t)pl.waves * 4 * 64 * 4);
   return launch_mfma16(t->seg_len / 8, grid, block, lds, stream, p);
 }
 

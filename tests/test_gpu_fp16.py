@@ -6,8 +6,9 @@ raw sign plane): its decode kernel and its matrix-core decode-GEMV.
   fp64 sums, |y - y_ref| <= 1e-3 * sum_k |w x|, at batch 1..16, with one and
   several blocks per row block;
 * code shapes: every float16 pattern (decode only: infinities and NaNs),
-  one-symbol fields, and weights whose pair code(ml) code(e) is longer than the
-  13-bit table window (the bit-serial path);
+  one-symbol fields, long exponent and low-mantissa codes together, and pairs
+  of weights whose six codes overflow the decoder's 64-bit window (the
+  bit-serial path);
 * the format's limits: other activation types and other group shapes are
   reported as unsupported.
 """
@@ -114,7 +115,20 @@ def _long_pairs(rows, cols, seed):
     return codec.join_fields16(rng.integers(0, 2, n), e, mh, ml).reshape(rows, cols)
 
 
-@pytest.mark.parametrize("kind", ["all_patterns", "single_symbols", "long_pairs"])
+def _window_overflow(rows, cols, seed):
+    """Geometric fields (12-bit codes for the rarest values) and 24 planted
+    pairs of adjacent weights, each weight holding the rarest value of all
+    three fields: two such weights need more than the 62 new bits of a window."""
+    rng = np.random.default_rng(seed)
+    n = rows * cols
+    e, mh, ml = (np.minimum(rng.geometric(0.5, n) - 1, 20).astype(np.uint32) for _ in range(3))
+    idx = rng.choice(n // 2, 24, replace=False) * 2
+    for f, top in ((e, 29), (mh, 31), (ml, 31)):
+        f[idx], f[idx + 1] = top, top - 1
+    return codec.join_fields16(rng.integers(0, 2, n), e, mh, ml).reshape(rows, cols)
+
+
+@pytest.mark.parametrize("kind", ["all_patterns", "single_symbols", "long_pairs", "window_overflow"])
 def test_code_shapes(torch, kind):
     print(f"fp16 codes {kind}", flush=True)
     if kind == "all_patterns":
@@ -124,15 +138,21 @@ def test_code_shapes(torch, kind):
         rng = np.random.default_rng(1)
         w = (0x3C00 | (rng.integers(0, 32, (96, 1024)) << 5) | (rng.integers(0, 2, (96, 1024)) << 15))
         w = w.astype(np.uint16)                         # e = 15 and ml = 0 everywhere
-    else:
+    elif kind == "long_pairs":
         w = _long_pairs(96, 1024, seed=4)
+    else:
+        w = _window_overflow(96, 1024, seed=5)
     blob = hl.encode(w, fp16=True)
     h = codec.parse_header(bytes(blob))
     if kind == "single_symbols":
         assert h["cb16"][0][0] == 1 and h["cb16"][2][0] == 1
     if kind == "long_pairs":
         lens = [max(c[2]) for c in h["cb16"]]
-        assert lens[0] + lens[2] > 13                   # e + ml past the window
+        assert lens[0] + lens[2] > 13                   # e + ml: long codes together
+    if kind == "window_overflow":
+        _, e, mh, ml = codec.split_fields16(w)
+        tot = sum(np.array(c[2])[f] for c, f in zip(h["cb16"], (e, mh, ml)))
+        assert (tot.reshape(-1, 2).sum(axis=1) > 62).sum() == 24
     dt = hl.DeviceTensor(blob)
     assert np.array_equal(_decode(torch, dt), w)
     if kind == "all_patterns":

@@ -2,7 +2,8 @@
 benchmark times (default segment length and group shape, cached workspace).
 
 Per matrix:
-Both container formats (split exponent; whole exponent on two workloads).
+All container formats (split exponent everywhere; whole exponent and float16
+on two workloads).
 * lossless: the device decode equals the generated weights bit for bit (a
   property at any size), and sampled groups decoded by the oracle's bit-serial
   decoder from the library's container equal them too;
@@ -16,7 +17,7 @@ The 70B-shaped stack is checked on its first and last layers.
 import numpy as np
 import pytest
 
-from gen import CONFIGS, config_matrices, gen_matrix, gen_x
+from gen import CONFIGS, bf16_bits_to_f16_bits, config_matrices, gen_matrix, gen_x
 from oracle import codec
 from oracle import gemv as ogemv
 
@@ -40,14 +41,17 @@ def _sample_rows(R, rng, n=40):
     return sorted(r for r in rows if 0 <= r < R)
 
 
-def _check_matrix(torch, spec, batches, x_dtype, size_check, whole=False):
-    print(f"workload {spec.cfg} layer {spec.layer} {spec.name} {spec.rows}x{spec.cols} whole={whole}", flush=True)
+def _check_matrix(torch, spec, batches, x_dtype, size_check, fmt="split"):
+    print(f"workload {spec.cfg} layer {spec.layer} {spec.name} {spec.rows}x{spec.cols} format={fmt}", flush=True)
     W = gen_matrix(spec)
-    blob = hl.encode(W, whole_exponent=whole)
+    weights = "bf16"
+    if fmt == "fp16":
+        W, x_dtype, weights = bf16_bits_to_f16_bits(W), "f16", "fp16"
+    blob = hl.encode(W, whole_exponent=fmt == "whole", fp16=fmt == "fp16")
     h = codec.parse_header(bytes(blob[:384]))
     S = h["seg_len"]
     if size_check:
-        size = codec.container_size8 if whole else codec.container_size
+        size = {"split": codec.container_size, "whole": codec.container_size8, "fp16": codec.container_size16}[fmt]
         assert blob.size == size(W, S)["total_bytes"]
     dt = hl.DeviceTensor(blob)
     # lossless at full size
@@ -69,7 +73,7 @@ def _check_matrix(torch, spec, batches, x_dtype, size_check, whole=False):
         else:
             x = torch.from_numpy(xs).cuda()
         y = dt.gemv(x).cpu().numpy()
-        yref, den = ogemv.gemv_rows(W, xs, rows=rows)
+        yref, den = ogemv.gemv_rows(W, xs, rows=rows, weights=weights)
         err = np.abs(y[:, rows] - yref) / (den + 1e-30)
         assert err.max() <= TOL, (B, float(err.max()))
     torch.cuda.synchronize()
@@ -83,13 +87,15 @@ def test_workload_full_size(torch, cfg):
         _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest)
 
 
+@pytest.mark.parametrize("fmt", ["whole", "fp16"])
 @pytest.mark.parametrize("cfg", [2, 4])
-def test_workload_full_size_whole_exponent(torch, cfg):
-    """The whole-exponent format on the 4096x4096 and the 8B-shaped layer workloads."""
+def test_workload_full_size_other_formats(torch, cfg, fmt):
+    """The whole-exponent format, and the float16 format on the float16 copies
+    of the weights, on the 4096x4096 and the 8B-shaped layer workloads."""
     specs = config_matrices(cfg)
     smallest = min(specs, key=lambda s: s.rows * s.cols)
     for spec in specs:
-        _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest, whole=True)
+        _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest, fmt=fmt)
 
 
 @pytest.mark.slow
