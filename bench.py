@@ -92,7 +92,7 @@ def recorded_traffic(batch: int, fmt: str):
         return None
     h = re.search(r"kernel source sha256\[:16\]: ([0-9a-f]{16})", text)
     b = re.search(r"batch: (\d+)", text)
-    f = re.search(r"format: (\w+)", text)
+    f = re.search(r"^format: (\w+)", text, re.M)
     t = re.search(r"traffic_bytes_per_launch: (\d+)", text)
     if not (h and b and t and f) or h.group(1) != kernel_hash() or int(b.group(1)) != batch or f.group(1) != fmt:
         return None
