@@ -80,7 +80,7 @@ _lib = None
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
            "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
-           "hl_decode_gemv", "hl_gemv_bf16"]
+           "hl_decode_gemv", "hl_gemm_workspace_bytes", "hl_decode_gemm", "hl_gemv_bf16"]
 
 
 def lib() -> ctypes.CDLL:
@@ -125,6 +125,11 @@ def lib() -> ctypes.CDLL:
     L.hl_gemv_workspace_bytes.argtypes = [c.POINTER(TensorView), c.c_uint32]
     L.hl_decode_gemv.restype = c.c_int
     L.hl_decode_gemv.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
+                                 c.c_void_p, c.c_size_t, c.c_void_p]
+    L.hl_gemm_workspace_bytes.restype = c.c_size_t
+    L.hl_gemm_workspace_bytes.argtypes = [c.POINTER(TensorView), c.c_uint32]
+    L.hl_decode_gemm.restype = c.c_int
+    L.hl_decode_gemm.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                  c.c_void_p, c.c_size_t, c.c_void_p]
     L.hl_gemv_bf16.restype = c.c_int
     L.hl_gemv_bf16.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.c_void_p, c.c_int, c.c_uint32,
@@ -279,6 +284,26 @@ class DeviceTensor:
         _check(lib().hl_decode_gemv(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
                                     ctypes.c_void_p(y.data_ptr()), ws_ptr, ws_n, _stream_ptr(stream)),
                "hl_decode_gemv")
+        return y
+
+    def gemm(self, x, y=None, stream=None):
+        """Y[n, r] = sum_k W[r, k] X[n, k]; X: [tokens, cols] bfloat16 (device).
+        Uses a cached zeroed workspace owned by the tensor, grown as needed."""
+        import torch
+        R, K = self.shape
+        if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous() or x.dtype != torch.bfloat16:
+            raise ValueError("x must be a contiguous [tokens, cols] bfloat16 tensor")
+        T = x.shape[0]
+        if y is None:
+            y = torch.empty((T, R), dtype=torch.float32, device=x.device)
+        need = int(lib().hl_gemm_workspace_bytes(ctypes.byref(self.view), T))
+        ws = getattr(self, "_gemm_ws", None)
+        if ws is None or ws.numel() < need:
+            ws = torch.zeros(max(need, 4), dtype=torch.uint8, device=self.blob.device)
+            self._gemm_ws = ws
+        _check(lib().hl_decode_gemm(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), HL_BF16, T,
+                                    ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                    _stream_ptr(stream)), "hl_decode_gemm")
         return y
 
 
