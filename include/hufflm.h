@@ -283,8 +283,8 @@ hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype
                          size_t workspace_bytes, void* stream);
 
 /* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows
- * (partial sums of every column block of four segments, and arrival
- * counters); 0 for tensors it does not take. */
+ * (partial sums of up to one range per column block of four segments); 0 for
+ * tensors it does not take. */
 size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
 
 /* Prefill product Y[n][r] = sum_k W[r][k] * X[n][k] for n < tokens (many
@@ -295,10 +295,9 @@ size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
  * y_dev: [tokens][rows] float32 (fully written); fp32 accumulation, every
  * output summed in a fixed order. bf16 formats (split or whole exponent) with
  * 16-row groups and S = 32 or 64; others give HL_EUNSUPPORTED.
- * workspace_dev: hl_gemm_workspace_bytes(t, tokens) bytes, zero-filled by the
- * caller once before first use and left ready for the next call; calls that
- * may run concurrently need separate workspaces. Errors: HL_EINVAL (also for
- * a missing or short workspace). */
+ * workspace_dev: hl_gemm_workspace_bytes(t, tokens) bytes (no initial
+ * contents needed); calls that may run concurrently need separate
+ * workspaces. Errors: HL_EINVAL (also for a missing or short workspace). */
 hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t tokens,
                          float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream);
 

@@ -992,42 +992,44 @@ struct GemmArgs {
   GroupArgs g;
   const uint16_t* x;  // bf16 [T][cols]
   float* y;           // [T][rows]
-  float* partial;     // workspace: CB x T x rows partial sums
-  uint32_t* counter;  // workspace: RS x chunks arrival counters, zero between calls
+  float* partial;     // workspace: KS x T x rows partial sums (KS > 1)
   uint32_t T;         // tokens
   uint32_t RS;        // row sets (16 row blocks each, one per wave)
+  uint32_t KS;        // column-block ranges (blocks per row set and chunk)
+  uint32_t cpb;       // column blocks per range
   uint32_t x_off;     // byte offset of the stream columns after the activation slice
 };
 
-// Activation slice in LDS: 16*NT token rows of 4*S bf16 (the block's column
-// block), 16-byte chunk c of row r stored at chunk c ^ (r & 15), so that the
-// 16 token rows a matrix-instruction operand reads fall in 16 different bank
-// groups.
+// Activation slice in LDS: 16*NT token rows of 4*S bf16 (one column block),
+// 16-byte chunk c of row r stored at chunk c ^ (r & 15), so that the 16 token
+// rows a matrix-instruction operand reads fall in 16 different bank groups.
 template <int SP>
 __device__ inline uint32_t xslice_offset(uint32_t row, uint32_t chunk) {
   constexpr uint32_t kRowBytes = 4 * SP * 8 * 2;
   return row * kRowBytes + ((chunk ^ (row & 15)) << 4);
 }
 
-// Y[n][r] = sum_k W[r][k] X[n][k] for many tokens n (prefill). Block (cb, rs,
-// ck): column block cb of the 16 row blocks of row set rs (wave w: row block
-// 16*rs + w, one group), tokens 128*ck .. of chunk ck, NT tiles of 16. The
-// column block's activations for the chunk are staged once in LDS and shared
-// by the waves; each decoded 8-weight step (the A operand of the 16x16x32
-// bf16 matrix instruction, as in the GEMV) is multiplied with the NT token
-// tiles (B operands from LDS). Partial sums per column block go to the
-// workspace; the last block of a row set and chunk to arrive adds them in
-// column-block order (results do not vary between runs).
+// Y[n][r] = sum_k W[r][k] X[n][k] for many tokens n (prefill). Block (ks, rs,
+// ck): the column blocks ks*cpb .. of the 16 row blocks of row set rs (wave
+// w: row block 16*rs + w), tokens 16*NT*ck .. of chunk ck, in NT tiles of 16.
+// Per column block the block stages its activations once in LDS, shared by
+// the waves, and each wave decodes its group step by step: each decoded
+// 8-weight step (the A operand of the 16x16x32 bf16 matrix instruction, as in
+// the GEMV) is multiplied with the NT token tiles (B operands from LDS). With
+// one range (KS = 1) the block writes Y; otherwise it writes its partial sums
+// and gemm_reduce_kernel adds the ranges in order (results do not vary
+// between runs).
 template <int SP, int NT>
 __global__ void __launch_bounds__(1024) gemm_mfma_kernel(GemmArgs p) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kChunks = 4 * S / 8;       // 16-byte chunks per token row
   constexpr uint32_t kRows = 16 * NT;           // token rows of the slice
+  constexpr uint32_t kCopies = kRows * kChunks / 64;
   const GroupArgs& a = p.g;
   const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
-  const uint32_t cb = blockIdx.x % a.CB;
-  const uint32_t rest = blockIdx.x / a.CB;
+  const uint32_t ks = blockIdx.x % p.KS;
+  const uint32_t rest = blockIdx.x / p.KS;
   const uint32_t rs = rest % p.RS, ck = rest / p.RS;
   const uint32_t rb = min(rs * 16 + wave, a.RB - 1);  // waves past the last row block repeat it
   const bool own = rs * 16 + wave < a.RB;
@@ -1044,91 +1046,79 @@ __global__ void __launch_bounds__(1024) gemm_mfma_kernel(GemmArgs p) {
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t jmax = a.col_rows - 3;
   const uint32_t rstride = G * 4 * 8;
-
-  // Prologue: metadata and raw bytes of all steps, then the table, stream and
-  // activation copies into LDS.
-  Meta m = load_meta(a, rb * a.CB + cb, lane);
-  uint2 rw[SP];
-  {
-    const uint8_t* r = a.raw + m.first * S + mu * 8;
-#pragma unroll
-    for (int k = 0; k < SP; ++k) rw[k] = *reinterpret_cast<const uint2*>(r + k * rstride);
-  }
-  asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
-  table_dma(a.lut);
-  uint32_t pos2 = issue_stream(a, cols, m, lane);
-  // The activation slice by direct copies: copy k of a wave fills the 1 KB at
-  // k*1024 of the slice; its lane L writes position L there and so loads the
-  // chunk that the swizzle puts at that position.
-  constexpr uint32_t kCopies = kRows * kChunks / 64;
-  for (uint32_t k = wave; k < kCopies; k += waves) {
-    const uint32_t pos = k * 64 + lane;
-    const uint32_t row = pos / kChunks, d = pos % kChunks;
-    const uint32_t tok = min(t0 + row, p.T - 1);
-    const uint32_t c = d ^ (row & 15);
-    dma16(p.x + (uint64_t)tok * a.cols + cb * 4 * S + c * 8, reinterpret_cast<uint32_t*>(xs + k * 1024));
-  }
-  wait_vm0();
-  __syncthreads();
+  const uint32_t kb0 = ks * p.cpb, kb1 = min(a.CB, kb0 + p.cpb);
 
   f32x4_t acc[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+  for (uint32_t cb = kb0; cb < kb1; ++cb) {
+    if (cb != kb0) block_sync_lds();  // every wave is done with the slice and its columns
+    // Metadata and raw bytes of all steps, then the table, stream and
+    // activation copies into LDS.
+    Meta m = load_meta(a, rb * a.CB + cb, lane);
+    uint2 rw[SP];
+    {
+      const uint8_t* r = a.raw + m.first * S + mu * 8;
 #pragma unroll
-  for (int k = 0; k < SP; ++k) {
-    uint32_t e[8];
-    decode8(sc, sc_off, jmax, pd, e);
-    uint4 wv;
-    wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
-    wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
-    wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
-    wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
-    const bf16x8_t A = __builtin_bit_cast(bf16x8_t, wv);
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const uint4 xb = *reinterpret_cast<const uint4*>(xs + xslice_offset<SP>(16 * j + i, q * SP + k));
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, xb), acc[j], 0, 0, 0);
+      for (int k = 0; k < SP; ++k) rw[k] = *reinterpret_cast<const uint2*>(r + k * rstride);
     }
-  }
+    asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
+    if (cb == kb0) table_dma(a.lut);
+    const uint32_t pos2 = issue_stream(a, cols, m, lane);
+    // Copy k of a wave fills the 1 KB at k*1024 of the slice; its lane L
+    // writes position L there and so loads the chunk that the swizzle puts
+    // at that position.
+    for (uint32_t k = wave; k < kCopies; k += waves) {
+      const uint32_t pos = k * 64 + lane;
+      const uint32_t row = pos / kChunks, d = pos % kChunks;
+      const uint32_t tok = min(t0 + row, p.T - 1);
+      dma16(p.x + (uint64_t)tok * a.cols + cb * 4 * S + (d ^ (row & 15)) * 8,
+            reinterpret_cast<uint32_t*>(xs + k * 1024));
+    }
+    wait_vm0();
+    __syncthreads();
 
-  // Partial sums of this column block: lane (q, i) holds rows 4q..4q+3 of
-  // token 16j + i of tile j.
-  const uint32_t R = a.rows;
-  if (own) {
+    uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const uint32_t tok = t0 + 16 * j + i;
-      if (tok >= p.T) continue;
-      float* dst = p.partial + ((uint64_t)cb * p.T + tok) * R + r0 + 4 * q;
+    for (int k = 0; k < SP; ++k) {
+      uint32_t e[8];
+      decode8(sc, sc_off, jmax, pd, e);
+      uint4 wv;
+      wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
+      wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
+      wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
+      wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
+      const bf16x8_t A = __builtin_bit_cast(bf16x8_t, wv);
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
-        if (4 * q + v < G) __hip_atomic_store(dst + v, acc[j][v], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      for (int j = 0; j < NT; ++j) {
+        const uint4 xb = *reinterpret_cast<const uint4*>(xs + xslice_offset<SP>(16 * j + i, q * SP + k));
+        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, xb), acc[j], 0, 0, 0);
+      }
     }
   }
-  wait_vm0();
-  __syncthreads();
-  uint32_t* flag = s_dyn;  // the slice is no longer read
-  if (threadIdx.x == 0) {
-    const uint32_t old =
-        __hip_atomic_fetch_add(p.counter + rs + ck * p.RS, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    flag[0] = old;
+  if (!own) return;
+  // lane (q, i) holds rows 4q..4q+3 of token 16j + i of tile j
+  const uint32_t R = a.rows;
+  float* out = p.KS == 1 ? p.y : p.partial + (uint64_t)ks * p.T * R;
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const uint32_t tok = t0 + 16 * j + i;
+    if (tok >= p.T) continue;
+    float* dst = out + (uint64_t)tok * R + r0 + 4 * q;
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      if (4 * q + v < G) dst[v] = acc[j][v];
   }
-  __syncthreads();
-  if (flag[0] != a.CB - 1) return;
-  // Last block of this row set and chunk: add the column blocks in order.
-  const uint32_t rlo = rs * 256, rhi = min(R, rlo + 256);
-  const uint32_t tn = min(kRows, p.T - t0);
-  const uint32_t nrow = rhi - rlo;
-  for (uint32_t idx = threadIdx.x; idx < nrow * tn; idx += blockDim.x) {
-    const uint32_t tok = t0 + idx / nrow, row = rlo + idx % nrow;
-    float sum = 0.f;
-    for (uint32_t c = 0; c < a.CB; ++c)
-      sum += __hip_atomic_load(p.partial + ((uint64_t)c * p.T + tok) * R + row, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-    p.y[(uint64_t)tok * R + row] = sum;
+}
+
+// Y = the sum of the KS partial products, in range order.
+__global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* partial, float* y, uint32_t KS,
+                                                          uint64_t n) {
+  for (uint64_t k = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; k < n; k += (uint64_t)gridDim.x * blockDim.x) {
+    float s = partial[k];
+    for (uint32_t r = 1; r < KS; ++r) s += partial[(uint64_t)r * n + k];
+    y[k] = s;
   }
-  if (threadIdx.x == 0) __hip_atomic_store(p.counter + rs + ck * p.RS, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ------------------------------------------------------------------ persistent fused GEMV
@@ -2057,8 +2047,7 @@ static uint32_t gemm_row_sets(const hl_tensor* t) { return (uint32_t)((t->rows +
 extern "C" size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens) {
   if (!t || tokens == 0 || t->seg_len == 0 || t->grp_rows != 16) return 0;
   const uint64_t CB = (t->cols / t->seg_len) / 4;
-  const uint64_t counters = (uint64_t)gemm_row_sets(t) * ((tokens + 15) / 16) * 4;
-  return (size_t)(((counters + 255) & ~255ull) + CB * tokens * t->rows * 4);
+  return (size_t)(CB * tokens * t->rows * 4);
 }
 
 template <int SP>
@@ -2099,15 +2088,23 @@ extern "C" hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dt
   p.T = tokens;
   p.RS = gemm_row_sets(t);
   p.x_off = (uint32_t)slice;
+  const uint32_t CB = pl.ga.CB;
   const uint32_t chunks = (tokens + 16 * nt - 1) / (16 * nt);
-  const uint64_t counters = (uint64_t)p.RS * ((tokens + 15) / 16) * 4;
-  p.counter = reinterpret_cast<uint32_t*>(workspace_dev);
-  p.partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + ((counters + 255) & ~255ull));
-  const uint64_t blocks = (uint64_t)pl.ga.CB * p.RS * chunks;
+  // Column blocks per block: all of them when the row sets and chunks alone
+  // give two blocks per CU; else split so that they do (one block fits a CU).
+  const uint64_t base = (uint64_t)p.RS * chunks, target = 2ull * device_cus();
+  p.cpb = base >= target ? CB : std::max<uint32_t>(1, (uint32_t)(CB * base / target));
+  p.KS = (CB + p.cpb - 1) / p.cpb;
+  p.partial = reinterpret_cast<float*>(workspace_dev);
+  const uint64_t blocks = (uint64_t)p.KS * base;
   if (blocks >= (1ull << 31)) return HL_EUNSUPPORTED;
   const size_t lds = slice + cols_bytes;
-  return SP == 8 ? launch_gemm_sp<8>(nt, dim3((uint32_t)blocks), lds, (hipStream_t)stream, p)
-                 : launch_gemm_sp<4>(nt, dim3((uint32_t)blocks), lds, (hipStream_t)stream, p);
+  st = SP == 8 ? launch_gemm_sp<8>(nt, dim3((uint32_t)blocks), lds, (hipStream_t)stream, p)
+               : launch_gemm_sp<4>(nt, dim3((uint32_t)blocks), lds, (hipStream_t)stream, p);
+  if (st != HL_OK || p.KS == 1) return st;
+  const uint64_t n = (uint64_t)tokens * t->rows;
+  const uint32_t rblocks = (uint32_t)std::min<uint64_t>((n + 255) / 256, (uint64_t)device_cus() * 8);
+  return launch(gemm_reduce_kernel, dim3(rblocks), dim3(256), 0, (hipStream_t)stream, p.partial, y_dev, p.KS, n);
 }
 
 extern "C" hl_status hl_gemv_bf16(const uint16_t* w_dev, uint64_t rows, uint64_t cols, const void* x_dev,
