@@ -35,7 +35,8 @@ constexpr int kLutBits = 13;
 constexpr int kLutN = 1 << kLutBits;   // joint window table entries
 constexpr int kAuxWords = 64;          // canonical tables for the long-code path
 constexpr int kAuxField = 24;          // words per field in the aux table
-constexpr uint32_t kEsc = 0x80u;       // entry of a pair longer than the window
+constexpr uint32_t kEsc = 0x80000080u; // entry of a pair longer than the window
+constexpr uint32_t kElKnown = 1u << 16; // ... whose el code fits: its length in bits 8..11, el in 12..15
 constexpr int kMaxWaves = 16;
 constexpr uint32_t kCol = 64;          // row stride of the stream columns, in words
 
@@ -43,9 +44,12 @@ static_assert(HL_LUT_BYTES >= (kLutN + kAuxWords) * 4, "table size");
 
 // Joint table entry: bits 0..4 = code bits of the (el, eh) pair, bits 23..30 =
 // the exponent byte eh<<4|el (its place in a float32), all other bits zero.
-// A window whose pair is longer than 13 bits maps to kEsc (0x80): as a shift
-// it moves nothing, as a position increment it adds 128, which eight pairs of
-// at most 13 bits cannot reach, so one compare per eight weights finds it.
+// A window whose pair is longer than 13 bits maps to kEsc (bits 7 and 31),
+// plus kElKnown with el's code length and value when el's code alone fits.
+// Bit 31 makes the entry negative, a one-compare test per table read; as a
+// shift it moves nothing (bits 0..5 are zero); as a position increment it adds
+// at least 128, which eight pairs of at most 13 bits cannot reach, so one
+// compare per eight weights finds an escape that the fast path left.
 // Aux table, per field f (0 = eh, 1 = el) at word f*24: [0] = nsym |
 // single<<8 | maxlen<<16; [l], l = 1..15: first_code<<16 | count<<8 | offset;
 // [16..19]: symbols sorted by (length, symbol), one byte each.
@@ -90,7 +94,7 @@ static Aux make_aux(const hl_codebook& cb) {
 // ------------------------------------------------------------------ device
 
 // Joint table and aux tables, at a fixed LDS address in every kernel that decodes.
-__shared__ uint32_t s_tab[kLutN + kAuxWords];
+__shared__ __attribute__((aligned(16))) uint32_t s_tab[kLutN + kAuxWords];
 extern __shared__ uint32_t s_dyn[];
 
 // One field, bit-serial canonical decode from `bits` (LSB = next bit), using
@@ -121,7 +125,9 @@ __global__ void __launch_bounds__(256) lut_kernel(uint32_t* lut, Aux aux) {
     uint32_t ua = 0, ub = 0;
     const int b = field_from_bits(aux.w + kAuxField, (uint32_t)v, kLutBits, &ub);  // el first
     const int a = b < 0 ? -1 : field_from_bits(aux.w, (uint32_t)v >> ub, kLutBits - ub, &ua);
-    lut[v] = (a < 0 || b < 0) ? kEsc : ((ua + ub) | ((uint32_t)((a << 4) | b) << 23));
+    lut[v] = b < 0   ? kEsc
+             : a < 0 ? kEsc | kElKnown | (ub << 8) | ((uint32_t)b << 12)
+                     : ((ua + ub) | ((uint32_t)((a << 4) | b) << 23));
   }
   for (int i = threadIdx.x; i < kAuxWords; i += blockDim.x) lut[kLutN + i] = aux.w[i];
 }
@@ -308,44 +314,93 @@ __device__ inline uint64_t shift_window(uint64_t w, uint32_t ent) {
   return r;
 }
 
-struct Dec4 {
-  uint32_t pos2, e0, e1, e2, e3;
+struct Pairs8 {  // eight bf16-path entries and the position after them
+  uint32_t pos2, e[8];
 };
 
-// Careful path: one weight at a time, long pairs decoded bit-serially.
+// Careful path for eight weights: the pairs of a window one after another,
+// as in the fast path, with a pair longer than the table's 13 bits decoded
+// field by field from the window's bits (el from the table entry when its
+// code fits in 13 bits, else bit by bit, then eh bit by bit). The window is
+// read again at the pair's position when fewer than 13 of its 62 bits are
+// left (fewer than 30 for a long pair). A rolled loop keeps the code small:
+// kernels that inline a copy per step stay within the instruction cache.
 // pos2: a clean position (no exponent bits above bit 22). The body is shared
 // by an out-of-line copy and an inlined one (see decode8).
-__device__ __attribute__((always_inline)) inline Dec4 decode4_careful_body(uint32_t sc_off, uint32_t jmax,
+__device__ __attribute__((always_inline)) inline Pairs8 decode8_careful_body(uint32_t sc_off, uint32_t jmax,
                                                                            uint32_t pos2) {
   asm volatile("" ::: "memory");  // keeps its table reads inside the (cold) path
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t* aux = s_tab + kLutN;
-  uint32_t e[4];
+  Pairs8 d;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    uint32_t ent = lut_at((uint32_t)load_window(sc, pos2, jmax));
-    if (ent & kEsc) {
-      uint32_t p = pos2 + 2;
-      const uint32_t b = slow_field(sc, aux + kAuxField, p, jmax + 2);  // el first
-      const uint32_t a = slow_field(sc, aux, p, jmax + 2);
-      ent = (p - pos2 - 2) | (((a << 4) | b) << 23);
+  for (int j = 0; j < 8; ++j) d.e[j] = 0;
+  uint64_t W = 0;
+  uint32_t used = 64;  // bits of W consumed (none loaded yet)
+#pragma unroll 1
+  for (uint32_t k = 0; k < 8; ++k) {
+    if (used > 62 - 13) {
+      W = load_window(sc, pos2, jmax);
+      used = 0;
     }
+    uint32_t ent = lut_at((uint32_t)W);
+    if (ent & kEsc) {
+      if (used > 62 - 30) {
+        W = load_window(sc, pos2, jmax);
+        used = 0;
+      }
+      const uint32_t bits = (uint32_t)(W >> 2);  // the code bits from the position on
+      uint32_t ub = 0, ua = 0;
+      int b;
+      if (ent & kElKnown) {  // the table decoded el: only eh is left, a code of a few bits
+        ub = (ent >> 8) & 0xF;
+        b = (int)((ent >> 12) & 0xF);
+      } else {
+        b = field_from_bits(aux + kAuxField, bits, 32, &ub);  // el first
+      }
+      int a = b < 0 ? -1 : field_from_bits(aux, bits >> ub, 32 - ub, &ua);
+      if (b < 0) b = 0, ub = 0;  // no code matches (a damaged stream): decode on, in bounds
+      if (a < 0) a = 0, ua = 0;
+      ent = (ua + ub) | ((uint32_t)((a << 4) | b) << 23);
+    }
+    W = shift_window(W, ent);
+    used += ent & 0xFF;
     pos2 += ent & 0xFF;
-    e[k] = ent;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) d.e[j] = k == (uint32_t)j ? ent : d.e[j];
   }
-  return Dec4{pos2, e[0], e[1], e[2], e[3]};
+  d.pos2 = pos2;
+  return d;
 }
 
-__device__ __noinline__ Dec4 decode4_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
-  return decode4_careful_body(sc_off, jmax, pos2);
+__device__ __noinline__ Pairs8 decode8_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
+  return decode8_careful_body(sc_off, jmax, pos2);
+}
+
+// A pair longer than the table window, within the fast path: el from the
+// escape entry, eh bit by bit from the window. Left as an escape (for the
+// careful path) when el's code is longer than the table window, when no eh
+// code matches, or when the pair runs past the window's 62 bits (`used` of
+// them are consumed).
+__device__ __attribute__((always_inline)) inline uint32_t long_pair(uint32_t ent, uint64_t W, uint32_t used) {
+  if (!(ent & kElKnown)) return ent;
+  const uint32_t ub = (ent >> 8) & 0xF, b = (ent >> 12) & 0xF;
+  uint32_t ua = 0;
+  const int a = field_from_bits(s_tab + kLutN, (uint32_t)(W >> 2) >> ub, 32 - ub, &ua);
+  if (a < 0 || used + ub + ua > 62) return ent;
+  return (ua + ub) | ((uint32_t)((a << 4) | b) << 23);
 }
 
 // Decodes 4 weights from one 64-bit window (four pairs of at most 13 bits
 // fit): table entries e[4] (bits 23..30 = exponent byte), p advanced by the
 // whole entries. Bits 0..22 of a position are the bit position; the exponent
 // bytes pile up above them and are never read.
+// A pair longer than the table window: a window with an escape among its four
+// reads (one wave-uniform test per window) is decoded again by the lanes that
+// had one, which resolve long pairs from the window's bits.
 __device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t& p, uint32_t* e) {
-  uint64_t W = load_window(sc, p, jmax);
+  const uint64_t W0 = load_window(sc, p, jmax);
+  uint64_t W = W0;
   e[0] = lut_at((uint32_t)W);
   W = shift_window(W, e[0]);
   e[1] = lut_at((uint32_t)W);
@@ -353,12 +408,29 @@ __device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t&
   e[2] = lut_at((uint32_t)W);
   W = shift_window(W, e[2]);
   e[3] = lut_at((uint32_t)W);
+  const uint32_t any = e[0] | e[1] | e[2] | e[3];
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0)) {
+    if ((int)any < 0) {
+      W = W0;
+      uint32_t used = 0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        uint32_t ent = lut_at((uint32_t)W);
+        if ((int)ent < 0) ent = long_pair(ent, W, used);
+        W = shift_window(W, ent);
+        used += ent & 0x3F;
+        e[k] = ent;
+      }
+    }
+  }
   p = p + e[0] + e[1] + e[2] + e[3];
 }
 
-// Decodes 8 weights. A long pair anywhere (an escape adds 128 to the low bits
-// of the position; eight short pairs add at most 104) sends the lane through
-// the careful path from the first of the eight. After an escape the second
+// Decodes 8 weights. A long pair that the fast path left (an escape adds 128
+// to the low bits of the position; eight pairs that the fast path decoded add
+// less, unless long pairs among them sum past 127, which only costs the
+// careful path) sends the lane through the careful path from the first of the
+// eight. After an escape the second
 // window may be read at a wrong (clamped, in-region) position; its entries are
 // discarded.
 // INLINE_SLOW selects an inlined, cold-placed careful path instead of a call:
@@ -371,18 +443,11 @@ __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jma
   decode4_fast(sc, jmax, p, e);
   decode4_fast(sc, jmax, p, e + 4);
   if (__builtin_expect(((p - p0) & (kPosMask & ~0x7Fu)) != 0, 0)) {
-    const Dec4 d0 = INLINE_SLOW ? decode4_careful_body(sc_off, jmax, p0 & kPosMask)
-                                : decode4_careful(sc_off, jmax, p0 & kPosMask);
-    const Dec4 d1 = INLINE_SLOW ? decode4_careful_body(sc_off, jmax, d0.pos2) : decode4_careful(sc_off, jmax, d0.pos2);
-    p = d1.pos2;
-    e[0] = d0.e0;
-    e[1] = d0.e1;
-    e[2] = d0.e2;
-    e[3] = d0.e3;
-    e[4] = d1.e0;
-    e[5] = d1.e1;
-    e[6] = d1.e2;
-    e[7] = d1.e3;
+    const Pairs8 d = INLINE_SLOW ? decode8_careful_body(sc_off, jmax, p0 & kPosMask)
+                               : decode8_careful(sc_off, jmax, p0 & kPosMask);
+    p = d.pos2;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) e[j] = d.e[j];
   }
   pos2 = p;
 }

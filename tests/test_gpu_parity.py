@@ -97,7 +97,11 @@ def test_long_codes_take_the_slow_path(torch, lmax):
     assert bytes(blob) == codec.encode(w, seg_len=64, lmax=lmax)
     h = codec.parse_header(bytes(blob))
     if lmax == 15:
-        assert max(h["el_len"]) + max(h["eh_len"]) > 13
+        # el codes past the table window too (the bit-by-bit el decode)
+        assert max(h["el_len"]) > 13 and max(h["el_len"]) + max(h["eh_len"]) > 13
+    if lmax == 12:
+        # pairs past the window whose el code fits in it (el from the table)
+        assert max(h["el_len"]) <= 13 < max(h["el_len"]) + max(h["eh_len"])
     dt = hl.DeviceTensor(blob)
     assert np.array_equal(_decode(torch, dt), w)
     x = random_x(2, 512, seed=1, dtype="bf16")
