@@ -391,6 +391,20 @@ __device__ __attribute__((always_inline)) inline uint32_t long_pair(uint32_t ent
   return (ua + ub) | ((uint32_t)((a << 4) | b) << 23);
 }
 
+// The four table reads of the window W0 again, resolving long pairs.
+__device__ __attribute__((always_inline)) inline void redo4(uint64_t W0, uint32_t* e) {
+  uint64_t W = W0;
+  uint32_t used = 0;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    uint32_t ent = lut_at((uint32_t)W);
+    if ((int)ent < 0) ent = long_pair(ent, W, used);
+    W = shift_window(W, ent);
+    used += ent & 0x3F;
+    e[k] = ent;
+  }
+}
+
 // Decodes 4 weights from one 64-bit window (four pairs of at most 13 bits
 // fit): table entries e[4] (bits 23..30 = exponent byte), p advanced by the
 // whole entries. Bits 0..22 of a position are the bit position; the exponent
@@ -409,20 +423,8 @@ __device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t&
   W = shift_window(W, e[2]);
   e[3] = lut_at((uint32_t)W);
   const uint32_t any = e[0] | e[1] | e[2] | e[3];
-  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0)) {
-    if ((int)any < 0) {
-      W = W0;
-      uint32_t used = 0;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        uint32_t ent = lut_at((uint32_t)W);
-        if ((int)ent < 0) ent = long_pair(ent, W, used);
-        W = shift_window(W, ent);
-        used += ent & 0x3F;
-        e[k] = ent;
-      }
-    }
-  }
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0))
+    if ((int)any < 0) redo4(W0, e);
   p = p + e[0] + e[1] + e[2] + e[3];
 }
 
@@ -2083,6 +2085,9 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     const size_t per_wave = (size_t)(jt + 1) * kCol * 4;
     uint32_t w = kMaxWaves;
     while (w > 1 && tab + w * per_wave > kMaxLds) --w;
+    // fewer waves per block when that gives every wave two groups: the
+    // second group's loads then overlap the first one's decode
+    while (w > 8 && (uint64_t)RB * CB < 2ull * cus * w) --w;
     if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
       p.C = CB;
       p.KS = 1;
