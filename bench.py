@@ -75,6 +75,7 @@ def parse():
                     help="container of the headline: split exponent (two 4-bit codes), whole exponent, or "
                          "the float16 {1,5,5,5} format on the float16 copy of the matrix")
     ap.add_argument("--no-variant", action="store_true", help="skip timing the other container formats")
+    ap.add_argument("--no-prefill", action="store_true", help="skip timing the prefill decode-GEMM")
     return ap.parse_args()
 
 
@@ -214,6 +215,41 @@ def measure_container(torch, hl, blob, spec, W, batches, args, single_launches, 
     return results, seg_len
 
 
+def measure_prefill(torch, hl, blob, spec, W, args, token_counts=(32, 128, 512)):
+    """Graph-timed prefill products Y = X W^T for several token counts over cold
+    replicas of the container, with torch's bf16 GEMM on cold replicas of the
+    uncompressed matrix as the comparator; sampled outputs of the timed launches
+    are checked against the oracle."""
+    from oracle import gemv as ogemv
+    from gen import random_x
+    R, K = spec.rows, spec.cols
+    n = R * K
+    nrep = max(2, math.ceil(COLD_BYTES / blob.size))
+    tensors = [hl.DeviceTensor(blob) for _ in range(nrep)]
+    wdev = torch.from_numpy(W.view(np.int16)).view(torch.bfloat16).cuda()
+    nrep_b = max(2, math.ceil(COLD_BYTES / (2 * n)))
+    wreps = [wdev.clone() for _ in range(nrep_b)]
+    out = {}
+    steps = max(10, min(args.steps, 100))
+    for T in token_counts:
+        xb = random_x(T, K, seed=T, dtype="bf16")
+        xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+        y = torch.empty((T, R), dtype=torch.float32, device="cuda")
+        tensors[0].gemm(xd, y)  # workspaces allocated outside the graph
+        for t_ in tensors:
+            t_._gemm_ws = tensors[0]._gemm_ws
+        ms = time_graph(torch, lambda i: tensors[i].gemm(xd, y), nrep, steps, 5)
+        rows = list(range(0, R, R // 8))
+        y_ref, den = ogemv.gemv_rows(W, xb[[0, T - 1]], rows=rows)
+        err = float(np.max(ogemv.rel_err(y.cpu().numpy()[[0, T - 1]][:, rows], y_ref, den)))
+        ms_t = time_graph(torch, lambda i: torch.nn.functional.linear(xd, wreps[i]), nrep_b, steps, 5)
+        out[f"tokens{T}"] = dict(ms=round(ms, 5), effective_weight_GBps=round(2 * n / (ms * 1e-3) / 1e9, 1),
+                                 TFLOPs=round(2 * n * T / (ms * 1e-3) / 1e12, 2), max_rel_err=err,
+                                 torch_bf16_linear_ms=round(ms_t, 5), speedup_vs_torch=round(ms_t / ms, 3))
+    del tensors, wreps
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -307,6 +343,12 @@ def main():
                 cmp[dt_name][batch] = c
             del wreps, wdev
 
+    # prefill: the batched decode-GEMM of the same container (each weight tile
+    # decoded once per chunk of up to 128 tokens), against torch's bf16 GEMM
+    prefill = {}
+    if not args.no_prefill and args.format != "fp16":
+        prefill = measure_prefill(torch, hl, blob, spec, Ws[args.format], args)
+
     cpu = None
     if not args.no_cpu:
         xb, _ = device_x(torch, spec, 1, args.format)
@@ -340,6 +382,8 @@ def main():
                     min(own[b].values()) / v[f"batch{b}"]["ms_per_step"], 3)
     if variants:
         extra["variants"] = variants
+    if prefill:
+        extra["prefill"] = prefill
     extra["encoder"] = encoder
     out = {
         "metric": METRIC,
