@@ -306,39 +306,27 @@ __device__ inline uint32_t lut_at(uint32_t w) {
                                             (w & ((kLutN - 1) << 2)));
 }
 
-// Window shift by a table entry: v_lshrrev_b64 uses bits 0..5 of the entry,
-// which are the pair length (or 0 for kEsc).
-__device__ inline uint64_t shift_window(uint64_t w, uint32_t ent) {
-  uint64_t r;
-  asm("v_lshrrev_b64 %0, %1, %2" : "=v"(r) : "v"(ent), "v"(w));
-  return r;
-}
+// Window shift by a table entry: bits 0..5 of the entry are the pair length
+// (0 for an escape); v_lshrrev_b64 reads only those bits of its count.
+__device__ inline uint64_t shift_window(uint64_t w, uint32_t ent) { return w >> (ent & 63u); }
 
-struct Pairs8 {  // eight bf16-path entries and the position after them
-  uint32_t pos2, e[8];
-};
-
-// Careful path for eight weights: the pairs of a window one after another,
-// as in the fast path, with a pair longer than the table's 13 bits decoded
-// field by field from the window's bits (el from the table entry when its
-// code fits in 13 bits, else bit by bit, then eh bit by bit). The window is
-// read again at the pair's position when fewer than 13 of its 62 bits are
-// left (fewer than 30 for a long pair). A rolled loop keeps the code small:
-// kernels that inline a copy per step stay within the instruction cache.
-// pos2: a clean position (no exponent bits above bit 22). The body is shared
-// by an out-of-line copy and an inlined one (see decode8).
-__device__ __attribute__((always_inline)) inline Pairs8 decode8_careful_body(uint32_t sc_off, uint32_t jmax,
-                                                                           uint32_t pos2) {
+// Careful path for the four weights of a window: the pairs one after
+// another, each pair longer than the table's 13 bits decoded field by field
+// from the window's bits (el from the table entry when its code fits in 13
+// bits, else bit by bit, then eh bit by bit). The window is read again at the
+// pair's position when fewer than 13 of its 62 bits are left (fewer than 30
+// for a long pair). A rolled loop keeps the (cold, inlined) code small.
+// pos2: the window's clean start position (no exponent bits above bit 22).
+__device__ __attribute__((always_inline)) inline void careful4(uint32_t sc_off, uint32_t jmax, uint32_t pos2,
+                                                              uint32_t* e) {
   asm volatile("" ::: "memory");  // keeps its table reads inside the (cold) path
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t* aux = s_tab + kLutN;
-  Pairs8 d;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) d.e[j] = 0;
+  uint32_t r[4] = {0, 0, 0, 0};
   uint64_t W = 0;
   uint32_t used = 64;  // bits of W consumed (none loaded yet)
 #pragma unroll 1
-  for (uint32_t k = 0; k < 8; ++k) {
+  for (uint32_t k = 0; k < 4; ++k) {
     if (used > 62 - 13) {
       W = load_window(sc, pos2, jmax);
       used = 0;
@@ -367,14 +355,10 @@ __device__ __attribute__((always_inline)) inline Pairs8 decode8_careful_body(uin
     used += ent & 0xFF;
     pos2 += ent & 0xFF;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) d.e[j] = k == (uint32_t)j ? ent : d.e[j];
+    for (int j = 0; j < 4; ++j) r[j] = k == (uint32_t)j ? ent : r[j];
   }
-  d.pos2 = pos2;
-  return d;
-}
-
-__device__ __noinline__ Pairs8 decode8_careful(uint32_t sc_off, uint32_t jmax, uint32_t pos2) {
-  return decode8_careful_body(sc_off, jmax, pos2);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) e[j] = r[j];
 }
 
 // A pair longer than the table window, within the fast path: el from the
@@ -412,7 +396,7 @@ __device__ __attribute__((always_inline)) inline void redo4(uint64_t W0, uint32_
 // A pair longer than the table window: a window with an escape among its four
 // reads (one wave-uniform test per window) is decoded again by the lanes that
 // had one, which resolve long pairs from the window's bits.
-__device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t& p, uint32_t* e) {
+__device__ inline void decode4_fast(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& p, uint32_t* e) {
   const uint64_t W0 = load_window(sc, p, jmax);
   uint64_t W = W0;
   e[0] = lut_at((uint32_t)W);
@@ -423,35 +407,19 @@ __device__ inline void decode4_fast(const uint32_t* sc, uint32_t jmax, uint32_t&
   W = shift_window(W, e[2]);
   e[3] = lut_at((uint32_t)W);
   const uint32_t any = e[0] | e[1] | e[2] | e[3];
-  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0))
-    if ((int)any < 0) redo4(W0, e);
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0)) {
+    if ((int)any < 0) {
+      redo4(W0, e);
+      if ((int)(e[0] | e[1] | e[2] | e[3]) < 0) careful4(sc_off, jmax, p & kPosMask, e);
+    }
+  }
   p = p + e[0] + e[1] + e[2] + e[3];
 }
 
-// Decodes 8 weights. A long pair that the fast path left (an escape adds 128
-// to the low bits of the position; eight pairs that the fast path decoded add
-// less, unless long pairs among them sum past 127, which only costs the
-// careful path) sends the lane through the careful path from the first of the
-// eight. After an escape the second
-// window may be read at a wrong (clamped, in-region) position; its entries are
-// discarded.
-// INLINE_SLOW selects an inlined, cold-placed careful path instead of a call:
-// a call makes the compiler wait for every load in flight whose register is
-// live across it, which the persistent kernel cannot afford.
-template <bool INLINE_SLOW = false>
+// Decodes 8 weights: two windows of four.
 __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* e) {
-  const uint32_t p0 = pos2;
-  uint32_t p = p0;
-  decode4_fast(sc, jmax, p, e);
-  decode4_fast(sc, jmax, p, e + 4);
-  if (__builtin_expect(((p - p0) & (kPosMask & ~0x7Fu)) != 0, 0)) {
-    const Pairs8 d = INLINE_SLOW ? decode8_careful_body(sc_off, jmax, p0 & kPosMask)
-                               : decode8_careful(sc_off, jmax, p0 & kPosMask);
-    p = d.pos2;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) e[j] = d.e[j];
-  }
-  pos2 = p;
+  decode4_fast(sc, sc_off, jmax, pos2, e);
+  decode4_fast(sc, sc_off, jmax, pos2, e + 4);
 }
 
 // Packed bf16 pair (weights k, k+1 of a raw dword) from two table entries.
@@ -1216,6 +1184,11 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   const uint32_t jmax = kRows - 3;
   const uint32_t i = lane & 15, q = lane >> 4;
   const uint16_t* xlane = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
+  // byte offset of the lane's activations from x (a wave-uniform base plus a
+  // 32-bit lane offset lets the prefetch loads address as scalar base +
+  // vector offset + immediate)
+  const uint32_t xoff = (min(i, p.B - 1) * a.cols + q * S) * 2u;
+  const uint8_t* xbytes = reinterpret_cast<const uint8_t*>(p.x);
   const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
   const uint32_t last_group = RB * CB - 1;
 
@@ -1286,16 +1259,17 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
       // then the metadata of the group after it
       uint32_t pos2n = stream_load<JT>(a, m1, lane, sw);
       m1 = load_meta(a, g2, lane);
-      // prefetch source: the next group, else the lane's cached activations at stride 0
-      const uint16_t* xcur = xlane + (wave + j * waves) * 4 * S;
-      const uint8_t* rp = okn ? a.raw + n_first * S + lane_mu(rbn) * 8 : reinterpret_cast<const uint8_t*>(xcur);
-      const uint16_t* xp = okn ? xlane + n_c0 * S : xcur;
-      const uint32_t rs = okn ? Gn * 32u : 0u, xs = okn ? 8u : 0u;
+      // prefetch source: the next group, else the lane's cached activations
+      const uint32_t cur_c0 = (wave + j * waves) * 4;
+      const uint8_t* rbase = okn ? a.raw + n_first * S : xbytes + cur_c0 * S * 2;
+      const uint32_t roff = okn ? lane_mu(rbn) * 8 : xoff;
+      const uint32_t rs = okn ? Gn * 32u : 0u;
+      const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * S * 2;
       uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
 #pragma unroll
       for (int k = 0; k < SP; ++k) {
         uint32_t e[8];
-        decode8<true>(sc, sc_off, jmax, pd, e);
+        decode8(sc, sc_off, jmax, pd, e);
         uint4 wv;
         wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
         wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
@@ -1303,8 +1277,9 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
         wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
                                                       __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
-        rw[k] = *reinterpret_cast<const uint2*>(rp + k * rs);
-        xv[k] = *reinterpret_cast<const uint4*>(xp + k * xs);
+        // x first: the wait for the raw bytes at their use then covers both
+        xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * 16);
+        rw[k] = *reinterpret_cast<const uint2*>(rbase + k * rs + roff);
       }
       wait_lgkm0();
       wave_sync_lds();
