@@ -917,7 +917,7 @@ __device__ inline void mfma_finish(const GemvArgs& p, const f32x4_t& acc, float*
 // are read straight into registers, KP steps ahead of their use, the last
 // chunk of a group prefetching the next group's first chunk. SP = S/8 steps
 // per group, unrolled so that every wait on a prefetch is exact.
-template <int SP>
+template <int SP, bool XT>
 __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
   constexpr int KP = SP < 8 ? SP : SP == 8 ? 8 : 4;  // 16 steps at depth 8 exceed 128 VGPRs
   const GroupArgs& a = p.g;
@@ -937,7 +937,12 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
   const uint32_t sc_off = wave * per_wave + mu;
   const uint32_t* sc = s_dyn + sc_off;
   const uint32_t rstride = N * 8;  // bytes between 8-weight steps of the raw plane
-  const uint16_t* xrow = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
+  // the lane's activations: x[n = i][(c0 + q)*S + 8k .. +8) at xlane + c0*XSEG + k*XSTEP (bytes), from x
+  // itself or (XT) from its tiled copy, where the 16 batch rows' pieces of one
+  // 8-column chunk are 256 contiguous bytes
+  constexpr uint32_t XSEG = XT ? SP * 256 : S * 2, XSTEP = XT ? 256 : 16;
+  const uint8_t* xlane = reinterpret_cast<const uint8_t*>(p.x) +
+                         (XT ? (q * SP * 16 + i) * 16u : ((uint64_t)min(i, p.B - 1) * a.cols + q * S) * 2u);
 
   const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
   uint32_t cb = kp * p.C + wave;
@@ -954,11 +959,11 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
   uint4 xv[KP];
   {
     const uint8_t* r = a.raw + m.first * S + mu * 8;
-    const uint16_t* x = xrow + m.c0 * S;
+    const uint8_t* x = xlane + m.c0 * XSEG;
 #pragma unroll
     for (int k = 0; k < KP; ++k) {
       rw[k] = *reinterpret_cast<const uint2*>(r + k * rstride);
-      xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
+      xv[k] = *reinterpret_cast<const uint4*>(x + k * XSTEP);
     }
   }
   // the first use of the metadata stays behind the loads above
@@ -977,21 +982,21 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
     wave_sync_lds();
     const uint32_t pos2l = (uint32_t)__shfl((int)pos2, (int)mu, 64);
     const uint8_t* rcur = a.raw + cur.first * S + mu * 8;
-    const uint16_t* xcur = xrow + cur.c0 * S;
+    const uint8_t* xcur = xlane + cur.c0 * XSEG;
     // Prefetch source of the last chunk: the next group; after the wave's
     // last group, the lane's own first activation chunk (cache-resident) at
     // stride 0, so that the pipeline's loads stay unconditional without
     // reading HBM again.
     const uint8_t* rnext = more ? a.raw + mn.first * S + mu * 8 : reinterpret_cast<const uint8_t*>(xcur);
-    const uint16_t* xnext = more ? xrow + mn.c0 * S : xcur;
-    const uint32_t rs_last = more ? rstride : 0u, xs_last = more ? 8u : 0u;
+    const uint8_t* xnext = more ? xlane + mn.c0 * XSEG : xcur;
+    const uint32_t rs_last = more ? rstride : 0u, xs_last = more ? XSTEP : 0u;
     uint32_t pd = pos2l;
 #pragma unroll
     for (int t0 = 0; t0 < SP; t0 += KP) {
       const bool last = t0 + KP == SP;
       const uint8_t* rp = last ? rnext : rcur + (t0 + KP) * rstride;
-      const uint16_t* xp = last ? xnext : xcur + (t0 + KP) * 8;
-      const uint32_t rs = last ? rs_last : rstride, xs = last ? xs_last : 8u;
+      const uint8_t* xp = last ? xnext : xcur + (t0 + KP) * XSTEP;
+      const uint32_t rs = last ? rs_last : rstride, xs = last ? xs_last : XSTEP;
 #pragma unroll
       for (int k = 0; k < KP; ++k) {
         uint32_t e[8];
@@ -1172,7 +1177,7 @@ __global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* partial, 
 // wait the compiler places is exact. At a row block's end the waves add their
 // accumulators through their columns in a fixed order (before the next
 // group's words go in) and four waves write y.
-template <int SP, int JT>
+template <int SP, int JT, bool XT>
 __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
@@ -1183,11 +1188,13 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   uint32_t* cols = s_dyn + wave * kBuf;
   const uint32_t jmax = kRows - 3;
   const uint32_t i = lane & 15, q = lane >> 4;
-  const uint16_t* xlane = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
-  // byte offset of the lane's activations from x (a wave-uniform base plus a
-  // 32-bit lane offset lets the prefetch loads address as scalar base +
-  // vector offset + immediate)
-  const uint32_t xoff = (min(i, p.B - 1) * a.cols + q * S) * 2u;
+  // byte offset of the lane's activations x[n = i][(c0 + q)*S + 8k .. +8) at
+  // x + c0*XSEG + xoff + k*XSTEP, from x itself or (XT) from its tiled copy,
+  // where the 16 batch rows' pieces of one 8-column chunk are 256 contiguous
+  // bytes (a wave-uniform base plus a 32-bit lane offset lets the prefetch
+  // loads address as scalar base + vector offset + immediate)
+  constexpr uint32_t XSEG = XT ? SP * 256 : S * 2, XSTEP = XT ? 256 : 16;
+  const uint32_t xoff = XT ? (q * SP * 16 + i) * 16u : (min(i, p.B - 1) * a.cols + q * S) * 2u;
   const uint8_t* xbytes = reinterpret_cast<const uint8_t*>(p.x);
   const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
   const uint32_t last_group = RB * CB - 1;
@@ -1222,11 +1229,11 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
     const uint32_t rb = g0 / CB;
     const uint32_t G = min(16u, a.rows - rb * 16);
     const uint8_t* r = a.raw + m0.first * S + lane_mu(rb) * 8;
-    const uint16_t* x = xlane + m0.c0 * S;
+    const uint8_t* x = xbytes + m0.c0 * XSEG + xoff;
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
       rw[k] = *reinterpret_cast<const uint2*>(r + k * G * 32u);
-      xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
+      xv[k] = *reinterpret_cast<const uint4*>(x + k * XSTEP);
     }
   }
   u32x4_a4 sw[JT / 4];
@@ -1261,10 +1268,10 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
       m1 = load_meta(a, g2, lane);
       // prefetch source: the next group, else the lane's cached activations
       const uint32_t cur_c0 = (wave + j * waves) * 4;
-      const uint8_t* rbase = okn ? a.raw + n_first * S : xbytes + cur_c0 * S * 2;
+      const uint8_t* rbase = okn ? a.raw + n_first * S : xbytes + cur_c0 * XSEG;
       const uint32_t roff = okn ? lane_mu(rbn) * 8 : xoff;
       const uint32_t rs = okn ? Gn * 32u : 0u;
-      const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * S * 2;
+      const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * XSEG;
       uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
 #pragma unroll
       for (int k = 0; k < SP; ++k) {
@@ -1278,7 +1285,7 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
                                                       __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
         // x first: the wait for the raw bytes at their use then covers both
-        xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * 16);
+        xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
         rw[k] = *reinterpret_cast<const uint2*>(rbase + k * rs + roff);
       }
       wait_lgkm0();
@@ -1312,6 +1319,17 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
     wave_sync_lds();
   }
   wait_vm0();  // prefetches past the last group
+}
+
+// Tiled copy of bf16 activations for batches above one: xt[c][n][0..8) =
+// x[min(n, B - 1)][8c .. 8c + 8) for the 16 lanes n of a matrix-instruction
+// B operand, so that the 16 lanes reading one 8-column chunk read 256
+// contiguous bytes (from x itself they touch 16 rows, 16 cache lines).
+__global__ void __launch_bounds__(256) xtile_kernel(const uint4* x, uint32_t B, uint32_t chunks, uint4* xt) {
+  const uint32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= chunks * 16) return;
+  const uint32_t c = k >> 4, n = min(k & 15u, B - 1);
+  xt[k] = x[(uint64_t)n * chunks + c];
 }
 
 // ------------------------------------------------------------------ float16 format
@@ -1817,21 +1835,28 @@ static int stream_rows_for(uint32_t seg_len, uint32_t col_rows) {
   return 0;
 }
 
-static hl_status launch_stream(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                               const GemvArgs& p) {
+template <bool XT>
+static hl_status launch_stream_x(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                                 const GemvArgs& p) {
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8>, grid, block, lds, s, p);
-    case 12: return launch(gemv_stream_kernel<4, 12>, grid, block, lds, s, p);
+    case 8: return launch(gemv_stream_kernel<4, 8, XT>, grid, block, lds, s, p);
+    case 12: return launch(gemv_stream_kernel<4, 12, XT>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
+}
+
+static hl_status launch_stream(bool xt, uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               const GemvArgs& p) {
+  return xt ? launch_stream_x<true>(seg_len, jt, grid, block, lds, s, p)
+            : launch_stream_x<false>(seg_len, jt, grid, block, lds, s, p);
 }
 
 // Segment lengths with a matrix-core instantiation (S = 8 * steps).
@@ -1839,16 +1864,22 @@ static bool mfma_steps_ok(uint32_t steps) {
   return steps == 1 || steps == 2 || steps == 4 || steps == 8 || steps == 16;
 }
 
-static hl_status launch_mfma(uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                             const GemvArgs& p) {
+template <bool XT>
+static hl_status launch_mfma_x(uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               const GemvArgs& p) {
   switch (steps) {
-    case 1: return launch(gemv_mfma_kernel<1>, grid, block, lds, s, p);
-    case 2: return launch(gemv_mfma_kernel<2>, grid, block, lds, s, p);
-    case 4: return launch(gemv_mfma_kernel<4>, grid, block, lds, s, p);
-    case 8: return launch(gemv_mfma_kernel<8>, grid, block, lds, s, p);
-    case 16: return launch(gemv_mfma_kernel<16>, grid, block, lds, s, p);
+    case 1: return launch(gemv_mfma_kernel<1, XT>, grid, block, lds, s, p);
+    case 2: return launch(gemv_mfma_kernel<2, XT>, grid, block, lds, s, p);
+    case 4: return launch(gemv_mfma_kernel<4, XT>, grid, block, lds, s, p);
+    case 8: return launch(gemv_mfma_kernel<8, XT>, grid, block, lds, s, p);
+    case 16: return launch(gemv_mfma_kernel<16, XT>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
+}
+
+static hl_status launch_mfma(bool xt, uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                             const GemvArgs& p) {
+  return xt ? launch_mfma_x<true>(steps, grid, block, lds, s, p) : launch_mfma_x<false>(steps, grid, block, lds, s, p);
 }
 
 template <int B>
@@ -1956,6 +1987,16 @@ static uint32_t ks_cap(uint32_t CB) { return std::min<uint32_t>(CB, 64); }
 
 static uint64_t workspace_counter_bytes(uint32_t RB) { return ((uint64_t)RB * 4 + 255) & ~255ull; }
 
+// Workspace layout: RB arrival counters, the split partial sums, then (batch
+// above one, 16-row groups) the tiled copy of bf16 activations: 32 bytes per
+// column.
+static uint64_t xtile_offset(uint32_t RB, uint32_t CB, uint32_t GR, uint32_t batch) {
+  return (workspace_counter_bytes(RB) + (uint64_t)ks_cap(CB) * batch * RB * GR * 4 + 255) & ~255ull;
+}
+static uint64_t xtile_bytes(const hl_tensor* t, uint32_t batch) {
+  return (batch > 1 && t->grp_rows == 16 && t->format != HL_FORMAT_FP16) ? (uint64_t)t->cols * 32 : 0;
+}
+
 extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
   if (!t || t->seg_len == 0 || t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS || batch < 1 ||
       batch > HL_MAX_BATCH)
@@ -1963,7 +2004,7 @@ extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
   const uint32_t GR = t->grp_rows;
   const uint32_t RB = (uint32_t)((t->rows + GR - 1) / GR);
   const uint32_t CB = (uint32_t)(t->cols / t->seg_len) / (HL_GROUP_SEGS / GR);
-  return workspace_counter_bytes(RB) + (uint64_t)ks_cap(CB) * batch * RB * GR * 4;
+  return xtile_offset(RB, CB, GR, batch) + xtile_bytes(t, batch);
 }
 
 // Column blocks per block (C) and blocks per row block (KS) of the
@@ -2052,6 +2093,24 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   p.B = batch;
   const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
   const uint32_t cus = (uint32_t)device_cus();
+  // Larger batches on the matrix cores read the activations from a tiled copy
+  // in the workspace (when it is large enough): the copy costs a launch (about
+  // 2.5 us), and reading 16 rows per 8-column chunk costs more the larger the
+  // batch and the matrix (4096x4096: +1.5 us at batch 8; 28672x8192: +3.5 us at
+  // batch 4, +41 us at batch 8, +109 us at batch 16).
+  const uint64_t n = t->rows * t->cols;
+  const bool want_xt = batch >= 12 || (batch >= 8 && n >= (32ull << 20)) || (batch >= 4 && n >= (128ull << 20));
+  bool xt = false;
+  if (mfma && want_xt && workspace_dev && workspace_bytes >= hl_gemv_workspace_bytes(t, batch)) {
+    uint4* tile = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(workspace_dev) +
+                                           xtile_offset(RB, CB, t->grp_rows, batch));
+    const uint32_t chunks = (uint32_t)(t->cols / 8);
+    st = launch(xtile_kernel, dim3((chunks * 16 + 255) / 256), dim3(256), 0, (hipStream_t)stream,
+                reinterpret_cast<const uint4*>(x_dev), batch, chunks, tile);
+    if (st != HL_OK) return st;
+    p.x = tile;
+    xt = true;
+  }
   // Persistent kernel: S = 32 or 64, at least one row block per CU and two
   // groups per wave.
   if (mfma && (t->seg_len == 64 || t->seg_len == 32)) {
@@ -2066,8 +2125,8 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
       p.C = CB;
       p.KS = 1;
-      return launch_stream(t->seg_len, jt, dim3(std::min(RB, cus)), dim3(w * 64), w * per_wave, (hipStream_t)stream,
-                           p);
+      return launch_stream(xt, t->seg_len, jt, dim3(std::min(RB, cus)), dim3(w * 64), w * per_wave,
+                           (hipStream_t)stream, p);
     }
   }
   // Column blocks per block and blocks per row block.
@@ -2077,7 +2136,7 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   if (mfma) {
     // the reduction reuses the wave regions: 4 floats per lane per wave
     const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * 4 * 64 * 4);
-    return launch_mfma(t->seg_len / 8, grid, block, lds, (hipStream_t)stream, p);
+    return launch_mfma(xt, t->seg_len / 8, grid, block, lds, (hipStream_t)stream, p);
   }
   const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * batch * 64 * 4);
   HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
