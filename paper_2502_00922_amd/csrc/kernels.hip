@@ -46,10 +46,9 @@ static_assert(HL_LUT_BYTES >= (kLutN + kAuxWords) * 4, "table size");
 // the exponent byte eh<<4|el (its place in a float32), all other bits zero.
 // A window whose pair is longer than 13 bits maps to kEsc (bits 7 and 31),
 // plus kElKnown with el's code length and value when el's code alone fits.
-// Bit 31 makes the entry negative, a one-compare test per table read; as a
-// shift it moves nothing (bits 0..5 are zero); as a position increment it adds
-// at least 128, which eight pairs of at most 13 bits cannot reach, so one
-// compare per eight weights finds an escape that the fast path left.
+// Bit 31 makes the entry negative: one test of the OR of a window's four
+// entries finds any escape; as a shift the entry moves nothing (bits 0..5 are
+// zero). Bit 7 keeps escape entries distinct from pair lengths (at most 13).
 // Aux table, per field f (0 = eh, 1 = el) at word f*24: [0] = nsym |
 // single<<8 | maxlen<<16; [l], l = 1..15: first_code<<16 | count<<8 | offset;
 // [16..19]: symbols sorted by (length, symbol), one byte each.
@@ -1603,7 +1602,7 @@ struct Signs {
 // structure (lane 16q + i decodes row i of segment q; the A operand is its 8
 // weights, the B operand x[n = i][8 activations]), with the float16 decode
 // (two table reads per weight) and one sign load per lane and group.
-template <int SP>
+template <int SP, bool XT>
 __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
   constexpr int KP = SP < 8 ? SP : SP == 8 ? 8 : 4;
   const GroupArgs& a = p.g;
@@ -1621,7 +1620,10 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
   const uint32_t mu = q * G + min(i, G - 1);  // the segment this lane decodes
   const uint32_t sc_off = a.t16_words + wave * per_wave + mu;
   const uint32_t* sc = s_dyn + sc_off;
-  const uint16_t* xrow = reinterpret_cast<const uint16_t*>(p.x) + (uint64_t)min(i, p.B - 1) * a.cols + q * S;
+  // activations from x or (XT) from its tiled copy (see gemv_mfma_kernel)
+  constexpr uint32_t XSEG = XT ? SP * 256 : S * 2, XSTEP = XT ? 256 : 16;
+  const uint8_t* xlane = reinterpret_cast<const uint8_t*>(p.x) +
+                         (XT ? (q * SP * 16 + i) * 16u : ((uint64_t)min(i, p.B - 1) * a.cols + q * S) * 2u);
 
   const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
   uint32_t cb = kp * p.C + wave;
@@ -1631,9 +1633,9 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
   uint4 xv[KP];
   Signs<SP> sg;
   {
-    const uint16_t* x = xrow + m.c0 * S;
+    const uint8_t* x = xlane + m.c0 * XSEG;
 #pragma unroll
-    for (int k = 0; k < KP; ++k) xv[k] = *reinterpret_cast<const uint4*>(x + k * 8);
+    for (int k = 0; k < KP; ++k) xv[k] = *reinterpret_cast<const uint4*>(x + k * XSTEP);
     sg.load(a.raw + (m.first + mu) * SP);
   }
   asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
@@ -1649,16 +1651,16 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
     wait_vm0();
     wave_sync_lds();
     const uint32_t pos2l = (uint32_t)__shfl((int)pos2, (int)mu, 64);
-    const uint16_t* xcur = xrow + cur.c0 * S;
-    const uint16_t* xnext = more ? xrow + mn.c0 * S : xcur;
-    const uint32_t xs_last = more ? 8u : 0u;
+    const uint8_t* xcur = xlane + cur.c0 * XSEG;
+    const uint8_t* xnext = more ? xlane + mn.c0 * XSEG : xcur;
+    const uint32_t xs_last = more ? XSTEP : 0u;
     const Signs<SP> sgc = sg;
     uint32_t pd = pos2l;
 #pragma unroll
     for (int t0 = 0; t0 < SP; t0 += KP) {
       const bool last = t0 + KP == SP;
-      const uint16_t* xp = last ? xnext : xcur + (t0 + KP) * 8;
-      const uint32_t xs = last ? xs_last : 8u;
+      const uint8_t* xp = last ? xnext : xcur + (t0 + KP) * XSTEP;
+      const uint32_t xs = last ? xs_last : XSTEP;
 #pragma unroll
       for (int k = 0; k < KP; ++k) {
         uint32_t h[8];
@@ -1994,7 +1996,7 @@ static uint64_t xtile_offset(uint32_t RB, uint32_t CB, uint32_t GR, uint32_t bat
   return (workspace_counter_bytes(RB) + (uint64_t)ks_cap(CB) * batch * RB * GR * 4 + 255) & ~255ull;
 }
 static uint64_t xtile_bytes(const hl_tensor* t, uint32_t batch) {
-  return (batch > 1 && t->grp_rows == 16 && t->format != HL_FORMAT_FP16) ? (uint64_t)t->cols * 32 : 0;
+  return (batch > 1 && t->grp_rows == 16) ? (uint64_t)t->cols * 32 : 0;
 }
 
 extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
@@ -2034,19 +2036,50 @@ static void choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, voi
   }
 }
 
-static hl_status launch_mfma16(uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                               const GemvArgs& p) {
+template <bool XT>
+static hl_status launch_mfma16_x(uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                                 const GemvArgs& p) {
   switch (steps) {
-    case 1: return launch(gemv16_mfma_kernel<1>, grid, block, lds, s, p);
-    case 2: return launch(gemv16_mfma_kernel<2>, grid, block, lds, s, p);
-    case 4: return launch(gemv16_mfma_kernel<4>, grid, block, lds, s, p);
-    case 8: return launch(gemv16_mfma_kernel<8>, grid, block, lds, s, p);
-    case 16: return launch(gemv16_mfma_kernel<16>, grid, block, lds, s, p);
+    case 1: return launch(gemv16_mfma_kernel<1, XT>, grid, block, lds, s, p);
+    case 2: return launch(gemv16_mfma_kernel<2, XT>, grid, block, lds, s, p);
+    case 4: return launch(gemv16_mfma_kernel<4, XT>, grid, block, lds, s, p);
+    case 8: return launch(gemv16_mfma_kernel<8, XT>, grid, block, lds, s, p);
+    case 16: return launch(gemv16_mfma_kernel<16, XT>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
 }
 
+static hl_status launch_mfma16(bool xt, uint32_t steps, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                               const GemvArgs& p) {
+  return xt ? launch_mfma16_x<true>(steps, grid, block, lds, s, p)
+            : launch_mfma16_x<false>(steps, grid, block, lds, s, p);
+}
+
 // Float16 format: the matrix-core kernel only (16-row groups, float16 x).
+// Larger batches on the matrix cores read the activations from a tiled copy
+// in the workspace (when it is large enough): the copy costs a launch (about
+// 2.5 us), and reading 16 rows per 8-column chunk costs more the larger the
+// batch and the matrix (4096x4096: +1.5 us at batch 8; 28672x8192: +3.5 us at
+// batch 4, +41 us at batch 8, +109 us at batch 16). On success with a tiled
+// copy, p->x points to it and *xt is set.
+static hl_status tile_activations(const hl_tensor* t, const void* x_dev, uint32_t batch, void* workspace_dev,
+                                  size_t workspace_bytes, hipStream_t stream, GemvArgs* p, bool* xt) {
+  *xt = false;
+  const uint64_t n = t->rows * t->cols;
+  const bool want = batch >= 12 || (batch >= 8 && n >= (32ull << 20)) || (batch >= 4 && n >= (128ull << 20));
+  if (!want || !workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch)) return HL_OK;
+  const uint32_t GR = t->grp_rows, RB = (uint32_t)((t->rows + GR - 1) / GR);
+  const uint32_t CB = (uint32_t)(t->cols / t->seg_len) / (HL_GROUP_SEGS / GR);
+  uint4* tile = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(workspace_dev) + xtile_offset(RB, CB, GR, batch));
+  const uint32_t chunks = (uint32_t)(t->cols / 8);
+  const hl_status st = launch(xtile_kernel, dim3((chunks * 16 + 255) / 256), dim3(256), 0, stream,
+                              reinterpret_cast<const uint4*>(x_dev), batch, chunks, tile);
+  if (st != HL_OK) return st;
+  p->x = tile;
+  *xt = true;
+  return HL_OK;
+}
+
 static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, float* y_dev, void* workspace_dev,
                         size_t workspace_bytes, hipStream_t stream) {
   if (t->grp_rows != 16 || t->seg_len % 8 || !mfma_steps_ok(t->seg_len / 8)) return HL_EUNSUPPORTED;
@@ -2060,10 +2093,13 @@ static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, f
   p.y = y_dev;
   p.B = batch;
   choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p);
+  bool xt = false;
+  st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, stream, &p, &xt);
+  if (st != HL_OK) return st;
   const dim3 grid(pl.ga.RB * p.KS), block(pl.waves * 64);
   // the reduction reuses the wave regions: 4 floats per lane per wave
   const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.ga.t16_words * 4 + (size_t)pl.waves * 4 * 64 * 4);
-  return launch_mfma16(t->seg_len / 8, grid, block, lds, stream, p);
+  return launch_mfma16(xt, t->seg_len / 8, grid, block, lds, stream, p);
 }
 
 extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
@@ -2093,23 +2129,10 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   p.B = batch;
   const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
   const uint32_t cus = (uint32_t)device_cus();
-  // Larger batches on the matrix cores read the activations from a tiled copy
-  // in the workspace (when it is large enough): the copy costs a launch (about
-  // 2.5 us), and reading 16 rows per 8-column chunk costs more the larger the
-  // batch and the matrix (4096x4096: +1.5 us at batch 8; 28672x8192: +3.5 us at
-  // batch 4, +41 us at batch 8, +109 us at batch 16).
-  const uint64_t n = t->rows * t->cols;
-  const bool want_xt = batch >= 12 || (batch >= 8 && n >= (32ull << 20)) || (batch >= 4 && n >= (128ull << 20));
   bool xt = false;
-  if (mfma && want_xt && workspace_dev && workspace_bytes >= hl_gemv_workspace_bytes(t, batch)) {
-    uint4* tile = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(workspace_dev) +
-                                           xtile_offset(RB, CB, t->grp_rows, batch));
-    const uint32_t chunks = (uint32_t)(t->cols / 8);
-    st = launch(xtile_kernel, dim3((chunks * 16 + 255) / 256), dim3(256), 0, (hipStream_t)stream,
-                reinterpret_cast<const uint4*>(x_dev), batch, chunks, tile);
+  if (mfma) {
+    st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, (hipStream_t)stream, &p, &xt);
     if (st != HL_OK) return st;
-    p.x = tile;
-    xt = true;
   }
   // Persistent kernel: S = 32 or 64, at least one row block per CU and two
   // groups per wave.
