@@ -388,15 +388,14 @@ __device__ __attribute__((always_inline)) inline void redo4(uint64_t W0, uint32_
   }
 }
 
-// Decodes 4 weights from one 64-bit window (four pairs of at most 13 bits
-// fit): table entries e[4] (bits 23..30 = exponent byte), p advanced by the
-// whole entries. Bits 0..22 of a position are the bit position; the exponent
-// bytes pile up above them and are never read.
+// Decodes 4 weights from the 64-bit window W0 at position p (four pairs of at
+// most 13 bits fit): table entries e[4] (bits 23..30 = exponent byte), p
+// advanced by the whole entries. Bits 0..22 of a position are the bit
+// position; the exponent bytes pile up above them and are never read.
 // A pair longer than the table window: a window with an escape among its four
 // reads (one wave-uniform test per window) is decoded again by the lanes that
 // had one, which resolve long pairs from the window's bits.
-__device__ inline void decode4_fast(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& p, uint32_t* e) {
-  const uint64_t W0 = load_window(sc, p, jmax);
+__device__ inline void decode4_win(uint64_t W0, uint32_t sc_off, uint32_t jmax, uint32_t& p, uint32_t* e) {
   uint64_t W = W0;
   e[0] = lut_at((uint32_t)W);
   W = shift_window(W, e[0]);
@@ -415,10 +414,28 @@ __device__ inline void decode4_fast(const uint32_t* sc, uint32_t sc_off, uint32_
   p = p + e[0] + e[1] + e[2] + e[3];
 }
 
-// Decodes 8 weights: two windows of four.
+// 64 bits of the three words (c, b, a) from bit p % 32 of a on.
+__device__ inline uint64_t funnel64(uint32_t c, uint32_t b, uint32_t a, uint32_t p) {
+  return ((uint64_t)__builtin_amdgcn_alignbit(c, b, p) << 32) | __builtin_amdgcn_alignbit(b, a, p);
+}
+
+// Decodes 8 weights: four words of the lane's column are read at once; the
+// first window is bits [p, p + 64) of them, the second starts where the first
+// four pairs ended, within the same four words when that is at most one word
+// further (a rare longer advance reads its window from the column). jmax - 1
+// bounds the first of the four rows (columns hold three rows of overrun).
 __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* e) {
-  decode4_fast(sc, sc_off, jmax, pos2, e);
-  decode4_fast(sc, sc_off, jmax, pos2, e + 4);
+  uint32_t p = pos2;
+  const uint32_t j = min((p & kPosMask) >> 5, jmax - 1);
+  const uint32_t w0 = col_word(sc, j), w1 = col_word(sc, j + 1), w2 = col_word(sc, j + 2), w3 = col_word(sc, j + 3);
+  decode4_win(funnel64(w2, w1, w0, p), sc_off, jmax, p, e);
+  const uint32_t rel = ((p & kPosMask) >> 5) - j;  // rows the position moved (wraps if it went back)
+  const bool r1 = rel != 0;  // selects, not a branch
+  uint64_t W = funnel64(r1 ? w3 : w2, r1 ? w2 : w1, r1 ? w1 : w0, p);
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64(rel > 1) != 0, 0))
+    if (rel > 1) W = load_window(sc, p, jmax);
+  decode4_win(W, sc_off, jmax, p, e + 4);
+  pos2 = p;
 }
 
 // Packed bf16 pair (weights k, k+1 of a raw dword) from two table entries.
@@ -1757,8 +1774,9 @@ struct Plan {
 static bool is_fp16(const hl_tensor* t) { return t->format == HL_FORMAT_FP16; }
 
 // Rows of the stream columns: row 0 padding, the longest segment starting at
-// bit 31 of row 1, two rows of window overrun.
-static uint32_t col_rows_for(uint32_t max_seg_bits) { return 1 + ((31 + max_seg_bits + 31) >> 5) + 2; }
+// bit 31 of row 1, three rows of window overrun (the bf16 decode reads four
+// words at once).
+static uint32_t col_rows_for(uint32_t max_seg_bits) { return 1 + ((31 + max_seg_bits + 31) >> 5) + 3; }
 
 // raw_lds: the kernel stages the raw plane (64*S bytes per wave) in LDS.
 static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bool raw_lds, Plan* pl) {
