@@ -877,12 +877,13 @@ __device__ inline void mfma_finish(const GemvArgs& p, const f32x4_t& acc, float*
   const uint32_t n = i, ldy = a.rows;
   const bool nb_ok = n < p.B;
   if (p.KS == 1) {
-    // waves 0..3 each finish one of the four values of every lane
-    if (wave >= 4 || wave >= waves) return;
-    const uint32_t v = wave;
-    float t = red[v * 64 + lane];
-    for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
-    if (nb_ok && 4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
+    // waves 0..3 each finish one of the four values of every lane (a block
+    // of fewer waves: wave w finishes values w, w + waves, ...)
+    for (uint32_t v = wave; v < 4; v += waves) {
+      float t = red[v * 64 + lane];
+      for (uint32_t w = 1; w < waves; ++w) t += red[(w * 4 + v) * 64 + lane];
+      if (nb_ok && 4 * q + v < G) p.y[(uint64_t)n * ldy + r0 + 4 * q + v] = t;
+    }
     return;
   }
   if (wave != 0) return;
@@ -962,15 +963,18 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
 
   const uint32_t cb_end = min(a.CB, (kp + 1) * p.C);
   uint32_t cb = kp * p.C + wave;
-  // Prologue: the first two groups' metadata and the first group's raw bytes
-  // and activations are requested together; once the metadata is in, the
-  // table and the first group's stream are copied to LDS, the two copies'
-  // latencies overlapping. All loads are unconditional (a wave without a
+  // Prologue: the first two groups' metadata and the table copy; once the
+  // metadata is in, the first group's stream is copied to LDS and its raw
+  // bytes and activations are requested behind it. The decode starts when the
+  // table and the stream are in (the raw bytes of a step are waited for at
+  // that step's product). All loads are unconditional (a wave without a
   // group reads its block's last group and discards it), so that no merge of
   // paths makes the compiler wait early.
   const uint32_t cb0 = min(cb, a.CB - 1);
   Meta m = load_meta(a, rb * a.CB + cb0, lane);
   Meta mn = load_meta(a, rb * a.CB + (cb + waves < cb_end ? cb + waves : cb0), lane);
+  table_dma(a.lut);
+  uint32_t pos2 = issue_stream(a, cols, m, lane);
   uint2 rw[KP];
   uint4 xv[KP];
   {
@@ -982,19 +986,16 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
       xv[k] = *reinterpret_cast<const uint4*>(x + k * XSTEP);
     }
   }
-  // the first use of the metadata stays behind the loads above
-  asm volatile("" : "+v"(m.nbw), "+v"(m.u0)::"memory");
-  table_dma(a.lut);
-  uint32_t pos2 = issue_stream(a, cols, m, lane);
-  wait_vm0();  // table and first stream copies (and the prefetches before them)
+  // everything but the 2*KP raw and activation loads: the table and stream copies
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * KP));
+  asm volatile("" ::: "memory");
   __syncthreads();
 
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
   for (; cb < cb_end; cb += waves) {
-    // Group cb's stream copy is in flight; mn is the next group's metadata.
+    // Group cb's stream is in the wave's columns; mn is the next group's metadata.
     const Meta cur = m;
     const bool more = cb + waves < cb_end;
-    wait_vm0();
     wave_sync_lds();
     const uint32_t pos2l = (uint32_t)__shfl((int)pos2, (int)mu, 64);
     const uint8_t* rcur = a.raw + cur.first * S + mu * 8;
@@ -1035,6 +1036,7 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
       m = mn;
       mn = load_meta(a, rb * a.CB + (cb + 2 * waves < cb_end ? cb + 2 * waves : cb + waves), lane);
       pos2 = issue_stream(a, cols, m, lane);
+      wait_vm0();  // that copy (and the prefetches before it)
     }
   }
   wait_vm0();  // prefetches past the last group
@@ -1236,9 +1238,14 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   advance(t1, j1);
   const uint32_t g0 = group(0, 0);
   const uint32_t g1 = rb_of(t1) < RB ? group(t1, j1) : g0;
+  // The stream words are requested before the raw bytes and activations, and
+  // the decode starts once they and the table are in: the raw bytes of a step
+  // are waited for only at that step's product.
   Meta m0 = load_meta(a, g0, lane);
   Meta m1 = load_meta(a, g1, lane);
   table_dma(a.lut);
+  u32x4_a4 sw[JT / 4];
+  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw);
   uint2 rw[SP];
   uint4 xv[SP];
   {
@@ -1252,10 +1259,11 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
       xv[k] = *reinterpret_cast<const uint4*>(x + k * XSTEP);
     }
   }
-  u32x4_a4 sw[JT / 4];
-  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw);
   stream_store<JT>(cols, sw, lane);
-  wait_vm0();  // the table copy
+  // everything but the 2*SP raw and activation loads: the table copy (and
+  // the metadata and stream words before it)
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * SP));
+  asm volatile("" ::: "memory");
   __syncthreads();
 
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
@@ -1769,6 +1777,10 @@ struct Plan {
   GroupArgs ga;
   uint32_t waves;
   size_t lds;       // dynamic LDS: (float16 tables) + the wave regions
+  size_t tab_dyn;   // bytes of the float16 tables in it
+  size_t wave_bytes;  // bytes of one wave region
+  // dynamic LDS of a block of w waves
+  size_t lds_for(uint32_t w) const { return tab_dyn + (size_t)w * wave_bytes; }
 };
 
 static bool is_fp16(const hl_tensor* t) { return t->format == HL_FORMAT_FP16; }
@@ -1822,6 +1834,8 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bo
   if (tab_static + lds > kMaxLds) return HL_EUNSUPPORTED;
   pl->waves = waves;
   pl->lds = lds;
+  pl->tab_dyn = tab_dyn;
+  pl->wave_bytes = (size_t)per_wave * 4;
   return HL_OK;
 }
 
@@ -2030,13 +2044,23 @@ extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
 // Column blocks per block (C) and blocks per row block (KS) of the
 // non-persistent kernels: enough blocks to fill the device, each wave decoding
 // at least one group; split over column blocks only with room for partials.
+// *block_waves = the waves a block is launched with (no more than its column
+// blocks).
 static void choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, void* workspace_dev,
-                         size_t workspace_bytes, GemvArgs* p) {
+                         size_t workspace_bytes, GemvArgs* p, uint32_t* block_waves) {
   const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
-  const uint64_t target_waves = (uint64_t)device_cus() * 16;
+  const uint32_t cus = (uint32_t)device_cus();
+  const uint64_t target_waves = (uint64_t)cus * 16;
   const uint32_t gpw = (uint32_t)std::max<uint64_t>(1, ((uint64_t)RB * CB + target_waves - 1) / target_waves);
   uint32_t C = std::min<uint32_t>(CB, pl.waves * gpw);
   uint32_t KS = (CB + C - 1) / C;
+  // a matrix with fewer row blocks than CUs: split its columns further, so
+  // that every CU gets a block (narrower blocks, one group per wave)
+  if ((uint64_t)RB * KS < cus) {
+    KS = std::min<uint32_t>(CB, (cus + RB - 1) / RB);
+    C = (CB + KS - 1) / KS;
+    KS = (CB + C - 1) / C;
+  }
   if (KS > ks_cap(CB)) {
     KS = ks_cap(CB);
     C = (CB + KS - 1) / KS;
@@ -2048,6 +2072,7 @@ static void choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, voi
   }
   p->C = C;
   p->KS = KS;
+  *block_waves = std::min<uint32_t>(pl.waves, C);
   if (KS > 1) {
     p->counter = reinterpret_cast<uint32_t*>(workspace_dev);
     p->partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
@@ -2110,13 +2135,14 @@ static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, f
   p.x = x_dev;
   p.y = y_dev;
   p.B = batch;
-  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p);
+  uint32_t w = 0;
+  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p, &w);
   bool xt = false;
   st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, stream, &p, &xt);
   if (st != HL_OK) return st;
-  const dim3 grid(pl.ga.RB * p.KS), block(pl.waves * 64);
+  const dim3 grid(pl.ga.RB * p.KS), block(w * 64);
   // the reduction reuses the wave regions: 4 floats per lane per wave
-  const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.ga.t16_words * 4 + (size_t)pl.waves * 4 * 64 * 4);
+  const size_t lds = std::max<size_t>(pl.lds_for(w), (size_t)pl.ga.t16_words * 4 + (size_t)w * 4 * 64 * 4);
   return launch_mfma16(xt, t->seg_len / 8, grid, block, lds, stream, p);
 }
 
@@ -2171,15 +2197,16 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     }
   }
   // Column blocks per block and blocks per row block.
-  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p);
+  uint32_t w = 0;
+  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p, &w);
   const uint32_t KS = p.KS;
-  const dim3 grid(RB * KS), block(pl.waves * 64);
+  const dim3 grid(RB * KS), block(w * 64);
   if (mfma) {
     // the reduction reuses the wave regions: 4 floats per lane per wave
-    const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * 4 * 64 * 4);
+    const size_t lds = std::max<size_t>(pl.lds_for(w), (size_t)w * 4 * 64 * 4);
     return launch_mfma(xt, t->seg_len / 8, grid, block, lds, (hipStream_t)stream, p);
   }
-  const size_t lds = std::max<size_t>(pl.lds, (size_t)pl.waves * batch * 64 * 4);
+  const size_t lds = std::max<size_t>(pl.lds_for(w), (size_t)w * batch * 64 * 4);
   HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
 }
 
