@@ -388,15 +388,13 @@ __device__ __attribute__((always_inline)) inline void redo4(uint64_t W0, uint32_
   }
 }
 
-// Decodes 4 weights from the 64-bit window W0 at position p (four pairs of at
-// most 13 bits fit): table entries e[4] (bits 23..30 = exponent byte), p
-// advanced by the whole entries. Bits 0..22 of a position are the bit
-// position; the exponent bytes pile up above them and are never read.
-// A pair longer than the table window: a window with an escape among its four
-// reads (one wave-uniform test per window) is decoded again by the lanes that
-// had one, which resolve long pairs from the window's bits.
-__device__ inline void decode4_win(uint64_t W0, uint32_t sc_off, uint32_t jmax, uint32_t& p, uint32_t* e) {
-  uint64_t W = W0;
+// Four table reads from the 64-bit window W (four pairs of at most 13 bits
+// fit): table entries e[4] (bits 23..30 = exponent byte), p advanced by the
+// whole entries. Bits 0..22 of a position are the bit position; the exponent
+// bytes pile up above them and are never read. An escape entry (a pair longer
+// than the table window) has bit 31 set and advances nothing useful; the
+// caller tests for it.
+__device__ inline void lookup4(uint64_t W, uint32_t& p, uint32_t* e) {
   e[0] = lut_at((uint32_t)W);
   W = shift_window(W, e[0]);
   e[1] = lut_at((uint32_t)W);
@@ -404,14 +402,16 @@ __device__ inline void decode4_win(uint64_t W0, uint32_t sc_off, uint32_t jmax, 
   e[2] = lut_at((uint32_t)W);
   W = shift_window(W, e[2]);
   e[3] = lut_at((uint32_t)W);
-  const uint32_t any = e[0] | e[1] | e[2] | e[3];
-  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0)) {
-    if ((int)any < 0) {
-      redo4(W0, e);
-      if ((int)(e[0] | e[1] | e[2] | e[3]) < 0) careful4(sc_off, jmax, p & kPosMask, e);
-    }
-  }
   p = p + e[0] + e[1] + e[2] + e[3];
+}
+
+// The four weights of window W (at clean position p) again, resolving long
+// pairs (from the window's bits, else by the careful path); p advanced.
+__device__ __attribute__((always_inline)) inline void resolve4(uint64_t W, uint32_t sc_off, uint32_t jmax,
+                                                              uint32_t& p, uint32_t* e) {
+  redo4(W, e);
+  if ((int)(e[0] | e[1] | e[2] | e[3]) < 0) careful4(sc_off, jmax, p, e);
+  p = (p + e[0] + e[1] + e[2] + e[3]) & kPosMask;
 }
 
 // 64 bits of the three words (c, b, a) from bit p % 32 of a on.
@@ -424,17 +424,35 @@ __device__ inline uint64_t funnel64(uint32_t c, uint32_t b, uint32_t a, uint32_t
 // four pairs ended, within the same four words when that is at most one word
 // further (a rare longer advance reads its window from the column). jmax - 1
 // bounds the first of the four rows (columns hold three rows of overrun).
+// One wave-uniform test of the OR of the eight entries finds any escape; a
+// lane that had one decodes the window with the escape again from its
+// registers (and, after an escape in the first, the second window from the
+// corrected position).
 __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jmax, uint32_t& pos2, uint32_t* e) {
   uint32_t p = pos2;
   const uint32_t j = min((p & kPosMask) >> 5, jmax - 1);
   const uint32_t w0 = col_word(sc, j), w1 = col_word(sc, j + 1), w2 = col_word(sc, j + 2), w3 = col_word(sc, j + 3);
-  decode4_win(funnel64(w2, w1, w0, p), sc_off, jmax, p, e);
+  lookup4(funnel64(w2, w1, w0, p), p, e);
+  const uint32_t pm = p;  // after the first four
   const uint32_t rel = ((p & kPosMask) >> 5) - j;  // rows the position moved (wraps if it went back)
   const bool r1 = rel != 0;  // selects, not a branch
   uint64_t W = funnel64(r1 ? w3 : w2, r1 ? w2 : w1, r1 ? w1 : w0, p);
   if (__builtin_expect(__builtin_amdgcn_ballot_w64(rel > 1) != 0, 0))
     if (rel > 1) W = load_window(sc, p, jmax);
-  decode4_win(W, sc_off, jmax, p, e + 4);
+  lookup4(W, p, e + 4);
+  const uint32_t any = e[0] | e[1] | e[2] | e[3] | e[4] | e[5] | e[6] | e[7];
+  if (__builtin_expect(__builtin_amdgcn_ballot_w64((int)any < 0) != 0, 0)) {
+    if ((int)any < 0) {
+      if ((int)(e[0] | e[1] | e[2] | e[3]) < 0) {
+        p = pos2 & kPosMask;
+        resolve4(funnel64(w2, w1, w0, p), sc_off, jmax, p, e);
+        W = load_window(sc, p, jmax);
+      } else {
+        p = pm & kPosMask;
+      }
+      resolve4(W, sc_off, jmax, p, e + 4);
+    }
+  }
   pos2 = p;
 }
 
