@@ -27,7 +27,9 @@ still has the hash recorded there.
 
 `--traffic-run` instead runs the launches that the counter passes measure:
 100 fused launches on the same workload and 10 plain 256 MiB device copies
-(the calibration of the byte counters).
+(the calibration of the byte counters). `--counter-run MATRIX` runs only 30
+fused launches (batch 1, cold replicas) on one matrix of the workloads, for
+instruction and LDS counter passes.
 """
 from __future__ import annotations
 
@@ -54,6 +56,9 @@ TRAFFIC_FILES = {"split": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_traf
                  "fp16": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_fp16_traffic.txt")}
 COPY_BYTES = 256 << 20
 # container format -> (encoder keywords, activation dtype of gen_x, weights of the oracle)
+# matrices of the workloads for --counter-run: name -> (workload number, matrix index)
+COUNTER_MATRICES = {"4096x4096": (2, 0), "1024x4096": (4, 1), "14336x4096": (4, 4), "4096x14336": (4, 6),
+                    "28672x8192": (5, 4)}
 FORMATS = {"split": ({}, "bf16", "bf16"),
            "whole": ({"whole_exponent": True}, "bf16", "bf16"),
            "fp16": ({"fp16": True}, "f16", "fp16")}
@@ -70,6 +75,8 @@ def parse():
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the launches the byte-counter passes measure")
+    ap.add_argument("--counter-run", metavar="MATRIX", choices=sorted(COUNTER_MATRICES),
+                    help="run only 30 fused launches on that workload matrix (instruction and LDS counter passes)")
     ap.add_argument("--no-graph", action="store_true", help="time individual launches instead of graph replays")
     ap.add_argument("--format", choices=list(FORMATS), default="split",
                     help="container of the headline: split exponent (two 4-bit codes), whole exponent, or "
@@ -267,6 +274,22 @@ def main():
     from gen import bf16_bits_to_f16_bits, config_matrices, gen_matrix
 
     hl.lib()
+    if args.counter_run:
+        cfg, idx = COUNTER_MATRICES[args.counter_run]
+        cspec = config_matrices(cfg)[idx]
+        Wc = gen_matrix(cspec)
+        if args.format == "fp16":
+            Wc = bf16_bits_to_f16_bits(Wc)
+        cblob = hl.encode(Wc, **FORMATS[args.format][0])
+        tensors = [hl.DeviceTensor(cblob) for _ in range(max(2, math.ceil(COLD_BYTES / cblob.size)))]
+        _, xd = device_x(torch, cspec, 1, args.format)
+        y = torch.empty((1, cspec.rows), dtype=torch.float32, device="cuda")
+        for i in range(30):
+            tensors[i % len(tensors)].gemv(xd, y)
+        torch.cuda.synchronize()
+        print(json.dumps({"counter_run": args.counter_run, "format": args.format, "launches": 30,
+                          "compressed_bytes": int(cblob.size), "kernel_sha256_16": kernel_hash()}), flush=True)
+        return
     spec = config_matrices(2)[0]
     R, K = spec.rows, spec.cols
     n = R * K
