@@ -7,9 +7,14 @@ give short, typical and long codes, so that the kernel's instantiations for
 different stream lengths all run:
 * constant exponents (both fields single-symbol: no stream bits at all);
 * N(0, 0.02) with outliers (the workloads' distribution);
-* log-uniform magnitudes over 2^-60 .. 2^60 (long codes).
-Outputs: every row against a float64 product of the exact bf16 values, and
-sampled rows against the oracle's exactly rounded sums, at batch 1, 5 and 16.
+* log-uniform magnitudes over 2^-60 .. 2^60 (long streams: about 7 code bits
+  per weight, so two pairs often exceed a 14-bit window);
+* a geometric low exponent nibble (codes up to the length limit: pairs past
+  the 13-bit window).
+Each in the split format (code limit 12 and 15) and the whole-exponent
+format. Outputs: every row against a float64 product of the exact bf16
+values, and sampled rows against the oracle's exactly rounded sums, at batch
+1, 5 and 16.
 """
 import numpy as np
 import pytest
@@ -39,17 +44,32 @@ def _weights(kind, rows, cols, seed):
         return f32_to_bf16_bits(v.astype(np.float32))
     if kind == "gaussian":
         return random_bf16((rows, cols), seed=seed)
+    if kind == "geometric":
+        # geometric low exponent nibble, a few high nibbles: codes up to the
+        # length limit, pairs longer than the 13-bit window
+        n = rows * cols
+        el = np.minimum(rng.geometric(0.45, n) - 1, 15)
+        eh = rng.choice([3, 6, 7, 8], n, p=[0.02, 0.08, 0.8, 0.1])
+        bits = (rng.integers(0, 2, n) << 15) | (eh << 11) | (el << 7) | rng.integers(0, 128, n)
+        return bits.astype(np.uint16).reshape(rows, cols)
     mag = np.exp2(rng.uniform(-60, 60, (rows, cols))).astype(np.float32)
     return f32_to_bf16_bits(mag * np.where(rng.random((rows, cols)) < 0.5, -1, 1).astype(np.float32))
 
 
-@pytest.mark.parametrize("S,cols", [(64, 8192), (32, 4096)])
-@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform"])
-def test_persistent_kernel(torch, S, cols, kind):
+# container formats: (encoder keywords); the longer split limit puts el codes
+# past the 13-bit joint window, whole exponents put two codes past the
+# 14-bit two-pair window often (both decoded by the kernel's slot fix-up)
+FORMATS = {"split": {}, "split_lmax15": {"lmax": 15}, "whole": {"whole_exponent": True}}
+
+
+@pytest.mark.parametrize("S,cols,fmt", [(64, 8192, "split"), (32, 4096, "split"), (64, 8192, "split_lmax15"),
+                                        (64, 8192, "whole"), (32, 4096, "whole")])
+@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform", "geometric"])
+def test_persistent_kernel(torch, S, cols, fmt, kind):
     rows = 4100
-    print(f"persistent S={S} {rows}x{cols} {kind}", flush=True)
+    print(f"persistent S={S} {rows}x{cols} {fmt} {kind}", flush=True)
     W = _weights(kind, rows, cols, seed=S + cols)
-    dt = hl.DeviceTensor(hl.encode(W, seg_len=S))
+    dt = hl.DeviceTensor(hl.encode(W, seg_len=S, **FORMATS[fmt]))
     assert dt.view.grp_rows == 16
     Wf = bf16_to_f64(W)
     rng = np.random.default_rng(S)
