@@ -13,14 +13,14 @@
 //
 // Work mapping (container tiling in include/hufflm.h): one wavefront decodes
 // one group = G rows x GC column segments (G*GC <= 64), lane mu owning the
-// segment of row r0 + mu % G and column segment c0 + mu / G.
-// Per group a wave copies, straight from HBM into its LDS region:
-//   * each lane's part of the group stream into a column of words (word j of
-//     lane lam at row j, column lam), so that window reads never share an
-//     LDS bank between lanes;
-//   * the raw sign/mantissa plane ([t/8][lane] in 8-byte units);
-//   * the activation slice x[b][c0*S .. (c0+GC)*S), which lanes of the same
-//     column segment read alike.
+// segment of row r0 + mu % G and column segment c0 + mu / G. Each lane's part
+// of the group stream goes into a column of the wave's LDS region (word j of
+// lane lam at row j, column lam), so that window reads never share an LDS
+// bank between lanes. The vector and decode kernels also stage the raw
+// sign/mantissa plane ([t/8][lane] in 8-byte units) and the activation slice
+// in LDS; the matrix-core kernels keep raw bytes and activations in
+// registers, prefetched steps ahead, and the persistent kernel loads the next
+// group's stream words into registers while it decodes the current group.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -569,20 +569,6 @@ __device__ inline uint32_t issue_stream(const GroupArgs& a, uint32_t* cols, Meta
   const uint32_t last = m.units * 4 - 1;
   // 32-bit byte offsets, so that the copy addresses as scalar base + lane offset
   for (uint32_t j = 0; j < J; ++j) dma4(src + (uint32_t)(min(ws + j, last) * 4u), cols + (j + 1) * kCol);
-  return 30u + bit0;
-}
-
-// The same with exactly JT rows (a compile-time count of copies, so that the
-// compiler can count the loads behind them). Rows past a lane's words repeat
-// the group's last word; a group without stream bits reads its first raw word.
-template <int JT>
-__device__ inline uint32_t issue_stream_fixed(const GroupArgs& a, uint32_t* cols, Meta& m, uint32_t lane) {
-  uint32_t ws, bit0;
-  stream_start(a, m, lane, ws, bit0);
-  const uint8_t* src = m.units ? reinterpret_cast<const uint8_t*>(a.stream + m.u0) : a.raw + m.first * a.S;
-  const uint32_t last = m.units ? m.units * 4 - 1 : 0u;
-#pragma unroll
-  for (int j = 0; j < JT; ++j) dma4(src + (uint32_t)(min(ws + j, last) * 4u), cols + (j + 1) * kCol);
   return 30u + bit0;
 }
 
