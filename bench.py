@@ -271,12 +271,12 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     import paper_2502_00922_amd as hl
-    from gen import bf16_bits_to_f16_bits, config_matrices, gen_matrix
+    from gen import bf16_bits_to_f16_bits, workload_matrices, gen_matrix
 
     hl.lib()
     if args.counter_run:
         cfg, idx = COUNTER_MATRICES[args.counter_run]
-        cspec = config_matrices(cfg)[idx]
+        cspec = workload_matrices(cfg)[idx]
         Wc = gen_matrix(cspec)
         if args.format == "fp16":
             Wc = bf16_bits_to_f16_bits(Wc)
@@ -290,7 +290,7 @@ def main():
         print(json.dumps({"counter_run": args.counter_run, "format": args.format, "launches": 30,
                           "compressed_bytes": int(cblob.size), "kernel_sha256_16": kernel_hash()}), flush=True)
         return
-    spec = config_matrices(2)[0]
+    spec = workload_matrices(2)[0]
     R, K = spec.rows, spec.cols
     n = R * K
     W = gen_matrix(spec)

@@ -63,7 +63,7 @@ def _llama70b_layer():
 # Workloads: 1 = one 1024x1024 matrix, 2 = one 4096x4096 projection with
 # per-row scales, 3 = a 7B-shaped MLP triple, 4 = one 8B-shaped decoder layer
 # with per-matrix scale, 5 = an 80-layer 70B-shaped stack.
-CONFIGS = {
+WORKLOADS = {
     1: dict(batches=(1,), x_dtype="f32", layers=1),
     2: dict(batches=(1, 4), x_dtype="bf16", layers=1),
     3: dict(batches=(1, 4, 16), x_dtype="bf16", layers=1),
@@ -72,7 +72,7 @@ CONFIGS = {
 }
 
 
-def config_matrices(cfg: int, layer: int = 0) -> List[MatrixSpec]:
+def workload_matrices(cfg: int, layer: int = 0) -> List[MatrixSpec]:
     if cfg == 1:
         return [MatrixSpec(1, 0, 0, "w", 1024, 1024)]
     if cfg == 2:

@@ -1,7 +1,7 @@
 """The seeded generator: row blocks equal the full draw; distributions as stated."""
 import numpy as np
 
-from gen import MatrixSpec, config_matrices, gen_matrix, gen_x, bf16_bits_to_f32
+from gen import MatrixSpec, workload_matrices, gen_matrix, gen_x, bf16_bits_to_f32
 
 
 def test_row_block_equals_full_draw():
@@ -13,14 +13,14 @@ def test_row_block_equals_full_draw():
 
 
 def test_config_shapes():
-    assert [(m.rows, m.cols) for m in config_matrices(4)] == [
+    assert [(m.rows, m.cols) for m in workload_matrices(4)] == [
         (4096, 4096), (1024, 4096), (1024, 4096), (4096, 4096),
         (14336, 4096), (14336, 4096), (4096, 14336)]
-    assert sum(m.rows * m.cols for m in config_matrices(5)) * 80 == 68451041280
+    assert sum(m.rows * m.cols for m in workload_matrices(5)) * 80 == 68451041280
 
 
 def test_distribution_workload1():
-    spec = config_matrices(1)[0]
+    spec = workload_matrices(1)[0]
     w = bf16_bits_to_f32(gen_matrix(spec)).astype(np.float64)
     assert abs(w.std() - 0.02 * np.sqrt(1 + 0.001 * 399)) < 2e-3
     big = np.abs(w) > 0.2

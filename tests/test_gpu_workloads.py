@@ -17,7 +17,7 @@ The 70B-shaped stack is checked on its first and last layers.
 import numpy as np
 import pytest
 
-from gen import CONFIGS, bf16_bits_to_f16_bits, config_matrices, gen_matrix, gen_x
+from gen import WORKLOADS, bf16_bits_to_f16_bits, workload_matrices, gen_matrix, gen_x
 from oracle import codec
 from oracle import gemv as ogemv
 
@@ -81,10 +81,10 @@ def _check_matrix(torch, spec, batches, x_dtype, size_check, fmt="split"):
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4])
 def test_workload_full_size(torch, cfg):
-    specs = config_matrices(cfg)
+    specs = workload_matrices(cfg)
     smallest = min(specs, key=lambda s: s.rows * s.cols)
     for spec in specs:
-        _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest)
+        _check_matrix(torch, spec, WORKLOADS[cfg]["batches"], WORKLOADS[cfg]["x_dtype"], spec is smallest)
 
 
 @pytest.mark.parametrize("fmt", ["whole", "fp16"])
@@ -92,16 +92,16 @@ def test_workload_full_size(torch, cfg):
 def test_workload_full_size_other_formats(torch, cfg, fmt):
     """The whole-exponent format, and the float16 format on the float16 copies
     of the weights, on the 4096x4096 and the 8B-shaped layer workloads."""
-    specs = config_matrices(cfg)
+    specs = workload_matrices(cfg)
     smallest = min(specs, key=lambda s: s.rows * s.cols)
     for spec in specs:
-        _check_matrix(torch, spec, CONFIGS[cfg]["batches"], CONFIGS[cfg]["x_dtype"], spec is smallest, fmt=fmt)
+        _check_matrix(torch, spec, WORKLOADS[cfg]["batches"], WORKLOADS[cfg]["x_dtype"], spec is smallest, fmt=fmt)
 
 
 @pytest.mark.slow
 @pytest.mark.parametrize("layer", [0, 79])
 def test_workload_70b_layer(torch, layer):
-    specs = config_matrices(5, layer)
+    specs = workload_matrices(5, layer)
     smallest = min(specs, key=lambda s: s.rows * s.cols)
     for spec in specs:
-        _check_matrix(torch, spec, CONFIGS[5]["batches"], CONFIGS[5]["x_dtype"], spec is smallest)
+        _check_matrix(torch, spec, WORKLOADS[5]["batches"], WORKLOADS[5]["x_dtype"], spec is smallest)

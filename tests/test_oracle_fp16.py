@@ -16,7 +16,7 @@ import os
 import numpy as np
 import pytest
 
-from gen import bf16_bits_to_f16_bits, config_matrices, gen_matrix, random_fp16
+from gen import bf16_bits_to_f16_bits, workload_matrices, gen_matrix, random_fp16
 from oracle import codec
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -128,7 +128,7 @@ def test_all_patterns_roundtrip():
 def test_entropies_against_the_split_table():
     """float16 copies of bf16-trained weights: per-field entropies near the
     paper's {1,5,5,5} row (1.00, 2.60, 4.97, 2.04 bits)."""
-    w = bf16_bits_to_f16_bits(gen_matrix(config_matrices(2)[0]))
+    w = bf16_bits_to_f16_bits(gen_matrix(workload_matrices(2)[0]))
     s, e, mh, ml = codec.split_fields16(w)
     H = [codec.entropy_bits(codec.histogram(f, n)) for f, n in ((s, 2), (e, 32), (mh, 32), (ml, 32))]
     for got, paper in zip(H, (1.00, 2.60, 4.97, 2.04)):

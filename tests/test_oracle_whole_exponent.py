@@ -22,7 +22,7 @@ import random
 import numpy as np
 import pytest
 
-from gen import config_matrices, gen_matrix, random_bf16
+from gen import workload_matrices, gen_matrix, random_bf16
 from oracle import codec
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
@@ -183,7 +183,7 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR, lmax):
 
 
 def test_chain_rule_and_workload_ratio():
-    spec = config_matrices(1)[0]
+    spec = workload_matrices(1)[0]
     w = gen_matrix(spec)
     _, eh, el, _ = codec.split_fields(w)
     e = codec.exponent_byte(w)
