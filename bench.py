@@ -29,7 +29,9 @@ still has the hash recorded there.
 100 fused launches on the same workload and 10 plain 256 MiB device copies
 (the calibration of the byte counters). `--counter-run MATRIX` runs only 30
 fused launches (batch 1, cold replicas) on one matrix of the workloads, for
-instruction and LDS counter passes.
+instruction and LDS counter passes. `--workloads` prints one JSON line per
+workload and batch size instead: every matrix of the workload decoded and
+multiplied back to back as one step (see measure_workloads).
 """
 from __future__ import annotations
 
@@ -75,6 +77,8 @@ def parse():
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the launches the byte-counter passes measure")
+    ap.add_argument("--workloads", action="store_true",
+                    help="time every workload (all its matrices back to back per step) instead of the headline")
     ap.add_argument("--counter-run", metavar="MATRIX", choices=sorted(COUNTER_MATRICES),
                     help="run only 30 fused launches on that workload matrix (instruction and LDS counter passes)")
     ap.add_argument("--no-graph", action="store_true", help="time individual launches instead of graph replays")
@@ -225,6 +229,95 @@ def measure_container(torch, hl, blob, spec, W, batches, args, single_launches, 
     return results, seg_len
 
 
+WORKLOAD_NAMES = {1: "1024x1024 bf16 matrix, fp32 x", 2: "4096x4096 projection with per-row scales",
+                  3: "7B-shaped MLP triple (gate, up 11008x4096; down 4096x11008)",
+                  4: "8B-shaped decoder layer (q, k, v, o, gate, up, down), per-matrix scale",
+                  5: "70B-shaped stack, 80 layers of q, k, v, o, gate, up, down (80 resident copies of one layer)"}
+
+
+def measure_workloads(torch, hl, steps_small=50):
+    """One JSON line per workload and batch. A step multiplies every matrix of
+    the workload once, back to back on one stream, in one HIP graph: for the
+    70B stack that is 80 layers x 7 matrices = 560 launches, over 80 resident
+    copies of one generated layer (about 100 GB of containers, so every layer
+    comes from HBM). Smaller workloads rotate over copies of the whole set
+    that together exceed the last-level cache. The comparator is the
+    uncompressed bf16 GEMV (the faster of hl_gemv_bf16 and torch's linear, per
+    step) over cold copies of the bf16 matrices (for the 70B stack 20 copies
+    of the layer, cycled)."""
+    from gen import WORKLOADS, workload_matrices, gen_matrix, gen_x
+    for w in sorted(WORKLOADS):
+        cfg = WORKLOADS[w]
+        specs = workload_matrices(w)
+        layers = cfg["layers"]
+        t0 = time.perf_counter()
+        mats = [gen_matrix(s) for s in specs]
+        blobs = [hl.encode(m) for m in mats]
+        comp = sum(int(b.size) for b in blobs)
+        n = sum(int(m.size) for m in mats)
+        base = [hl.DeviceTensor(b) for b in blobs]
+        copies = max(layers, math.ceil(COLD_BYTES / comp))
+        sets = [base] + [[t.copy() for t in base] for _ in range(copies - 1)]
+        # one workspace per matrix position, shared by its copies (launches run one after another)
+        for j, t in enumerate(base):
+            ws = t.workspace()
+            for st in sets[1:]:
+                st[j]._ws = ws
+        wb = [torch.from_numpy(m.view(np.int16)).view(torch.bfloat16).cuda() for m in mats]
+        copies_b = max(min(layers, 20), math.ceil(COLD_BYTES / (2 * n)))
+        sets_b = [wb] + [[t.clone() for t in wb] for _ in range(copies_b - 1)]
+        torch.cuda.synchronize()
+        setup_s = time.perf_counter() - t0
+        steps = 3 if layers > 1 else steps_small
+        for B in cfg["batches"]:
+            xs = {}
+            for s in specs:
+                if s.cols not in xs:
+                    xb = gen_x(s, B, cfg["x_dtype"])
+                    xs[s.cols] = (torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+                                  if xb.dtype == np.uint16 else torch.from_numpy(xb).cuda())
+            ys = [torch.empty((B, s.rows), dtype=torch.float32, device="cuda") for s in specs]
+
+            def fused(i):
+                for l in range(layers):
+                    for t, s, y in zip(sets[(i * layers + l) % copies], specs, ys):
+                        t.gemv(xs[s.cols], y)
+
+            def lib_bf16(i):
+                for l in range(layers):
+                    for wt, s, y in zip(sets_b[(i * layers + l) % copies_b], specs, ys):
+                        hl.gemv_bf16(wt, xs[s.cols], y)
+
+            def torch_bf16(i):
+                for l in range(layers):
+                    for wt, s in zip(sets_b[(i * layers + l) % copies_b], specs):
+                        torch.nn.functional.linear(xs[s.cols], wt)
+
+            nrep = max(1, copies // layers)
+            ms = time_graph(torch, fused, nrep, steps, 1)
+            nrep_b = max(1, copies_b // layers)
+            ms_b = time_graph(torch, lib_bf16, nrep_b, steps, 1)
+            if cfg["x_dtype"] == "bf16":
+                ms_b = min(ms_b, time_graph(torch, torch_bf16, nrep_b, steps, 1))
+            cr = 2 * n / comp
+            line = dict(workload=w, name=WORKLOAD_NAMES[w], matrices=len(specs) * layers, batch=B,
+                        weights=n * layers, compressed_bytes=comp * layers, compression_ratio=round(cr, 4),
+                        bits_per_weight=round(8 * comp / n, 4), ms_per_step=round(ms, 5),
+                        compressed_GBps=round(comp * layers / (ms * 1e-3) / 1e9, 1),
+                        hbm_frac=round(comp * layers / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                        effective_GBps=round(2 * n * layers / (ms * 1e-3) / 1e9, 1),
+                        bf16_ms_per_step=round(ms_b, 5), speedup_vs_bf16=round(ms_b / ms, 3),
+                        speedup_target=round(0.9 * cr, 3), cold_copies=copies, setup_s=round(setup_s, 1))
+            if w == 1:
+                dec = torch.empty(mats[0].shape, dtype=torch.int16, device="cuda")
+                line["decode_ms"] = round(time_graph(torch, lambda i: sets[i % copies][0].decode(dec), copies,
+                                                     steps, 1), 5)
+            print(json.dumps(line), flush=True)
+        del sets, sets_b, base, wb
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
 def measure_prefill(torch, hl, blob, spec, W, args, token_counts=(32, 128, 512)):
     """Graph-timed prefill products Y = X W^T for several token counts over cold
     replicas of the container, with torch's bf16 GEMM on cold replicas of the
@@ -274,6 +367,9 @@ def main():
     from gen import bf16_bits_to_f16_bits, workload_matrices, gen_matrix
 
     hl.lib()
+    if args.workloads:
+        measure_workloads(torch, hl)
+        return
     if args.counter_run:
         cfg, idx = COUNTER_MATRICES[args.counter_run]
         cspec = workload_matrices(cfg)[idx]

@@ -233,6 +233,17 @@ class DeviceTensor:
                "hl_tensor_view")
         _check(lib().hl_tensor_prepare(ctypes.byref(self.view), _stream_ptr(stream)), "hl_tensor_prepare")
 
+    def copy(self):
+        """Another resident copy of the same container and table (device to
+        device; the host-side validation of the container is not repeated)."""
+        t = DeviceTensor.__new__(DeviceTensor)
+        t.blob = self.blob.clone()
+        t.lut = self.lut.clone()
+        t.view = TensorView.from_buffer_copy(self.view)
+        t.view.blob_dev = t.blob.data_ptr()
+        t.view.lut_dev = t.lut.data_ptr()
+        return t
+
     @property
     def shape(self):
         return int(self.view.rows), int(self.view.cols)
