@@ -152,3 +152,19 @@ def test_errors_are_reported(torch):
         dt.gemv(torch.zeros((17, 128), dtype=torch.bfloat16, device="cuda"))
     with pytest.raises(ValueError):
         dt.gemv(torch.zeros((1, 64), dtype=torch.bfloat16, device="cuda"))
+
+
+def test_device_copy(torch):
+    # a device-to-device copy of a container and its table decodes and
+    # multiplies exactly like the original, also after the original is gone
+    print("device copy", flush=True)
+    w = random_bf16((300, 2048), seed=21)
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=64))
+    x = _to_dev_x(torch, random_x(3, 2048, seed=4, dtype="bf16"))
+    y0 = dt.gemv(x).cpu().numpy()
+    cp = dt.copy()
+    assert cp.blob.data_ptr() != dt.blob.data_ptr() and cp.lut.data_ptr() != dt.lut.data_ptr()
+    del dt
+    torch.cuda.synchronize()
+    assert np.array_equal(cp.gemv(x).cpu().numpy(), y0)
+    assert np.array_equal(_decode(torch, cp), w)
