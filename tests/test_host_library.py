@@ -29,6 +29,15 @@ def test_exports_match_header(L):
     assert set(hl.EXPORTS) == names
 
 
+def test_binding_constants_match_header():
+    # the binding allocates tables and checks batches with the header's sizes
+    text = open(os.path.join(ROOT, "include", "hufflm.h")).read()
+    defs = {k: int(v) for k, v in re.findall(r"#define (HL_[A-Z0-9_]+) (\d+)u?", text)}
+    assert hl.LUT_BYTES == defs["HL_LUT_BYTES"]
+    assert hl.MAX_BATCH == defs["HL_MAX_BATCH"]
+    assert hl.HEADER_BYTES == defs["HL_HEADER_BYTES"]
+
+
 def _codebook_lists(cb):
     return (cb.eh.nsym, cb.eh.single, list(cb.eh.len), cb.el.nsym, cb.el.single, list(cb.el.len))
 
