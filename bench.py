@@ -244,7 +244,8 @@ def measure_workloads(torch, hl, steps_small=50):
     that together exceed the last-level cache. The comparator is the
     uncompressed bf16 GEMV (the faster of hl_gemv_bf16 and torch's linear, per
     step) over cold copies of the bf16 matrices (for the 70B stack 20 copies
-    of the layer, cycled)."""
+    of the layer, cycled). Workloads with matrices that share x also time the
+    step with each such set (q, k, v; gate, up) in one grouped launch."""
     from gen import WORKLOADS, workload_matrices, gen_matrix, gen_x
     for w in sorted(WORKLOADS):
         cfg = WORKLOADS[w]
@@ -293,8 +294,24 @@ def measure_workloads(torch, hl, steps_small=50):
                     for wt, s in zip(sets_b[(i * layers + l) % copies_b], specs):
                         torch.nn.functional.linear(xs[s.cols], wt)
 
+            # grouped: the matrices that share x (q, k, v; gate, up) in one launch each
+            names = [s.name for s in specs]
+            parts = [[j for j, nm in enumerate(names) if nm in ("q", "k", "v")],
+                     [j for j, nm in enumerate(names) if nm in ("gate", "up")]]
+            parts = [g for g in parts if len(g) > 1]
+            singles = [j for j in range(len(specs)) if not any(j in g for g in parts)]
+
+            def grouped(i):
+                for l in range(layers):
+                    st = sets[(i * layers + l) % copies]
+                    for g in parts:
+                        hl.gemv_multi([st[j] for j in g], xs[specs[g[0]].cols], [ys[j] for j in g])
+                    for j in singles:
+                        st[j].gemv(xs[specs[j].cols], ys[j])
+
             nrep = max(1, copies // layers)
             ms = time_graph(torch, fused, nrep, steps, 1)
+            ms_g = time_graph(torch, grouped, nrep, steps, 1) if parts and cfg["x_dtype"] == "bf16" else None
             nrep_b = max(1, copies_b // layers)
             ms_b = time_graph(torch, lib_bf16, nrep_b, steps, 1)
             if cfg["x_dtype"] == "bf16":
@@ -308,6 +325,10 @@ def measure_workloads(torch, hl, steps_small=50):
                         effective_GBps=round(2 * n * layers / (ms * 1e-3) / 1e9, 1),
                         bf16_ms_per_step=round(ms_b, 5), speedup_vs_bf16=round(ms_b / ms, 3),
                         speedup_target=round(0.9 * cr, 3), cold_copies=copies, setup_s=round(setup_s, 1))
+            if ms_g is not None:
+                line.update(grouped=[[names[j] for j in g] for g in parts], grouped_ms_per_step=round(ms_g, 5),
+                            grouped_compressed_GBps=round(comp * layers / (ms_g * 1e-3) / 1e9, 1),
+                            grouped_speedup_vs_bf16=round(ms_b / ms_g, 3))
             if w == 1:
                 dec = torch.empty(mats[0].shape, dtype=torch.int16, device="cuda")
                 line["decode_ms"] = round(time_graph(torch, lambda i: sets[i % copies][0].decode(dec), copies,

@@ -282,6 +282,23 @@ hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype
                          uint32_t batch, float* y_dev, void* workspace_dev,
                          size_t workspace_bytes, void* stream);
 
+/* The products of up to 4 matrices that share x, y_devs[m][b][r] =
+ * sum_k W_m[r][k] * x[b][k] (a decode step's q, k and v projections, or its
+ * gate and up projections), as hl_decode_gemv computes each. ts[m]: views
+ * with the same number of columns. When every matrix is in a bf16 format with
+ * 16-row groups and the same segment length of 32 or 64, x is bf16 and the
+ * matrices have at least one row block per CU together, one launch decodes
+ * them all: its blocks are divided among the matrices in proportion to their
+ * row blocks, so the launch and first-load latency of small matrices is paid
+ * once. Otherwise the matrices are multiplied one after another with
+ * hl_decode_gemv. workspace_dev: at least the largest
+ * hl_gemv_workspace_bytes(ts[m], batch), under hl_decode_gemv's rules.
+ * Errors: HL_EINVAL (also for matrices with different column counts), and
+ * those of hl_decode_gemv. */
+hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const void* x_dev,
+                               hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
+                               void* workspace_dev, size_t workspace_bytes, void* stream);
+
 /* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows
  * (partial sums of up to one range per column block of four segments); 0 for
  * tensors it does not take. */

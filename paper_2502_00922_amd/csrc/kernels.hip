@@ -1199,12 +1199,33 @@ __global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* partial, 
 // wait the compiler places is exact. At a row block's end the waves add their
 // accumulators through their columns in a fixed order (before the next
 // group's words go in) and four waves write y.
+// Arguments of the persistent kernel: up to kMaxParts matrices with the same
+// columns and container geometry that share x (a grouped launch); blocks
+// [part0[m], part0[m + 1]) work on matrix m and write y[m].
+constexpr uint32_t kMaxParts = 4;
+struct StreamArgs {
+  GemvArgs p;  // x, batch (p.g and p.y unused)
+  GroupArgs g[kMaxParts];
+  float* y[kMaxParts];
+  uint32_t part0[kMaxParts + 1];
+  uint32_t n;
+};
+
 template <int SP, int JT, bool XT>
-__global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
+__global__ void __launch_bounds__(1024) gemv_stream_kernel(StreamArgs sa) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
-  const GroupArgs& a = p.g;
+  const GemvArgs& p = sa.p;
+  // this block's matrix (wave-uniform selects, no indexing into the arguments)
+  uint32_t m = 0;
+  for (uint32_t k = 1; k < sa.n; ++k) m += blockIdx.x >= sa.part0[k] ? 1u : 0u;
+  GroupArgs a = sa.g[0];
+  float* yp = sa.y[0];
+  if (m == 1) a = sa.g[1], yp = sa.y[1];
+  if (m == 2) a = sa.g[2], yp = sa.y[2];
+  if (m == 3) a = sa.g[3], yp = sa.y[3];
+  const uint32_t bid = blockIdx.x - sa.part0[m], nblk = sa.part0[m + 1] - sa.part0[m];
   const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
   uint32_t* cols = s_dyn + wave * kBuf;
@@ -1221,10 +1242,10 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
   const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
   const uint32_t last_group = RB * CB - 1;
 
-  // the wave's groups in order: round t (row block blockIdx.x + t*grid), step
-  // j; branch-free (a branch between a load and its use makes the compiler's
-  // wait for it conservative)
-  auto rb_of = [&](uint32_t t) { return blockIdx.x + t * gridDim.x; };
+  // the wave's groups in order: round t (row block bid + t*nblk of the
+  // block's matrix), step j; branch-free (a branch between a load and its use
+  // makes the compiler's wait for it conservative)
+  auto rb_of = [&](uint32_t t) { return bid + t * nblk; };
   auto advance = [&](uint32_t& t, uint32_t& j) {
     const bool same = wave + (j + 1) * waves < CB;
     t = same ? t : t + 1;
@@ -1339,7 +1360,7 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(GemvArgs p) {
       const uint32_t v = wave;
       float sum = 0.f;
       for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + w * kBuf)[v * 64 + lane];
-      if (i < p.B && 4 * q + v < G) p.y[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
+      if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
     }
     block_sync_lds();
     stream_store<JT>(cols, sw, lane);  // the next group's words, held back for the sum
@@ -1875,7 +1896,7 @@ static int stream_rows_for(uint32_t seg_len, uint32_t col_rows) {
 
 template <bool XT>
 static hl_status launch_stream_x(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                                 const GemvArgs& p) {
+                                 const StreamArgs& p) {
   if (seg_len == 64) {
     switch (jt) {
       case 12: return launch(gemv_stream_kernel<8, 12, XT>, grid, block, lds, s, p);
@@ -1892,7 +1913,7 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, dim3 grid, dim3 block
 }
 
 static hl_status launch_stream(bool xt, uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                               const GemvArgs& p) {
+                               const StreamArgs& p) {
   return xt ? launch_stream_x<true>(seg_len, jt, grid, block, lds, s, p)
             : launch_stream_x<false>(seg_len, jt, grid, block, lds, s, p);
 }
@@ -2196,8 +2217,15 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
       p.C = CB;
       p.KS = 1;
-      return launch_stream(xt, t->seg_len, jt, dim3(std::min(RB, cus)), dim3(w * 64), w * per_wave,
-                           (hipStream_t)stream, p);
+      StreamArgs sa;
+      std::memset(&sa, 0, sizeof(sa));
+      sa.p = p;
+      sa.g[0] = pl.ga;
+      sa.y[0] = y_dev;
+      sa.n = 1;
+      sa.part0[1] = std::min(RB, cus);
+      return launch_stream(xt, t->seg_len, jt, dim3(sa.part0[1]), dim3(w * 64), w * per_wave, (hipStream_t)stream,
+                           sa);
     }
   }
   // Column blocks per block and blocks per row block.
@@ -2212,6 +2240,86 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   }
   const size_t lds = std::max<size_t>(pl.lds_for(w), (size_t)w * batch * 64 * 4);
   HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
+}
+
+extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const void* x_dev,
+                                          hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
+                                          void* workspace_dev, size_t workspace_bytes, void* stream) {
+  if (!ts || !y_devs || !x_dev || count < 1 || count > kMaxParts || batch < 1 || batch > HL_MAX_BATCH)
+    return HL_EINVAL;
+  for (uint32_t k = 0; k < count; ++k)
+    if (!ts[k] || !y_devs[k] || ts[k]->cols != ts[0]->cols) return HL_EINVAL;
+  // One launch of the persistent kernel when every matrix has its container
+  // geometry (bf16 formats, 16-row groups, the same S of 32 or 64) and bf16 x;
+  // otherwise the matrices one after another.
+  bool grouped = count > 1 && x_dtype == HL_BF16;
+  for (uint32_t k = 0; k < count && grouped; ++k)
+    grouped = !is_fp16(ts[k]) && ts[k]->grp_rows == 16 && ts[k]->seg_len == ts[0]->seg_len &&
+              (ts[k]->seg_len == 64 || ts[k]->seg_len == 32);
+  const uint32_t cus = (uint32_t)device_cus();
+  Plan pl[kMaxParts];
+  int jt = 0;
+  uint64_t groups = 0, rbs = 0;
+  for (uint32_t k = 0; k < count && grouped; ++k) {
+    if (make_plan(ts[k], 0, false, &pl[k]) != HL_OK) return HL_EINVAL;
+    const int j = stream_rows_for(ts[k]->seg_len, pl[k].ga.col_rows);
+    grouped = j != 0;
+    jt = std::max(jt, j);
+    groups += (uint64_t)pl[k].ga.RB * pl[k].ga.CB;
+    rbs += pl[k].ga.RB;
+  }
+  uint32_t w = kMaxWaves;
+  const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
+  const size_t per_wave = (size_t)(jt + 1) * kCol * 4;
+  if (grouped) {
+    while (w > 1 && tab + w * per_wave > kMaxLds) --w;
+    while (w > 8 && groups < 2ull * cus * w) --w;
+    grouped = w >= 8 && pl[0].ga.CB >= w && rbs >= cus;
+  }
+  if (!grouped) {
+    for (uint32_t k = 0; k < count; ++k) {
+      const hl_status st = hl_decode_gemv(ts[k], x_dev, x_dtype, batch, y_devs[k], workspace_dev, workspace_bytes,
+                                          stream);
+      if (st != HL_OK) return st;
+    }
+    return HL_OK;
+  }
+  // Blocks per matrix: one each, then one more at a time to the matrix with the
+  // most row blocks per block, until every CU has a block.
+  uint32_t nb[kMaxParts], used = count;
+  for (uint32_t k = 0; k < count; ++k) nb[k] = 1;
+  while (used < cus) {
+    uint32_t best = 0, worst = 0;
+    for (uint32_t k = 0; k < count; ++k) {
+      const uint32_t per = (pl[k].ga.RB + nb[k] - 1) / nb[k];
+      if (per > worst || (per == worst && pl[k].ga.RB > pl[best].ga.RB)) worst = per, best = k;
+    }
+    if (worst <= 1) break;
+    ++nb[best];
+    ++used;
+  }
+  GemvArgs p;
+  std::memset(&p, 0, sizeof(p));
+  p.x = x_dev;
+  p.B = batch;
+  p.C = pl[0].ga.CB;
+  p.KS = 1;
+  bool xt = false;
+  uint32_t big = 0;  // the tiled activations go where the largest matrix's workspace puts them
+  for (uint32_t k = 1; k < count; ++k) big = ts[k]->rows > ts[big]->rows ? k : big;
+  const hl_status st = tile_activations(ts[big], x_dev, batch, workspace_dev, workspace_bytes, (hipStream_t)stream,
+                                        &p, &xt);
+  if (st != HL_OK) return st;
+  StreamArgs sa;
+  std::memset(&sa, 0, sizeof(sa));
+  sa.p = p;
+  sa.n = count;
+  for (uint32_t k = 0; k < count; ++k) {
+    sa.g[k] = pl[k].ga;
+    sa.y[k] = y_devs[k];
+    sa.part0[k + 1] = sa.part0[k] + nb[k];
+  }
+  return launch_stream(xt, ts[0]->seg_len, jt, dim3(used), dim3(w * 64), w * per_wave, (hipStream_t)stream, sa);
 }
 
 // ------------------------------------------------------------------ prefill GEMM host side

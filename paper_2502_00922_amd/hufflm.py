@@ -80,7 +80,8 @@ _lib = None
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
            "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
-           "hl_decode_gemv", "hl_gemm_workspace_bytes", "hl_decode_gemm", "hl_gemv_bf16"]
+           "hl_decode_gemv", "hl_decode_gemv_multi", "hl_gemm_workspace_bytes", "hl_decode_gemm",
+           "hl_gemv_bf16"]
 
 
 def lib() -> ctypes.CDLL:
@@ -126,6 +127,9 @@ def lib() -> ctypes.CDLL:
     L.hl_decode_gemv.restype = c.c_int
     L.hl_decode_gemv.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                  c.c_void_p, c.c_size_t, c.c_void_p]
+    L.hl_decode_gemv_multi.restype = c.c_int
+    L.hl_decode_gemv_multi.argtypes = [c.c_void_p, c.c_uint32, c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
+                                       c.c_void_p, c.c_size_t, c.c_void_p]
     L.hl_gemm_workspace_bytes.restype = c.c_size_t
     L.hl_gemm_workspace_bytes.argtypes = [c.POINTER(TensorView), c.c_uint32]
     L.hl_decode_gemm.restype = c.c_int
@@ -316,6 +320,37 @@ class DeviceTensor:
                                     ctypes.c_void_p(y.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
                                     _stream_ptr(stream)), "hl_decode_gemm")
         return y
+
+
+def gemv_multi(tensors, x, ys=None, stream=None, workspace=None):
+    """ys[m][b, r] = sum_k W_m[r, k] x[b, k] for up to 4 DeviceTensors with the
+    same columns that share x (one grouped launch where the library can).
+
+    ``workspace`` defaults to the largest of the tensors' cached workspaces;
+    pass False to run without one."""
+    import torch
+    if not 1 <= len(tensors) <= 4:
+        raise ValueError("one to four tensors")
+    K = tensors[0].shape[1]
+    if x.dim() == 1:
+        x = x.unsqueeze(0)
+    if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous():
+        raise ValueError("x must be a contiguous [batch, cols] tensor")
+    dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16, torch.float16: HL_F16}.get(x.dtype)
+    if dt is None:
+        raise ValueError("x must be float32, bfloat16 or float16")
+    if ys is None:
+        ys = [torch.empty((x.shape[0], t.shape[0]), dtype=torch.float32, device=x.device) for t in tensors]
+    if workspace is None:
+        workspace = max((t.workspace() for t in tensors), key=lambda w: w.numel())
+    ws_ptr, ws_n = (None, 0) if workspace is False else (ctypes.c_void_p(workspace.data_ptr()), workspace.numel())
+    views = (ctypes.POINTER(TensorView) * len(tensors))(*[ctypes.pointer(t.view) for t in tensors])
+    outs = (ctypes.c_void_p * len(tensors))(*[y.data_ptr() for y in ys])
+    _check(lib().hl_decode_gemv_multi(ctypes.cast(views, ctypes.c_void_p), len(tensors),
+                                      ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
+                                      ctypes.cast(outs, ctypes.c_void_p), ws_ptr, ws_n, _stream_ptr(stream)),
+           "hl_decode_gemv_multi")
+    return ys
 
 
 def gemv_bf16(w, x, y=None, stream=None):

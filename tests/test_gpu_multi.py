@@ -1,0 +1,71 @@
+"""GPU parity of the grouped GEMV (hl_decode_gemv_multi): matrices that share
+x decoded in one launch, its blocks divided among them. Every output against
+a float64 product of the exact bf16 values and sampled rows against the
+oracle, and against each matrix multiplied alone; same bar as the other GEMV
+tests (|y - y_ref| / (sum |w x| + 1e-30) <= 1e-3).
+
+Cases: an 8B-shaped q, k, v (4096, 1024 and 1024 rows: the 1024-row matrices
+alone are too small for the persistent kernel), a gate/up pair with a ragged
+row block, a mix of split and whole-exponent containers, and a group that
+does not take the grouped launch (S = 128) and runs one matrix at a time.
+"""
+import numpy as np
+import pytest
+
+from gen import random_bf16, random_x
+from oracle import gemv as ogemv
+from oracle.gemv import bf16_to_f64
+
+hl = pytest.importorskip("paper_2502_00922_amd.hufflm")
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch():
+    t = pytest.importorskip("torch")
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+CASES = {
+    "qkv": ([4096, 1024, 1024], 4096, [{}, {}, {}]),
+    "gate_up_ragged": ([4100, 4100], 4096, [{}, {}]),
+    "mixed_formats": ([2048, 1024, 3072, 512], 4096, [{}, {"whole_exponent": True}, {}, {"whole_exponent": True}]),
+    "not_grouped": ([256, 512], 1024, [{"seg_len": 128}, {"seg_len": 128}]),
+}
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_grouped_gemv(torch, case):
+    rows, cols, kws = CASES[case]
+    print(f"grouped {case} rows={rows} cols={cols}", flush=True)
+    Ws = [random_bf16((r, cols), seed=100 + k) for k, r in enumerate(rows)]
+    ts = [hl.DeviceTensor(hl.encode(w, **kw)) for w, kw in zip(Ws, kws)]
+    for B in (1, 5, 16):
+        xs = random_x(B, cols, seed=B, dtype="bf16")
+        x = torch.from_numpy(xs.view(np.int16)).cuda().view(torch.bfloat16)
+        ys = [y.cpu().numpy().astype(np.float64) for y in hl.gemv_multi(ts, x)]
+        torch.cuda.synchronize()
+        Xf = bf16_to_f64(xs)
+        for k, (W, y) in enumerate(zip(Ws, ys)):
+            Wf = bf16_to_f64(W)
+            err = np.abs(y - Xf @ Wf.T) / (np.abs(Xf) @ np.abs(Wf).T + 1e-30)
+            assert err.max() <= TOL, (case, B, k, float(err.max()))
+            alone = ts[k].gemv(x).cpu().numpy().astype(np.float64)
+            assert (np.abs(alone - y) / (np.abs(Xf) @ np.abs(Wf).T + 1e-30)).max() <= 2 * TOL
+            sample = [0, W.shape[0] // 2, W.shape[0] - 1]
+            yo, do = ogemv.gemv_rows(W, xs, rows=sample)
+            assert (np.abs(y[:, sample] - yo) / (do + 1e-30)).max() <= TOL
+
+
+def test_grouped_gemv_errors(torch):
+    a = hl.DeviceTensor(hl.encode(random_bf16((64, 512), seed=1)))
+    b = hl.DeviceTensor(hl.encode(random_bf16((64, 1024), seed=2)))
+    x = torch.zeros((1, 512), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(hl.HLError):
+        hl.gemv_multi([a, b], x)  # different column counts
+    with pytest.raises(ValueError):
+        hl.gemv_multi([a] * 5, x)
