@@ -286,7 +286,7 @@ hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype
  * sum_k W_m[r][k] * x[b][k] (a decode step's q, k and v projections, or its
  * gate and up projections), as hl_decode_gemv computes each. ts[m]: views
  * with the same number of columns. When every matrix is in a bf16 format with
- * 16-row groups and the same segment length of 32 or 64, x is bf16 and the
+ * 16-row groups and segments of 64 weights, x is bf16 and the
  * matrices have at least one row block per CU together, one launch decodes
  * them all: its blocks are divided among the matrices in proportion to their
  * row blocks, so the launch and first-load latency of small matrices is paid

@@ -24,6 +24,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <cstring>
 
 #include "hl_internal.h"
@@ -1211,21 +1212,35 @@ struct StreamArgs {
   uint32_t n;
 };
 
-template <int SP, int JT, bool XT>
-__global__ void __launch_bounds__(1024) gemv_stream_kernel(StreamArgs sa) {
+// One matrix (Args = GemvArgs), or a grouped launch (Args = StreamArgs: a
+// block first finds its matrix, with a dependent load before its arguments;
+// the one-matrix kernel keeps the small argument block and reads it at fixed
+// places).
+template <class Args>
+__device__ inline const GemvArgs& gemv_args(const Args& x) {
+  if constexpr (std::is_same_v<Args, StreamArgs>) return x.p; else return x;
+}
+
+template <int SP, int JT, bool XT, class Args>
+__global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
-  const GemvArgs& p = sa.p;
-  // this block's matrix (wave-uniform selects, no indexing into the arguments)
-  uint32_t m = 0;
-  for (uint32_t k = 1; k < sa.n; ++k) m += blockIdx.x >= sa.part0[k] ? 1u : 0u;
-  GroupArgs a = sa.g[0];
-  float* yp = sa.y[0];
-  if (m == 1) a = sa.g[1], yp = sa.y[1];
-  if (m == 2) a = sa.g[2], yp = sa.y[2];
-  if (m == 3) a = sa.g[3], yp = sa.y[3];
-  const uint32_t bid = blockIdx.x - sa.part0[m], nblk = sa.part0[m + 1] - sa.part0[m];
+  constexpr bool kMulti = std::is_same_v<Args, StreamArgs>;
+  const GemvArgs& p = gemv_args(sa);
+  // this block's matrix (wave-uniform; its arguments are read in place)
+  const GroupArgs* ap = &p.g;
+  float* yp = p.y;
+  uint32_t bid = blockIdx.x, nblk = gridDim.x;
+  if constexpr (kMulti) {
+    uint32_t m = 0;
+    for (uint32_t k = 1; k < sa.n; ++k) m += blockIdx.x >= sa.part0[k] ? 1u : 0u;
+    ap = &sa.g[m];
+    yp = sa.y[m];
+    bid = blockIdx.x - sa.part0[m];
+    nblk = sa.part0[m + 1] - sa.part0[m];
+  }
+  const GroupArgs& a = *ap;
   const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
   uint32_t* cols = s_dyn + wave * kBuf;
@@ -1895,27 +1910,38 @@ static int stream_rows_for(uint32_t seg_len, uint32_t col_rows) {
 }
 
 template <bool XT>
-static hl_status launch_stream_x(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                                 const StreamArgs& p) {
+static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block, size_t lds,
+                                 hipStream_t s, const StreamArgs& p) {
+  if (seg_len == 64 && multi) {
+    switch (jt) {
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs>, grid, block, lds, s, p);
+      default: return HL_EUNSUPPORTED;
+    }
+  }
+  if (multi) return HL_EUNSUPPORTED;
+  const GemvArgs& g = p.p;  // one matrix: the small argument block
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs>, grid, block, lds, s, g);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs>, grid, block, lds, s, g);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8, XT>, grid, block, lds, s, p);
-    case 12: return launch(gemv_stream_kernel<4, 12, XT>, grid, block, lds, s, p);
+    case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs>, grid, block, lds, s, g);
+    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs>, grid, block, lds, s, g);
     default: return HL_EUNSUPPORTED;
   }
 }
 
-static hl_status launch_stream(bool xt, uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                               const StreamArgs& p) {
-  return xt ? launch_stream_x<true>(seg_len, jt, grid, block, lds, s, p)
-            : launch_stream_x<false>(seg_len, jt, grid, block, lds, s, p);
+// Grouped launches (multi) exist for S = 64.
+static hl_status launch_stream(bool xt, uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block, size_t lds,
+                               hipStream_t s, const StreamArgs& p) {
+  return xt ? launch_stream_x<true>(seg_len, jt, multi, grid, block, lds, s, p)
+            : launch_stream_x<false>(seg_len, jt, multi, grid, block, lds, s, p);
 }
 
 // Segment lengths with a matrix-core instantiation (S = 8 * steps).
@@ -2217,15 +2243,13 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
     if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
       p.C = CB;
       p.KS = 1;
-      StreamArgs sa;
+      StreamArgs sa;  // one matrix: only sa.p (with p.g, p.y) reaches the kernel
       std::memset(&sa, 0, sizeof(sa));
       sa.p = p;
-      sa.g[0] = pl.ga;
-      sa.y[0] = y_dev;
       sa.n = 1;
       sa.part0[1] = std::min(RB, cus);
-      return launch_stream(xt, t->seg_len, jt, dim3(sa.part0[1]), dim3(w * 64), w * per_wave, (hipStream_t)stream,
-                           sa);
+      return launch_stream(xt, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64), w * per_wave,
+                           (hipStream_t)stream, sa);
     }
   }
   // Column blocks per block and blocks per row block.
@@ -2250,12 +2274,11 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
   for (uint32_t k = 0; k < count; ++k)
     if (!ts[k] || !y_devs[k] || ts[k]->cols != ts[0]->cols) return HL_EINVAL;
   // One launch of the persistent kernel when every matrix has its container
-  // geometry (bf16 formats, 16-row groups, the same S of 32 or 64) and bf16 x;
-  // otherwise the matrices one after another.
+  // geometry (bf16 formats, 16-row groups, S = 64) and bf16 x; otherwise the
+  // matrices one after another.
   bool grouped = count > 1 && x_dtype == HL_BF16;
   for (uint32_t k = 0; k < count && grouped; ++k)
-    grouped = !is_fp16(ts[k]) && ts[k]->grp_rows == 16 && ts[k]->seg_len == ts[0]->seg_len &&
-              (ts[k]->seg_len == 64 || ts[k]->seg_len == 32);
+    grouped = !is_fp16(ts[k]) && ts[k]->grp_rows == 16 && ts[k]->seg_len == 64;
   const uint32_t cus = (uint32_t)device_cus();
   Plan pl[kMaxParts];
   int jt = 0;
@@ -2319,7 +2342,7 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
     sa.y[k] = y_devs[k];
     sa.part0[k + 1] = sa.part0[k] + nb[k];
   }
-  return launch_stream(xt, ts[0]->seg_len, jt, dim3(used), dim3(w * 64), w * per_wave, (hipStream_t)stream, sa);
+  return launch_stream(xt, ts[0]->seg_len, jt, true, dim3(used), dim3(w * 64), w * per_wave, (hipStream_t)stream, sa);
 }
 
 // ------------------------------------------------------------------ prefill GEMM host side
