@@ -159,6 +159,16 @@ def time_launches(torch, launch, nrep, steps, warmup):
     return float(per.mean()), float(np.median(per)), t0.elapsed_time(t1) / steps
 
 
+def hbm_read_probe(torch, hl, gib: int = 2, steps: int = 20) -> float:
+    """Achievable HBM read rate (GB/s) on this GPU: the library's streaming-read
+    probe over `gib` GiB (far past the last-level cache), graph-timed."""
+    t = torch.empty((gib << 30) // 4, dtype=torch.int32, device="cuda").fill_(1)
+    out = torch.empty(int(hl.lib().hl_read_probe_blocks()), dtype=torch.int32, device="cuda")
+    ms = time_graph(torch, lambda i: hl.hufflm.read_probe(t, out), 1, steps, 2)
+    del t
+    return (gib << 30) / (ms * 1e-3) / 1e9
+
+
 def cpu_oracle_baseline(blob: bytes, x, seconds: float, weights: str):
     """The oracle, as it stands, on a bounded sample: bit-serial decode of whole
     groups plus the exactly rounded fp64 partial products of those weights."""
@@ -528,6 +538,11 @@ def main():
     if prefill:
         extra["prefill"] = prefill
     extra["encoder"] = encoder
+    # the same compressed rate against what a plain streaming read reaches here
+    probe = hbm_read_probe(torch, hl)
+    extra["hbm_read_probe"] = dict(GBps=round(probe, 1), fraction_of_peak=round(probe / HBM_PEAK_GBS, 4),
+                                   fused_fraction_of_probe=round(achieved / probe, 4),
+                                   note="hl_read_probe: one streaming read of 2 GiB, graph-timed")
     out = {
         "metric": METRIC,
         "value": round(value, 1),

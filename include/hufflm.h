@@ -318,6 +318,13 @@ size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
 hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t tokens,
                          float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream);
 
+/* Measurement probe: reads `bytes` (a multiple of 16, 16-byte aligned) of
+ * device memory once, the rate plain streaming reads of HBM reach on this
+ * device; out_dev: hl_read_probe_blocks() words (overwritten, contents of no
+ * use). Errors: HL_EINVAL. */
+uint32_t hl_read_probe_blocks(void);
+hl_status hl_read_probe(const void* src_dev, size_t bytes, uint32_t* out_dev, void* stream);
+
 /* Uncompressed comparator: the same product from plain bf16 W [rows][cols]
  * in device memory. */
 hl_status hl_gemv_bf16(const uint16_t* w_dev, uint64_t rows, uint64_t cols,

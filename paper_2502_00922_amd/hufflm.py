@@ -81,7 +81,7 @@ EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_bui
            "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
            "hl_decode_gemv", "hl_decode_gemv_multi", "hl_gemm_workspace_bytes", "hl_decode_gemm",
-           "hl_gemv_bf16"]
+           "hl_gemv_bf16", "hl_read_probe_blocks", "hl_read_probe"]
 
 
 def lib() -> ctypes.CDLL:
@@ -135,6 +135,10 @@ def lib() -> ctypes.CDLL:
     L.hl_decode_gemm.restype = c.c_int
     L.hl_decode_gemm.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                  c.c_void_p, c.c_size_t, c.c_void_p]
+    L.hl_read_probe_blocks.restype = c.c_uint32
+    L.hl_read_probe_blocks.argtypes = []
+    L.hl_read_probe.restype = c.c_int
+    L.hl_read_probe.argtypes = [c.c_void_p, c.c_size_t, c.c_void_p, c.c_void_p]
     L.hl_gemv_bf16.restype = c.c_int
     L.hl_gemv_bf16.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.c_void_p, c.c_int, c.c_uint32,
                                c.c_void_p, c.c_void_p]
@@ -351,6 +355,16 @@ def gemv_multi(tensors, x, ys=None, stream=None, workspace=None):
                                       ctypes.cast(outs, ctypes.c_void_p), ws_ptr, ws_n, _stream_ptr(stream)),
            "hl_decode_gemv_multi")
     return ys
+
+
+def read_probe(buf, out=None, stream=None):
+    """Reads the device tensor ``buf`` once (a streaming-read probe of HBM)."""
+    import torch
+    if out is None:
+        out = torch.empty(int(lib().hl_read_probe_blocks()), dtype=torch.int32, device=buf.device)
+    _check(lib().hl_read_probe(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
+                               ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)), "hl_read_probe")
+    return out
 
 
 def gemv_bf16(w, x, y=None, stream=None):

@@ -168,3 +168,16 @@ def test_device_copy(torch):
     torch.cuda.synchronize()
     assert np.array_equal(cp.gemv(x).cpu().numpy(), y0)
     assert np.array_equal(_decode(torch, cp), w)
+
+
+def test_read_probe(torch):
+    # the streaming-read probe reads every word once: the XOR of its per-block
+    # words is the XOR of the buffer
+    print("read probe", flush=True)
+    rng = np.random.default_rng(3)
+    words = rng.integers(0, 1 << 32, (1 << 20) + 12, dtype=np.uint64).astype(np.uint32)
+    buf = torch.from_numpy(words.view(np.int32)).cuda()
+    out = hl.read_probe(buf)
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32))
+    assert int(got) == int(np.bitwise_xor.reduce(words))
