@@ -10,7 +10,11 @@ different stream lengths all run:
 * log-uniform magnitudes over 2^-60 .. 2^60 (long streams: about 7 code bits
   per weight, so two pairs often exceed a 14-bit window);
 * a geometric low exponent nibble (codes up to the length limit: pairs past
-  the 13-bit window).
+  the 13-bit window);
+* long moves: every pair fits the 13-bit window (no escapes), but every
+  64th row holds pairs of 10 to 13 bits, so four pairs often move a lane's
+  position past the four words it read and its second window is read from
+  the column (the decode's rare wave-uniform branch).
 Each in the split format (code limit 12 and 15) and the whole-exponent
 format. Outputs: every row against a float64 product of the exact bf16
 values, and sampled rows against the oracle's exactly rounded sums, at batch
@@ -52,25 +56,37 @@ def _weights(kind, rows, cols, seed):
         eh = rng.choice([3, 6, 7, 8], n, p=[0.02, 0.08, 0.8, 0.1])
         bits = (rng.integers(0, 2, n) << 15) | (eh << 11) | (el << 7) | rng.integers(0, 128, n)
         return bits.astype(np.uint16).reshape(rows, cols)
+    if kind == "long_moves":
+        # eh uniform over 4..11 (3-bit codes); el geometric over 0..10 (codes
+        # of 1..10 bits: the longest pair is exactly 13 bits), except in
+        # every 64th row, where it is uniform over 7..10 (the longest codes)
+        eh = rng.integers(4, 12, (rows, cols))
+        el = np.minimum(rng.geometric(0.5, (rows, cols)) - 1, 10)
+        el = np.where((np.arange(rows) % 64 == 0)[:, None], rng.integers(7, 11, (rows, cols)), el)
+        bits = (rng.integers(0, 2, (rows, cols)) << 15) | (eh << 11) | (el << 7) | rng.integers(0, 128, (rows, cols))
+        return bits.astype(np.uint16)
     mag = np.exp2(rng.uniform(-60, 60, (rows, cols))).astype(np.float32)
     return f32_to_bf16_bits(mag * np.where(rng.random((rows, cols)) < 0.5, -1, 1).astype(np.float32))
 
 
 # container formats: (encoder keywords); the longer split limit puts el codes
-# past the 13-bit joint window, whole exponents put two codes past the
-# 14-bit two-pair window often (both decoded by the kernel's slot fix-up)
+# past the 13-bit joint window (escape entries); whole exponents have codes
+# of at most 13 bits (no escapes)
 FORMATS = {"split": {}, "split_lmax15": {"lmax": 15}, "whole": {"whole_exponent": True}}
 
 
 @pytest.mark.parametrize("S,cols,fmt", [(64, 8192, "split"), (32, 4096, "split"), (64, 8192, "split_lmax15"),
                                         (64, 8192, "whole"), (32, 4096, "whole")])
-@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform", "geometric"])
+@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform", "geometric", "long_moves"])
 def test_persistent_kernel(torch, S, cols, fmt, kind):
     rows = 4100
     print(f"persistent S={S} {rows}x{cols} {fmt} {kind}", flush=True)
     W = _weights(kind, rows, cols, seed=S + cols)
     dt = hl.DeviceTensor(hl.encode(W, seg_len=S, **FORMATS[fmt]))
     assert dt.view.grp_rows == 16
+    if kind == "long_moves" and fmt == "split":
+        cb = dt.view.cb  # every pair fits the 13-bit window: long moves without escapes
+        assert max(cb.eh.len) + max(cb.el.len) <= 13
     Wf = bf16_to_f64(W)
     rng = np.random.default_rng(S)
     sample = sorted({0, 15, 16, rows - 5, rows - 4, rows - 1} | set(int(r) for r in rng.integers(0, rows, 10)))
