@@ -1190,7 +1190,9 @@ __global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* partial, 
 // least one 16-row block per block of the grid and at least as many column
 // blocks as waves. Block b takes row blocks b, b + grid, ...; its waves take
 // the row block's column blocks wave, wave + waves, ... The table is copied
-// once per block.
+// once per block. With DEC it decodes to bf16 instead (hl_decode): a lane
+// keeps its segment's weights (S*2 bytes of one row) and stores them at the
+// group's end, with no activations and no sums.
 //
 // While a wave decodes group k from its LDS columns, group k+1's stream words
 // (JT per lane, four per load), raw bytes and activations are loaded into
@@ -1221,8 +1223,8 @@ __device__ inline const GemvArgs& gemv_args(const Args& x) {
   if constexpr (std::is_same_v<Args, StreamArgs>) return x.p; else return x;
 }
 
-template <int SP, int JT, bool XT, class Args>
-__global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
+template <int SP, int JT, bool XT, class Args, bool DEC>
+__global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
@@ -1241,6 +1243,7 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
     nblk = sa.part0[m + 1] - sa.part0[m];
   }
   const GroupArgs& a = *ap;
+  uint16_t* const outp = reinterpret_cast<uint16_t*>(yp);  // decoding: the bf16 output (GemvArgs::y)
   const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
   uint32_t* cols = s_dyn + wave * kBuf;
@@ -1292,17 +1295,16 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
     const uint32_t rb = g0 / CB;
     const uint32_t G = min(16u, a.rows - rb * 16);
     const uint8_t* r = a.raw + m0.first * S + lane_mu(rb) * 8;
-    const uint8_t* x = xbytes + m0.c0 * XSEG + xoff;
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
       rw[k] = *reinterpret_cast<const uint2*>(r + k * G * 32u);
-      xv[k] = *reinterpret_cast<const uint4*>(x + k * XSTEP);
+      if constexpr (!DEC) xv[k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff + k * XSTEP);
     }
   }
   stream_store<JT>(cols, sw, lane);
-  // everything but the 2*SP raw and activation loads: the table copy (and
-  // the metadata and stream words before it)
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * SP));
+  // everything but the raw and activation loads (2*SP; SP when decoding):
+  // the table copy (and the metadata and stream words before it)
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(DEC ? SP : 2 * SP));
   asm volatile("" ::: "memory");
   __syncthreads();
 
@@ -1331,12 +1333,16 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
       uint32_t pos2n = stream_load<JT>(a, m1, lane, sw);
       m1 = load_meta(a, g2, lane);
       // prefetch source: the next group, else the lane's cached activations
+      // (decoding: the current group's raw bytes)
       const uint32_t cur_c0 = (wave + j * waves) * 4;
-      const uint8_t* rbase = okn ? a.raw + n_first * S : xbytes + cur_c0 * XSEG;
-      const uint32_t roff = okn ? lane_mu(rbn) * 8 : xoff;
+      const uint8_t* rbase = okn    ? a.raw + n_first * S
+                             : DEC ? a.raw + ((uint64_t)rb * 16u * a.L + (uint64_t)cur_c0 * G) * S
+                                   : xbytes + cur_c0 * XSEG;
+      const uint32_t roff = okn ? lane_mu(rbn) * 8 : DEC ? mu * 8 : xoff;
       const uint32_t rs = okn ? Gn * 32u : 0u;
       const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * XSEG;
       uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+      uint4 dv[DEC ? SP : 1];  // decoding: the lane's weights of the group
 #pragma unroll
       for (int k = 0; k < SP; ++k) {
         uint32_t e[8];
@@ -1346,11 +1352,24 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
         wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
         wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
         wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
-                                                      __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
-        // x first: the wait for the raw bytes at their use then covers both
-        xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
+        if constexpr (DEC) {
+          dv[k] = wv;
+        } else {
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
+                                                        __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
+          // x first: the wait for the raw bytes at their use then covers both
+          xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
+        }
         rw[k] = *reinterpret_cast<const uint2*>(rbase + k * rs + roff);
+      }
+      if constexpr (DEC) {
+        // row r0 + i, columns (c0 + q)*S .. + S: stored back to back, so
+        // that each of the lane's cache lines is written whole at once
+        if (i < G) {
+          uint4* o = reinterpret_cast<uint4*>(outp + (uint64_t)(rb * 16 + i) * a.cols + (cur_c0 + q) * S);
+#pragma unroll
+          for (int k = 0; k < SP; ++k) o[k] = dv[k];
+        }
       }
       wait_lgkm0();
       wave_sync_lds();
@@ -1365,19 +1384,21 @@ __global__ void __launch_bounds__(1024) gemv_stream_kernel(Args sa) {
     }
     // End of the row block: add the waves' accumulators in a fixed order
     // (LDS-only barriers: the loads in flight stay in flight).
-    block_sync_lds();
-    float* red = reinterpret_cast<float*>(cols);
+    if constexpr (!DEC) {
+      block_sync_lds();
+      float* red = reinterpret_cast<float*>(cols);
 #pragma unroll
-    for (int v = 0; v < 4; ++v) red[v * 64 + lane] = acc[v];
-    acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    block_sync_lds();
-    if (wave < 4) {
-      const uint32_t v = wave;
-      float sum = 0.f;
-      for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + w * kBuf)[v * 64 + lane];
-      if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
+      for (int v = 0; v < 4; ++v) red[v * 64 + lane] = acc[v];
+      acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      block_sync_lds();
+      if (wave < 4) {
+        const uint32_t v = wave;
+        float sum = 0.f;
+        for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + w * kBuf)[v * 64 + lane];
+        if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
+      }
+      block_sync_lds();
     }
-    block_sync_lds();
     stream_store<JT>(cols, sw, lane);  // the next group's words, held back for the sum
     wait_lgkm0();
     wave_sync_lds();
@@ -1914,9 +1935,9 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
                                  hipStream_t s, const StreamArgs& p) {
   if (seg_len == 64 && multi) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
@@ -1924,15 +1945,15 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
   const GemvArgs& g = p.p;  // one matrix: the small argument block
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs>, grid, block, lds, s, g);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs>, grid, block, lds, s, g);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs>, grid, block, lds, s, g);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false>, grid, block, lds, s, g);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false>, grid, block, lds, s, g);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs>, grid, block, lds, s, g);
-    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs>, grid, block, lds, s, g);
+    case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false>, grid, block, lds, s, g);
+    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false>, grid, block, lds, s, g);
     default: return HL_EUNSUPPORTED;
   }
 }
@@ -1942,6 +1963,24 @@ static hl_status launch_stream(bool xt, uint32_t seg_len, int jt, bool multi, di
                                hipStream_t s, const StreamArgs& p) {
   return xt ? launch_stream_x<true>(seg_len, jt, multi, grid, block, lds, s, p)
             : launch_stream_x<false>(seg_len, jt, multi, grid, block, lds, s, p);
+}
+
+// Decoding to bf16 with the persistent kernel (p.y = the output).
+static hl_status launch_stream_dec(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                                   const GemvArgs& p) {
+  if (seg_len == 64) {
+    switch (jt) {
+      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true>, grid, block, lds, s, p);
+      default: return HL_EUNSUPPORTED;
+    }
+  }
+  switch (jt) {
+    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true>, grid, block, lds, s, p);
+    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true>, grid, block, lds, s, p);
+    default: return HL_EUNSUPPORTED;
+  }
 }
 
 // Segment lengths with a matrix-core instantiation (S = 8 * steps).
@@ -2049,12 +2088,48 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
   return launch(lut_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, aux);
 }
 
+// Launch shape of the persistent kernel for one matrix: stream words per lane
+// (*jt), waves per block (*waves) and LDS bytes per wave; false when the
+// matrix does not fit it (16-row groups of the bf16 formats at S = 32 or 64,
+// at least one row block per CU and two groups per wave of at least 8 waves
+// per block, every segment within the largest stream word count).
+static bool stream_shape(const hl_tensor* t, const GroupArgs& ga, int* jt, uint32_t* waves, size_t* per_wave) {
+  if (is_fp16(t) || t->grp_rows != 16 || (t->seg_len != 64 && t->seg_len != 32)) return false;
+  const uint32_t CB = ga.CB, RB = ga.RB, cus = (uint32_t)device_cus();
+  *jt = stream_rows_for(t->seg_len, ga.col_rows);
+  const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
+  *per_wave = (size_t)(*jt + 1) * kCol * 4;
+  uint32_t w = kMaxWaves;
+  while (w > 1 && tab + w * *per_wave > kMaxLds) --w;
+  // fewer waves per block when that gives every wave two groups: the
+  // second group's loads then overlap the first one's decode
+  while (w > 8 && (uint64_t)RB * CB < 2ull * cus * w) --w;
+  *waves = w;
+  return *jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w;
+}
+
 extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream) {
   if (!out_dev) return HL_EINVAL;
   Plan pl;
   hl_status st = make_plan(t, 0, !is_fp16(t), &pl);
   if (st != HL_OK) return st;
   const uint32_t n_grp = pl.ga.RB * pl.ga.CB;
+  // large matrices: the persistent kernel, its product replaced by stores
+  int jt = 0;
+  uint32_t w = 0;
+  size_t per_wave = 0;
+  if (stream_shape(t, pl.ga, &jt, &w, &per_wave)) {
+    GemvArgs p;
+    std::memset(&p, 0, sizeof(p));
+    p.g = pl.ga;
+    p.y = reinterpret_cast<float*>(out_dev);
+    p.B = 1;
+    p.C = pl.ga.CB;
+    p.KS = 1;
+    w = 8;  // the kernel's bound when decoding (registers for a group's weights)
+    return launch_stream_dec(t->seg_len, jt, dim3(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus())),
+                             dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
+  }
   if (is_fp16(t)) {
     const uint32_t per_cu = std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)pl.lds));
     const uint32_t blocks = std::min<uint32_t>((n_grp + pl.waves - 1) / pl.waves, device_cus() * per_cu);
@@ -2231,16 +2306,11 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   }
   // Persistent kernel: S = 32 or 64, at least one row block per CU and two
   // groups per wave.
-  if (mfma && (t->seg_len == 64 || t->seg_len == 32)) {
-    const int jt = stream_rows_for(t->seg_len, pl.ga.col_rows);
-    const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
-    const size_t per_wave = (size_t)(jt + 1) * kCol * 4;
-    uint32_t w = kMaxWaves;
-    while (w > 1 && tab + w * per_wave > kMaxLds) --w;
-    // fewer waves per block when that gives every wave two groups: the
-    // second group's loads then overlap the first one's decode
-    while (w > 8 && (uint64_t)RB * CB < 2ull * cus * w) --w;
-    if (jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w) {
+  if (mfma) {
+    int jt = 0;
+    uint32_t w = 0;
+    size_t per_wave = 0;
+    if (stream_shape(t, pl.ga, &jt, &w, &per_wave)) {
       p.C = CB;
       p.KS = 1;
       StreamArgs sa;  // one matrix: only sa.p (with p.g, p.y) reaches the kernel

@@ -16,7 +16,8 @@ different stream lengths all run:
   position past the four words it read and its second window is read from
   the column (the decode's rare wave-uniform branch).
 Each in the split format (code limit 12 and 15) and the whole-exponent
-format. Outputs: every row against a float64 product of the exact bf16
+format. The full decode of each container (the same kernel storing the
+weights) must be bit-exact. Outputs: every row against a float64 product of the exact bf16
 values, and sampled rows against the oracle's exactly rounded sums, at batch
 1, 5 and 16.
 """
@@ -101,4 +102,7 @@ def test_persistent_kernel(torch, S, cols, fmt, kind):
         assert err.max() <= TOL, (B, float(err.max()), int(np.argmax(err.max(0))))
         yo, do = ogemv.gemv_rows(W, xs, rows=sample)
         assert (np.abs(y[:, sample] - yo) / (do + 1e-30)).max() <= TOL
+    # the full decode of the same container runs on the persistent kernel
+    # too (its product replaced by stores): bit-exact
+    assert np.array_equal(dt.decode().cpu().numpy().view(np.uint16), W)
     torch.cuda.synchronize()
