@@ -20,7 +20,8 @@
 // sign/mantissa plane ([t/8][lane] in 8-byte units) and the activation slice
 // in LDS; the matrix-core kernels keep raw bytes and activations in
 // registers, prefetched steps ahead, and the persistent kernel loads the next
-// group's stream words into registers while it decodes the current group.
+// group's stream words into registers while it decodes the current group (in
+// its decode form it also decodes large matrices to bf16).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
