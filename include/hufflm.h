@@ -260,8 +260,14 @@ hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
  * longer than the window) and the per-length tables are zero. */
 hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
 
+/* Device buffers of the calls below (x, decoded weights, workspaces, plain
+ * bf16 weights) are read or written in 16-byte pieces and must be 16-byte
+ * aligned (any hipMalloc or torch allocation is); float32 outputs must be
+ * 4-byte aligned. A misaligned pointer gives HL_EINVAL. */
+
 /* Decode the whole matrix to bf16 bit patterns, out_dev[rows*cols]
- * (row-major). Bit-exact with the encoder's input. */
+ * (row-major). Bit-exact with the encoder's input. Errors: HL_EINVAL (also
+ * for a misaligned out_dev). */
 hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream);
 
 /* Bytes of device workspace hl_decode_gemv may use for cross-block partial
@@ -277,7 +283,7 @@ size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch);
  * caller once before first use; each call leaves it ready for the next. Calls
  * that may run concurrently need separate workspaces. With NULL (or too
  * small) the product is still computed, with less parallelism for matrices
- * with few rows. Errors: HL_EINVAL. */
+ * with few rows. Errors: HL_EINVAL (also for misaligned x, y or workspace). */
 hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype,
                          uint32_t batch, float* y_dev, void* workspace_dev,
                          size_t workspace_bytes, void* stream);

@@ -2089,6 +2089,11 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
   return launch(lut_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, aux);
 }
 
+// Buffers the kernels read or write in 16-byte pieces (activations, decoded
+// weights, workspace, uncompressed weights) must be 16-byte aligned, fp32
+// outputs 4-byte aligned; a null workspace is allowed where it is optional.
+static bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
 // Launch shape of the persistent kernel for one matrix: stream words per lane
 // (*jt), waves per block (*waves) and LDS bytes per wave; false when the
 // matrix does not fit it (16-row groups of the bf16 formats at S = 32 or 64,
@@ -2110,7 +2115,7 @@ static bool stream_shape(const hl_tensor* t, const GroupArgs& ga, int* jt, uint3
 }
 
 extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream) {
-  if (!out_dev) return HL_EINVAL;
+  if (!out_dev || !aligned(out_dev, 16)) return HL_EINVAL;
   Plan pl;
   hl_status st = make_plan(t, 0, !is_fp16(t), &pl);
   if (st != HL_OK) return st;
@@ -2278,6 +2283,7 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   if (!t || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH ||
       (x_dtype != HL_F32 && x_dtype != HL_BF16 && x_dtype != HL_F16))
     return HL_EINVAL;
+  if (!aligned(x_dev, 16) || !aligned(y_dev, 4) || !aligned(workspace_dev, 16)) return HL_EINVAL;
   if (t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS) return HL_EINVAL;
   if (is_fp16(t) != (x_dtype == HL_F16)) return HL_EUNSUPPORTED;
   if (is_fp16(t)) return gemv16(t, x_dev, batch, y_dev, workspace_dev, workspace_bytes, (hipStream_t)stream);
@@ -2342,8 +2348,9 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
                                           void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (!ts || !y_devs || !x_dev || count < 1 || count > kMaxParts || batch < 1 || batch > HL_MAX_BATCH)
     return HL_EINVAL;
+  if (!aligned(x_dev, 16) || !aligned(workspace_dev, 16)) return HL_EINVAL;
   for (uint32_t k = 0; k < count; ++k)
-    if (!ts[k] || !y_devs[k] || ts[k]->cols != ts[0]->cols) return HL_EINVAL;
+    if (!ts[k] || !y_devs[k] || !aligned(y_devs[k], 4) || ts[k]->cols != ts[0]->cols) return HL_EINVAL;
   // One launch of the persistent kernel when every matrix has its container
   // geometry (bf16 formats, 16-row groups, S = 64) and bf16 x; otherwise the
   // matrices one after another.
@@ -2442,6 +2449,7 @@ static hl_status launch_gemm_sp(uint32_t nt, dim3 grid, size_t lds, hipStream_t 
 extern "C" hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t tokens,
                                     float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
   if (!t || !x_dev || !y_dev || tokens == 0 || tokens >= (1u << 24)) return HL_EINVAL;
+  if (!aligned(x_dev, 16) || !aligned(y_dev, 4) || !aligned(workspace_dev, 16)) return HL_EINVAL;
   if (x_dtype != HL_BF16 || is_fp16(t) || t->grp_rows != 16 || (t->seg_len != 32 && t->seg_len != 64))
     return HL_EUNSUPPORTED;
   if (!workspace_dev || workspace_bytes < hl_gemm_workspace_bytes(t, tokens)) return HL_EINVAL;
@@ -2490,6 +2498,7 @@ extern "C" hl_status hl_gemv_bf16(const uint16_t* w_dev, uint64_t rows, uint64_t
   if (!w_dev || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH || rows == 0 || cols == 0 ||
       cols % 8 || (x_dtype != HL_F32 && x_dtype != HL_BF16))
     return HL_EINVAL;
+  if (!aligned(w_dev, 16) || !aligned(x_dev, 16) || !aligned(y_dev, 4)) return HL_EINVAL;
   if (rows >= (1ull << 31) || cols >= (1ull << 31)) return HL_EUNSUPPORTED;
   const uint32_t blocks = (uint32_t)std::min<uint64_t>((rows + 3) / 4, (uint64_t)device_cus() * 8);
   const bool xb = x_dtype == HL_BF16;

@@ -154,6 +154,25 @@ def test_errors_are_reported(torch):
         dt.gemv(torch.zeros((1, 64), dtype=torch.bfloat16, device="cuda"))
 
 
+def test_misaligned_buffers_rejected(torch):
+    # buffers the kernels access in 16-byte pieces must be 16-byte aligned:
+    # a view 2 bytes into an allocation is refused on the host, nothing runs
+    w = random_bf16((64, 256), seed=2)
+    dt = hl.DeviceTensor(hl.encode(w))
+    base = torch.zeros(64 * 256 + 8, dtype=torch.int16, device="cuda")
+    with pytest.raises(hl.HLError):
+        dt.decode(base[1:1 + 64 * 256].view(64, 256))
+    xb = torch.zeros(256 + 8, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(hl.HLError):
+        dt.gemv(xb[1:257].view(1, 256))
+    # the aligned views of the same buffers work
+    out = dt.decode(base[8:8 + 64 * 256].view(64, 256))
+    assert np.array_equal(out.cpu().numpy().view(np.uint16), w)
+    y = dt.gemv(xb[8:264].view(1, 256))
+    torch.cuda.synchronize()
+    assert np.all(y.cpu().numpy() == 0)
+
+
 def test_device_copy(torch):
     # a device-to-device copy of a container and its table decodes and
     # multiplies exactly like the original, also after the original is gone

@@ -38,6 +38,25 @@ def test_binding_constants_match_header():
     assert hl.HEADER_BYTES == defs["HL_HEADER_BYTES"]
 
 
+def test_misaligned_pointers_rejected_before_device_work(L):
+    # the alignment checks come before any device work, so fake device
+    # addresses (never dereferenced) that are 2 bytes off a 16-byte boundary
+    # give HL_EINVAL without a GPU
+    import ctypes
+    t = hl.TensorView()
+    good, bad = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10002)
+    assert L.hl_decode(ctypes.byref(t), bad, None) == hl.HL_EINVAL
+    assert L.hl_decode_gemv(ctypes.byref(t), bad, hl.HL_BF16, 1, good, None, 0, None) == hl.HL_EINVAL
+    assert L.hl_decode_gemv(ctypes.byref(t), good, hl.HL_BF16, 1, good, bad, 1 << 20, None) == hl.HL_EINVAL
+    assert L.hl_decode_gemm(ctypes.byref(t), bad, hl.HL_BF16, 4, good, good, 1 << 20, None) == hl.HL_EINVAL
+    assert L.hl_gemv_bf16(bad, 8, 8, good, hl.HL_BF16, 1, good, None) == hl.HL_EINVAL
+    assert L.hl_gemv_bf16(good, 8, 8, good, hl.HL_BF16, 1, ctypes.c_void_p(0x10001), None) == hl.HL_EINVAL
+    ts = (ctypes.POINTER(hl.TensorView) * 1)(ctypes.pointer(t))
+    ys = (ctypes.c_void_p * 1)(0x10000)
+    assert L.hl_decode_gemv_multi(ctypes.cast(ts, ctypes.c_void_p), 1, bad, hl.HL_BF16, 1,
+                                  ctypes.cast(ys, ctypes.c_void_p), None, 0, None) == hl.HL_EINVAL
+
+
 def _codebook_lists(cb):
     return (cb.eh.nsym, cb.eh.single, list(cb.eh.len), cb.el.nsym, cb.el.single, list(cb.el.len))
 
