@@ -169,6 +169,39 @@ def gen_matrix(spec: MatrixSpec, rows: Optional[slice] = None, threads: int = 0)
     return out
 
 
+def device_seed(spec: MatrixSpec) -> int:
+    """63-bit seed of a matrix for gen_matrix_device, from (0, cfg, layer, matrix)."""
+    key = np.random.SeedSequence([0, spec.cfg, spec.layer, spec.index, 9]).generate_state(2, np.uint32)
+    return int(key[0]) | (int(key[1] & np.uint32(0x7FFFFFFF)) << 32)
+
+
+def gen_matrix_device(spec: MatrixSpec, torch, device="cuda"):
+    """The same distribution as gen_matrix, drawn on the GPU (torch's seeded
+    Philox generator) for stacks too large to draw on the host in reasonable
+    time: values N(0, std) (std as in gen_matrix), then an independent
+    Bernoulli(0.001) mask from the same generator multiplying by 20, the
+    per-row or per-matrix scales of gen_matrix (drawn on the host from the
+    same streams), float32 -> bfloat16 round-to-nearest-even (torch's cast).
+    Returns a bfloat16 tensor [rows, cols] on `device`. The values are
+    deterministic for a given seed, torch version and device model; they
+    differ from gen_matrix's (another generator)."""
+    R, K = spec.rows, spec.cols
+    g = torch.Generator(device=device)
+    g.manual_seed(device_seed(spec))
+    std = np.float32(BASE_STD)
+    if spec.layer_scale:
+        std = np.float32(BASE_STD / np.sqrt(_stream(spec, 3).uniform(1.0, 4.0)))
+    w = torch.randn((R, K), generator=g, device=device, dtype=torch.float32)
+    w.mul_(float(std))
+    mask = torch.rand((R, K), generator=g, device=device, dtype=torch.float32) < OUTLIER_P
+    w = torch.where(mask, w * np.float32(OUTLIER_MUL), w)
+    del mask
+    if spec.row_scale:
+        z = _stream(spec, 3).standard_normal(R, dtype=np.float32)
+        w.mul_(torch.from_numpy(np.exp(np.float32(0.3) * z).astype(np.float32)).to(device)[:, None])
+    return w.to(torch.bfloat16)
+
+
 def gen_x(spec: MatrixSpec, batch: int, dtype: str) -> np.ndarray:
     """Activation rows x[batch][cols]: float32, bf16 bits (uint16) if dtype ==
     'bf16', or float16 values if dtype == 'f16'."""

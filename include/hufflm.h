@@ -270,8 +270,9 @@ hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
  * for a misaligned out_dev). */
 hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream);
 
-/* Bytes of device workspace hl_decode_gemv may use for cross-block partial
- * sums of `t` at this batch (0 on bad arguments). */
+/* Bytes of device workspace hl_decode_gemv may use for `t` at this batch
+ * (the tiled activations of larger batches and the cross-block partial sums;
+ * 0 on bad arguments). */
 size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch);
 
 /* y[b][r] = sum_k W[r][k] * x[b][k] for b < batch, decoding W on the fly in
@@ -323,13 +324,6 @@ size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
  * workspaces. Errors: HL_EINVAL (also for a missing or short workspace). */
 hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t tokens,
                          float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream);
-
-/* Measurement probe: reads `bytes` (a multiple of 16, 16-byte aligned) of
- * device memory once, the rate plain streaming reads of HBM reach on this
- * device; out_dev: hl_read_probe_blocks() words (overwritten, contents of no
- * use). Errors: HL_EINVAL. */
-uint32_t hl_read_probe_blocks(void);
-hl_status hl_read_probe(const void* src_dev, size_t bytes, uint32_t* out_dev, void* stream);
 
 /* Uncompressed comparator: the same product from plain bf16 W [rows][cols]
  * in device memory. */

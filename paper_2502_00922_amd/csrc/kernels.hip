@@ -837,20 +837,22 @@ __global__ void __launch_bounds__(1024) gemv_kernel(GemvArgs p) {
   }
   // Several blocks share this row block: publish the partial sums, and the
   // last block to arrive adds them in k-part order and resets the counter.
-  // Partials are written and read with agent-scope atomics, which bypass the
-  // per-XCD caches; once the stores are complete (vmcnt 0) the counter
-  // increment orders them, so no cache write-back or invalidate is needed.
+  // Partials are written and read with agent-scope atomics; the counter
+  // increment is an agent-scope acquire-release, so the parts stored before
+  // it (release) are visible to the block that sees the last count
+  // (acquire, then a fence for the lanes that did not take part in it).
   const uint32_t ldp = a.RB * a.GR;
   if (lane < G)
 #pragma unroll
     for (int b = 0; b < B; ++b)
       __hip_atomic_store(p.partial + ((uint64_t)kp * B + b) * ldp + r0 + lane, s[b], __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
-  wait_vm0();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // every lane's parts, before the count
   uint32_t old = 0;
-  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
   old = __shfl(old, 0, 64);
   if (old != p.KS - 1) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // every lane reads the parts published before the count
   if (lane < G) {
 #pragma unroll
     for (int b = 0; b < B; ++b) {
@@ -908,11 +910,12 @@ __device__ inline void mfma_finish(const GemvArgs& p, const f32x4_t& acc, float*
       if (4 * q + v < G)
         __hip_atomic_store(p.partial + ((uint64_t)kp * p.B + n) * ldp + r0 + 4 * q + v, s[v], __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
-  wait_vm0();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // every lane's parts, before the count
   uint32_t old = 0;
-  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (lane == 0) old = __hip_atomic_fetch_add(p.counter + rb, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
   old = __shfl(old, 0, 64);
   if (old != p.KS - 1) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");  // every lane reads the parts published before the count
   if (nb_ok) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
@@ -2039,9 +2042,16 @@ static hl_status launch_bf16_b(bool xbf16, dim3 grid, dim3 block, hipStream_t s,
 
 using namespace hl;
 
+// Buffers the kernels read or write in 16-byte pieces (activations, decoded
+// weights, workspace, uncompressed weights) must be 16-byte aligned, fp32
+// outputs 4-byte aligned; a null workspace is allowed where it is optional.
+static bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
 extern "C" hl_status hl_tensor_view(const void* blob_dev, const void* blob_host, size_t blob_bytes,
                                     uint32_t* lut_dev, hl_tensor* out) {
   if (!blob_dev || !blob_host || !lut_dev || !out || blob_bytes < HL_HEADER_BYTES) return HL_EINVAL;
+  // the kernels copy the table and the group streams in 16-byte pieces
+  if (!aligned(blob_dev, 16) || !aligned(lut_dev, 16)) return HL_EINVAL;
   Header H;
   uint32_t mseg = 0;
   const hl_status v = validate_blob(reinterpret_cast<const uint8_t*>(blob_host), blob_bytes, &H, &mseg);
@@ -2089,10 +2099,6 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
   return launch(lut_kernel, dim3(1), dim3(256), 0, (hipStream_t)stream, t->lut_dev, aux);
 }
 
-// Buffers the kernels read or write in 16-byte pieces (activations, decoded
-// weights, workspace, uncompressed weights) must be 16-byte aligned, fp32
-// outputs 4-byte aligned; a null workspace is allowed where it is optional.
-static bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
 // Launch shape of the persistent kernel for one matrix: stream words per lane
 // (*jt), waves per block (*waves) and LDS bytes per wave; false when the
@@ -2151,35 +2157,18 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
 
 static uint32_t ks_cap(uint32_t CB) { return std::min<uint32_t>(CB, 64); }
 
-static uint64_t workspace_counter_bytes(uint32_t RB) { return ((uint64_t)RB * 4 + 255) & ~255ull; }
-
-// Workspace layout: RB arrival counters, the split partial sums, then (batch
-// above one, 16-row groups) the tiled copy of bf16 activations: 32 bytes per
-// column.
-static uint64_t xtile_offset(uint32_t RB, uint32_t CB, uint32_t GR, uint32_t batch) {
-  return (workspace_counter_bytes(RB) + (uint64_t)ks_cap(CB) * batch * RB * GR * 4 + 255) & ~255ull;
+// Workspace layout: the tiled copy of bf16 activations (batch above one,
+// 16-row groups: 32 bytes per column), then RB arrival counters and the
+// split partial sums of the non-persistent kernels.
+static uint64_t xtile_region(const hl_tensor* t, uint32_t batch) {
+  return (batch > 1 && t->grp_rows == 16) ? ((uint64_t)t->cols * 32 + 255) & ~255ull : 0;
 }
-static uint64_t xtile_bytes(const hl_tensor* t, uint32_t batch) {
-  return (batch > 1 && t->grp_rows == 16) ? (uint64_t)t->cols * 32 : 0;
-}
+static uint64_t counter_bytes(uint32_t RB) { return ((uint64_t)RB * 4 + 255) & ~255ull; }
 
-extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
-  if (!t || t->seg_len == 0 || t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS || batch < 1 ||
-      batch > HL_MAX_BATCH)
-    return 0;
-  const uint32_t GR = t->grp_rows;
-  const uint32_t RB = (uint32_t)((t->rows + GR - 1) / GR);
-  const uint32_t CB = (uint32_t)(t->cols / t->seg_len) / (HL_GROUP_SEGS / GR);
-  return xtile_offset(RB, CB, GR, batch) + xtile_bytes(t, batch);
-}
-
-// Column blocks per block (C) and blocks per row block (KS) of the
-// non-persistent kernels: enough blocks to fill the device, each wave decoding
-// at least one group; split over column blocks only with room for partials.
-// *block_waves = the waves a block is launched with (no more than its column
-// blocks).
-static void choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, void* workspace_dev,
-                         size_t workspace_bytes, GemvArgs* p, uint32_t* block_waves) {
+// Column blocks per block (*C) and blocks per row block (*KS) of the
+// non-persistent kernels: enough blocks to fill the device, each wave
+// decoding at least one group.
+static void split_shape(const Plan& pl, uint32_t* C_out, uint32_t* KS_out) {
   const uint32_t CB = pl.ga.CB, RB = pl.ga.RB;
   const uint32_t cus = (uint32_t)device_cus();
   const uint64_t target_waves = (uint64_t)cus * 16;
@@ -2198,17 +2187,45 @@ static void choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, voi
     C = (CB + KS - 1) / KS;
     KS = (CB + C - 1) / C;
   }
-  if (KS > 1 && (!workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch))) {
+  *C_out = C;
+  *KS_out = KS;
+}
+
+// Workspace bytes of a split over KS k-parts (counters and partial sums).
+static uint64_t split_bytes(const Plan& pl, uint32_t batch, uint32_t KS) {
+  return KS > 1 ? counter_bytes(pl.ga.RB) + (uint64_t)KS * batch * pl.ga.RB * pl.ga.GR * 4 : 0;
+}
+
+__global__ void __launch_bounds__(256) zero_kernel(uint32_t* p, uint32_t n) {
+  for (uint32_t k = blockIdx.x * blockDim.x + threadIdx.x; k < n; k += gridDim.x * blockDim.x) p[k] = 0;
+}
+
+// Split of the non-persistent kernels, with room for partials in the
+// workspace (else one block per row block). *block_waves = the waves a block
+// is launched with (no more than its column blocks). With `clear`, the
+// arrival counters are zeroed by a small kernel on `stream` first (a
+// workspace shared with calls of other shapes, whose bytes there are not
+// counters).
+static hl_status choose_split(const hl_tensor* t, const Plan& pl, uint32_t batch, void* workspace_dev,
+                              size_t workspace_bytes, bool clear, hipStream_t stream, GemvArgs* p,
+                              uint32_t* block_waves) {
+  uint32_t C = 0, KS = 0;
+  split_shape(pl, &C, &KS);
+  const uint64_t base = xtile_region(t, batch);
+  if (KS > 1 && (!workspace_dev || workspace_bytes < base + split_bytes(pl, batch, KS))) {
     KS = 1;  // no room for partial sums: one block per row block
-    C = CB;
+    C = pl.ga.CB;
   }
   p->C = C;
   p->KS = KS;
   *block_waves = std::min<uint32_t>(pl.waves, C);
   if (KS > 1) {
-    p->counter = reinterpret_cast<uint32_t*>(workspace_dev);
-    p->partial = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(workspace_dev) + workspace_counter_bytes(RB));
+    uint8_t* w = reinterpret_cast<uint8_t*>(workspace_dev) + base;
+    p->counter = reinterpret_cast<uint32_t*>(w);
+    p->partial = reinterpret_cast<float*>(w + counter_bytes(pl.ga.RB));
+    if (clear) return launch(zero_kernel, dim3((pl.ga.RB + 255) / 256), dim3(256), 0, stream, p->counter, pl.ga.RB);
   }
+  return HL_OK;
 }
 
 template <bool XT>
@@ -2242,10 +2259,8 @@ static hl_status tile_activations(const hl_tensor* t, const void* x_dev, uint32_
   *xt = false;
   const uint64_t n = t->rows * t->cols;
   const bool want = batch >= 12 || (batch >= 8 && n >= (32ull << 20)) || (batch >= 4 && n >= (128ull << 20));
-  if (!want || !workspace_dev || workspace_bytes < hl_gemv_workspace_bytes(t, batch)) return HL_OK;
-  const uint32_t GR = t->grp_rows, RB = (uint32_t)((t->rows + GR - 1) / GR);
-  const uint32_t CB = (uint32_t)(t->cols / t->seg_len) / (HL_GROUP_SEGS / GR);
-  uint4* tile = reinterpret_cast<uint4*>(reinterpret_cast<uint8_t*>(workspace_dev) + xtile_offset(RB, CB, GR, batch));
+  if (!want || !workspace_dev || workspace_bytes < xtile_region(t, batch)) return HL_OK;
+  uint4* tile = reinterpret_cast<uint4*>(workspace_dev);
   const uint32_t chunks = (uint32_t)(t->cols / 8);
   const hl_status st = launch(xtile_kernel, dim3((chunks * 16 + 255) / 256), dim3(256), 0, stream,
                               reinterpret_cast<const uint4*>(x_dev), batch, chunks, tile);
@@ -2256,7 +2271,7 @@ static hl_status tile_activations(const hl_tensor* t, const void* x_dev, uint32_
 }
 
 static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, float* y_dev, void* workspace_dev,
-                        size_t workspace_bytes, hipStream_t stream) {
+                        size_t workspace_bytes, bool clear, hipStream_t stream) {
   if (t->grp_rows != 16 || t->seg_len % 8 || !mfma_steps_ok(t->seg_len / 8)) return HL_EUNSUPPORTED;
   Plan pl;
   hl_status st = make_plan(t, 0, false, &pl);
@@ -2268,7 +2283,8 @@ static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, f
   p.y = y_dev;
   p.B = batch;
   uint32_t w = 0;
-  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p, &w);
+  st = choose_split(t, pl, batch, workspace_dev, workspace_bytes, clear, stream, &p, &w);
+  if (st != HL_OK) return st;
   bool xt = false;
   st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, stream, &p, &xt);
   if (st != HL_OK) return st;
@@ -2278,25 +2294,72 @@ static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, f
   return launch_mfma16(xt, t->seg_len / 8, grid, block, lds, stream, p);
 }
 
-extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
-                                    float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
+// Which kernel family a product runs on and its plan: 16-row groups with
+// bf16 activations run on the matrix cores (the persistent kernel where it
+// fits, *persistent); the vector kernel stages raw bytes and the activation
+// slice (GC*S columns per batch row, *x_words) in LDS.
+static hl_status gemv_plan(const hl_tensor* t, hl_dtype x_dtype, uint32_t batch, Plan* pl, bool* mfma,
+                           bool* persistent, uint32_t* x_words) {
+  const bool xb = x_dtype == HL_BF16;
+  *mfma = xb && t->grp_rows == 16 && t->seg_len % 8 == 0 && mfma_steps_ok(t->seg_len / 8);
+  const uint32_t slice = (HL_GROUP_SEGS / t->grp_rows) * t->seg_len;
+  *x_words = xb ? slice * batch / 2 : slice * batch;
+  const hl_status st = make_plan(t, *mfma ? 0 : *x_words, !*mfma, pl);
+  if (st != HL_OK) return st;
+  int jt = 0;
+  uint32_t w = 0;
+  size_t per_wave = 0;
+  *persistent = *mfma && stream_shape(t, pl->ga, &jt, &w, &per_wave);
+  return HL_OK;
+}
+
+// Workspace bytes a product uses at most (tiled activations, counters and
+// partial sums); 0 for bad arguments.
+static uint64_t gemv_need(const hl_tensor* t, hl_dtype x_dtype, uint32_t batch) {
+  Plan pl;
+  if (is_fp16(t)) {
+    if (x_dtype != HL_F16 || make_plan(t, 0, false, &pl) != HL_OK) return 0;
+  } else {
+    bool mfma = false, persistent = false;
+    uint32_t xw = 0;
+    if (x_dtype == HL_F16 || gemv_plan(t, x_dtype, batch, &pl, &mfma, &persistent, &xw) != HL_OK) return 0;
+    if (persistent) return xtile_region(t, batch);
+  }
+  uint32_t C = 0, KS = 0;
+  split_shape(pl, &C, &KS);
+  return xtile_region(t, batch) + split_bytes(pl, batch, KS);
+}
+
+extern "C" size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch) {
+  if (!t || t->seg_len == 0 || t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS || batch < 1 ||
+      batch > HL_MAX_BATCH)
+    return 0;
+  if (is_fp16(t)) return (size_t)gemv_need(t, HL_F16, batch);
+  return (size_t)std::max(gemv_need(t, HL_F32, batch), gemv_need(t, HL_BF16, batch));
+}
+
+static hl_status gemv_args_ok(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
+                              const float* y_dev) {
   if (!t || !x_dev || !y_dev || batch < 1 || batch > HL_MAX_BATCH ||
       (x_dtype != HL_F32 && x_dtype != HL_BF16 && x_dtype != HL_F16))
     return HL_EINVAL;
-  if (!aligned(x_dev, 16) || !aligned(y_dev, 4) || !aligned(workspace_dev, 16)) return HL_EINVAL;
-  if (t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS) return HL_EINVAL;
+  if (!aligned(x_dev, 16) || !aligned(y_dev, 4)) return HL_EINVAL;
+  if (t->grp_rows == 0 || t->grp_rows > HL_GROUP_SEGS || t->seg_len == 0) return HL_EINVAL;
   if (is_fp16(t) != (x_dtype == HL_F16)) return HL_EUNSUPPORTED;
-  if (is_fp16(t)) return gemv16(t, x_dev, batch, y_dev, workspace_dev, workspace_bytes, (hipStream_t)stream);
-  const bool xb = x_dtype == HL_BF16;
-  // 16-row groups with bf16 activations run on the matrix cores; the vector
-  // kernel stages raw bytes and the activation slice (GC*S columns per batch
-  // row) in LDS.
-  const bool mfma = xb && t->grp_rows == 16 && t->seg_len % 8 == 0 && mfma_steps_ok(t->seg_len / 8);
-  const uint32_t slice = (HL_GROUP_SEGS / t->grp_rows) * t->seg_len;
-  const uint32_t x_words = xb ? slice * batch / 2 : slice * batch;
+  return HL_OK;
+}
+
+// The product of hl_decode_gemv; `clear`: zero the split's arrival counters
+// first (the workspace may hold other bytes there).
+static hl_status gemv_impl(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch, float* y_dev,
+                           void* workspace_dev, size_t workspace_bytes, bool clear, hipStream_t stream) {
+  if (is_fp16(t)) return gemv16(t, x_dev, batch, y_dev, workspace_dev, workspace_bytes, clear, stream);
   Plan pl;
-  hl_status st = make_plan(t, mfma ? 0 : x_words, !mfma, &pl);
+  bool mfma = false, persistent = false;
+  uint32_t x_words = 0;
+  hl_status st = gemv_plan(t, x_dtype, batch, &pl, &mfma, &persistent, &x_words);
   if (st != HL_OK) return st;
+  const bool xb = x_dtype == HL_BF16;
   GemvArgs p;
   std::memset(&p, 0, sizeof(p));
   p.g = pl.ga;
@@ -2308,12 +2371,12 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   const uint32_t cus = (uint32_t)device_cus();
   bool xt = false;
   if (mfma) {
-    st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, (hipStream_t)stream, &p, &xt);
+    st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, stream, &p, &xt);
     if (st != HL_OK) return st;
   }
   // Persistent kernel: S = 32 or 64, at least one row block per CU and two
   // groups per wave.
-  if (mfma) {
+  if (persistent) {
     int jt = 0;
     uint32_t w = 0;
     size_t per_wave = 0;
@@ -2325,22 +2388,31 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
       sa.p = p;
       sa.n = 1;
       sa.part0[1] = std::min(RB, cus);
-      return launch_stream(xt, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64), w * per_wave,
-                           (hipStream_t)stream, sa);
+      return launch_stream(xt, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64), w * per_wave, stream,
+                           sa);
     }
   }
   // Column blocks per block and blocks per row block.
   uint32_t w = 0;
-  choose_split(t, pl, batch, workspace_dev, workspace_bytes, &p, &w);
+  st = choose_split(t, pl, batch, workspace_dev, workspace_bytes, clear, stream, &p, &w);
+  if (st != HL_OK) return st;
   const uint32_t KS = p.KS;
   const dim3 grid(RB * KS), block(w * 64);
   if (mfma) {
     // the reduction reuses the wave regions: 4 floats per lane per wave
     const size_t lds = std::max<size_t>(pl.lds_for(w), (size_t)w * 4 * 64 * 4);
-    return launch_mfma(xt, t->seg_len / 8, grid, block, lds, (hipStream_t)stream, p);
+    return launch_mfma(xt, t->seg_len / 8, grid, block, lds, stream, p);
   }
   const size_t lds = std::max<size_t>(pl.lds_for(w), (size_t)w * batch * 64 * 4);
-  HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, (hipStream_t)stream, p);
+  HL_BATCH_SWITCH(launch_gemv_b, batch, xb, grid, block, lds, stream, p);
+}
+
+extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
+                                    float* y_dev, void* workspace_dev, size_t workspace_bytes, void* stream) {
+  const hl_status st = gemv_args_ok(t, x_dev, x_dtype, batch, y_dev);
+  if (st != HL_OK) return st;
+  if (!aligned(workspace_dev, 16)) return HL_EINVAL;
+  return gemv_impl(t, x_dev, x_dtype, batch, y_dev, workspace_dev, workspace_bytes, false, (hipStream_t)stream);
 }
 
 extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const void* x_dev,
@@ -2378,9 +2450,14 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
     grouped = w >= 8 && pl[0].ga.CB >= w && rbs >= cus;
   }
   if (!grouped) {
+    // one product after another on the shared workspace: a split product
+    // zeroes its counters first (another matrix's product may have left
+    // partial sums where they lie)
     for (uint32_t k = 0; k < count; ++k) {
-      const hl_status st = hl_decode_gemv(ts[k], x_dev, x_dtype, batch, y_devs[k], workspace_dev, workspace_bytes,
-                                          stream);
+      hl_status st = gemv_args_ok(ts[k], x_dev, x_dtype, batch, y_devs[k]);
+      if (st == HL_OK)
+        st = gemv_impl(ts[k], x_dev, x_dtype, batch, y_devs[k], workspace_dev, workspace_bytes, count > 1,
+                       (hipStream_t)stream);
       if (st != HL_OK) return st;
     }
     return HL_OK;

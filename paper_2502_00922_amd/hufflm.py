@@ -81,7 +81,7 @@ EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_bui
            "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
            "hl_decode_gemv", "hl_decode_gemv_multi", "hl_gemm_workspace_bytes", "hl_decode_gemm",
-           "hl_gemv_bf16", "hl_read_probe_blocks", "hl_read_probe"]
+           "hl_gemv_bf16"]
 
 
 def lib() -> ctypes.CDLL:
@@ -135,10 +135,6 @@ def lib() -> ctypes.CDLL:
     L.hl_decode_gemm.restype = c.c_int
     L.hl_decode_gemm.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                  c.c_void_p, c.c_size_t, c.c_void_p]
-    L.hl_read_probe_blocks.restype = c.c_uint32
-    L.hl_read_probe_blocks.argtypes = []
-    L.hl_read_probe.restype = c.c_int
-    L.hl_read_probe.argtypes = [c.c_void_p, c.c_size_t, c.c_void_p, c.c_void_p]
     L.hl_gemv_bf16.restype = c.c_int
     L.hl_gemv_bf16.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.c_void_p, c.c_int, c.c_uint32,
                                c.c_void_p, c.c_void_p]
@@ -227,6 +223,60 @@ def _stream_ptr(stream=None):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def _dev_arg(t, name: str, dtypes=None, shape=None, numel: int = 0):
+    """Checks a device buffer's dtype, shape (or at least `numel` elements)
+    and contiguity before it reaches a kernel. The C ABI takes no sizes for
+    these buffers, so a wrong one would be read or written out of bounds on
+    the device; raises ValueError instead."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise ValueError(f"{name}: dtype {t.dtype} not in {tuple(dtypes)}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {numel} needed")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _on_device(device, **bufs):
+    """Every given buffer lives on `device`, a GPU (else ValueError): a host
+    pointer would reach the kernel as a device address."""
+    for name, t in bufs.items():
+        if t is None or t is False:
+            continue
+        if not t.is_cuda or (device is not None and t.device != device):
+            raise ValueError(f"{name} must be on {device if device is not None else 'the GPU'}, not {t.device}")
+
+
+def _x_dtype(x):
+    import torch
+    dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16, torch.float16: HL_F16}.get(x.dtype)
+    if dt is None:
+        raise ValueError("x must be float32, bfloat16 or float16")
+    return dt
+
+
+def _check_x(x, K: int):
+    """x as a [batch, K] tensor of a supported dtype, batch in 1..16."""
+    import torch
+    if x.dim() == 1:
+        x = x.unsqueeze(0)
+    if x.dim() != 2 or x.shape[1] != K or not 1 <= x.shape[0] <= MAX_BATCH:
+        raise ValueError(f"x must be [batch <= {MAX_BATCH}, {K}], got {tuple(x.shape)}")
+    _dev_arg(x, "x", (torch.float32, torch.bfloat16, torch.float16))
+    return x
+
+
+def _check_ws(ws):
+    if ws is False or ws is None:
+        return ws
+    return _dev_arg(ws, "workspace")
+
+
 class DeviceTensor:
     """A container resident in device memory plus its decode table."""
 
@@ -266,6 +316,8 @@ class DeviceTensor:
         R, K = self.shape
         if out is None:
             out = torch.empty((R, K), dtype=torch.int16, device=self.blob.device)
+        _dev_arg(out, "out", (torch.int16, torch.bfloat16, torch.float16), numel=R * K)
+        _on_device(self.blob.device, out=out)
         _check(lib().hl_decode(ctypes.byref(self.view), ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)),
                "hl_decode")
         return out
@@ -287,19 +339,18 @@ class DeviceTensor:
         pass False to run without one."""
         import torch
         R, K = self.shape
-        if x.dim() == 1:
-            x = x.unsqueeze(0)
-        if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous():
-            raise ValueError("x must be a contiguous [batch, cols] tensor")
-        dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16, torch.float16: HL_F16}.get(x.dtype)
-        if dt is None:
-            raise ValueError("x must be float32, bfloat16 or float16")
+        dev = self.blob.device
+        x = _check_x(x, K)
+        dt = _x_dtype(x)
         if y is None:
             y = torch.empty((x.shape[0], R), dtype=torch.float32, device=x.device)
+        _dev_arg(y, "y", (torch.float32,), numel=x.shape[0] * R)
+        _check_ws(workspace)
+        _on_device(dev, x=x, y=y, workspace=workspace)
         if workspace is None:
             workspace = self.workspace()
         ws_ptr, ws_n = (None, 0) if workspace is False else (ctypes.c_void_p(workspace.data_ptr()),
-                                                              workspace.numel())
+                                                              workspace.numel() * workspace.element_size())
         _check(lib().hl_decode_gemv(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
                                     ctypes.c_void_p(y.data_ptr()), ws_ptr, ws_n, _stream_ptr(stream)),
                "hl_decode_gemv")
@@ -310,11 +361,15 @@ class DeviceTensor:
         Uses a cached zeroed workspace owned by the tensor, grown as needed."""
         import torch
         R, K = self.shape
-        if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous() or x.dtype != torch.bfloat16:
-            raise ValueError("x must be a contiguous [tokens, cols] bfloat16 tensor")
+        dev = self.blob.device
+        if x.dim() != 2 or x.shape[1] != K or x.shape[0] < 1:
+            raise ValueError(f"x must be [tokens, {K}], got {tuple(x.shape)}")
+        _dev_arg(x, "x", (torch.bfloat16,))
         T = x.shape[0]
         if y is None:
             y = torch.empty((T, R), dtype=torch.float32, device=x.device)
+        _dev_arg(y, "y", (torch.float32,), numel=T * R)
+        _on_device(dev, x=x, y=y)
         need = int(lib().hl_gemm_workspace_bytes(ctypes.byref(self.view), T))
         ws = getattr(self, "_gemm_ws", None)
         if ws is None or ws.numel() < need:
@@ -336,18 +391,23 @@ def gemv_multi(tensors, x, ys=None, stream=None, workspace=None):
     if not 1 <= len(tensors) <= 4:
         raise ValueError("one to four tensors")
     K = tensors[0].shape[1]
-    if x.dim() == 1:
-        x = x.unsqueeze(0)
-    if x.dim() != 2 or x.shape[1] != K or not x.is_contiguous():
-        raise ValueError("x must be a contiguous [batch, cols] tensor")
-    dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16, torch.float16: HL_F16}.get(x.dtype)
-    if dt is None:
-        raise ValueError("x must be float32, bfloat16 or float16")
+    dev = tensors[0].blob.device
+    if any(t.shape[1] != K or t.blob.device != dev for t in tensors):
+        raise ValueError("the tensors must have the same columns and device")
+    x = _check_x(x, K)
+    dt = _x_dtype(x)
     if ys is None:
         ys = [torch.empty((x.shape[0], t.shape[0]), dtype=torch.float32, device=x.device) for t in tensors]
+    if len(ys) != len(tensors):
+        raise ValueError("one output per tensor")
+    for m, (t, y) in enumerate(zip(tensors, ys)):
+        _dev_arg(y, f"ys[{m}]", (torch.float32,), numel=x.shape[0] * t.shape[0])
+    _check_ws(workspace)
+    _on_device(dev, x=x, workspace=workspace, **{f"ys[{m}]": y for m, y in enumerate(ys)})
     if workspace is None:
         workspace = max((t.workspace() for t in tensors), key=lambda w: w.numel())
-    ws_ptr, ws_n = (None, 0) if workspace is False else (ctypes.c_void_p(workspace.data_ptr()), workspace.numel())
+    ws_ptr, ws_n = (None, 0) if workspace is False else (ctypes.c_void_p(workspace.data_ptr()),
+                                                          workspace.numel() * workspace.element_size())
     views = (ctypes.POINTER(TensorView) * len(tensors))(*[ctypes.pointer(t.view) for t in tensors])
     outs = (ctypes.c_void_p * len(tensors))(*[y.data_ptr() for y in ys])
     _check(lib().hl_decode_gemv_multi(ctypes.cast(views, ctypes.c_void_p), len(tensors),
@@ -357,25 +417,21 @@ def gemv_multi(tensors, x, ys=None, stream=None, workspace=None):
     return ys
 
 
-def read_probe(buf, out=None, stream=None):
-    """Reads the device tensor ``buf`` once (a streaming-read probe of HBM)."""
-    import torch
-    if out is None:
-        out = torch.empty(int(lib().hl_read_probe_blocks()), dtype=torch.int32, device=buf.device)
-    _check(lib().hl_read_probe(ctypes.c_void_p(buf.data_ptr()), buf.numel() * buf.element_size(),
-                               ctypes.c_void_p(out.data_ptr()), _stream_ptr(stream)), "hl_read_probe")
-    return out
-
-
 def gemv_bf16(w, x, y=None, stream=None):
     """Uncompressed comparator: w [rows, cols] bf16 (or int16 bits) on the device."""
     import torch
+    if w.dim() != 2:
+        raise ValueError("w must be [rows, cols]")
     R, K = w.shape
-    if x.dim() == 1:
-        x = x.unsqueeze(0)
-    dt = {torch.float32: HL_F32, torch.bfloat16: HL_BF16}[x.dtype]
+    _dev_arg(w, "w", (torch.bfloat16, torch.int16))
+    x = _check_x(x, K)
+    if x.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("x must be float32 or bfloat16")
+    dt = _x_dtype(x)
     if y is None:
         y = torch.empty((x.shape[0], R), dtype=torch.float32, device=x.device)
+    _dev_arg(y, "y", (torch.float32,), numel=x.shape[0] * R)
+    _on_device(w.device if w.is_cuda else None, w=w, x=x, y=y)
     _check(lib().hl_gemv_bf16(ctypes.c_void_p(w.data_ptr()), R, K, ctypes.c_void_p(x.data_ptr()), dt,
                               x.shape[0], ctypes.c_void_p(y.data_ptr()), _stream_ptr(stream)), "hl_gemv_bf16")
     return y

@@ -65,7 +65,15 @@ def test_grouped_gemv_errors(torch):
     a = hl.DeviceTensor(hl.encode(random_bf16((64, 512), seed=1)))
     b = hl.DeviceTensor(hl.encode(random_bf16((64, 1024), seed=2)))
     x = torch.zeros((1, 512), dtype=torch.bfloat16, device="cuda")
-    with pytest.raises(hl.HLError):
-        hl.gemv_multi([a, b], x)  # different column counts
+    with pytest.raises(ValueError):
+        hl.gemv_multi([a, b], x)  # different column counts: the binding refuses them
+    # ... and so does the library, through the C ABI
+    import ctypes
+    y = [torch.empty((1, 64), dtype=torch.float32, device="cuda") for _ in range(2)]
+    views = (ctypes.POINTER(hl.TensorView) * 2)(ctypes.pointer(a.view), ctypes.pointer(b.view))
+    outs = (ctypes.c_void_p * 2)(y[0].data_ptr(), y[1].data_ptr())
+    assert hl.lib().hl_decode_gemv_multi(ctypes.cast(views, ctypes.c_void_p), 2, ctypes.c_void_p(x.data_ptr()),
+                                         hl.HL_BF16, 1, ctypes.cast(outs, ctypes.c_void_p), None, 0,
+                                         None) == hl.HL_EINVAL
     with pytest.raises(ValueError):
         hl.gemv_multi([a] * 5, x)

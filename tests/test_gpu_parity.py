@@ -148,8 +148,13 @@ def test_bf16_comparator(torch, xdt):
 def test_errors_are_reported(torch):
     w = random_bf16((64, 128), seed=1)
     dt = hl.DeviceTensor(hl.encode(w, seg_len=128))
-    with pytest.raises(hl.HLError):
-        dt.gemv(torch.zeros((17, 128), dtype=torch.bfloat16, device="cuda"))
+    x17 = torch.zeros((17, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):
+        dt.gemv(x17)  # batch above 16: the binding refuses it, and so does the library
+    import ctypes
+    y = torch.empty((17, 64), dtype=torch.float32, device="cuda")
+    assert hl.lib().hl_decode_gemv(ctypes.byref(dt.view), ctypes.c_void_p(x17.data_ptr()), hl.HL_BF16, 17,
+                                   ctypes.c_void_p(y.data_ptr()), None, 0, None) == hl.HL_EINVAL
     with pytest.raises(ValueError):
         dt.gemv(torch.zeros((1, 64), dtype=torch.bfloat16, device="cuda"))
 
@@ -187,16 +192,3 @@ def test_device_copy(torch):
     torch.cuda.synchronize()
     assert np.array_equal(cp.gemv(x).cpu().numpy(), y0)
     assert np.array_equal(_decode(torch, cp), w)
-
-
-def test_read_probe(torch):
-    # the streaming-read probe reads every word once: the XOR of its per-block
-    # words is the XOR of the buffer
-    print("read probe", flush=True)
-    rng = np.random.default_rng(3)
-    words = rng.integers(0, 1 << 32, (1 << 20) + 12, dtype=np.uint64).astype(np.uint32)
-    buf = torch.from_numpy(words.view(np.int32)).cuda()
-    out = hl.read_probe(buf)
-    torch.cuda.synchronize()
-    got = np.bitwise_xor.reduce(out.cpu().numpy().view(np.uint32))
-    assert int(got) == int(np.bitwise_xor.reduce(words))

@@ -322,3 +322,67 @@ def test_fp16_validate_rejects_damage():
     assert hl.validate(damaged(93, 1)) == hl.HL_ECORRUPT                  # header bytes 92..127
     assert hl.validate(damaged(h["off_seg_bits"], 0xFFFF, 2)) == hl.HL_ECORRUPT
     assert hl.validate(damaged(7, 0)) == hl.HL_ECORRUPT                   # split header over the body
+
+
+def test_view_rejects_misaligned_blob_and_table(L):
+    # containers packed back to back may leave a blob 8 bytes off a 16-byte
+    # boundary; the kernels copy blob and table in 16-byte pieces
+    import ctypes
+    w = random_bf16((16, 256), seed=3)
+    blob = hl.encode(w, seg_len=64)
+    t = hl.TensorView()
+    good, bad = ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10008)
+    assert L.hl_tensor_view(bad, blob.ctypes.data, blob.size, good, ctypes.byref(t)) == hl.HL_EINVAL
+    assert L.hl_tensor_view(good, blob.ctypes.data, blob.size, bad, ctypes.byref(t)) == hl.HL_EINVAL
+    assert L.hl_tensor_view(good, blob.ctypes.data, blob.size, good, ctypes.byref(t)) == hl.HL_OK
+
+
+def _fake_tensor(rows, cols):
+    # a view with shape only and a blob on the meta device: every check below
+    # must raise before any library call could reach a kernel
+    import torch
+    dt = hl.DeviceTensor.__new__(hl.DeviceTensor)
+    dt.view = hl.TensorView()
+    dt.view.rows, dt.view.cols = rows, cols
+    dt.blob = torch.empty(16, dtype=torch.uint8, device="meta")
+    return dt
+
+
+def test_binding_rejects_bad_buffers_before_launch():
+    import torch
+    dt = _fake_tensor(64, 128)
+    x = torch.zeros((2, 128), dtype=torch.bfloat16)
+    y = torch.zeros((2, 64), dtype=torch.float32)
+    bad = [
+        dict(x=torch.zeros((2, 127), dtype=torch.bfloat16)),             # wrong columns
+        dict(x=torch.zeros((17, 128), dtype=torch.bfloat16)),            # batch above 16
+        dict(x=torch.zeros((2, 128), dtype=torch.int32)),                # wrong dtype
+        dict(x=torch.zeros((128, 2), dtype=torch.bfloat16).t()),         # not contiguous
+        dict(y=torch.zeros((2, 63), dtype=torch.float32)),               # output too small
+        dict(y=torch.zeros((2, 64), dtype=torch.float64)),               # output dtype
+        dict(),                                                          # host tensors
+    ]
+    for kw in bad:
+        args = dict(x=x, y=y)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            dt.gemv(args["x"], args["y"], workspace=False)
+        with pytest.raises(ValueError):
+            hl.gemv_multi([dt], args["x"], [args["y"]], workspace=False)
+    with pytest.raises(ValueError):
+        dt.decode(out=torch.zeros((64, 127), dtype=torch.int16))
+    with pytest.raises(ValueError):
+        dt.decode(out=torch.zeros((64, 128), dtype=torch.float32))
+    with pytest.raises(ValueError):
+        dt.decode(out=torch.zeros((64, 128), dtype=torch.int16))  # host
+    with pytest.raises(ValueError):
+        dt.gemm(torch.zeros((5, 128), dtype=torch.float32))
+    with pytest.raises(ValueError):
+        dt.gemm(torch.zeros((5, 128), dtype=torch.bfloat16), torch.zeros((5, 10), dtype=torch.float32))
+    w = torch.zeros((64, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        hl.gemv_bf16(w, torch.zeros((1, 100), dtype=torch.bfloat16))
+    with pytest.raises(ValueError):
+        hl.gemv_bf16(w.float(), x)
+    with pytest.raises(ValueError):
+        hl.gemv_bf16(w, x, y)  # host tensors
