@@ -128,6 +128,7 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1, HL_F16 = 2 } hl_dtype;
 #define HL_CB16_BYTES 128u    /* float16 code tables after the header */
 #define HL_LMAX16_MIN 5u
 #define HL_LMAX16_MAX 12u
+#define HL_NOALLOC_SCRATCH_BYTES (4u << 20)  /* scratch of hl_decode_gemv_noalloc, per GPU */
 
 typedef enum { HL_FORMAT_SPLIT = 0, HL_FORMAT_WHOLE_EXPONENT = 1, HL_FORMAT_FP16 = 2 } hl_format;
 
@@ -288,6 +289,22 @@ size_t hl_gemv_workspace_bytes(const hl_tensor* t, uint32_t batch);
 hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype,
                          uint32_t batch, float* y_dev, void* workspace_dev,
                          size_t workspace_bytes, void* stream);
+
+/* hl_decode_gemv without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops that
+ * forbid allocation): the tiled activations and partial sums go to a scratch
+ * array of HL_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it
+ * runs on until the process ends (its address is looked up on the first call
+ * on a GPU). No device memory is allocated or freed. The arrival counters a
+ * split product uses are zeroed by a small kernel on `stream` before it (no
+ * memset). Every call on one GPU shares that GPU's scratch: calls that overlap
+ * on one GPU (other streams, other host threads) race and give wrong results.
+ * Arguments and results as hl_decode_gemv; the same kernels run, so outputs
+ * equal hl_decode_gemv's bit for bit. Errors: those of hl_decode_gemv, and
+ * HL_EUNSUPPORTED when the product would need more than
+ * HL_NOALLOC_SCRATCH_BYTES of scratch. */
+hl_status hl_decode_gemv_noalloc(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype,
+                                 uint32_t batch, float* y_dev, void* stream);
 
 /* The products of up to 4 matrices that share x, y_devs[m][b][r] =
  * sum_k W_m[r][k] * x[b][k] (a decode step's q, k and v projections, or its

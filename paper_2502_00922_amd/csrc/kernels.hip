@@ -27,6 +27,7 @@
 #include <algorithm>
 #include <type_traits>
 #include <cstring>
+#include <mutex>
 
 #include "hl_internal.h"
 #include "hufflm.h"
@@ -2413,6 +2414,45 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   if (st != HL_OK) return st;
   if (!aligned(workspace_dev, 16)) return HL_EINVAL;
   return gemv_impl(t, x_dev, x_dtype, batch, y_dev, workspace_dev, workspace_bytes, false, (hipStream_t)stream);
+}
+
+// ------------------------------------------------------------------ allocation-free product
+
+// Scratch memory of hl_decode_gemv_noalloc: one array per GPU the library
+// runs on, held until the process ends. In host code `scratch` is a
+// stand-in, not a device address: the address of a GPU's copy comes from
+// hipGetSymbolAddress (with that GPU current) and is what the kernels get.
+static __device__ __align__(256) uint8_t scratch[HL_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch[kMaxDevices];
+
+// The current GPU's scratch address, looked up once per GPU.
+static hl_status scratch_address(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return HL_EHIP;
+  if (dev >= kMaxDevices) return HL_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return HL_EHIP;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return HL_OK;
+}
+
+extern "C" hl_status hl_decode_gemv_noalloc(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch,
+                                            float* y_dev, void* stream) {
+  hl_status st = gemv_args_ok(t, x_dev, x_dtype, batch, y_dev);
+  if (st != HL_OK) return st;
+  const uint64_t need = gemv_need(t, x_dtype, batch);
+  if (need > HL_NOALLOC_SCRATCH_BYTES) return HL_EUNSUPPORTED;
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != HL_OK) return st;
+  return gemv_impl(t, x_dev, x_dtype, batch, y_dev, ws, HL_NOALLOC_SCRATCH_BYTES, true, (hipStream_t)stream);
 }
 
 extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const void* x_dev,

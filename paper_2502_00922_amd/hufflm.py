@@ -80,7 +80,7 @@ _lib = None
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
            "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
-           "hl_decode_gemv", "hl_decode_gemv_multi", "hl_gemm_workspace_bytes", "hl_decode_gemm",
+           "hl_decode_gemv", "hl_decode_gemv_noalloc", "hl_decode_gemv_multi", "hl_gemm_workspace_bytes", "hl_decode_gemm",
            "hl_gemv_bf16"]
 
 
@@ -127,6 +127,9 @@ def lib() -> ctypes.CDLL:
     L.hl_decode_gemv.restype = c.c_int
     L.hl_decode_gemv.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                  c.c_void_p, c.c_size_t, c.c_void_p]
+    L.hl_decode_gemv_noalloc.restype = c.c_int
+    L.hl_decode_gemv_noalloc.argtypes = [c.POINTER(TensorView), c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
+                                         c.c_void_p]
     L.hl_decode_gemv_multi.restype = c.c_int
     L.hl_decode_gemv_multi.argtypes = [c.c_void_p, c.c_uint32, c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                        c.c_void_p, c.c_size_t, c.c_void_p]
@@ -354,6 +357,19 @@ class DeviceTensor:
         _check(lib().hl_decode_gemv(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
                                     ctypes.c_void_p(y.data_ptr()), ws_ptr, ws_n, _stream_ptr(stream)),
                "hl_decode_gemv")
+        return y
+
+    def gemv_noalloc(self, x, y, stream=None):
+        """The product of gemv without a workspace (hl_decode_gemv_noalloc):
+        the library's per-GPU scratch holds the partial sums. y must be given."""
+        import torch
+        R, K = self.shape
+        x = _check_x(x, K)
+        _dev_arg(y, "y", (torch.float32,), numel=x.shape[0] * R)
+        _on_device(self.blob.device, x=x, y=y)
+        _check(lib().hl_decode_gemv_noalloc(ctypes.byref(self.view), ctypes.c_void_p(x.data_ptr()), _x_dtype(x),
+                                            x.shape[0], ctypes.c_void_p(y.data_ptr()), _stream_ptr(stream)),
+               "hl_decode_gemv_noalloc")
         return y
 
     def gemm(self, x, y=None, stream=None):

@@ -55,6 +55,7 @@ def test_misaligned_pointers_rejected_before_device_work(L):
     ys = (ctypes.c_void_p * 1)(0x10000)
     assert L.hl_decode_gemv_multi(ctypes.cast(ts, ctypes.c_void_p), 1, bad, hl.HL_BF16, 1,
                                   ctypes.cast(ys, ctypes.c_void_p), None, 0, None) == hl.HL_EINVAL
+    assert L.hl_decode_gemv_noalloc(ctypes.byref(t), bad, hl.HL_BF16, 1, good, None) == hl.HL_EINVAL
 
 
 def _codebook_lists(cb):
@@ -369,6 +370,8 @@ def test_binding_rejects_bad_buffers_before_launch():
             dt.gemv(args["x"], args["y"], workspace=False)
         with pytest.raises(ValueError):
             hl.gemv_multi([dt], args["x"], [args["y"]], workspace=False)
+        with pytest.raises(ValueError):
+            dt.gemv_noalloc(args["x"], args["y"])
     with pytest.raises(ValueError):
         dt.decode(out=torch.zeros((64, 127), dtype=torch.int16))
     with pytest.raises(ValueError):
