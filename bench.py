@@ -87,6 +87,13 @@ def parse():
                     help="container format of the --counter-run matrix and of the 4096x4096 detail's first entry")
     ap.add_argument("--no-variant", action="store_true", help="skip timing the other container formats")
     ap.add_argument("--no-prefill", action="store_true", help="skip timing the prefill decode-GEMM")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("TRACE_DIR", "BENCH_LOG"),
+                    help="print the profile summary of a rocprofv3 --kernel-trace --stats run of the headline "
+                         "(run_kernel_stats.csv and run_kernel_trace.csv in TRACE_DIR; the run's JSON line in "
+                         "BENCH_LOG) and exit; no GPU needed")
+    ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "RUN_LOG"),
+                    help="print the HBM-traffic summary of two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) of "
+                         "--traffic-run and exit; no GPU needed")
     return ap.parse_args()
 
 
@@ -660,8 +667,115 @@ def traffic_run(torch, hl):
                       "container_bytes": st["comp"], "copy_bytes": COPY_BYTES, "copies": 10}), flush=True)
 
 
+def _csv_rows(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def _json_line(path, key):
+    for line in open(path):
+        line = line.strip()
+        if line.startswith("{") and key in line:
+            return json.loads(line)
+    raise SystemExit(f"no JSON line with {key} in {path}")
+
+
+def summarize_trace(trace_dir, bench_log):
+    """Profile summary of the headline under rocprofv3 --kernel-trace --stats:
+    the per-kernel statistics, and from the per-dispatch trace the timed graph
+    of grouped token steps (the launches after the first call and the warm-up
+    graph): the fused kernels' summed durations per step against the
+    benchmark's own per-step time."""
+    d = _json_line(bench_log, '"metric"')
+    st = d["detail"]["stack70b"]
+    layers, steps, warmup = st["layers"], d["steps"], d["warmup"]
+    per_step = st["launches_per_step"]
+    out = ["Kernel statistics (run_kernel_stats.csv, durations in ns):",
+           f"{'Name':78s} {'Calls':>7s} {'AverageNs':>11s} {'MinNs':>9s} {'MaxNs':>9s}"]
+    for r in _csv_rows(os.path.join(trace_dir, "run_kernel_stats.csv")):
+        n = r["Name"] if len(r["Name"]) <= 78 else r["Name"][:75] + "..."
+        out.append(f"{n:78s} {int(r['Calls']):7d} {float(r['AverageNs']):11.1f} {int(float(r['MinNs'])):9d} "
+                   f"{int(float(r['MaxNs'])):9d}")
+    disp = [r for r in _csv_rows(os.path.join(trace_dir, "run_kernel_trace.csv"))
+            if "gemv_stream_kernel" in r["Kernel_Name"]]
+    disp.sort(key=lambda r: int(r["Start_Timestamp"]))
+    first = per_step * (1 + warmup)
+    timed = disp[first:first + per_step * steps]
+    if len(timed) != per_step * steps:
+        raise SystemExit(f"expected {per_step * steps} timed dispatches, found {len(timed)}")
+    dur = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in timed]
+    span = int(timed[-1]["End_Timestamp"]) - int(timed[0]["Start_Timestamp"])
+    names = {}
+    for r, t in zip(timed, dur):
+        k = r["Kernel_Name"].split("(")[0]
+        c, tot = names.get(k, (0, 0))
+        names[k] = (c + 1, tot + t)
+    alg = d["roofline"]["achieved"] * d["ms_per_step"] * 1e-3 * 1e9
+    ksum = sum(dur) / steps
+    out += ["", f"Timed graph of the headline: {steps} token steps x {per_step} launches = {len(timed)} dispatches "
+            f"(after {per_step} launches outside the graph and a warm-up graph of {warmup} steps):"]
+    for k, (c, tot) in sorted(names.items()):
+        out.append(f"  {k}: {c} dispatches, average {tot / c / 1e3:.2f} us")
+    out += [f"  fused-kernel time per step (sum of dispatch durations / steps): {ksum / 1e6:.4f} ms",
+            f"  first start to last end / steps: {span / steps / 1e6:.4f} ms "
+            f"(the benchmark's events: {d['ms_per_step']} ms per step)",
+            f"  algorithmic bytes per step (containers + x + y of all launches): {alg / 1e9:.3f} GB",
+            f"  -> from the summed kernel time: {alg / (ksum * 1e-9) / 1e9:.1f} GB/s "
+            f"({alg / (ksum * 1e-9) / 1e9 / HBM_PEAK_GBS:.4f} of 8 TB/s); the benchmark's line: "
+            f"{d['roofline']['achieved']} GB/s ({d['roofline']['frac']})",
+            f"  average fused dispatch: {sum(dur) / len(dur) / 1e3:.2f} us for {alg / per_step / 1e6:.2f} MB "
+            f"of algorithmic bytes",
+            f"kernel source sha256[:16]: {kernel_hash()}"]
+    print("\n".join(out))
+
+
+def summarize_traffic(fetch_dir, write_dir, run_log):
+    """HBM traffic of the fused kernels from two rocprofv3 --pmc passes of
+    --traffic-run: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the fused
+    kernels, each scaled by what the same counter reads for the run's plain
+    256 MiB device copies (the last 10 copy dispatches), per layer of the
+    stack (one grouped token step over one layer = 4 launches)."""
+    t = _json_line(run_log, '"traffic_run"')
+
+    def load(d):
+        rows = [r for f in sorted(os.listdir(d)) if f.endswith("counter_collection.csv")
+                for r in _csv_rows(os.path.join(d, f))]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        fused = [float(r["Counter_Value"]) for r in rows if "gemv_stream_kernel" in r["Kernel_Name"]]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]][-10:]
+        return fused, copies
+
+    ff, fc = load(fetch_dir)
+    wf, wc = load(write_dir)
+    n = t["launches_per_step"] * t["steps"]
+    if len(ff) != n or len(wf) != n or len(fc) != 10 or len(wc) != 10:
+        raise SystemExit(f"unexpected dispatch counts: fused {len(ff)}/{len(wf)} (expected {n}), copies {len(fc)}/{len(wc)}")
+    rcal = t["copy_bytes"] / (sum(fc) / 10 * 1024)
+    wcal = t["copy_bytes"] / (sum(wc) / 10 * 1024)
+    layers_steps = t["layers"] * t["steps"]
+    read = sum(ff) * 1024 * rcal / layers_steps
+    write = sum(wf) * 1024 * wcal / layers_steps
+    alg = t["alg_bytes_per_layer"]
+    print("\n".join([
+        f"Fused kernels of {t['steps']} grouped token steps over a {t['layers']}-layer stack ({n} dispatches); "
+        f"10 device copies of {t['copy_bytes']} bytes as calibration.",
+        f"FETCH_SIZE calibration: copy reads {sum(fc) / 10:.0f} KiB per dispatch -> factor {rcal:.4f}",
+        f"WRITE_SIZE calibration: copy writes {sum(wc) / 10:.0f} KiB per dispatch -> factor {wcal:.4f}",
+        f"per layer (4 launches): read {read:.0f} B, written {write:.0f} B, algorithmic {alg} B",
+        f"traffic / algorithmic bytes: {(read + write) / alg:.4f}",
+        f"traffic_bytes_per_layer: {int(round(read + write))}",
+        f"kernel source sha256[:16]: {t['kernel_sha256_16']}"]))
+
+
 def main():
     args = parse()
+    if args.summarize_trace:
+        summarize_trace(*args.summarize_trace)
+        return
+    if args.summarize_traffic:
+        summarize_traffic(*args.summarize_traffic)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the sharded layout is described in the design notes)", file=sys.stderr)
