@@ -24,7 +24,9 @@
  * (weight, symbol); lmax-1 rounds of pairing consecutive items and stable
  * merging with the leaves by (weight, kind); the first 2(n-1) items of the
  * last list are taken; length = occurrences). A field with one present
- * symbol has length 0 and emits no bits. Code values are canonical (RFC 1951
+ * symbol has length 0 and emits no bits. With a joint limit pair_max (see
+ * hl_build_codebook) the two fields' limits are a and min(lmax, pair_max - a)
+ * for the a of least total code length. Code values are canonical (RFC 1951
  * Sec. 3.2.2 assignment).
  *
  * Tiling: segment (r, cs) is W[r][cs*S .. cs*S+S) (S divides cols, S % 8 == 0,
@@ -128,6 +130,7 @@ typedef enum { HL_F32 = 0, HL_BF16 = 1, HL_F16 = 2 } hl_dtype;
 #define HL_CB16_BYTES 128u    /* float16 code tables after the header */
 #define HL_LMAX16_MIN 5u
 #define HL_LMAX16_MAX 12u
+#define HL_PAIR_MAX 11u       /* the fused kernel's table window: pairs of codes up to it take the fast form */
 #define HL_NOALLOC_SCRATCH_BYTES (4u << 20)  /* scratch of hl_decode_gemv_noalloc, per GPU */
 
 typedef enum { HL_FORMAT_SPLIT = 0, HL_FORMAT_WHOLE_EXPONENT = 1, HL_FORMAT_FP16 = 2 } hl_format;
@@ -192,10 +195,18 @@ const char* hl_status_str(hl_status s);
 uint32_t hl_default_seg_len(uint64_t cols);
 
 /* Per-matrix codebooks of the two exponent fields (Sec. 5.1) from n bf16
- * bit patterns. lmax in [4, 15] (12 matches the maximum code length the paper
- * reports, Sec. 5.2). Errors: HL_EINVAL for n == 0, null pointers or lmax out
- * of range. */
-hl_status hl_build_codebook(const uint16_t* w_bf16, size_t n, uint32_t lmax,
+ * bit patterns. Each code is limited to lmax bits, lmax in [4, 15] (12
+ * matches the maximum code length the paper reports, Sec. 5.2). With
+ * pair_max > 0 the longest eh code plus the longest el code is also at most
+ * pair_max bits, so that one window of pair_max bits holds every weight's two
+ * codes (the decoder's window match of Sec. 3.2 applied to the pair one
+ * table lookup decodes): among the splits a + (pair_max - a) of the limit,
+ * a = 0 .. lmax, the codes of least total length (each the length-limited
+ * optimum for its limit), the smallest a on a tie. 11 is the fused kernel's
+ * table window (HL_PAIR_MAX); 0 = no joint limit. Errors: HL_EINVAL for
+ * n == 0, null pointers, lmax out of range, pair_max above 30 or too small
+ * for the alphabets. */
+hl_status hl_build_codebook(const uint16_t* w_bf16, size_t n, uint32_t lmax, uint32_t pair_max,
                             hl_codebook* out);
 
 /* Group rows the encoder uses when asked for 0: 16 (16 rows x 4 segments)

@@ -218,6 +218,50 @@ def limited_lengths(freqs: Sequence[int], lmax: int) -> List[int]:
     return package_merge_lengths(freqs, lmax)
 
 
+def min_limit(freqs: Sequence[int]) -> int:
+    """Smallest length limit a prefix code of the present symbols can meet:
+    0 for one symbol (no bits), else ceil(log2(count))."""
+    n = sum(1 for f in freqs if f > 0)
+    return 0 if n <= 1 else (n - 1).bit_length()
+
+
+def code_cost(freqs: Sequence[int], lengths: Sequence[int]) -> int:
+    """Total code bits: sum of frequency times length."""
+    return sum(f * l for f, l in zip(freqs, lengths))
+
+
+def pair_limited_lengths(feh: Sequence[int], fel: Sequence[int], lmax: int,
+                         pair_max: int) -> Tuple[List[int], List[int]]:
+    """Lengths of the two exponent codes of the split format: each code at
+    most lmax bits long and, with pair_max > 0, the longest eh code plus the
+    longest el code at most pair_max bits, so that every weight's two codes
+    fit one decoder window of pair_max bits (the window match of Sec. 3.2,
+    applied to the pair that one table lookup decodes).
+
+    Any pair of codes meeting the joint limit has some longest eh code a, so
+    its cost is at least that of the optimal codes limited to a and to
+    pair_max - a (each length-limited optimum by the rule of limited_lengths).
+    The result is therefore the cheapest of those splits, a = 0 .. lmax; on
+    equal cost the smallest a. pair_max = 0: each code limited to lmax only."""
+    if not pair_max:
+        return limited_lengths(feh, lmax), limited_lengths(fel, lmax)
+    best = None
+    for a in range(0, lmax + 1):
+        b = min(lmax, pair_max - a)
+        if b < min_limit(fel):
+            break
+        if a < min_limit(feh):
+            continue
+        le = limited_lengths(feh, a) if a else [0] * len(feh)
+        ll = limited_lengths(fel, b) if b else [0] * len(fel)
+        cost = code_cost(feh, le) + code_cost(fel, ll)
+        if best is None or cost < best[0]:
+            best = (cost, le, ll)
+    if best is None:
+        raise ValueError("pair limit too small for the alphabets")
+    return best[1], best[2]
+
+
 def canonical_codes(lengths: Sequence[int]) -> List[int]:
     """Canonical code values (RFC 1951 Sec. 3.2.2): shorter codes first, equal
     lengths in increasing symbol order. Entries with length 0 get code 0."""
@@ -258,8 +302,12 @@ class FieldCode:
 
     @classmethod
     def from_freqs(cls, freqs: Sequence[int], lmax: int) -> "FieldCode":
+        return cls.from_lengths(limited_lengths(freqs, lmax), freqs)
+
+    @classmethod
+    def from_lengths(cls, lengths: Sequence[int], freqs: Sequence[int]) -> "FieldCode":
         present = [s for s, f in enumerate(freqs) if f > 0]
-        return cls(limited_lengths(freqs, lmax), len(present), present[0] if len(present) == 1 else 0)
+        return cls(lengths, len(present), present[0] if len(present) == 1 else 0)
 
     def decode_one(self, bits: List[int], pos: int) -> Tuple[int, int]:
         """Read one code MSB-first starting at bit ``pos``; returns (symbol, new pos)."""
@@ -398,10 +446,16 @@ def sign_plane(w: np.ndarray, seg_len: int, grp_rows: int) -> np.ndarray:
     return plane
 
 
-def build_codebooks(w: np.ndarray, lmax: int = 12) -> Tuple[FieldCode, FieldCode]:
-    """Per-matrix codebooks for the two exponent nibbles (Sec. 5.1)."""
+PAIR_MAX = 11              # default joint limit of a weight's two exponent codes
+
+
+def build_codebooks(w: np.ndarray, lmax: int = 12, pair_max: int = PAIR_MAX) -> Tuple[FieldCode, FieldCode]:
+    """Per-matrix codebooks for the two exponent nibbles (Sec. 5.1), each
+    code limited to lmax bits and the pair to pair_max (pair_limited_lengths)."""
     _, eh, el, _ = split_fields(w)
-    return FieldCode.from_freqs(histogram(eh), lmax), FieldCode.from_freqs(histogram(el), lmax)
+    feh, fel = histogram(eh), histogram(el)
+    leh, lel = pair_limited_lengths(feh, fel, lmax, pair_max)
+    return FieldCode.from_lengths(leh, feh), FieldCode.from_lengths(lel, fel)
 
 
 def segment_stream(eh_seg, el_seg, ceh: FieldCode, cel: FieldCode) -> Tuple[int, int]:
@@ -422,13 +476,14 @@ def segment_stream(eh_seg, el_seg, ceh: FieldCode, cel: FieldCode) -> Tuple[int,
 
 
 def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
-           codebooks: Tuple[FieldCode, FieldCode] = None, grp_rows: int = None) -> bytes:
+           codebooks: Tuple[FieldCode, FieldCode] = None, grp_rows: int = None,
+           pair_max: int = PAIR_MAX) -> bytes:
     """Compress a bf16 matrix [rows, cols] (uint16 bit patterns) into HLF1 bytes."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     rows, cols = w.shape
     GR = default_grp_rows(cols, seg_len) if grp_rows is None else grp_rows
     check_shape(rows, cols, seg_len, lmax, GR)
-    ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
+    ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax, pair_max)
     _, eh, el, _ = split_fields(w)
 
     def seg_stream(r, a, S):
@@ -776,12 +831,13 @@ def payload_bits(w: np.ndarray, ceh: FieldCode, cel: FieldCode) -> int:
 
 
 def container_size(w: np.ndarray, seg_len: int, lmax: int = 12,
-                   codebooks: Tuple[FieldCode, FieldCode] = None, grp_rows: int = None) -> Dict[str, int]:
+                   codebooks: Tuple[FieldCode, FieldCode] = None, grp_rows: int = None,
+                   pair_max: int = PAIR_MAX) -> Dict[str, int]:
     """Exact container size of ``encode(w, seg_len, lmax, grp_rows=...)`` from the
     code lengths alone (sum of code lengths per segment, 128-bit padding per
     group, section alignment), without building the stream."""
     w = np.asarray(w, dtype=np.uint16)
-    ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax)
+    ceh, cel = codebooks if codebooks is not None else build_codebooks(w, lmax, pair_max)
     _, eh, el, _ = split_fields(w)
     le = np.array(ceh.lengths if ceh.nsym > 1 else [0] * NSYM, dtype=np.int64)
     ll = np.array(cel.lengths if cel.nsym > 1 else [0] * NSYM, dtype=np.int64)

@@ -101,13 +101,62 @@ static void limited_lengths(const uint64_t* f, int n, int lmax, uint8_t* len) {
   if (mx > lmax) package_merge(f, n, lmax, len);
 }
 
-static void field_code_from_counts(const uint64_t f[16], int lmax, hl_field_code* fc) {
+static void field_presence(const uint64_t f[16], hl_field_code* fc) {
   int nsym = 0, single = 0;
   for (int s = 0; s < 16; ++s)
     if (f[s]) { ++nsym; single = s; }
   fc->nsym = (uint8_t)nsym;
   fc->single = (uint8_t)(nsym == 1 ? single : 0);
-  limited_lengths(f, 16, lmax, fc->len);
+}
+
+// Smallest length limit a prefix code of the present symbols can meet: 0 for
+// one symbol, else ceil(log2(count)).
+static int min_limit(const uint64_t f[16]) {
+  int n = 0;
+  for (int s = 0; s < 16; ++s) n += f[s] ? 1 : 0;
+  int b = 0;
+  while (n > 1 && (1 << b) < n) ++b;
+  return b;
+}
+
+static uint64_t code_cost(const uint64_t f[16], const uint8_t* len) {
+  uint64_t c = 0;
+  for (int s = 0; s < 16; ++s) c += f[s] * len[s];
+  return c;
+}
+
+// The two exponent codes: each at most lmax bits and, with pair_max > 0, the
+// longest eh code plus the longest el code at most pair_max bits. Every code
+// pair meeting the joint limit has some longest eh code a, so it costs at
+// least the optimal codes limited to a and pair_max - a: the result is the
+// cheapest of those splits, a = 0 .. lmax, the smallest a on equal cost.
+// False when pair_max is too small for the alphabets.
+static bool pair_limited_lengths(const uint64_t feh[16], const uint64_t fel[16], int lmax, int pair_max,
+                                 uint8_t leh[16], uint8_t lel[16]) {
+  if (pair_max <= 0) {
+    limited_lengths(feh, 16, lmax, leh);
+    limited_lengths(fel, 16, lmax, lel);
+    return true;
+  }
+  bool found = false;
+  uint64_t best = 0;
+  const int mh = min_limit(feh), ml = min_limit(fel);
+  for (int a = 0; a <= lmax; ++a) {
+    const int b = std::min(lmax, pair_max - a);
+    if (b < ml) break;
+    if (a < mh) continue;
+    uint8_t ta[16] = {0}, tb[16] = {0};
+    if (a) limited_lengths(feh, 16, a, ta);
+    if (b) limited_lengths(fel, 16, b, tb);
+    const uint64_t c = code_cost(feh, ta) + code_cost(fel, tb);
+    if (!found || c < best) {
+      found = true;
+      best = c;
+      std::memcpy(leh, ta, 16);
+      std::memcpy(lel, tb, 16);
+    }
+  }
+  return found;
 }
 
 void canonical_codes(const uint8_t* len, int n, uint32_t* code) {
@@ -459,12 +508,18 @@ static std::vector<uint64_t> histogram(const uint16_t* w, size_t n, int shift, u
   return f;
 }
 
-extern "C" hl_status hl_build_codebook(const uint16_t* w, size_t n, uint32_t lmax, hl_codebook* out) {
-  if (!w || !out || n == 0 || lmax < 4 || lmax > 15) return HL_EINVAL;
+extern "C" hl_status hl_build_codebook(const uint16_t* w, size_t n, uint32_t lmax, uint32_t pair_max,
+                                       hl_codebook* out) {
+  if (!w || !out || n == 0 || lmax < 4 || lmax > 15 || pair_max > 30) return HL_EINVAL;
   const std::vector<uint64_t> feh = histogram(w, n, 11, 15), fel = histogram(w, n, 7, 15);
-  out->lmax = lmax;
-  field_code_from_counts(feh.data(), (int)lmax, &out->eh);
-  field_code_from_counts(fel.data(), (int)lmax, &out->el);
+  hl_codebook cb;
+  std::memset(&cb, 0, sizeof(cb));
+  cb.lmax = lmax;
+  field_presence(feh.data(), &cb.eh);
+  field_presence(fel.data(), &cb.el);
+  if (!pair_limited_lengths(feh.data(), fel.data(), (int)lmax, (int)pair_max, cb.eh.len, cb.el.len))
+    return HL_EINVAL;
+  *out = cb;
   return HL_OK;
 }
 

@@ -459,6 +459,68 @@ __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jma
   pos2 = p;
 }
 
+// ---- bounded pairs: every weight's codes fit 11 bits
+// When the longest code pair of a matrix is at most kBpBits bits, an
+// 11-bit window holds a whole pair: the table has 2048 entries (the joint
+// table's first 2048, whose upper window bits are zero) and is kept in LDS
+// in kBpCopies copies, entry v of copy c at word v*kBpCopies + c, lane l
+// reading copy l % kBpCopies: the 32 lanes of a half-wave then spread over
+// the banks by copy as well as by entry, instead of colliding on the banks
+// of the short, frequent pairs. Four pairs then move the position at most 44
+// bits, so the four column words of a step always hold the second window
+// (no long-move branch), and no entry is an escape (no escape test).
+// Positions here are column bit positions minus 5: the window's low 16 bits
+// then hold five old bits and the 11-bit index already scaled by 32, the
+// byte offset of the entry's first copy.
+constexpr int kBpBits = 11;
+static_assert(kBpBits == HL_PAIR_MAX, "the encoder's default joint limit is the table window");
+constexpr uint32_t kBpN = 1u << kBpBits;
+constexpr uint32_t kBpCopies = 8;
+constexpr uint32_t kBpWords = kBpN * kBpCopies;  // 64 KB, at the start of the dynamic LDS
+
+// Fills the replicated table at the start of the dynamic LDS from the
+// global joint table (its first kBpN entries); two 16-byte stores per entry.
+__device__ inline void bp_table_fill(const uint32_t* lut) {
+  for (uint32_t v = threadIdx.x; v < kBpN; v += blockDim.x) {
+    const uint32_t e = lut[v];
+    uint4* d = reinterpret_cast<uint4*>(s_dyn + v * kBpCopies);
+    d[0] = make_uint4(e, e, e, e);
+    d[1] = make_uint4(e, e, e, e);
+  }
+}
+
+__device__ inline uint32_t bp_at(uint32_t w, uint32_t lane_off) {
+  const uint32_t off = (w & ((kBpN - 1) << 5)) | lane_off;
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + off);
+}
+
+__device__ inline void bp_lookup4(uint64_t W, uint32_t& p, uint32_t* e, uint32_t lane_off) {
+  e[0] = bp_at((uint32_t)W, lane_off);
+  W = shift_window(W, e[0]);
+  e[1] = bp_at((uint32_t)W, lane_off);
+  W = shift_window(W, e[1]);
+  e[2] = bp_at((uint32_t)W, lane_off);
+  W = shift_window(W, e[2]);
+  e[3] = bp_at((uint32_t)W, lane_off);
+  p = p + e[0] + e[1] + e[2] + e[3];
+}
+
+// decode8 for bounded pairs: no branch. jmax - 1 bounds the first of the
+// four rows read (columns hold three rows of overrun).
+__device__ inline void bp_decode8(const uint32_t* sc, uint32_t jmax, uint32_t& pos5, uint32_t* e,
+                                  uint32_t lane_off) {
+  uint32_t p = pos5;
+  const uint32_t j = min((p & kPosMask) >> 5, jmax - 1);
+  const uint32_t w0 = col_word(sc, j), w1 = col_word(sc, j + 1), w2 = col_word(sc, j + 2), w3 = col_word(sc, j + 3);
+  bp_lookup4(funnel64(w2, w1, w0, p), p, e, lane_off);
+  // rows moved: 0, 1 or 2 (more only when the first row was clamped)
+  const uint32_t rel = ((p & kPosMask) >> 5) - j;
+  const bool r1 = rel == 1, r2 = rel >= 2;
+  const uint32_t c = (r1 || r2) ? w3 : w2, b = r2 ? w3 : r1 ? w2 : w1, a = r2 ? w2 : r1 ? w1 : w0;
+  bp_lookup4(funnel64(c, b, a, p), p, e + 4, lane_off);
+  pos5 = p;
+}
+
 // Packed bf16 pair (weights k, k+1 of a raw dword) from two table entries.
 __device__ inline uint32_t pack_pair(uint32_t rawdw, int k, uint32_t e0, uint32_t e1) {
   const uint32_t b0 = (uint32_t)(k & 3), b1 = (uint32_t)((k + 1) & 3);
@@ -480,6 +542,15 @@ __device__ inline float dot2(uint32_t w, uint32_t x, float acc) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, w),
                                          __builtin_bit_cast(bf16x2_t, x), acc, false);
 }
+
+// Wait states after a matrix instruction before the next instruction may
+// overwrite its A or B operand registers. Measured on gfx950: with the
+// packed weights of the next step written into the A operand's registers by
+// the instruction right after v_mfma_f32_16x16x32_bf16, the product
+// intermittently used the new values (whole row blocks wrong); the compiler
+// placed no wait states there. Five are enough and cost nothing measurable
+// (the other waves of the SIMD issue meanwhile).
+__device__ inline void mfma_operand_guard() { asm volatile("s_nop 4"); }
 
 // ------------------------------------------------------------------ staging
 
@@ -1035,6 +1106,7 @@ __global__ void __launch_bounds__(1024) gemv_mfma_kernel(GemvArgs p) {
         wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
         acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
                                                       __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
+        mfma_operand_guard();
         rw[k] = *reinterpret_cast<const uint2*>(rp + k * rs);
         xv[k] = *reinterpret_cast<const uint4*>(xp + k * xs);
       }
@@ -1161,6 +1233,7 @@ __global__ void __launch_bounds__(1024) gemm_mfma_kernel(GemmArgs p) {
       for (int j = 0; j < NT; ++j) {
         const uint4 xb = *reinterpret_cast<const uint4*>(xs + xslice_offset<SP>(16 * j + i, q * SP + k));
         acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, xb), acc[j], 0, 0, 0);
+        mfma_operand_guard();
       }
     }
   }
@@ -1228,10 +1301,11 @@ __device__ inline const GemvArgs& gemv_args(const Args& x) {
   if constexpr (std::is_same_v<Args, StreamArgs>) return x.p; else return x;
 }
 
-template <int SP, int JT, bool XT, class Args, bool DEC>
+template <int SP, int JT, bool XT, class Args, bool DEC, bool BP>
 __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
+  constexpr uint32_t kTab = BP ? kBpWords : 0;  // dynamic LDS words before the wave regions
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
   constexpr bool kMulti = std::is_same_v<Args, StreamArgs>;
   const GemvArgs& p = gemv_args(sa);
@@ -1251,9 +1325,10 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
   uint16_t* const outp = reinterpret_cast<uint16_t*>(yp);  // decoding: the bf16 output (GemvArgs::y)
   const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const uint32_t waves = blockDim.x >> 6;
-  uint32_t* cols = s_dyn + wave * kBuf;
+  uint32_t* cols = s_dyn + kTab + wave * kBuf;
   const uint32_t jmax = kRows - 3;
   const uint32_t i = lane & 15, q = lane >> 4;
+  const uint32_t lane_off = (lane % kBpCopies) * 4;  // bounded pairs: the lane's table copy
   // byte offset of the lane's activations x[n = i][(c0 + q)*S + 8k .. +8) at
   // x + c0*XSEG + xoff + k*XSTEP, from x itself or (XT) from its tiled copy,
   // where the 16 batch rows' pieces of one 8-column chunk are 256 contiguous
@@ -1291,9 +1366,12 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
   // are waited for only at that step's product.
   Meta m0 = load_meta(a, g0, lane);
   Meta m1 = load_meta(a, g1, lane);
-  table_dma(a.lut);
+  if constexpr (!BP) table_dma(a.lut);
   u32x4_a4 sw[JT / 4];
-  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw);
+  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw) - (BP ? 3u : 0u);
+  // bounded pairs: the table is replicated through registers (its global
+  // copy is hot in the L2), after the stream words were requested
+  if constexpr (BP) bp_table_fill(a.lut);
   uint2 rw[SP];
   uint4 xv[SP];
   {
@@ -1318,7 +1396,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
     const uint32_t rb = rb_of(t);
     const uint32_t G = min(16u, a.rows - rb * 16);
     const uint32_t mu = q * G + min(i, G - 1);
-    const uint32_t sc_off = wave * kBuf + mu;
+    const uint32_t sc_off = kTab + wave * kBuf + mu;
     const uint32_t* sc = s_dyn + sc_off;
     for (uint32_t j = 0; j < nj; ++j) {
       if (wave + j * waves >= CB) continue;
@@ -1335,7 +1413,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
       const uint32_t n_c0 = m1.c0;
       // the next group's stream words (this group's again after the last),
       // then the metadata of the group after it
-      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw);
+      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw) - (BP ? 3u : 0u);
       m1 = load_meta(a, g2, lane);
       // prefetch source: the next group, else the lane's cached activations
       // (decoding: the current group's raw bytes)
@@ -1351,7 +1429,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
 #pragma unroll
       for (int k = 0; k < SP; ++k) {
         uint32_t e[8];
-        decode8(sc, sc_off, jmax, pd, e);
+        if constexpr (BP) bp_decode8(sc, jmax, pd, e, lane_off); else decode8(sc, sc_off, jmax, pd, e);
         uint4 wv;
         wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
         wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
@@ -1362,6 +1440,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
         } else {
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
                                                         __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
+          mfma_operand_guard();
           // x first: the wait for the raw bytes at their use then covers both
           xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
         }
@@ -1399,7 +1478,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
       if (wave < 4) {
         const uint32_t v = wave;
         float sum = 0.f;
-        for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + w * kBuf)[v * 64 + lane];
+        for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + kTab + w * kBuf)[v * 64 + lane];
         if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
       }
       block_sync_lds();
@@ -1759,6 +1838,7 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
         const uint4 wv = pack8_f16(h, sgc.byte(t0 + k));
         acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, wv),
                                                      __builtin_bit_cast(f16x8_t, xv[k]), acc, 0, 0, 0);
+        mfma_operand_guard();
         xv[k] = *reinterpret_cast<const uint4*>(xp + k * xs);
       }
     }
@@ -1935,14 +2015,14 @@ static int stream_rows_for(uint32_t seg_len, uint32_t col_rows) {
   return 0;
 }
 
-template <bool XT>
+template <bool XT, bool BP>
 static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block, size_t lds,
                                  hipStream_t s, const StreamArgs& p) {
   if (seg_len == 64 && multi) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false, BP>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false, BP>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false, BP>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
@@ -1950,24 +2030,29 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
   const GemvArgs& g = p.p;  // one matrix: the small argument block
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false>, grid, block, lds, s, g);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false>, grid, block, lds, s, g);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false>, grid, block, lds, s, g);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false, BP>, grid, block, lds, s, g);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false, BP>, grid, block, lds, s, g);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false, BP>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
-  switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false>, grid, block, lds, s, g);
-    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false>, grid, block, lds, s, g);
-    default: return HL_EUNSUPPORTED;
+  if constexpr (!BP) {
+    switch (jt) {
+      case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false, false>, grid, block, lds, s, g);
+      case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false, false>, grid, block, lds, s, g);
+      default: return HL_EUNSUPPORTED;
+    }
   }
+  return HL_EUNSUPPORTED;
 }
 
-// Grouped launches (multi) exist for S = 64.
-static hl_status launch_stream(bool xt, uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block, size_t lds,
-                               hipStream_t s, const StreamArgs& p) {
-  return xt ? launch_stream_x<true>(seg_len, jt, multi, grid, block, lds, s, p)
-            : launch_stream_x<false>(seg_len, jt, multi, grid, block, lds, s, p);
+// Grouped launches (multi) exist for S = 64, bounded pairs (bp) for S = 64.
+static hl_status launch_stream(bool xt, bool bp, uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block,
+                               size_t lds, hipStream_t s, const StreamArgs& p) {
+  if (bp) return xt ? launch_stream_x<true, true>(seg_len, jt, multi, grid, block, lds, s, p)
+                    : launch_stream_x<false, true>(seg_len, jt, multi, grid, block, lds, s, p);
+  return xt ? launch_stream_x<true, false>(seg_len, jt, multi, grid, block, lds, s, p)
+            : launch_stream_x<false, false>(seg_len, jt, multi, grid, block, lds, s, p);
 }
 
 // Decoding to bf16 with the persistent kernel (p.y = the output).
@@ -1975,15 +2060,15 @@ static hl_status launch_stream_dec(uint32_t seg_len, int jt, dim3 grid, dim3 blo
                                    const GemvArgs& p) {
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, false>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true, false>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true, false>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true>, grid, block, lds, s, p);
-    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true>, grid, block, lds, s, p);
+    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true, false>, grid, block, lds, s, p);
+    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true, false>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
 }
@@ -2106,11 +2191,31 @@ extern "C" hl_status hl_tensor_prepare(const hl_tensor* t, void* stream) {
 // matrix does not fit it (16-row groups of the bf16 formats at S = 32 or 64,
 // at least one row block per CU and two groups per wave of at least 8 waves
 // per block, every segment within the largest stream word count).
+// Longest code of a weight's exponent (the pair of the split format, the one
+// code of the whole-exponent format), over the symbols present.
+static uint32_t longest_exponent_code(const hl_tensor* t) {
+  uint32_t a = 0, b = 0;
+  if (t->format == HL_FORMAT_SPLIT) {
+    for (int k = 0; k < 16; ++k) a = std::max<uint32_t>(a, t->cb.eh.len[k]), b = std::max<uint32_t>(b, t->cb.el.len[k]);
+  } else if (t->format == HL_FORMAT_WHOLE_EXPONENT) {
+    for (int k = 0; k < 256; ++k) a = std::max<uint32_t>(a, t->cb8.len[k]);
+  } else {
+    return 99;
+  }
+  return a + b;
+}
+
+// The persistent kernel's bounded-pair form applies (S = 64, pairs within
+// the 11-bit window).
+static bool bounded_pairs(const hl_tensor* t) {
+  return t->seg_len == 64 && longest_exponent_code(t) <= (uint32_t)kBpBits;
+}
+
 static bool stream_shape(const hl_tensor* t, const GroupArgs& ga, int* jt, uint32_t* waves, size_t* per_wave) {
   if (is_fp16(t) || t->grp_rows != 16 || (t->seg_len != 64 && t->seg_len != 32)) return false;
   const uint32_t CB = ga.CB, RB = ga.RB, cus = (uint32_t)device_cus();
   *jt = stream_rows_for(t->seg_len, ga.col_rows);
-  const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
+  const size_t tab = bounded_pairs(t) ? (size_t)kBpWords * 4 : (size_t)(kLutN + kAuxWords) * 4;
   *per_wave = (size_t)(*jt + 1) * kCol * 4;
   uint32_t w = kMaxWaves;
   while (w > 1 && tab + w * *per_wave > kMaxLds) --w;
@@ -2140,6 +2245,8 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
     p.C = pl.ga.CB;
     p.KS = 1;
     w = 8;  // the kernel's bound when decoding (registers for a group's weights)
+    // the decode form keeps the joint table (the bounded-pair form measured
+    // slower here: 28672x8192 307 us against 273 us)
     return launch_stream_dec(t->seg_len, jt, dim3(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus())),
                              dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
   }
@@ -2389,8 +2496,9 @@ static hl_status gemv_impl(const hl_tensor* t, const void* x_dev, hl_dtype x_dty
       sa.p = p;
       sa.n = 1;
       sa.part0[1] = std::min(RB, cus);
-      return launch_stream(xt, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64), w * per_wave, stream,
-                           sa);
+      const bool bp = bounded_pairs(t);
+      return launch_stream(xt, bp, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64),
+                           (bp ? kBpWords * 4 : 0) + w * per_wave, stream, sa);
     }
   }
   // Column blocks per block and blocks per row block.
@@ -2482,7 +2590,9 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
     rbs += pl[k].ga.RB;
   }
   uint32_t w = kMaxWaves;
-  const size_t tab = (size_t)(kLutN + kAuxWords) * 4;
+  bool bp = grouped;  // the bounded-pair kernel when every matrix has bounded pairs
+  for (uint32_t k = 0; k < count && bp; ++k) bp = bounded_pairs(ts[k]);
+  const size_t tab = bp ? (size_t)kBpWords * 4 : (size_t)(kLutN + kAuxWords) * 4;
   const size_t per_wave = (size_t)(jt + 1) * kCol * 4;
   if (grouped) {
     while (w > 1 && tab + w * per_wave > kMaxLds) --w;
@@ -2537,7 +2647,8 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
     sa.y[k] = y_devs[k];
     sa.part0[k + 1] = sa.part0[k] + nb[k];
   }
-  return launch_stream(xt, ts[0]->seg_len, jt, true, dim3(used), dim3(w * 64), w * per_wave, (hipStream_t)stream, sa);
+  return launch_stream(xt, bp, ts[0]->seg_len, jt, true, dim3(used), dim3(w * 64), (bp ? kBpWords * 4 : 0) + w * per_wave,
+                       (hipStream_t)stream, sa);
 }
 
 // ------------------------------------------------------------------ prefill GEMM host side

@@ -100,7 +100,7 @@ def lib() -> ctypes.CDLL:
     L.hl_default_grp_rows.restype = c.c_uint32
     L.hl_default_grp_rows.argtypes = [c.c_uint64, c.c_uint32]
     L.hl_build_codebook.restype = c.c_int
-    L.hl_build_codebook.argtypes = [c.c_void_p, c.c_size_t, c.c_uint32, c.POINTER(Codebook)]
+    L.hl_build_codebook.argtypes = [c.c_void_p, c.c_size_t, c.c_uint32, c.c_uint32, c.POINTER(Codebook)]
     L.hl_encode.restype = c.c_int
     L.hl_encode.argtypes = [c.c_void_p, c.c_uint64, c.c_uint64, c.POINTER(Codebook), c.c_uint32,
                             c.c_uint32, c.c_uint32, c.c_void_p, c.POINTER(c.c_size_t)]
@@ -158,10 +158,15 @@ def default_seg_len(cols: int) -> int:
     return int(lib().hl_default_seg_len(cols))
 
 
-def build_codebook(w: np.ndarray, lmax: int = 12) -> Codebook:
+PAIR_MAX = 11  # default joint limit of a weight's two exponent codes (the fused kernel's table window)
+
+
+def build_codebook(w: np.ndarray, lmax: int = 12, pair_max: int = PAIR_MAX) -> Codebook:
+    """Codes of the two exponent fields: each at most lmax bits, the pair at
+    most pair_max bits (0: no joint limit)."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     cb = Codebook()
-    _check(lib().hl_build_codebook(w.ctypes.data, w.size, lmax, ctypes.byref(cb)), "hl_build_codebook")
+    _check(lib().hl_build_codebook(w.ctypes.data, w.size, lmax, pair_max, ctypes.byref(cb)), "hl_build_codebook")
     return cb
 
 
@@ -186,12 +191,14 @@ def default_grp_rows(cols: int, seg_len: int = 0) -> int:
 
 
 def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook=None,
-           nthreads: int = 0, grp_rows: int = 0, whole_exponent: bool = False, fp16: bool = False) -> np.ndarray:
+           nthreads: int = 0, grp_rows: int = 0, whole_exponent: bool = False, fp16: bool = False,
+           pair_max: int = PAIR_MAX) -> np.ndarray:
     """HLF1 container (uint8 array) of a bf16 matrix given as uint16 bits [rows, cols].
 
     whole_exponent selects the format with one 256-symbol exponent code
     (``codebook`` then is a Codebook8); fp16 takes float16 bits and selects the
-    {1,5,5,5} format (``codebook``: a Codebook16)."""
+    {1,5,5,5} format (``codebook``: a Codebook16). pair_max (split format):
+    joint limit of a weight's two exponent codes, 0 for none."""
     w = np.ascontiguousarray(w, dtype=np.uint16)
     if w.ndim != 2:
         raise ValueError("expected a 2-D matrix")
@@ -203,7 +210,7 @@ def encode(w: np.ndarray, seg_len: int = 0, lmax: int = 12, codebook=None,
         cb = codebook if codebook is not None else build_codebook8(w, lmax)
         fn, name = L.hl_encode8, "hl_encode8"
     else:
-        cb = codebook if codebook is not None else build_codebook(w, lmax)
+        cb = codebook if codebook is not None else build_codebook(w, lmax, pair_max)
         fn, name = L.hl_encode, "hl_encode"
     n = ctypes.c_size_t(0)
     _check(fn(w.ctypes.data, w.shape[0], w.shape[1], ctypes.byref(cb), seg_len, grp_rows, nthreads,

@@ -70,14 +70,18 @@ def _weights(kind, rows, cols, seed):
     return f32_to_bf16_bits(mag * np.where(rng.random((rows, cols)) < 0.5, -1, 1).astype(np.float32))
 
 
-# container formats: (encoder keywords); the longer split limit puts el codes
-# past the 13-bit joint window (escape entries); whole exponents have codes
-# of at most 13 bits (no escapes)
-FORMATS = {"split": {}, "split_lmax15": {"lmax": 15}, "whole": {"whole_exponent": True}}
+# container formats: (encoder keywords). The default split codes keep every
+# weight's pair within 11 bits (at S = 64 the kernel's bounded-pair form:
+# replicated 11-bit table, no escape or long-move branch); without the joint
+# limit pairs reach 13 bits (long moves of the window) and with the longer
+# limit el codes pass the 13-bit window (escape entries); whole exponents
+# have codes of at most 13 bits (no escapes)
+FORMATS = {"split": {}, "split_unbounded": {"pair_max": 0}, "split_lmax15": {"lmax": 15, "pair_max": 0},
+           "whole": {"whole_exponent": True}}
 
 
-@pytest.mark.parametrize("S,cols,fmt", [(64, 8192, "split"), (32, 4096, "split"), (64, 8192, "split_lmax15"),
-                                        (64, 8192, "whole"), (32, 4096, "whole")])
+@pytest.mark.parametrize("S,cols,fmt", [(64, 8192, "split"), (32, 4096, "split"), (64, 8192, "split_unbounded"),
+                                        (64, 8192, "split_lmax15"), (64, 8192, "whole"), (32, 4096, "whole")])
 @pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform", "geometric", "long_moves"])
 def test_persistent_kernel(torch, S, cols, fmt, kind):
     rows = 4100
@@ -85,9 +89,12 @@ def test_persistent_kernel(torch, S, cols, fmt, kind):
     W = _weights(kind, rows, cols, seed=S + cols)
     dt = hl.DeviceTensor(hl.encode(W, seg_len=S, **FORMATS[fmt]))
     assert dt.view.grp_rows == 16
-    if kind == "long_moves" and fmt == "split":
-        cb = dt.view.cb  # every pair fits the 13-bit window: long moves without escapes
+    cb = dt.view.cb
+    if kind == "long_moves" and fmt == "split_unbounded":
+        # every pair fits the 13-bit window: long moves without escapes
         assert max(cb.eh.len) + max(cb.el.len) <= 13
+    if fmt == "split":
+        assert max(cb.eh.len) + max(cb.el.len) <= hl.PAIR_MAX
     Wf = bf16_to_f64(W)
     rng = np.random.default_rng(S)
     sample = sorted({0, 15, 16, rows - 5, rows - 4, rows - 1} | set(int(r) for r in rng.integers(0, rows, 10)))

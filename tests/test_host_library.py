@@ -389,3 +389,25 @@ def test_binding_rejects_bad_buffers_before_launch():
         hl.gemv_bf16(w.float(), x)
     with pytest.raises(ValueError):
         hl.gemv_bf16(w, x, y)  # host tensors
+
+
+@pytest.mark.parametrize("pair_max", [0, 7, 8, 9, 10, 11, 13, 30])
+def test_pair_limited_codebook_equals_oracle(pair_max):
+    # the joint limit of a weight's two codes binds on these weights (eh over
+    # four values, el codes of up to 11 bits): codebooks and containers equal
+    # the oracle's for limits from the smallest feasible one up
+    from gen import workload_matrices, gen_matrix
+    w = gen_matrix(workload_matrices(2)[0], rows=slice(0, 256))
+    cb = hl.build_codebook(w, lmax=12, pair_max=pair_max)
+    ceh, cel = codec.build_codebooks(w, 12, pair_max)
+    assert _codebook_lists(cb) == (ceh.nsym, ceh.single, ceh.lengths, cel.nsym, cel.single, cel.lengths)
+    if pair_max:
+        assert max(cb.eh.len) + max(cb.el.len) <= pair_max
+    assert bytes(hl.encode(w, pair_max=pair_max)) == codec.encode(w, seg_len=64, pair_max=pair_max)
+
+
+def test_pair_limit_too_small_is_refused():
+    from gen import workload_matrices, gen_matrix
+    w = gen_matrix(workload_matrices(2)[0], rows=slice(0, 64))
+    with pytest.raises(hl.HLError):
+        hl.build_codebook(w, lmax=12, pair_max=3)

@@ -436,3 +436,73 @@ def test_container_size_matches_written_container(shape, S):
     assert cs["max_grp_units"] == h["max_grp_units"] and cs["off_raw"] == h["off_raw"]
     ceh, cel = codec.build_codebooks(w)
     assert cs["code_bits"] + 8 * w.size == codec.payload_bits(w, ceh, cel)
+
+
+# ---- joint limit of a weight's two exponent codes (split format)
+
+def _field_vectors(freqs, lmax):
+    """Every complete prefix-code length vector of a field with lengths <= lmax
+    (non-decreasing lengths given to symbols of non-increasing frequency:
+    optimal for each multiset), as (cost, longest); a one-symbol field: (0, 0)."""
+    f = sorted((x for x in freqs if x > 0), reverse=True)
+    n = len(f)
+    if n == 1:
+        return [(0, 0)]
+    out = []
+    for ls in itertools.combinations_with_replacement(range(1, lmax + 1), n):
+        if sum(Fraction(1, 2 ** l) for l in ls) == 1:
+            out.append((sum(a * b for a, b in zip(f, ls)), max(ls)))
+    return out
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_pair_limit_optimal_bruteforce(seed):
+    # the cheapest pair of codes under both limits, by enumerating every pair
+    # of complete length vectors (nothing of the oracle's rule is used)
+    rnd = random.Random(500 + seed)
+    feh, fel = [0] * 16, [0] * 16
+    for s in rnd.sample(range(16), rnd.randint(1, 4)):
+        feh[s] = rnd.choice([1, 3, 10, 1000, rnd.randint(1, 5000)])
+    for s in rnd.sample(range(16), rnd.randint(2, 6)):
+        fel[s] = rnd.choice([1, 2, 7, 60, 900, rnd.randint(1, 5000)])
+    lmax = rnd.choice([4, 5, 6])
+    J = rnd.randint(codec.min_limit(feh) + codec.min_limit(fel), 10)
+    leh, lel = codec.pair_limited_lengths(feh, fel, lmax, J)
+    assert max(leh) + max(lel) <= J and max(leh) <= lmax and max(lel) <= lmax
+    for f, l in ((feh, leh), (fel, lel)):
+        assert all((l[i] > 0) == (f[i] > 0) for i in range(16)) or sum(1 for x in f if x) == 1
+        if sum(1 for x in f if x) > 1:
+            assert codec.kraft_sum(l) == 1
+    best = min(ca + cb for ca, ma in _field_vectors(feh, lmax) for cb, mb in _field_vectors(fel, lmax)
+               if ma + mb <= J)
+    assert _cost(feh, leh) + _cost(fel, lel) == best
+
+
+def test_pair_limit_special_cases():
+    rnd = random.Random(7)
+    feh = [0] * 16
+    feh[7], feh[6], feh[8] = 99000, 700, 300
+    fel = [0] * 16
+    for s in range(16):
+        fel[s] = max(1, int(40000 * 0.5 ** abs(s - 9)))
+    # no joint limit, or one that does not bind: the independent limited codes
+    for J in (0, 30):
+        assert codec.pair_limited_lengths(feh, fel, 12, J) == (codec.limited_lengths(feh, 12),
+                                                                codec.limited_lengths(fel, 12))
+    # a binding limit costs at least as much, never less, and meets the limit
+    free = _cost(feh, codec.limited_lengths(feh, 12)) + _cost(fel, codec.limited_lengths(fel, 12))
+    prev = free
+    for J in range(20, 6, -1):
+        leh, lel = codec.pair_limited_lengths(feh, fel, 12, J)
+        c = _cost(feh, leh) + _cost(fel, lel)
+        assert max(leh) + max(lel) <= J and c >= prev
+        prev = c
+    # one-symbol fields take no bits and leave the whole limit to the other
+    one = [0] * 16
+    one[5] = 10
+    leh, lel = codec.pair_limited_lengths(one, fel, 12, 11)
+    assert leh == [0] * 16 and lel == codec.limited_lengths(fel, 11)
+    # a limit below what the alphabets need is refused
+    with pytest.raises(ValueError):
+        codec.pair_limited_lengths(feh, fel, 12, codec.min_limit(feh) + codec.min_limit(fel) - 1)
+    del rnd
