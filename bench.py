@@ -485,7 +485,11 @@ def build_stack(torch, hl, layers: int, keep_bf16: int):
         for row in stack[1:]:
             row[j]._ws = ws
     torch.cuda.synchronize()
-    return dict(stack=stack, bf16=bf16, host_last=host_last, comp=comp, n=n,
+    # container bytes of a layer's four launches (q+k+v, o, gate+up, down), layer average
+    sizes = [[t.nbytes for t in row] for row in stack]
+    launch_bytes = [sum(r[0] + r[1] + r[2] for r in sizes) // layers, sum(r[3] for r in sizes) // layers,
+                    sum(r[4] + r[5] for r in sizes) // layers, sum(r[6] for r in sizes) // layers]
+    return dict(stack=stack, bf16=bf16, host_last=host_last, comp=comp, n=n, launch_bytes=launch_bytes,
                 setup_s=time.perf_counter() - t0, encode_s=enc_s)
 
 
@@ -717,6 +721,15 @@ def summarize_trace(trace_dir, bench_log):
             f"(after {per_step} launches outside the graph and a warm-up graph of {warmup} steps):"]
     for k, (c, tot) in sorted(names.items()):
         out.append(f"  {k}: {c} dispatches, average {tot / c / 1e3:.2f} us")
+    # per launch of a layer (q/k/v grouped, o, gate/up grouped, down), with
+    # the compressed bytes of its matrices from the run's line
+    lb = st.get("launch_bytes")
+    if lb and per_step == 4 * layers:
+        for k, name in enumerate(("q, k, v (grouped)", "o", "gate, up (grouped)", "down")):
+            ds = dur[k::4]
+            avg = sum(ds) / len(ds)
+            out.append(f"  launch {k} of a layer, {name}: average {avg / 1e3:.2f} us, "
+                       f"{lb[k] / 1e6:.2f} MB of containers -> {lb[k] / avg:.1f} GB/s")
     out += [f"  fused-kernel time per step (sum of dispatch durations / steps): {ksum / 1e6:.4f} ms",
             f"  first start to last end / steps: {span / steps / 1e6:.4f} ms "
             f"(the benchmark's events: {d['ms_per_step']} ms per step)",
@@ -828,7 +841,7 @@ def main():
         compressed_GBps=round(comp / (ms * 1e-3) / 1e9, 1),
         ms_per_step_one_launch_per_matrix=round(r["ms_single"], 4),
         compressed_GBps_one_launch_per_matrix=round(comp / (r["ms_single"] * 1e-3) / 1e9, 1),
-        max_rel_err_last_layer=r["max_rel_err"])
+        max_rel_err_last_layer=r["max_rel_err"], launch_bytes=st["launch_bytes"])
     if "hl_gemv_bf16_ms" in r:
         best = min(r["hl_gemv_bf16_ms"], r["torch_linear_ms"])
         stack_detail.update(

@@ -476,14 +476,19 @@ constexpr int kBpBits = 11;
 static_assert(kBpBits == HL_PAIR_MAX, "the encoder's default joint limit is the table window");
 constexpr uint32_t kBpN = 1u << kBpBits;
 constexpr uint32_t kBpCopies = 8;
-constexpr uint32_t kBpWords = kBpN * kBpCopies;  // 64 KB, at the start of the dynamic LDS
+constexpr uint32_t kBpWords = kBpN * kBpCopies;  // 64 KB
 
-// Fills the replicated table at the start of the dynamic LDS from the
-// global joint table (its first kBpN entries); two 16-byte stores per entry.
+// The replicated table, a static LDS array of its own: at a fixed address
+// in the kernels that use it (no other static LDS there), so that a lookup's
+// address is one and-or of the window and the lane's copy offset.
+__shared__ __attribute__((aligned(32))) uint32_t s_bp[kBpWords];
+
+// Fills the replicated table from the global joint table (its first kBpN
+// entries); two 16-byte stores per entry.
 __device__ inline void bp_table_fill(const uint32_t* lut) {
   for (uint32_t v = threadIdx.x; v < kBpN; v += blockDim.x) {
     const uint32_t e = lut[v];
-    uint4* d = reinterpret_cast<uint4*>(s_dyn + v * kBpCopies);
+    uint4* d = reinterpret_cast<uint4*>(s_bp + v * kBpCopies);
     d[0] = make_uint4(e, e, e, e);
     d[1] = make_uint4(e, e, e, e);
   }
@@ -491,7 +496,7 @@ __device__ inline void bp_table_fill(const uint32_t* lut) {
 
 __device__ inline uint32_t bp_at(uint32_t w, uint32_t lane_off) {
   const uint32_t off = (w & ((kBpN - 1) << 5)) | lane_off;
-  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_dyn) + off);
+  return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_bp) + off);
 }
 
 __device__ inline void bp_lookup4(uint64_t W, uint32_t& p, uint32_t* e, uint32_t lane_off) {
@@ -1305,7 +1310,7 @@ template <int SP, int JT, bool XT, class Args, bool DEC, bool BP>
 __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) {
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
-  constexpr uint32_t kTab = BP ? kBpWords : 0;  // dynamic LDS words before the wave regions
+  constexpr uint32_t kTab = 0;  // dynamic LDS words before the wave regions
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
   constexpr bool kMulti = std::is_same_v<Args, StreamArgs>;
   const GemvArgs& p = gemv_args(sa);
@@ -2497,8 +2502,8 @@ static hl_status gemv_impl(const hl_tensor* t, const void* x_dev, hl_dtype x_dty
       sa.n = 1;
       sa.part0[1] = std::min(RB, cus);
       const bool bp = bounded_pairs(t);
-      return launch_stream(xt, bp, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64),
-                           (bp ? kBpWords * 4 : 0) + w * per_wave, stream, sa);
+      return launch_stream(xt, bp, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64), w * per_wave,
+                           stream, sa);
     }
   }
   // Column blocks per block and blocks per row block.
@@ -2647,7 +2652,7 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
     sa.y[k] = y_devs[k];
     sa.part0[k + 1] = sa.part0[k] + nb[k];
   }
-  return launch_stream(xt, bp, ts[0]->seg_len, jt, true, dim3(used), dim3(w * 64), (bp ? kBpWords * 4 : 0) + w * per_wave,
+  return launch_stream(xt, bp, ts[0]->seg_len, jt, true, dim3(used), dim3(w * 64), w * per_wave,
                        (hipStream_t)stream, sa);
 }
 
