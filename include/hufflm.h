@@ -260,8 +260,13 @@ hl_status hl_validate(const void* blob_host, size_t blob_bytes);
 
 /* Build a device view of a container copied to `blob_dev` (blob_bytes long)
  * from its host copy `blob_host` (the same bytes), which is fully validated
- * (as hl_validate, O(n_seg)). lut_dev must point to HL_LUT_BYTES of device
- * memory that the view uses from now on. Errors: HL_EINVAL, HL_ECORRUPT. */
+ * (as hl_validate, O(n_seg)): the compressed weights stay resident in device
+ * memory in this form and are never expanded there (Sec. 1 contributions:
+ * weights kept compressed in memory, decompressed only to be multiplied).
+ * lut_dev must point to HL_LUT_BYTES of device memory that the view uses
+ * from now on. blob_dev and lut_dev must be 16-byte aligned (the kernels
+ * copy both in 16-byte pieces). Errors: HL_EINVAL (also for a misaligned
+ * pointer), HL_ECORRUPT. */
 hl_status hl_tensor_view(const void* blob_dev, const void* blob_host,
                          size_t blob_bytes, uint32_t* lut_dev, hl_tensor* out);
 
@@ -277,9 +282,13 @@ hl_status hl_tensor_prepare(const hl_tensor* t, void* stream);
  * aligned (any hipMalloc or torch allocation is); float32 outputs must be
  * 4-byte aligned. A misaligned pointer gives HL_EINVAL. */
 
-/* Decode the whole matrix to bf16 bit patterns, out_dev[rows*cols]
- * (row-major). Bit-exact with the encoder's input. Errors: HL_EINVAL (also
- * for a misaligned out_dev). */
+/* Decode the whole matrix to bf16 bit patterns (float16 for the float16
+ * format), out_dev[rows*cols] (row-major): the decoder of Sec. 3.2 (window
+ * match, symbol, pointer advance by the code length, concatenation with the
+ * raw sign and mantissa) without the product; the layer-wise full
+ * decompression the paper contrasts with its own (Sec. 1, Sec. 2.1).
+ * Bit-exact with the encoder's input. Errors: HL_EINVAL (also for a
+ * misaligned out_dev). */
 hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream);
 
 /* Bytes of device workspace hl_decode_gemv may use for `t` at this batch
