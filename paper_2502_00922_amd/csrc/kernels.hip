@@ -483,14 +483,31 @@ constexpr uint32_t kBpWords = kBpN * kBpCopies;  // 64 KB
 // address is one and-or of the window and the lane's copy offset.
 __shared__ __attribute__((aligned(32))) uint32_t s_bp[kBpWords];
 
-// Fills the replicated table from the global joint table (its first kBpN
-// entries); two 16-byte stores per entry.
-__device__ inline void bp_table_fill(const uint32_t* lut) {
-  for (uint32_t v = threadIdx.x; v < kBpN; v += blockDim.x) {
-    const uint32_t e = lut[v];
-    uint4* d = reinterpret_cast<uint4*>(s_bp + v * kBpCopies);
-    d[0] = make_uint4(e, e, e, e);
-    d[1] = make_uint4(e, e, e, e);
+// The replicated table is filled from the global joint table (its first
+// kBpN entries) in two halves: the thread's entries are loaded into registers
+// (blocks of at least kBpMinThreads threads: at most kBpPerThread each) at the
+// kernel's start, and stored to LDS, in kBpCopies copies, once other loads
+// have been requested behind them.
+constexpr uint32_t kBpMinThreads = 512;
+constexpr uint32_t kBpPerThread = kBpN / kBpMinThreads;
+
+__device__ inline void bp_table_load(const uint32_t* lut, uint32_t (&te)[kBpPerThread]) {
+#pragma unroll
+  for (uint32_t k = 0; k < kBpPerThread; ++k) {
+    const uint32_t v = threadIdx.x + k * blockDim.x;
+    te[k] = v < kBpN ? lut[v] : 0u;
+  }
+}
+
+__device__ inline void bp_table_store(const uint32_t (&te)[kBpPerThread]) {
+#pragma unroll
+  for (uint32_t k = 0; k < kBpPerThread; ++k) {
+    const uint32_t v = threadIdx.x + k * blockDim.x, e = te[k];
+    if (v < kBpN) {
+      uint4* d = reinterpret_cast<uint4*>(s_bp + v * kBpCopies);
+      d[0] = make_uint4(e, e, e, e);
+      d[1] = make_uint4(e, e, e, e);
+    }
   }
 }
 
@@ -1360,23 +1377,24 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
     return q * G + min(i, G - 1);
   };
 
-  // Prologue: the first two groups' metadata, the table (copied to LDS), the
-  // first group's raw bytes and activations and its stream words.
+  // Prologue. The table (bounded pairs: its entries into registers; else
+  // the copy to LDS) and the first two groups' metadata are requested first;
+  // the table entries are stored to LDS while the metadata is on its way.
+  // Then the first group's stream words, and right behind them its raw bytes
+  // and activations: the decode starts once the stream words are in (loads
+  // return in order), and the raw bytes of a step are waited for only at that
+  // step's product.
   uint32_t t1 = 0, j1 = 0;
   advance(t1, j1);
   const uint32_t g0 = group(0, 0);
   const uint32_t g1 = rb_of(t1) < RB ? group(t1, j1) : g0;
-  // The stream words are requested before the raw bytes and activations, and
-  // the decode starts once they and the table are in: the raw bytes of a step
-  // are waited for only at that step's product.
+  uint32_t te[kBpPerThread];
+  if constexpr (BP) bp_table_load(a.lut, te); else table_dma(a.lut);
   Meta m0 = load_meta(a, g0, lane);
   Meta m1 = load_meta(a, g1, lane);
-  if constexpr (!BP) table_dma(a.lut);
+  if constexpr (BP) bp_table_store(te);
   u32x4_a4 sw[JT / 4];
   uint32_t pos2 = stream_load<JT>(a, m0, lane, sw) - (BP ? 3u : 0u);
-  // bounded pairs: the table is replicated through registers (its global
-  // copy is hot in the L2), after the stream words were requested
-  if constexpr (BP) bp_table_fill(a.lut);
   uint2 rw[SP];
   uint4 xv[SP];
   {
@@ -1390,8 +1408,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
     }
   }
   stream_store<JT>(cols, sw, lane);
-  // everything but the raw and activation loads (2*SP; SP when decoding):
-  // the table copy (and the metadata and stream words before it)
+  // everything but the raw and activation loads (2*SP; SP when decoding)
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(DEC ? SP : 2 * SP));
   asm volatile("" ::: "memory");
   __syncthreads();
@@ -2054,6 +2071,8 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
 // Grouped launches (multi) exist for S = 64, bounded pairs (bp) for S = 64.
 static hl_status launch_stream(bool xt, bool bp, uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block,
                                size_t lds, hipStream_t s, const StreamArgs& p) {
+  // the bounded-pair table fill takes at most kBpPerThread entries per thread
+  if (bp && block.x < kBpMinThreads) return HL_EINVAL;
   if (bp) return xt ? launch_stream_x<true, true>(seg_len, jt, multi, grid, block, lds, s, p)
                     : launch_stream_x<false, true>(seg_len, jt, multi, grid, block, lds, s, p);
   return xt ? launch_stream_x<true, false>(seg_len, jt, multi, grid, block, lds, s, p)
