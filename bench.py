@@ -54,14 +54,11 @@ HBM_PEAK_GBS = 8000.0
 COLD_BYTES = 1.2 * (1 << 30)
 KERNEL_SRC = os.path.join(ROOT, "paper_2502_00922_amd", "csrc", "kernels.hip")
 STACK_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "stack70b_b1_traffic.txt")
-TRAFFIC_FILES = {"split": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_traffic.txt"),
-                 "whole": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_whole_exponent_traffic.txt"),
-                 "fp16": os.path.join(ROOT, "profiles", "gemv_4096x4096_b1_fp16_traffic.txt")}
 COPY_BYTES = 256 << 20
 # container format -> (encoder keywords, activation dtype of gen_x, weights of the oracle)
 # matrices of the workloads for --counter-run: name -> (workload number, matrix index)
 COUNTER_MATRICES = {"4096x4096": (2, 0), "1024x4096": (4, 1), "14336x4096": (4, 4), "4096x14336": (4, 6),
-                    "28672x8192": (5, 4)}
+                    "8192x8192": (5, 3), "28672x8192": (5, 4)}
 FORMATS = {"split": ({}, "bf16", "bf16"),
            "whole": ({"whole_exponent": True}, "bf16", "bf16"),
            "fp16": ({"fp16": True}, "f16", "fp16")}
@@ -73,7 +70,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20, help="timed token steps of the headline")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--layers", type=int, default=80, help="layers of the 70B-shaped stack (80 = the workload)")
-    ap.add_argument("--matrix-steps", type=int, default=400, help="timed launches per 4096x4096 measurement")
+    ap.add_argument("--matrix-steps", type=int, default=400,
+                    help="launches timed one by one (HIP events) per 4096x4096 measurement")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-compare", action="store_true")
     ap.add_argument("--no-detail", action="store_true", help="only the headline stack (no 4096x4096 detail)")
@@ -91,6 +89,14 @@ def parse():
                     help="print the profile summary of a rocprofv3 --kernel-trace --stats run of the headline "
                          "(run_kernel_stats.csv and run_kernel_trace.csv in TRACE_DIR; the run's JSON line in "
                          "BENCH_LOG) and exit; no GPU needed")
+    ap.add_argument("--ab-run", action="store_true",
+                    help="run only the batch-1 matrix-core against vector-kernel comparison (for a kernel trace)")
+    ap.add_argument("--summarize-runs", nargs=2, metavar=("TRACE_DIR", "RUN_LOG"),
+                    help="print the per-run summary of a rocprofv3 --kernel-trace run of --ab-run (consecutive "
+                         "dispatches of one kernel and grid) and exit; no GPU needed")
+    ap.add_argument("--summarize-counters", nargs="+", metavar="PATH",
+                    help="RUN_LOG DIR [DIR ...]: print the counter summary of rocprofv3 --pmc passes of "
+                         "--counter-run (one directory per pass) and exit; no GPU needed")
     ap.add_argument("--summarize-traffic", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "RUN_LOG"),
                     help="print the HBM-traffic summary of two rocprofv3 --pmc passes (FETCH_SIZE, WRITE_SIZE) of "
                          "--traffic-run and exit; no GPU needed")
@@ -99,23 +105,6 @@ def parse():
 
 def kernel_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
-
-
-def recorded_traffic(batch: int, fmt: str):
-    """HBM bytes per launch from the committed counter summary, if it was taken
-    from the current kernel source for this container format and batch size;
-    else None."""
-    try:
-        text = open(TRAFFIC_FILES[fmt]).read()
-    except OSError:
-        return None
-    h = re.search(r"kernel source sha256\[:16\]: ([0-9a-f]{16})", text)
-    b = re.search(r"batch: (\d+)", text)
-    f = re.search(r"^format: (\w+)", text, re.M)
-    t = re.search(r"traffic_bytes_per_launch: (\d+)", text)
-    if not (h and b and t and f) or h.group(1) != kernel_hash() or int(b.group(1)) != batch or f.group(1) != fmt:
-        return None
-    return int(t.group(1))
 
 
 def recorded_stack_traffic(layers: int):
@@ -158,6 +147,15 @@ def time_graph(torch, launch, nrep, steps, warmup):
         t1.record(stream)
     torch.cuda.synchronize()
     return t0.elapsed_time(t1) / steps
+
+
+def time_graph_long(torch, launch, nrep, target_ms=200.0):
+    """time_graph with a timed region of about target_ms (and a warm-up graph
+    of half that): the GPU's clocks settle only under sustained load, and
+    regions of a few milliseconds read up to 25% slow."""
+    probe = time_graph(torch, launch, nrep, 20, 5)
+    steps = max(20, int(target_ms / probe))
+    return time_graph(torch, launch, nrep, steps, steps // 2)
 
 
 def time_launches(torch, launch, nrep, steps, warmup):
@@ -278,7 +276,7 @@ def measure_container(torch, hl, blob, spec, W, batches, args, single_launches, 
             mean_ms, med_ms, ev_step_ms = time_launches(torch, launch, nrep, args.matrix_steps, 40)
         else:
             mean_ms = med_ms = ev_step_ms = None
-        step_ms = time_graph(torch, launch, nrep, args.matrix_steps, 40)
+        step_ms = time_graph_long(torch, launch, nrep, 100.0)
         rows = list(range(0, R, R // 16))
         y_ref, den = ogemv.gemv_rows(W, xb, rows=rows, weights=FORMATS[fmt][2])
         err = float(np.max(ogemv.rel_err(y.cpu().numpy()[:, rows], y_ref, den)))
@@ -417,7 +415,6 @@ def measure_prefill(torch, hl, blob, spec, W, args, token_counts=(32, 128, 512))
     nrep_b = max(2, math.ceil(COLD_BYTES / (2 * n)))
     wreps = [wdev.clone() for _ in range(nrep_b)]
     out = {}
-    steps = max(10, min(args.matrix_steps, 100))
     for T in token_counts:
         xb = random_x(T, K, seed=T, dtype="bf16")
         xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
@@ -425,11 +422,11 @@ def measure_prefill(torch, hl, blob, spec, W, args, token_counts=(32, 128, 512))
         tensors[0].gemm(xd, y)  # workspaces allocated outside the graph
         for t_ in tensors:
             t_._gemm_ws = tensors[0]._gemm_ws
-        ms = time_graph(torch, lambda i: tensors[i].gemm(xd, y), nrep, steps, 5)
+        ms = time_graph_long(torch, lambda i: tensors[i].gemm(xd, y), nrep, 100.0)
         rows = list(range(0, R, R // 8))
         y_ref, den = ogemv.gemv_rows(W, xb[[0, T - 1]], rows=rows)
         err = float(np.max(ogemv.rel_err(y.cpu().numpy()[[0, T - 1]][:, rows], y_ref, den)))
-        ms_t = time_graph(torch, lambda i: torch.nn.functional.linear(xd, wreps[i]), nrep_b, steps, 5)
+        ms_t = time_graph_long(torch, lambda i: torch.nn.functional.linear(xd, wreps[i]), nrep_b, 100.0)
         out[f"tokens{T}"] = dict(ms=round(ms, 5), effective_weight_GBps=round(2 * n / (ms * 1e-3) / 1e9, 1),
                                  TFLOPs=round(2 * n * T / (ms * 1e-3) / 1e12, 2), max_rel_err=err,
                                  torch_bf16_linear_ms=round(ms_t, 5), speedup_vs_torch=round(ms_t / ms, 3))
@@ -533,7 +530,7 @@ def measure_stack(torch, hl, st, args):
         rows = sorted({0, sp.rows - 1, *range(7, sp.rows, sp.rows // 6)})
         y_ref, den = ogemv.gemv_rows(W, xh[sp.cols], rows=rows)
         err = max(err, float(np.max(ogemv.rel_err(y_host[j][:, rows], y_ref, den))))
-    ms_single = time_graph(torch, single, 1, max(3, args.steps // 4), 2)
+    ms_single = time_graph(torch, single, 1, max(5, args.steps // 4), args.warmup)
     launches = layers * 4
     alg = st["comp"] + layers * (3 * 8192 * 2 + sum(sp.rows * 4 for sp in specs))
     out = dict(ms=ms, ms_single=ms_single, launches=launches, alg_bytes=alg, max_rel_err=err)
@@ -550,9 +547,9 @@ def measure_stack(torch, hl, st, args):
                 for wt, sp in zip(bf[l % len(bf)], specs):
                     torch.nn.functional.linear(xs[sp.cols], wt)
 
-        cs = max(3, args.steps // 4)
-        out["hl_gemv_bf16_ms"] = time_graph(torch, lib_bf16, 1, cs, 2)
-        out["torch_linear_ms"] = time_graph(torch, torch_bf16, 1, cs, 2)
+        cs = max(5, args.steps // 4)
+        out["hl_gemv_bf16_ms"] = time_graph(torch, lib_bf16, 1, cs, args.warmup)
+        out["torch_linear_ms"] = time_graph(torch, torch_bf16, 1, cs, args.warmup)
     return out
 
 
@@ -574,7 +571,7 @@ def mfma_vs_vector(torch, hl):
             reps = [hl.DeviceTensor(blob) for _ in range(max(2, math.ceil(COLD_BYTES / blob.size)))]
             for t_ in reps:
                 t_.workspace()
-            ms = time_graph(torch, lambda i: reps[i].gemv(xd, y), len(reps), 100 if sp.rows < 8192 else 30, 5)
+            ms = time_graph_long(torch, lambda i: reps[i].gemv(xd, y), len(reps))
             r[label] = dict(ms=round(ms, 5), compressed_GBps=round(blob.size / (ms * 1e-3) / 1e9, 1))
             del reps
         out[name] = r
@@ -616,9 +613,6 @@ def matrix_detail(torch, hl, args):
                 e.update(ms_per_single_launch_events=round(rr["mean_ms"], 5),
                          ms_per_step_single_launches=round(rr["ev_step_ms"], 5))
             v[f"batch{b}"] = e
-        tr = recorded_traffic(1, f)
-        if tr is not None:
-            v["batch1"]["traffic_bytes"] = tr
         out[f] = v
     if not args.no_compare:
         for dt_name, Wc in (("bf16", W), ("fp16", Ws["fp16"])):
@@ -629,10 +623,11 @@ def matrix_detail(torch, hl, args):
             for b in batches:
                 _, xd = device_x(torch, spec, b, "split" if dt_name == "bf16" else "fp16")
                 y = torch.empty((b, R), dtype=torch.float32, device="cuda")
-                c = {"torch_linear_ms": time_graph(torch, lambda i: torch.nn.functional.linear(xd, wreps[i]),
-                                                   nrep_b, 200, 10)}
+                c = {"torch_linear_ms": time_graph_long(
+                    torch, lambda i: torch.nn.functional.linear(xd, wreps[i]), nrep_b, 100.0)}
                 if dt_name == "bf16":
-                    c["hl_gemv_bf16_ms"] = time_graph(torch, lambda i: hl.gemv_bf16(wreps[i], xd, y), nrep_b, 200, 10)
+                    c["hl_gemv_bf16_ms"] = time_graph_long(torch, lambda i: hl.gemv_bf16(wreps[i], xd, y), nrep_b,
+                                                           100.0)
                 for f in FORMATS:
                     if f in out and (f == "fp16") == (dt_name == "fp16"):
                         e = out[f][f"batch{b}"]
@@ -781,6 +776,110 @@ def summarize_traffic(fetch_dir, write_dir, run_log):
         f"kernel source sha256[:16]: {t['kernel_sha256_16']}"]))
 
 
+def summarize_runs(trace_dir, run_log):
+    """Kernel-trace summary of --ab-run: the library's dispatches in time
+    order, grouped into runs of consecutive dispatches of one kernel and grid
+    (each timing is a launch outside the graph, a warm-up graph and the timed
+    graph), with the run's mean and median duration; then the run's own line."""
+    d = _json_line(run_log, '"ab_run"')
+    disp = [r for r in _csv_rows(os.path.join(trace_dir, "run_kernel_trace.csv")) if "hl::" in r["Kernel_Name"]]
+    disp.sort(key=lambda r: int(r["Start_Timestamp"]))
+    runs = []
+    for r in disp:
+        key = (r["Kernel_Name"].split("(")[0], r["Grid_Size_X"], r["Workgroup_Size_X"])
+        dur = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        if runs and runs[-1][0] == key:
+            runs[-1][1].append(dur)
+        else:
+            runs.append((key, [dur]))
+    out = ["Runs of consecutive dispatches (kernel, grid x workgroup threads): count, mean and median duration "
+           "of the run's last half (the timed graph's steady state):"]
+    for (name, grid, wg), ds in runs:
+        if len(ds) < 10:
+            continue
+        tail = sorted(ds[len(ds) // 2:])
+        out.append(f"  {name}  grid {grid} x {wg}: {len(ds)} dispatches, mean {sum(tail) / len(tail) / 1e3:.2f} us, "
+                   f"median {tail[len(tail) // 2] / 1e3:.2f} us")
+    out.append("The run's line (graph-timed, HIP events):")
+    for m, r in d["mfma_vs_vector_batch1"].items():
+        out.append(f"  {m}: " + ", ".join(f"{k} {v['ms'] * 1e3:.2f} us ({v['compressed_GBps']} GB/s)"
+                                          for k, v in r.items()))
+    out.append(f"kernel source sha256[:16]: {d['kernel_sha256_16']}")
+    print("\n".join(out))
+
+
+# wave-level counters (units of 4 cycles, per SIMD) and CU-level counters are
+# summed over the chip; the derived figures divide by the chip's 256 CUs and
+# 1024 SIMDs at 2.4 GHz
+N_CU, N_SIMD, CLOCK_GHZ = 256, 1024, 2.4
+
+
+def summarize_counters(run_log, *dirs):
+    """Counter summary of --counter-run: per-dispatch means of every counter of
+    the fused kernel over the passes, per cycle of its median duration, and the
+    derived utilisations (LDS, VALU, matrix core, waits) and instructions per
+    8 weights of a lane."""
+    d = _json_line(run_log, '"counter_run"')
+    vals, durs, name = {}, [], None
+    for dd in dirs:
+        for f in sorted(os.listdir(dd)):
+            if not f.endswith("counter_collection.csv"):
+                continue
+            for r in _csv_rows(os.path.join(dd, f)):
+                if "gemv_stream_kernel" not in r["Kernel_Name"]:
+                    continue
+                name = r["Kernel_Name"]
+                vals.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                durs.append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    if not vals:
+        raise SystemExit("no fused-kernel dispatches in the counter files")
+    dur = sorted(durs)[len(durs) // 2]
+    cyc = dur * CLOCK_GHZ
+    m = {k: sum(v) / len(v) for k, v in vals.items()}
+    rows, cols = (int(t) for t in d["counter_run"].split("x"))
+    out = [f"Kernel: {name}; {d['launches']} dispatches per pass; median duration {dur} ns "
+           f"({cyc:.0f} cycles at {CLOCK_GHZ} GHz).",
+           "Per-dispatch means, and per cycle of the kernel's duration:"]
+    for k in sorted(m):
+        out.append(f"  {k:32s} {m[k]:16.0f} {m[k] / cyc:12.3f} per cycle")
+    out.append("Derived (CU-level counters summed over the CUs, wave-cycle counters in units of 4 cycles, a "
+               "wave64 VALU instruction 4 cycles of its SIMD):")
+
+    def pct(label, v, extra=""):
+        out.append(f"  {label:38s} {100 * v:5.1f}%{extra}")
+
+    if "SQ_BUSY_CU_CYCLES" in m:
+        pct("CUs busy", m["SQ_BUSY_CU_CYCLES"] / (N_CU * cyc))
+    if "SQ_LDS_IDX_ACTIVE" in m:
+        extra = ""
+        if "SQ_LDS_BANK_CONFLICT" in m:
+            extra = f"   (bank-conflict cycles: {100 * m['SQ_LDS_BANK_CONFLICT'] / m['SQ_LDS_IDX_ACTIVE']:.1f}% of them)"
+        pct("LDS unit active, per CU", m["SQ_LDS_IDX_ACTIVE"] / (N_CU * cyc), extra)
+    if "SQ_ACTIVE_INST_VALU" in m:
+        pct("VALU issue, per SIMD", 4 * m["SQ_ACTIVE_INST_VALU"] / (N_SIMD * cyc))
+    if "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+        pct("matrix core busy, per SIMD", m["SQ_VALU_MFMA_BUSY_CYCLES"] / (N_SIMD * cyc))
+    if "SQ_WAVE_CYCLES" in m:
+        if "SQ_WAIT_ANY" in m:
+            pct("wave time in s_waitcnt", m["SQ_WAIT_ANY"] / m["SQ_WAVE_CYCLES"])
+        if "SQ_WAIT_INST_ANY" in m:
+            extra = ""
+            if "SQ_WAIT_INST_LDS" in m:
+                extra = f"   (LDS instructions: {100 * m['SQ_WAIT_INST_LDS'] / m['SQ_WAVE_CYCLES']:.1f}%)"
+            pct("wave time waiting to issue", m["SQ_WAIT_INST_ANY"] / m["SQ_WAVE_CYCLES"], extra)
+    if "SQ_WAVES" in m:
+        per_wave = rows * cols / m["SQ_WAVES"]
+        steps = rows * cols / 8 / 64  # 8-weight steps of a wave, summed over the waves
+        parts = [f"{lab} {m[c] / steps:.1f}" for lab, c in (("VALU", "SQ_INSTS_VALU"), ("LDS", "SQ_INSTS_LDS"),
+                                                            ("SALU", "SQ_INSTS_SALU"), ("MFMA", "SQ_INSTS_MFMA"))
+                 if c in m]
+        out.append(f"  instructions per 8 weights of a lane: {', '.join(parts)} "
+                   f"(whole kernel, {per_wave:.0f} weights per wave)")
+    out.append(f"matrix {d['counter_run']}, format {d['format']}, {d['compressed_bytes']} container bytes")
+    out.append(f"kernel source sha256[:16]: {d['kernel_sha256_16']}")
+    print("\n".join(out))
+
+
 def main():
     args = parse()
     if args.summarize_trace:
@@ -789,11 +888,17 @@ def main():
     if args.summarize_traffic:
         summarize_traffic(*args.summarize_traffic)
         return
+    if args.summarize_runs:
+        summarize_runs(*args.summarize_runs)
+        return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the sharded layout is described in the design notes)", file=sys.stderr)
         sys.exit(2)
-    headline = not (args.workloads or args.counter_run or args.traffic_run)
+    headline = not (args.workloads or args.counter_run or args.traffic_run or args.ab_run)
     # the oracle on all host cores first, in processes forked before anything touches the GPU
     cpu = cpu_oracle_baseline() if headline and not args.no_cpu else None
     import torch
@@ -809,6 +914,10 @@ def main():
         return
     if args.traffic_run:
         traffic_run(torch, hl)
+        return
+    if args.ab_run:
+        print(json.dumps({"ab_run": True, "mfma_vs_vector_batch1": mfma_vs_vector(torch, hl),
+                          "kernel_sha256_16": kernel_hash()}), flush=True)
         return
     if args.counter_run:
         cfg, idx = COUNTER_MATRICES[args.counter_run]
