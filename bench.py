@@ -294,17 +294,16 @@ WORKLOAD_NAMES = {1: "1024x1024 bf16 matrix, fp32 x", 2: "4096x4096 projection w
                   5: "70B-shaped stack, 80 layers of q, k, v, o, gate, up, down (80 resident copies of one layer)"}
 
 
-def measure_workloads(torch, hl, steps_small=50):
-    """One JSON line per workload and batch. A step multiplies every matrix of
-    the workload once, back to back on one stream, in one HIP graph: for the
-    70B stack that is 80 layers x 7 matrices = 560 launches, over 80 resident
-    copies of one generated layer (about 100 GB of containers, so every layer
-    comes from HBM). Smaller workloads rotate over copies of the whole set
-    that together exceed the last-level cache. The comparator is the
-    uncompressed bf16 GEMV (the faster of hl_gemv_bf16 and torch's linear, per
-    step) over cold copies of the bf16 matrices (for the 70B stack 20 copies
-    of the layer, cycled). Workloads with matrices that share x also time the
-    step with each such set (q, k, v; gate, up) in one grouped launch."""
+def measure_workloads(torch, hl):
+    """One JSON line per workload and batch, for the workloads below the 70B
+    stack (whose 80 distinct layers are the headline). A step multiplies every
+    matrix of the workload once, back to back on one stream, in one HIP graph
+    timed over about 100 ms; steps rotate over copies of the whole set that
+    together exceed the last-level cache. The comparator is the uncompressed
+    bf16 GEMV (the faster of hl_gemv_bf16 and torch's linear, per step) over
+    cold copies of the bf16 matrices. Workloads with matrices that share x also
+    time the step with each such set (q, k, v; gate, up) in one grouped
+    launch."""
     from gen import WORKLOADS, workload_matrices, gen_matrix, gen_x
     for w in sorted(WORKLOADS):
         if w == 5:
@@ -330,7 +329,6 @@ def measure_workloads(torch, hl, steps_small=50):
         sets_b = [wb] + [[t.clone() for t in wb] for _ in range(copies_b - 1)]
         torch.cuda.synchronize()
         setup_s = time.perf_counter() - t0
-        steps = 3 if layers > 1 else steps_small
         for B in cfg["batches"]:
             xs = {}
             for s in specs:
@@ -371,12 +369,12 @@ def measure_workloads(torch, hl, steps_small=50):
                         st[j].gemv(xs[specs[j].cols], ys[j])
 
             nrep = max(1, copies // layers)
-            ms = time_graph(torch, fused, nrep, steps, 1)
-            ms_g = time_graph(torch, grouped, nrep, steps, 1) if parts and cfg["x_dtype"] == "bf16" else None
+            ms = time_graph_long(torch, fused, nrep, 100.0)
+            ms_g = time_graph_long(torch, grouped, nrep, 100.0) if parts and cfg["x_dtype"] == "bf16" else None
             nrep_b = max(1, copies_b // layers)
-            ms_b = time_graph(torch, lib_bf16, nrep_b, steps, 1)
+            ms_b = time_graph_long(torch, lib_bf16, nrep_b, 100.0)
             if cfg["x_dtype"] == "bf16":
-                ms_b = min(ms_b, time_graph(torch, torch_bf16, nrep_b, steps, 1))
+                ms_b = min(ms_b, time_graph_long(torch, torch_bf16, nrep_b, 100.0))
             cr = 2 * n / comp
             line = dict(workload=w, name=WORKLOAD_NAMES[w], matrices=len(specs) * layers, batch=B,
                         weights=n * layers, compressed_bytes=comp * layers, compression_ratio=round(cr, 4),
@@ -392,8 +390,8 @@ def measure_workloads(torch, hl, steps_small=50):
                             grouped_speedup_vs_bf16=round(ms_b / ms_g, 3))
             if w == 1:
                 dec = torch.empty(mats[0].shape, dtype=torch.int16, device="cuda")
-                line["decode_ms"] = round(time_graph(torch, lambda i: sets[i % copies][0].decode(dec), copies,
-                                                     steps, 1), 5)
+                line["decode_ms"] = round(time_graph_long(torch, lambda i: sets[i % copies][0].decode(dec), copies,
+                                                          100.0), 5)
             print(json.dumps(line), flush=True)
         del sets, sets_b, base, wb
         torch.cuda.synchronize()
@@ -532,7 +530,8 @@ def measure_stack(torch, hl, st, args):
         err = max(err, float(np.max(ogemv.rel_err(y_host[j][:, rows], y_ref, den))))
     ms_single = time_graph(torch, single, 1, max(5, args.steps // 4), args.warmup)
     launches = layers * 4
-    alg = st["comp"] + layers * (3 * 8192 * 2 + sum(sp.rows * 4 for sp in specs))
+    # per layer: x of the q/k/v, o and gate/up launches (8192 columns) and of down (28672), y of every matrix
+    alg = st["comp"] + layers * ((3 * 8192 + 28672) * 2 + sum(sp.rows * 4 for sp in specs))
     out = dict(ms=ms, ms_single=ms_single, launches=launches, alg_bytes=alg, max_rel_err=err)
     if st["bf16"] and not args.no_compare:
         bf = st["bf16"]
@@ -660,7 +659,7 @@ def traffic_run(torch, hl):
     for _ in range(10):
         dst.copy_(src)
     torch.cuda.synchronize()
-    per_layer = st["comp"] // 4 + 3 * 8192 * 2 + sum(sp.rows * 4 for sp in specs)
+    per_layer = st["comp"] // 4 + (3 * 8192 + 28672) * 2 + sum(sp.rows * 4 for sp in specs)
     print(json.dumps({"traffic_run": True, "kernel_sha256_16": kernel_hash(), "layers": 4, "steps": 3,
                       "launches_per_step": 16, "alg_bytes_per_layer": per_layer,
                       "container_bytes": st["comp"], "copy_bytes": COPY_BYTES, "copies": 10}), flush=True)
