@@ -472,10 +472,14 @@ __device__ inline void decode8(const uint32_t* sc, uint32_t sc_off, uint32_t jma
 // Positions here are column bit positions minus 5: the window's low 16 bits
 // then hold five old bits and the 11-bit index already scaled by 32, the
 // byte offset of the entry's first copy.
-constexpr int kBpBits = 11;
-static_assert(kBpBits == HL_PAIR_MAX, "the encoder's default joint limit is the table window");
+#ifndef HL_BP_BITS
+#define HL_BP_BITS HL_PAIR_MAX
+#endif
+constexpr int kBpBits = HL_BP_BITS;
+static_assert(kBpBits <= (int)HL_PAIR_MAX && kBpBits >= 9, "table window");
 constexpr uint32_t kBpN = 1u << kBpBits;
-constexpr uint32_t kBpCopies = 8;
+constexpr uint32_t kBpCopies = 1u << (14 - kBpBits);
+constexpr uint32_t kBpShift = 16 - kBpBits;  // log2 of an entry's bytes over all copies
 constexpr uint32_t kBpWords = kBpN * kBpCopies;  // 64 KB
 
 // The replicated table, a static LDS array of its own: at a fixed address
@@ -505,14 +509,14 @@ __device__ inline void bp_table_store(const uint32_t (&te)[kBpPerThread]) {
     const uint32_t v = threadIdx.x + k * blockDim.x, e = te[k];
     if (v < kBpN) {
       uint4* d = reinterpret_cast<uint4*>(s_bp + v * kBpCopies);
-      d[0] = make_uint4(e, e, e, e);
-      d[1] = make_uint4(e, e, e, e);
+#pragma unroll
+      for (uint32_t c = 0; c < kBpCopies / 4; ++c) d[c] = make_uint4(e, e, e, e);
     }
   }
 }
 
 __device__ inline uint32_t bp_at(uint32_t w, uint32_t lane_off) {
-  const uint32_t off = (w & ((kBpN - 1) << 5)) | lane_off;
+  const uint32_t off = (w & ((kBpN - 1) << kBpShift)) | lane_off;
   return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_bp) + off);
 }
 
@@ -1394,7 +1398,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
   Meta m1 = load_meta(a, g1, lane);
   if constexpr (BP) bp_table_store(te);
   u32x4_a4 sw[JT / 4];
-  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw) - (BP ? 3u : 0u);
+  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw) - (BP ? kBpShift - 2 : 0u);
   uint2 rw[SP];
   uint4 xv[SP];
   {
@@ -1435,7 +1439,7 @@ __global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) 
       const uint32_t n_c0 = m1.c0;
       // the next group's stream words (this group's again after the last),
       // then the metadata of the group after it
-      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw) - (BP ? 3u : 0u);
+      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw) - (BP ? kBpShift - 2 : 0u);
       m1 = load_meta(a, g2, lane);
       // prefetch source: the next group, else the lane's cached activations
       // (decoding: the current group's raw bytes)
