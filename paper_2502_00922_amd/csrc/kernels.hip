@@ -1288,234 +1288,6 @@ __global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* partial, 
   }
 }
 
-// ------------------------------------------------------------------ persistent fused GEMV
-
-// Persistent form of the matrix-core kernel for S = 8*SP (SP = 4 or 8) and matrices with at
-// least one 16-row block per block of the grid and at least as many column
-// blocks as waves. Block b takes row blocks b, b + grid, ...; its waves take
-// the row block's column blocks wave, wave + waves, ... The table is copied
-// once per block. With DEC it decodes to bf16 instead (hl_decode): a lane
-// keeps its segment's weights (S*2 bytes of one row) and stores them at the
-// group's end, with no activations and no sums.
-//
-// While a wave decodes group k from its LDS columns, group k+1's stream words
-// (JT per lane, four per load), raw bytes and activations are loaded into
-// registers and group k+2's metadata arrives; after the decode the stream
-// words are written to the columns. Only ordinary loads are in flight in the
-// loop (no LDS copies, which the compiler does not order with them), so every
-// wait the compiler places is exact. At a row block's end the waves add their
-// accumulators through their columns in a fixed order (before the next
-// group's words go in) and four waves write y.
-// Arguments of the persistent kernel: up to kMaxParts matrices with the same
-// columns and container geometry that share x (a grouped launch); blocks
-// [part0[m], part0[m + 1]) work on matrix m and write y[m].
-constexpr uint32_t kMaxParts = 4;
-struct StreamArgs {
-  GemvArgs p;  // x, batch (p.g and p.y unused)
-  GroupArgs g[kMaxParts];
-  float* y[kMaxParts];
-  uint32_t part0[kMaxParts + 1];
-  uint32_t n;
-};
-
-// One matrix (Args = GemvArgs), or a grouped launch (Args = StreamArgs: a
-// block first finds its matrix, with a dependent load before its arguments;
-// the one-matrix kernel keeps the small argument block and reads it at fixed
-// places).
-template <class Args>
-__device__ inline const GemvArgs& gemv_args(const Args& x) {
-  if constexpr (std::is_same_v<Args, StreamArgs>) return x.p; else return x;
-}
-
-template <int SP, int JT, bool XT, class Args, bool DEC, bool BP>
-__global__ void __launch_bounds__(DEC ? 512 : 1024) gemv_stream_kernel(Args sa) {
-  constexpr uint32_t S = SP * 8;
-  constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
-  constexpr uint32_t kTab = 0;  // dynamic LDS words before the wave regions
-  static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
-  constexpr bool kMulti = std::is_same_v<Args, StreamArgs>;
-  const GemvArgs& p = gemv_args(sa);
-  // this block's matrix (wave-uniform; its arguments are read in place)
-  const GroupArgs* ap = &p.g;
-  float* yp = p.y;
-  uint32_t bid = blockIdx.x, nblk = gridDim.x;
-  if constexpr (kMulti) {
-    uint32_t m = 0;
-    for (uint32_t k = 1; k < sa.n; ++k) m += blockIdx.x >= sa.part0[k] ? 1u : 0u;
-    ap = &sa.g[m];
-    yp = sa.y[m];
-    bid = blockIdx.x - sa.part0[m];
-    nblk = sa.part0[m + 1] - sa.part0[m];
-  }
-  const GroupArgs& a = *ap;
-  uint16_t* const outp = reinterpret_cast<uint16_t*>(yp);  // decoding: the bf16 output (GemvArgs::y)
-  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t waves = blockDim.x >> 6;
-  uint32_t* cols = s_dyn + kTab + wave * kBuf;
-  const uint32_t jmax = kRows - 3;
-  const uint32_t i = lane & 15, q = lane >> 4;
-  const uint32_t lane_off = (lane % kBpCopies) * 4;  // bounded pairs: the lane's table copy
-  // byte offset of the lane's activations x[n = i][(c0 + q)*S + 8k .. +8) at
-  // x + c0*XSEG + xoff + k*XSTEP, from x itself or (XT) from its tiled copy,
-  // where the 16 batch rows' pieces of one 8-column chunk are 256 contiguous
-  // bytes (a wave-uniform base plus a 32-bit lane offset lets the prefetch
-  // loads address as scalar base + vector offset + immediate)
-  constexpr uint32_t XSEG = XT ? SP * 256 : S * 2, XSTEP = XT ? 256 : 16;
-  const uint32_t xoff = XT ? (q * SP * 16 + i) * 16u : (min(i, p.B - 1) * a.cols + q * S) * 2u;
-  const uint8_t* xbytes = reinterpret_cast<const uint8_t*>(p.x);
-  const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
-  const uint32_t last_group = RB * CB - 1;
-
-  // the wave's groups in order: round t (row block bid + t*nblk of the
-  // block's matrix), step j; branch-free (a branch between a load and its use
-  // makes the compiler's wait for it conservative)
-  auto rb_of = [&](uint32_t t) { return bid + t * nblk; };
-  auto advance = [&](uint32_t& t, uint32_t& j) {
-    const bool same = wave + (j + 1) * waves < CB;
-    t = same ? t : t + 1;
-    j = same ? j + 1 : 0u;
-  };
-  auto group = [&](uint32_t t, uint32_t j) { return min(rb_of(t) * CB + wave + j * waves, last_group); };
-  auto lane_mu = [&](uint32_t rb) {
-    const uint32_t G = min(16u, a.rows - rb * 16);
-    return q * G + min(i, G - 1);
-  };
-
-  // Prologue. The table (bounded pairs: its entries into registers; else
-  // the copy to LDS) and the first two groups' metadata are requested first;
-  // the table entries are stored to LDS while the metadata is on its way.
-  // Then the first group's stream words, and right behind them its raw bytes
-  // and activations: the decode starts once the stream words are in (loads
-  // return in order), and the raw bytes of a step are waited for only at that
-  // step's product.
-  uint32_t t1 = 0, j1 = 0;
-  advance(t1, j1);
-  const uint32_t g0 = group(0, 0);
-  const uint32_t g1 = rb_of(t1) < RB ? group(t1, j1) : g0;
-  uint32_t te[kBpPerThread];
-  if constexpr (BP) bp_table_load(a.lut, te); else table_dma(a.lut);
-  Meta m0 = load_meta(a, g0, lane);
-  Meta m1 = load_meta(a, g1, lane);
-  if constexpr (BP) bp_table_store(te);
-  u32x4_a4 sw[JT / 4];
-  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw) - (BP ? kBpShift - 2 : 0u);
-  uint2 rw[SP];
-  uint4 xv[SP];
-  {
-    const uint32_t rb = g0 / CB;
-    const uint32_t G = min(16u, a.rows - rb * 16);
-    const uint8_t* r = a.raw + m0.first * S + lane_mu(rb) * 8;
-#pragma unroll
-    for (int k = 0; k < SP; ++k) {
-      rw[k] = *reinterpret_cast<const uint2*>(r + k * G * 32u);
-      if constexpr (!DEC) xv[k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff + k * XSTEP);
-    }
-  }
-  stream_store<JT>(cols, sw, lane);
-  // everything but the raw and activation loads (2*SP; SP when decoding)
-  __builtin_amdgcn_s_waitcnt(waitcnt_vm(DEC ? SP : 2 * SP));
-  asm volatile("" ::: "memory");
-  __syncthreads();
-
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-  for (uint32_t t = 0; rb_of(t) < RB; ++t) {
-    const uint32_t rb = rb_of(t);
-    const uint32_t G = min(16u, a.rows - rb * 16);
-    const uint32_t mu = q * G + min(i, G - 1);
-    const uint32_t sc_off = kTab + wave * kBuf + mu;
-    const uint32_t* sc = s_dyn + sc_off;
-    for (uint32_t j = 0; j < nj; ++j) {
-      if (wave + j * waves >= CB) continue;
-      // the next two groups of this wave
-      uint32_t tn = t, jn = j;
-      advance(tn, jn);
-      const bool okn = rb_of(tn) < RB;
-      uint32_t t2 = tn, j2 = jn;
-      advance(t2, j2);
-      const uint32_t g2 = rb_of(t2) < RB ? group(t2, j2) : group(t, j);
-      const uint32_t rbn = okn ? rb_of(tn) : rb;
-      const uint32_t Gn = min(16u, a.rows - rbn * 16);
-      const uint64_t n_first = m1.first;
-      const uint32_t n_c0 = m1.c0;
-      // the next group's stream words (this group's again after the last),
-      // then the metadata of the group after it
-      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw) - (BP ? kBpShift - 2 : 0u);
-      m1 = load_meta(a, g2, lane);
-      // prefetch source: the next group, else the lane's cached activations
-      // (decoding: the current group's raw bytes)
-      const uint32_t cur_c0 = (wave + j * waves) * 4;
-      const uint8_t* rbase = okn    ? a.raw + n_first * S
-                             : DEC ? a.raw + ((uint64_t)rb * 16u * a.L + (uint64_t)cur_c0 * G) * S
-                                   : xbytes + cur_c0 * XSEG;
-      const uint32_t roff = okn ? lane_mu(rbn) * 8 : DEC ? mu * 8 : xoff;
-      const uint32_t rs = okn ? Gn * 32u : 0u;
-      const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * XSEG;
-      uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
-      uint4 dv[DEC ? SP : 1];  // decoding: the lane's weights of the group
-#pragma unroll
-      for (int k = 0; k < SP; ++k) {
-        uint32_t e[8];
-        if constexpr (BP) bp_decode8(sc, jmax, pd, e, lane_off); else decode8(sc, sc_off, jmax, pd, e);
-        uint4 wv;
-        wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
-        wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
-        wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
-        wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
-        if constexpr (DEC) {
-          dv[k] = wv;
-        } else {
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
-                                                        __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
-          mfma_operand_guard();
-          // x first: the wait for the raw bytes at their use then covers both
-          xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
-        }
-        rw[k] = *reinterpret_cast<const uint2*>(rbase + k * rs + roff);
-      }
-      if constexpr (DEC) {
-        // row r0 + i, columns (c0 + q)*S .. + S: stored back to back, so
-        // that each of the lane's cache lines is written whole at once
-        if (i < G) {
-          uint4* o = reinterpret_cast<uint4*>(outp + (uint64_t)(rb * 16 + i) * a.cols + (cur_c0 + q) * S);
-#pragma unroll
-          for (int k = 0; k < SP; ++k) o[k] = dv[k];
-        }
-      }
-      wait_lgkm0();
-      wave_sync_lds();
-      pos2 = pos2n;
-      // the next group's words go in now, unless this was the wave's last
-      // group of the row block (the columns first carry the row block's sum)
-      if (okn && rb_of(tn) == rb) {
-        stream_store<JT>(cols, sw, lane);
-        wait_lgkm0();
-        wave_sync_lds();
-      }
-    }
-    // End of the row block: add the waves' accumulators in a fixed order
-    // (LDS-only barriers: the loads in flight stay in flight).
-    if constexpr (!DEC) {
-      block_sync_lds();
-      float* red = reinterpret_cast<float*>(cols);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) red[v * 64 + lane] = acc[v];
-      acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      block_sync_lds();
-      if (wave < 4) {
-        const uint32_t v = wave;
-        float sum = 0.f;
-        for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + kTab + w * kBuf)[v * 64 + lane];
-        if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
-      }
-      block_sync_lds();
-    }
-    stream_store<JT>(cols, sw, lane);  // the next group's words, held back for the sum
-    wait_lgkm0();
-    wave_sync_lds();
-  }
-  wait_vm0();  // prefetches past the last group
-}
-
 // Tiled copy of bf16 activations for batches above one: xt[c][n][0..8) =
 // x[min(n, B - 1)][8c .. 8c + 8) for the 16 lanes n of a matrix-instruction
 // B operand, so that the 16 lanes reading one 8-column chunk read 256
@@ -1881,6 +1653,266 @@ __global__ void __launch_bounds__(1024) gemv16_mfma_kernel(GemvArgs p) {
   mfma_finish(p, acc, reinterpret_cast<float*>(s_dyn + a.t16_words), wave, waves, lane, rb, kp, r0, G);
 }
 
+// ------------------------------------------------------------------ persistent fused GEMV
+
+// Persistent form of the matrix-core kernel for S = 8*SP (SP = 4 or 8) and matrices with at
+// least one 16-row block per block of the grid and at least as many column
+// blocks as waves. Block b takes row blocks b, b + grid, ...; its waves take
+// the row block's column blocks wave, wave + waves, ... The table is copied
+// once per block. With DEC it decodes to bf16 instead (hl_decode): a lane
+// keeps its segment's weights (S*2 bytes of one row) and stores them at the
+// group's end, with no activations and no sums.
+//
+// While a wave decodes group k from its LDS columns, group k+1's stream words
+// (JT per lane, four per load), raw bytes and activations are loaded into
+// registers and group k+2's metadata arrives; after the decode the stream
+// words are written to the columns. Only ordinary loads are in flight in the
+// loop (no LDS copies, which the compiler does not order with them), so every
+// wait the compiler places is exact. At a row block's end the waves add their
+// accumulators through their columns in a fixed order (before the next
+// group's words go in) and four waves write y.
+// Arguments of the persistent kernel: up to kMaxParts matrices with the same
+// columns and container geometry that share x (a grouped launch); blocks
+// [part0[m], part0[m + 1]) work on matrix m and write y[m].
+constexpr uint32_t kMaxParts = 4;
+struct StreamArgs {
+  GemvArgs p;  // x, batch (p.g and p.y unused)
+  GroupArgs g[kMaxParts];
+  float* y[kMaxParts];
+  uint32_t part0[kMaxParts + 1];
+  uint32_t n;
+};
+
+// One matrix (Args = GemvArgs), or a grouped launch (Args = StreamArgs: a
+// block first finds its matrix, with a dependent load before its arguments;
+// the one-matrix kernel keeps the small argument block and reads it at fixed
+// places).
+template <class Args>
+__device__ inline const GemvArgs& gemv_args(const Args& x) {
+  if constexpr (std::is_same_v<Args, StreamArgs>) return x.p; else return x;
+}
+
+// TB selects the decode table: 0 the joint table (bf16 formats), 1 the
+// bounded-pair table (split format, pairs of at most kBpBits bits), 2 the
+// float16 format's three field tables (at the start of the dynamic LDS, its
+// sign plane instead of raw bytes, the float16 matrix instruction).
+// Blocks of at most 16 waves (8 decoding, 12 for the float16 product, whose
+// longer stream columns need more registers).
+constexpr uint32_t stream_threads(bool dec, int tb) { return dec ? 512 : tb == 2 ? 768 : 1024; }
+
+template <int SP, int JT, bool XT, class Args, bool DEC, int TB>
+__global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Args sa) {
+  constexpr bool BP = TB == 1, F16 = TB == 2;
+  constexpr uint32_t S = SP * 8;
+  constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
+  static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
+  static_assert(!(F16 && std::is_same_v<Args, StreamArgs>), "the float16 form runs one matrix per launch");
+  constexpr bool kMulti = std::is_same_v<Args, StreamArgs>;
+  const GemvArgs& p = gemv_args(sa);
+  // this block's matrix (wave-uniform; its arguments are read in place)
+  const GroupArgs* ap = &p.g;
+  float* yp = p.y;
+  uint32_t bid = blockIdx.x, nblk = gridDim.x;
+  if constexpr (kMulti) {
+    uint32_t m = 0;
+    for (uint32_t k = 1; k < sa.n; ++k) m += blockIdx.x >= sa.part0[k] ? 1u : 0u;
+    ap = &sa.g[m];
+    yp = sa.y[m];
+    bid = blockIdx.x - sa.part0[m];
+    nblk = sa.part0[m + 1] - sa.part0[m];
+  }
+  const GroupArgs& a = *ap;
+  uint16_t* const outp = reinterpret_cast<uint16_t*>(yp);  // decoding: the 16-bit output (GemvArgs::y)
+  const uint32_t lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t waves = blockDim.x >> 6;
+  const uint32_t kTab = F16 ? a.t16_words : 0u;  // dynamic LDS words before the wave regions
+  uint32_t* cols = s_dyn + kTab + wave * kBuf;
+  const uint32_t jmax = kRows - 3;
+  const uint32_t i = lane & 15, q = lane >> 4;
+  const uint32_t lane_off = (lane % kBpCopies) * 4;  // bounded pairs: the lane's table copy
+  // byte offset of the lane's activations x[n = i][(c0 + q)*S + 8k .. +8) at
+  // x + c0*XSEG + xoff + k*XSTEP, from x itself or (XT) from its tiled copy,
+  // where the 16 batch rows' pieces of one 8-column chunk are 256 contiguous
+  // bytes (a wave-uniform base plus a 32-bit lane offset lets the prefetch
+  // loads address as scalar base + vector offset + immediate)
+  constexpr uint32_t XSEG = XT ? SP * 256 : S * 2, XSTEP = XT ? 256 : 16;
+  const uint32_t xoff = XT ? (q * SP * 16 + i) * 16u : (min(i, p.B - 1) * a.cols + q * S) * 2u;
+  const uint8_t* xbytes = reinterpret_cast<const uint8_t*>(p.x);
+  const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
+  const uint32_t last_group = RB * CB - 1;
+
+  // the wave's groups in order: round t (row block bid + t*nblk of the
+  // block's matrix), step j; branch-free (a branch between a load and its use
+  // makes the compiler's wait for it conservative)
+  auto rb_of = [&](uint32_t t) { return bid + t * nblk; };
+  auto advance = [&](uint32_t& t, uint32_t& j) {
+    const bool same = wave + (j + 1) * waves < CB;
+    t = same ? t : t + 1;
+    j = same ? j + 1 : 0u;
+  };
+  auto group = [&](uint32_t t, uint32_t j) { return min(rb_of(t) * CB + wave + j * waves, last_group); };
+  auto lane_mu = [&](uint32_t rb) {
+    const uint32_t G = min(16u, a.rows - rb * 16);
+    return q * G + min(i, G - 1);
+  };
+
+  // Prologue. The table (bounded pairs: its entries into registers; else
+  // the copy to LDS) and the first two groups' metadata are requested first;
+  // the table entries are stored to LDS while the metadata is on its way.
+  // Then the first group's stream words, and right behind them its raw bytes
+  // and activations: the decode starts once the stream words are in (loads
+  // return in order), and the raw bytes of a step are waited for only at that
+  // step's product.
+  uint32_t t1 = 0, j1 = 0;
+  advance(t1, j1);
+  const uint32_t g0 = group(0, 0);
+  const uint32_t g1 = rb_of(t1) < RB ? group(t1, j1) : g0;
+  uint32_t te[kBpPerThread];
+  if constexpr (BP) bp_table_load(a.lut, te);
+  else if constexpr (F16) table16_dma(a);
+  else table_dma(a.lut);
+  Meta m0 = load_meta(a, g0, lane);
+  Meta m1 = load_meta(a, g1, lane);
+  if constexpr (BP) bp_table_store(te);
+  u32x4_a4 sw[JT / 4];
+  uint32_t pos2 = stream_load<JT>(a, m0, lane, sw) - (BP ? kBpShift - 2 : 0u);
+  uint2 rw[F16 ? 1 : SP];  // raw bytes of the next group's steps (bf16 formats)
+  Signs<SP> sg, sgn;       // float16: the lane's sign bytes of this and the next group
+  uint4 xv[SP];
+  {
+    const uint32_t rb = g0 / CB;
+    const uint32_t G = min(16u, a.rows - rb * 16);
+    if constexpr (F16) sg.load(a.raw + (m0.first + lane_mu(rb)) * SP);
+#pragma unroll
+    for (int k = 0; k < SP; ++k) {
+      if constexpr (!F16) rw[k] = *reinterpret_cast<const uint2*>(a.raw + m0.first * S + lane_mu(rb) * 8 + k * G * 32u);
+      if constexpr (!DEC) xv[k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff + k * XSTEP);
+    }
+  }
+  stream_store<JT>(cols, sw, lane);
+  // everything but the raw (or sign) and activation loads
+  constexpr int kRawLoads = F16 ? 1 : SP;
+  __builtin_amdgcn_s_waitcnt(waitcnt_vm(kRawLoads + (DEC ? 0 : SP)));
+  asm volatile("" ::: "memory");
+  __syncthreads();
+
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  for (uint32_t t = 0; rb_of(t) < RB; ++t) {
+    const uint32_t rb = rb_of(t);
+    const uint32_t G = min(16u, a.rows - rb * 16);
+    const uint32_t mu = q * G + min(i, G - 1);
+    const uint32_t sc_off = kTab + wave * kBuf + mu;
+    const uint32_t* sc = s_dyn + sc_off;
+    for (uint32_t j = 0; j < nj; ++j) {
+      if (wave + j * waves >= CB) continue;
+      // the next two groups of this wave
+      uint32_t tn = t, jn = j;
+      advance(tn, jn);
+      const bool okn = rb_of(tn) < RB;
+      uint32_t t2 = tn, j2 = jn;
+      advance(t2, j2);
+      const uint32_t g2 = rb_of(t2) < RB ? group(t2, j2) : group(t, j);
+      const uint32_t rbn = okn ? rb_of(tn) : rb;
+      const uint32_t Gn = min(16u, a.rows - rbn * 16);
+      const uint64_t n_first = m1.first;
+      const uint32_t n_c0 = m1.c0;
+      // the next group's stream words (this group's again after the last),
+      // then the metadata of the group after it
+      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw) - (BP ? kBpShift - 2 : 0u);
+      m1 = load_meta(a, g2, lane);
+      // prefetch source: the next group, else the lane's cached activations
+      // (decoding: the current group's raw bytes)
+      const uint32_t cur_c0 = (wave + j * waves) * 4;
+      const uint8_t* rbase = okn    ? a.raw + n_first * S
+                             : DEC ? a.raw + ((uint64_t)rb * 16u * a.L + (uint64_t)cur_c0 * G) * S
+                                   : xbytes + cur_c0 * XSEG;
+      const uint32_t roff = okn ? lane_mu(rbn) * 8 : DEC ? mu * 8 : xoff;
+      const uint32_t rs = okn ? Gn * 32u : 0u;
+      const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * XSEG;
+      uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
+      uint4 dv[DEC ? SP : 1];  // decoding: the lane's weights of the group
+      // float16: the next group's sign bytes (after the wave's last group of
+      // the launch, the plane's first bytes, discarded)
+      const uint8_t* sgnext = okn ? a.raw + (n_first + lane_mu(rbn)) * SP : a.raw;
+#pragma unroll
+      for (int k = 0; k < SP; ++k) {
+        uint4 wv;
+        if constexpr (F16) {
+          uint32_t h[8];
+          decode8_f16(a, sc, sc_off, jmax, pd, h);
+          wv = pack8_f16(h, sg.byte(k));
+        } else {
+          uint32_t e[8];
+          if constexpr (BP) bp_decode8(sc, jmax, pd, e, lane_off); else decode8(sc, sc_off, jmax, pd, e);
+          wv.x = pack_pair(rw[k].x, 0, e[0], e[1]);
+          wv.y = pack_pair(rw[k].x, 2, e[2], e[3]);
+          wv.z = pack_pair(rw[k].y, 0, e[4], e[5]);
+          wv.w = pack_pair(rw[k].y, 2, e[6], e[7]);
+        }
+        if constexpr (DEC) {
+          dv[k] = wv;
+        } else {
+          if constexpr (F16)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, wv),
+                                                         __builtin_bit_cast(f16x8_t, xv[k]), acc, 0, 0, 0);
+          else
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
+                                                          __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
+          mfma_operand_guard();
+          // x first: the wait for the raw bytes at their use then covers both
+          xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
+        }
+        if constexpr (F16) {
+          if (k == 0) sgn.load(sgnext);
+        } else {
+          rw[k] = *reinterpret_cast<const uint2*>(rbase + k * rs + roff);
+        }
+      }
+      if constexpr (F16) sg = sgn;
+      if constexpr (DEC) {
+        // row r0 + i, columns (c0 + q)*S .. + S: stored back to back, so
+        // that each of the lane's cache lines is written whole at once
+        if (i < G) {
+          uint4* o = reinterpret_cast<uint4*>(outp + (uint64_t)(rb * 16 + i) * a.cols + (cur_c0 + q) * S);
+#pragma unroll
+          for (int k = 0; k < SP; ++k) o[k] = dv[k];
+        }
+      }
+      wait_lgkm0();
+      wave_sync_lds();
+      pos2 = pos2n;
+      // the next group's words go in now, unless this was the wave's last
+      // group of the row block (the columns first carry the row block's sum)
+      if (okn && rb_of(tn) == rb) {
+        stream_store<JT>(cols, sw, lane);
+        wait_lgkm0();
+        wave_sync_lds();
+      }
+    }
+    // End of the row block: add the waves' accumulators in a fixed order
+    // (LDS-only barriers: the loads in flight stay in flight).
+    if constexpr (!DEC) {
+      block_sync_lds();
+      float* red = reinterpret_cast<float*>(cols);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) red[v * 64 + lane] = acc[v];
+      acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      block_sync_lds();
+      if (wave < 4) {
+        const uint32_t v = wave;
+        float sum = 0.f;
+        for (uint32_t w = 0; w < waves; ++w) sum += reinterpret_cast<const float*>(s_dyn + kTab + w * kBuf)[v * 64 + lane];
+        if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
+      }
+      block_sync_lds();
+    }
+    stream_store<JT>(cols, sw, lane);  // the next group's words, held back for the sum
+    wait_lgkm0();
+    wave_sync_lds();
+  }
+  wait_vm0();  // prefetches past the last group
+}
+
 // ------------------------------------------------------------------ bf16 GEMV
 
 // One wave per row; lanes stride the row in 8-weight chunks; dot2 on pairs.
@@ -2031,24 +2063,26 @@ static hl_status launch_gemv_b(bool xbf16, dim3 grid, dim3 block, size_t lds, hi
 
 // Stream words per lane the persistent kernel is built for (the smallest one
 // not below the tensor's longest segment is used), per segment length.
-static int stream_rows_for(uint32_t seg_len, uint32_t col_rows) {
-  static const int kJT64[] = {12, 16, 20}, kJT32[] = {8, 12};
+static int stream_rows_for(uint32_t seg_len, uint32_t col_rows, bool f16) {
+  // the float16 format's codes take about 10 bits per weight, the bf16
+  // formats' about 4
+  static const int kJT64[] = {12, 16, 20}, kJT32[] = {8, 12}, kJT64h[] = {24, 28, 32}, kJT32h[] = {12, 16};
   if (seg_len != 64 && seg_len != 32) return 0;
-  const int* set = seg_len == 64 ? kJT64 : kJT32;
+  const int* set = seg_len == 64 ? (f16 ? kJT64h : kJT64) : (f16 ? kJT32h : kJT32);
   const int n = seg_len == 64 ? 3 : 2;
   for (int k = 0; k < n; ++k)
     if ((uint32_t)set[k] >= col_rows - 1) return set[k];
   return 0;
 }
 
-template <bool XT, bool BP>
+template <bool XT, int TB>
 static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block, size_t lds,
                                  hipStream_t s, const StreamArgs& p) {
   if (seg_len == 64 && multi) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false, BP>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false, BP>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false, BP>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false, TB>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false, TB>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false, TB>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
@@ -2056,16 +2090,16 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
   const GemvArgs& g = p.p;  // one matrix: the small argument block
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false, BP>, grid, block, lds, s, g);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false, BP>, grid, block, lds, s, g);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false, BP>, grid, block, lds, s, g);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false, TB>, grid, block, lds, s, g);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false, TB>, grid, block, lds, s, g);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false, TB>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
-  if constexpr (!BP) {
+  if constexpr (TB == 0) {
     switch (jt) {
-      case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false, false>, grid, block, lds, s, g);
-      case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false, false>, grid, block, lds, s, g);
+      case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false, 0>, grid, block, lds, s, g);
+      case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false, 0>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
@@ -2077,10 +2111,37 @@ static hl_status launch_stream(bool xt, bool bp, uint32_t seg_len, int jt, bool 
                                size_t lds, hipStream_t s, const StreamArgs& p) {
   // the bounded-pair table fill takes at most kBpPerThread entries per thread
   if (bp && block.x < kBpMinThreads) return HL_EINVAL;
-  if (bp) return xt ? launch_stream_x<true, true>(seg_len, jt, multi, grid, block, lds, s, p)
-                    : launch_stream_x<false, true>(seg_len, jt, multi, grid, block, lds, s, p);
-  return xt ? launch_stream_x<true, false>(seg_len, jt, multi, grid, block, lds, s, p)
-            : launch_stream_x<false, false>(seg_len, jt, multi, grid, block, lds, s, p);
+  if (bp) return xt ? launch_stream_x<true, 1>(seg_len, jt, multi, grid, block, lds, s, p)
+                    : launch_stream_x<false, 1>(seg_len, jt, multi, grid, block, lds, s, p);
+  return xt ? launch_stream_x<true, 0>(seg_len, jt, multi, grid, block, lds, s, p)
+            : launch_stream_x<false, 0>(seg_len, jt, multi, grid, block, lds, s, p);
+}
+
+// The float16 format on the persistent kernel (one matrix, float16 x; with
+// DEC its decode to float16).
+template <bool XT, bool DEC>
+static hl_status launch_stream16_x(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                                   const GemvArgs& g) {
+  if (seg_len == 64) {
+    switch (jt) {
+      case 24: return launch(gemv_stream_kernel<8, 24, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+      case 28: return launch(gemv_stream_kernel<8, 28, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+      case 32: return launch(gemv_stream_kernel<8, 32, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+      default: return HL_EUNSUPPORTED;
+    }
+  }
+  switch (jt) {
+    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+    case 16: return launch(gemv_stream_kernel<4, 16, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+    default: return HL_EUNSUPPORTED;
+  }
+}
+
+static hl_status launch_stream16(bool xt, bool dec, uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds,
+                                 hipStream_t s, const GemvArgs& g) {
+  if (dec) return launch_stream16_x<false, true>(seg_len, jt, grid, block, lds, s, g);
+  return xt ? launch_stream16_x<true, false>(seg_len, jt, grid, block, lds, s, g)
+            : launch_stream16_x<false, false>(seg_len, jt, grid, block, lds, s, g);
 }
 
 // Decoding to bf16 with the persistent kernel (p.y = the output).
@@ -2088,15 +2149,15 @@ static hl_status launch_stream_dec(uint32_t seg_len, int jt, dim3 grid, dim3 blo
                                    const GemvArgs& p) {
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, false>, grid, block, lds, s, p);
-      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true, false>, grid, block, lds, s, p);
-      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true, false>, grid, block, lds, s, p);
+      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true, 0>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true, 0>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true, false>, grid, block, lds, s, p);
-    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true, false>, grid, block, lds, s, p);
+    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true, 0>, grid, block, lds, s, p);
+    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
 }
@@ -2240,18 +2301,24 @@ static bool bounded_pairs(const hl_tensor* t) {
 }
 
 static bool stream_shape(const hl_tensor* t, const GroupArgs& ga, int* jt, uint32_t* waves, size_t* per_wave) {
-  if (is_fp16(t) || t->grp_rows != 16 || (t->seg_len != 64 && t->seg_len != 32)) return false;
+  if (t->grp_rows != 16 || (t->seg_len != 64 && t->seg_len != 32)) return false;
   const uint32_t CB = ga.CB, RB = ga.RB, cus = (uint32_t)device_cus();
-  *jt = stream_rows_for(t->seg_len, ga.col_rows);
-  const size_t tab = bounded_pairs(t) ? (size_t)kBpWords * 4 : (size_t)(kLutN + kAuxWords) * 4;
+  *jt = stream_rows_for(t->seg_len, ga.col_rows, is_fp16(t));
+  const size_t tab = is_fp16(t)         ? (size_t)ga.t16_words * 4
+                     : bounded_pairs(t) ? (size_t)kBpWords * 4
+                                        : (size_t)(kLutN + kAuxWords) * 4;
   *per_wave = (size_t)(*jt + 1) * kCol * 4;
-  uint32_t w = kMaxWaves;
+  uint32_t w = std::min<uint32_t>(kMaxWaves, stream_threads(false, is_fp16(t) ? 2 : 0) / 64);
   while (w > 1 && tab + w * *per_wave > kMaxLds) --w;
   // fewer waves per block when that gives every wave two groups: the
   // second group's loads then overlap the first one's decode
   while (w > 8 && (uint64_t)RB * CB < 2ull * cus * w) --w;
   *waves = w;
-  return *jt && w >= 8 && CB >= w && RB >= cus && (uint64_t)RB * CB >= 2ull * cus * w;
+  // float16: two row blocks per CU at least (4096x4096, one per CU: 25.9 us
+  // against 24.3 us on the non-persistent kernel; 14336x4096 65.8 against
+  // 86.2 us)
+  const uint32_t min_rb = is_fp16(t) ? 2 * cus : cus;
+  return *jt && w >= 8 && CB >= w && RB >= min_rb && (uint64_t)RB * CB >= 2ull * cus * w;
 }
 
 extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stream) {
@@ -2273,6 +2340,11 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
     p.C = pl.ga.CB;
     p.KS = 1;
     w = 8;  // the kernel's bound when decoding (registers for a group's weights)
+    const dim3 grid(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus()));
+    // float16: its tables lead the dynamic LDS
+    if (is_fp16(t))
+      return launch_stream16(false, true, t->seg_len, jt, grid, dim3(w * 64),
+                             (size_t)pl.ga.t16_words * 4 + w * per_wave, (hipStream_t)stream, p);
     // the decode form keeps the joint table (the bounded-pair form measured
     // slower here: 28672x8192 307 us against 273 us)
     return launch_stream_dec(t->seg_len, jt, dim3(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus())),
@@ -2418,10 +2490,22 @@ static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, f
   p.x = x_dev;
   p.y = y_dev;
   p.B = batch;
+  // large matrices: the persistent kernel (S = 32 or 64, a row block per CU
+  // and two groups per wave), its tables ahead of the wave regions
+  int jt = 0;
   uint32_t w = 0;
+  size_t per_wave = 0;
+  bool xt = false;
+  if (stream_shape(t, pl.ga, &jt, &w, &per_wave)) {
+    st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, stream, &p, &xt);
+    if (st != HL_OK) return st;
+    p.C = pl.ga.CB;
+    p.KS = 1;
+    return launch_stream16(xt, false, t->seg_len, jt, dim3(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus())),
+                           dim3(w * 64), (size_t)pl.ga.t16_words * 4 + w * per_wave, stream, p);
+  }
   st = choose_split(t, pl, batch, workspace_dev, workspace_bytes, clear, stream, &p, &w);
   if (st != HL_OK) return st;
-  bool xt = false;
   st = tile_activations(t, x_dev, batch, workspace_dev, workspace_bytes, stream, &p, &xt);
   if (st != HL_OK) return st;
   const dim3 grid(pl.ga.RB * p.KS), block(w * 64);
@@ -2455,6 +2539,10 @@ static uint64_t gemv_need(const hl_tensor* t, hl_dtype x_dtype, uint32_t batch) 
   Plan pl;
   if (is_fp16(t)) {
     if (x_dtype != HL_F16 || make_plan(t, 0, false, &pl) != HL_OK) return 0;
+    int jt = 0;
+    uint32_t w = 0;
+    size_t per_wave = 0;
+    if (stream_shape(t, pl.ga, &jt, &w, &per_wave)) return xtile_region(t, batch);
   } else {
     bool mfma = false, persistent = false;
     uint32_t xw = 0;
@@ -2611,7 +2699,7 @@ extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t c
   uint64_t groups = 0, rbs = 0;
   for (uint32_t k = 0; k < count && grouped; ++k) {
     if (make_plan(ts[k], 0, false, &pl[k]) != HL_OK) return HL_EINVAL;
-    const int j = stream_rows_for(ts[k]->seg_len, pl[k].ga.col_rows);
+    const int j = stream_rows_for(ts[k]->seg_len, pl[k].ga.col_rows, false);
     grouped = j != 0;
     jt = std::max(jt, j);
     groups += (uint64_t)pl[k].ga.RB * pl[k].ga.CB;

@@ -176,3 +176,36 @@ def test_unsupported_requests(torch):
     db = hl.DeviceTensor(hl.encode(random_bf16((64, 512), seed=1)))
     with pytest.raises(hl.HLError):
         db.gemv(torch.zeros((1, 512), dtype=torch.float16, device="cuda"))
+
+
+@pytest.mark.parametrize("S,cols", [(64, 4096), (32, 2048)])
+@pytest.mark.parametrize("kind", ["gaussian", "long_pairs", "window_overflow"])
+def test_persistent_kernel(torch, S, cols, kind):
+    """Matrices with two row blocks per CU and two groups per wave (8196
+    rows: a ragged last row block) run the persistent kernel's float16 form: its
+    product against a float64 product of the exact float16 values (every row)
+    and the oracle (sampled rows) at batch 1, 5 and 16, and its decode form
+    bit-exact. The planted window overflows take the bit-serial path inside
+    the persistent loop."""
+    rows = 8196
+    print(f"fp16 persistent S={S} {rows}x{cols} {kind}", flush=True)
+    if kind == "gaussian":
+        w = random_fp16((rows, cols), seed=S + cols)
+    elif kind == "long_pairs":
+        w = _long_pairs(rows, cols, seed=S)
+    else:
+        w = _window_overflow(rows, cols, seed=S)
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=S, fp16=True))
+    assert dt.view.grp_rows == 16
+    wf = w.view(np.float16).astype(np.float64)
+    rng = np.random.default_rng(S)
+    sample = sorted({0, 15, 16, rows - 5, rows - 4, rows - 1} | set(int(r) for r in rng.integers(0, rows, 10)))
+    for batch in (1, 5, 16):
+        x = random_x(batch, cols, seed=batch, dtype="f16")
+        y = dt.gemv(_x(torch, x)).cpu().numpy().astype(np.float64)
+        xf = x.astype(np.float64)
+        err = np.abs(y - xf @ wf.T) / (np.abs(xf) @ np.abs(wf).T + 1e-30)
+        assert err.max() <= TOL, (batch, float(err.max()))
+        yo, do = ogemv.gemv_rows(w, x, rows=sample, weights="fp16")
+        assert (np.abs(y[:, sample] - yo) / (do + 1e-30)).max() <= TOL
+    assert np.array_equal(_decode(torch, dt), w)
