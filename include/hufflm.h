@@ -343,18 +343,21 @@ hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const
                                hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
                                void* workspace_dev, size_t workspace_bytes, void* stream);
 
-/* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows
- * (partial sums of up to one range per column block of four segments); 0 for
+/* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows:
+ * up to 112 tokens the partial sums of up to one range per column block of
+ * four segments, beyond that the decoded weights (rows * cols * 2); 0 for
  * tensors it does not take. */
 size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
 
 /* Prefill product Y[n][r] = sum_k W[r][k] * X[n][k] for n < tokens (many
- * activation rows; the paper's prompts of tens of tokens, Sec. 4): each
- * 16-row x 4-segment weight tile is decoded once per chunk of up to 128
- * tokens and multiplied with all of them on the matrix cores (Sec. 3.2:
- * weights decompressed only to be multiplied). x_dev: [tokens][cols] bf16;
- * y_dev: [tokens][rows] float32 (fully written); fp32 accumulation, every
- * output summed in a fixed order. bf16 formats (split or whole exponent) with
+ * activation rows; the paper's prompts of tens of tokens, Sec. 4). Up to 112
+ * tokens each 16-row x 4-segment weight tile is decoded once per chunk of up
+ * to 128 tokens and multiplied with all of them on the matrix cores (Sec.
+ * 3.2: weights decompressed only to be multiplied), every output summed in a
+ * fixed order; beyond that, where the product is compute-bound (Sec. 5), the
+ * matrix is decoded once into the workspace (hl_decode) and multiplied by
+ * hipBLASLt. x_dev: [tokens][cols] bf16; y_dev: [tokens][rows] float32 (fully
+ * written); fp32 accumulation. bf16 formats (split or whole exponent) with
  * 16-row groups and S = 32 or 64; others give HL_EUNSUPPORTED.
  * workspace_dev: hl_gemm_workspace_bytes(t, tokens) bytes (no initial
  * contents needed); calls that may run concurrently need separate

@@ -18,6 +18,8 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-munsafe-fp-atomics",
     "-Wall", "-Wno-unused-result",
+    # the prefill product of many tokens multiplies the decoded weights with hipBLASLt
+    "-lhipblaslt",
 ]
 
 

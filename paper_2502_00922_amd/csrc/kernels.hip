@@ -23,6 +23,7 @@
 // group's stream words into registers while it decodes the current group (in
 // its decode form it also decodes large matrices to bf16).
 #include <hip/hip_runtime.h>
+#include <hipblaslt/hipblaslt.h>
 
 #include <algorithm>
 #include <type_traits>
@@ -2455,18 +2456,18 @@ static hl_status launch_mfma16(bool xt, uint32_t steps, dim3 grid, dim3 block, s
             : launch_mfma16_x<false>(steps, grid, block, lds, s, p);
 }
 
-// Float16 format: the matrix-core kernel only (16-row groups, float16 x).
 // Larger batches on the matrix cores read the activations from a tiled copy
 // in the workspace (when it is large enough): the copy costs a launch (about
 // 2.5 us), and reading 16 rows per 8-column chunk costs more the larger the
 // batch and the matrix (4096x4096: +1.5 us at batch 8; 28672x8192: +3.5 us at
-// batch 4, +41 us at batch 8, +109 us at batch 16). On success with a tiled
-// copy, p->x points to it and *xt is set.
+// batch 4, +41 us at batch 8, +109 us at batch 16; the 8B layer's grouped
+// step at batch 5-7 124-142 us read directly, 120 us tiled at batch 8). On
+// success with a tiled copy, p->x points to it and *xt is set.
 static hl_status tile_activations(const hl_tensor* t, const void* x_dev, uint32_t batch, void* workspace_dev,
                                   size_t workspace_bytes, hipStream_t stream, GemvArgs* p, bool* xt) {
   *xt = false;
   const uint64_t n = t->rows * t->cols;
-  const bool want = batch >= 12 || (batch >= 8 && n >= (32ull << 20)) || (batch >= 4 && n >= (128ull << 20));
+  const bool want = batch >= 12 || (batch >= 5 && n >= (32ull << 20)) || (batch >= 4 && n >= (128ull << 20));
   if (!want || !workspace_dev || workspace_bytes < xtile_region(t, batch)) return HL_OK;
   uint4* tile = reinterpret_cast<uint4*>(workspace_dev);
   const uint32_t chunks = (uint32_t)(t->cols / 8);
@@ -2478,6 +2479,8 @@ static hl_status tile_activations(const hl_tensor* t, const void* x_dev, uint32_
   return HL_OK;
 }
 
+// Float16 format (16-row groups, float16 x): the persistent kernel's float16
+// form for large matrices, else the matrix-core kernel.
 static hl_status gemv16(const hl_tensor* t, const void* x_dev, uint32_t batch, float* y_dev, void* workspace_dev,
                         size_t workspace_bytes, bool clear, hipStream_t stream) {
   if (t->grp_rows != 16 || t->seg_len % 8 || !mfma_steps_ok(t->seg_len / 8)) return HL_EUNSUPPORTED;
@@ -2773,10 +2776,78 @@ constexpr uint32_t kGemmMaxTiles = 8;  // token tiles of 16 per block
 
 static uint32_t gemm_row_sets(const hl_tensor* t) { return (uint32_t)((t->rows + 255) / 256); }
 
+// Prefill above this many tokens: the weights are decoded once to bf16 in the
+// workspace and multiplied by the vendor GEMM (hipBLASLt). Up to it the fused
+// kernel decodes each tile once per chunk of up to 128 tokens (4096x4096: 24.6
+// us at 32 tokens, 50.3 us at 128; decode + GEMM 42 us at 129 tokens, 51 us at
+// 512, where the fused kernel, decoding four times, took 110 us).
+constexpr uint32_t kGemmFusedMaxTokens = 112;
+
 extern "C" size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens) {
   if (!t || tokens == 0 || t->seg_len == 0 || t->grp_rows != 16) return 0;
+  if (tokens > kGemmFusedMaxTokens) return (size_t)(t->rows * t->cols * 2);  // the decoded weights
   const uint64_t CB = (t->cols / t->seg_len) / 4;
   return (size_t)(CB * tokens * t->rows * 4);
+}
+
+// One hipBLASLt handle per GPU, created on first use with that GPU current.
+static std::mutex g_lt_mu;
+static hipblasLtHandle_t g_lt[kMaxDevices];
+
+static hl_status lt_handle(hipblasLtHandle_t* out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return HL_EHIP;
+  if (dev >= kMaxDevices) return HL_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_lt_mu);
+  if (!g_lt[dev] && hipblasLtCreate(&g_lt[dev]) != HIPBLAS_STATUS_SUCCESS) {
+    g_lt[dev] = nullptr;
+    return HL_EHIP;
+  }
+  *out = g_lt[dev];
+  return HL_OK;
+}
+
+// Y[n][r] = sum_k W[r][k] X[n][k] from bf16 W [rows][cols] and X [tokens][cols]
+// into float32 Y [tokens][rows]: in column-major terms D (rows x tokens, ld
+// rows) = A^T B with A = W as a cols x rows matrix and B = X as cols x tokens.
+// No GEMM workspace (an algorithm that needs none), so nothing is cleared on
+// the stream.
+static hl_status gemm_bf16_lt(const uint16_t* w, const uint16_t* x, float* y, uint64_t rows, uint64_t cols,
+                              uint32_t tokens, hipStream_t stream) {
+  hipblasLtHandle_t h = nullptr;
+  hl_status st = lt_handle(&h);
+  if (st != HL_OK) return st;
+  hipblasLtMatmulDesc_t op = nullptr;
+  hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, ld = nullptr;
+  hipblasLtMatmulPreference_t pref = nullptr;
+  st = HL_EHIP;
+  const hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
+  const uint64_t no_ws = 0;
+  hipblasLtMatmulHeuristicResult_t heur[1];
+  int found = 0;
+  const float alpha = 1.f, beta = 0.f;
+  if (hipblasLtMatmulDescCreate(&op, HIPBLAS_COMPUTE_32F, HIP_R_32F) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatmulDescSetAttribute(op, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof(ta)) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatmulDescSetAttribute(op, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof(tb)) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatrixLayoutCreate(&la, HIP_R_16BF, cols, rows, (int64_t)cols) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatrixLayoutCreate(&lb, HIP_R_16BF, cols, tokens, (int64_t)cols) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatrixLayoutCreate(&ld, HIP_R_32F, rows, tokens, (int64_t)rows) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatmulPreferenceCreate(&pref) == HIPBLAS_STATUS_SUCCESS &&
+      hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &no_ws,
+                                            sizeof(no_ws)) == HIPBLAS_STATUS_SUCCESS) {
+    if (hipblasLtMatmulAlgoGetHeuristic(h, op, la, lb, ld, ld, pref, 1, heur, &found) != HIPBLAS_STATUS_SUCCESS ||
+        found < 1)
+      st = HL_EUNSUPPORTED;
+    else if (hipblasLtMatmul(h, op, &alpha, w, la, x, lb, &beta, y, ld, y, ld, &heur[0].algo, nullptr, 0,
+                             stream) == HIPBLAS_STATUS_SUCCESS)
+      st = HL_OK;
+  }
+  if (pref) hipblasLtMatmulPreferenceDestroy(pref);
+  if (ld) hipblasLtMatrixLayoutDestroy(ld);
+  if (lb) hipblasLtMatrixLayoutDestroy(lb);
+  if (la) hipblasLtMatrixLayoutDestroy(la);
+  if (op) hipblasLtMatmulDescDestroy(op);
+  return st;
 }
 
 template <int SP>
@@ -2797,6 +2868,14 @@ extern "C" hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dt
   if (x_dtype != HL_BF16 || is_fp16(t) || t->grp_rows != 16 || (t->seg_len != 32 && t->seg_len != 64))
     return HL_EUNSUPPORTED;
   if (!workspace_dev || workspace_bytes < hl_gemm_workspace_bytes(t, tokens)) return HL_EINVAL;
+  if (tokens > kGemmFusedMaxTokens) {
+    // many tokens: decode once (bit-exact bf16 in the workspace), then the GEMM
+    uint16_t* w = reinterpret_cast<uint16_t*>(workspace_dev);
+    const hl_status st = hl_decode(t, w, stream);
+    if (st != HL_OK) return st;
+    return gemm_bf16_lt(w, reinterpret_cast<const uint16_t*>(x_dev), y_dev, t->rows, t->cols, tokens,
+                        (hipStream_t)stream);
+  }
   Plan pl;
   hl_status st = make_plan(t, 0, false, &pl);
   if (st != HL_OK) return st;
