@@ -122,9 +122,12 @@ def recorded_stack_traffic(layers: int):
     return int(t.group(1)) * layers
 
 
-def time_graph(torch, launch, nrep, steps, warmup):
+def time_graph(torch, launch, nrep, steps, warmup, replays=1):
     """Per-step time (ms) of `steps` back-to-back launches captured in one HIP
-    graph (after a graph of `warmup` launches), events on the capture stream."""
+    graph (after a graph of `warmup` launches), events on the capture stream.
+    With replays > 1 the timed graph is replayed that many times in a row and
+    the list of per-step times is returned (the first is the single-replay
+    figure)."""
     stream = torch.cuda.Stream()
     stream.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(stream):
@@ -138,15 +141,17 @@ def time_graph(torch, launch, nrep, steps, warmup):
         for i in range(steps):
             launch((warmup + i) % nrep)
     torch.cuda.synchronize()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(replays + 1)]
     with torch.cuda.stream(stream):
         gw.replay()
         torch.cuda.synchronize()
-        t0.record(stream)
-        gt.replay()
-        t1.record(stream)
+        ev[0].record(stream)
+        for r in range(replays):
+            gt.replay()
+            ev[r + 1].record(stream)
     torch.cuda.synchronize()
-    return t0.elapsed_time(t1) / steps
+    per = [ev[r].elapsed_time(ev[r + 1]) / steps for r in range(replays)]
+    return per if replays > 1 else per[0]
 
 
 def time_graph_long(torch, launch, nrep, target_ms=200.0):
@@ -519,7 +524,10 @@ def measure_stack(torch, hl, st, args):
             for j, sp in enumerate(specs):
                 row[j].gemv(xs[sp.cols], ys[j])
 
-    ms = time_graph(torch, grouped, 1, args.steps, args.warmup)
+    # the timed graph (K steps after W warm-up steps), then four more replays
+    # of it for the spread
+    ms_replays = time_graph(torch, grouped, 1, args.steps, args.warmup, replays=5)
+    ms = ms_replays[0]
     # parity of the timed step: the outputs now hold the last layer's products
     y_host = [y.cpu().numpy() for y in ys]
     err = 0.0
@@ -532,7 +540,8 @@ def measure_stack(torch, hl, st, args):
     launches = layers * 4
     # per layer: x of the q/k/v, o and gate/up launches (8192 columns) and of down (28672), y of every matrix
     alg = st["comp"] + layers * ((3 * 8192 + 28672) * 2 + sum(sp.rows * 4 for sp in specs))
-    out = dict(ms=ms, ms_single=ms_single, launches=launches, alg_bytes=alg, max_rel_err=err)
+    out = dict(ms=ms, ms_replays=ms_replays, ms_single=ms_single, launches=launches, alg_bytes=alg,
+               max_rel_err=err)
     if st["bf16"] and not args.no_compare:
         bf = st["bf16"]
 
@@ -949,7 +958,9 @@ def main():
         compressed_GBps=round(comp / (ms * 1e-3) / 1e9, 1),
         ms_per_step_one_launch_per_matrix=round(r["ms_single"], 4),
         compressed_GBps_one_launch_per_matrix=round(comp / (r["ms_single"] * 1e-3) / 1e9, 1),
-        max_rel_err_last_layer=r["max_rel_err"], launch_bytes=st["launch_bytes"])
+        max_rel_err_last_layer=r["max_rel_err"], launch_bytes=st["launch_bytes"],
+        ms_per_step_replays=[round(v, 4) for v in r["ms_replays"]],
+        ms_per_step_p10_median_p90=[round(float(np.percentile(r["ms_replays"], q)), 4) for q in (10, 50, 90)])
     if "hl_gemv_bf16_ms" in r:
         best = min(r["hl_gemv_bf16_ms"], r["torch_linear_ms"])
         stack_detail.update(
@@ -957,6 +968,7 @@ def main():
                 r["torch_linear_ms"], 4),
             bf16_GBps=round(2 * n / (best * 1e-3) / 1e9, 1),
             speedup_vs_best_uncompressed=round(best / ms, 3), speedup_target=round(0.9 * cr, 3),
+            compressed_rate_over_bf16_stream=round((comp / (ms * 1e-3)) / (2 * n / (best * 1e-3)), 3),
             comparator_note=f"uncompressed bf16 GEMV of {len(st['bf16'])} resident layers cycled over the "
                             f"{layers} layer slots, same launches per matrix")
     extra = {"stack70b": stack_detail}
