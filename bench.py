@@ -74,6 +74,8 @@ def parse():
                     help="launches timed one by one (HIP events) per 4096x4096 measurement")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-compare", action="store_true")
+    ap.add_argument("--no-prefetch", action="store_true",
+                    help="launches of the headline step without reading the next launch's first groups ahead")
     ap.add_argument("--no-detail", action="store_true", help="only the headline stack (no 4096x4096 detail)")
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the launches the byte-counter passes measure")
@@ -493,6 +495,16 @@ def build_stack(torch, hl, layers: int, keep_bf16: int):
                 setup_s=time.perf_counter() - t0, encode_s=enc_s)
 
 
+def stack_launches(stack, ys):
+    """The launches of one token step over the stack, in order: per layer
+    q/k/v grouped, o, gate/up grouped, down; (tensors, x columns, outputs)."""
+    out = []
+    for row in stack:
+        out += [([row[j] for j in (0, 1, 2)], 8192, [ys[j] for j in (0, 1, 2)]), ([row[3]], 8192, [ys[3]]),
+                ([row[j] for j in (4, 5)], 8192, [ys[j] for j in (4, 5)]), ([row[6]], 28672, [ys[6]])]
+    return out
+
+
 def measure_stack(torch, hl, st, args):
     """One token step (batch 1) through the stack, as HIP graphs: grouped
     (q, k, v and gate, up in one launch each: 4 launches per layer) and one
@@ -510,14 +522,14 @@ def measure_stack(torch, hl, st, args):
             xh[sp.cols] = gen_x(sp, 1, "bf16")
     xs = {k: torch.from_numpy(v.view(np.int16)).view(torch.bfloat16).cuda() for k, v in xh.items()}
     ys = [torch.empty((1, sp.rows), dtype=torch.float32, device="cuda") for sp in specs]
-    qkv, gu = (0, 1, 2), (4, 5)
+    launches = stack_launches(stack, ys)
 
     def grouped(i):
-        for row in stack:
-            hl.gemv_multi([row[j] for j in qkv], xs[8192], [ys[j] for j in qkv])
-            row[3].gemv(xs[8192], ys[3])
-            hl.gemv_multi([row[j] for j in gu], xs[8192], [ys[j] for j in gu])
-            row[6].gemv(xs[28672], ys[6])
+        # each launch reads the next one's first groups into the caches
+        # during its last ones (the step's last launch: the next step's first)
+        for k, (ts, c, yy) in enumerate(launches):
+            nxt = None if args.no_prefetch else launches[(k + 1) % len(launches)][0]
+            hl.gemv_multi(ts, xs[c], yy, prefetch=nxt)
 
     def single(i):
         for row in stack:
@@ -648,7 +660,7 @@ def matrix_detail(torch, hl, args):
     return out
 
 
-def traffic_run(torch, hl):
+def traffic_run(torch, hl, args):
     """The launches of the byte-counter passes: 3 grouped token steps over a
     4-layer stack, then 10 plain 256 MiB device copies (calibration)."""
     st = build_stack(torch, hl, 4, 0)
@@ -657,12 +669,11 @@ def traffic_run(torch, hl):
     specs = workload_matrices(5, 0)
     xs = {sp.cols: torch.from_numpy(gen_x(sp, 1, "bf16").view(np.int16)).view(torch.bfloat16).cuda() for sp in specs}
     ys = [torch.empty((1, sp.rows), dtype=torch.float32, device="cuda") for sp in specs]
+    launches = stack_launches(stack, ys)
     for _ in range(3):
-        for row in stack:
-            hl.gemv_multi([row[j] for j in (0, 1, 2)], xs[8192], [ys[j] for j in (0, 1, 2)])
-            row[3].gemv(xs[8192], ys[3])
-            hl.gemv_multi([row[j] for j in (4, 5)], xs[8192], [ys[j] for j in (4, 5)])
-            row[6].gemv(xs[28672], ys[6])
+        for k, (ts, c, yy) in enumerate(launches):
+            nxt = None if args.no_prefetch else launches[(k + 1) % len(launches)][0]
+            hl.gemv_multi(ts, xs[c], yy, prefetch=nxt)
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
     dst = torch.empty_like(src)
     for _ in range(10):
@@ -921,7 +932,7 @@ def main():
         measure_workloads(torch, hl)
         return
     if args.traffic_run:
-        traffic_run(torch, hl)
+        traffic_run(torch, hl, args)
         return
     if args.ab_run:
         print(json.dumps({"ab_run": True, "mfma_vs_vector_batch1": mfma_vs_vector(torch, hl),
@@ -994,7 +1005,9 @@ def main():
         "config": {"workload": f"70B-shaped weight stack, {layers} layers x (q, o 8192x8192; k, v 1024x8192; "
                                "gate, up 28672x8192; down 8192x28672), every matrix drawn from its own seed "
                                "(N(0,0.02) + 0.1% outliers x20), resident compressed; one decode step, batch 1, "
-                               "fused decode-GEMV of every matrix (q/k/v and gate/up grouped)",
+                               "fused decode-GEMV of every matrix (q/k/v and gate/up grouped"
+                               + ("" if args.no_prefetch else "; each launch reads the next one's first groups "
+                                  "into the caches during its last ones") + ")",
                    "batch": 1, "x_dtype": "bf16", "seg_len": 64, "format": "bf16, split exponent (4+4)",
                    "compressed_bytes": comp, "compression_ratio": round(cr, 4),
                    "bits_per_weight": round(8 * comp / n, 4)},
