@@ -521,7 +521,9 @@ __device__ inline uint32_t bp_at(uint32_t w, uint32_t lane_off) {
   return *reinterpret_cast<const uint32_t*>(reinterpret_cast<const uint8_t*>(s_bp) + off);
 }
 
-__device__ inline void bp_lookup4(uint64_t W, uint32_t& p, uint32_t* e, uint32_t lane_off) {
+// Four table reads from the window W, shifted past each pair read (W ends
+// shifted past all four).
+__device__ inline void bp_lookup4(uint64_t& W, uint32_t* e, uint32_t lane_off) {
   e[0] = bp_at((uint32_t)W, lane_off);
   W = shift_window(W, e[0]);
   e[1] = bp_at((uint32_t)W, lane_off);
@@ -529,23 +531,30 @@ __device__ inline void bp_lookup4(uint64_t W, uint32_t& p, uint32_t* e, uint32_t
   e[2] = bp_at((uint32_t)W, lane_off);
   W = shift_window(W, e[2]);
   e[3] = bp_at((uint32_t)W, lane_off);
-  p = p + e[0] + e[1] + e[2] + e[3];
 }
 
-// decode8 for bounded pairs: no branch. jmax - 1 bounds the first of the
-// four rows read (columns hold three rows of overrun).
+// decode8 for bounded pairs: no branch. The first window is bits [p, p + 64)
+// of four column words; the four pairs read from it take at most 44 bits,
+// and the second window is what is left of it with the next 32 bits of the
+// words (bits [p + 64, p + 96)) put right behind: at least 52 bits, more than
+// the 49 its four lookups can reach. (Fields of one symbol have 0-bit codes:
+// four pairs take at least 4 bits, except where both fields have one symbol,
+// and then every window reads one and the same entry, so the refill's place
+// does not matter.) jmax - 1
+// bounds the first of the four rows read (columns hold three rows of overrun).
 __device__ inline void bp_decode8(const uint32_t* sc, uint32_t jmax, uint32_t& pos5, uint32_t* e,
                                   uint32_t lane_off) {
-  uint32_t p = pos5;
+  const uint32_t p = pos5;
   const uint32_t j = min((p & kPosMask) >> 5, jmax - 1);
   const uint32_t w0 = col_word(sc, j), w1 = col_word(sc, j + 1), w2 = col_word(sc, j + 2), w3 = col_word(sc, j + 3);
-  bp_lookup4(funnel64(w2, w1, w0, p), p, e, lane_off);
-  // rows moved: 0, 1 or 2 (more only when the first row was clamped)
-  const uint32_t rel = ((p & kPosMask) >> 5) - j;
-  const bool r1 = rel == 1, r2 = rel >= 2;
-  const uint32_t c = (r1 || r2) ? w3 : w2, b = r2 ? w3 : r1 ? w2 : w1, a = r2 ? w2 : r1 ? w1 : w0;
-  bp_lookup4(funnel64(c, b, a, p), p, e + 4, lane_off);
-  pos5 = p;
+  uint64_t W = funnel64(w2, w1, w0, p);
+  const uint32_t t = __builtin_amdgcn_alignbit(w3, w2, p);
+  bp_lookup4(W, e, lane_off);
+  W = shift_window(W, e[3]);
+  const uint32_t p4 = p + e[0] + e[1] + e[2] + e[3];
+  W |= (uint64_t)t << ((p - p4) & 63u);  // 64 - (bits of the four pairs)
+  bp_lookup4(W, e + 4, lane_off);
+  pos5 = p4 + e[4] + e[5] + e[6] + e[7];
 }
 
 // Packed bf16 pair (weights k, k+1 of a raw dword) from two table entries.
