@@ -1850,21 +1850,33 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
   uint2 rw[F16 ? 1 : SP];  // raw bytes of the next group's steps (bf16 formats)
   Signs<SP> sg, sgn;       // float16: the lane's sign bytes of this and the next group
   uint4 xv[SP];
+  // raw bytes of the first group's first half of the steps with its stream
+  // words, the second half once those are in: every wave requests its first
+  // group at once, and a wave's stream words would otherwise queue behind
+  // the other waves' raw bytes for all eight steps
+  constexpr int kEarlyRaw = F16 ? 0 : SP / 2;
+  const uint8_t* raw0 = nullptr;
   {
     const uint32_t rb = g0 / CB;
     const uint32_t G = min(16u, a.rows - rb * 16);
+    raw0 = a.raw + m0.first * S + lane_mu(rb) * 8;
     if constexpr (F16) sg.load(a.raw + (m0.first + lane_mu(rb)) * SP);
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
-      if constexpr (!F16) rw[k] = *reinterpret_cast<const uint2*>(a.raw + m0.first * S + lane_mu(rb) * 8 + k * G * 32u);
+      if constexpr (!F16) if (k < kEarlyRaw) rw[k] = *reinterpret_cast<const uint2*>(raw0 + k * G * 32u);
       if constexpr (!DEC) xv[k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff + k * XSTEP);
     }
   }
   stream_store<JT>(cols, sw, lane);
   // everything but the raw (or sign) and activation loads
-  constexpr int kRawLoads = F16 ? 1 : SP;
+  constexpr int kRawLoads = F16 ? 1 : kEarlyRaw;
   __builtin_amdgcn_s_waitcnt(waitcnt_vm(kRawLoads + (DEC ? 0 : SP)));
   asm volatile("" ::: "memory");
+  if constexpr (!F16) {
+    const uint32_t G = min(16u, a.rows - (g0 / CB) * 16);
+#pragma unroll
+    for (int k = kEarlyRaw; k < SP; ++k) rw[k] = *reinterpret_cast<const uint2*>(raw0 + k * G * 32u);
+  }
   __syncthreads();
 
   f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
