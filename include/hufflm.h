@@ -41,21 +41,29 @@
  *
  * Stream: for each weight of a segment in order, code(el) then code(eh),
  * each emitted most-significant bit first; the stream is packed least
- * significant bit first (bit k is bit k%8 of byte k/8). The segments of a
- * group are concatenated in mu order without gaps; each group stream starts on a 16-byte
- * boundary and is zero-padded to a multiple of 128 bits.
+ * significant bit first (bit k is bit k%8 of byte k/8). Segment mu of a group
+ * occupies stored(mu) = base + seg_len[mu] bits: its codes, then zero bits up
+ * to that length. base is the least code-bit count among the group's
+ * segments, or the greatest minus 255 when they span more than 255 bits (the
+ * shorter segments are then padded to base), so that every seg_len fits one
+ * byte. The segments of a group are concatenated in mu order; each group
+ * stream starts on a 16-byte boundary and is zero-padded to a multiple of 128
+ * bits. (The paper's decoder reads one stream serially, Sec. 3.2, and needs
+ * no lengths; here every segment is decoded from its own start.)
  *
  * Layout (sections start at 64-byte boundaries, zero padding between):
  *   0      header (128 bytes, below)
- *   off_seg_bits  uint16 seg_bits[n_seg]   code bits of each segment
- *   off_grp_off   uint32 grp_off[n_grp+1]  group stream start, in 16-byte
- *                                          units from off_stream
+ *   off_seg_bits  uint8 seg_len[n_seg]      stored bits of each segment over
+ *                                           its group's base
+ *   off_grp_off   uint32 grp_meta[2n_grp+1] group g: [2g] stream start in
+ *                                           16-byte units from off_stream,
+ *                                           [2g+1] base; [2n_grp] the end
  *   off_stream    group streams
  *   off_raw       uint8 raw[n]: (s<<7)|m; group g starts at S times its first
  *                 segment number; weight t of segment mu is at ((t/8)*N + mu)*8
  *                 + t%8 within the group
  *   total_bytes = off_raw + n
- * Header: u32 magic 0x31464C48 ('HLF1'), u16 version 1, u8 lmax, u8 flags,
+ * Header: u32 magic 0x31464C48 ('HLF1'), u16 version 2, u8 lmax, u8 flags,
  *   u64 rows, u64 cols, u32 seg_len, u32 group_rows (GR), u64 n_seg,
  *   u64 n_grp, u64 off_seg_bits, u64 off_grp_off, u64 off_stream,
  *   u64 off_raw, u64 total_bytes, u32 max_grp_units, u8 eh_nsym, u8 el_nsym,
@@ -119,7 +127,7 @@ typedef enum {
 typedef enum { HL_F32 = 0, HL_BF16 = 1, HL_F16 = 2 } hl_dtype;
 
 #define HL_MAGIC 0x31464C48u
-#define HL_VERSION 1u
+#define HL_VERSION 2u
 #define HL_HEADER_BYTES 128u
 #define HL_GROUP_SEGS 64u
 #define HL_MAX_BATCH 16u
@@ -177,7 +185,8 @@ typedef struct {
   uint32_t* lut_dev;         /* HL_LUT_BYTES, filled by hl_tensor_prepare */
   uint64_t rows, cols, n_seg, n_grp, total_bytes;
   uint64_t off_seg_bits, off_grp_off, off_stream, off_raw;
-  uint32_t seg_len, grp_rows, lmax, max_grp_units, max_seg_bits;
+  uint32_t seg_len, grp_rows, lmax, max_grp_units;
+  uint32_t max_seg_bits;     /* the longest stored segment (base + seg_len) */
   uint32_t format;           /* hl_format: which of cb / cb8 / cb16 is in use (the others are zero) */
   hl_codebook cb;
   hl_codebook8 cb8;
@@ -255,7 +264,9 @@ hl_status hl_encode16(const uint16_t* w_f16, uint64_t rows, uint64_t cols,
 
 /* Full structural check of a container held in host memory: header, section
  * offsets, codebooks (Kraft sum exactly 1, lengths <= lmax), per-group
- * stream sizes against seg_bits. O(n_seg). Returns HL_OK or HL_ECORRUPT. */
+ * stream sizes against the stored segment lengths (base + seg_len, each at
+ * most S times the longest code of a weight). O(n_seg). Returns HL_OK or
+ * HL_ECORRUPT. */
 hl_status hl_validate(const void* blob_host, size_t blob_bytes);
 
 /* Build a device view of a container copied to `blob_dev` (blob_bytes long)

@@ -33,11 +33,19 @@ g = rb*(L/GC) + cb. Its G*GC segments are numbered mu = j*G + i for row
 offset i < G and segment offset j < GC.
 
 Container layout (little-endian; sections start at 64-byte boundaries):
-  header (128 B), seg_bits u16[n_seg] in group order, grp_off u32[n_grp + 1]
-  (16-byte units), stream (one 16-byte aligned bit stream per group, its
-  segments concatenated in mu order), raw u8[n] (sign<<7 | mantissa; group g's
-  bytes start at S times the number of segments before it; weight t of
-  segment mu at ((t // 8) * N + mu) * 8 + t % 8, N = G*GC).
+  header (128 B), seg_len u8[n_seg] in group order, grp_meta u32[2*n_grp + 1],
+  stream (one 16-byte aligned bit stream per group, its segments concatenated
+  in mu order), raw u8[n] (sign<<7 | mantissa; group g's bytes start at S
+  times the number of segments before it; weight t of segment mu at
+  ((t // 8) * N + mu) * 8 + t % 8, N = G*GC).
+Segment lengths (ours: the paper's decoder reads its stream serially, Sec.
+3.2, and needs none; segments here decode in parallel from their own starts): a
+segment occupies base + seg_len[k] bits of its group's stream, its codes
+first, then zero bits; grp_meta[2g] is group g's stream start in 16-byte
+units, grp_meta[2g + 1] its base, grp_meta[2*n_grp] the end of the last
+stream. base is the group's shortest code-bit count, or its longest minus 255
+when the counts span more than 255 (the shorter segments are then padded to
+base), so that every length fits one byte (stored_lengths).
 
 Whole-exponent variant (header flags = 1): the 8 exponent bits of a weight
 are one symbol of a single per-matrix 256-symbol Huffman code (the {1,8,7}
@@ -70,7 +78,7 @@ from typing import Dict, List, Sequence, Tuple
 import numpy as np
 
 MAGIC = 0x31464C48          # 'HLF1'
-VERSION = 1
+VERSION = 2                 # one-byte segment lengths over a per-group base
 HEADER_BYTES = 128
 GROUP_SEGS = 64             # segments per group (one per lane of a 64-wide wavefront)
 RAW_UNIT = 8                # bytes of one segment's raw plane stored contiguously
@@ -356,9 +364,9 @@ def layout(rows: int, cols: int, seg_len: int, grp_rows: int = GROUP_SEGS,
     GC = GROUP_SEGS // grp_rows
     n_grp = (rows + grp_rows - 1) // grp_rows * (L // GC)
     extra = {FLAG_SPLIT: 0, FLAG_WHOLE_EXPONENT: LEN8_BYTES, FLAG_FP16: CB16_BYTES}[flags]
-    off_seg_bits = _align(HEADER_BYTES + extra)
-    off_grp_off = _align(off_seg_bits + 2 * n_seg)
-    off_stream = _align(off_grp_off + 4 * (n_grp + 1))
+    off_seg_bits = _align(HEADER_BYTES + extra)      # seg_len u8[n_seg]
+    off_grp_off = _align(off_seg_bits + n_seg)        # grp_meta u32[2*n_grp + 1]
+    off_stream = _align(off_grp_off + 4 * (2 * n_grp + 1))
     return dict(n=n, n_seg=n_seg, n_grp=n_grp, L=L, GC=GC, off_seg_bits=off_seg_bits,
                 off_grp_off=off_grp_off, off_stream=off_stream)
 
@@ -495,6 +503,17 @@ def encode(w: np.ndarray, seg_len: int, lmax: int = 12,
     return _assemble(w, seg_len, GR, FLAG_SPLIT, seg_stream, header, b"")
 
 
+SEG_LEN_SPAN = 255          # one-byte segment lengths over the group's base
+
+
+def stored_lengths(code_bits: Sequence[int]) -> Tuple[int, List[int]]:
+    """(base, stored bit counts) of one group's segments from their code-bit
+    counts: base is the least count, or the greatest minus 255 when the counts
+    span more than that; a segment shorter than base is padded to it."""
+    base = max(min(code_bits), max(code_bits) - SEG_LEN_SPAN)
+    return base, [max(c, base) for c in code_bits]
+
+
 def _assemble(w, seg_len, GR, flags, seg_stream, header, codebook_section) -> bytes:
     """Container bytes from a per-segment stream function (all formats)."""
     rows, cols = w.shape
@@ -502,25 +521,27 @@ def _assemble(w, seg_len, GR, flags, seg_stream, header, codebook_section) -> by
     n, n_seg, n_grp = lay["n"], lay["n_seg"], lay["n_grp"]
     S = seg_len
 
-    seg_bits = np.zeros(n_seg, dtype=np.uint16)
-    grp_off = np.zeros(n_grp + 1, dtype=np.uint32)
+    seg_len8 = np.zeros(n_seg, dtype=np.uint8)
+    grp_meta = np.zeros(2 * n_grp + 1, dtype=np.uint32)
     chunks: List[bytes] = []
     units_total = 0
     max_units = 0
     for g in range(n_grp):
         r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
+        segs = [seg_stream(r0 + mu % G, (c0 + mu // G) * S, S) for mu in range(G * GC)]
+        base, stored = stored_lengths([nb for _, nb in segs])
         gacc, gpos = 0, 0
-        for mu in range(G * GC):
-            acc, nb = seg_stream(r0 + mu % G, (c0 + mu // G) * S, S)
-            seg_bits[first + mu] = nb
-            gacc |= acc << gpos
-            gpos += nb
+        for mu, (acc, nb) in enumerate(segs):
+            seg_len8[first + mu] = stored[mu] - base
+            gacc |= acc << gpos            # codes, then zero bits up to the stored length
+            gpos += stored[mu]
         units = (gpos + 127) // 128
         chunks.append(gacc.to_bytes(units * UNIT_BYTES, "little"))
-        grp_off[g] = units_total
+        grp_meta[2 * g] = units_total
+        grp_meta[2 * g + 1] = base
         units_total += units
         max_units = max(max_units, units)
-    grp_off[n_grp] = units_total
+    grp_meta[2 * n_grp] = units_total
     stream = b"".join(chunks)
 
     off_raw = _align(lay["off_stream"] + len(stream))
@@ -531,8 +552,8 @@ def _assemble(w, seg_len, GR, flags, seg_stream, header, codebook_section) -> by
     out[0:HEADER_BYTES] = header(n_seg, n_grp, lay["off_seg_bits"], lay["off_grp_off"],
                                  lay["off_stream"], off_raw, total, max_units)
     out[HEADER_BYTES:HEADER_BYTES + len(codebook_section)] = codebook_section
-    out[lay["off_seg_bits"]:lay["off_seg_bits"] + 2 * n_seg] = seg_bits.tobytes()
-    out[lay["off_grp_off"]:lay["off_grp_off"] + 4 * (n_grp + 1)] = grp_off.tobytes()
+    out[lay["off_seg_bits"]:lay["off_seg_bits"] + n_seg] = seg_len8.tobytes()
+    out[lay["off_grp_off"]:lay["off_grp_off"] + 4 * (2 * n_grp + 1)] = grp_meta.tobytes()
     out[lay["off_stream"]:lay["off_stream"] + len(stream)] = stream
     out[off_raw:off_raw + n] = raw.tobytes()
     return bytes(out)
@@ -738,6 +759,31 @@ def header_codebooks(h) -> Tuple[FieldCode, FieldCode]:
             FieldCode(h["el_len"], h["el_nsym"], h["el_single"]))
 
 
+def segment_lengths(blob: bytes, h=None) -> Tuple[np.ndarray, np.ndarray]:
+    """(stored bit count of every segment in group order, group stream starts
+    in 16-byte units with the end of the last appended) from the container's
+    one-byte lengths and per-group bases."""
+    h = parse_header(blob) if h is None else h
+    n_seg, n_grp = h["n_seg"], h["n_grp"]
+    rows, cols, S, GR = h["rows"], h["cols"], h["seg_len"], h["grp_rows"]
+    seg8 = np.frombuffer(blob, np.uint8, n_seg, h["off_seg_bits"]).astype(np.int64)
+    meta = np.frombuffer(blob, np.uint32, 2 * n_grp + 1, h["off_grp_off"]).astype(np.int64)
+    stored = np.zeros(n_seg, dtype=np.int64)
+    for g in range(n_grp):
+        _, G, _, first, GC = group_geometry(rows, cols, S, g, GR)
+        stored[first:first + G * GC] = seg8[first:first + G * GC] + meta[2 * g + 1]
+    return stored, meta[0::2]
+
+
+def _segment_end(bits: List[int], start: int, pos: int, stored: int) -> int:
+    """The next segment's start: a segment's codes take at most its stored
+    length (less only where it was padded to its group's base), and any
+    padding is zero bits."""
+    if pos - start > stored or any(bits[pos:start + stored]):
+        raise ValueError("segment length mismatch")
+    return start + stored
+
+
 def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
     """Bit-serial decode of one group.
 
@@ -751,8 +797,7 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
     else:
         ceh, cel = header_codebooks(h)
     rows, cols, S, GR = h["rows"], h["cols"], h["seg_len"], h["grp_rows"]
-    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
-    grp_off = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    stored, grp_off = segment_lengths(blob, h)
     raw_plane = np.frombuffer(blob, np.uint8, rows * cols, h["off_raw"])
     r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
     a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
@@ -772,8 +817,7 @@ def decode_group(blob: bytes, g: int) -> Tuple[int, int, int, int, np.ndarray]:
             else:
                 el[t], pos = cel.decode_one(bits, pos)
                 eh[t], pos = ceh.decode_one(bits, pos)
-        if pos - start != int(seg_bits[first + mu]):
-            raise ValueError("segment length mismatch")
+        pos = _segment_end(bits, start, pos, int(stored[first + mu]))
         cols_of = (c0 + j) * S + np.arange(S)
         rp = raw_pos(np.full(S, r0 + i), cols_of, rows, cols, S, GR)
         r = raw_plane[rp].astype(np.uint32)
@@ -785,8 +829,7 @@ def _decode_group16(blob: bytes, h, g: int):
     """decode_group for the float16 format."""
     ce, cmh, cml = header_codebooks16(h)
     rows, cols, S, GR = h["rows"], h["cols"], h["seg_len"], h["grp_rows"]
-    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
-    grp_off = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    stored, grp_off = segment_lengths(blob, h)
     signs = np.frombuffer(blob, np.uint8, rows * cols // 8, h["off_raw"])
     r0, G, c0, first, GC = group_geometry(rows, cols, S, g, GR)
     a = h["off_stream"] + int(grp_off[g]) * UNIT_BYTES
@@ -802,8 +845,7 @@ def _decode_group16(blob: bytes, h, g: int):
             f[2, t], pos = cml.decode_one(bits, pos)
             f[0, t], pos = ce.decode_one(bits, pos)
             f[1, t], pos = cmh.decode_one(bits, pos)
-        if pos - start != int(seg_bits[first + mu]):
-            raise ValueError("segment length mismatch")
+        pos = _segment_end(bits, start, pos, int(stored[first + mu]))
         t = np.arange(S)
         sb = signs[(first + mu) * (S // 8) + t // 8]
         out[i, j * S:(j + 1) * S] = join_fields16((sb >> (t % 8)) & 1, f[0], f[1], f[2])
@@ -855,8 +897,9 @@ def _size_from_bits(bits, shape, seg_len, lmax, grp_rows, flags) -> Dict[str, in
     units = 0
     max_units = 0
     for rb in range(0, rows, GR):
-        per_cs = seg[rb:rb + GR].sum(axis=0)                              # [L]
-        per_grp = per_cs.reshape(L // GC, GC).sum(axis=1)
+        blk = seg[rb:rb + GR].reshape(-1, L // GC, GC).transpose(1, 0, 2).reshape(L // GC, -1)  # [CB, G*GC]
+        base = np.maximum(blk.min(axis=1), blk.max(axis=1) - SEG_LEN_SPAN)  # stored_lengths, per group
+        per_grp = np.maximum(blk, base[:, None]).sum(axis=1)
         u = (per_grp + 127) // 128
         units += int(u.sum())
         max_units = max(max_units, int(u.max()))

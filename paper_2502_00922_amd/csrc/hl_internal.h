@@ -6,10 +6,16 @@
 
 namespace hl {
 
+// Section offsets of a container: off_seg_bits holds one byte per segment
+// (its stored length over its group's base), off_grp_off the u32 start (in
+// 16-byte units) and base of every group, then the end of the last stream.
 struct Layout {
   uint64_t n, n_seg, n_grp, L, off_seg_bits, off_grp_off, off_stream;
   uint32_t GR, GC;
 };
+
+// A group's stored segment lengths span at most this many bits over its base.
+constexpr uint32_t kSegLenSpan = 255;
 
 // Group g = rb*(L/GC) + cb: rows r0 .. r0+G-1 and column segments
 // c0 .. c0+GC-1; segment mu = j*G + i is (r0 + i, c0 + j); `first` is the

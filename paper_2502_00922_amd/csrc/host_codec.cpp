@@ -276,8 +276,8 @@ Layout make_layout(uint64_t rows, uint64_t cols, uint32_t S, uint32_t GR, uint32
                            : format == HL_FORMAT_FP16        ? HL_CB16_BYTES
                                                              : 0;
   L.off_seg_bits = align64(HL_HEADER_BYTES + section);
-  L.off_grp_off = align64(L.off_seg_bits + 2 * L.n_seg);
-  L.off_stream = align64(L.off_grp_off + 4 * (L.n_grp + 1));
+  L.off_grp_off = align64(L.off_seg_bits + L.n_seg);               // one byte per segment
+  L.off_stream = align64(L.off_grp_off + 4 * (2 * L.n_grp + 1));   // start and base per group, the end
   return L;
 }
 
@@ -662,21 +662,37 @@ static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, ui
   });
   for (auto b : bad)
     if (b) return HL_EINVAL;
-  // Group stream sizes (16-byte units) and offsets.
-  std::vector<uint32_t> grp_off(L.n_grp + 1);
+  // Stored segment lengths: the group's base (its least code-bit count, or
+  // its greatest minus 255 when they span more) plus one byte per segment,
+  // shorter segments padded to base with zero bits. Group stream sizes
+  // (16-byte units), starts and bases.
+  std::vector<uint8_t> seg_len8(L.n_seg);
+  std::vector<uint32_t> grp_meta(2 * L.n_grp + 1);
   uint64_t units = 0;
   uint32_t max_units = 0;
   for (uint64_t g = 0; g < L.n_grp; ++g) {
     GroupGeom q = group_geom(rows, L.L, GR, g);
+    const uint32_t NG = q.G * q.GC;
+    uint32_t lo = 0xFFFFFFFFu, hi = 0;
+    for (uint32_t mu = 0; mu < NG; ++mu) {
+      lo = std::min<uint32_t>(lo, seg_bits[q.first + mu]);
+      hi = std::max<uint32_t>(hi, seg_bits[q.first + mu]);
+    }
+    const uint32_t base = hi > lo + kSegLenSpan ? hi - kSegLenSpan : lo;
     uint64_t bits = 0;
-    for (uint32_t mu = 0; mu < q.G * q.GC; ++mu) bits += seg_bits[q.first + mu];
+    for (uint32_t mu = 0; mu < NG; ++mu) {
+      const uint32_t stored = std::max<uint32_t>(seg_bits[q.first + mu], base);
+      seg_len8[q.first + mu] = (uint8_t)(stored - base);
+      bits += stored;
+    }
     uint64_t u = (bits + 127) / 128;
-    grp_off[g] = (uint32_t)units;
+    grp_meta[2 * g] = (uint32_t)units;
+    grp_meta[2 * g + 1] = base;
     units += u;
     max_units = std::max<uint32_t>(max_units, (uint32_t)u);
     if (units > 0xFFFFFFFFull) return HL_EUNSUPPORTED;
   }
-  grp_off[L.n_grp] = (uint32_t)units;
+  grp_meta[2 * L.n_grp] = (uint32_t)units;
   const uint64_t off_raw = align64(L.off_stream + units * 16);
   const uint64_t total = off_raw + raw_bytes(L.n, format);
   if (!out) { *out_bytes = total; return HL_OK; }
@@ -684,15 +700,16 @@ static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, ui
   uint8_t* o = (uint8_t*)out;
   std::memset(o, 0, L.off_stream);  // header, codebook section, padding, metadata
   pack_header(o, rows, cols, S, format, lmax, cb, cb8, cb16, L, off_raw, total, max_units);
-  std::memcpy(o + L.off_seg_bits, seg_bits.data(), 2 * L.n_seg);
-  std::memcpy(o + L.off_grp_off, grp_off.data(), 4 * (L.n_grp + 1));
+  std::memcpy(o + L.off_seg_bits, seg_len8.data(), L.n_seg);
+  std::memcpy(o + L.off_grp_off, grp_meta.data(), 4 * (2 * L.n_grp + 1));
   std::memset(o + L.off_stream + units * 16, 0, off_raw - (L.off_stream + units * 16));
   // Pass 2: group streams and raw plane, independent per group.
   parallel_for(L.n_grp, nt, [&](uint64_t ga, uint64_t gb) {
     for (uint64_t g = ga; g < gb; ++g) {
       GroupGeom q = group_geom(rows, L.L, GR, g);
-      uint32_t* dst = (uint32_t*)(o + L.off_stream + (uint64_t)grp_off[g] * 16);
-      const uint64_t nwords = (uint64_t)(grp_off[g + 1] - grp_off[g]) * 4;
+      uint32_t* dst = (uint32_t*)(o + L.off_stream + (uint64_t)grp_meta[2 * g] * 16);
+      const uint64_t nwords = (uint64_t)(grp_meta[2 * g + 2] - grp_meta[2 * g]) * 4;
+      const uint32_t base = grp_meta[2 * g + 1];
       uint64_t acc = 0;
       int nb = 0;
       uint64_t wi = 0;
@@ -728,6 +745,12 @@ static hl_status encode_body(const uint16_t* w, uint64_t rows, uint64_t cols, ui
             cd.emit(v, put);
             rdst[((t >> 3) * NG + mu) * 8 + (t & 7)] = (uint8_t)(((v >> 8) & 0x80) | (v & 0x7F));
           }
+        }
+        // a segment shorter than the group's base: zero bits up to it
+        for (uint32_t pad = base > seg_bits[q.first + mu] ? base - seg_bits[q.first + mu] : 0; pad;) {
+          const uint32_t k = std::min<uint32_t>(pad, 16);
+          put(0, k);
+          pad -= k;
         }
       }
       while (wi < nwords) {  // tail bits, then zero padding to 128 bits
@@ -808,26 +831,28 @@ hl_status validate_blob(const uint8_t* b, size_t bytes, Header* out, uint32_t* m
   if (!b || bytes < HL_HEADER_BYTES) return HL_ECORRUPT;
   Header H;
   if (!parse_header(b, bytes, &H) || !header_consistent(H, bytes)) return HL_ECORRUPT;
-  const uint16_t* sb = (const uint16_t*)(b + H.off_seg_bits);
-  const uint32_t* go = (const uint32_t*)(b + H.off_grp_off);
-  if (go[0] != 0) return HL_ECORRUPT;
+  const uint8_t* sb = b + H.off_seg_bits;                             // one byte per segment
+  const uint32_t* gm = (const uint32_t*)(b + H.off_grp_off);          // start, base per group; end
+  if (gm[0] != 0) return HL_ECORRUPT;
   uint32_t mx = 0, mseg = 0;
   const uint64_t max_seg = (uint64_t)H.seg_len * weight_bits_max(H);
   const uint64_t L = H.cols / H.seg_len;
   for (uint64_t g = 0; g < H.n_grp; ++g) {
     GroupGeom q = group_geom(H.rows, L, H.grp_rows, g);
+    const uint32_t base = gm[2 * g + 1];
     uint64_t bits = 0;
     for (uint32_t mu = 0; mu < q.G * q.GC; ++mu) {
-      const uint32_t v = sb[q.first + mu];
+      const uint64_t v = (uint64_t)base + sb[q.first + mu];
       if (v > max_seg) return HL_ECORRUPT;
       bits += v;
-      mseg = std::max(mseg, v);
+      mseg = std::max(mseg, (uint32_t)v);
     }
-    if (go[g + 1] < go[g] || go[g + 1] - go[g] != (bits + 127) / 128) return HL_ECORRUPT;
-    mx = std::max(mx, go[g + 1] - go[g]);
+    const uint32_t u0 = gm[2 * g], u1 = gm[2 * g + 2];
+    if (u1 < u0 || u1 - u0 != (bits + 127) / 128) return HL_ECORRUPT;
+    mx = std::max(mx, u1 - u0);
   }
   if (mx != H.max_grp_units) return HL_ECORRUPT;
-  if (H.off_raw != align64(H.off_stream + (uint64_t)go[H.n_grp] * 16)) return HL_ECORRUPT;
+  if (H.off_raw != align64(H.off_stream + (uint64_t)gm[2 * H.n_grp] * 16)) return HL_ECORRUPT;
   if (out) *out = H;
   if (max_seg_bits) *max_seg_bits = mseg;
   return HL_OK;

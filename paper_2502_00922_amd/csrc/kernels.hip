@@ -591,8 +591,8 @@ __device__ inline void mfma_operand_guard() { asm volatile("s_nop 4"); }
 // ------------------------------------------------------------------ staging
 
 struct GroupArgs {
-  const uint16_t* seg_bits;
-  const uint32_t* grp_off;
+  const uint8_t* seg_len8;   // per segment: its stored length over its group's base
+  const uint32_t* grp_meta;  // per group: stream start (16-byte units), base; then the end
   const uint4* stream;
   const uint8_t* raw;
   const uint32_t* lut;   // global copy: kLutN entries + aux
@@ -609,9 +609,13 @@ struct GroupArgs {
 struct Meta {
   uint64_t first;  // group-order number of the group's first segment
   uint32_t r0, G, N, c0;
-  uint32_t nbw;    // the dword holding the lane's 16-bit segment length
+  uint32_t nbw;    // the dword holding the lane's one-byte segment length
   uint32_t u0, units;
 };
+
+// Which word of a group's table entry a lane loads: lane 0 the group's
+// stream start, lane 1 its end (the next group's start), lane 2 its base.
+__device__ inline uint32_t meta_pick(uint32_t lane) { return lane == 1 ? 2u : lane == 2 ? 1u : 0u; }
 
 // Group g's geometry, and its metadata loads (vector loads, counted by vmcnt).
 __device__ inline Meta load_meta(const GroupArgs& a, uint32_t g, uint32_t lane) {
@@ -623,11 +627,12 @@ __device__ inline Meta load_meta(const GroupArgs& a, uint32_t g, uint32_t lane) 
   m.N = m.G * a.GC;
   m.first = (uint64_t)m.r0 * a.L + (uint64_t)m.c0 * m.G;
   // A whole dword, used as loaded (no conversion that would wait on it here);
-  // the half-word is picked and masked to lanes < N at use. The dword at an
-  // even index of the last segment reaches 2 bytes past the lengths table,
-  // into the padding before the group offsets.
-  m.nbw = reinterpret_cast<const uint32_t*>(a.seg_bits)[(m.first + min(lane, m.N - 1)) >> 1];
-  m.u0 = a.grp_off[g + (lane & 1)];  // lane 0: start, lane 1: end
+  // the byte is picked and masked to lanes < N at use. The dword of the last
+  // segments reaches at most 3 bytes past the lengths table, into the
+  // padding before the group table (the lengths end off a 4-byte boundary
+  // only where the next section's 64-byte alignment leaves padding).
+  m.nbw = reinterpret_cast<const uint32_t*>(a.seg_len8)[(m.first + min(lane, m.N - 1)) >> 2];
+  m.u0 = a.grp_meta[2 * g + meta_pick(lane)];
   m.units = 0;
   return m;
 }
@@ -648,12 +653,13 @@ __device__ inline uint32_t stream_start(const GroupArgs& a, Meta& m, uint32_t la
                                         uint32_t& bit0) {
   uint32_t v0 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 0);
   uint32_t v1 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 1);
+  const uint32_t base = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 2);
   v0 = min(v0, a.stream_units);
   v1 = min(max(v1, v0), a.stream_units);
   m.u0 = v0;
   m.units = min(v1 - v0, a.max_units);
-  const uint32_t half = (uint32_t)(m.first + min(lane, m.N - 1)) & 1u;
-  const uint32_t nb = lane < m.N ? (m.nbw >> (16 * half)) & 0xFFFFu : 0u;
+  const uint32_t byte = (uint32_t)(m.first + min(lane, m.N - 1)) & 3u;
+  const uint32_t nb = lane < m.N ? base + ((m.nbw >> (8 * byte)) & 0xFFu) : 0u;
   uint32_t incl = nb;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
@@ -1718,8 +1724,8 @@ struct StreamArgs {
 // the first group of the same block and wave of that launch (discarded), so
 // that the next launch's first round comes from the caches. n = 0: none.
 struct PrefetchArgs {
-  const uint16_t* seg_bits[kMaxParts];
-  const uint32_t* grp_off[kMaxParts];
+  const uint8_t* seg_len8[kMaxParts];
+  const uint32_t* grp_meta[kMaxParts];
   const uint4* stream[kMaxParts];
   const uint8_t* raw[kMaxParts];
   uint32_t CB[kMaxParts], RB[kMaxParts], L[kMaxParts], rows[kMaxParts];
@@ -1802,8 +1808,8 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
   // The next launch's first group for this block and wave (the prefetch
   // target): its arrays and geometry, selected with fixed indices.
   bool pfon = false;
-  const uint16_t* p_seg = a.seg_bits;
-  const uint32_t* p_go = a.grp_off;
+  const uint8_t* p_seg = a.seg_len8;
+  const uint32_t* p_go = a.grp_meta;
   const uint4* p_str = a.stream;
   const uint8_t* p_raw = a.raw;
   uint32_t p_cb = 1, p_l = 1, p_rows = 16, p_rb = 0;
@@ -1811,8 +1817,8 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
 #pragma unroll
     for (uint32_t k = 0; k < kMaxParts; ++k) {
       if (k < pf.n && blockIdx.x >= pf.part0[k] && blockIdx.x < pf.part0[k + 1]) {
-        p_seg = pf.seg_bits[k];
-        p_go = pf.grp_off[k];
+        p_seg = pf.seg_len8[k];
+        p_go = pf.grp_meta[k];
         p_str = pf.stream[k];
         p_raw = pf.raw[k];
         p_cb = pf.CB[k];
@@ -1911,12 +1917,12 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
       m1 = load_meta(a, g2, lane);
       if constexpr (!DEC && !F16) {
         // the target's two metadata loads in place of the dummy ones
-        const uint32_t* sb = reinterpret_cast<const uint32_t*>(p2 ? p_seg : a.seg_bits);
-        const uint32_t* go = p2 ? p_go : a.grp_off;
+        const uint32_t* sb = reinterpret_cast<const uint32_t*>(p2 ? p_seg : a.seg_len8);
+        const uint32_t* go = p2 ? p_go : a.grp_meta;
         const uint64_t fm = p2 ? p_first : m1.first;
         const uint32_t nm = p2 ? p_G * 4u : m1.N, gm = p2 ? p_g : g2;
-        m1.nbw = sb[(fm + min(lane, nm - 1)) >> 1];
-        m1.u0 = go[gm + (lane & 1)];
+        m1.nbw = sb[(fm + min(lane, nm - 1)) >> 2];
+        m1.u0 = go[2 * gm + meta_pick(lane)];
         p_meta = p_meta || p2;
       }
       // prefetch source: the next group, else the next launch's first group,
@@ -2107,8 +2113,8 @@ static hl_status make_plan(const hl_tensor* t, uint32_t extra_words_per_wave, bo
   GroupArgs& a = pl->ga;
   std::memset(&a, 0, sizeof(a));
   const uint8_t* b = t->blob_dev;
-  a.seg_bits = reinterpret_cast<const uint16_t*>(b + t->off_seg_bits);
-  a.grp_off = reinterpret_cast<const uint32_t*>(b + t->off_grp_off);
+  a.seg_len8 = b + t->off_seg_bits;
+  a.grp_meta = reinterpret_cast<const uint32_t*>(b + t->off_grp_off);
   a.stream = reinterpret_cast<const uint4*>(b + t->off_stream);
   a.raw = b + t->off_raw;
   a.lut = t->lut_dev;
@@ -2847,8 +2853,8 @@ static bool group_shape(const hl_tensor* const* ts, uint32_t count, GroupShape* 
 }
 
 static void prefetch_matrix(PrefetchArgs* pf, uint32_t k, const GroupArgs& ga) {
-  pf->seg_bits[k] = ga.seg_bits;
-  pf->grp_off[k] = ga.grp_off;
+  pf->seg_len8[k] = ga.seg_len8;
+  pf->grp_meta[k] = ga.grp_meta;
   pf->stream[k] = ga.stream;
   pf->raw[k] = ga.raw;
   pf->CB[k] = ga.CB;

@@ -14,7 +14,10 @@ different stream lengths all run:
 * long moves: every pair fits the 13-bit window (no escapes), but every
   64th row holds pairs of 10 to 13 bits, so four pairs often move a lane's
   position past the four words it read and its second window is read from
-  the column (the decode's rare wave-uniform branch).
+  the column (the decode's rare wave-uniform branch);
+* spread: the workloads' distribution with about one 64-column piece in 97
+  log-uniform (long codes), so that some groups' segments span more than 255
+  code bits and the shorter ones are padded to the group's base.
 Each in the split format (code limit 12 and 15) and the whole-exponent
 format. The full decode of each container (the same kernel storing the
 weights) must be bit-exact. Outputs: every row against a float64 product of the exact bf16
@@ -25,6 +28,7 @@ import numpy as np
 import pytest
 
 from gen import f32_to_bf16_bits, random_bf16, random_x
+from oracle import codec
 from oracle import gemv as ogemv
 from oracle.gemv import bf16_to_f64
 
@@ -67,7 +71,11 @@ def _weights(kind, rows, cols, seed):
         bits = (rng.integers(0, 2, (rows, cols)) << 15) | (eh << 11) | (el << 7) | rng.integers(0, 128, (rows, cols))
         return bits.astype(np.uint16)
     mag = np.exp2(rng.uniform(-60, 60, (rows, cols))).astype(np.float32)
-    return f32_to_bf16_bits(mag * np.where(rng.random((rows, cols)) < 0.5, -1, 1).astype(np.float32))
+    wide = f32_to_bf16_bits(mag * np.where(rng.random((rows, cols)) < 0.5, -1, 1).astype(np.float32))
+    if kind == "spread":
+        piece = (np.arange(rows)[:, None] * 31 + np.arange(cols)[None, :] // 64) % 97 == 0
+        return np.where(piece, wide, random_bf16((rows, cols), seed=seed))
+    return wide
 
 
 # container formats: (encoder keywords). The default split codes keep every
@@ -82,12 +90,17 @@ FORMATS = {"split": {}, "split_unbounded": {"pair_max": 0}, "split_lmax15": {"lm
 
 @pytest.mark.parametrize("S,cols,fmt", [(64, 8192, "split"), (32, 4096, "split"), (64, 8192, "split_unbounded"),
                                         (64, 8192, "split_lmax15"), (64, 8192, "whole"), (32, 4096, "whole")])
-@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform", "geometric", "long_moves"])
+@pytest.mark.parametrize("kind", ["constant_exponent", "gaussian", "log_uniform", "geometric", "long_moves", "spread"])
 def test_persistent_kernel(torch, S, cols, fmt, kind):
     rows = 4100
     print(f"persistent S={S} {rows}x{cols} {fmt} {kind}", flush=True)
     W = _weights(kind, rows, cols, seed=S + cols)
-    dt = hl.DeviceTensor(hl.encode(W, seg_len=S, **FORMATS[fmt]))
+    blob = hl.encode(W, seg_len=S, **FORMATS[fmt])
+    if kind == "spread" and S == 64:
+        # padded segments present: some stored length is 255 over its base
+        h = codec.parse_header(bytes(blob))
+        assert np.frombuffer(bytes(blob), np.uint8, h["n_seg"], h["off_seg_bits"]).max() == 255
+    dt = hl.DeviceTensor(blob)
     assert dt.view.grp_rows == 16
     cb = dt.view.cb
     if kind == "long_moves" and fmt == "split_unbounded":
@@ -112,4 +125,21 @@ def test_persistent_kernel(torch, S, cols, fmt, kind):
     # the full decode of the same container runs on the persistent kernel
     # too (its product replaced by stores): bit-exact
     assert np.array_equal(dt.decode().cpu().numpy().view(np.uint16), W)
+    torch.cuda.synchronize()
+
+
+def test_padded_segments_small(torch):
+    """One 16 x 4 group whose segments span more than 255 code bits (the
+    shorter ones padded to the group's base), on the non-persistent kernels:
+    decode bit-exact, products against the oracle."""
+    from test_oracle_pins import _spread_lengths_matrix
+    W = _spread_lengths_matrix()
+    dt = hl.DeviceTensor(hl.encode(W, seg_len=64, grp_rows=16))
+    assert np.array_equal(dt.decode().cpu().numpy().view(np.uint16), W)
+    for B in (1, 5):
+        xs = random_x(B, W.shape[1], seed=B, dtype="bf16")
+        x = torch.from_numpy(xs.view(np.int16)).cuda().view(torch.bfloat16)
+        y = dt.gemv(x).cpu().numpy().astype(np.float64)
+        yo, do = ogemv.gemv_rows(W, xs, rows=list(range(W.shape[0])))
+        assert (np.abs(y - yo) / (do + 1e-30)).max() <= TOL
     torch.cuda.synchronize()

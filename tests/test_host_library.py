@@ -87,6 +87,18 @@ def test_byte_identical_to_oracle(shape, S, lmax, GR):
     assert hl.validate(a) == 0
 
 
+def test_byte_identical_with_padded_segments():
+    """A group whose segments' code bits span more than 255: the library pads
+    the shorter segments to the group's base exactly as the oracle does."""
+    from test_oracle_pins import _spread_lengths_matrix
+    w = _spread_lengths_matrix()
+    a = bytes(hl.encode(w, seg_len=64, grp_rows=16))
+    assert a == codec.encode(w, seg_len=64, grp_rows=16)
+    assert hl.validate(a) == 0
+    h = codec.parse_header(a)
+    assert max(a[h["off_seg_bits"]:h["off_seg_bits"] + 64]) == 255
+
+
 def test_byte_identical_adversarial():
     rng = np.random.default_rng(9)
     # exponents drawn geometrically: el code would exceed lmax 8 -> package-merge

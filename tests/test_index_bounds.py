@@ -7,8 +7,8 @@ the clamps of the group's stream start and length, each lane's first stream
 word from the prefix sum of the segment lengths, the words it loads, the raw
 bytes, the four column rows of every 8-weight step and the table index), and
 checks every address against the container and the LDS regions while the
-inputs are damaged at random: segment lengths and group offsets replaced by
-arbitrary values, and every table entry's length field arbitrary (stream bits
+inputs are damaged at random: segment length bytes, group starts and bases
+replaced by arbitrary values, and every table entry's length field arbitrary (stream bits
 that decode to anything). Geometry comes from real containers."""
 import numpy as np
 import pytest
@@ -22,7 +22,7 @@ KCOL = 64          # column row stride (words)
 POS_MASK = 0x7FFFFF
 
 
-def _model_group(h, seg_bits, grp_off, g, JT, rng, bounded):
+def _model_group(h, seg8, grp_meta, g, JT, rng, bounded):
     """Byte ranges the group's wave reads from the container, and the LDS
     column rows it touches; the position entries are arbitrary."""
     S, GR, rows, cols = h["seg_len"], h["grp_rows"], h["rows"], h["cols"]
@@ -37,18 +37,21 @@ def _model_group(h, seg_bits, grp_off, g, JT, rng, bounded):
     stream_units = (h["off_raw"] - h["off_stream"]) // 16
     max_units = h["max_grp_units"]
     reads = []
-    # metadata: the dword of each lane's 16-bit length, the group's two offsets
+    # metadata: the dword of each lane's one-byte length; the group's start,
+    # base and end (lanes 0, 2, 1; the other lanes reload the start)
     for lane in range(64):
-        reads.append((h["off_seg_bits"] + ((first + min(lane, N - 1)) >> 1) * 4, 4))
-    reads.append((h["off_grp_off"] + g * 4, 8))
-    v0 = min(int(grp_off[g]), stream_units)
-    v1 = min(max(int(grp_off[g + 1]), v0), stream_units)
+        reads.append((h["off_seg_bits"] + ((first + min(lane, N - 1)) >> 2) * 4, 4))
+        reads.append((h["off_grp_off"] + (2 * g + {1: 2, 2: 1}.get(lane, 0)) * 4, 4))
+    v0 = min(int(grp_meta[2 * g]), stream_units)
+    v1 = min(max(int(grp_meta[2 * g + 2]), v0), stream_units)
+    base = int(grp_meta[2 * g + 1])
     units = min(v1 - v0, max_units)
-    nb = [int(seg_bits[first + min(l, N - 1)]) if l < N else 0 for l in range(64)]
-    incl = np.cumsum(nb)
+    # 32-bit lane arithmetic, as in the kernel (a damaged base wraps)
+    nb = [(base + int(seg8[first + min(l, N - 1)])) & 0xFFFFFFFF if l < N else 0 for l in range(64)]
+    incl = np.cumsum(np.array(nb, dtype=np.uint64)) & 0xFFFFFFFF
     rows_used = []
     for lane in range(64):
-        start = min(int(incl[lane]) - nb[lane], units * 128)
+        start = min((int(incl[lane]) - nb[lane]) & 0xFFFFFFFF, units * 128)
         ws, bit0 = start >> 5, start & 31
         if units:
             base = h["off_stream"] + (v0 * 4 + ws) * 4
@@ -79,16 +82,16 @@ def test_persistent_kernel_reads_stay_in_bounds(seed):
     h = codec.parse_header(blob)
     n_seg, n_grp = h["n_seg"], h["n_grp"]
     off_sb, off_go = h["off_seg_bits"], h["off_grp_off"]
-    seg_bits = np.frombuffer(blob, np.uint16, n_seg, off_sb).copy()
-    grp_off = np.frombuffer(blob, np.uint32, n_grp + 1, off_go).copy()
-    max_seg = int(seg_bits.max())
+    seg8 = np.frombuffer(blob, np.uint8, n_seg, off_sb).copy()
+    grp_meta = np.frombuffer(blob, np.uint32, 2 * n_grp + 1, off_go).copy()
+    max_seg = int(codec.segment_lengths(blob, h)[0].max())
     col_rows = 1 + ((31 + max_seg + 31) >> 5) + 3
     JT = next(j for j in (12, 16, 20) if j >= col_rows - 1)
     for trial in range(40):
-        sb, go = seg_bits.copy(), grp_off.copy()
+        sb, go = seg8.copy(), grp_meta.copy()
         if trial % 2:
-            sb = rng.integers(0, 1 << 16, n_seg).astype(np.uint16)
-            go = rng.integers(0, 1 << 32, n_grp + 1, dtype=np.uint64).astype(np.uint32)
+            sb = rng.integers(0, 1 << 8, n_seg).astype(np.uint8)
+            go = rng.integers(0, 1 << 32, 2 * n_grp + 1, dtype=np.uint64).astype(np.uint32)
         for g in range(n_grp):
             reads, rows_used, krows = _model_group(h, sb, go, g, JT, rng, bounded=bool(trial % 4 < 2))
             for off, size in reads:

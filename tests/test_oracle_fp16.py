@@ -56,7 +56,9 @@ def test_tiny_fp16_hand_derived():
     blob = codec.encode16(w, seg_len=8)
     h = codec.parse_header(blob)
     assert h["flags"] == 2 and h["off_seg_bits"] == 256
-    assert int(np.frombuffer(blob, np.uint16, 1, h["off_seg_bits"])[0]) == int(meta["seg_bits"][0])
+    # one segment in one group: its length is the group's base, its byte 0
+    assert blob[h["off_seg_bits"]] == 0
+    assert np.frombuffer(blob, np.uint32, 3, h["off_grp_off"]).tolist()[:2] == [0, int(meta["seg_bits"][0])]
     assert blob[h["off_stream"]:h["off_stream"] + 16].hex() == "".join(meta["stream"])
     assert blob[h["off_raw"]:h["off_raw"] + 1].hex() == meta["signs"][0]
     assert len(blob) == h["off_raw"] + 1
@@ -89,8 +91,7 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR, lmax):
     ce, cmh, cml = codec.header_codebooks16(h)
     for c in (ce, cmh, cml):
         assert c.nsym == 1 or (max(c.lengths) <= lmax and codec.kraft_sum(c.lengths) == 1)
-    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
-    grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    seg_bits, grp = codec.segment_lengths(blob, h)
     signs = np.frombuffer(blob, np.uint8, w.size // 8, h["off_raw"])
     _, e, mh, ml = codec.split_fields16(w)
     for g in (0, h["n_grp"] - 1):
@@ -108,7 +109,7 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR, lmax):
                 assert (ve, vh, vl) == (e[r, c + t], mh[r, c + t], ml[r, c + t])
                 sb = (signs[(first + mu) * (S // 8) + t // 8] >> (t % 8)) & 1
                 assert sb == w[r, c + t] >> 15
-            assert pos - start == seg_bits[first + mu]
+            assert pos - start == seg_bits[first + mu]   # no group here spans more than 255 bits
         assert len(bits) - pos < 128
     # size additivity: code bits = sum over fields of frequency x length
     tot = 0

@@ -232,7 +232,9 @@ def test_tiny_container_hand_derived():
     w = codec.join_fields(s, eh, el, m).reshape(1, 8)
     blob = codec.encode(w, seg_len=8)
     h = codec.parse_header(blob)
-    assert int(np.frombuffer(blob, np.uint16, 1, h["off_seg_bits"])[0]) == int(meta["seg_bits"][0])
+    # one segment in one group: its length is the group's base, its byte 0
+    assert blob[h["off_seg_bits"]] == 0
+    assert np.frombuffer(blob, np.uint32, 3, h["off_grp_off"]).tolist() == [0, int(meta["seg_bits"][0]), 1]
     stream = blob[h["off_stream"]:h["off_stream"] + 16]
     assert stream.hex() == "".join(meta["stream"])
     for key, field in (("eh_len", "eh_len"), ("el_len", "el_len")):
@@ -266,8 +268,7 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR):
     h = codec.parse_header(blob)
     assert h["grp_rows"] == GR
     ceh, cel = codec.header_codebooks(h)
-    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
-    grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    stored, grp = codec.segment_lengths(blob, h)
     _, eh, el, _ = codec.split_fields(w)
     # independent window-match decode of the first and the last group
     for g in (0, h["n_grp"] - 1):
@@ -282,8 +283,64 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR):
                 b, pos = _cam_window_decode(bits, pos, cel, h["lmax"])
                 a, pos = _cam_window_decode(bits, pos, ceh, h["lmax"])
                 assert (a, b) == (eh[r, c + t], el[r, c + t])
-            assert pos - start == seg_bits[first + mu]
+            assert pos - start == stored[first + mu]   # no group here spans more than 255 bits
         assert (len(bits) - pos) < 128            # group padding below one 128-bit unit
+
+
+def _spread_lengths_matrix():
+    """16 x 256 bf16 (one 16 x 4 group at S = 64) whose segment (row 0,
+    columns 0..63) holds rare exponents with long codes while every other
+    weight is the common 1.0-like pattern: its segments' code bits span far
+    more than 255 bits."""
+    rng = np.random.default_rng(5)
+    s = rng.integers(0, 2, (16, 256))
+    m = rng.integers(0, 128, (16, 256))
+    eh = np.full((16, 256), 7)
+    el = np.full((16, 256), 15)
+    el[:, ::2] = 14                                      # two common el values: 1-bit codes
+    eh[0, :64] = rng.integers(0, 7, 64)                  # rare eh and el values in one segment
+    el[0, :64] = rng.integers(0, 14, 64)
+    return codec.join_fields(s, eh, el, m)
+
+
+def test_segment_lengths_padded_to_the_group_base():
+    """Stored segment lengths (the container's one-byte lengths): base = the
+    least code-bit count of the group, or the greatest minus 255; shorter
+    segments padded with zero bits to base. Checked against per-segment code
+    bits computed from the code lengths alone, and by a window-match decode
+    that steps over the padding."""
+    w = _spread_lengths_matrix()
+    blob = codec.encode(w, seg_len=64, grp_rows=16)
+    h = codec.parse_header(blob)
+    assert h["n_grp"] == 1
+    ceh, cel = codec.header_codebooks(h)
+    _, eh, el, _ = codec.split_fields(w)
+    bits = np.array(ceh.lengths)[eh] + np.array(cel.lengths)[el]
+    code = [int(bits[mu % 16, (mu // 16) * 64:(mu // 16 + 1) * 64].sum()) for mu in range(64)]
+    assert max(code) - min(code) > 255
+    base = max(code) - 255
+    seg8 = np.frombuffer(blob, np.uint8, 64, h["off_seg_bits"])
+    meta = np.frombuffer(blob, np.uint32, 3, h["off_grp_off"])
+    assert meta[1] == base
+    assert seg8.tolist() == [max(c, base) - base for c in code]
+    assert seg8.max() == 255 and (seg8 == 0).sum() == sum(c <= base for c in code)
+    stored, grp = codec.segment_lengths(blob, h)
+    assert int(grp[1] - grp[0]) == (int(stored.sum()) + 127) // 128
+    bg = blob[h["off_stream"]: h["off_stream"] + int(grp[1]) * 16]
+    bits_l = np.unpackbits(np.frombuffer(bg, np.uint8), bitorder="little").tolist()
+    pos = 0
+    for mu in range(64):
+        r, c = mu % 16, (mu // 16) * 64
+        start = pos
+        for t in range(64):
+            b, pos = _cam_window_decode(bits_l, pos, cel, h["lmax"])
+            a, pos = _cam_window_decode(bits_l, pos, ceh, h["lmax"])
+            assert (a, b) == (eh[r, c + t], el[r, c + t])
+        assert pos - start == code[mu]
+        assert not any(bits_l[pos:start + int(stored[mu])])   # the padding is zero bits
+        pos = start + int(stored[mu])
+    assert (codec.decode(blob) == w).all()
+    assert codec.container_size(w, 64, grp_rows=16)["total_bytes"] == len(blob)
 
 
 @pytest.mark.parametrize("GR", [64, 32, 16, 8, 1])
@@ -317,14 +374,16 @@ def test_size_accounting_and_ratio_identity():
     ceh, cel = codec.build_codebooks(w)
     blob = codec.encode(w, seg_len=128)
     h = codec.parse_header(blob)
-    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"]).astype(int)
+    seg_bits, grp = codec.segment_lengths(blob, h)
     # per-field coded sizes add up to the stream (entropy-of-splits caption, Sec. 3.1)
-    assert codec.payload_bits(w, ceh, cel) == seg_bits.sum() + 8 * w.size
-    grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"]).astype(int)
+    assert codec.payload_bits(w, ceh, cel) == seg_bits.sum() + 8 * w.size   # no padded segment here
     for g in range(h["n_grp"]):
         _, G, _, first, GC = codec.group_geometry(h["rows"], h["cols"], h["seg_len"], g, h["grp_rows"])
         bits = seg_bits[first: first + G * GC].sum()
         assert grp[g + 1] - grp[g] == (bits + 127) // 128
+    # metadata: one byte per segment, two words per group and one more
+    assert h["off_grp_off"] - h["off_seg_bits"] >= h["n_seg"]
+    assert h["off_stream"] - h["off_grp_off"] >= 4 * (2 * h["n_grp"] + 1)
     assert h["total_bytes"] == len(blob) == h["off_raw"] + w.size
     ratio = 2 * w.size / len(blob)
     bits_per_param = 8 * len(blob) / w.size

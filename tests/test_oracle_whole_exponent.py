@@ -133,7 +133,9 @@ def test_tiny_whole_exponent_hand_derived():
     blob = codec.encode8(w, seg_len=8)
     h = codec.parse_header(blob)
     assert h["flags"] == 1 and h["off_seg_bits"] == 384 and h["nsym8"] == 4
-    assert int(np.frombuffer(blob, np.uint16, 1, h["off_seg_bits"])[0]) == int(meta["seg_bits"][0])
+    # one segment in one group: its length is the group's base, its byte 0
+    assert blob[h["off_seg_bits"]] == 0
+    assert np.frombuffer(blob, np.uint32, 3, h["off_grp_off"]).tolist()[:2] == [0, int(meta["seg_bits"][0])]
     assert blob[h["off_stream"]:h["off_stream"] + 16].hex() == "".join(meta["stream"])
     want = {int(a): int(b) for a, b in (kv.split(":") for kv in meta["len"])}
     assert {i: l for i, l in enumerate(h["len8"]) if l} == want
@@ -164,8 +166,7 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR, lmax):
     lengths = h["len8"]
     assert max(lengths) <= lmax and codec.kraft_sum(lengths) == 1
     codes = codec.canonical_codes(lengths)
-    seg_bits = np.frombuffer(blob, np.uint16, h["n_seg"], h["off_seg_bits"])
-    grp = np.frombuffer(blob, np.uint32, h["n_grp"] + 1, h["off_grp_off"])
+    seg_bits, grp = codec.segment_lengths(blob, h)
     e = codec.exponent_byte(w)
     for g in (0, h["n_grp"] - 1):
         r0, G, c0, first, GC = codec.group_geometry(h["rows"], h["cols"], S, g, GR)
@@ -178,7 +179,7 @@ def test_roundtrip_and_window_match_decoder(shape, S, GR, lmax):
             for t in range(S):
                 v, pos = _window_decode(bits, pos, lengths, codes, lmax)
                 assert v == e[r, c + t]
-            assert pos - start == seg_bits[first + mu]
+            assert pos - start == seg_bits[first + mu]   # no group here spans more than 255 bits
         assert len(bits) - pos < 128
 
 
