@@ -74,8 +74,6 @@ def parse():
                     help="launches timed one by one (HIP events) per 4096x4096 measurement")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-compare", action="store_true")
-    ap.add_argument("--no-prefetch", action="store_true",
-                    help="launches of the headline step without reading the next launch's first groups ahead")
     ap.add_argument("--no-detail", action="store_true", help="only the headline stack (no 4096x4096 detail)")
     ap.add_argument("--traffic-run", action="store_true",
                     help="run only the launches the byte-counter passes measure")
@@ -367,13 +365,15 @@ def measure_workloads(torch, hl):
             parts = [g for g in parts if len(g) > 1]
             singles = [j for j in range(len(specs)) if not any(j in g for g in parts)]
 
+            # the launches of a layer in the workload's order, a grouped set at its
+            # first member
+            order = sorted([g for g in parts] + [[j] for j in singles], key=lambda g: g[0])
+
             def grouped(i):
                 for l in range(layers):
                     st = sets[(i * layers + l) % copies]
-                    for g in parts:
+                    for g in order:
                         hl.gemv_multi([st[j] for j in g], xs[specs[g[0]].cols], [ys[j] for j in g])
-                    for j in singles:
-                        st[j].gemv(xs[specs[j].cols], ys[j])
 
             nrep = max(1, copies // layers)
             ms = time_graph_long(torch, fused, nrep, 100.0)
@@ -392,7 +392,8 @@ def measure_workloads(torch, hl):
                         bf16_ms_per_step=round(ms_b, 5), speedup_vs_bf16=round(ms_b / ms, 3),
                         speedup_target=round(0.9 * cr, 3), cold_copies=copies, setup_s=round(setup_s, 1))
             if ms_g is not None:
-                line.update(grouped=[[names[j] for j in g] for g in parts], grouped_ms_per_step=round(ms_g, 5),
+                line.update(grouped=[[names[j] for j in g] for g in parts],
+                            grouped_ms_per_step=round(ms_g, 5),
                             grouped_compressed_GBps=round(comp * layers / (ms_g * 1e-3) / 1e9, 1),
                             grouped_speedup_vs_bf16=round(ms_b / ms_g, 3))
             if w == 1:
@@ -525,11 +526,8 @@ def measure_stack(torch, hl, st, args):
     launches = stack_launches(stack, ys)
 
     def grouped(i):
-        # each launch reads the next one's first groups into the caches
-        # during its last ones (the step's last launch: the next step's first)
-        for k, (ts, c, yy) in enumerate(launches):
-            nxt = None if args.no_prefetch else launches[(k + 1) % len(launches)][0]
-            hl.gemv_multi(ts, xs[c], yy, prefetch=nxt)
+        for ts, c, yy in launches:
+            hl.gemv_multi(ts, xs[c], yy)
 
     def single(i):
         for row in stack:
@@ -671,9 +669,8 @@ def traffic_run(torch, hl, args):
     ys = [torch.empty((1, sp.rows), dtype=torch.float32, device="cuda") for sp in specs]
     launches = stack_launches(stack, ys)
     for _ in range(3):
-        for k, (ts, c, yy) in enumerate(launches):
-            nxt = None if args.no_prefetch else launches[(k + 1) % len(launches)][0]
-            hl.gemv_multi(ts, xs[c], yy, prefetch=nxt)
+        for ts, c, yy in launches:
+            hl.gemv_multi(ts, xs[c], yy)
     src = torch.empty(COPY_BYTES, dtype=torch.uint8, device="cuda").fill_(1)
     dst = torch.empty_like(src)
     for _ in range(10):
@@ -1005,9 +1002,7 @@ def main():
         "config": {"workload": f"70B-shaped weight stack, {layers} layers x (q, o 8192x8192; k, v 1024x8192; "
                                "gate, up 28672x8192; down 8192x28672), every matrix drawn from its own seed "
                                "(N(0,0.02) + 0.1% outliers x20), resident compressed; one decode step, batch 1, "
-                               "fused decode-GEMV of every matrix (q/k/v and gate/up grouped"
-                               + ("" if args.no_prefetch else "; each launch reads the next one's first groups "
-                                  "into the caches during its last ones") + ")",
+                               "fused decode-GEMV of every matrix (q/k/v and gate/up grouped)",
                    "batch": 1, "x_dtype": "bf16", "seg_len": 64, "format": "bf16, split exponent (4+4)",
                    "compressed_bytes": comp, "compression_ratio": round(cr, 4),
                    "bits_per_weight": round(8 * comp / n, 4)},

@@ -354,23 +354,6 @@ hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const
                                hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
                                void* workspace_dev, size_t workspace_bytes, void* stream);
 
-/* hl_decode_gemv_multi, and during the last group of each wave of its
- * persistent-kernel launch the first group of the same block and wave of the
- * launch that follows on the stream is read into the caches (its metadata,
- * stream and raw bytes; nothing is written), so that launch starts from the
- * caches instead of HBM. next[0..next_count) are the matrices of that next
- * call of hl_decode_gemv_multi (or, with next_count = 1, hl_decode_gemv),
- * with bf16 activations, which the library lays out the same way: for a
- * sequence of decode-step products whose next weights are known (the layers
- * of a model). Results are identical to hl_decode_gemv_multi's. The prefetch
- * applies where both launches run the persistent kernel at S = 64, else it is
- * skipped. Errors: those of hl_decode_gemv_multi, and HL_EINVAL for next ==
- * NULL with next_count > 0 (or the reverse), next_count > 4, or a NULL entry. */
-hl_status hl_decode_gemv_multi_prefetch(const hl_tensor* const* ts, uint32_t count, const void* x_dev,
-                                        hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
-                                        void* workspace_dev, size_t workspace_bytes,
-                                        const hl_tensor* const* next, uint32_t next_count, void* stream);
-
 /* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows:
  * up to 112 tokens the partial sums of up to one range per column block of
  * four segments, beyond that the decoded weights (rows * cols * 2); 0 for

@@ -708,25 +708,6 @@ __device__ inline uint32_t stream_load(const GroupArgs& a, Meta& m, uint32_t lan
   return 30u + bit0;
 }
 
-// stream_load, or (pf) a touch of another container's group stream: the 4 KB
-// from stream + (lane 0's m.u0) in 16-byte units, read into the same
-// registers (the caller discards them).
-template <int JT>
-__device__ inline uint32_t stream_load_or_touch(const GroupArgs& a, Meta& m, uint32_t lane,
-                                                u32x4_a4 (&sw)[JT / 4], bool pf, const uint4* stream) {
-  const uint32_t pu0 = (uint32_t)__builtin_amdgcn_readlane((int)m.u0, 0);
-  uint32_t ws, bit0;
-  stream_start(a, m, lane, ws, bit0);
-  const uint32_t* base = pf        ? reinterpret_cast<const uint32_t*>(stream + pu0)
-                         : m.units ? reinterpret_cast<const uint32_t*>(a.stream + m.u0)
-                                   : reinterpret_cast<const uint32_t*>(a.raw + m.first * a.S);
-  const uint32_t w0 = pf ? lane * 4u : m.units ? ws : 0u;
-  const uint32_t step = pf ? 256u : 4u;
-#pragma unroll
-  for (int k = 0; k < JT / 4; ++k) sw[k] = *reinterpret_cast<const u32x4_a4*>(base + w0 + step * k);
-  return 30u + bit0;
-}
-
 // Writes the words of stream_load to the lane's column (rows 1..JT).
 template <int JT>
 __device__ inline void stream_store(uint32_t* cols, const u32x4_a4 (&sw)[JT / 4], uint32_t lane) {
@@ -1718,21 +1699,6 @@ struct StreamArgs {
   uint32_t n;
 };
 
-// The launch that follows on the stream: its matrices' arrays and geometry
-// (16-row groups, S = 64) and its blocks per matrix and waves per block.
-// During its last group a wave reads the metadata, stream and raw bytes of
-// the first group of the same block and wave of that launch (discarded), so
-// that the next launch's first round comes from the caches. n = 0: none.
-struct PrefetchArgs {
-  const uint8_t* seg_len8[kMaxParts];
-  const uint32_t* grp_meta[kMaxParts];
-  const uint4* stream[kMaxParts];
-  const uint8_t* raw[kMaxParts];
-  uint32_t CB[kMaxParts], RB[kMaxParts], L[kMaxParts], rows[kMaxParts];
-  uint32_t part0[kMaxParts + 1];
-  uint32_t n, waves;
-};
-
 // One matrix (Args = GemvArgs), or a grouped launch (Args = StreamArgs: a
 // block first finds its matrix, with a dependent load before its arguments;
 // the one-matrix kernel keeps the small argument block and reads it at fixed
@@ -1751,7 +1717,7 @@ __device__ inline const GemvArgs& gemv_args(const Args& x) {
 constexpr uint32_t stream_threads(bool dec, int tb) { return dec ? 512 : tb == 2 ? 768 : 1024; }
 
 template <int SP, int JT, bool XT, class Args, bool DEC, int TB>
-__global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Args sa, PrefetchArgs pf) {
+__global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Args sa) {
   constexpr bool BP = TB == 1, F16 = TB == 2;
   constexpr uint32_t S = SP * 8;
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
@@ -1805,33 +1771,6 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
     const uint32_t G = min(16u, a.rows - rb * 16);
     return q * G + min(i, G - 1);
   };
-  // The next launch's first group for this block and wave (the prefetch
-  // target): its arrays and geometry, selected with fixed indices.
-  bool pfon = false;
-  const uint8_t* p_seg = a.seg_len8;
-  const uint32_t* p_go = a.grp_meta;
-  const uint4* p_str = a.stream;
-  const uint8_t* p_raw = a.raw;
-  uint32_t p_cb = 1, p_l = 1, p_rows = 16, p_rb = 0;
-  if constexpr (!DEC && !F16) {
-#pragma unroll
-    for (uint32_t k = 0; k < kMaxParts; ++k) {
-      if (k < pf.n && blockIdx.x >= pf.part0[k] && blockIdx.x < pf.part0[k + 1]) {
-        p_seg = pf.seg_len8[k];
-        p_go = pf.grp_meta[k];
-        p_str = pf.stream[k];
-        p_raw = pf.raw[k];
-        p_cb = pf.CB[k];
-        p_l = pf.L[k];
-        p_rows = pf.rows[k];
-        p_rb = blockIdx.x - pf.part0[k];
-        pfon = wave < pf.waves && wave < pf.CB[k] && p_rb < pf.RB[k];
-      }
-    }
-  }
-  const uint32_t p_g = p_rb * p_cb + wave, p_G = min(16u, p_rows - p_rb * 16);
-  const uint64_t p_first = (uint64_t)p_rb * 16u * p_l + (uint64_t)wave * 4u * p_G;
-  bool p_meta = false;  // the target's metadata has been requested (into m1)
 
   // Prologue. The table (bounded pairs: its entries into registers; else
   // the copy to LDS) and the first two groups' metadata are requested first;
@@ -1900,41 +1839,23 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
       const bool okn = rb_of(tn) < RB;
       uint32_t t2 = tn, j2 = jn;
       advance(t2, j2);
-      const bool ok2 = rb_of(t2) < RB;
-      const uint32_t g2 = ok2 ? group(t2, j2) : group(t, j);
+      const uint32_t g2 = rb_of(t2) < RB ? group(t2, j2) : group(t, j);
       const uint32_t rbn = okn ? rb_of(tn) : rb;
       const uint32_t Gn = min(16u, a.rows - rbn * 16);
       const uint64_t n_first = m1.first;
       const uint32_t n_c0 = m1.c0;
-      // the wave's last group: touch the next launch's first group (its
-      // metadata was requested during the group before)
-      const bool pfl = !okn && p_meta;
       // the next group's stream words (this group's again after the last),
-      // then the metadata of the group after it (the target's when that is
-      // the next launch's first)
-      uint32_t pos2n = stream_load_or_touch<JT>(a, m1, lane, sw, pfl, p_str) - (BP ? kBpShift - 2 : 0u);
-      const bool p2 = okn && !ok2 && pfon;
+      // then the metadata of the group after it
+      uint32_t pos2n = stream_load<JT>(a, m1, lane, sw) - (BP ? kBpShift - 2 : 0u);
       m1 = load_meta(a, g2, lane);
-      if constexpr (!DEC && !F16) {
-        // the target's two metadata loads in place of the dummy ones
-        const uint32_t* sb = reinterpret_cast<const uint32_t*>(p2 ? p_seg : a.seg_len8);
-        const uint32_t* go = p2 ? p_go : a.grp_meta;
-        const uint64_t fm = p2 ? p_first : m1.first;
-        const uint32_t nm = p2 ? p_G * 4u : m1.N, gm = p2 ? p_g : g2;
-        m1.nbw = sb[(fm + min(lane, nm - 1)) >> 2];
-        m1.u0 = go[2 * gm + meta_pick(lane)];
-        p_meta = p_meta || p2;
-      }
-      // prefetch source: the next group, else the next launch's first group,
-      // else the lane's cached activations (decoding: the current group's
-      // raw bytes)
+      // prefetch source: the next group, else the lane's cached activations
+      // (decoding: the current group's raw bytes)
       const uint32_t cur_c0 = (wave + j * waves) * 4;
       const uint8_t* rbase = okn    ? a.raw + n_first * S
-                             : pfl ? p_raw + p_first * S
                              : DEC ? a.raw + ((uint64_t)rb * 16u * a.L + (uint64_t)cur_c0 * G) * S
                                    : xbytes + cur_c0 * XSEG;
-      const uint32_t roff = okn ? lane_mu(rbn) * 8 : pfl ? (q * p_G + min(i, p_G - 1)) * 8 : DEC ? mu * 8 : xoff;
-      const uint32_t rs = okn ? Gn * 32u : pfl ? p_G * 32u : 0u;
+      const uint32_t roff = okn ? lane_mu(rbn) * 8 : DEC ? mu * 8 : xoff;
+      const uint32_t rs = okn ? Gn * 32u : 0u;
       const uint8_t* xbase = xbytes + (okn ? n_c0 : cur_c0) * XSEG;
       uint32_t pd = (uint32_t)__shfl((int)pos2, (int)mu, 64);
       uint4 dv[DEC ? SP : 1];  // decoding: the lane's weights of the group
@@ -2014,7 +1935,7 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB)) gemv_stream_kernel(Ar
       block_sync_lds();
     }
     // the next group's words, held back for the sum (none after the last
-    // row block: there the registers hold the next launch's, or nothing)
+    // row block, which has no next group)
     if (rb_of(t + 1) < RB) {
       stream_store<JT>(cols, sw, lane);
       wait_lgkm0();
@@ -2188,12 +2109,12 @@ static int stream_rows_for(uint32_t seg_len, uint32_t col_rows, bool f16) {
 
 template <bool XT, int TB>
 static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block, size_t lds,
-                                 hipStream_t s, const StreamArgs& p, const PrefetchArgs& pf) {
+                                 hipStream_t s, const StreamArgs& p) {
   if (seg_len == 64 && multi) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false, TB>, grid, block, lds, s, p, pf);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false, TB>, grid, block, lds, s, p, pf);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false, TB>, grid, block, lds, s, p, pf);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, StreamArgs, false, TB>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, StreamArgs, false, TB>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, StreamArgs, false, TB>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
@@ -2201,16 +2122,16 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
   const GemvArgs& g = p.p;  // one matrix: the small argument block
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false, TB>, grid, block, lds, s, g, pf);
-      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false, TB>, grid, block, lds, s, g, pf);
-      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false, TB>, grid, block, lds, s, g, pf);
+      case 12: return launch(gemv_stream_kernel<8, 12, XT, GemvArgs, false, TB>, grid, block, lds, s, g);
+      case 16: return launch(gemv_stream_kernel<8, 16, XT, GemvArgs, false, TB>, grid, block, lds, s, g);
+      case 20: return launch(gemv_stream_kernel<8, 20, XT, GemvArgs, false, TB>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
   if constexpr (TB == 0) {
     switch (jt) {
-      case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false, 0>, grid, block, lds, s, g, pf);
-      case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false, 0>, grid, block, lds, s, g, pf);
+      case 8: return launch(gemv_stream_kernel<4, 8, XT, GemvArgs, false, 0>, grid, block, lds, s, g);
+      case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, false, 0>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
@@ -2219,13 +2140,13 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
 
 // Grouped launches (multi) exist for S = 64, bounded pairs (bp) for S = 64.
 static hl_status launch_stream(bool xt, bool bp, uint32_t seg_len, int jt, bool multi, dim3 grid, dim3 block,
-                               size_t lds, hipStream_t s, const StreamArgs& p, const PrefetchArgs& pf) {
+                               size_t lds, hipStream_t s, const StreamArgs& p) {
   // the bounded-pair table fill takes at most kBpPerThread entries per thread
   if (bp && block.x < kBpMinThreads) return HL_EINVAL;
-  if (bp) return xt ? launch_stream_x<true, 1>(seg_len, jt, multi, grid, block, lds, s, p, pf)
-                    : launch_stream_x<false, 1>(seg_len, jt, multi, grid, block, lds, s, p, pf);
-  return xt ? launch_stream_x<true, 0>(seg_len, jt, multi, grid, block, lds, s, p, pf)
-            : launch_stream_x<false, 0>(seg_len, jt, multi, grid, block, lds, s, p, pf);
+  if (bp) return xt ? launch_stream_x<true, 1>(seg_len, jt, multi, grid, block, lds, s, p)
+                    : launch_stream_x<false, 1>(seg_len, jt, multi, grid, block, lds, s, p);
+  return xt ? launch_stream_x<true, 0>(seg_len, jt, multi, grid, block, lds, s, p)
+            : launch_stream_x<false, 0>(seg_len, jt, multi, grid, block, lds, s, p);
 }
 
 // The float16 format on the persistent kernel (one matrix, float16 x; with
@@ -2235,15 +2156,15 @@ static hl_status launch_stream16_x(uint32_t seg_len, int jt, dim3 grid, dim3 blo
                                    const GemvArgs& g) {
   if (seg_len == 64) {
     switch (jt) {
-      case 24: return launch(gemv_stream_kernel<8, 24, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g, PrefetchArgs{});
-      case 28: return launch(gemv_stream_kernel<8, 28, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g, PrefetchArgs{});
-      case 32: return launch(gemv_stream_kernel<8, 32, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g, PrefetchArgs{});
+      case 24: return launch(gemv_stream_kernel<8, 24, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+      case 28: return launch(gemv_stream_kernel<8, 28, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+      case 32: return launch(gemv_stream_kernel<8, 32, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g, PrefetchArgs{});
-    case 16: return launch(gemv_stream_kernel<4, 16, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g, PrefetchArgs{});
+    case 12: return launch(gemv_stream_kernel<4, 12, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
+    case 16: return launch(gemv_stream_kernel<4, 16, XT, GemvArgs, DEC, 2>, grid, block, lds, s, g);
     default: return HL_EUNSUPPORTED;
   }
 }
@@ -2260,15 +2181,15 @@ static hl_status launch_stream_dec(uint32_t seg_len, int jt, dim3 grid, dim3 blo
                                    const GemvArgs& p) {
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p, PrefetchArgs{});
-      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true, 0>, grid, block, lds, s, p, PrefetchArgs{});
-      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true, 0>, grid, block, lds, s, p, PrefetchArgs{});
+      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true, 0>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true, 0>, grid, block, lds, s, p);
       default: return HL_EUNSUPPORTED;
     }
   }
   switch (jt) {
-    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true, 0>, grid, block, lds, s, p, PrefetchArgs{});
-    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p, PrefetchArgs{});
+    case 8: return launch(gemv_stream_kernel<4, 8, false, GemvArgs, true, 0>, grid, block, lds, s, p);
+    case 12: return launch(gemv_stream_kernel<4, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p);
     default: return HL_EUNSUPPORTED;
   }
 }
@@ -2688,13 +2609,8 @@ static hl_status gemv_args_ok(const hl_tensor* t, const void* x_dev, hl_dtype x_
 
 // The product of hl_decode_gemv; `clear`: zero the split's arrival counters
 // first (the workspace may hold other bytes there).
-static const PrefetchArgs kNoPrefetch{};
-
-// `pf`: the launch that follows, whose first round the persistent kernel
-// reads into the caches during its last groups (S = 64 only).
 static hl_status gemv_impl(const hl_tensor* t, const void* x_dev, hl_dtype x_dtype, uint32_t batch, float* y_dev,
-                           void* workspace_dev, size_t workspace_bytes, bool clear, hipStream_t stream,
-                           const PrefetchArgs& pf) {
+                           void* workspace_dev, size_t workspace_bytes, bool clear, hipStream_t stream) {
   if (is_fp16(t)) return gemv16(t, x_dev, batch, y_dev, workspace_dev, workspace_bytes, clear, stream);
   Plan pl;
   bool mfma = false, persistent = false;
@@ -2732,7 +2648,7 @@ static hl_status gemv_impl(const hl_tensor* t, const void* x_dev, hl_dtype x_dty
       sa.part0[1] = std::min(RB, cus);
       const bool bp = bounded_pairs(t);
       return launch_stream(xt, bp, t->seg_len, jt, false, dim3(sa.part0[1]), dim3(w * 64), w * per_wave,
-                           stream, sa, t->seg_len == 64 ? pf : kNoPrefetch);
+                           stream, sa);
     }
   }
   // Column blocks per block and blocks per row block.
@@ -2755,8 +2671,7 @@ extern "C" hl_status hl_decode_gemv(const hl_tensor* t, const void* x_dev, hl_dt
   const hl_status st = gemv_args_ok(t, x_dev, x_dtype, batch, y_dev);
   if (st != HL_OK) return st;
   if (!aligned(workspace_dev, 16)) return HL_EINVAL;
-  return gemv_impl(t, x_dev, x_dtype, batch, y_dev, workspace_dev, workspace_bytes, false, (hipStream_t)stream,
-                   kNoPrefetch);
+  return gemv_impl(t, x_dev, x_dtype, batch, y_dev, workspace_dev, workspace_bytes, false, (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ allocation-free product
@@ -2795,8 +2710,7 @@ extern "C" hl_status hl_decode_gemv_noalloc(const hl_tensor* t, const void* x_de
   void* ws = nullptr;
   st = scratch_address(&ws);
   if (st != HL_OK) return st;
-  return gemv_impl(t, x_dev, x_dtype, batch, y_dev, ws, HL_NOALLOC_SCRATCH_BYTES, true, (hipStream_t)stream,
-                   kNoPrefetch);
+  return gemv_impl(t, x_dev, x_dtype, batch, y_dev, ws, HL_NOALLOC_SCRATCH_BYTES, true, (hipStream_t)stream);
 }
 
 // Shape of a grouped launch of the persistent kernel over ts[0..count) (bf16
@@ -2852,56 +2766,9 @@ static bool group_shape(const hl_tensor* const* ts, uint32_t count, GroupShape* 
   return true;
 }
 
-static void prefetch_matrix(PrefetchArgs* pf, uint32_t k, const GroupArgs& ga) {
-  pf->seg_len8[k] = ga.seg_len8;
-  pf->grp_meta[k] = ga.grp_meta;
-  pf->stream[k] = ga.stream;
-  pf->raw[k] = ga.raw;
-  pf->CB[k] = ga.CB;
-  pf->RB[k] = ga.RB;
-  pf->L[k] = ga.L;
-  pf->rows[k] = ga.rows;
-}
-
-// The prefetch target of a launch followed by a launch over next[0..count):
-// that launch's matrices and block partition as it will run them on the
-// persistent kernel (S = 64, bf16 formats, bf16 x); n = 0 when it will not.
-static PrefetchArgs prefetch_for(const hl_tensor* const* next, uint32_t count) {
-  PrefetchArgs pf;
-  std::memset(&pf, 0, sizeof(pf));
-  if (!next || count < 1 || count > kMaxParts) return pf;
-  if (count == 1) {
-    const hl_tensor* t = next[0];
-    Plan pl;
-    bool mfma = false, persistent = false;
-    uint32_t xw = 0;
-    if (!t || is_fp16(t) || t->seg_len != 64 || gemv_plan(t, HL_BF16, 1, &pl, &mfma, &persistent, &xw) != HL_OK ||
-        !persistent)
-      return pf;
-    int jt = 0;
-    uint32_t w = 0;
-    size_t per_wave = 0;
-    if (!stream_shape(t, pl.ga, &jt, &w, &per_wave)) return pf;
-    prefetch_matrix(&pf, 0, pl.ga);
-    pf.part0[1] = std::min(pl.ga.RB, (uint32_t)device_cus());
-    pf.waves = w;
-    pf.n = 1;
-    return pf;
-  }
-  GroupShape g;
-  if (!group_shape(next, count, &g)) return pf;
-  for (uint32_t k = 0; k < count; ++k) {
-    prefetch_matrix(&pf, k, g.pl[k].ga);
-    pf.part0[k + 1] = pf.part0[k] + g.nb[k];
-  }
-  pf.waves = g.w;
-  pf.n = count;
-  return pf;
-}
-
 static hl_status gemv_multi_impl(const hl_tensor* const* ts, uint32_t count, const void* x_dev, hl_dtype x_dtype,
                                  uint32_t batch, float* const* y_devs, void* workspace_dev, size_t workspace_bytes,
-                                 hipStream_t stream, const PrefetchArgs& pf) {
+                                 hipStream_t stream) {
   if (!ts || !y_devs || !x_dev || count < 1 || count > kMaxParts || batch < 1 || batch > HL_MAX_BATCH)
     return HL_EINVAL;
   if (!aligned(x_dev, 16) || !aligned(workspace_dev, 16)) return HL_EINVAL;
@@ -2914,12 +2781,11 @@ static hl_status gemv_multi_impl(const hl_tensor* const* ts, uint32_t count, con
   if (!(x_dtype == HL_BF16 && group_shape(ts, count, &g))) {
     // one product after another on the shared workspace: a split product
     // zeroes its counters first (another matrix's product may have left
-    // partial sums where they lie); a single matrix keeps the prefetch
+    // partial sums where they lie)
     for (uint32_t k = 0; k < count; ++k) {
       hl_status st = gemv_args_ok(ts[k], x_dev, x_dtype, batch, y_devs[k]);
       if (st == HL_OK)
-        st = gemv_impl(ts[k], x_dev, x_dtype, batch, y_devs[k], workspace_dev, workspace_bytes, count > 1, stream,
-                       count == 1 ? pf : kNoPrefetch);
+        st = gemv_impl(ts[k], x_dev, x_dtype, batch, y_devs[k], workspace_dev, workspace_bytes, count > 1, stream);
       if (st != HL_OK) return st;
     }
     return HL_OK;
@@ -2945,25 +2811,14 @@ static hl_status gemv_multi_impl(const hl_tensor* const* ts, uint32_t count, con
     sa.part0[k + 1] = sa.part0[k] + g.nb[k];
   }
   return launch_stream(xt, g.bp, ts[0]->seg_len, g.jt, true, dim3(g.used), dim3(g.w * 64), g.w * g.per_wave,
-                       stream, sa, pf);
+                       stream, sa);
 }
 
 extern "C" hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const void* x_dev,
                                           hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
                                           void* workspace_dev, size_t workspace_bytes, void* stream) {
   return gemv_multi_impl(ts, count, x_dev, x_dtype, batch, y_devs, workspace_dev, workspace_bytes,
-                         (hipStream_t)stream, kNoPrefetch);
-}
-
-extern "C" hl_status hl_decode_gemv_multi_prefetch(const hl_tensor* const* ts, uint32_t count, const void* x_dev,
-                                                   hl_dtype x_dtype, uint32_t batch, float* const* y_devs,
-                                                   void* workspace_dev, size_t workspace_bytes,
-                                                   const hl_tensor* const* next, uint32_t next_count, void* stream) {
-  if ((next == nullptr) != (next_count == 0) || next_count > kMaxParts) return HL_EINVAL;
-  for (uint32_t k = 0; k < next_count; ++k)
-    if (!next[k]) return HL_EINVAL;
-  return gemv_multi_impl(ts, count, x_dev, x_dtype, batch, y_devs, workspace_dev, workspace_bytes,
-                         (hipStream_t)stream, prefetch_for(next, next_count));
+                         (hipStream_t)stream);
 }
 
 // ------------------------------------------------------------------ prefill GEMM host side

@@ -80,8 +80,8 @@ _lib = None
 EXPORTS = ["hl_status_str", "hl_default_seg_len", "hl_default_grp_rows", "hl_build_codebook", "hl_encode",
            "hl_build_codebook8", "hl_encode8", "hl_build_codebook16", "hl_encode16", "hl_validate",
            "hl_tensor_view", "hl_tensor_prepare", "hl_decode", "hl_gemv_workspace_bytes",
-           "hl_decode_gemv", "hl_decode_gemv_noalloc", "hl_decode_gemv_multi", "hl_decode_gemv_multi_prefetch",
-           "hl_gemm_workspace_bytes", "hl_decode_gemm",
+           "hl_decode_gemv", "hl_decode_gemv_noalloc", "hl_decode_gemv_multi", "hl_gemm_workspace_bytes",
+           "hl_decode_gemm",
            "hl_gemv_bf16"]
 
 
@@ -134,10 +134,6 @@ def lib() -> ctypes.CDLL:
     L.hl_decode_gemv_multi.restype = c.c_int
     L.hl_decode_gemv_multi.argtypes = [c.c_void_p, c.c_uint32, c.c_void_p, c.c_int, c.c_uint32, c.c_void_p,
                                        c.c_void_p, c.c_size_t, c.c_void_p]
-    L.hl_decode_gemv_multi_prefetch.restype = c.c_int
-    L.hl_decode_gemv_multi_prefetch.argtypes = [c.c_void_p, c.c_uint32, c.c_void_p, c.c_int, c.c_uint32,
-                                                c.c_void_p, c.c_void_p, c.c_size_t, c.c_void_p, c.c_uint32,
-                                                c.c_void_p]
     L.hl_gemm_workspace_bytes.restype = c.c_size_t
     L.hl_gemm_workspace_bytes.argtypes = [c.POINTER(TensorView), c.c_uint32]
     L.hl_decode_gemm.restype = c.c_int
@@ -409,15 +405,12 @@ class DeviceTensor:
         return y
 
 
-def gemv_multi(tensors, x, ys=None, stream=None, workspace=None, prefetch=None):
+def gemv_multi(tensors, x, ys=None, stream=None, workspace=None):
     """ys[m][b, r] = sum_k W_m[r, k] x[b, k] for up to 4 DeviceTensors with the
     same columns that share x (one grouped launch where the library can).
 
     ``workspace`` defaults to the largest of the tensors' cached workspaces;
-    pass False to run without one. ``prefetch``: the DeviceTensors of the
-    gemv_multi (or, one tensor, gemv) call that follows on the stream, whose
-    first groups this launch reads into the caches during its last ones
-    (same results)."""
+    pass False to run without one."""
     import torch
     if not 1 <= len(tensors) <= 4:
         raise ValueError("one to four tensors")
@@ -441,17 +434,6 @@ def gemv_multi(tensors, x, ys=None, stream=None, workspace=None, prefetch=None):
                                                           workspace.numel() * workspace.element_size())
     views = (ctypes.POINTER(TensorView) * len(tensors))(*[ctypes.pointer(t.view) for t in tensors])
     outs = (ctypes.c_void_p * len(tensors))(*[y.data_ptr() for y in ys])
-    if prefetch:
-        if not 1 <= len(prefetch) <= 4 or any(t.blob.device != dev for t in prefetch):
-            raise ValueError("prefetch: one to four tensors on the same device")
-        nxt = (ctypes.POINTER(TensorView) * len(prefetch))(*[ctypes.pointer(t.view) for t in prefetch])
-        _check(lib().hl_decode_gemv_multi_prefetch(ctypes.cast(views, ctypes.c_void_p), len(tensors),
-                                                   ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
-                                                   ctypes.cast(outs, ctypes.c_void_p), ws_ptr, ws_n,
-                                                   ctypes.cast(nxt, ctypes.c_void_p), len(prefetch),
-                                                   _stream_ptr(stream)),
-               "hl_decode_gemv_multi_prefetch")
-        return ys
     _check(lib().hl_decode_gemv_multi(ctypes.cast(views, ctypes.c_void_p), len(tensors),
                                       ctypes.c_void_p(x.data_ptr()), dt, x.shape[0],
                                       ctypes.cast(outs, ctypes.c_void_p), ws_ptr, ws_n, _stream_ptr(stream)),

@@ -77,48 +77,3 @@ def test_grouped_gemv_errors(torch):
                                          None) == hl.HL_EINVAL
     with pytest.raises(ValueError):
         hl.gemv_multi([a] * 5, x)
-
-
-def test_prefetch_of_the_next_launch(torch):
-    """A chain of launches shaped like a decoder layer (grouped q/k/v, o,
-    grouped gate/up, down, then q/k/v again), each reading the next launch's
-    first groups into the caches during its last ones: outputs equal, bit for
-    bit, those of the same launches without the prefetch, at batch 1, 5 and
-    16; a next launch that does not run the persistent kernel (a lone
-    1024-row matrix) is skipped; argument errors."""
-    print("prefetch chain", flush=True)
-    shapes = {"q": (4096, 4096), "k": (1024, 4096), "v": (1024, 4096), "o": (4096, 4096),
-              "gate": (8192, 4096), "up": (8192, 4096), "down": (4096, 8192), "small": (1024, 4096)}
-    W = {n: random_bf16(s, seed=300 + k) for k, (n, s) in enumerate(shapes.items())}
-    T = {n: hl.DeviceTensor(hl.encode(w)) for n, w in W.items()}
-    chain = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"], ["q", "k", "v"], ["small"], ["o"]]
-    for B in (1, 5, 16):
-        xs = {c: torch.from_numpy(random_x(B, c, seed=B + c, dtype="bf16").view(np.int16)).cuda().view(torch.bfloat16)
-              for c in (4096, 8192)}
-        got, ref = [], []
-        for k, names in enumerate(chain):
-            ts = [T[n] for n in names]
-            x = xs[ts[0].shape[1]]
-            nxt = [T[n] for n in chain[k + 1]] if k + 1 < len(chain) else None
-            got.append([y.clone() for y in hl.gemv_multi(ts, x, prefetch=nxt)])
-        for names in chain:
-            ts = [T[n] for n in names]
-            ref.append([y.clone() for y in hl.gemv_multi(ts, xs[ts[0].shape[1]])])
-        torch.cuda.synchronize()
-        for names, g, r in zip(chain, got, ref):
-            for n, a, b in zip(names, g, r):
-                assert torch.equal(a, b), (B, n)
-        # and the products themselves, on sampled rows
-        w = W["gate"]
-        rows = [0, 4095, 8191]
-        xh = xs[4096].view(torch.int16).cpu().numpy().view(np.uint16)
-        yo, do = ogemv.gemv_rows(w, xh, rows=rows)
-        assert (np.abs(got[2][0].cpu().numpy()[:, rows] - yo) / (do + 1e-30)).max() <= TOL
-    x = xs[4096]
-    import ctypes
-    views = (ctypes.POINTER(hl.TensorView) * 1)(ctypes.pointer(T["o"].view))
-    y = torch.empty((16, 4096), dtype=torch.float32, device="cuda")
-    outs = (ctypes.c_void_p * 1)(y.data_ptr())
-    assert hl.lib().hl_decode_gemv_multi_prefetch(ctypes.cast(views, ctypes.c_void_p), 1, ctypes.c_void_p(x.data_ptr()),
-                                                  hl.HL_BF16, 16, ctypes.cast(outs, ctypes.c_void_p), None, 0, None,
-                                                  2, None) == hl.HL_EINVAL
