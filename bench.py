@@ -89,11 +89,15 @@ def parse():
                     help="print the profile summary of a rocprofv3 --kernel-trace --stats run of the headline "
                          "(run_kernel_stats.csv and run_kernel_trace.csv in TRACE_DIR; the run's JSON line in "
                          "BENCH_LOG) and exit; no GPU needed")
+    ap.add_argument("--secondary-run", action="store_true",
+                    help="time the decode, float16 and whole-exponent GEMVs and the prefill decode-GEMM one after "
+                         "another (for a kernel trace; see --summarize-runs) and print one JSON line")
     ap.add_argument("--ab-run", action="store_true",
                     help="run only the batch-1 matrix-core against vector-kernel comparison (for a kernel trace)")
     ap.add_argument("--summarize-runs", nargs=2, metavar=("TRACE_DIR", "RUN_LOG"),
-                    help="print the per-run summary of a rocprofv3 --kernel-trace run of --ab-run (consecutive "
-                         "dispatches of one kernel and grid) and exit; no GPU needed")
+                    help="print the summary of a rocprofv3 --kernel-trace run of --ab-run (runs of consecutive "
+                         "dispatches of one kernel and grid) or of --secondary-run (dispatches by kernel and grid) "
+                         "and exit; no GPU needed")
     ap.add_argument("--summarize-counters", nargs="+", metavar="PATH",
                     help="RUN_LOG DIR [DIR ...]: print the counter summary of rocprofv3 --pmc passes of "
                          "--counter-run (one directory per pass) and exit; no GPU needed")
@@ -596,6 +600,50 @@ def mfma_vs_vector(torch, hl):
     return out
 
 
+def secondary_run(torch, hl):
+    """The library's other kernels one operation after another, each on cold
+    replicas and graph-timed (for a kernel trace): the decode to 16-bit
+    weights in every container format, the float16 and whole-exponent GEMVs at
+    batch 1, on the 4096x4096 projection and the 70B gate matrix, and the
+    prefill decode-GEMM of the projection at 32, 128 and 512 tokens."""
+    from gen import bf16_bits_to_f16_bits, workload_matrices, gen_matrix, random_x
+    out = {}
+    for mname, (cfg, idx) in (("4096x4096", (2, 0)), ("28672x8192", (5, 4))):
+        sp = workload_matrices(cfg)[idx]
+        W = gen_matrix(sp)
+        n = sp.rows * sp.cols
+        dec = torch.empty((sp.rows, sp.cols), dtype=torch.int16, device="cuda")
+        for f in FORMATS:
+            blob = hl.encode(bf16_bits_to_f16_bits(W) if f == "fp16" else W, **FORMATS[f][0])
+            reps = [hl.DeviceTensor(blob) for _ in range(max(2, math.ceil(COLD_BYTES / blob.size)))]
+            r = {}
+            ms = time_graph_long(torch, lambda i: reps[i].decode(dec), len(reps))
+            r["decode"] = dict(ms=round(ms, 5), compressed_GBps=round(blob.size / (ms * 1e-3) / 1e9, 1),
+                               read_and_written_GBps=round((blob.size + 2 * n) / (ms * 1e-3) / 1e9, 1))
+            if f != "split":
+                for t_ in reps:
+                    t_.workspace()
+                _, xd = device_x(torch, sp, 1, f)
+                y = torch.empty((1, sp.rows), dtype=torch.float32, device="cuda")
+                ms = time_graph_long(torch, lambda i: reps[i].gemv(xd, y), len(reps))
+                r["gemv_batch1"] = dict(ms=round(ms, 5), compressed_GBps=round(blob.size / (ms * 1e-3) / 1e9, 1))
+            if f == "split" and mname == "4096x4096":
+                for T in (32, 128, 512):
+                    xb = random_x(T, sp.cols, seed=T, dtype="bf16")
+                    xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+                    y = torch.empty((T, sp.rows), dtype=torch.float32, device="cuda")
+                    reps[0].gemm(xd, y)  # workspace allocated outside the graph
+                    for t_ in reps:
+                        t_._gemm_ws = reps[0]._gemm_ws
+                    ms = time_graph_long(torch, lambda i: reps[i].gemm(xd, y), len(reps))
+                    r[f"prefill_tokens{T}"] = dict(ms=round(ms, 5),
+                                                   TFLOPs=round(2 * n * T / (ms * 1e-3) / 1e12, 2))
+            out[f"{mname}_{f}"] = r
+            del reps
+            torch.cuda.empty_cache()
+    return out
+
+
 def matrix_detail(torch, hl, args):
     """The 4096x4096 projection (per-row scales): batches 1, 4 and 16 in every
     container format with comparators, the prefill decode-GEMM and the host
@@ -797,6 +845,9 @@ def summarize_runs(trace_dir, run_log):
     order, grouped into runs of consecutive dispatches of one kernel and grid
     (each timing is a launch outside the graph, a warm-up graph and the timed
     graph), with the run's mean and median duration; then the run's own line."""
+    if '"secondary_run"' in open(run_log).read():
+        summarize_secondary(trace_dir, run_log)
+        return
     d = _json_line(run_log, '"ab_run"')
     disp = [r for r in _csv_rows(os.path.join(trace_dir, "run_kernel_trace.csv")) if "hl::" in r["Kernel_Name"]]
     disp.sort(key=lambda r: int(r["Start_Timestamp"]))
@@ -820,6 +871,35 @@ def summarize_runs(trace_dir, run_log):
     for m, r in d["mfma_vs_vector_batch1"].items():
         out.append(f"  {m}: " + ", ".join(f"{k} {v['ms'] * 1e3:.2f} us ({v['compressed_GBps']} GB/s)"
                                           for k, v in r.items()))
+    out.append(f"kernel source sha256[:16]: {d['kernel_sha256_16']}")
+    print("\n".join(out))
+
+
+def summarize_secondary(trace_dir, run_log):
+    """Kernel-trace summary of --secondary-run: every kernel of the library
+    (and hipBLASLt's, for the prefill of many tokens) by name, grid and
+    workgroup, in the order first seen: dispatch count, mean and median
+    duration; then the run's line."""
+    d = _json_line(run_log, '"secondary_run"')
+    rows = [r for r in _csv_rows(os.path.join(trace_dir, "run_kernel_trace.csv"))
+            if "hl::" in r["Kernel_Name"] or r["Kernel_Name"].startswith("Cijk")]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    by = {}
+    for r in rows:
+        name = r["Kernel_Name"].split("(")[0]
+        key = (name if len(name) <= 110 else name[:107] + "...", r["Grid_Size_X"], r["Workgroup_Size_X"])
+        by.setdefault(key, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    out = ["Dispatches by kernel, grid x workgroup threads (in the order first seen): count, mean and median "
+           "duration over all of them (probe, warm-up and timed graphs):"]
+    for (name, grid, wg), ds in by.items():
+        ds_sorted = sorted(ds)
+        out.append(f"  {name}  grid {grid} x {wg}: {len(ds)} dispatches, mean {sum(ds) / len(ds) / 1e3:.2f} us, "
+                   f"median {ds_sorted[len(ds) // 2] / 1e3:.2f} us")
+    out.append("The run's line (graph-timed, HIP events, cold replicas):")
+    for m, r in d["operations"].items():
+        out.append(f"  {m}: " + "; ".join(
+            f"{k} {v['ms'] * 1e3:.2f} us (" + ", ".join(f"{a} {b}" for a, b in v.items() if a != "ms") + ")"
+            for k, v in r.items()))
     out.append(f"kernel source sha256[:16]: {d['kernel_sha256_16']}")
     print("\n".join(out))
 
@@ -914,7 +994,7 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the sharded layout is described in the design notes)", file=sys.stderr)
         sys.exit(2)
-    headline = not (args.workloads or args.counter_run or args.traffic_run or args.ab_run)
+    headline = not (args.workloads or args.counter_run or args.traffic_run or args.ab_run or args.secondary_run)
     # the oracle on all host cores first, in processes forked before anything touches the GPU
     cpu = cpu_oracle_baseline() if headline and not args.no_cpu else None
     import torch
@@ -933,6 +1013,10 @@ def main():
         return
     if args.ab_run:
         print(json.dumps({"ab_run": True, "mfma_vs_vector_batch1": mfma_vs_vector(torch, hl),
+                          "kernel_sha256_16": kernel_hash()}), flush=True)
+        return
+    if args.secondary_run:
+        print(json.dumps({"secondary_run": True, "operations": secondary_run(torch, hl),
                           "kernel_sha256_16": kernel_hash()}), flush=True)
         return
     if args.counter_run:
