@@ -361,11 +361,14 @@ hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const
 size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
 
 /* Prefill product Y[n][r] = sum_k W[r][k] * X[n][k] for n < tokens (many
- * activation rows; the paper's prompts of tens of tokens, Sec. 4). Up to 112
- * tokens each 16-row x 4-segment weight tile is decoded once per chunk of up
- * to 128 tokens and multiplied with all of them on the matrix cores (Sec.
- * 3.2: weights decompressed only to be multiplied), every output summed in a
- * fixed order; beyond that, where the product is compute-bound (Sec. 5), the
+ * activation rows; the paper's prompts of tens of tokens, Sec. 4). Up to 32
+ * tokens on matrices with at least one 16-row block per compute unit, the
+ * persistent fused decode-GEMV multiplies each decoded 8-weight step with one
+ * or two 16-token tiles (the activations first copied to the workspace in
+ * 16- or 32-row chunks); otherwise, up to 112 tokens, each 16-row x 4-segment
+ * weight tile is decoded once per chunk of up to 128 tokens and multiplied
+ * with all of them on the matrix cores (Sec. 3.2: weights decompressed only
+ * to be multiplied); every output summed in a fixed order; beyond that, where the product is compute-bound (Sec. 5), the
  * matrix is decoded once into the workspace (hl_decode) and multiplied by
  * hipBLASLt. x_dev: [tokens][cols] bf16; y_dev: [tokens][rows] float32 (fully
  * written); fp32 accumulation. bf16 formats (split or whole exponent) with

@@ -6,7 +6,8 @@ Every output against a float64 product of the exact bf16 values and sampled
 outputs against the oracle's exactly rounded sums, |y - y_ref| <= 1e-3 *
 sum_k |w x|: token counts 1 .. 300 (one and several chunks, ragged last
 tile), ragged row sets and row blocks, S = 32 and 64, both bf16 formats,
-repeated calls on one workspace; unsupported requests are reported.
+repeated calls on one workspace; up to 32 tokens on the persistent kernel
+(one or two 16-token tiles); unsupported requests are reported.
 """
 import numpy as np
 import pytest
@@ -66,6 +67,41 @@ def test_shapes_and_formats(torch, shape, S, whole):
     assert dt.view.grp_rows == 16
     for T in (33, 128):
         _check(torch, dt, w, T, seed=T + S)
+
+
+def _persistent_shape(torch, rows, cols, S):
+    """Whether a product of this shape runs on the persistent kernel: at least
+    one 16-row block per compute unit and two 256-column groups per wave of a
+    block of eight."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    RB, CB = -(-rows // 16), cols // (4 * S)
+    return RB >= cus and CB >= 8 and RB * CB >= 2 * cus * 8
+
+
+@pytest.mark.parametrize("shape,S,fmt", [((4100, 4096), 64, "split"), ((4100, 4096), 64, "whole"),
+                                         ((4096, 4096), 32, "split"), ((4112, 8192), 64, "split_unbounded")])
+def test_persistent_up_to_32_tokens(torch, shape, S, fmt):
+    """Up to 32 tokens on matrices the persistent kernel takes: one 16-token
+    tile per decode step, or two (17..32 tokens), sums per row block in one
+    block; ragged last row block (4100 rows), bounded-pair and joint tables."""
+    print(f"gemm persistent {shape} S={S} {fmt}", flush=True)
+    assert _persistent_shape(torch, shape[0], shape[1], S)
+    kw = {"whole": {"whole_exponent": True}, "split_unbounded": {"pair_max": 0}}.get(fmt, {})
+    w = random_bf16(shape, seed=shape[0] + S + len(fmt))
+    dt = hl.DeviceTensor(hl.encode(w, seg_len=S, **kw))
+    for T in (1, 7, 16, 17, 23, 32):
+        print(f"  T={T}", flush=True)
+        _check(torch, dt, w, T, seed=T + S)
+
+
+def test_persistent_two_tiles_repeat(torch):
+    print("gemm persistent two tiles repeated", flush=True)
+    w = random_bf16((4100, 4096), seed=11)
+    dt = hl.DeviceTensor(hl.encode(w))
+    x = _xdev(torch, random_x(29, 4096, seed=12, dtype="bf16"))
+    y1 = dt.gemm(x).cpu().numpy()
+    for _ in range(3):
+        assert np.array_equal(y1, dt.gemm(x).cpu().numpy())   # fixed summation order
 
 
 def test_repeated_calls_share_the_workspace(torch):
