@@ -356,8 +356,9 @@ hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const
 
 /* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows:
  * up to 112 tokens the partial sums of up to one range per column block of
- * four segments, beyond that the decoded weights (rows * cols * 2); 0 for
- * tensors it does not take. */
+ * four segments (on the persistent kernel's matrices, up to 32 tokens, only
+ * the tiled activations use it), beyond that the decoded weights
+ * (rows * cols * 2); 0 for tensors it does not take. */
 size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
 
 /* Prefill product Y[n][r] = sum_k W[r][k] * X[n][k] for n < tokens (many
