@@ -94,6 +94,36 @@ def test_persistent_up_to_32_tokens(torch, shape, S, fmt):
         _check(torch, dt, w, T, seed=T + S)
 
 
+def test_persistent_two_tiles_70b_gate(torch):
+    """The 70B gate matrix (28672x8192, drawn from its own seed) at 24 and 32
+    tokens on the two-tile form: sampled rows against the oracle's exactly
+    rounded sums, every output against a float32 product of the original
+    weights (torch, on the GPU), within 1e-3 of sum_k |w x|."""
+    from gen import workload_matrices, gen_matrix
+    spec = workload_matrices(5)[4]
+    print(f"gemm persistent two tiles {spec.rows}x{spec.cols}", flush=True)
+    w = gen_matrix(spec)
+    dt = hl.DeviceTensor(hl.encode(w))
+    assert _persistent_shape(torch, spec.rows, spec.cols, 64)
+    wf = torch.from_numpy(w.view(np.int16)).cuda().view(torch.bfloat16).float()
+    rng = np.random.default_rng(5)
+    rows = sorted({0, spec.rows - 1} | set(int(r) for r in rng.integers(0, spec.rows, 6)))
+    for T in (24, 32):
+        print(f"  T={T}", flush=True)
+        x = random_x(T, spec.cols, seed=T, dtype="bf16")
+        xd = _xdev(torch, x)
+        y = dt.gemm(xd)
+        xf = xd.float()
+        ref = xf @ wf.T
+        den = xf.abs() @ wf.abs().T
+        err = ((y - ref).abs() / (den + 1e-30)).max().item()
+        assert err <= TOL, (T, err)
+        yo, do = ogemv.gemv_rows(w, x, rows=rows)
+        yh = y.cpu().numpy().astype(np.float64)
+        assert np.max(np.abs(yh[:, rows] - yo) / (do + 1e-30)) <= TOL
+    del wf
+
+
 def test_persistent_two_tiles_repeat(torch):
     print("gemm persistent two tiles repeated", flush=True)
     w = random_bf16((4100, 4096), seed=11)
