@@ -410,7 +410,7 @@ def measure_workloads(torch, hl):
         torch.cuda.empty_cache()
 
 
-def measure_prefill(torch, hl, blob, spec, W, args, token_counts=(32, 128, 512)):
+def measure_prefill(torch, hl, blob, spec, W, args, token_counts=(32, 64, 128, 512)):
     """Graph-timed prefill products Y = X W^T for several token counts over cold
     replicas of the container, with torch's bf16 GEMM on cold replicas of the
     uncompressed matrix as the comparator; sampled outputs of the timed launches
@@ -605,7 +605,7 @@ def secondary_run(torch, hl):
     replicas and graph-timed (for a kernel trace): the decode to 16-bit
     weights in every container format, the float16 and whole-exponent GEMVs at
     batch 1, on the 4096x4096 projection and the 70B gate matrix, and the
-    prefill decode-GEMM of the projection at 32, 128 and 512 tokens."""
+    prefill decode-GEMM of the projection at 32, 64, 128 and 512 tokens."""
     from gen import bf16_bits_to_f16_bits, workload_matrices, gen_matrix, random_x
     out = {}
     for mname, (cfg, idx) in (("4096x4096", (2, 0)), ("28672x8192", (5, 4))):
@@ -628,7 +628,7 @@ def secondary_run(torch, hl):
                 ms = time_graph_long(torch, lambda i: reps[i].gemv(xd, y), len(reps))
                 r["gemv_batch1"] = dict(ms=round(ms, 5), compressed_GBps=round(blob.size / (ms * 1e-3) / 1e9, 1))
             if f == "split" and mname == "4096x4096":
-                for T in (32, 128, 512):
+                for T in (32, 64, 128, 512):
                     xb = random_x(T, sp.cols, seed=T, dtype="bf16")
                     xd = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
                     y = torch.empty((T, sp.rows), dtype=torch.float32, device="cuda")

@@ -1305,9 +1305,10 @@ __global__ void __launch_bounds__(256) gemm_reduce_kernel(const float* partial, 
 }
 
 // Tiled copy of bf16 activations for batches above one: xt[c][n][0..8) =
-// x[min(n, B - 1)][8c .. 8c + 8) for the 16 lanes n of a matrix-instruction
-// B operand, so that the 16 lanes reading one 8-column chunk read 256
-// contiguous bytes (from x itself they touch 16 rows, 16 cache lines).
+// x[min(n, B - 1)][8c .. 8c + 8) for the R = 16 rows n of a matrix-instruction
+// B operand (or 32, 64: two or four of them, one after another), so that the
+// 16 lanes reading one 8-column chunk read 256 contiguous bytes (from x itself
+// they touch 16 rows, 16 cache lines).
 template <uint32_t R>
 __global__ void __launch_bounds__(256) xtile_kernel(const uint4* x, uint32_t B, uint32_t chunks, uint4* xt) {
   const uint32_t k = blockIdx.x * blockDim.x + threadIdx.x;
@@ -1714,12 +1715,12 @@ __device__ inline const GemvArgs& gemv_args(const Args& x) {
 // float16 format's three field tables (at the start of the dynamic LDS, its
 // sign plane instead of raw bytes, the float16 matrix instruction).
 // NT = 16-token tiles of activations per matrix instruction step: 1 (up to 16
-// activation rows), or 2 for prefill products of 17 to 32 tokens (one bf16
-// matrix, activations read directly).
-// Blocks of at most 16 waves (8 decoding or with two tiles, 12 for the float16
-// product, whose longer stream columns need more registers).
+// activation rows), or 2 or 4 for prefill products of 17 to 32 or 33 to 64
+// tokens (one bf16 matrix, activations from their tiled copy).
+// Blocks of at most 16 waves (8 decoding or with several tiles, 12 for the
+// float16 product, whose longer stream columns need more registers).
 constexpr uint32_t stream_threads(bool dec, int tb, int nt = 1) {
-  return dec || nt == 2 ? 512 : tb == 2 ? 768 : 1024;
+  return dec || nt > 1 ? 512 : tb == 2 ? 768 : 1024;
 }
 
 template <int SP, int JT, bool XT, class Args, bool DEC, int TB, int NT = 1>
@@ -1729,8 +1730,10 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
   constexpr uint32_t kRows = JT + 1, kBuf = kRows * kCol;
   static_assert(JT % 4 == 0 && kBuf >= 256, "layout");
   static_assert(!(F16 && std::is_same_v<Args, StreamArgs>), "the float16 form runs one matrix per launch");
-  static_assert(NT == 1 || (NT == 2 && !DEC && !F16 && std::is_same_v<Args, GemvArgs> && kBuf >= 512),
-                "two token tiles: one bf16 matrix, both tiles' sums in a wave region");
+  static_assert(NT == 1 || ((NT == 2 || NT == 4) && XT && !DEC && !F16 && std::is_same_v<Args, GemvArgs> &&
+                            kBuf >= 256u * NT),
+                "several token tiles: one bf16 matrix, every tile's sums in a wave region");
+  constexpr int NE = NT > 1 ? NT - 1 : 1;  // the tiles after the first (their arrays)
   constexpr bool kMulti = std::is_same_v<Args, StreamArgs>;
   const GemvArgs& p = gemv_args(sa);
   // this block's matrix (wave-uniform; its arguments are read in place)
@@ -1759,12 +1762,11 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
   // where the 16 batch rows' pieces of one 8-column chunk are 256 contiguous
   // bytes (a wave-uniform base plus a 32-bit lane offset lets the prefetch
   // loads address as scalar base + vector offset + immediate)
-  // (two tiles: 32 rows per chunk in the tiled copy, the second tile's 16
-  // right after the first's)
+  // (NT tiles: 16 NT rows per chunk in the tiled copy, tile after tile)
   constexpr uint32_t XSEG = XT ? SP * 256 * NT : S * 2, XSTEP = XT ? 256 * NT : 16;
   const uint32_t xoff = XT ? (q * SP * 16 * NT + i) * 16u : (min(i, p.B - 1) * a.cols + q * S) * 2u;
-  // the second tile: activation rows 16 + i (the last one repeated past B)
-  const uint32_t xoff2 = NT == 1 ? 0u : XT ? xoff + 256u : (min(16 + i, p.B - 1) * a.cols + q * S) * 2u;
+  // tile u > 0: activation rows 16u + i, 256u bytes after the first tile's
+  // in the tiled copy
   const uint8_t* xbytes = reinterpret_cast<const uint8_t*>(p.x);
   const uint32_t CB = a.CB, RB = a.RB, nj = (CB + waves - 1) / waves;
   const uint32_t last_group = RB * CB - 1;
@@ -1807,7 +1809,7 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
   uint2 rw[F16 ? 1 : SP];  // raw bytes of the next group's steps (bf16 formats)
   Signs<SP> sg, sgn;       // float16: the lane's sign bytes of this and the next group
   uint4 xv[SP];
-  uint4 xv2[NT == 2 ? SP : 1];  // the second tile's activations
+  uint4 xe[NE][SP];  // the other tiles' activations
   // raw bytes of the first group's first half of the steps with its stream
   // words, the second half once those are in: every wave requests its first
   // group at once, and a wave's stream words would otherwise queue behind
@@ -1823,7 +1825,18 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
     for (int k = 0; k < SP; ++k) {
       if constexpr (!F16) if (k < kEarlyRaw) rw[k] = *reinterpret_cast<const uint2*>(raw0 + k * G * 32u);
       if constexpr (!DEC) xv[k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff + k * XSTEP);
-      if constexpr (NT == 2) xv2[k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff2 + k * XSTEP);
+#pragma unroll
+      for (int u = 1; u < NT; ++u)
+        xe[u - 1][k] = *reinterpret_cast<const uint4*>(xbytes + m0.c0 * XSEG + xoff + 256u * u + k * XSTEP);
+    }
+    if constexpr (NT == 4) {
+      // a precaution: no scalar write into these loads' scalar base right
+      // behind them (such a write two instructions after a buffer load was
+      // the one pattern of a form of this kernel that gave wrong products;
+      // of the forms here only this one's prologue had it)
+      __builtin_amdgcn_sched_barrier(0);
+      asm volatile("s_nop 2");
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
   stream_store<JT>(cols, sw, lane);
@@ -1838,7 +1851,10 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
   }
   __syncthreads();
 
-  f32x4_t acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4_t acce[NE];  // the other tiles' sums
+#pragma unroll
+  for (int u = 0; u < NE; ++u) acce[u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (uint32_t t = 0; rb_of(t) < RB; ++t) {
     const uint32_t rb = rb_of(t);
     const uint32_t G = min(16u, a.rows - rb * 16);
@@ -1903,25 +1919,32 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
           if constexpr (NT == 1) {
             mfma_operand_guard();
           } else {
-            // two tiles: each matrix instruction directly followed by its
-            // guard, in this order (left to the scheduler, the instructions
-            // moved into the next step's decode, or the guard between the
-            // two, and a write to their operand registers came right after)
+            // several tiles: each matrix instruction directly followed by
+            // its guard, in this order (left to the scheduler, the
+            // instructions moved into the next step's decode, or the guard
+            // between two of them, and a write to their operand registers
+            // came right after)
             __builtin_amdgcn_sched_barrier(0);
             acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
                                                           __builtin_bit_cast(bf16x8_t, xv[k]), acc, 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
             mfma_operand_guard();
             __builtin_amdgcn_sched_barrier(0);
-            acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
-                                                           __builtin_bit_cast(bf16x8_t, xv2[k]), acc2, 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-            mfma_operand_guard();
-            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int u = 0; u < NT - 1; ++u) {
+              acce[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wv),
+                                                                __builtin_bit_cast(bf16x8_t, xe[u][k]), acce[u], 0, 0,
+                                                                0);
+              __builtin_amdgcn_sched_barrier(0);
+              mfma_operand_guard();
+              __builtin_amdgcn_sched_barrier(0);
+            }
           }
           // x first: the wait for the raw bytes at their use then covers both
           xv[k] = *reinterpret_cast<const uint4*>(xbase + xoff + k * XSTEP);
-          if constexpr (NT == 2) xv2[k] = *reinterpret_cast<const uint4*>(xbase + xoff2 + k * XSTEP);
+#pragma unroll
+          for (int u = 1; u < NT; ++u)
+            xe[u - 1][k] = *reinterpret_cast<const uint4*>(xbase + xoff + 256u * u + k * XSTEP);
         }
         if constexpr (F16) {
           if (k == 0) sgn.load(sgnext);
@@ -1958,10 +1981,11 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
 #pragma unroll
       for (int v = 0; v < 4; ++v) red[v * 64 + lane] = acc[v];
       acc = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      if constexpr (NT == 2) {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) red[256 + v * 64 + lane] = acc2[v];
-        acc2 = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int u = 0; u < NT - 1; ++u) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) red[256 * (u + 1) + v * 64 + lane] = acce[u][v];
+        acce[u] = f32x4_t{0.f, 0.f, 0.f, 0.f};
       }
       block_sync_lds();
       if constexpr (NT == 1) {
@@ -1972,9 +1996,9 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
           if (i < p.B && 4 * q + v < G) yp[(uint64_t)i * a.rows + rb * 16 + 4 * q + v] = sum;
         }
       } else {
-        // waves 0-3 the first tile's rows, 4-7 the second's (blocks of 8 waves)
-        if (wave < 8) {
-          const uint32_t v = wave & 3, tile = wave >> 2, n = tile * 16 + i;
+        // wave u % waves sums piece v = u % 4 of tile u / 4 (blocks of 8 waves)
+        for (uint32_t u = wave; u < 4u * NT; u += waves) {
+          const uint32_t v = u & 3, tile = u >> 2, n = tile * 16 + i;
           float sum = 0.f;
           for (uint32_t w = 0; w < waves; ++w)
             sum += reinterpret_cast<const float*>(s_dyn + kTab + w * kBuf)[tile * 256 + v * 64 + lane];
@@ -2187,20 +2211,29 @@ static hl_status launch_stream_x(uint32_t seg_len, int jt, bool multi, dim3 grid
   return HL_EUNSUPPORTED;
 }
 
-// The two-tile form (17 to 32 activation rows): one matrix, x from its tiled
-// copy (32 rows per 8-column chunk).
-template <int TB>
-static hl_status launch_stream_nt2_tb(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                                      const GemvArgs& g) {
+// The forms with NT = 2 or 4 tiles (17 to 32 or 33 to 64 activation rows):
+// one matrix, x from its tiled copy (16 NT rows per 8-column chunk). Four
+// tiles need columns of at least 16 words (their sums fill 4 KB of a wave's
+// region).
+static bool tiles_supported(int nt, uint32_t seg_len, int jt) {
+  return nt == 2 || (nt == 4 && seg_len == 64 && jt >= 16);
+}
+
+template <int TB, int NT>
+static hl_status launch_stream_tiles_tb(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+                                        const GemvArgs& g) {
   if (seg_len == 64) {
     switch (jt) {
-      case 12: return launch(gemv_stream_kernel<8, 12, true, GemvArgs, false, TB, 2>, grid, block, lds, s, g);
-      case 16: return launch(gemv_stream_kernel<8, 16, true, GemvArgs, false, TB, 2>, grid, block, lds, s, g);
-      case 20: return launch(gemv_stream_kernel<8, 20, true, GemvArgs, false, TB, 2>, grid, block, lds, s, g);
+      case 12:
+        if constexpr (NT == 2)
+          return launch(gemv_stream_kernel<8, 12, true, GemvArgs, false, TB, 2>, grid, block, lds, s, g);
+        return HL_EUNSUPPORTED;
+      case 16: return launch(gemv_stream_kernel<8, 16, true, GemvArgs, false, TB, NT>, grid, block, lds, s, g);
+      case 20: return launch(gemv_stream_kernel<8, 20, true, GemvArgs, false, TB, NT>, grid, block, lds, s, g);
       default: return HL_EUNSUPPORTED;
     }
   }
-  if constexpr (TB == 0) {
+  if constexpr (TB == 0 && NT == 2) {
     switch (jt) {
       case 8: return launch(gemv_stream_kernel<4, 8, true, GemvArgs, false, 0, 2>, grid, block, lds, s, g);
       case 12: return launch(gemv_stream_kernel<4, 12, true, GemvArgs, false, 0, 2>, grid, block, lds, s, g);
@@ -2210,11 +2243,15 @@ static hl_status launch_stream_nt2_tb(uint32_t seg_len, int jt, dim3 grid, dim3 
   return HL_EUNSUPPORTED;
 }
 
-static hl_status launch_stream_nt2(bool bp, uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds,
-                                   hipStream_t s, const GemvArgs& g) {
-  if (block.x != stream_threads(false, bp ? 1 : 0, 2)) return HL_EINVAL;  // eight waves: both tiles' sums
-  return bp ? launch_stream_nt2_tb<1>(seg_len, jt, grid, block, lds, s, g)
-            : launch_stream_nt2_tb<0>(seg_len, jt, grid, block, lds, s, g);
+static hl_status launch_stream_tiles(int nt, bool bp, uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds,
+                                     hipStream_t s, const GemvArgs& g) {
+  // eight waves: every tile's sums at the row-block end
+  if (!tiles_supported(nt, seg_len, jt) || block.x != stream_threads(false, bp ? 1 : 0, nt)) return HL_EINVAL;
+  if (nt == 4)
+    return bp ? launch_stream_tiles_tb<1, 4>(seg_len, jt, grid, block, lds, s, g)
+              : launch_stream_tiles_tb<0, 4>(seg_len, jt, grid, block, lds, s, g);
+  return bp ? launch_stream_tiles_tb<1, 2>(seg_len, jt, grid, block, lds, s, g)
+            : launch_stream_tiles_tb<0, 2>(seg_len, jt, grid, block, lds, s, g);
 }
 
 // Grouped launches (multi) exist for S = 64, bounded pairs (bp) for S = 64.
@@ -2999,19 +3036,20 @@ extern "C" hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dt
   if (x_dtype != HL_BF16 || is_fp16(t) || t->grp_rows != 16 || (t->seg_len != 32 && t->seg_len != 64))
     return HL_EUNSUPPORTED;
   if (!workspace_dev || workspace_bytes < hl_gemm_workspace_bytes(t, tokens)) return HL_EINVAL;
-  if (tokens <= 2 * kTile) {
-    // up to 32 tokens on matrices the persistent kernel takes: one or two
-    // 16-token tiles per step of its decode, each row block summed in its
-    // block (no partial sums); the activations tiled in the workspace (16 or
-    // 32 rows per 8-column chunk, so that a wave's reads of one chunk are
-    // contiguous)
+  if (tokens <= 4 * kTile) {
+    // up to 64 tokens on matrices the persistent kernel takes: one, two or
+    // four 16-token tiles per step of its decode, each row block summed in
+    // its block (no partial sums); the activations tiled in the workspace (16
+    // rows per tile and 8-column chunk, so that a wave's reads of one chunk
+    // are contiguous)
     Plan pp;
     hl_status sp = make_plan(t, 0, false, &pp);
     if (sp != HL_OK) return sp;
     int jt = 0;
     uint32_t w = 0;
     size_t per_wave = 0;
-    if (stream_shape(t, pp.ga, &jt, &w, &per_wave)) {
+    const int nt = tokens <= kTile ? 1 : tokens <= 2 * kTile ? 2 : 4;
+    if (stream_shape(t, pp.ga, &jt, &w, &per_wave) && (nt == 1 || tiles_supported(nt, t->seg_len, jt))) {
       GemvArgs p;
       std::memset(&p, 0, sizeof(p));
       p.g = pp.ga;
@@ -3022,16 +3060,18 @@ extern "C" hl_status hl_decode_gemm(const hl_tensor* t, const void* x_dev, hl_dt
       p.KS = 1;
       const bool bp = bounded_pairs(t);
       const dim3 grid(std::min<uint32_t>(pp.ga.RB, (uint32_t)device_cus()));
-      if (tokens > kTile) {
-        const uint32_t chunks = (uint32_t)(t->cols / 8);
-        if (workspace_bytes < (size_t)chunks * 2 * kTile * 16) return HL_EINVAL;
+      if (nt > 1) {
+        const uint32_t chunks = (uint32_t)(t->cols / 8), R = nt * kTile;
+        if (workspace_bytes < (size_t)chunks * R * 16) return HL_EINVAL;
         uint4* tile = reinterpret_cast<uint4*>(workspace_dev);
-        sp = launch(xtile_kernel<2 * kTile>, dim3((chunks * 2 * kTile + 255) / 256), dim3(256), 0,
-                    (hipStream_t)stream, reinterpret_cast<const uint4*>(x_dev), tokens, chunks, tile);
+        const dim3 tgrid((chunks * R + 255) / 256);
+        const uint4* xs = reinterpret_cast<const uint4*>(x_dev);
+        sp = nt == 2 ? launch(xtile_kernel<2 * kTile>, tgrid, dim3(256), 0, (hipStream_t)stream, xs, tokens, chunks, tile)
+                     : launch(xtile_kernel<4 * kTile>, tgrid, dim3(256), 0, (hipStream_t)stream, xs, tokens, chunks, tile);
         if (sp != HL_OK) return sp;
         p.x = tile;
-        w = stream_threads(false, bp ? 1 : 0, 2) / 64;
-        return launch_stream_nt2(bp, t->seg_len, jt, grid, dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
+        w = stream_threads(false, bp ? 1 : 0, nt) / 64;
+        return launch_stream_tiles(nt, bp, t->seg_len, jt, grid, dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
       }
       bool xt = false;
       sp = tile_activations(t, x_dev, tokens, workspace_dev, workspace_bytes, (hipStream_t)stream, &p, &xt);

@@ -6,8 +6,8 @@ Every output against a float64 product of the exact bf16 values and sampled
 outputs against the oracle's exactly rounded sums, |y - y_ref| <= 1e-3 *
 sum_k |w x|: token counts 1 .. 300 (one and several chunks, ragged last
 tile), ragged row sets and row blocks, S = 32 and 64, both bf16 formats,
-repeated calls on one workspace; up to 32 tokens on the persistent kernel
-(one or two 16-token tiles); unsupported requests are reported.
+repeated calls on one workspace; up to 64 tokens on the persistent kernel
+(one, two or four 16-token tiles); unsupported requests are reported.
 """
 import numpy as np
 import pytest
@@ -80,35 +80,36 @@ def _persistent_shape(torch, rows, cols, S):
 
 @pytest.mark.parametrize("shape,S,fmt", [((4100, 4096), 64, "split"), ((4100, 4096), 64, "whole"),
                                          ((4096, 4096), 32, "split"), ((4112, 8192), 64, "split_unbounded")])
-def test_persistent_up_to_32_tokens(torch, shape, S, fmt):
-    """Up to 32 tokens on matrices the persistent kernel takes: one 16-token
-    tile per decode step, or two (17..32 tokens), sums per row block in one
-    block; ragged last row block (4100 rows), bounded-pair and joint tables."""
+def test_persistent_up_to_64_tokens(torch, shape, S, fmt):
+    """Up to 64 tokens on matrices the persistent kernel takes: one 16-token
+    tile per decode step, two (17..32 tokens) or four (33..64, columns of 16
+    words or more; else the chunked kernel), sums per row block in one block;
+    ragged last row block (4100 rows), bounded-pair and joint tables."""
     print(f"gemm persistent {shape} S={S} {fmt}", flush=True)
     assert _persistent_shape(torch, shape[0], shape[1], S)
     kw = {"whole": {"whole_exponent": True}, "split_unbounded": {"pair_max": 0}}.get(fmt, {})
     w = random_bf16(shape, seed=shape[0] + S + len(fmt))
     dt = hl.DeviceTensor(hl.encode(w, seg_len=S, **kw))
-    for T in (1, 7, 16, 17, 23, 32):
+    for T in (1, 7, 16, 17, 23, 32, 33, 50, 64):
         print(f"  T={T}", flush=True)
         _check(torch, dt, w, T, seed=T + S)
 
 
-def test_persistent_two_tiles_70b_gate(torch):
-    """The 70B gate matrix (28672x8192, drawn from its own seed) at 24 and 32
-    tokens on the two-tile form: sampled rows against the oracle's exactly
+def test_persistent_tiles_70b_gate(torch):
+    """The 70B gate matrix (28672x8192, drawn from its own seed) at 24, 32 and
+    64 tokens on the two- and four-tile forms: sampled rows against the oracle's exactly
     rounded sums, every output against a float32 product of the original
     weights (torch, on the GPU), within 1e-3 of sum_k |w x|."""
     from gen import workload_matrices, gen_matrix
     spec = workload_matrices(5)[4]
-    print(f"gemm persistent two tiles {spec.rows}x{spec.cols}", flush=True)
+    print(f"gemm persistent tiles {spec.rows}x{spec.cols}", flush=True)
     w = gen_matrix(spec)
     dt = hl.DeviceTensor(hl.encode(w))
     assert _persistent_shape(torch, spec.rows, spec.cols, 64)
     wf = torch.from_numpy(w.view(np.int16)).cuda().view(torch.bfloat16).float()
     rng = np.random.default_rng(5)
     rows = sorted({0, spec.rows - 1} | set(int(r) for r in rng.integers(0, spec.rows, 6)))
-    for T in (24, 32):
+    for T in (24, 32, 64):
         print(f"  T={T}", flush=True)
         x = random_x(T, spec.cols, seed=T, dtype="bf16")
         xd = _xdev(torch, x)
@@ -124,14 +125,15 @@ def test_persistent_two_tiles_70b_gate(torch):
     del wf
 
 
-def test_persistent_two_tiles_repeat(torch):
-    print("gemm persistent two tiles repeated", flush=True)
+def test_persistent_tiles_repeat(torch):
+    print("gemm persistent tiles repeated", flush=True)
     w = random_bf16((4100, 4096), seed=11)
     dt = hl.DeviceTensor(hl.encode(w))
-    x = _xdev(torch, random_x(29, 4096, seed=12, dtype="bf16"))
-    y1 = dt.gemm(x).cpu().numpy()
-    for _ in range(3):
-        assert np.array_equal(y1, dt.gemm(x).cpu().numpy())   # fixed summation order
+    for T in (29, 61):
+        x = _xdev(torch, random_x(T, 4096, seed=12, dtype="bf16"))
+        y1 = dt.gemm(x).cpu().numpy()
+        for _ in range(3):
+            assert np.array_equal(y1, dt.gemm(x).cpu().numpy())   # fixed summation order
 
 
 def test_repeated_calls_share_the_workspace(torch):
