@@ -1717,10 +1717,12 @@ __device__ inline const GemvArgs& gemv_args(const Args& x) {
 // NT = 16-token tiles of activations per matrix instruction step: 1 (up to 16
 // activation rows), or 2 or 4 for prefill products of 17 to 32 or 33 to 64
 // tokens (one bf16 matrix, activations from their tiled copy).
-// Blocks of at most 16 waves (8 decoding or with several tiles, 12 for the
-// float16 product, whose longer stream columns need more registers).
+// Blocks of at most 16 waves (12 decoding bf16 formats, whose registers hold
+// a group's weights until its stores; 8 decoding float16 or with several
+// tiles; 12 for the float16 product, whose longer stream columns need more
+// registers).
 constexpr uint32_t stream_threads(bool dec, int tb, int nt = 1) {
-  return dec || nt > 1 ? 512 : tb == 2 ? 768 : 1024;
+  return dec ? (tb == 2 ? 512 : 768) : nt > 1 ? 512 : tb == 2 ? 768 : 1024;
 }
 
 template <int SP, int JT, bool XT, class Args, bool DEC, int TB, int NT = 1>
@@ -2487,7 +2489,8 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
     p.B = 1;
     p.C = pl.ga.CB;
     p.KS = 1;
-    w = 8;  // the kernel's bound when decoding (registers for a group's weights)
+    // the kernel's bound when decoding (registers for a group's weights)
+    w = stream_threads(true, is_fp16(t) ? 2 : 0) / 64;
     const dim3 grid(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus()));
     // float16: its tables lead the dynamic LDS
     if (is_fp16(t))
