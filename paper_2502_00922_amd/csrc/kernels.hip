@@ -1717,12 +1717,11 @@ __device__ inline const GemvArgs& gemv_args(const Args& x) {
 // NT = 16-token tiles of activations per matrix instruction step: 1 (up to 16
 // activation rows), or 2 or 4 for prefill products of 17 to 32 or 33 to 64
 // tokens (one bf16 matrix, activations from their tiled copy).
-// Blocks of at most 16 waves (12 decoding bf16 formats, whose registers hold
-// a group's weights until its stores; 8 decoding float16 or with several
-// tiles; 12 for the float16 product, whose longer stream columns need more
-// registers).
+// Blocks of at most 16 waves (8 decoding, whose registers hold a group's
+// weights until its stores, or with several tiles; 12 for the float16
+// product, whose longer stream columns need more registers).
 constexpr uint32_t stream_threads(bool dec, int tb, int nt = 1) {
-  return dec ? (tb == 2 ? 512 : 768) : nt > 1 ? 512 : tb == 2 ? 768 : 1024;
+  return dec || nt > 1 ? 512 : tb == 2 ? 768 : 1024;
 }
 
 template <int SP, int JT, bool XT, class Args, bool DEC, int TB, int NT = 1>
@@ -1955,13 +1954,45 @@ __global__ void __launch_bounds__(stream_threads(DEC, TB, NT)) gemv_stream_kerne
         }
       }
       if constexpr (F16) sg = sgn;
-      if constexpr (DEC) {
-        // row r0 + i, columns (c0 + q)*S .. + S: stored back to back, so
-        // that each of the lane's cache lines is written whole at once
+      if constexpr (DEC && F16) {
+        // float16 (its decode already LDS-bound: the transposition below cost
+        // 5% there): row r0 + i, columns (c0 + q)*S .. + S back to back
         if (i < G) {
           uint4* o = reinterpret_cast<uint4*>(outp + (uint64_t)(rb * 16 + i) * a.cols + (cur_c0 + q) * S);
 #pragma unroll
           for (int k = 0; k < SP; ++k) o[k] = dv[k];
+        }
+      } else if constexpr (DEC) {
+        // The group's 16 rows x 4 segments, transposed through the wave's
+        // column region (its stream words are consumed), four rows at a time,
+        // so that each store instruction writes whole output rows: 32 (S =
+        // 64) or 16 lanes per row of 4 segments, 16 bytes each. Stored
+        // straight from the lanes (row i, segment q: 16-byte chunks 128 or 64
+        // bytes apart), every store instruction touched 64 cache lines:
+        // 28672x8192 265 us against 170 us with whole rows (timing run).
+        // Chunk kk of tile row m (= row * 4 + segment) sits in slot
+        // kk ^ (m % SP) of that row, so that a write's lanes spread over the banks.
+        constexpr uint32_t kLanesPerRow = 4 * SP, kRowsPerStore = 64 / kLanesPerRow, kPassRows = 4;
+        uint4* tile = reinterpret_cast<uint4*>(cols);
+        const uint32_t c = lane % kLanesPerRow, cq = c / SP, ck = c % SP;
+        uint16_t* orow = outp + (uint64_t)(rb * 16) * a.cols + cur_c0 * S + c * 8;
+#pragma unroll
+        for (uint32_t h = 0; h < 16; h += kPassRows) {
+          if (i - h < kPassRows) {
+            const uint32_t m = (i - h) * 4 + q;
+#pragma unroll
+            for (int k = 0; k < SP; ++k) tile[m * SP + ((uint32_t)k ^ (m % SP))] = dv[k];
+          }
+          wait_lgkm0();
+          wave_sync_lds();
+#pragma unroll
+          for (uint32_t r0 = 0; r0 < kPassRows; r0 += kRowsPerStore) {
+            const uint32_t rr = r0 + lane / kLanesPerRow, m = rr * 4 + cq;
+            const uint4 v = tile[m * SP + (ck ^ (m % SP))];
+            if (h + rr < G) *reinterpret_cast<uint4*>(orow + (uint64_t)(h + rr) * a.cols) = v;
+          }
+          wait_lgkm0();
+          wave_sync_lds();
         }
       }
       wait_lgkm0();
