@@ -355,7 +355,7 @@ hl_status hl_decode_gemv_multi(const hl_tensor* const* ts, uint32_t count, const
                                void* workspace_dev, size_t workspace_bytes, void* stream);
 
 /* Bytes of device workspace hl_decode_gemm needs for `tokens` activation rows:
- * up to 112 tokens the partial sums of up to one range per column block of
+ * up to 64 tokens the partial sums of up to one range per column block of
  * four segments (on the persistent kernel's matrices, up to 64 tokens, only
  * the tiled activations use it), beyond that the decoded weights
  * (rows * cols * 2); 0 for tensors it does not take. */
@@ -367,7 +367,7 @@ size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens);
  * persistent fused decode-GEMV multiplies each decoded 8-weight step with
  * one, two or four 16-token tiles (the activations first copied to the
  * workspace in chunks of 16 rows per tile; four tiles for S = 64 and stream
- * columns of 16 words or more); otherwise, up to 112 tokens, each 16-row x 4-segment
+ * columns of 16 words or more); otherwise, up to 64 tokens, each 16-row x 4-segment
  * weight tile is decoded once per chunk of up to 128 tokens and multiplied
  * with all of them on the matrix cores (Sec. 3.2: weights decompressed only
  * to be multiplied); every output summed in a fixed order; beyond that, where the product is compute-bound (Sec. 5), the

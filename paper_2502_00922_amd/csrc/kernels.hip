@@ -2978,11 +2978,11 @@ constexpr uint32_t kGemmMaxTiles = 8;  // token tiles of 16 per block
 static uint32_t gemm_row_sets(const hl_tensor* t) { return (uint32_t)((t->rows + 255) / 256); }
 
 // Prefill above this many tokens: the weights are decoded once to bf16 in the
-// workspace and multiplied by the vendor GEMM (hipBLASLt). Up to it the fused
-// kernel decodes each tile once per chunk of up to 128 tokens (4096x4096: 24.6
-// us at 32 tokens, 50.3 us at 128; decode + GEMM 42 us at 129 tokens, 51 us at
-// 512, where the fused kernel, decoding four times, took 110 us).
-constexpr uint32_t kGemmFusedMaxTokens = 112;
+// workspace and multiplied by the vendor GEMM (hipBLASLt). Up to it the
+// persistent kernel's tiled forms, or the fused kernel that decodes each tile
+// once per chunk of tokens (4096x4096, cold: decode + GEMM 32.9-36.9 us at 65
+// to 112 tokens against 42.6-48.2 us fused; 39.3 us at 128, 45.4 us at 512).
+constexpr uint32_t kGemmFusedMaxTokens = 64;
 constexpr uint32_t kTile = 16;  // activation rows of one matrix-instruction tile
 
 extern "C" size_t hl_gemm_workspace_bytes(const hl_tensor* t, uint32_t tokens) {
