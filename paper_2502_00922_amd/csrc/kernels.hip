@@ -2326,8 +2326,17 @@ static hl_status launch_stream16(bool xt, bool dec, uint32_t seg_len, int jt, di
 }
 
 // Decoding to bf16 with the persistent kernel (p.y = the output).
-static hl_status launch_stream_dec(uint32_t seg_len, int jt, dim3 grid, dim3 block, size_t lds, hipStream_t s,
-                                   const GemvArgs& p) {
+static hl_status launch_stream_dec(uint32_t seg_len, int jt, bool bp, dim3 grid, dim3 block, size_t lds,
+                                   hipStream_t s, const GemvArgs& p) {
+  if (bp && block.x < kBpMinThreads) return HL_EINVAL;  // the bounded-pair table fill
+  if (bp && seg_len == 64) {
+    switch (jt) {
+      case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, 1>, grid, block, lds, s, p);
+      case 16: return launch(gemv_stream_kernel<8, 16, false, GemvArgs, true, 1>, grid, block, lds, s, p);
+      case 20: return launch(gemv_stream_kernel<8, 20, false, GemvArgs, true, 1>, grid, block, lds, s, p);
+      default: return HL_EUNSUPPORTED;
+    }
+  }
   if (seg_len == 64) {
     switch (jt) {
       case 12: return launch(gemv_stream_kernel<8, 12, false, GemvArgs, true, 0>, grid, block, lds, s, p);
@@ -2527,10 +2536,12 @@ extern "C" hl_status hl_decode(const hl_tensor* t, uint16_t* out_dev, void* stre
     if (is_fp16(t))
       return launch_stream16(false, true, t->seg_len, jt, grid, dim3(w * 64),
                              (size_t)pl.ga.t16_words * 4 + w * per_wave, (hipStream_t)stream, p);
-    // the decode form keeps the joint table (the bounded-pair form measured
-    // slower here: 28672x8192 307 us against 273 us)
-    return launch_stream_dec(t->seg_len, jt, dim3(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus())),
-                             dim3(w * 64), w * per_wave, (hipStream_t)stream, p);
+    // the bounded-pair table where the encoder's joint limit holds (with the
+    // whole-row stores it decodes 28672x8192 in 175.9 us against 187.7 us
+    // with the joint table; stored straight from the lanes, 307 against 273)
+    return launch_stream_dec(t->seg_len, jt, bounded_pairs(t),
+                             dim3(std::min<uint32_t>(pl.ga.RB, (uint32_t)device_cus())), dim3(w * 64), w * per_wave,
+                             (hipStream_t)stream, p);
   }
   if (is_fp16(t)) {
     const uint32_t per_cu = std::max<uint32_t>(1, std::min<uint32_t>(8, kMaxLds / (uint32_t)pl.lds));
